@@ -1,0 +1,160 @@
+/*
+ * wl.h — C ABI of the MI355X (gfx950) library for randomized 1-WL stable
+ * colouring (randomized linear-algebraic colour refinement).
+ *
+ * Method: "Scaling Weisfeiler-Leman Expressiveness Analysis to Massive Graphs
+ * with GPUs" (Biondi, Tribastone, Tschaikowski).
+ *   - Algorithm 1 (Randomized Stable Coloring, Section 4.1): per round, draw
+ *     one random value per colour, take the image z = A w, and split every
+ *     colour class by z.
+ *   - Algorithm 2 (Randomized Batched Stable Coloring, Section 4.2): cut the
+ *     edge set into batches, refine each batch with its boundary nodes frozen
+ *     as singletons (Eq. batch-init), merge (Eq. merge), contract to the
+ *     quotient graph (Definition "Quotient Graph", Eq. sc) and repeat.
+ *
+ * Arithmetic: exact modular arithmetic in F_p, p = 2^61 - 1.  The random
+ * value of colour b in round r is W(seed, r, b): the (b+1)-th output of a
+ * SplitMix64 stream whose state is mix(mix(seed + g) + (r+1) g), reduced
+ * mod p (g = 0x9E3779B97F4A7C15, mix = the SplitMix64 output function).
+ * New colour of node i = rank of the pair (c_i, z_i) among all distinct pairs
+ * in lexicographic order.  Rounds repeat until the colour count does not
+ * change; the round that confirms this is counted.
+ *
+ * Conventions shared by every entry point
+ *   - Graphs are CSR.  Row i lists the out-neighbours of node i (the
+ *     stability condition of the paper is on out-weights).  Column order
+ *     inside a row does not matter; repeated columns count with
+ *     multiplicity.  Self-loops are allowed.
+ *   - The caller owns every buffer.  The library allocates no device or host
+ *     memory of its own: all scratch space is the caller's 'workspace'
+ *     (device memory, 256-byte aligned), sized by wl_workspace_size().
+ *   - All device work is enqueued on 'stream' (a hipStream_t; NULL = the
+ *     null stream).  Entry points that return host scalars synchronise that
+ *     stream before returning.
+ *   - Return value: WL_OK (0) or a negative WL_E* code; wl_last_error() then
+ *     gives a message (thread-local).  Outputs are defined only on WL_OK,
+ *     except WL_EMAXROUNDS (see wl_stable_coloring).  No C++ exception ever
+ *     crosses this interface.
+ *   - Preconditions checked on the host: n < 2^32, nnz consistent with the
+ *     row pointer, non-NULL pointers where required.  Set the environment
+ *     variable WL_VALIDATE=1 to also check, on the device, that row pointers
+ *     are non-decreasing and every column index is < n (costs one pass).
+ *   - Row sums of the weights must stay below p (true for every graph with
+ *     uint32 weights and fewer than 2^29 entries per row, and preserved by
+ *     quotients).
+ */
+#ifndef WL_H
+#define WL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define WL_OK 0
+#define WL_EINVAL (-1)      /* malformed arguments or graph                */
+#define WL_EBUDGET (-2)     /* workspace smaller than required             */
+#define WL_EOVERFLOW (-3)   /* n >= 2^32, or a quotient weight overflowed  */
+#define WL_EMAXROUNDS (-4)  /* round cap reached before stability          */
+#define WL_ENOTSTABLE (-5)  /* wl_verify_stable: colouring is not stable   */
+#define WL_EHIP (-6)        /* a HIP runtime call failed                   */
+
+/* CSR adjacency.  Exactly one of row_ptr32 / row_ptr64 is non-NULL; it has
+ * n+1 entries, row_ptr[0] == 0 and row_ptr[n] == nnz.  col_idx has nnz
+ * entries, each < n.  weight is NULL (every entry weighs 1) or has nnz
+ * entries (a_ij in N_0; weighted graphs arise as quotients).  Whether the
+ * pointers are device or host memory is stated per entry point. */
+typedef struct wl_csr {
+    uint64_t n;
+    uint64_t nnz;
+    const uint32_t *row_ptr32;
+    const uint64_t *row_ptr64;
+    const uint32_t *col_idx;
+    const uint32_t *weight;
+} wl_csr;
+
+/* Workspace (device bytes) needed by the in-core entry points
+ * (wl_refine_round, wl_stable_coloring, wl_verify_stable) for graph g.
+ * Only g->n and g->nnz are read; the pointers may be NULL.
+ * Returns WL_EINVAL for a NULL argument, WL_EOVERFLOW for n >= 2^32. */
+int wl_workspace_size(const wl_csr *g, uint64_t *bytes_out);
+
+/* Smallest workspace accepted by wl_stable_coloring_batched for a graph
+ * with g->n nodes: the node-sized state plus room for a batch of
+ * 'max_batch_entries' CSR entries (pass 0 to ask for the size that holds the
+ * whole graph in one batch). */
+int wl_batched_workspace_size(const wl_csr *g, uint64_t max_batch_entries,
+                              uint64_t *bytes_out);
+
+/* One round of Algorithm 1 (Section 4.1).
+ *   g          device CSR.
+ *   color_in   device, n entries, each < k_in (a colouring; ids need not all
+ *              be used).  k_in <= max(n, 1).
+ *   seed,round select the random values W(seed, round, .).
+ *   color_out  device, n entries; receives the rank of (color_in[i], z_i)
+ *              among the distinct pairs.  May alias color_in.
+ *   k_out      host; number of distinct pairs (colours after the round).
+ * Errors: WL_EINVAL (bad sizes, NULL pointers, k_in > n, or a colour >= k_in
+ * when it is detected on the device), WL_EBUDGET, WL_EHIP. */
+int wl_refine_round(const wl_csr *g, const uint32_t *color_in, uint32_t k_in,
+                    uint64_t seed, uint32_t round, uint32_t *color_out,
+                    uint32_t *k_out, void *workspace, uint64_t ws_bytes,
+                    void *stream);
+
+/* Algorithm 1 to completion: the coarsest stable colouring refining the
+ * initial partition (Theorem 1; with probability >= 1 - rounds * n / p).
+ *   g           device CSR.
+ *   init_color  device, n labels, or NULL for the trivial partition.  The
+ *               initial colour of node i is the dense rank of its label.
+ *   max_rounds  cap on rounds (0 = n + 1, which is never reached).
+ *   color_out   device, n entries: final colours, dense in [0, k).  These
+ *               are the raw lexicographic-rank ids of the last round.
+ *   k_out, rounds_out  host; colour count and number of rounds (the
+ *               confirming round included; 0 when n == 0).
+ * On WL_EMAXROUNDS color_out/k_out/rounds_out hold the state after the last
+ * round that ran.  Errors: WL_EINVAL, WL_EBUDGET, WL_EMAXROUNDS, WL_EHIP. */
+int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
+                       uint64_t seed, uint32_t max_rounds, uint32_t *color_out,
+                       uint32_t *k_out, uint32_t *rounds_out, void *workspace,
+                       uint64_t ws_bytes, void *stream);
+
+/* Algorithm 2 (Section 4.2) for graphs whose edge arrays stay in host
+ * memory; only one batch of entries is on the device at a time.
+ *   g_host      host CSR (pinned memory recommended: batches are copied
+ *               host-to-device asynchronously).
+ *   init_host   host labels or NULL (trivial partition).
+ *   max_batch_entries  cap M_b on entries per batch; 0 = the largest cap the
+ *               workspace allows.  Batches are contiguous CSR entry ranges
+ *               cut at row boundaries; a row longer than the cap is split and
+ *               its node is a boundary node.
+ *   color_out_host  host, n entries: first-occurrence canonical colours
+ *               (node 0 gets 0, each new colour the next id), so equal
+ *               partitions give equal arrays.
+ *   k_out, rounds_out (sum over all batch runs), outer_out (outer
+ *   iterations), coarsest_out (1 when the last outer iteration had a single
+ *   batch, which makes the result the coarsest stable colouring; 0 when the
+ *   contraction stopped at a fixed point with several batches).
+ * Errors: WL_EINVAL, WL_EBUDGET, WL_EOVERFLOW, WL_EMAXROUNDS, WL_EHIP. */
+int wl_stable_coloring_batched(const wl_csr *g_host, const uint32_t *init_host,
+                               uint64_t seed, uint64_t max_batch_entries,
+                               uint32_t *color_out_host, uint32_t *k_out,
+                               uint32_t *rounds_out, uint32_t *outer_out,
+                               int *coarsest_out, void *workspace,
+                               uint64_t ws_bytes, void *stream);
+
+/* Exact stability certificate (Definition "Stable Coloring"): WL_OK when
+ * every two nodes of each colour class have equal total out-weight into
+ * every class, WL_ENOTSTABLE otherwise.  Deterministic (no randomness).
+ *   g      device CSR;  color  device, n entries, each < k;  k <= n. */
+int wl_verify_stable(const wl_csr *g, const uint32_t *color, uint32_t k,
+                     void *workspace, uint64_t ws_bytes, void *stream);
+
+/* Message for the last non-zero return on this thread ("" if none). */
+const char *wl_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WL_H */

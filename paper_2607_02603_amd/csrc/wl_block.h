@@ -1,0 +1,40 @@
+// Workgroup-level scan primitives for 256-thread (4 x wave64) blocks.
+#pragma once
+#include "wl_ctx.h"
+#include "wl_device.h"
+
+namespace wl {
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    uint32_t o = __shfl_up(v, off, kWave);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
+// Exclusive scan over the 256 threads of a block; returns the thread's
+// exclusive prefix and writes the block total to *total.  'sh' must hold
+// kBlock / kWave words of shared memory.  Contains __syncthreads().
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* sh,
+                                                    uint32_t* total) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  uint32_t inc = wave_incl_scan(v);
+  if (lane == kWave - 1) sh[wid] = inc;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kBlock / kWave; ++w) {
+    uint32_t s = sh[w];
+    if (w < wid) base += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - v;
+}
+
+}  // namespace wl

@@ -1,0 +1,90 @@
+// Shared structures of the device path: the per-call device state, the
+// pointer bundle every kernel receives, and the tuning constants.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wl {
+
+constexpr int kBlock = 256;          // threads per workgroup (4 waves)
+constexpr uint32_t kSmallMax = 2048; // class/bucket size sorted in LDS
+constexpr uint32_t kTile = 4096;     // elements per tile in the MSD passes
+constexpr uint32_t kTilePerThread = kTile / kBlock;
+constexpr int kRadixBits = 8;
+constexpr int kRadix = 1 << kRadixBits;
+constexpr int kPasses = 8;           // 61-bit keys: 7 passes of 8 bits + 5
+constexpr uint32_t kMatBit = 0x80000000u;  // small segment keys are in 'keys'
+constexpr uint32_t kHeavyChunk = 4096;     // entries per heavy-row chunk
+constexpr int kNumBins = 4;                // row-length bins of the SpMV
+constexpr int kScanBlocks = 1024;          // blocks of the device-wide scans
+
+// Row-length bins of the SpMV: lanes per row.
+//   bin 0: len <= 8        4 lanes
+//   bin 1: len <= 64      16 lanes
+//   bin 2: len <= 4096    64 lanes (one wave)
+//   bin 3: len  > 4096    chunks of kHeavyChunk entries, one wave each
+__host__ __device__ __forceinline__ int row_bin(uint64_t len) {
+  return len <= 8 ? 0 : (len <= 64 ? 1 : (len <= kHeavyChunk ? 2 : 3));
+}
+
+// Device-resident scalars of one call.
+struct DevState {
+  uint32_t k;           // colour count before the current round
+  uint32_t k_new;       // colour count after it
+  uint32_t round;       // index of the round to run next
+  uint32_t done;        // 0 running, 1 stable, 2 round cap reached
+  uint32_t max_rounds;  // stop after this many rounds in total
+  uint32_t n_small;     // entries in the small-segment list
+  uint32_t n_big[2];    // entries in the two big-segment lists
+  uint32_t n_tiles;     // tiles of the current big list
+  uint32_t err;         // input errors seen on the device (bit mask)
+  uint32_t n_chunks;    // heavy-row chunks of the SpMV schedule
+  uint32_t bin_cnt[kNumBins];
+  uint32_t bin_start[kNumBins];
+  uint32_t pad[5];
+  uint64_t seed;
+};
+
+struct HeavyChunk {
+  uint64_t beg, end;  // entry range
+  uint32_t row;       // node
+  uint32_t h;         // index of the heavy row (accumulator slot)
+};
+
+// Every pointer a kernel may touch.  Passed by value.
+struct Ctx {
+  uint32_t n;
+  uint64_t nnz;
+  const uint32_t* rp32;
+  const uint64_t* rp64;
+  const uint32_t* col;
+  const uint32_t* wgt;
+  DevState* st;
+  uint32_t* c;         // colours, node order
+  uint64_t* x;         // per-node random value of the round
+  uint64_t* z;         // image A x
+  uint32_t* perm;      // nodes grouped by colour (positions)
+  uint32_t* perm_tmp;
+  uint64_t* keys;      // z in position order (big segments)
+  uint64_t* keys_tmp;
+  uint8_t* flags;      // 1 where a new (colour, z) group starts
+  uint8_t* act;        // 1 if the node's class has >= 2 members
+  uint32_t* ids;       // inclusive scan of flags minus one
+  uint32_t* cstart;    // class c occupies perm[cstart[c] .. cstart[c+1])
+  uint2* small_list;   // (start, len | kMatBit)
+  uint2* big_list0;
+  uint2* big_list1;
+  uint32_t* tile_off;  // tiles of the current big list (exclusive scan)
+  uint32_t* bhist;     // per (big segment, bucket)
+  unsigned long long* bmin;
+  unsigned long long* bmax;
+  uint32_t* bcur;
+  uint32_t* scan_part; // kScanBlocks partial sums
+  uint32_t* rows;      // SpMV bin lists, concatenated
+  uint32_t* bin_part;  // kNumBins * kScanBlocks
+  HeavyChunk* chunks;
+  unsigned long long* hacc;  // two accumulators per heavy row
+  uint32_t max_small, max_big, max_chunks, max_heavy;
+};
+
+}  // namespace wl

@@ -1,0 +1,547 @@
+// Host driver and C ABI (include/wl.h) of the gfx950 path.
+//
+// Algorithm 1 (Section 4.1): each round is
+//   x_i = W(seed, r, c_i)  ->  z = A x (mod p)  ->  relabel by (c_i, z_i)
+// and rounds repeat until the colour count is unchanged.  The library keeps
+// the nodes grouped by colour between rounds, skips singleton classes, and
+// never allocates: every buffer is carved from the caller's workspace.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "../../include/wl.h"
+#include "wl_ctx.h"
+#include "wl_relabel.h"
+#include "wl_spmv.h"
+
+using namespace wl;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+#define HIP_TRY(expr)                                                      \
+  do {                                                                     \
+    hipError_t e_ = (expr);                                                \
+    if (e_ != hipSuccess)                                                  \
+      return fail(WL_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+#define HIP_LAUNCH_CHECK()                                                    \
+  do {                                                                        \
+    hipError_t e_ = hipGetLastError();                                        \
+    if (e_ != hipSuccess)                                                     \
+      return fail(WL_EHIP, "kernel launch failed: %s", hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr uint64_t kAlign = 256;
+uint64_t align_up(uint64_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Sizes of every workspace region for a graph with n nodes, nnz entries.
+struct Layout {
+  uint64_t n, nnz;
+  uint32_t max_small, max_big, max_chunks, max_heavy;
+  uint64_t off_st, off_x, off_z, off_keys, off_keys_tmp, off_perm, off_perm_tmp,
+      off_ids, off_cstart, off_flags, off_act, off_small, off_big0, off_big1,
+      off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
+      off_binpart, off_chunks, off_hacc;
+  uint64_t total;
+};
+
+Layout make_layout(uint64_t n, uint64_t nnz) {
+  Layout L{};
+  L.n = n;
+  L.nnz = nnz;
+  L.max_small = (uint32_t)(n / 2 + 1);
+  L.max_big = (uint32_t)(n / (kSmallMax + 1) + 1);
+  L.max_heavy = (uint32_t)std::min<uint64_t>(n, nnz / (kHeavyChunk + 1) + 1);
+  L.max_chunks = (uint32_t)(nnz / kHeavyChunk + L.max_heavy + 1);
+  uint64_t o = 0;
+  auto take = [&](uint64_t bytes) {
+    uint64_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  L.off_st = take(sizeof(DevState));
+  L.off_x = take(8 * n);
+  L.off_z = take(8 * n);
+  L.off_keys = take(8 * n);
+  L.off_keys_tmp = take(8 * n);
+  L.off_perm = take(4 * n);
+  L.off_perm_tmp = take(4 * n);
+  L.off_ids = take(4 * (n + 1));
+  L.off_cstart = take(4 * (n + 2));
+  L.off_flags = take(n + 1);
+  L.off_act = take(n + 1);
+  L.off_small = take(8ull * L.max_small);
+  L.off_big0 = take(8ull * L.max_big);
+  L.off_big1 = take(8ull * L.max_big);
+  L.off_tile = take(4ull * (L.max_big + 1));
+  L.off_bhist = take(4ull * L.max_big * kRadix);
+  L.off_bmin = take(8ull * L.max_big * kRadix);
+  L.off_bmax = take(8ull * L.max_big * kRadix);
+  L.off_bcur = take(4ull * L.max_big * kRadix);
+  L.off_scan = take(4ull * kScanBlocks);
+  L.off_rows = take(4 * n);
+  L.off_binpart = take(4ull * kNumBins * kScanBlocks);
+  L.off_chunks = take(sizeof(HeavyChunk) * (uint64_t)L.max_chunks);
+  L.off_hacc = take(16ull * L.max_heavy);
+  L.total = o;
+  return L;
+}
+
+Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
+  Ctx c{};
+  c.n = (uint32_t)L.n;
+  c.nnz = L.nnz;
+  c.rp32 = g->row_ptr32;
+  c.rp64 = g->row_ptr64;
+  c.col = g->col_idx;
+  c.wgt = g->weight;
+  c.st = (DevState*)(ws + L.off_st);
+  c.c = colors;
+  c.x = (uint64_t*)(ws + L.off_x);
+  c.z = (uint64_t*)(ws + L.off_z);
+  c.keys = (uint64_t*)(ws + L.off_keys);
+  c.keys_tmp = (uint64_t*)(ws + L.off_keys_tmp);
+  c.perm = (uint32_t*)(ws + L.off_perm);
+  c.perm_tmp = (uint32_t*)(ws + L.off_perm_tmp);
+  c.ids = (uint32_t*)(ws + L.off_ids);
+  c.cstart = (uint32_t*)(ws + L.off_cstart);
+  c.flags = ws + L.off_flags;
+  c.act = ws + L.off_act;
+  c.small_list = (uint2*)(ws + L.off_small);
+  c.big_list0 = (uint2*)(ws + L.off_big0);
+  c.big_list1 = (uint2*)(ws + L.off_big1);
+  c.tile_off = (uint32_t*)(ws + L.off_tile);
+  c.bhist = (uint32_t*)(ws + L.off_bhist);
+  c.bmin = (unsigned long long*)(ws + L.off_bmin);
+  c.bmax = (unsigned long long*)(ws + L.off_bmax);
+  c.bcur = (uint32_t*)(ws + L.off_bcur);
+  c.scan_part = (uint32_t*)(ws + L.off_scan);
+  c.rows = (uint32_t*)(ws + L.off_rows);
+  c.bin_part = (uint32_t*)(ws + L.off_binpart);
+  c.chunks = (HeavyChunk*)(ws + L.off_chunks);
+  c.hacc = (unsigned long long*)(ws + L.off_hacc);
+  c.max_small = L.max_small;
+  c.max_big = L.max_big;
+  c.max_chunks = L.max_chunks;
+  c.max_heavy = L.max_heavy;
+  return c;
+}
+
+uint32_t grid_for(uint64_t work, uint32_t per_block = kBlock,
+                  uint32_t cap = 8192) {
+  uint64_t b = (work + per_block - 1) / per_block;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (uint32_t)b;
+}
+
+uint32_t scan_blocks(uint64_t n) {
+  uint64_t b = (n + 4 * kBlock - 1) / (4 * kBlock);
+  return (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(b, kScanBlocks));
+}
+
+int check_graph(const wl_csr* g) {
+  if (!g) return fail(WL_EINVAL, "graph is NULL");
+  if (g->n >= (1ull << 32))
+    return fail(WL_EOVERFLOW, "n = %llu does not fit 32-bit node ids",
+                (unsigned long long)g->n);
+  if ((g->row_ptr32 == nullptr) == (g->row_ptr64 == nullptr))
+    return fail(WL_EINVAL, "exactly one of row_ptr32/row_ptr64 must be set");
+  if (g->row_ptr32 && g->nnz >= (1ull << 32))
+    return fail(WL_EINVAL, "nnz >= 2^32 needs row_ptr64");
+  if (g->nnz > 0 && g->col_idx == nullptr)
+    return fail(WL_EINVAL, "col_idx is NULL");
+  return WL_OK;
+}
+
+// Reads row_ptr[n] from the device and compares it with nnz.
+int check_nnz_device(const wl_csr* g, hipStream_t s) {
+  uint64_t last = 0;
+  if (g->row_ptr32) {
+    uint32_t v = 0;
+    HIP_TRY(hipMemcpyAsync(&v, g->row_ptr32 + g->n, 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    last = v;
+  } else {
+    HIP_TRY(hipMemcpyAsync(&last, g->row_ptr64 + g->n, 8, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+  }
+  if (last != g->nnz)
+    return fail(WL_EINVAL, "row_ptr[n] = %llu but nnz = %llu",
+                (unsigned long long)last, (unsigned long long)g->nnz);
+  return WL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Device-side validation (WL_VALIDATE=1) and small set-up kernels.
+// ---------------------------------------------------------------------------
+
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_validate(Ctx ctx) {
+  const RP* rp = rowptr<RP>(ctx);
+  for (uint64_t i = blockIdx.x * (uint64_t)kBlock + threadIdx.x; i < ctx.n;
+       i += (uint64_t)gridDim.x * kBlock)
+    if (rp[i + 1] < rp[i]) atomicOr(&ctx.st->err, 1u);
+  for (uint64_t e = blockIdx.x * (uint64_t)kBlock + threadIdx.x; e < ctx.nnz;
+       e += (uint64_t)gridDim.x * kBlock)
+    if (ctx.col[e] >= ctx.n) atomicOr(&ctx.st->err, 2u);
+}
+
+__global__ void __launch_bounds__(kBlock) k_check_colors(Ctx ctx,
+                                                         const uint32_t* col,
+                                                         uint32_t k) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock)
+    if (col[i] >= k) atomicOr(&ctx.st->err, 4u);
+}
+
+__global__ void __launch_bounds__(kBlock) k_iota_zero(Ctx ctx) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock) {
+    ctx.perm[i] = i;
+    ctx.c[i] = 0;
+    ctx.act[i] = ctx.n >= 2 ? 1 : 0;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctx.cstart[0] = 0;
+    ctx.cstart[1] = ctx.n;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_labels_to_z(Ctx ctx,
+                                                        const uint32_t* lab) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock)
+    ctx.z[i] = lab[i];
+}
+
+// Counting sort of the nodes by colour (colours < k): cstart, perm, act.
+__global__ void __launch_bounds__(kBlock) k_count_colors(Ctx ctx, uint32_t k) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i <= k;
+       i += gridDim.x * kBlock)
+    ctx.ids[i] = 0;
+}
+__global__ void __launch_bounds__(kBlock) k_hist_colors(Ctx ctx) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock)
+    atomicAdd(&ctx.ids[ctx.c[i]], 1u);
+}
+// One block: cstart = exclusive scan of ids[0..k]; ids becomes the cursor.
+__global__ void __launch_bounds__(kBlock) k_scan_colors(Ctx ctx, uint32_t k) {
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base <= k; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i <= k ? ctx.ids[i] : 0;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(v, sh, &tot);
+    if (i <= k) {
+      ctx.cstart[i] = carry + ex;
+      ctx.ids[i] = carry + ex;
+    }
+    carry += tot;
+  }
+}
+__global__ void __launch_bounds__(kBlock) k_place_colors(Ctx ctx) {
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock) {
+    const uint32_t c = ctx.c[i];
+    const uint32_t at = atomicAdd(&ctx.ids[c], 1u);
+    ctx.perm[at] = i;
+    ctx.act[i] = (ctx.cstart[c + 1] - ctx.cstart[c]) >= 2 ? 1 : 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// One call's device session.
+// ---------------------------------------------------------------------------
+
+struct Session {
+  Layout L;
+  Ctx ctx;
+  hipStream_t s;
+  bool rp64;
+  bool weighted;
+  DevState host;  // last copy of the device state
+  uint32_t nscan;
+
+  int pull() {
+    HIP_TRY(hipMemcpyAsync(&host, ctx.st, sizeof(DevState), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    return WL_OK;
+  }
+
+  int init_state(uint64_t seed, uint32_t k, uint32_t round, uint32_t max_rounds) {
+    DevState h{};
+    h.k = k;
+    h.round = round;
+    h.max_rounds = max_rounds;
+    h.seed = seed;
+    host = h;
+    HIP_TRY(hipMemcpyAsync(ctx.st, &h, sizeof(DevState), hipMemcpyHostToDevice, s));
+    return WL_OK;
+  }
+
+  int validate_device() {
+    const char* v = getenv("WL_VALIDATE");
+    if (!v || v[0] != '1') return WL_OK;
+    uint32_t g = grid_for(std::max<uint64_t>(L.n, L.nnz));
+    if (rp64)
+      hipLaunchKernelGGL(k_validate<uint64_t>, dim3(g), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_validate<uint32_t>, dim3(g), dim3(kBlock), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    if (host.err & 1u) return fail(WL_EINVAL, "row_ptr is not non-decreasing");
+    if (host.err & 2u) return fail(WL_EINVAL, "a column index is >= n");
+    return WL_OK;
+  }
+
+  // SpMV schedule (row bins and heavy chunks); once per call.
+  int build_schedule() {
+    const uint32_t nb = scan_blocks(L.n);
+    if (rp64)
+      hipLaunchKernelGGL(k_bins_count<uint64_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_bins_count<uint32_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_bins_scan, dim3(1), dim3(kBlock), 0, s, ctx, nb);
+    if (rp64)
+      hipLaunchKernelGGL(k_bins_fill<uint64_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_bins_fill<uint32_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
+    if (rp64)
+      hipLaunchKernelGGL(k_heavy_prep<uint64_t>, dim3(1), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_heavy_prep<uint32_t>, dim3(1), dim3(kBlock), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    return pull();
+  }
+
+  template <typename RP, bool W>
+  void spmv_t() {
+    const DevState& h = host;
+    uint32_t g0 = grid_for((uint64_t)h.bin_cnt[0] * 4);
+    uint32_t g1 = grid_for((uint64_t)h.bin_cnt[1] * 16);
+    uint32_t g2 = grid_for((uint64_t)h.bin_cnt[2] * 64);
+    uint32_t g3 = grid_for((uint64_t)h.n_chunks * 64);
+    if (h.bin_cnt[0])
+      hipLaunchKernelGGL((k_spmv_group<4, RP, W>), dim3(g0), dim3(kBlock), 0, s, ctx, 0);
+    if (h.bin_cnt[1])
+      hipLaunchKernelGGL((k_spmv_group<16, RP, W>), dim3(g1), dim3(kBlock), 0, s, ctx, 1);
+    if (h.bin_cnt[2])
+      hipLaunchKernelGGL((k_spmv_group<64, RP, W>), dim3(g2), dim3(kBlock), 0, s, ctx, 2);
+    if (h.n_chunks) {
+      hipLaunchKernelGGL((k_spmv_heavy<RP, W>), dim3(g3), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_spmv_heavy_fin, dim3(grid_for(h.bin_cnt[3])), dim3(kBlock),
+                         0, s, ctx);
+    }
+  }
+
+  void spmv() {
+    if (rp64) {
+      if (weighted) spmv_t<uint64_t, true>(); else spmv_t<uint64_t, false>();
+    } else {
+      if (weighted) spmv_t<uint32_t, true>(); else spmv_t<uint32_t, false>();
+    }
+  }
+
+  // Relabel by (c, z) for the current grouping; count_round = 0 for the
+  // canonicalisation of the initial labels.
+  int relabel(int count_round) {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_fill_u8, dim3(gn), dim3(kBlock), 0, s, ctx, ctx.flags,
+                       (uint64_t)L.n, (uint8_t)0);
+    hipLaunchKernelGGL(k_segments, dim3(grid_for(host.k, kBlock, 4096)), dim3(kBlock),
+                       0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    for (int pass = 0; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
+      hipLaunchKernelGGL(k_big_tiles, dim3(1), dim3(kBlock), 0, s, ctx, pass);
+      if (pass == 0)
+        hipLaunchKernelGGL(k_big_gather, dim3(2048), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_big_clear,
+                         dim3(grid_for((uint64_t)host.n_big[pass & 1] * kRadix)),
+                         dim3(kBlock), 0, s, ctx, pass);
+      hipLaunchKernelGGL(k_big_hist, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+      hipLaunchKernelGGL(k_big_scan, dim3(std::min<uint32_t>(host.n_big[pass & 1], 4096)),
+                         dim3(kBlock), 0, s, ctx, pass);
+      hipLaunchKernelGGL(k_big_scatter, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+      hipLaunchKernelGGL(k_big_copyback, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+      HIP_LAUNCH_CHECK();
+      if (int r = pull()) return r;
+    }
+    if (host.n_small)
+      hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
+                         dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_scan_part, dim3(nscan), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
+    hipLaunchKernelGGL(k_scan_final, dim3(nscan), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_cstart, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_scatter_colors, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_round_end, dim3(1), dim3(1), 0, s, ctx, count_round);
+    HIP_LAUNCH_CHECK();
+    return pull();
+  }
+
+  int round() {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
+    hipLaunchKernelGGL(k_weights, dim3(gn), dim3(kBlock), 0, s, ctx);
+    spmv();
+    HIP_LAUNCH_CHECK();
+    return relabel(1);
+  }
+};
+
+int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
+                 uint64_t ws_bytes, void* stream) {
+  S.L = make_layout(g->n, g->nnz);
+  if (!ws) return fail(WL_EINVAL, "workspace is NULL");
+  if ((uintptr_t)ws % kAlign)
+    return fail(WL_EINVAL, "workspace must be %llu-byte aligned",
+                (unsigned long long)kAlign);
+  if (ws_bytes < S.L.total)
+    return fail(WL_EBUDGET, "workspace has %llu bytes, %llu needed",
+                (unsigned long long)ws_bytes, (unsigned long long)S.L.total);
+  S.ctx = make_ctx(S.L, g, (uint8_t*)ws, colors);
+  S.s = (hipStream_t)stream;
+  S.rp64 = g->row_ptr64 != nullptr;
+  S.weighted = g->weight != nullptr;
+  S.nscan = scan_blocks(g->n);
+  return WL_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char* wl_last_error(void) { return g_err; }
+
+int wl_workspace_size(const wl_csr* g, uint64_t* bytes_out) {
+  g_err[0] = 0;
+  if (!g || !bytes_out) return fail(WL_EINVAL, "NULL argument");
+  if (g->n >= (1ull << 32)) return fail(WL_EOVERFLOW, "n does not fit 32 bits");
+  *bytes_out = make_layout(g->n, g->nnz).total;
+  return WL_OK;
+}
+
+int wl_batched_workspace_size(const wl_csr* g, uint64_t max_batch_entries,
+                              uint64_t* bytes_out) {
+  (void)max_batch_entries;
+  if (!g || !bytes_out) return fail(WL_EINVAL, "NULL argument");
+  return fail(WL_EINVAL, "batched refinement is not available in this build");
+}
+
+int wl_refine_round(const wl_csr* g, const uint32_t* color_in, uint32_t k_in,
+                    uint64_t seed, uint32_t round, uint32_t* color_out,
+                    uint32_t* k_out, void* workspace, uint64_t ws_bytes,
+                    void* stream) {
+  g_err[0] = 0;
+  if (int r = check_graph(g)) return r;
+  if (!k_out) return fail(WL_EINVAL, "k_out is NULL");
+  if (g->n == 0) {
+    *k_out = 0;
+    return WL_OK;
+  }
+  if (!color_in || !color_out) return fail(WL_EINVAL, "colour buffer is NULL");
+  if (k_in == 0 || k_in > g->n)
+    return fail(WL_EINVAL, "k_in = %u must be in [1, n]", k_in);
+  Session S;
+  if (int r = open_session(S, g, color_out, workspace, ws_bytes, stream)) return r;
+  if (int r = check_nnz_device(g, S.s)) return r;
+  if (int r = S.init_state(seed, k_in, round, round + 1)) return r;
+  if (int r = S.validate_device()) return r;
+  const uint32_t gn = grid_for(g->n, kBlock, 4096);
+  hipLaunchKernelGGL(k_check_colors, dim3(gn), dim3(kBlock), 0, S.s, S.ctx, color_in,
+                     k_in);
+  HIP_LAUNCH_CHECK();
+  if (int r = S.pull()) return r;
+  if (S.host.err & 4u) return fail(WL_EINVAL, "a colour is >= k_in");
+  if (color_out != color_in)
+    HIP_TRY(hipMemcpyAsync(color_out, color_in, 4 * g->n, hipMemcpyDeviceToDevice, S.s));
+  hipLaunchKernelGGL(k_count_colors, dim3(grid_for(k_in + 1)), dim3(kBlock), 0, S.s,
+                     S.ctx, k_in);
+  hipLaunchKernelGGL(k_hist_colors, dim3(gn), dim3(kBlock), 0, S.s, S.ctx);
+  hipLaunchKernelGGL(k_scan_colors, dim3(1), dim3(kBlock), 0, S.s, S.ctx, k_in);
+  hipLaunchKernelGGL(k_place_colors, dim3(gn), dim3(kBlock), 0, S.s, S.ctx);
+  HIP_LAUNCH_CHECK();
+  if (int r = S.build_schedule()) return r;
+  if (int r = S.round()) return r;
+  *k_out = S.host.k;
+  return WL_OK;
+}
+
+int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t seed,
+                       uint32_t max_rounds, uint32_t* color_out, uint32_t* k_out,
+                       uint32_t* rounds_out, void* workspace, uint64_t ws_bytes,
+                       void* stream) {
+  g_err[0] = 0;
+  if (int r = check_graph(g)) return r;
+  if (!k_out || !rounds_out) return fail(WL_EINVAL, "output scalar is NULL");
+  *k_out = 0;
+  *rounds_out = 0;
+  if (g->n == 0) return WL_OK;
+  if (!color_out) return fail(WL_EINVAL, "color_out is NULL");
+  Session S;
+  if (int r = open_session(S, g, color_out, workspace, ws_bytes, stream)) return r;
+  if (int r = check_nnz_device(g, S.s)) return r;
+  const uint32_t cap = max_rounds ? max_rounds : (uint32_t)std::min<uint64_t>(g->n + 1, 0xFFFFFFFFull);
+  if (int r = S.init_state(seed, 1, 0, cap)) return r;
+  if (int r = S.validate_device()) return r;
+  const uint32_t gn = grid_for(g->n, kBlock, 4096);
+  hipLaunchKernelGGL(k_iota_zero, dim3(gn), dim3(kBlock), 0, S.s, S.ctx);
+  HIP_LAUNCH_CHECK();
+  if (init_color) {
+    hipLaunchKernelGGL(k_labels_to_z, dim3(gn), dim3(kBlock), 0, S.s, S.ctx, init_color);
+    HIP_LAUNCH_CHECK();
+    if (int r = S.relabel(0)) return r;
+  }
+  if (int r = S.build_schedule()) return r;
+  while (!S.host.done) {
+    if (int r = S.round()) return r;
+  }
+  *k_out = S.host.k;
+  *rounds_out = S.host.round;
+  if (S.host.done == 2)
+    return fail(WL_EMAXROUNDS, "no stable colouring after %u rounds", S.host.round);
+  return WL_OK;
+}
+
+int wl_stable_coloring_batched(const wl_csr* g_host, const uint32_t* init_host,
+                               uint64_t seed, uint64_t max_batch_entries,
+                               uint32_t* color_out_host, uint32_t* k_out,
+                               uint32_t* rounds_out, uint32_t* outer_out,
+                               int* coarsest_out, void* workspace, uint64_t ws_bytes,
+                               void* stream) {
+  (void)g_host; (void)init_host; (void)seed; (void)max_batch_entries;
+  (void)color_out_host; (void)k_out; (void)rounds_out; (void)outer_out;
+  (void)coarsest_out; (void)workspace; (void)ws_bytes; (void)stream;
+  return fail(WL_EINVAL, "batched refinement is not available in this build");
+}
+
+int wl_verify_stable(const wl_csr* g, const uint32_t* color, uint32_t k,
+                     void* workspace, uint64_t ws_bytes, void* stream) {
+  (void)g; (void)color; (void)k; (void)workspace; (void)ws_bytes; (void)stream;
+  return fail(WL_EINVAL, "stability certificate is not available in this build");
+}
+
+}  // extern "C"

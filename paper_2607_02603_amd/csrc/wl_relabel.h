@@ -1,0 +1,420 @@
+// Relabel step of Algorithm 1 (Section 4.1): the new colour of node i is the
+// rank of the pair (c_i, z_i) among the distinct pairs in lexicographic order.
+//
+// The nodes are kept grouped by colour in 'perm' (class c occupies
+// perm[cstart[c] .. cstart[c+1])), in increasing colour order.  So the
+// lexicographic order of the pairs is: class order, then z inside a class,
+// and the relabel is a segmented sort of z inside every class of two or more
+// nodes:
+//   - classes (and later buckets) of at most kSmallMax nodes are sorted in
+//     LDS by one workgroup (bitonic network);
+//   - larger ones go through most-significant-digit radix passes over 8-bit
+//     digits of z; a bucket whose smallest and largest key agree is finished
+//     at once (equal keys need no order), which is the common case in early
+//     rounds where a large class has few distinct images.
+// Order inside a group of equal pairs is irrelevant, so the passes scatter
+// with atomics.  A byte flag marks the first position of every group; an
+// inclusive scan of the flags gives the ranks; 'cstart' and 'perm' become the
+// grouping of the next round.
+#pragma once
+#include "wl_block.h"
+
+namespace wl {
+
+__device__ __forceinline__ uint32_t digit_of(uint64_t key, int pass) {
+  const int hi = 61 - kRadixBits * pass;
+  const int lo = hi > kRadixBits ? hi - kRadixBits : 0;
+  return (uint32_t)((key >> lo) & ((1ull << (hi - lo)) - 1));
+}
+
+__global__ void k_round_begin(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  st->n_small = 0;
+  st->n_big[0] = 0;
+  st->n_big[1] = 0;
+  st->n_tiles = 0;
+}
+
+__global__ void __launch_bounds__(kBlock) k_fill_u8(Ctx ctx, uint8_t* p,
+                                                    uint64_t cnt, uint8_t v) {
+  if (ctx.st->done) return;
+  for (uint64_t i = blockIdx.x * (uint64_t)kBlock + threadIdx.x; i < cnt;
+       i += (uint64_t)gridDim.x * kBlock)
+    p[i] = v;
+}
+
+// One entry per class: flag its first position, queue it if it has >= 2
+// members.
+__global__ void __launch_bounds__(kBlock) k_segments(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t k = st->k;
+  for (uint32_t j = blockIdx.x * kBlock + threadIdx.x; j < k;
+       j += gridDim.x * kBlock) {
+    const uint32_t s = ctx.cstart[j], e = ctx.cstart[j + 1];
+    if (e <= s) continue;
+    ctx.flags[s] = 1;
+    const uint32_t len = e - s;
+    if (len < 2) continue;
+    if (len <= kSmallMax) {
+      uint32_t idx = atomicAdd(&st->n_small, 1u);
+      ctx.small_list[idx] = make_uint2(s, len);
+    } else {
+      uint32_t idx = atomicAdd(&st->n_big[0], 1u);
+      ctx.big_list0[idx] = make_uint2(s, len);
+    }
+  }
+}
+
+__device__ __forceinline__ const uint2* big_list(const Ctx& c, int which) {
+  return which ? c.big_list1 : c.big_list0;
+}
+__device__ __forceinline__ uint2* big_list_w(const Ctx& c, int which) {
+  return which ? c.big_list1 : c.big_list0;
+}
+
+// One block: tile offsets of the big list used by 'pass'.
+__global__ void __launch_bounds__(kBlock) k_big_tiles(Ctx ctx, int pass) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const int cur = pass & 1;
+  const uint32_t nb = st->n_big[cur];
+  if (nb == 0) return;
+  const uint2* L = big_list(ctx, cur);
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nb; base += kBlock) {
+    uint32_t i = base + threadIdx.x;
+    uint32_t t = i < nb ? (L[i].y + kTile - 1) / kTile : 0;
+    uint32_t tot;
+    uint32_t ex = block_excl_scan(t, sh, &tot);
+    if (i < nb) ctx.tile_off[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) {
+    ctx.tile_off[nb] = carry;
+    st->n_tiles = carry;
+    st->n_big[cur ^ 1] = 0;
+  }
+}
+
+// Segment index of tile t: last i with tile_off[i] <= t.
+__device__ __forceinline__ uint32_t tile_segment(const uint32_t* off,
+                                                 uint32_t nb, uint32_t t) {
+  uint32_t lo = 0, hi = nb - 1;
+  while (lo < hi) {
+    uint32_t mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= t)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  return lo;
+}
+
+struct TileRange {
+  uint32_t seg, beg, end, seg_start;
+};
+
+__device__ __forceinline__ TileRange tile_range(const Ctx& ctx, int cur,
+                                                uint32_t nb, uint32_t t) {
+  const uint2* L = big_list(ctx, cur);
+  TileRange r;
+  r.seg = tile_segment(ctx.tile_off, nb, t);
+  const uint2 s = L[r.seg];
+  r.seg_start = s.x;
+  r.beg = s.x + (t - ctx.tile_off[r.seg]) * kTile;
+  r.end = min(s.x + s.y, r.beg + kTile);
+  return r;
+}
+
+// First pass only: keys of the big segments in position order.
+__global__ void __launch_bounds__(kBlock) k_big_gather(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t nb = st->n_big[0], nt = st->n_tiles;
+  if (nb == 0) return;
+  for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
+    TileRange r = tile_range(ctx, 0, nb, t);
+    for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock)
+      ctx.keys[p] = ctx.z[ctx.perm[p]];
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_big_clear(Ctx ctx, int pass) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t nb = st->n_big[pass & 1];
+  const uint32_t tot = nb * kRadix;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < tot;
+       i += gridDim.x * kBlock) {
+    ctx.bhist[i] = 0;
+    ctx.bmin[i] = ~0ull;
+    ctx.bmax[i] = 0;
+  }
+}
+
+// Histogram of the pass digit per (segment, bucket), with min/max key.
+__global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const int cur = pass & 1;
+  const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
+  if (nb == 0) return;
+  __shared__ uint32_t cnt[kRadix];
+  __shared__ unsigned long long mn[kRadix], mx[kRadix];
+  for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
+    TileRange r = tile_range(ctx, cur, nb, t);
+    cnt[threadIdx.x] = 0;
+    mn[threadIdx.x] = ~0ull;
+    mx[threadIdx.x] = 0;
+    __syncthreads();
+    for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
+      const uint64_t key = ctx.keys[p];
+      const uint32_t d = digit_of(key, pass);
+      atomicAdd(&cnt[d], 1u);
+      atomicMin(&mn[d], (unsigned long long)key);
+      atomicMax(&mx[d], (unsigned long long)key);
+    }
+    __syncthreads();
+    const uint32_t b = threadIdx.x;
+    if (cnt[b]) {
+      const uint32_t g = r.seg * kRadix + b;
+      atomicAdd(&ctx.bhist[g], cnt[b]);
+      atomicMin(&ctx.bmin[g], mn[b]);
+      atomicMax(&ctx.bmax[g], mx[b]);
+    }
+    __syncthreads();
+  }
+}
+
+// One block per big segment: bucket offsets, flags at bucket starts, and the
+// follow-up work: finished (one key), LDS sort, or another radix pass.
+__global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const int cur = pass & 1;
+  const uint32_t nb = st->n_big[cur];
+  const uint2* L = big_list(ctx, cur);
+  uint2* N = big_list_w(ctx, cur ^ 1);
+  __shared__ uint32_t sh[kBlock / kWave];
+  for (uint32_t sgi = blockIdx.x; sgi < nb; sgi += gridDim.x) {
+    const uint2 s = L[sgi];
+    const uint32_t g = sgi * kRadix + threadIdx.x;
+    const uint32_t h = ctx.bhist[g];
+    uint32_t tot;
+    const uint32_t off = block_excl_scan(h, sh, &tot);
+    ctx.bcur[g] = off;
+    if (h) {
+      const uint32_t pos = s.x + off;
+      ctx.flags[pos] = 1;
+      if (h >= 2 && ctx.bmin[g] != ctx.bmax[g]) {
+        if (h <= kSmallMax) {
+          uint32_t idx = atomicAdd(&st->n_small, 1u);
+          ctx.small_list[idx] = make_uint2(pos, h | kMatBit);
+        } else {
+          uint32_t idx = atomicAdd(&st->n_big[cur ^ 1], 1u);
+          N[idx] = make_uint2(pos, h);
+        }
+      }
+    }
+  }
+}
+
+// Scatter every element of the big segments into its bucket (keys_tmp,
+// perm_tmp).  Slots inside a bucket are taken with atomics.
+__global__ void __launch_bounds__(kBlock) k_big_scatter(Ctx ctx, int pass) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const int cur = pass & 1;
+  const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
+  if (nb == 0) return;
+  __shared__ uint32_t lcnt[kRadix];
+  __shared__ uint32_t lbase[kRadix];
+  for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
+    TileRange r = tile_range(ctx, cur, nb, t);
+    lcnt[threadIdx.x] = 0;
+    __syncthreads();
+    uint32_t slot[kTilePerThread];
+    uint32_t dg[kTilePerThread];
+#pragma unroll
+    for (uint32_t q = 0; q < kTilePerThread; ++q) {
+      const uint32_t p = r.beg + q * kBlock + threadIdx.x;
+      if (p < r.end) {
+        dg[q] = digit_of(ctx.keys[p], pass);
+        slot[q] = atomicAdd(&lcnt[dg[q]], 1u);
+      }
+    }
+    __syncthreads();
+    const uint32_t b = threadIdx.x;
+    if (lcnt[b]) lbase[b] = atomicAdd(&ctx.bcur[r.seg * kRadix + b], lcnt[b]);
+    __syncthreads();
+#pragma unroll
+    for (uint32_t q = 0; q < kTilePerThread; ++q) {
+      const uint32_t p = r.beg + q * kBlock + threadIdx.x;
+      if (p < r.end) {
+        const uint32_t dst = r.seg_start + lbase[dg[q]] + slot[q];
+        ctx.keys_tmp[dst] = ctx.keys[p];
+        ctx.perm_tmp[dst] = ctx.perm[p];
+      }
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_big_copyback(Ctx ctx, int pass) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const int cur = pass & 1;
+  const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
+  if (nb == 0) return;
+  for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
+    TileRange r = tile_range(ctx, cur, nb, t);
+    for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
+      ctx.keys[p] = ctx.keys_tmp[p];
+      ctx.perm[p] = ctx.perm_tmp[p];
+    }
+  }
+}
+
+// One workgroup per small segment: bitonic sort of (z, node) in LDS, then
+// flags where z changes.
+__global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t ns = st->n_small;
+  __shared__ unsigned long long skey[kSmallMax];
+  __shared__ uint32_t sval[kSmallMax];
+  for (uint32_t si = blockIdx.x; si < ns; si += gridDim.x) {
+    const uint2 sg = ctx.small_list[si];
+    const uint32_t s = sg.x, len = sg.y & ~kMatBit;
+    const bool mat = (sg.y & kMatBit) != 0;
+    uint32_t P = 2;
+    while (P < len) P <<= 1;
+    for (uint32_t t = threadIdx.x; t < P; t += kBlock) {
+      if (t < len) {
+        const uint32_t v = ctx.perm[s + t];
+        sval[t] = v;
+        skey[t] = mat ? ctx.keys[s + t] : ctx.z[v];
+      } else {
+        sval[t] = 0;
+        skey[t] = ~0ull;
+      }
+    }
+    __syncthreads();
+    for (uint32_t kk = 2; kk <= P; kk <<= 1) {
+      for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+        for (uint32_t i = threadIdx.x; i < P; i += kBlock) {
+          const uint32_t l = i ^ j;
+          if (l > i) {
+            const bool asc = (i & kk) == 0;
+            const unsigned long long a = skey[i], b = skey[l];
+            if ((a > b) == asc) {
+              skey[i] = b;
+              skey[l] = a;
+              const uint32_t tv = sval[i];
+              sval[i] = sval[l];
+              sval[l] = tv;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+    for (uint32_t t = threadIdx.x; t < len; t += kBlock) {
+      ctx.perm[s + t] = sval[t];
+      if (t > 0 && skey[t] != skey[t - 1]) ctx.flags[s + t] = 1;
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Device-wide inclusive scan of the byte flags -> ranks (ids = scan - 1).
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void scan_range(uint32_t n, uint32_t b, uint32_t nblk,
+                                           uint32_t* lo, uint32_t* hi) {
+  const uint32_t per = ((n + nblk - 1) / nblk + kBlock - 1) / kBlock * kBlock;
+  *lo = min(n, b * per);
+  *hi = min(n, *lo + per);
+}
+
+__global__ void __launch_bounds__(kBlock) k_scan_part(Ctx ctx) {
+  if (ctx.st->done) return;
+  uint32_t lo, hi;
+  scan_range(ctx.n, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t s = 0;
+  for (uint32_t p = lo + threadIdx.x; p < hi; p += kBlock) s += ctx.flags[p];
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t tot;
+  block_excl_scan(s, sh, &tot);
+  if (threadIdx.x == 0) ctx.scan_part[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(kBlock) k_scan_top(Ctx ctx, uint32_t nblk) {
+  if (ctx.st->done) return;
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nblk; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i < nblk ? ctx.scan_part[i] : 0;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(v, sh, &tot);
+    if (i < nblk) ctx.scan_part[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) ctx.st->k_new = carry;
+}
+
+__global__ void __launch_bounds__(kBlock) k_scan_final(Ctx ctx) {
+  if (ctx.st->done) return;
+  uint32_t lo, hi;
+  scan_range(ctx.n, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t run = ctx.scan_part[blockIdx.x];
+  __shared__ uint32_t sh[kBlock / kWave];
+  for (uint32_t base = lo; base < hi; base += kBlock) {
+    const uint32_t p = base + threadIdx.x;
+    const uint32_t f = p < hi ? ctx.flags[p] : 0;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(f, sh, &tot);
+    if (p < hi) ctx.ids[p] = run + ex + f - 1;
+    run += tot;
+  }
+}
+
+// New class starts, then colours and activity per node.
+__global__ void __launch_bounds__(kBlock) k_cstart(Ctx ctx) {
+  if (ctx.st->done) return;
+  for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n;
+       p += gridDim.x * kBlock)
+    if (ctx.flags[p]) ctx.cstart[ctx.ids[p]] = p;
+  if (blockIdx.x == 0 && threadIdx.x == 0) ctx.cstart[ctx.st->k_new] = ctx.n;
+}
+
+__global__ void __launch_bounds__(kBlock) k_scatter_colors(Ctx ctx) {
+  if (ctx.st->done) return;
+  for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n;
+       p += gridDim.x * kBlock) {
+    const uint32_t v = ctx.perm[p], id = ctx.ids[p];
+    ctx.c[v] = id;
+    ctx.act[v] = (ctx.cstart[id + 1] - ctx.cstart[id]) >= 2 ? 1 : 0;
+  }
+}
+
+__global__ void k_round_end(Ctx ctx, int count_round) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t kn = st->k_new;
+  if (count_round) {
+    st->round += 1;
+    if (kn == st->k)
+      st->done = 1;
+    else if (st->round >= st->max_rounds)
+      st->done = 2;
+  }
+  st->k = kn;
+}
+
+}  // namespace wl

@@ -1,0 +1,105 @@
+"""The C ABI library loads and exports every symbol include/wl.h declares;
+host-only argument checks (no GPU work is started by these calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_02603_amd as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _ensure_built():
+    if not os.path.exists(wl.LIB_PATH):
+        from paper_2607_02603_amd import build
+        build.build_wl()
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "wl.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(wl_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    syms = declared_symbols()
+    for name in ("wl_refine_round", "wl_stable_coloring", "wl_stable_coloring_batched",
+                 "wl_workspace_size", "wl_verify_stable", "wl_last_error"):
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol():
+    _ensure_built()
+    L = ctypes.CDLL(wl.LIB_PATH)
+    for name in declared_symbols():
+        assert hasattr(L, name), name
+    assert sorted(wl.EXPORTED) == declared_symbols()
+
+
+def _csr(n, nnz, rp32=True):
+    s = wl.WlCsr()
+    s.n = n
+    s.nnz = nnz
+    s.row_ptr32 = 8 if rp32 else None
+    s.row_ptr64 = None if rp32 else 8
+    s.col_idx = 16 if nnz else None
+    s.weight = None
+    return s
+
+
+def test_workspace_size_host_only():
+    _ensure_built()
+    L = wl.lib()
+    out = ctypes.c_uint64(0)
+    s = _csr(1000, 5000)
+    assert L.wl_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    small = out.value
+    s = _csr(100000, 5000000)
+    assert L.wl_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    assert out.value > small
+    # linear in n: roughly 60-70 bytes per node plus a little per entry
+    assert 40 * 100000 < out.value < 120 * 100000 + 64 * 5000000 // 2048 * 1024
+
+
+def test_host_side_errors():
+    _ensure_built()
+    L = wl.lib()
+    out = ctypes.c_uint64(0)
+    assert L.wl_workspace_size(None, ctypes.byref(out)) == wl.WL_EINVAL
+    big = _csr(1 << 32, 0)
+    assert L.wl_workspace_size(ctypes.byref(big), ctypes.byref(out)) == wl.WL_EOVERFLOW
+    assert b"32" in L.wl_last_error()
+    # both row pointers set
+    s = _csr(10, 20)
+    s.row_ptr64 = 8
+    k = ctypes.c_uint32(0)
+    r = ctypes.c_uint32(0)
+    code = L.wl_stable_coloring(ctypes.byref(s), None, 0, 0, ctypes.c_void_p(8),
+                                ctypes.byref(k), ctypes.byref(r), ctypes.c_void_p(256),
+                                1 << 20, None)
+    assert code == wl.WL_EINVAL
+    assert b"row_ptr" in L.wl_last_error()
+    # NULL outputs
+    s = _csr(10, 20)
+    assert L.wl_stable_coloring(ctypes.byref(s), None, 0, 0, None, None, None, None, 0,
+                                None) == wl.WL_EINVAL
+    # k_in out of range in wl_refine_round (checked before any device work)
+    code = L.wl_refine_round(ctypes.byref(s), ctypes.c_void_p(8), 0, 0, 0,
+                             ctypes.c_void_p(8), ctypes.byref(k), ctypes.c_void_p(256),
+                             1 << 20, None)
+    assert code == wl.WL_EINVAL
+    # workspace too small / misaligned are reported before any device work
+    s = _csr(0, 0)
+    assert L.wl_stable_coloring(ctypes.byref(s), None, 0, 0, ctypes.c_void_p(8),
+                                ctypes.byref(k), ctypes.byref(r), None, 0,
+                                None) == wl.WL_OK
+    assert k.value == 0 and r.value == 0
+
+
+def test_binding_refuses_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(wl, "_LIB", None)
+    monkeypatch.setattr(wl, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        wl.lib()
