@@ -1,0 +1,185 @@
+"""Benchmark: randomized 1-WL stable colouring on one MI355X.
+
+A step is one whole call of wl_stable_coloring (canonical start, every
+SpMV + relabel round, the confirming round) on a graph already resident in
+HBM.  Default workload: undirected R-MAT scale 27, edge factor 16,
+(a, b, c, d) = (0.57, 0.19, 0.19, 0.05), symmetrised and deduplicated,
+uint64 row pointers, generated on the GPU from seed 0.
+
+Prints one JSON line: GTEPS per refinement round (directed CSR entries x
+rounds / time-to-stable), time-to-stable in ms_per_step, the roofline of the
+dominant kernel and the CPU oracle timed on a bounded sample.
+"""
+import argparse
+import json
+import os
+import subprocess
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+WORKLOADS = {
+    "er": dict(desc="Erdos-Renyi G(n=20000, m=80000), seed 0"),
+    "grid": dict(desc="2D grid 1024x1024, 4-neighbour"),
+    "chunglu": dict(desc="Chung-Lu n=4e6, 64e6 sampled pairs, exponent 2.1, seed 0"),
+    "rmat27": dict(desc="R-MAT scale 27, edge factor 16, (0.57,0.19,0.19,0.05), "
+                        "symmetrised+dedup, seed 0"),
+}
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def make_graph(name, device):
+    import torch
+    from paper_2607_02603_amd import inputs
+    import paper_2607_02603_amd as wl
+    if name == "er":
+        g = inputs.er_graph()
+    elif name == "grid":
+        g = inputs.grid_graph(1024)
+    elif name == "chunglu":
+        g = inputs.chung_lu(device=device)
+    elif name == "rmat27":
+        g = inputs.rmat(27, 16, device=device)
+    else:
+        raise SystemExit(f"unknown workload {name}")
+    if isinstance(g.row_ptr, torch.Tensor):
+        rp = g.row_ptr
+        if g.nnz < 2**31 and name != "rmat27":
+            rp = rp.to(torch.int32)
+        return wl.Graph(g.n, rp, g.col), g
+    return wl.Graph.from_numpy(g.n, g.row_ptr, g.col, device=device), g
+
+
+def cpu_baseline(dg, seconds_target=15.0):
+    """The CPU oracle (one randomized round: image + relabel) on a bounded
+    sample of the same graph: the first rows of the CSR, with a pseudo-random
+    colouring of 2^20 colours.  Returns GTEPS of the sample."""
+    import numpy as np
+    import oracle
+    rp = dg.row_ptr.cpu().numpy().astype(np.uint64)
+    n = dg.n
+    # grow the sample until the oracle takes a few seconds, then extrapolate
+    rows = min(n, 1 << 16)
+    rng = np.random.default_rng(0)
+    colors = rng.integers(0, 1 << 20, size=n, dtype=np.uint32)
+    best = None
+    while True:
+        m_s = int(rp[rows])
+        col = dg.col_idx[:m_s].cpu().numpy().view(np.uint32)
+        sub_rp = rp[: rows + 1].copy()
+        t0 = time.perf_counter()
+        z = oracle.image(sub_rp, col, None, colors, 1 << 20, 0, 1)
+        oracle.relabel(colors[:rows], z)
+        dt = time.perf_counter() - t0
+        best = (rows, m_s, dt)
+        if dt > seconds_target / 3 or rows == n:
+            break
+        rows = min(n, rows * 4)
+    rows, m_s, dt = best
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": m_s / dt / 1e9, "unit": "GTEPS", "cores": threads,
+            "kind": "oracle",
+            "sample": f"one oracle round (image + relabel) over the first {rows} rows "
+                      f"({m_s} entries) of the same graph, 2^20 pseudo-random colours, "
+                      f"{dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="rmat27", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_02603_amd as wl
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    dg, _ = make_graph(args.workload, dev)
+    torch.cuda.synchronize()
+    log(f"graph {args.workload}: n={dg.n} nnz={dg.nnz} built in "
+        f"{time.perf_counter() - t0:.1f}s")
+    ws = wl.workspace(wl.wl_workspace_size(dg), dev)
+    colors = torch.empty(dg.n, dtype=torch.int32, device=dev)
+    for i in range(args.warmup):
+        _, k, rounds = wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
+        log(f"warmup {i}: colours={k} rounds={rounds}")
+    # untimed run: work of every SpMV launch (rows, gathered entries)
+    wl.wl_stats_enable(wl.WL_STATS_TIME | wl.WL_STATS_WORK)
+    wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
+    work = wl.wl_stats_get()
+    # timed runs: HIP events around every SpMV launch on the library's stream
+    wl.wl_stats_enable(wl.WL_STATS_TIME)
+    torch.cuda.synchronize()
+    times, spmv_ms = [], []
+    for i in range(args.steps):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        _, k, rounds = wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
+        torch.cuda.synchronize()
+        times.append(time.perf_counter() - t1)
+        st = wl.wl_stats_get()
+        spmv_ms.append(st["spmv_ms"])
+        log(f"step {i}: {times[-1] * 1e3:.2f} ms colours={k} rounds={rounds} "
+            f"spmv {st['spmv_ms']:.2f} ms in {st['spmv_launches']} launches")
+    wl.wl_stats_enable(0)
+    step_s = sum(times) / len(times)
+    gteps = dg.nnz * rounds / step_s / 1e9
+    # Algorithmic bytes of the SpMV kernel: 4 B column index + 8 B gathered
+    # value per entry, row pointer + 8 B image per row.
+    rp_bytes = 8 if dg.row_ptr.dtype == torch.int64 else 4
+    spmv_bytes = (12 * work["spmv_entries"] + (rp_bytes + 8) * work["spmv_rows"]
+                  + (rp_bytes + 8) * work["uniform_rows"])
+    spmv_s = sum(spmv_ms) / len(spmv_ms) / 1e3
+    launches = max(1, work["spmv_launches"])
+    achieved = spmv_bytes / spmv_s / 1e9 if spmv_s > 0 else 0.0
+    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                "kernel": "k_spmv", "launches_per_step": launches,
+                "avg_launch_ms": spmv_s * 1e3 / launches,
+                "bytes_per_launch": spmv_bytes / launches}
+    model_bytes = (12 * dg.nnz + (36 + rp_bytes) * dg.n) * rounds
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(dg)
+        log(f"cpu baseline: {cpu}")
+    out = {
+        "metric": "GTEPS per refinement round (directed CSR entries x rounds / "
+                  "time-to-stable-coloring)",
+        "value": gteps,
+        "unit": "GTEPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.workload]["desc"], "n": dg.n,
+                   "nnz": dg.nnz, "colours": k, "rounds": rounds,
+                   "time_to_stable_ms": step_s * 1e3,
+                   "spmv_ms_per_step": spmv_s * 1e3,
+                   "model_round_bytes_frac": model_bytes / step_s / 1e9 / HBM_PEAK_GBS},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

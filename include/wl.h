@@ -153,6 +153,29 @@ int wl_verify_stable(const wl_csr *g, const uint32_t *color, uint32_t k,
 /* Message for the last non-zero return on this thread ("" if none). */
 const char *wl_last_error(void);
 
+/* Diagnostics (instrumentation of this library, not part of the method).
+ * wl_stats_enable(flags) turns them on for the calling thread:
+ *   WL_STATS_TIME  record HIP events on 'stream' around every SpMV launch
+ *                  and around the whole call;
+ *   WL_STATS_WORK  also count, with one extra reduction kernel per round,
+ *                  the rows and CSR entries the SpMV launches read (this
+ *                  adds device work: use it in an untimed run).
+ * wl_stats_get() returns the figures of the last in-core call on this thread.
+ * Both return WL_OK, or WL_EINVAL for a NULL pointer / unknown flag. */
+#define WL_STATS_TIME 1
+#define WL_STATS_WORK 2
+typedef struct wl_stats {
+    uint32_t rounds;          /* rounds of the last call                    */
+    uint32_t spmv_launches;   /* SpMV launches in the last call             */
+    double spmv_ms;           /* their summed device time (WL_STATS_TIME)   */
+    double call_ms;           /* device time of the whole call              */
+    uint64_t spmv_rows;       /* rows whose image was computed (WORK)       */
+    uint64_t spmv_entries;    /* CSR entries gathered (WORK)                */
+    uint64_t uniform_rows;    /* rows done by the one-colour shortcut (WORK)*/
+} wl_stats;
+int wl_stats_enable(int flags);
+int wl_stats_get(wl_stats *out);
+
 #ifdef __cplusplus
 }
 #endif

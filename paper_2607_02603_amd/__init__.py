@@ -29,13 +29,26 @@ _NAMES = {-1: "WL_EINVAL", -2: "WL_EBUDGET", -3: "WL_EOVERFLOW",
 
 EXPORTED = ["wl_workspace_size", "wl_batched_workspace_size", "wl_refine_round",
             "wl_stable_coloring", "wl_stable_coloring_batched", "wl_verify_stable",
-            "wl_last_error"]
+            "wl_stats_enable", "wl_stats_get", "wl_last_error"]
+
+WL_STATS_TIME = 1
+WL_STATS_WORK = 2
 
 
 class WlError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__(f"{_NAMES.get(code, code)}: {msg}")
         self.code = code
+
+
+class WlStats(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_uint32), ("spmv_launches", ctypes.c_uint32),
+                ("spmv_ms", ctypes.c_double), ("call_ms", ctypes.c_double),
+                ("spmv_rows", ctypes.c_uint64), ("spmv_entries", ctypes.c_uint64),
+                ("uniform_rows", ctypes.c_uint64)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
 
 
 class WlCsr(ctypes.Structure):
@@ -65,6 +78,8 @@ def lib():
         L.wl_stable_coloring_batched.argtypes = [P(WlCsr), vp, u64, u64, vp, P(u32),
                                                  P(u32), P(u32), P(i32), vp, u64, vp]
         L.wl_verify_stable.argtypes = [P(WlCsr), vp, u32, vp, u64, vp]
+        L.wl_stats_enable.argtypes = [i32]
+        L.wl_stats_get.argtypes = [P(WlStats)]
         L.wl_last_error.restype = ctypes.c_char_p
         for f in EXPORTED[:-1]:
             getattr(L, f).restype = i32
@@ -232,3 +247,15 @@ def wl_verify_stable(g, color, k, ws=None, stream=None):
         return False
     _check(code)
     return True
+
+
+def wl_stats_enable(flags):
+    """Turn diagnostics on for this thread (WL_STATS_TIME | WL_STATS_WORK)."""
+    _check(lib().wl_stats_enable(flags))
+
+
+def wl_stats_get():
+    """Diagnostics of the last in-core call on this thread, as a dict."""
+    st = WlStats()
+    _check(lib().wl_stats_get(ctypes.byref(st)))
+    return st.as_dict()

@@ -8,6 +8,7 @@ namespace wl {
 
 constexpr int kBlock = 256;          // threads per workgroup (4 waves)
 constexpr uint32_t kSmallMax = 2048; // class/bucket size sorted in LDS
+constexpr uint32_t kTinyMax = 64;    // class/bucket size sorted in one wave
 constexpr uint32_t kTile = 4096;     // elements per tile in the MSD passes
 constexpr uint32_t kTilePerThread = kTile / kBlock;
 constexpr int kRadixBits = 8;
@@ -17,6 +18,7 @@ constexpr uint32_t kMatBit = 0x80000000u;  // small segment keys are in 'keys'
 constexpr uint32_t kHeavyChunk = 4096;     // entries per heavy-row chunk
 constexpr int kNumBins = 4;                // row-length bins of the SpMV
 constexpr int kScanBlocks = 1024;          // blocks of the device-wide scans
+constexpr uint32_t kTableMax = 65535;      // largest k of the compact gathers
 
 // Row-length bins of the SpMV: lanes per row.
 //   bin 0: len <= 8        4 lanes
@@ -41,14 +43,26 @@ struct DevState {
   uint32_t n_chunks;    // heavy-row chunks of the SpMV schedule
   uint32_t bin_cnt[kNumBins];
   uint32_t bin_start[kNumBins];
-  uint32_t pad[5];
+  uint32_t n_tiny;      // entries in the tiny-segment list (<= 64 nodes)
+  uint32_t pad[4];
   uint64_t seed;
+  unsigned long long work_rows;     // diagnostics: rows the SpMV computed
+  unsigned long long work_entries;  // diagnostics: entries it gathered
+  unsigned long long work_uniform;  // diagnostics: rows of the 1-colour path
 };
 
 struct HeavyChunk {
-  uint64_t beg, end;  // entry range
-  uint32_t row;       // node
-  uint32_t h;         // index of the heavy row (accumulator slot)
+  uint64_t beg;   // first entry
+  uint32_t len;   // entries (<= kHeavyChunk)
+  uint32_t row;   // node
+  uint32_t h;     // index of the heavy row (accumulator slot)
+  uint32_t nc;    // chunks of that row
+};
+
+// Block ranges of the single SpMV launch: [0, heavy) heavy chunks,
+// [heavy, b2) one wave per row, [b2, b1) 16 lanes per row, [b1, b0) 4 lanes.
+struct SpmvGrid {
+  uint32_t heavy, b2, b1, b0;
 };
 
 // Every pointer a kernel may touch.  Passed by value.
@@ -62,6 +76,9 @@ struct Ctx {
   DevState* st;
   uint32_t* c;         // colours, node order
   uint64_t* x;         // per-node random value of the round
+  uint64_t* wtab;      // per-colour random values (k <= 65535)
+  uint16_t* c16;       // compact colours (k <= 65535)
+  uint8_t* c8;         // compact colours (k <= 255)
   uint64_t* z;         // image A x
   uint32_t* perm;      // nodes grouped by colour (positions)
   uint32_t* perm_tmp;
@@ -71,7 +88,8 @@ struct Ctx {
   uint8_t* act;        // 1 if the node's class has >= 2 members
   uint32_t* ids;       // inclusive scan of flags minus one
   uint32_t* cstart;    // class c occupies perm[cstart[c] .. cstart[c+1])
-  uint2* small_list;   // (start, len | kMatBit)
+  uint2* small_list;   // (start, len | kMatBit), 64 < len <= kSmallMax
+  uint2* tiny_list;    // (start, len | kMatBit), 2 <= len <= 64
   uint2* big_list0;
   uint2* big_list1;
   uint32_t* tile_off;  // tiles of the current big list (exclusive scan)
@@ -84,7 +102,10 @@ struct Ctx {
   uint32_t* bin_part;  // kNumBins * kScanBlocks
   HeavyChunk* chunks;
   unsigned long long* hacc;  // two accumulators per heavy row
+  uint32_t* hcnt;            // finished chunks per heavy row
   uint32_t max_small, max_big, max_chunks, max_heavy;
+  int weighted;
+  int nt_stream;       // stream col_idx with non-temporal loads
 };
 
 }  // namespace wl

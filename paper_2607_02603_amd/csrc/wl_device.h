@@ -55,6 +55,13 @@ __device__ __forceinline__ uint64_t mul_small_fold(uint32_t a, uint64_t x) {
   return (lo & kP) + ((hi << 3) | (lo >> 61));
 }
 
+// a * b mod p for canonical a, b.
+__device__ __forceinline__ uint64_t mulp(uint64_t a, uint64_t b) {
+  const uint64_t lo = a * b;
+  const uint64_t hi = __umul64hi(a, b);
+  return fold61((lo & kP) + ((hi << 3) | (lo >> 61)));
+}
+
 // ---------------------------------------------------------------------------
 // SplitMix64 (Steele, Lea, Flood 2014) and the per-colour random values.
 // ---------------------------------------------------------------------------

@@ -23,6 +23,8 @@ using namespace wl;
 namespace {
 
 thread_local char g_err[512] = "";
+thread_local int g_stats_flags = 0;
+thread_local wl_stats g_stats{};
 
 int fail(int code, const char* fmt, ...) {
   va_list ap;
@@ -54,9 +56,9 @@ struct Layout {
   uint64_t n, nnz;
   uint32_t max_small, max_big, max_chunks, max_heavy;
   uint64_t off_st, off_x, off_z, off_keys, off_keys_tmp, off_perm, off_perm_tmp,
-      off_ids, off_cstart, off_flags, off_act, off_small, off_big0, off_big1,
+      off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
-      off_binpart, off_chunks, off_hacc;
+      off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16;
   uint64_t total;
 };
 
@@ -85,7 +87,8 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_cstart = take(4 * (n + 2));
   L.off_flags = take(n + 1);
   L.off_act = take(n + 1);
-  L.off_small = take(8ull * L.max_small);
+  L.off_small = take(8ull * (n / (kTinyMax + 1) + 1));
+  L.off_tiny = take(8ull * L.max_small);
   L.off_big0 = take(8ull * L.max_big);
   L.off_big1 = take(8ull * L.max_big);
   L.off_tile = take(4ull * (L.max_big + 1));
@@ -98,6 +101,9 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_binpart = take(4ull * kNumBins * kScanBlocks);
   L.off_chunks = take(sizeof(HeavyChunk) * (uint64_t)L.max_chunks);
   L.off_hacc = take(16ull * L.max_heavy);
+  L.off_hcnt = take(4ull * L.max_heavy);
+  L.off_wtab = take(8ull * std::min<uint64_t>(n, kTableMax));
+  L.off_c16 = take(2 * n);
   L.total = o;
   return L;
 }
@@ -123,6 +129,7 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.flags = ws + L.off_flags;
   c.act = ws + L.off_act;
   c.small_list = (uint2*)(ws + L.off_small);
+  c.tiny_list = (uint2*)(ws + L.off_tiny);
   c.big_list0 = (uint2*)(ws + L.off_big0);
   c.big_list1 = (uint2*)(ws + L.off_big1);
   c.tile_off = (uint32_t*)(ws + L.off_tile);
@@ -135,6 +142,15 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.bin_part = (uint32_t*)(ws + L.off_binpart);
   c.chunks = (HeavyChunk*)(ws + L.off_chunks);
   c.hacc = (unsigned long long*)(ws + L.off_hacc);
+  c.hcnt = (uint32_t*)(ws + L.off_hcnt);
+  c.wtab = (uint64_t*)(ws + L.off_wtab);
+  c.c16 = (uint16_t*)(ws + L.off_c16);
+  c.c8 = ws + L.off_c16;
+  c.weighted = g->weight != nullptr;
+  {
+    const char* nt = getenv("WL_NT_STREAM");
+    c.nt_stream = nt && nt[0] == '1';
+  }
   c.max_small = L.max_small;
   c.max_big = L.max_big;
   c.max_chunks = L.max_chunks;
@@ -279,11 +295,59 @@ struct Session {
   bool weighted;
   DevState host;  // last copy of the device state
   uint32_t nscan;
+  // diagnostics
+  int sflags = 0;
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  bool spmv_pending = false;
+  wl_stats stats{};
+
+  ~Session() {
+    for (hipEvent_t& e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+
+  int stats_begin() {
+    sflags = g_stats_flags;
+    stats = wl_stats{};
+    if (sflags & WL_STATS_TIME) {
+      for (hipEvent_t& e : ev) HIP_TRY(hipEventCreate(&e));
+      HIP_TRY(hipEventRecord(ev[2], s));
+    }
+    return WL_OK;
+  }
+
+  // after a synchronising pull: fold the timed SpMV launch in
+  int stats_collect() {
+    if ((sflags & WL_STATS_TIME) && spmv_pending) {
+      float ms = 0;
+      HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
+      stats.spmv_ms += ms;
+      spmv_pending = false;
+    }
+    return WL_OK;
+  }
+
+  int stats_end() {
+    if (sflags & WL_STATS_TIME) {
+      HIP_TRY(hipEventRecord(ev[3], s));
+      HIP_TRY(hipEventSynchronize(ev[3]));
+      float ms = 0;
+      HIP_TRY(hipEventElapsedTime(&ms, ev[2], ev[3]));
+      stats.call_ms = ms;
+    }
+    if (int r = pull()) return r;
+    stats.rounds = host.round;
+    stats.spmv_rows = host.work_rows;
+    stats.spmv_entries = host.work_entries;
+    stats.uniform_rows = host.work_uniform;
+    g_stats = stats;
+    return WL_OK;
+  }
 
   int pull() {
     HIP_TRY(hipMemcpyAsync(&host, ctx.st, sizeof(DevState), hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    return WL_OK;
+    return stats_collect();
   }
 
   int init_state(uint64_t seed, uint32_t k, uint32_t round, uint32_t max_rounds) {
@@ -332,24 +396,43 @@ struct Session {
     return pull();
   }
 
+  template <typename RP, bool W, int M>
+  void spmv_launch(const SpmvGrid& g) {
+    hipLaunchKernelGGL((k_spmv<RP, W, M>), dim3(g.b0), dim3(kBlock), 0, s, ctx, g);
+  }
+
   template <typename RP, bool W>
   void spmv_t() {
     const DevState& h = host;
-    uint32_t g0 = grid_for((uint64_t)h.bin_cnt[0] * 4);
-    uint32_t g1 = grid_for((uint64_t)h.bin_cnt[1] * 16);
-    uint32_t g2 = grid_for((uint64_t)h.bin_cnt[2] * 64);
-    uint32_t g3 = grid_for((uint64_t)h.n_chunks * 64);
-    if (h.bin_cnt[0])
-      hipLaunchKernelGGL((k_spmv_group<4, RP, W>), dim3(g0), dim3(kBlock), 0, s, ctx, 0);
-    if (h.bin_cnt[1])
-      hipLaunchKernelGGL((k_spmv_group<16, RP, W>), dim3(g1), dim3(kBlock), 0, s, ctx, 1);
-    if (h.bin_cnt[2])
-      hipLaunchKernelGGL((k_spmv_group<64, RP, W>), dim3(g2), dim3(kBlock), 0, s, ctx, 2);
-    if (h.n_chunks) {
-      hipLaunchKernelGGL((k_spmv_heavy<RP, W>), dim3(g3), dim3(kBlock), 0, s, ctx);
-      hipLaunchKernelGGL(k_spmv_heavy_fin, dim3(grid_for(h.bin_cnt[3])), dim3(kBlock),
-                         0, s, ctx);
+    const bool uniform = !W && h.k == 1;
+    SpmvGrid g;
+    g.heavy = h.n_chunks ? grid_for(h.n_chunks, kBlock / kWave) : 0;
+    g.b2 = g.heavy + (h.bin_cnt[2] ? grid_for(h.bin_cnt[2], kBlock / 64) : 0);
+    g.b1 = g.b2 + (h.bin_cnt[1] ? grid_for(h.bin_cnt[1], kBlock / 16) : 0);
+    g.b0 = g.b1 + (h.bin_cnt[0] ? grid_for(h.bin_cnt[0], kBlock / 4) : 0);
+    if (g.b0 == 0) return;
+    const int mode = h.k <= 255 ? kGather8 : (h.k <= kTableMax ? kGather16 : kGatherX);
+    if (!uniform)
+      hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock),
+                         0, s, ctx, mode);
+    if (sflags & WL_STATS_WORK)
+      hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
+                         dim3(kBlock), 0, s, ctx);
+    if (sflags & WL_STATS_TIME) (void)hipEventRecord(ev[0], s);
+    if (uniform)
+      hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
+                         dim3(kBlock), 0, s, ctx);
+    else if (mode == kGather8)
+      spmv_launch<RP, W, kGather8>(g);
+    else if (mode == kGather16)
+      spmv_launch<RP, W, kGather16>(g);
+    else
+      spmv_launch<RP, W, kGatherX>(g);
+    if (sflags & WL_STATS_TIME) {
+      (void)hipEventRecord(ev[1], s);
+      spmv_pending = true;
     }
+    stats.spmv_launches++;
   }
 
   void spmv() {
@@ -385,6 +468,9 @@ struct Session {
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
     }
+    if (host.n_tiny)
+      hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(host.n_tiny, kBlock / kWave, 8192)),
+                         dim3(kBlock), 0, s, ctx);
     if (host.n_small)
       hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
                          dim3(kBlock), 0, s, ctx);
@@ -399,9 +485,7 @@ struct Session {
   }
 
   int round() {
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
-    hipLaunchKernelGGL(k_weights, dim3(gn), dim3(kBlock), 0, s, ctx);
     spmv();
     HIP_LAUNCH_CHECK();
     return relabel(1);
@@ -435,6 +519,18 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
 extern "C" {
 
 const char* wl_last_error(void) { return g_err; }
+
+int wl_stats_enable(int flags) {
+  if (flags & ~(WL_STATS_TIME | WL_STATS_WORK)) return fail(WL_EINVAL, "unknown flag");
+  g_stats_flags = flags;
+  return WL_OK;
+}
+
+int wl_stats_get(wl_stats* out) {
+  if (!out) return fail(WL_EINVAL, "NULL argument");
+  *out = g_stats;
+  return WL_OK;
+}
 
 int wl_workspace_size(const wl_csr* g, uint64_t* bytes_out) {
   g_err[0] = 0;
@@ -484,8 +580,10 @@ int wl_refine_round(const wl_csr* g, const uint32_t* color_in, uint32_t k_in,
   hipLaunchKernelGGL(k_scan_colors, dim3(1), dim3(kBlock), 0, S.s, S.ctx, k_in);
   hipLaunchKernelGGL(k_place_colors, dim3(gn), dim3(kBlock), 0, S.s, S.ctx);
   HIP_LAUNCH_CHECK();
+  if (int r = S.stats_begin()) return r;
   if (int r = S.build_schedule()) return r;
   if (int r = S.round()) return r;
+  if (int r = S.stats_end()) return r;
   *k_out = S.host.k;
   return WL_OK;
 }
@@ -507,6 +605,7 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
   const uint32_t cap = max_rounds ? max_rounds : (uint32_t)std::min<uint64_t>(g->n + 1, 0xFFFFFFFFull);
   if (int r = S.init_state(seed, 1, 0, cap)) return r;
   if (int r = S.validate_device()) return r;
+  if (int r = S.stats_begin()) return r;
   const uint32_t gn = grid_for(g->n, kBlock, 4096);
   hipLaunchKernelGGL(k_iota_zero, dim3(gn), dim3(kBlock), 0, S.s, S.ctx);
   HIP_LAUNCH_CHECK();
@@ -519,6 +618,7 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
   while (!S.host.done) {
     if (int r = S.round()) return r;
   }
+  if (int r = S.stats_end()) return r;
   *k_out = S.host.k;
   *rounds_out = S.host.round;
   if (S.host.done == 2)

@@ -31,6 +31,7 @@ __global__ void k_round_begin(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
   st->n_small = 0;
+  st->n_tiny = 0;
   st->n_big[0] = 0;
   st->n_big[1] = 0;
   st->n_tiles = 0;
@@ -44,26 +45,47 @@ __global__ void __launch_bounds__(kBlock) k_fill_u8(Ctx ctx, uint8_t* p,
     p[i] = v;
 }
 
+// Appends 'want' items to a device list: one atomic per block, slots
+// handed out by a block scan (order inside the list is irrelevant).
+// Contains __syncthreads(); every thread of the block must call it.
+__device__ __forceinline__ uint32_t block_append(bool want, uint32_t* counter,
+                                                 uint32_t* sh, uint32_t* base_sh) {
+  uint32_t tot;
+  const uint32_t ex = block_excl_scan(want ? 1u : 0u, sh, &tot);
+  if (threadIdx.x == 0) *base_sh = tot ? atomicAdd(counter, tot) : 0u;
+  __syncthreads();
+  const uint32_t at = *base_sh + ex;
+  __syncthreads();
+  return at;
+}
+
 // One entry per class: flag its first position, queue it if it has >= 2
-// members.
+// members (small classes for the LDS sort, big ones for the radix passes).
 __global__ void __launch_bounds__(kBlock) k_segments(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
+  __shared__ uint32_t sh[kBlock / kWave];
+  __shared__ uint32_t base_sh;
   const uint32_t k = st->k;
-  for (uint32_t j = blockIdx.x * kBlock + threadIdx.x; j < k;
-       j += gridDim.x * kBlock) {
-    const uint32_t s = ctx.cstart[j], e = ctx.cstart[j + 1];
-    if (e <= s) continue;
-    ctx.flags[s] = 1;
-    const uint32_t len = e - s;
-    if (len < 2) continue;
-    if (len <= kSmallMax) {
-      uint32_t idx = atomicAdd(&st->n_small, 1u);
-      ctx.small_list[idx] = make_uint2(s, len);
-    } else {
-      uint32_t idx = atomicAdd(&st->n_big[0], 1u);
-      ctx.big_list0[idx] = make_uint2(s, len);
+  const uint32_t stride = gridDim.x * kBlock;
+  for (uint32_t j0 = blockIdx.x * kBlock; j0 < k; j0 += stride) {
+    const uint32_t j = j0 + threadIdx.x;
+    uint32_t s = 0, len = 0;
+    if (j < k) {
+      s = ctx.cstart[j];
+      const uint32_t e = ctx.cstart[j + 1];
+      len = e > s ? e - s : 0;
+      if (len) ctx.flags[s] = 1;
     }
+    const bool tiny = len >= 2 && len <= kTinyMax;
+    const bool small = len > kTinyMax && len <= kSmallMax;
+    const bool big = len > kSmallMax;
+    const uint32_t t = block_append(tiny, &st->n_tiny, sh, &base_sh);
+    if (tiny) ctx.tiny_list[t] = make_uint2(s, len);
+    const uint32_t a = block_append(small, &st->n_small, sh, &base_sh);
+    if (small) ctx.small_list[a] = make_uint2(s, len);
+    const uint32_t b = block_append(big, &st->n_big[0], sh, &base_sh);
+    if (big) ctx.big_list0[b] = make_uint2(s, len);
   }
 }
 
@@ -210,7 +232,10 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
       const uint32_t pos = s.x + off;
       ctx.flags[pos] = 1;
       if (h >= 2 && ctx.bmin[g] != ctx.bmax[g]) {
-        if (h <= kSmallMax) {
+        if (h <= kTinyMax) {
+          uint32_t idx = atomicAdd(&st->n_tiny, 1u);
+          ctx.tiny_list[idx] = make_uint2(pos, h | kMatBit);
+        } else if (h <= kSmallMax) {
           uint32_t idx = atomicAdd(&st->n_small, 1u);
           ctx.small_list[idx] = make_uint2(pos, h | kMatBit);
         } else {
@@ -286,6 +311,7 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
   const uint32_t ns = st->n_small;
   __shared__ unsigned long long skey[kSmallMax];
   __shared__ uint32_t sval[kSmallMax];
+  __shared__ int differ;
   for (uint32_t si = blockIdx.x; si < ns; si += gridDim.x) {
     const uint2 sg = ctx.small_list[si];
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
@@ -303,6 +329,13 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
       }
     }
     __syncthreads();
+    // all images equal: nothing splits, nothing to reorder
+    if (threadIdx.x == 0) differ = 0;
+    __syncthreads();
+    for (uint32_t t = threadIdx.x; t < len; t += kBlock)
+      if (skey[t] != skey[0]) differ = 1;
+    __syncthreads();
+    if (!differ) continue;
     for (uint32_t kk = 2; kk <= P; kk <<= 1) {
       for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
         for (uint32_t i = threadIdx.x; i < P; i += kBlock) {
@@ -327,6 +360,51 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
       if (t > 0 && skey[t] != skey[t - 1]) ctx.flags[s + t] = 1;
     }
     __syncthreads();
+  }
+}
+
+// One wave per tiny segment (<= 64 nodes): bitonic sort of (z, node) across
+// the lanes with shuffles, flags where z changes.  Skipped when all images of
+// the segment are equal.
+__global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t nt = st->n_tiny;
+  const uint32_t lane = lane_id();
+  const uint32_t nwaves = gridDim.x * (kBlock / kWave);
+  for (uint32_t si = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; si < nt;
+       si += nwaves) {
+    const uint2 sg = ctx.tiny_list[si];
+    const uint32_t s = sg.x, len = sg.y & ~kMatBit;
+    const bool mat = (sg.y & kMatBit) != 0;
+    unsigned long long key = ~0ull;
+    uint32_t v = 0;
+    if (lane < len) {
+      v = ctx.perm[s + lane];
+      key = mat ? ctx.keys[s + lane] : ctx.z[v];
+    }
+    const unsigned long long first = __shfl(key, 0, kWave);
+    if (__ballot(lane < len && key != first) == 0) continue;
+#pragma unroll
+    for (uint32_t kk = 2; kk <= (uint32_t)kWave; kk <<= 1) {
+#pragma unroll
+      for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+        const unsigned long long pk = __shfl_xor(key, (int)j, kWave);
+        const uint32_t pv = __shfl_xor(v, (int)j, kWave);
+        const bool up = (lane & kk) == 0;
+        const bool lower = (lane & j) == 0;
+        const bool take = (lower == up) ? (pk < key) : (pk > key);
+        if (take) {
+          key = pk;
+          v = pv;
+        }
+      }
+    }
+    const unsigned long long prev = __shfl_up(key, 1, kWave);
+    if (lane < len) {
+      ctx.perm[s + lane] = v;
+      if (lane > 0 && key != prev) ctx.flags[s + lane] = 1;
+    }
   }
 }
 

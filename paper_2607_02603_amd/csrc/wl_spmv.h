@@ -119,97 +119,194 @@ __global__ void __launch_bounds__(kBlock) k_heavy_prep(Ctx ctx) {
     for (uint32_t t = 0; t < nc; ++t) {
       HeavyChunk ch;
       ch.beg = b0 + (uint64_t)t * kHeavyChunk;
-      ch.end = min(e0, ch.beg + kHeavyChunk);
+      ch.len = (uint32_t)(min(e0, ch.beg + kHeavyChunk) - ch.beg);
       ch.row = row;
       ch.h = h;
+      ch.nc = nc;
       ctx.chunks[carry + ex + t] = ch;
     }
     carry += tot;
   }
   if (threadIdx.x == 0) ctx.st->n_chunks = carry;
   for (uint32_t h = threadIdx.x; h < 2 * nh; h += kBlock) ctx.hacc[h] = 0;
+  for (uint32_t h = threadIdx.x; h < nh; h += kBlock) ctx.hcnt[h] = 0;
 }
 
 // ---------------------------------------------------------------------------
-// Per-node random values x_i = W(seed, round, c_i).
+// SpMV: one launch per round.  Each lane keeps U independent gathers in
+// flight per iteration.
 // ---------------------------------------------------------------------------
 
-__global__ void __launch_bounds__(kBlock) k_weights(Ctx ctx) {
-  if (ctx.st->done) return;
-  const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
-       i += gridDim.x * kBlock)
-    ctx.x[i] = color_weight(key, ctx.c[i]);
+// Where the SpMV reads the random value of a neighbour j:
+//   kGatherX   x[j]                      (any number of colours)
+//   kGather16  tbl[c16[j]], c16 = colour  (k <= 65535: 2 bytes per node)
+//   kGather8   tbl[c8[j]],  c8  = colour  (k <= 255:   1 byte per node)
+// The compact colour arrays shrink the randomly gathered footprint 4-8x; the
+// table of k values stays in cache.
+enum GatherMode { kGatherX = 0, kGather16 = 1, kGather8 = 2 };
+
+template <int M>
+__device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j) {
+  if (M == kGather16) return ctx.wtab[ctx.c16[j]];
+  if (M == kGather8) return ctx.wtab[ctx.c8[j]];
+  return ctx.x[j];
 }
 
-// ---------------------------------------------------------------------------
-// SpMV kernels
-// ---------------------------------------------------------------------------
+template <int U, bool W, int M>
+__device__ __forceinline__ void accumulate(const Ctx& ctx, Acc96& a, uint64_t e0,
+                                           uint64_t end, uint32_t stride) {
+  uint32_t j[U];
+  bool ok[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint64_t e = e0 + (uint64_t)u * stride;
+    ok[u] = e < end;
+    j[u] = ok[u] ? (ctx.nt_stream ? __builtin_nontemporal_load(ctx.col + e) : ctx.col[e])
+                 : 0u;
+  }
+  uint64_t v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    v[u] = ok[u] ? gather_value<M>(ctx, j[u]) : 0ull;
+    if (W && ok[u]) v[u] = mul_small_fold(ctx.wgt[e0 + (uint64_t)u * stride], v[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < U; ++u) acc_add(a, v[u]);
+}
 
-template <int G, typename RP, bool W>
-__global__ void __launch_bounds__(kBlock) k_spmv_group(Ctx ctx, int bin) {
-  if (ctx.st->done) return;
+template <int G, int U, typename RP, bool W, int M>
+__device__ __forceinline__ void spmv_rows(const Ctx& ctx, int bin, uint32_t bid,
+                                          uint32_t nblk) {
   const RP* rp = rowptr<RP>(ctx);
   const uint32_t cnt = ctx.st->bin_cnt[bin];
   const uint32_t* list = ctx.rows + ctx.st->bin_start[bin];
   const uint32_t sub = threadIdx.x % G;
-  const uint32_t ngroups = gridDim.x * (kBlock / G);
-  for (uint32_t t = (blockIdx.x * kBlock + threadIdx.x) / G; t < cnt;
-       t += ngroups) {
+  const uint32_t gpb = kBlock / G;
+  const uint32_t ngroups = nblk * gpb;
+  for (uint32_t t = bid * gpb + threadIdx.x / G; t < cnt; t += ngroups) {
     const uint32_t row = list[t];
     if (!ctx.act[row]) continue;
     const uint64_t beg = rp[row], end = rp[row + 1];
     Acc96 a{0, 0};
-    for (uint64_t e = beg + sub; e < end; e += G) {
-      uint64_t v = ctx.x[ctx.col[e]];
-      if (W) v = mul_small_fold(ctx.wgt[e], v);
-      acc_add(a, v);
-    }
-    uint64_t r = group_sum_p<G>(acc_reduce(a));
+    for (uint64_t e0 = beg + sub; e0 < end; e0 += (uint64_t)G * U)
+      accumulate<U, W, M>(ctx, a, e0, end, G);
+    const uint64_t r = group_sum_p<G>(acc_reduce(a));
     if (sub == 0) ctx.z[row] = r;
   }
 }
 
-template <typename RP, bool W>
-__global__ void __launch_bounds__(kBlock) k_spmv_heavy(Ctx ctx) {
-  if (ctx.st->done) return;
+template <bool W, int M>
+__device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
+                                           uint32_t nblk) {
   const uint32_t nch = ctx.st->n_chunks;
   const int lane = lane_id();
-  const uint32_t nwaves = gridDim.x * (kBlock / kWave);
-  for (uint32_t t = (blockIdx.x * kBlock + threadIdx.x) / kWave; t < nch;
+  const uint32_t nwaves = nblk * (kBlock / kWave);
+  for (uint32_t t = bid * (kBlock / kWave) + threadIdx.x / kWave; t < nch;
        t += nwaves) {
     const HeavyChunk ch = ctx.chunks[t];
     if (!ctx.act[ch.row]) continue;
     Acc96 a{0, 0};
-    for (uint64_t e = ch.beg + lane; e < ch.end; e += kWave) {
-      uint64_t v = ctx.x[ctx.col[e]];
-      if (W) v = mul_small_fold(ctx.wgt[e], v);
-      acc_add(a, v);
-    }
-    uint64_t r = group_sum_p<kWave>(acc_reduce(a));
+    const uint64_t end = ch.beg + ch.len;
+    for (uint64_t e0 = ch.beg + lane; e0 < end; e0 += (uint64_t)kWave * 4)
+      accumulate<4, W, M>(ctx, a, e0, end, kWave);
+    const uint64_t r = group_sum_p<kWave>(acc_reduce(a));
     if (lane == 0) {
+      // Partial sums of the row's chunks meet in two 64-bit accumulators
+      // (low and high 32-bit halves of canonical residues); the chunk that
+      // finishes last folds them into z and resets them for the next round.
       atomicAdd(&ctx.hacc[2 * ch.h], (unsigned long long)(r & 0xFFFFFFFFull));
       atomicAdd(&ctx.hacc[2 * ch.h + 1], (unsigned long long)(r >> 32));
+      __threadfence();
+      const uint32_t seen = atomicAdd(&ctx.hcnt[ch.h], 1u);
+      if (seen == ch.nc - 1) {
+        __threadfence();
+        const uint64_t lo = atomicExch(&ctx.hacc[2 * ch.h], 0ull);
+        const uint64_t hi = fold61(atomicExch(&ctx.hacc[2 * ch.h + 1], 0ull));
+        atomicExch(&ctx.hcnt[ch.h], 0u);
+        // hi * 2^32 = (hi mod 2^29) * 2^32 + (hi >> 29) * 2^61, 2^61 = 1.
+        const uint64_t t2 = ((hi & 0x1FFFFFFFull) << 32) + (hi >> 29);
+        ctx.z[ch.row] = addp(fold61(t2), fold61(lo));
+      }
     }
   }
 }
 
-// z of the heavy rows = hi * 2^32 + lo (mod p); clears the accumulators.
-__global__ void __launch_bounds__(kBlock) k_spmv_heavy_fin(Ctx ctx) {
+template <typename RP, bool W, int M>
+__global__ void __launch_bounds__(kBlock) k_spmv(Ctx ctx, SpmvGrid g) {
   if (ctx.st->done) return;
-  const uint32_t nh = ctx.st->bin_cnt[3];
-  const uint32_t* list = ctx.rows + ctx.st->bin_start[3];
-  for (uint32_t h = blockIdx.x * kBlock + threadIdx.x; h < nh;
-       h += gridDim.x * kBlock) {
-    const uint32_t row = list[h];
-    if (ctx.act[row]) {
-      uint64_t lo = ctx.hacc[2 * h], hi = fold61(ctx.hacc[2 * h + 1]);
-      // hi * 2^32 = (hi mod 2^29) * 2^32 + (hi >> 29) * 2^61, 2^61 = 1.
-      uint64_t t = ((hi & 0x1FFFFFFFull) << 32) + (hi >> 29);
-      ctx.z[row] = addp(fold61(t), fold61(lo));
+  const uint32_t b = blockIdx.x;
+  if (b < g.heavy)
+    spmv_heavy<W, M>(ctx, b, g.heavy);
+  else if (b < g.b2)
+    spmv_rows<64, 4, RP, W, M>(ctx, 2, b - g.heavy, g.b2 - g.heavy);
+  else if (b < g.b1)
+    spmv_rows<16, 4, RP, W, M>(ctx, 1, b - g.b2, g.b1 - g.b2);
+  else
+    spmv_rows<4, 2, RP, W, M>(ctx, 0, b - g.b1, g.b0 - g.b1);
+}
+
+// One colour and unit weights: every x_j is the same w, so
+// z_i = deg_i * w (mod p) exactly, without touching col_idx.
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_spmv_uniform(Ctx ctx) {
+  if (ctx.st->done) return;
+  const RP* rp = rowptr<RP>(ctx);
+  const uint64_t w0 = color_weight(round_key(ctx.st->seed, ctx.st->round), 0);
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock)
+    if (ctx.act[i]) ctx.z[i] = mulp(fold61(rp[i + 1] - rp[i]), w0);
+}
+
+// Per-round random values for the gather: compact colour array plus the
+// table of the k colour values (k <= 65535), or x per node otherwise.
+__global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
+  if (ctx.st->done) return;
+  const uint32_t k = ctx.st->k;
+  const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
+  const uint32_t tid = blockIdx.x * kBlock + threadIdx.x;
+  const uint32_t stride = gridDim.x * kBlock;
+  if (mode == kGatherX) {
+    for (uint32_t i = tid; i < ctx.n; i += stride) ctx.x[i] = color_weight(key, ctx.c[i]);
+    return;
+  }
+  for (uint32_t b = tid; b < k; b += stride) ctx.wtab[b] = color_weight(key, b);
+  if (mode == kGather16)
+    for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c16[i] = (uint16_t)ctx.c[i];
+  else
+    for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c8[i] = (uint8_t)ctx.c[i];
+}
+
+// Diagnostics: rows and entries the next SpMV launch will read.
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx) {
+  if (ctx.st->done) return;
+  const RP* rp = rowptr<RP>(ctx);
+  const bool uniform = !ctx.weighted && ctx.st->k == 1;
+  unsigned long long rows = 0, ents = 0;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
+       i += gridDim.x * kBlock)
+    if (ctx.act[i]) {
+      rows += 1;
+      ents += rp[i + 1] - rp[i];
     }
-    ctx.hacc[2 * h] = 0;
-    ctx.hacc[2 * h + 1] = 0;
+  __shared__ unsigned long long sr[kBlock], se[kBlock];
+  sr[threadIdx.x] = rows;
+  se[threadIdx.x] = ents;
+  __syncthreads();
+  for (int o = kBlock / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) {
+      sr[threadIdx.x] += sr[threadIdx.x + o];
+      se[threadIdx.x] += se[threadIdx.x + o];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && sr[0]) {
+    if (uniform) {
+      atomicAdd(&ctx.st->work_uniform, sr[0]);
+    } else {
+      atomicAdd(&ctx.st->work_rows, sr[0]);
+      atomicAdd(&ctx.st->work_entries, se[0]);
+    }
   }
 }
 

@@ -55,19 +55,47 @@ __global__ void __launch_bounds__(kB) k_count(Src S, uint64_t s0, uint64_t cnt,
     if (h[b]) atomicAdd(&counts[b], (unsigned long long)h[b]);
 }
 
+// Each block takes kPer samples per thread, ranks its keys per bucket in LDS
+// and reserves room with one global atomic per bucket.
+constexpr int kPer = 8;
+
 __global__ void __launch_bounds__(kB) k_scatter(Src S, uint64_t s0, uint64_t cnt,
-                                                uint32_t shift,
+                                                uint32_t shift, uint32_t nbk,
                                                 unsigned long long* cursor,
                                                 uint64_t* keys) {
-  for (uint64_t q = blockIdx.x * (uint64_t)kB + threadIdx.x; q < cnt;
-       q += (uint64_t)gridDim.x * kB) {
-    uint64_t u, v;
-    if (draw(S, s0 + q, &u, &v)) {
-      unsigned long long a = atomicAdd(&cursor[u >> shift], 1ull);
-      keys[a] = (u << 32) | v;
-      unsigned long long b = atomicAdd(&cursor[v >> shift], 1ull);
-      keys[b] = (v << 32) | u;
+  __shared__ uint32_t lcnt[kMaxBuckets];
+  __shared__ unsigned long long lbase[kMaxBuckets];
+  const uint64_t per_block = (uint64_t)kB * kPer;
+  for (uint64_t base = blockIdx.x * per_block; base < cnt;
+       base += (uint64_t)gridDim.x * per_block) {
+    for (uint32_t b = threadIdx.x; b < nbk; b += kB) lcnt[b] = 0;
+    __syncthreads();
+    uint64_t key[2 * kPer];
+    uint32_t slot[2 * kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const uint64_t q = base + (uint64_t)i * kB + threadIdx.x;
+      uint64_t u = 0, v = 0;
+      bool ok = q < cnt && draw(S, s0 + q, &u, &v);
+      key[2 * i] = ok ? ((u << 32) | v) : ~0ull;
+      key[2 * i + 1] = ok ? ((v << 32) | u) : ~0ull;
+      if (ok) {
+        slot[2 * i] = atomicAdd(&lcnt[u >> shift], 1u);
+        slot[2 * i + 1] = atomicAdd(&lcnt[v >> shift], 1u);
+      }
     }
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < nbk; b += kB)
+      if (lcnt[b]) lbase[b] = atomicAdd(&cursor[b], (unsigned long long)lcnt[b]);
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2 * kPer; ++i) {
+      if (key[i] != ~0ull) {
+        const uint32_t b = (uint32_t)((key[i] >> 32) >> shift);
+        keys[lbase[b] + slot[i]] = key[i];
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -107,7 +135,7 @@ int launch(const Src& S, int phase, uint64_t s0, uint64_t cnt, uint32_t shift,
                        shift, nbk, arr);
   else
     hipLaunchKernelGGL(k_scatter, dim3((uint32_t)blocks), dim3(kB), 0, st, S, s0,
-                       cnt, shift, arr, keys);
+                       cnt, shift, nbk, arr, keys);
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
 
