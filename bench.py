@@ -98,6 +98,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="rmat27", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="first copy 1 GiB device-to-device (a plain copy kernel of "
+                         "known size, to calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -107,6 +110,12 @@ def main():
     import torch
     import paper_2607_02603_amd as wl
     dev = torch.device("cuda:0")
+    if args.copy_probe:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     t0 = time.perf_counter()
     dg, _ = make_graph(args.workload, dev)
     torch.cuda.synchronize()
@@ -141,8 +150,7 @@ def main():
     # Algorithmic bytes of the SpMV kernel: 4 B column index + 8 B gathered
     # value per entry, row pointer + 8 B image per row.
     rp_bytes = 8 if dg.row_ptr.dtype == torch.int64 else 4
-    spmv_bytes = (12 * work["spmv_entries"] + (rp_bytes + 8) * work["spmv_rows"]
-                  + (rp_bytes + 8) * work["uniform_rows"])
+    spmv_bytes = 12 * work["spmv_entries"] + (rp_bytes + 8) * work["spmv_rows"]
     spmv_s = sum(spmv_ms) / len(spmv_ms) / 1e3
     launches = max(1, work["spmv_launches"])
     achieved = spmv_bytes / spmv_s / 1e9 if spmv_s > 0 else 0.0

@@ -165,13 +165,16 @@ const char *wl_last_error(void);
 #define WL_STATS_TIME 1
 #define WL_STATS_WORK 2
 typedef struct wl_stats {
-    uint32_t rounds;          /* rounds of the last call                    */
-    uint32_t spmv_launches;   /* SpMV launches in the last call             */
-    double spmv_ms;           /* their summed device time (WL_STATS_TIME)   */
-    double call_ms;           /* device time of the whole call              */
-    uint64_t spmv_rows;       /* rows whose image was computed (WORK)       */
-    uint64_t spmv_entries;    /* CSR entries gathered (WORK)                */
-    uint64_t uniform_rows;    /* rows done by the one-colour shortcut (WORK)*/
+    uint32_t rounds;           /* rounds of the last call                   */
+    uint32_t spmv_launches;    /* launches of the gathering SpMV kernel     */
+    double spmv_ms;            /* their summed device time (WL_STATS_TIME)  */
+    double call_ms;            /* device time of the whole call             */
+    uint64_t spmv_rows;        /* rows whose image it computed (WORK)       */
+    uint64_t spmv_entries;     /* CSR entries it gathered (WORK)            */
+    uint32_t uniform_launches; /* launches of the one-colour kernel         */
+    uint32_t pad;
+    double uniform_ms;         /* their summed device time                  */
+    uint64_t uniform_rows;     /* rows they computed (WORK)                 */
 } wl_stats;
 int wl_stats_enable(int flags);
 int wl_stats_get(wl_stats *out);

@@ -45,7 +45,8 @@ class WlStats(ctypes.Structure):
     _fields_ = [("rounds", ctypes.c_uint32), ("spmv_launches", ctypes.c_uint32),
                 ("spmv_ms", ctypes.c_double), ("call_ms", ctypes.c_double),
                 ("spmv_rows", ctypes.c_uint64), ("spmv_entries", ctypes.c_uint64),
-                ("uniform_rows", ctypes.c_uint64)]
+                ("uniform_launches", ctypes.c_uint32), ("pad", ctypes.c_uint32),
+                ("uniform_ms", ctypes.c_double), ("uniform_rows", ctypes.c_uint64)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

@@ -44,7 +44,8 @@ struct DevState {
   uint32_t bin_cnt[kNumBins];
   uint32_t bin_start[kNumBins];
   uint32_t n_tiny;      // entries in the tiny-segment list (<= 64 nodes)
-  uint32_t pad[4];
+  uint32_t dense;       // 1 if the colours in use are exactly [0, k)
+  uint32_t pad[3];
   uint64_t seed;
   unsigned long long work_rows;     // diagnostics: rows the SpMV computed
   unsigned long long work_entries;  // diagnostics: entries it gathered

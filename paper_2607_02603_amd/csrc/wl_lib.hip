@@ -299,6 +299,7 @@ struct Session {
   int sflags = 0;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   bool spmv_pending = false;
+  bool pending_uniform = false;
   wl_stats stats{};
 
   ~Session() {
@@ -321,7 +322,10 @@ struct Session {
     if ((sflags & WL_STATS_TIME) && spmv_pending) {
       float ms = 0;
       HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
-      stats.spmv_ms += ms;
+      if (pending_uniform)
+        stats.uniform_ms += ms;
+      else
+        stats.spmv_ms += ms;
       spmv_pending = false;
     }
     return WL_OK;
@@ -350,9 +354,11 @@ struct Session {
     return stats_collect();
   }
 
-  int init_state(uint64_t seed, uint32_t k, uint32_t round, uint32_t max_rounds) {
+  int init_state(uint64_t seed, uint32_t k, uint32_t round, uint32_t max_rounds,
+                 uint32_t dense) {
     DevState h{};
     h.k = k;
+    h.dense = dense;
     h.round = round;
     h.max_rounds = max_rounds;
     h.seed = seed;
@@ -388,10 +394,19 @@ struct Session {
       hipLaunchKernelGGL(k_bins_fill<uint64_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
     else
       hipLaunchKernelGGL(k_bins_fill<uint32_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    const uint32_t nh = host.bin_cnt[3];
+    const uint32_t hb = std::max<uint32_t>(1, std::min<uint32_t>(kScanBlocks, (nh + 255) / 256));
     if (rp64)
-      hipLaunchKernelGGL(k_heavy_prep<uint64_t>, dim3(1), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_heavy_count<uint64_t>, dim3(hb), dim3(kBlock), 0, s, ctx);
     else
-      hipLaunchKernelGGL(k_heavy_prep<uint32_t>, dim3(1), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_heavy_count<uint32_t>, dim3(hb), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_heavy_scan, dim3(1), dim3(kBlock), 0, s, ctx, hb);
+    if (rp64)
+      hipLaunchKernelGGL(k_heavy_fill<uint64_t>, dim3(hb), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_heavy_fill<uint32_t>, dim3(hb), dim3(kBlock), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     return pull();
   }
@@ -431,8 +446,12 @@ struct Session {
     if (sflags & WL_STATS_TIME) {
       (void)hipEventRecord(ev[1], s);
       spmv_pending = true;
+      pending_uniform = uniform;
     }
-    stats.spmv_launches++;
+    if (uniform)
+      stats.uniform_launches++;
+    else
+      stats.spmv_launches++;
   }
 
   void spmv() {
@@ -564,7 +583,7 @@ int wl_refine_round(const wl_csr* g, const uint32_t* color_in, uint32_t k_in,
   Session S;
   if (int r = open_session(S, g, color_out, workspace, ws_bytes, stream)) return r;
   if (int r = check_nnz_device(g, S.s)) return r;
-  if (int r = S.init_state(seed, k_in, round, round + 1)) return r;
+  if (int r = S.init_state(seed, k_in, round, round + 1, 0)) return r;
   if (int r = S.validate_device()) return r;
   const uint32_t gn = grid_for(g->n, kBlock, 4096);
   hipLaunchKernelGGL(k_check_colors, dim3(gn), dim3(kBlock), 0, S.s, S.ctx, color_in,
@@ -603,7 +622,7 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
   if (int r = open_session(S, g, color_out, workspace, ws_bytes, stream)) return r;
   if (int r = check_nnz_device(g, S.s)) return r;
   const uint32_t cap = max_rounds ? max_rounds : (uint32_t)std::min<uint64_t>(g->n + 1, 0xFFFFFFFFull);
-  if (int r = S.init_state(seed, 1, 0, cap)) return r;
+  if (int r = S.init_state(seed, 1, 0, cap, 1)) return r;
   if (int r = S.validate_device()) return r;
   if (int r = S.stats_begin()) return r;
   const uint32_t gn = grid_for(g->n, kBlock, 4096);

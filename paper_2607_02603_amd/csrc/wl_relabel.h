@@ -463,8 +463,12 @@ __global__ void __launch_bounds__(kBlock) k_scan_final(Ctx ctx) {
 }
 
 // New class starts, then colours and activity per node.
+// When the colours in use are exactly [0, k) and no class split
+// (k_new == k), the ranks equal the old colours: colours, grouping and
+// activity are already right and both kernels return.
 __global__ void __launch_bounds__(kBlock) k_cstart(Ctx ctx) {
   if (ctx.st->done) return;
+  if (ctx.st->dense && ctx.st->k_new == ctx.st->k) return;
   for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n;
        p += gridDim.x * kBlock)
     if (ctx.flags[p]) ctx.cstart[ctx.ids[p]] = p;
@@ -473,6 +477,7 @@ __global__ void __launch_bounds__(kBlock) k_cstart(Ctx ctx) {
 
 __global__ void __launch_bounds__(kBlock) k_scatter_colors(Ctx ctx) {
   if (ctx.st->done) return;
+  if (ctx.st->dense && ctx.st->k_new == ctx.st->k) return;
   for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n;
        p += gridDim.x * kBlock) {
     const uint32_t v = ctx.perm[p], id = ctx.ids[p];

@@ -96,26 +96,74 @@ __global__ void __launch_bounds__(kBlock) k_bins_fill(Ctx ctx) {
   }
 }
 
-// One block: chunk list of the heavy rows (bin 3).
+// Chunk list of the heavy rows (bin 3), in three launches: chunks per block
+// of heavy rows, exclusive scan of the block totals, fill.
+__device__ __forceinline__ void heavy_range(uint32_t nh, uint32_t b, uint32_t nblk,
+                                            uint32_t* lo, uint32_t* hi) {
+  const uint32_t per = (nh + nblk - 1) / nblk;
+  *lo = min(nh, b * per);
+  *hi = min(nh, *lo + per);
+}
+
 template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_heavy_prep(Ctx ctx) {
+__device__ __forceinline__ uint32_t heavy_chunks_of(const Ctx& ctx, uint32_t row) {
   const RP* rp = rowptr<RP>(ctx);
-  __shared__ uint32_t sh[kBlock / kWave];
+  return (uint32_t)((rp[row + 1] - rp[row] + kHeavyChunk - 1) / kHeavyChunk);
+}
+
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_heavy_count(Ctx ctx) {
   const uint32_t nh = ctx.st->bin_cnt[3];
   const uint32_t* list = ctx.rows + ctx.st->bin_start[3];
+  uint32_t lo, hi;
+  heavy_range(nh, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t c = 0;
+  for (uint32_t h = lo + threadIdx.x; h < hi; h += kBlock)
+    c += heavy_chunks_of<RP>(ctx, list[h]);
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t tot;
+  block_excl_scan(c, sh, &tot);
+  if (threadIdx.x == 0) ctx.scan_part[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(kBlock) k_heavy_scan(Ctx ctx, uint32_t nblk) {
+  __shared__ uint32_t sh[kBlock / kWave];
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < nh; base += kBlock) {
-    uint32_t h = base + threadIdx.x;
+  for (uint32_t base = 0; base < nblk; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i < nblk ? ctx.scan_part[i] : 0;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(v, sh, &tot);
+    if (i < nblk) ctx.scan_part[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) ctx.st->n_chunks = carry;
+}
+
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_heavy_fill(Ctx ctx) {
+  const RP* rp = rowptr<RP>(ctx);
+  const uint32_t nh = ctx.st->bin_cnt[3];
+  const uint32_t* list = ctx.rows + ctx.st->bin_start[3];
+  uint32_t lo, hi;
+  heavy_range(nh, blockIdx.x, gridDim.x, &lo, &hi);
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t carry = ctx.scan_part[blockIdx.x];
+  for (uint32_t base = lo; base < hi; base += kBlock) {
+    const uint32_t h = base + threadIdx.x;
     uint32_t nc = 0, row = 0;
     uint64_t b0 = 0, e0 = 0;
-    if (h < nh) {
+    if (h < hi) {
       row = list[h];
       b0 = rp[row];
       e0 = rp[row + 1];
       nc = (uint32_t)((e0 - b0 + kHeavyChunk - 1) / kHeavyChunk);
+      ctx.hacc[2 * h] = 0;
+      ctx.hacc[2 * h + 1] = 0;
+      ctx.hcnt[h] = 0;
     }
     uint32_t tot;
-    uint32_t ex = block_excl_scan(nc, sh, &tot);
+    const uint32_t ex = block_excl_scan(nc, sh, &tot);
     for (uint32_t t = 0; t < nc; ++t) {
       HeavyChunk ch;
       ch.beg = b0 + (uint64_t)t * kHeavyChunk;
@@ -127,9 +175,6 @@ __global__ void __launch_bounds__(kBlock) k_heavy_prep(Ctx ctx) {
     }
     carry += tot;
   }
-  if (threadIdx.x == 0) ctx.st->n_chunks = carry;
-  for (uint32_t h = threadIdx.x; h < 2 * nh; h += kBlock) ctx.hacc[h] = 0;
-  for (uint32_t h = threadIdx.x; h < nh; h += kBlock) ctx.hcnt[h] = 0;
 }
 
 // ---------------------------------------------------------------------------
