@@ -120,7 +120,11 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
                        uint64_t ws_bytes, void *stream);
 
 /* Algorithm 2 (Section 4.2) for graphs whose edge arrays stay in host
- * memory; only one batch of entries is on the device at a time.
+ * memory; only one batch of entries is on the device at a time.  Each batch
+ * runs Algorithm 1 with the nodes outside it frozen as singletons; the
+ * quotient graphs between outer iterations are built on the device, chunk by
+ * chunk, and kept in pinned host memory that this call allocates and frees
+ * (at most the size of the input's edge arrays).  Needs n < 2^30.
  *   g_host      host CSR (pinned memory recommended: batches are copied
  *               host-to-device asynchronously).
  *   init_host   host labels or NULL (trivial partition).

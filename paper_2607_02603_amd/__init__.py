@@ -225,7 +225,8 @@ def wl_stable_coloring_batched(g_host, init_host=None, seed=0, max_batch_entries
     """Algorithm 2.  g_host: Graph with host tensors (pinned recommended).
     Returns (colors (host int32), k, rounds, outer, coarsest)."""
     if ws is None:
-        nb = ws_bytes or wl_batched_workspace_size(g_host, max_batch_entries)
+        cap = min(max_batch_entries, max(g_host.nnz, 1)) if max_batch_entries else 0
+        nb = ws_bytes or wl_batched_workspace_size(g_host, cap)
         ws = workspace(nb, device)
     out = torch.empty(g_host.n, dtype=torch.int32)
     k, r, o = ctypes.c_uint32(0), ctypes.c_uint32(0), ctypes.c_uint32(0)

@@ -107,6 +107,12 @@ struct Ctx {
   uint32_t max_small, max_big, max_chunks, max_heavy;
   int weighted;
   int nt_stream;       // stream col_idx with non-temporal loads
+  // Batch mode (Algorithm 2): the rows are nodes [ext_lo, ext_lo + n) of a
+  // larger graph; a column outside that range is a node frozen as its own
+  // singleton class, whose value is W(seed, r, 2^32 + column).
+  int batch;
+  uint32_t ext_lo;
+  int keys_mat;        // segment keys are already in 'keys' (no gather of z)
 };
 
 }  // namespace wl

@@ -83,6 +83,12 @@ __device__ __forceinline__ uint64_t color_weight(uint64_t key, uint32_t c) {
   return fold61(mix64(key + ((uint64_t)c + 1) * kGamma));
 }
 
+// Same stream, 64-bit colour id (ids >= 2^32 name the frozen singleton
+// classes of nodes outside a batch).
+__device__ __forceinline__ uint64_t color_weight64(uint64_t key, uint64_t c) {
+  return fold61(mix64(key + (c + 1) * kGamma));
+}
+
 // ---------------------------------------------------------------------------
 // wave64 helpers
 // ---------------------------------------------------------------------------

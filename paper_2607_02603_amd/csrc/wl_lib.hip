@@ -8,6 +8,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <utility>
+#include <vector>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -17,6 +19,7 @@
 #include "wl_ctx.h"
 #include "wl_relabel.h"
 #include "wl_spmv.h"
+#include "wl_quotient.h"
 
 using namespace wl;
 
@@ -419,7 +422,7 @@ struct Session {
   template <typename RP, bool W>
   void spmv_t() {
     const DevState& h = host;
-    const bool uniform = !W && h.k == 1;
+    const bool uniform = !W && h.k == 1 && !ctx.batch;
     SpmvGrid g;
     g.heavy = h.n_chunks ? grid_for(h.n_chunks, kBlock / kWave) : 0;
     g.b2 = g.heavy + (h.bin_cnt[2] ? grid_for(h.bin_cnt[2], kBlock / 64) : 0);
@@ -465,6 +468,19 @@ struct Session {
   // Relabel by (c, z) for the current grouping; count_round = 0 for the
   // canonicalisation of the initial labels.
   int relabel(int count_round) {
+    if (int r = segmented_sort()) return r;
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_cstart, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_scatter_colors, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_round_end, dim3(1), dim3(1), 0, s, ctx, count_round);
+    HIP_LAUNCH_CHECK();
+    return pull();
+  }
+
+  // Sorts the keys inside every class of the current grouping, flags the
+  // first position of every distinct (class, key) and ranks the flags
+  // (ids, k_new).
+  int segmented_sort() {
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
     hipLaunchKernelGGL(k_fill_u8, dim3(gn), dim3(kBlock), 0, s, ctx, ctx.flags,
                        (uint64_t)L.n, (uint8_t)0);
@@ -474,7 +490,7 @@ struct Session {
     if (int r = pull()) return r;
     for (int pass = 0; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
       hipLaunchKernelGGL(k_big_tiles, dim3(1), dim3(kBlock), 0, s, ctx, pass);
-      if (pass == 0)
+      if (pass == 0 && !ctx.keys_mat)
         hipLaunchKernelGGL(k_big_gather, dim3(2048), dim3(kBlock), 0, s, ctx);
       hipLaunchKernelGGL(k_big_clear,
                          dim3(grid_for((uint64_t)host.n_big[pass & 1] * kRadix)),
@@ -496,11 +512,26 @@ struct Session {
     hipLaunchKernelGGL(k_scan_part, dim3(nscan), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
     hipLaunchKernelGGL(k_scan_final, dim3(nscan), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_cstart, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_scatter_colors, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_round_end, dim3(1), dim3(1), 0, s, ctx, count_round);
     HIP_LAUNCH_CHECK();
-    return pull();
+    return WL_OK;
+  }
+
+  // Algorithm 1 to completion on the session's graph, from labels on the
+  // device (or the trivial partition).  Leaves colours in ctx.c.
+  int run_rsc(const uint32_t* init_dev) {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_iota_zero, dim3(gn), dim3(kBlock), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    if (init_dev) {
+      hipLaunchKernelGGL(k_labels_to_z, dim3(gn), dim3(kBlock), 0, s, ctx, init_dev);
+      HIP_LAUNCH_CHECK();
+      if (int r = relabel(0)) return r;
+    }
+    if (int r = build_schedule()) return r;
+    while (!host.done) {
+      if (int r = round()) return r;
+    }
+    return WL_OK;
   }
 
   int round() {
@@ -526,6 +557,452 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
   S.rp64 = g->row_ptr64 != nullptr;
   S.weighted = g->weight != nullptr;
   S.nscan = scan_blocks(g->n);
+  return WL_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Algorithm 2 (Section 4.2): batched refinement with quotient contraction.
+// ---------------------------------------------------------------------------
+
+// The current graph G_t in host memory (the caller's arrays for t = 0, the
+// library's pinned quotient arrays afterwards).
+struct HostGraph {
+  uint64_t n = 0, m = 0;
+  const uint32_t* rp32 = nullptr;
+  const uint64_t* rp64 = nullptr;
+  const uint32_t* col = nullptr;
+  const uint32_t* wt = nullptr;
+  uint64_t rp(uint64_t i) const { return rp64 ? rp64[i] : (uint64_t)rp32[i]; }
+  // first row i in [0, n] with rp(i) >= v
+  uint64_t lower_row(uint64_t v) const {
+    uint64_t lo = 0, hi = n;
+    while (lo < hi) {
+      uint64_t mid = (lo + hi) / 2;
+      if (rp(mid) < v) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+  }
+};
+
+// Device workspace of the refinement phase: a batch's local CSR and labels
+// plus the in-core state for up to n0 rows and mb entries.
+struct RefineLayout {
+  uint64_t stage, rp, col, wt, lab, colors, core, total;
+};
+RefineLayout refine_layout(uint64_t n0, uint64_t mb) {
+  RefineLayout L{};
+  uint64_t o = 0;
+  auto take = [&](uint64_t b) { uint64_t at = o; o = align_up(o + b); return at; };
+  L.stage = take(8 * (n0 + 1));
+  L.rp = take(8 * (n0 + 1));
+  L.col = take(4 * mb);
+  L.wt = take(4 * mb);
+  L.lab = take(4 * n0);
+  L.colors = take(4 * n0);
+  L.core = take(make_layout(n0, mb).total);
+  L.total = o;
+  return L;
+}
+
+// Device workspace of the quotient phase: block of every node, representative
+// flags, a chunk of rows (mq entries) and the sort state for mq keys.
+struct QuotLayout {
+  uint64_t blk, isrep, stage, rp, qoff, col, wt, core, total;
+};
+QuotLayout quot_layout(uint64_t n0, uint64_t mq) {
+  QuotLayout L{};
+  uint64_t o = 0;
+  auto take = [&](uint64_t b) { uint64_t at = o; o = align_up(o + b); return at; };
+  L.blk = take(4 * n0);
+  L.isrep = take(n0 + 1);
+  L.stage = take(8 * (n0 + 1));
+  L.rp = take(8 * (n0 + 1));
+  L.qoff = take(8 * (n0 + 1));
+  L.col = take(4 * mq);
+  L.wt = take(4 * mq);
+  L.core = take(make_layout(mq, 0).total);
+  L.total = o;
+  return L;
+}
+
+template <typename F>
+uint64_t largest_fitting(F total_of, uint64_t budget, uint64_t cap) {
+  uint64_t lo = 0, hi = cap;
+  while (lo < hi) {
+    uint64_t mid = lo + (hi - lo + 1) / 2;
+    if (total_of(mid) <= budget) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Greedy batch cut of the entry array: ranges of at most mb entries ending
+// at a row boundary, a row longer than mb cut inside (reading of Algorithm 2).
+std::vector<uint64_t> cut_batches(const HostGraph& G, uint64_t mb) {
+  std::vector<uint64_t> starts;
+  uint64_t s = 0, row = 0;
+  const uint64_t m = G.m;
+  do {
+    starts.push_back(s);
+    if (m - s <= mb) { s = m; break; }
+    const uint64_t lim = s + mb;
+    while (row < G.n && G.rp(row + 1) <= lim) ++row;
+    uint64_t e = G.rp(row);
+    if (e <= s) e = lim;
+    s = e;
+  } while (s < m);
+  starts.push_back(m);
+  return starts;
+}
+
+struct PinnedBuf {
+  void* p = nullptr;
+  ~PinnedBuf() { if (p) (void)hipHostFree(p); }
+  int alloc(uint64_t bytes) {
+    if (p) { (void)hipHostFree(p); p = nullptr; }
+    if (bytes == 0) bytes = 8;
+    hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) return fail(WL_EHIP, "hipHostMalloc(%llu) failed: %s",
+                                     (unsigned long long)bytes, hipGetErrorString(e));
+    return WL_OK;
+  }
+};
+
+int copy_rows_h2d(const HostGraph& G, uint64_t r0, uint64_t nrows, uint8_t* stage,
+                  uint64_t* rp_dev, hipStream_t s) {
+  if (G.rp64) {
+    HIP_TRY(hipMemcpyAsync(stage, G.rp64 + r0, 8 * (nrows + 1), hipMemcpyHostToDevice, s));
+    hipLaunchKernelGGL(k_rebase_rows<uint64_t>, dim3(grid_for(nrows + 1)), dim3(kBlock), 0,
+                       s, (const uint64_t*)stage, rp_dev, (uint32_t)nrows);
+  } else {
+    HIP_TRY(hipMemcpyAsync(stage, G.rp32 + r0, 4 * (nrows + 1), hipMemcpyHostToDevice, s));
+    hipLaunchKernelGGL(k_rebase_rows<uint32_t>, dim3(grid_for(nrows + 1)), dim3(kBlock), 0,
+                       s, (const uint32_t*)stage, rp_dev, (uint32_t)nrows);
+  }
+  HIP_LAUNCH_CHECK();
+  return WL_OK;
+}
+
+struct QuotientOut {
+  std::vector<uint64_t> deg;      // entries per block
+  uint32_t* col = nullptr;        // pinned, capacity cap
+  uint32_t* wt = nullptr;
+  uint64_t m = 0, cap = 0;
+};
+
+// Sorts and reduces the keys of one chunk on the device; appends the
+// distinct (block, target, weight) triples in order (or into 'spill' for a
+// row processed in pieces).
+int quotient_chunk(Session& S, uint64_t nkeys, uint32_t bfirst, QuotientOut& Q,
+                   std::vector<std::pair<uint32_t, uint64_t>>* spill,
+                   std::vector<uint64_t>& hkey, std::vector<uint64_t>& hw) {
+  hipLaunchKernelGGL(k_q_begin, dim3(grid_for(nkeys, kBlock, 4096)), dim3(kBlock), 0, S.s,
+                     S.ctx, (uint32_t)nkeys);
+  HIP_LAUNCH_CHECK();
+  if (int r = S.segmented_sort()) return r;
+  hipLaunchKernelGGL(k_q_reduce, dim3(grid_for(nkeys, kBlock, 4096)), dim3(kBlock), 0, S.s,
+                     S.ctx, (uint32_t)nkeys);
+  HIP_LAUNCH_CHECK();
+  if (int r = S.pull()) return r;
+  const uint32_t nd = S.host.k_new;
+  hkey.resize(nd);
+  hw.resize(nd);
+  HIP_TRY(hipMemcpyAsync(hkey.data(), S.ctx.z, 8ull * nd, hipMemcpyDeviceToHost, S.s));
+  HIP_TRY(hipMemcpyAsync(hw.data(), S.ctx.x, 8ull * nd, hipMemcpyDeviceToHost, S.s));
+  HIP_TRY(hipStreamSynchronize(S.s));
+  const uint64_t mask = (1ull << kQShift) - 1;
+  for (uint32_t d = 0; d < nd; ++d) {
+    const uint64_t brel = hkey[d] >> kQShift, tgt = hkey[d] & mask;
+    if (spill) {
+      spill->push_back({(uint32_t)tgt, hw[d]});
+      continue;
+    }
+    if (hw[d] > 0xFFFFFFFFull)
+      return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
+    if (Q.m >= Q.cap) return fail(WL_EINVAL, "quotient larger than expected");
+    Q.deg[bfirst + brel] += 1;
+    Q.col[Q.m] = (uint32_t)tgt;
+    Q.wt[Q.m] = (uint32_t)hw[d];
+    Q.m++;
+  }
+  return WL_OK;
+}
+
+int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
+                uint64_t max_batch, uint32_t* color_out, uint32_t* k_out,
+                uint32_t* rounds_out, uint32_t* outer_out, int* coarsest_out,
+                void* ws, uint64_t ws_bytes, hipStream_t s) {
+  const uint64_t n0 = g->n;
+  uint8_t* W = (uint8_t*)ws;
+  // batch cap from the budget
+  const uint64_t mb_fit = largest_fitting(
+      [&](uint64_t mb) { return refine_layout(n0, mb).total; }, ws_bytes, 1ull << 40);
+  if (mb_fit == 0)
+    return fail(WL_EBUDGET, "workspace of %llu bytes is too small for %llu nodes",
+                (unsigned long long)ws_bytes, (unsigned long long)n0);
+  // a cap of at least nnz is one batch either way
+  uint64_t mb = max_batch ? std::min<uint64_t>(max_batch, std::max<uint64_t>(g->nnz, 1))
+                          : mb_fit;
+  if (mb > mb_fit)
+    return fail(WL_EBUDGET, "a batch of %llu entries needs more than %llu bytes",
+                (unsigned long long)mb, (unsigned long long)ws_bytes);
+  const uint64_t mq = largest_fitting(
+      [&](uint64_t q) { return quot_layout(n0, q).total; }, ws_bytes, (1ull << 31) - 1);
+  if (mq == 0) return fail(WL_EBUDGET, "workspace too small for the quotient phase");
+
+  HostGraph G;
+  G.n = n0;
+  G.m = g->nnz;
+  G.rp32 = g->row_ptr32;
+  G.rp64 = g->row_ptr64;
+  G.col = g->col_idx;
+  G.wt = g->weight;
+  std::vector<uint32_t> labels;  // labels of G_t's nodes (raw), empty = none
+  if (init_host) labels.assign(init_host, init_host + n0);
+  std::vector<uint32_t> map0(n0);
+  for (uint64_t i = 0; i < n0; ++i) map0[i] = (uint32_t)i;
+  PinnedBuf qrp_buf, qcol_buf, qwt_buf;  // current quotient (G_t, t >= 1)
+  PinnedBuf nrp_buf, ncol_buf, nwt_buf;  // quotient under construction
+  uint64_t rounds = 0;
+  uint32_t outer = 0;
+  std::vector<uint32_t> key, loc, blk, mapk;
+  std::vector<uint8_t> isrep;
+  std::vector<uint64_t> hkey, hw;
+
+  for (uint64_t t = 0;; ++t) {
+    const uint64_t n = G.n;
+    const std::vector<uint64_t> starts = cut_batches(G, mb);
+    const uint64_t nb = starts.size() - 1;
+    // ---- refinement of every batch (Eq. batch-init), merge keys (Eq. merge)
+    const RefineLayout RL = refine_layout(n0, mb);
+    key.assign(n, 0xFFFFFFFFu);
+    uint64_t base = 0;
+    for (uint64_t b = 0; b < nb; ++b) {
+      const uint64_t sb = starts[b], eb = starts[b + 1];
+      uint64_t r_lo = G.lower_row(sb);
+      uint64_t r_hi = (b + 1 == nb) ? n : G.lower_row(eb);
+      if (r_hi > r_lo && G.rp(r_hi) > eb) --r_hi;  // the last row continues
+      if (r_hi <= r_lo) {
+        // no inner node: every node is a frozen singleton, Algorithm 1 stops
+        // after the one round that confirms it
+        rounds += 1;
+        continue;
+      }
+      const uint64_t nl = r_hi - r_lo, e0 = G.rp(r_lo), ml = G.rp(r_hi) - e0;
+      uint64_t* rp_dev = (uint64_t*)(W + RL.rp);
+      uint32_t* col_dev = (uint32_t*)(W + RL.col);
+      uint32_t* wt_dev = G.wt ? (uint32_t*)(W + RL.wt) : nullptr;
+      uint32_t* lab_dev = labels.empty() ? nullptr : (uint32_t*)(W + RL.lab);
+      uint32_t* colors_dev = (uint32_t*)(W + RL.colors);
+      if (int r = copy_rows_h2d(G, r_lo, nl, W + RL.stage, rp_dev, s)) return r;
+      if (ml) {
+        HIP_TRY(hipMemcpyAsync(col_dev, G.col + e0, 4 * ml, hipMemcpyHostToDevice, s));
+        if (wt_dev)
+          HIP_TRY(hipMemcpyAsync(wt_dev, G.wt + e0, 4 * ml, hipMemcpyHostToDevice, s));
+      }
+      if (lab_dev)
+        HIP_TRY(hipMemcpyAsync(lab_dev, labels.data() + r_lo, 4 * nl,
+                               hipMemcpyHostToDevice, s));
+      wl_csr lg{};
+      lg.n = nl;
+      lg.nnz = ml;
+      lg.row_ptr64 = rp_dev;
+      lg.col_idx = col_dev;
+      lg.weight = wt_dev;
+      Session S;
+      if (int r = open_session(S, &lg, colors_dev, W + RL.core, RL.total - RL.core, s))
+        return r;
+      S.ctx.batch = 1;
+      S.ctx.ext_lo = (uint32_t)r_lo;
+      const uint64_t sb_seed = seed + ((t << 32) + b + 1) * 0x9E3779B97F4A7C15ull;
+      uint64_t z = sb_seed;  // mix(seed + (2^32 t + b + 1) g)
+      z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+      z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+      z ^= z >> 31;
+      if (int r = S.init_state(z, 1, 0, (uint32_t)std::min<uint64_t>(nl + 1, 0xFFFFFFFFull), 1))
+        return r;
+      if (int r = S.run_rsc(lab_dev)) return r;
+      if (S.host.done == 2) return fail(WL_EMAXROUNDS, "batch refinement did not stabilise");
+      rounds += S.host.round;
+      loc.resize(nl);
+      HIP_TRY(hipMemcpyAsync(loc.data(), colors_dev, 4 * nl, hipMemcpyDeviceToHost, s));
+      HIP_TRY(hipStreamSynchronize(s));
+      for (uint64_t i = 0; i < nl; ++i) key[r_lo + i] = (uint32_t)(base + loc[i]);
+      base += S.host.k;
+    }
+    // ---- merged partition: first-occurrence ids; boundary nodes singletons
+    mapk.assign(base, 0xFFFFFFFFu);
+    blk.resize(n);
+    isrep.assign(n, 0);
+    uint32_t next = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+      const uint32_t kk = key[i];
+      if (kk == 0xFFFFFFFFu) {
+        isrep[i] = 1;
+        blk[i] = next++;
+      } else {
+        if (mapk[kk] == 0xFFFFFFFFu) {
+          mapk[kk] = next++;
+          isrep[i] = 1;
+        }
+        blk[i] = mapk[kk];
+      }
+    }
+    ++outer;
+    for (uint64_t v = 0; v < n0; ++v) map0[v] = blk[map0[v]];
+    const uint64_t nq = next;
+    if (nb == 1 || nq == n) {
+      *coarsest_out = (nb == 1) ? 1 : 0;
+      break;
+    }
+    // ---- quotient graph (Definition "Quotient Graph"), on the device
+    uint64_t qcap = 0;
+    for (uint64_t i = 0; i < n; ++i)
+      if (isrep[i]) qcap += G.rp(i + 1) - G.rp(i);
+    QuotientOut Q;
+    Q.deg.assign(nq, 0);
+    if (int r = ncol_buf.alloc(4 * qcap)) return r;
+    if (int r = nwt_buf.alloc(4 * qcap)) return r;
+    Q.col = (uint32_t*)ncol_buf.p;
+    Q.wt = (uint32_t*)nwt_buf.p;
+    Q.cap = qcap;
+    const QuotLayout QL = quot_layout(n0, mq);
+    uint32_t* blk_dev = (uint32_t*)(W + QL.blk);
+    uint8_t* isrep_dev = W + QL.isrep;
+    uint64_t* rp_dev = (uint64_t*)(W + QL.rp);
+    uint64_t* qoff_dev = (uint64_t*)(W + QL.qoff);
+    uint32_t* col_dev = (uint32_t*)(W + QL.col);
+    uint32_t* wt_dev = (uint32_t*)(W + QL.wt);
+    HIP_TRY(hipMemcpyAsync(blk_dev, blk.data(), 4 * n, hipMemcpyHostToDevice, s));
+    HIP_TRY(hipMemcpyAsync(isrep_dev, isrep.data(), n, hipMemcpyHostToDevice, s));
+    std::vector<uint64_t> qoff;
+    uint64_t a = 0;
+    while (a < n) {
+      // rows [a, bnd) with at most mq entries, at least one row
+      uint64_t bnd = a + 1;
+      const uint64_t ea = G.rp(a);
+      {
+        uint64_t lo = a + 1, hi = n;  // last row end <= ea + mq
+        while (lo < hi) {
+          uint64_t mid = lo + (hi - lo + 1) / 2;
+          if (G.rp(mid) - ea <= mq) lo = mid; else hi = mid - 1;
+        }
+        bnd = lo;
+      }
+      const uint64_t ent = G.rp(bnd) - ea;
+      if (ent > mq) {
+        // a single row longer than the chunk: pieces, merged on the host
+        if (isrep[a]) {
+          std::vector<std::pair<uint32_t, uint64_t>> spill;
+          for (uint64_t off = 0; off < ent; off += mq) {
+            const uint64_t len = std::min(mq, ent - off);
+            const uint64_t rp2[2] = {0, len};
+            HIP_TRY(hipMemcpyAsync(rp_dev, rp2, 16, hipMemcpyHostToDevice, s));
+            const uint64_t z0 = 0;
+            HIP_TRY(hipMemcpyAsync(qoff_dev, &z0, 8, hipMemcpyHostToDevice, s));
+            HIP_TRY(hipMemcpyAsync(col_dev, G.col + ea + off, 4 * len,
+                                   hipMemcpyHostToDevice, s));
+            if (G.wt)
+              HIP_TRY(hipMemcpyAsync(wt_dev, G.wt + ea + off, 4 * len,
+                                     hipMemcpyHostToDevice, s));
+            wl_csr sg{};
+            sg.n = len;
+            sg.nnz = 0;
+            sg.row_ptr64 = rp_dev;
+            Session S;
+            if (int r = open_session(S, &sg, nullptr, W + QL.core, QL.total - QL.core, s))
+              return r;
+            S.ctx.keys_mat = 1;
+            if (int r = S.init_state(0, 1, 0, 1, 1)) return r;
+            hipLaunchKernelGGL(k_q_keys, dim3(1), dim3(kBlock), 0, s, S.ctx, rp_dev,
+                               col_dev, G.wt ? wt_dev : nullptr, blk_dev, isrep_dev,
+                               qoff_dev, 1u, (uint32_t)a, blk[a]);
+            HIP_LAUNCH_CHECK();
+            if (int r = quotient_chunk(S, len, blk[a], Q, &spill, hkey, hw)) return r;
+          }
+          std::sort(spill.begin(), spill.end());
+          for (size_t i = 0; i < spill.size();) {
+            size_t j = i;
+            uint64_t w = 0;
+            while (j < spill.size() && spill[j].first == spill[i].first) w += spill[j++].second;
+            if (w > 0xFFFFFFFFull) return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
+            if (Q.m >= Q.cap) return fail(WL_EINVAL, "quotient larger than expected");
+            Q.deg[blk[a]] += 1;
+            Q.col[Q.m] = spill[i].first;
+            Q.wt[Q.m] = (uint32_t)w;
+            Q.m++;
+            i = j;
+          }
+        }
+        a = a + 1;
+        continue;
+      }
+      const uint64_t nrows = bnd - a;
+      qoff.resize(nrows);
+      uint64_t run = 0;
+      uint32_t bfirst = 0xFFFFFFFFu;
+      for (uint64_t r = 0; r < nrows; ++r) {
+        qoff[r] = run;
+        if (isrep[a + r]) {
+          if (bfirst == 0xFFFFFFFFu) bfirst = blk[a + r];
+          run += G.rp(a + r + 1) - G.rp(a + r);
+        }
+      }
+      if (run > 0) {
+        if (int r = copy_rows_h2d(G, a, nrows, W + QL.stage, rp_dev, s)) return r;
+        HIP_TRY(hipMemcpyAsync(qoff_dev, qoff.data(), 8 * nrows, hipMemcpyHostToDevice, s));
+        HIP_TRY(hipMemcpyAsync(col_dev, G.col + ea, 4 * ent, hipMemcpyHostToDevice, s));
+        if (G.wt)
+          HIP_TRY(hipMemcpyAsync(wt_dev, G.wt + ea, 4 * ent, hipMemcpyHostToDevice, s));
+        wl_csr sg{};
+        sg.n = run;
+        sg.nnz = 0;
+        sg.row_ptr64 = rp_dev;
+        Session S;
+        if (int r = open_session(S, &sg, nullptr, W + QL.core, QL.total - QL.core, s))
+          return r;
+        S.ctx.keys_mat = 1;
+        if (int r = S.init_state(0, 1, 0, 1, 1)) return r;
+        hipLaunchKernelGGL(k_q_keys, dim3(grid_for(nrows, kBlock / kWave, 8192)),
+                           dim3(kBlock), 0, s, S.ctx, rp_dev, col_dev,
+                           G.wt ? wt_dev : nullptr, blk_dev, isrep_dev, qoff_dev,
+                           (uint32_t)nrows, (uint32_t)a, bfirst);
+        HIP_LAUNCH_CHECK();
+        if (int r = quotient_chunk(S, run, bfirst, Q, nullptr, hkey, hw)) return r;
+      }
+      a = bnd;
+    }
+    // new row pointers and labels
+    if (int r = nrp_buf.alloc(8 * (nq + 1))) return r;
+    uint64_t* qrp = (uint64_t*)nrp_buf.p;
+    qrp[0] = 0;
+    for (uint64_t q = 0; q < nq; ++q) qrp[q + 1] = qrp[q] + Q.deg[q];
+    if (!labels.empty()) {
+      std::vector<uint32_t> nl(nq);
+      for (uint64_t i = 0; i < n; ++i)
+        if (isrep[i]) nl[blk[i]] = labels[i];
+      labels.swap(nl);
+    }
+    std::swap(qrp_buf.p, nrp_buf.p);
+    std::swap(qcol_buf.p, ncol_buf.p);
+    std::swap(qwt_buf.p, nwt_buf.p);
+    G.n = nq;
+    G.m = Q.m;
+    G.rp32 = nullptr;
+    G.rp64 = (const uint64_t*)qrp_buf.p;
+    G.col = (const uint32_t*)qcol_buf.p;
+    G.wt = (const uint32_t*)qwt_buf.p;
+  }
+  // final colours: first occurrence over the original nodes
+  mapk.assign(n0, 0xFFFFFFFFu);
+  uint32_t k = 0;
+  for (uint64_t v = 0; v < n0; ++v) {
+    uint32_t& slot = mapk[map0[v]];
+    if (slot == 0xFFFFFFFFu) slot = k++;
+    color_out[v] = slot;
+  }
+  *k_out = k;
+  *rounds_out = (uint32_t)std::min<uint64_t>(rounds, 0xFFFFFFFFull);
+  *outer_out = outer;
   return WL_OK;
 }
 
@@ -561,9 +1038,13 @@ int wl_workspace_size(const wl_csr* g, uint64_t* bytes_out) {
 
 int wl_batched_workspace_size(const wl_csr* g, uint64_t max_batch_entries,
                               uint64_t* bytes_out) {
-  (void)max_batch_entries;
+  g_err[0] = 0;
   if (!g || !bytes_out) return fail(WL_EINVAL, "NULL argument");
-  return fail(WL_EINVAL, "batched refinement is not available in this build");
+  if (g->n >= (1ull << kQShift))
+    return fail(WL_EOVERFLOW, "the batched path needs n < 2^%d", kQShift);
+  const uint64_t mb = max_batch_entries ? max_batch_entries : std::max<uint64_t>(g->nnz, 1);
+  *bytes_out = std::max(refine_layout(g->n, mb).total, quot_layout(g->n, 1).total);
+  return WL_OK;
 }
 
 int wl_refine_round(const wl_csr* g, const uint32_t* color_in, uint32_t k_in,
@@ -625,18 +1106,7 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
   if (int r = S.init_state(seed, 1, 0, cap, 1)) return r;
   if (int r = S.validate_device()) return r;
   if (int r = S.stats_begin()) return r;
-  const uint32_t gn = grid_for(g->n, kBlock, 4096);
-  hipLaunchKernelGGL(k_iota_zero, dim3(gn), dim3(kBlock), 0, S.s, S.ctx);
-  HIP_LAUNCH_CHECK();
-  if (init_color) {
-    hipLaunchKernelGGL(k_labels_to_z, dim3(gn), dim3(kBlock), 0, S.s, S.ctx, init_color);
-    HIP_LAUNCH_CHECK();
-    if (int r = S.relabel(0)) return r;
-  }
-  if (int r = S.build_schedule()) return r;
-  while (!S.host.done) {
-    if (int r = S.round()) return r;
-  }
+  if (int r = S.run_rsc(init_color)) return r;
   if (int r = S.stats_end()) return r;
   *k_out = S.host.k;
   *rounds_out = S.host.round;
@@ -651,10 +1121,26 @@ int wl_stable_coloring_batched(const wl_csr* g_host, const uint32_t* init_host,
                                uint32_t* rounds_out, uint32_t* outer_out,
                                int* coarsest_out, void* workspace, uint64_t ws_bytes,
                                void* stream) {
-  (void)g_host; (void)init_host; (void)seed; (void)max_batch_entries;
-  (void)color_out_host; (void)k_out; (void)rounds_out; (void)outer_out;
-  (void)coarsest_out; (void)workspace; (void)ws_bytes; (void)stream;
-  return fail(WL_EINVAL, "batched refinement is not available in this build");
+  g_err[0] = 0;
+  if (int r = check_graph(g_host)) return r;
+  if (!k_out || !rounds_out || !outer_out || !coarsest_out)
+    return fail(WL_EINVAL, "output scalar is NULL");
+  *k_out = 0;
+  *rounds_out = 0;
+  *outer_out = 0;
+  *coarsest_out = 1;
+  if (g_host->n >= (1ull << kQShift))
+    return fail(WL_EOVERFLOW, "the batched path needs n < 2^%d", kQShift);
+  if (g_host->n == 0) return WL_OK;
+  if (!color_out_host) return fail(WL_EINVAL, "color_out_host is NULL");
+  if (!workspace) return fail(WL_EINVAL, "workspace is NULL");
+  if ((uintptr_t)workspace % kAlign) return fail(WL_EINVAL, "workspace must be 256-byte aligned");
+  const uint64_t last = g_host->row_ptr64 ? g_host->row_ptr64[g_host->n]
+                                          : g_host->row_ptr32[g_host->n];
+  if (last != g_host->nnz) return fail(WL_EINVAL, "row_ptr[n] != nnz");
+  return batched_run(g_host, init_host, seed, max_batch_entries, color_out_host, k_out,
+                     rounds_out, outer_out, coarsest_out, workspace, ws_bytes,
+                     (hipStream_t)stream);
 }
 
 int wl_verify_stable(const wl_csr* g, const uint32_t* color, uint32_t k,

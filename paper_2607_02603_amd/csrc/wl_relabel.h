@@ -80,10 +80,11 @@ __global__ void __launch_bounds__(kBlock) k_segments(Ctx ctx) {
     const bool tiny = len >= 2 && len <= kTinyMax;
     const bool small = len > kTinyMax && len <= kSmallMax;
     const bool big = len > kSmallMax;
+    const uint32_t mat = ctx.keys_mat ? kMatBit : 0u;
     const uint32_t t = block_append(tiny, &st->n_tiny, sh, &base_sh);
-    if (tiny) ctx.tiny_list[t] = make_uint2(s, len);
+    if (tiny) ctx.tiny_list[t] = make_uint2(s, len | mat);
     const uint32_t a = block_append(small, &st->n_small, sh, &base_sh);
-    if (small) ctx.small_list[a] = make_uint2(s, len);
+    if (small) ctx.small_list[a] = make_uint2(s, len | mat);
     const uint32_t b = block_append(big, &st->n_big[0], sh, &base_sh);
     if (big) ctx.big_list0[b] = make_uint2(s, len);
   }

@@ -191,7 +191,13 @@ __global__ void __launch_bounds__(kBlock) k_heavy_fill(Ctx ctx) {
 enum GatherMode { kGatherX = 0, kGather16 = 1, kGather8 = 2 };
 
 template <int M>
-__device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j) {
+__device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j,
+                                                 uint64_t rkey) {
+  if (ctx.batch) {
+    const uint32_t jl = j - ctx.ext_lo;
+    if (jl >= ctx.n) return color_weight64(rkey, (1ull << 32) + j);
+    j = jl;
+  }
   if (M == kGather16) return ctx.wtab[ctx.c16[j]];
   if (M == kGather8) return ctx.wtab[ctx.c8[j]];
   return ctx.x[j];
@@ -199,7 +205,8 @@ __device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j) {
 
 template <int U, bool W, int M>
 __device__ __forceinline__ void accumulate(const Ctx& ctx, Acc96& a, uint64_t e0,
-                                           uint64_t end, uint32_t stride) {
+                                           uint64_t end, uint32_t stride,
+                                           uint64_t rkey) {
   uint32_t j[U];
   bool ok[U];
 #pragma unroll
@@ -212,7 +219,7 @@ __device__ __forceinline__ void accumulate(const Ctx& ctx, Acc96& a, uint64_t e0
   uint64_t v[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    v[u] = ok[u] ? gather_value<M>(ctx, j[u]) : 0ull;
+    v[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
     if (W && ok[u]) v[u] = mul_small_fold(ctx.wgt[e0 + (uint64_t)u * stride], v[u]);
   }
 #pragma unroll
@@ -221,7 +228,7 @@ __device__ __forceinline__ void accumulate(const Ctx& ctx, Acc96& a, uint64_t e0
 
 template <int G, int U, typename RP, bool W, int M>
 __device__ __forceinline__ void spmv_rows(const Ctx& ctx, int bin, uint32_t bid,
-                                          uint32_t nblk) {
+                                          uint32_t nblk, uint64_t rkey) {
   const RP* rp = rowptr<RP>(ctx);
   const uint32_t cnt = ctx.st->bin_cnt[bin];
   const uint32_t* list = ctx.rows + ctx.st->bin_start[bin];
@@ -234,7 +241,7 @@ __device__ __forceinline__ void spmv_rows(const Ctx& ctx, int bin, uint32_t bid,
     const uint64_t beg = rp[row], end = rp[row + 1];
     Acc96 a{0, 0};
     for (uint64_t e0 = beg + sub; e0 < end; e0 += (uint64_t)G * U)
-      accumulate<U, W, M>(ctx, a, e0, end, G);
+      accumulate<U, W, M>(ctx, a, e0, end, G, rkey);
     const uint64_t r = group_sum_p<G>(acc_reduce(a));
     if (sub == 0) ctx.z[row] = r;
   }
@@ -242,7 +249,7 @@ __device__ __forceinline__ void spmv_rows(const Ctx& ctx, int bin, uint32_t bid,
 
 template <bool W, int M>
 __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
-                                           uint32_t nblk) {
+                                           uint32_t nblk, uint64_t rkey) {
   const uint32_t nch = ctx.st->n_chunks;
   const int lane = lane_id();
   const uint32_t nwaves = nblk * (kBlock / kWave);
@@ -253,7 +260,7 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
     Acc96 a{0, 0};
     const uint64_t end = ch.beg + ch.len;
     for (uint64_t e0 = ch.beg + lane; e0 < end; e0 += (uint64_t)kWave * 4)
-      accumulate<4, W, M>(ctx, a, e0, end, kWave);
+      accumulate<4, W, M>(ctx, a, e0, end, kWave, rkey);
     const uint64_t r = group_sum_p<kWave>(acc_reduce(a));
     if (lane == 0) {
       // Partial sums of the row's chunks meet in two 64-bit accumulators
@@ -279,15 +286,16 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
 template <typename RP, bool W, int M>
 __global__ void __launch_bounds__(kBlock) k_spmv(Ctx ctx, SpmvGrid g) {
   if (ctx.st->done) return;
+  const uint64_t rkey = ctx.batch ? round_key(ctx.st->seed, ctx.st->round) : 0;
   const uint32_t b = blockIdx.x;
   if (b < g.heavy)
-    spmv_heavy<W, M>(ctx, b, g.heavy);
+    spmv_heavy<W, M>(ctx, b, g.heavy, rkey);
   else if (b < g.b2)
-    spmv_rows<64, 4, RP, W, M>(ctx, 2, b - g.heavy, g.b2 - g.heavy);
+    spmv_rows<64, 4, RP, W, M>(ctx, 2, b - g.heavy, g.b2 - g.heavy, rkey);
   else if (b < g.b1)
-    spmv_rows<16, 4, RP, W, M>(ctx, 1, b - g.b2, g.b1 - g.b2);
+    spmv_rows<16, 4, RP, W, M>(ctx, 1, b - g.b2, g.b1 - g.b2, rkey);
   else
-    spmv_rows<4, 2, RP, W, M>(ctx, 0, b - g.b1, g.b0 - g.b1);
+    spmv_rows<4, 2, RP, W, M>(ctx, 0, b - g.b1, g.b0 - g.b1, rkey);
 }
 
 // One colour and unit weights: every x_j is the same w, so

@@ -1,0 +1,119 @@
+"""GPU parity of Algorithm 2 (wl_stable_coloring_batched) with the batched
+oracle: identical first-occurrence colours, colour count, rounds summed over
+the batch runs, outer iterations and the coarsest flag."""
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_02603_amd as wl
+from oracle import bruteforce as bf
+from paper_2607_02603_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _host_graph(rp, col, wt=None):
+    n = len(rp) - 1
+    g = wl.Graph.from_numpy(n, rp, col, wt, device=None)
+    return wl.Graph(n, g.row_ptr.pin_memory(), g.col_idx.pin_memory(),
+                    None if g.weight is None else g.weight.pin_memory())
+
+
+def _check(rp, col, wt=None, init=None, mb=8, seed=0):
+    g = _host_graph(rp, col, wt)
+    init_t = None if init is None else torch.from_numpy(np.asarray(init, np.uint32).view(np.int32))
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, init_t, seed, mb)
+    got = c.numpy().view(np.uint32)
+    ref, kr, rr, orr, cr, st = oracle.batched_coloring(rp, col, wt, init, seed, mb)
+    assert st == 0
+    assert np.array_equal(got, ref)
+    assert (k, outer, coarsest) == (kr, orr, cr)
+    assert r == rr
+    assert oracle.is_stable(rp, col, wt, got)
+    return got, k, r, outer, coarsest
+
+
+@pytest.mark.parametrize("mb", [1, 3, 8, 40, 300, 10**9])
+def test_rmat_small_various_caps(mb):
+    g = inputs.rmat(9, 6, seed=6)
+    print(f"rmat9 mb={mb}", flush=True)
+    _check(g.row_ptr, g.col, mb=mb, seed=mb)
+
+
+def test_single_batch_equals_in_core():
+    g = inputs.rmat(11, 8, seed=5)
+    got, k, r, outer, coarsest = _check(g.row_ptr, g.col, mb=10**9)
+    assert coarsest and outer == 1
+    ref = oracle.stable_coloring(g.row_ptr, g.col)[0]
+    assert np.array_equal(got, oracle.first_occurrence(ref)[0])
+
+
+def test_disjoint_paths_contract_to_coarsest():
+    edges = [(4 * t + i, 4 * t + i + 1) for t in range(30) for i in range(3)]
+    rp, col = bf.to_csr(120, edges)
+    got, k, r, outer, coarsest = _check(rp, col, mb=12)
+    assert outer >= 2 and coarsest and k == 2
+
+
+def test_grid_fixed_point_case_ii():
+    g = inputs.grid_graph(6, 7)
+    got, k, r, outer, coarsest = _check(g.row_ptr, g.col, mb=12)
+    assert outer == 1 and not coarsest
+
+
+@pytest.mark.parametrize("trial", range(6))
+def test_random_weighted_directed(trial):
+    rng = random.Random(40 + trial)
+    n = rng.randint(5, 200)
+    edges = [(rng.randrange(n), rng.randrange(n)) for _ in range(rng.randint(n, 6 * n))]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    wt = np.array([rng.randint(1, 5) for _ in range(col.size)], np.uint32)
+    init = None
+    if trial % 2:
+        init = np.array([rng.choice([3, 9]) for _ in range(n)], np.uint32)
+    for mb in (5, 37, 10**6):
+        _check(rp, col, wt, init, mb=mb, seed=trial)
+
+
+def test_long_multi_edge_row_quotient_pieces():
+    # a row with far more entries than nodes: the quotient phase cuts it
+    # into pieces when the workspace is tight
+    n = 12
+    edges = [(0, 1 + (i % 11)) for i in range(3000)] + [(i, i + 1) for i in range(1, 11)]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    g = _host_graph(rp, col)
+    mb = 16
+    need = wl.wl_batched_workspace_size(g, mb)
+    ws = wl.workspace(need)
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, None, 0, mb, ws=ws)
+    ref, kr, rr, orr, cr, st = oracle.batched_coloring(rp, col, None, None, 0, mb)
+    assert np.array_equal(c.numpy().view(np.uint32), ref)
+    assert (k, r, outer, coarsest) == (kr, rr, orr, cr)
+
+
+def test_edge_cases():
+    # edgeless graph, one node, empty graph
+    for n in (1, 5):
+        rp = np.zeros(n + 1, np.uint64)
+        col = np.zeros(0, np.uint32)
+        _check(rp, col, mb=4)
+    g = _host_graph(np.zeros(1, np.uint64), np.zeros(0, np.uint32))
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, None, 0, 4)
+    assert (k, r) == (0, 0)
+
+
+def test_budget_errors():
+    g0 = inputs.rmat(8, 4, seed=1)
+    g = _host_graph(g0.row_ptr, g0.col)
+    need = wl.wl_batched_workspace_size(g, 50)
+    ws = wl.workspace(need)
+    # a larger cap than the workspace allows
+    with pytest.raises(wl.WlError) as e:
+        wl.wl_stable_coloring_batched(g, None, 0, 10**9, ws=ws)
+    assert e.value.code == wl.WL_EBUDGET
+    # cap 0 = the largest that fits: still a valid, stable result
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, None, 0, 0, ws=ws)
+    assert oracle.is_stable(g0.row_ptr, g0.col, None, c.numpy().view(np.uint32))
