@@ -296,7 +296,8 @@ struct Session {
   hipStream_t s;
   bool rp64;
   bool weighted;
-  DevState host;  // last copy of the device state
+  DevState host;      // last copy of the device state
+  DevState init_src;  // source of the initial state copy
   uint32_t nscan;
   // diagnostics
   int sflags = 0;
@@ -357,6 +358,9 @@ struct Session {
     return stats_collect();
   }
 
+  // The source of the copy is a member that outlives it, and the copy is
+  // synchronised: an asynchronous copy from pageable host memory may read
+  // the source after this function returns.
   int init_state(uint64_t seed, uint32_t k, uint32_t round, uint32_t max_rounds,
                  uint32_t dense) {
     DevState h{};
@@ -366,7 +370,9 @@ struct Session {
     h.max_rounds = max_rounds;
     h.seed = seed;
     host = h;
-    HIP_TRY(hipMemcpyAsync(ctx.st, &h, sizeof(DevState), hipMemcpyHostToDevice, s));
+    init_src = h;
+    HIP_TRY(hipMemcpyAsync(ctx.st, &init_src, sizeof(DevState), hipMemcpyHostToDevice, s));
+    HIP_TRY(hipStreamSynchronize(s));
     return WL_OK;
   }
 
@@ -639,19 +645,45 @@ uint64_t largest_fitting(F total_of, uint64_t budget, uint64_t cap) {
 // at a row boundary, a row longer than mb cut inside (reading of Algorithm 2).
 std::vector<uint64_t> cut_batches(const HostGraph& G, uint64_t mb) {
   std::vector<uint64_t> starts;
-  uint64_t s = 0, row = 0;
+  uint64_t s = 0;
   const uint64_t m = G.m;
   do {
     starts.push_back(s);
     if (m - s <= mb) { s = m; break; }
     const uint64_t lim = s + mb;
-    while (row < G.n && G.rp(row + 1) <= lim) ++row;
-    uint64_t e = G.rp(row);
+    // last row boundary <= lim
+    uint64_t lo = 0, hi = G.n;
+    while (lo < hi) {
+      uint64_t mid = lo + (hi - lo + 1) / 2;
+      if (G.rp(mid) <= lim) lo = mid; else hi = mid - 1;
+    }
+    uint64_t e = G.rp(lo);
     if (e <= s) e = lim;
     s = e;
   } while (s < m);
   starts.push_back(m);
   return starts;
+}
+
+// Inner rows of batch b (Definition "Inner and boundary nodes"): the rows
+// that start inside it and end inside it; empty rows belong to the batch
+// whose range contains their offset.
+void inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts, uint64_t b,
+                uint64_t* r_lo, uint64_t* r_hi) {
+  const uint64_t nb = starts.size() - 1, eb = starts[b + 1];
+  *r_lo = G.lower_row(starts[b]);
+  *r_hi = (b + 1 == nb) ? G.n : G.lower_row(eb);
+  if (*r_hi > *r_lo && G.rp(*r_hi) > eb) --*r_hi;  // the last row continues
+}
+
+uint64_t max_inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts) {
+  uint64_t mx = 0;
+  for (uint64_t b = 0; b + 1 < starts.size(); ++b) {
+    uint64_t lo, hi;
+    inner_rows(G, starts, b, &lo, &hi);
+    if (hi > lo) mx = std::max(mx, hi - lo);
+  }
+  return mx;
 }
 
 struct PinnedBuf {
@@ -733,21 +765,8 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
                 void* ws, uint64_t ws_bytes, hipStream_t s) {
   const uint64_t n0 = g->n;
   uint8_t* W = (uint8_t*)ws;
-  // batch cap from the budget
-  const uint64_t mb_fit = largest_fitting(
-      [&](uint64_t mb) { return refine_layout(n0, mb).total; }, ws_bytes, 1ull << 40);
-  if (mb_fit == 0)
-    return fail(WL_EBUDGET, "workspace of %llu bytes is too small for %llu nodes",
-                (unsigned long long)ws_bytes, (unsigned long long)n0);
-  // a cap of at least nnz is one batch either way
-  uint64_t mb = max_batch ? std::min<uint64_t>(max_batch, std::max<uint64_t>(g->nnz, 1))
-                          : mb_fit;
-  if (mb > mb_fit)
-    return fail(WL_EBUDGET, "a batch of %llu entries needs more than %llu bytes",
-                (unsigned long long)mb, (unsigned long long)ws_bytes);
-  const uint64_t mq = largest_fitting(
-      [&](uint64_t q) { return quot_layout(n0, q).total; }, ws_bytes, (1ull << 31) - 1);
-  if (mq == 0) return fail(WL_EBUDGET, "workspace too small for the quotient phase");
+  const char* tr = getenv("WL_TRACE_BATCHED");
+  const bool trace = tr && tr[0] == '1';
 
   HostGraph G;
   G.n = n0;
@@ -767,20 +786,55 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   std::vector<uint32_t> key, loc, blk, mapk;
   std::vector<uint8_t> isrep;
   std::vector<uint64_t> hkey, hw;
+  std::vector<uint64_t> piece_rp(3);
 
   for (uint64_t t = 0;; ++t) {
     const uint64_t n = G.n;
-    const std::vector<uint64_t> starts = cut_batches(G, mb);
+    // ---- batch cap: the caller's, or the largest whose batches fit
+    const uint64_t mall = std::max<uint64_t>(G.m, 1);  // a cap >= nnz is one batch
+    uint64_t mb;
+    std::vector<uint64_t> starts;
+    if (max_batch) {
+      mb = std::min(max_batch, mall);
+      starts = cut_batches(G, mb);
+    } else {
+      auto fits = [&](uint64_t cap) {
+        const std::vector<uint64_t> st = cut_batches(G, cap);
+        return refine_layout(max_inner_rows(G, st), cap).total <= ws_bytes;
+      };
+      uint64_t lo = 0, hi = std::min(mall, ws_bytes / 8);
+      while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (fits(mid)) lo = mid; else hi = mid - 1;
+      }
+      if (lo == 0)
+        return fail(WL_EBUDGET, "workspace of %llu bytes holds no batch",
+                    (unsigned long long)ws_bytes);
+      mb = lo;
+      starts = cut_batches(G, mb);
+    }
     const uint64_t nb = starts.size() - 1;
+    const uint64_t rows_cap = max_inner_rows(G, starts);
+    const RefineLayout RL = refine_layout(rows_cap, mb);
+    if (RL.total > ws_bytes)
+      return fail(WL_EBUDGET, "a batch of %llu entries and %llu rows needs %llu bytes, "
+                  "the workspace has %llu", (unsigned long long)mb,
+                  (unsigned long long)rows_cap, (unsigned long long)RL.total,
+                  (unsigned long long)ws_bytes);
+    const uint64_t mq = largest_fitting(
+        [&](uint64_t q) { return quot_layout(n, q).total; }, ws_bytes, (1ull << 31) - 1);
+    if (mq == 0) return fail(WL_EBUDGET, "workspace too small for the quotient phase");
+    if (trace)
+      fprintf(stderr, "[wl batched] t=%llu n=%llu m=%llu cap=%llu batches=%llu rows_cap=%llu "
+              "quotient_chunk=%llu\n", (unsigned long long)t, (unsigned long long)n,
+              (unsigned long long)G.m, (unsigned long long)mb, (unsigned long long)nb,
+              (unsigned long long)rows_cap, (unsigned long long)mq);
     // ---- refinement of every batch (Eq. batch-init), merge keys (Eq. merge)
-    const RefineLayout RL = refine_layout(n0, mb);
     key.assign(n, 0xFFFFFFFFu);
     uint64_t base = 0;
     for (uint64_t b = 0; b < nb; ++b) {
-      const uint64_t sb = starts[b], eb = starts[b + 1];
-      uint64_t r_lo = G.lower_row(sb);
-      uint64_t r_hi = (b + 1 == nb) ? n : G.lower_row(eb);
-      if (r_hi > r_lo && G.rp(r_hi) > eb) --r_hi;  // the last row continues
+      uint64_t r_lo, r_hi;
+      inner_rows(G, starts, b, &r_lo, &r_hi);
       if (r_hi <= r_lo) {
         // no inner node: every node is a frozen singleton, Algorithm 1 stops
         // after the one round that confirms it
@@ -823,6 +877,10 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       if (int r = S.run_rsc(lab_dev)) return r;
       if (S.host.done == 2) return fail(WL_EMAXROUNDS, "batch refinement did not stabilise");
       rounds += S.host.round;
+      if (trace)
+        fprintf(stderr, "[wl batched]   batch %llu rows [%llu, %llu) entries %llu colours %u rounds %u\n",
+                (unsigned long long)b, (unsigned long long)r_lo, (unsigned long long)r_hi,
+                (unsigned long long)ml, S.host.k, S.host.round);
       loc.resize(nl);
       HIP_TRY(hipMemcpyAsync(loc.data(), colors_dev, 4 * nl, hipMemcpyDeviceToHost, s));
       HIP_TRY(hipStreamSynchronize(s));
@@ -850,6 +908,9 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     ++outer;
     for (uint64_t v = 0; v < n0; ++v) map0[v] = blk[map0[v]];
     const uint64_t nq = next;
+    if (trace)
+      fprintf(stderr, "[wl batched] t=%llu merged blocks=%llu rounds so far=%llu\n",
+              (unsigned long long)t, (unsigned long long)nq, (unsigned long long)rounds);
     if (nb == 1 || nq == n) {
       *coarsest_out = (nb == 1) ? 1 : 0;
       break;
@@ -865,7 +926,7 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     Q.col = (uint32_t*)ncol_buf.p;
     Q.wt = (uint32_t*)nwt_buf.p;
     Q.cap = qcap;
-    const QuotLayout QL = quot_layout(n0, mq);
+    const QuotLayout QL = quot_layout(n, mq);
     uint32_t* blk_dev = (uint32_t*)(W + QL.blk);
     uint8_t* isrep_dev = W + QL.isrep;
     uint64_t* rp_dev = (uint64_t*)(W + QL.rp);
@@ -895,10 +956,12 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
           std::vector<std::pair<uint32_t, uint64_t>> spill;
           for (uint64_t off = 0; off < ent; off += mq) {
             const uint64_t len = std::min(mq, ent - off);
-            const uint64_t rp2[2] = {0, len};
-            HIP_TRY(hipMemcpyAsync(rp_dev, rp2, 16, hipMemcpyHostToDevice, s));
-            const uint64_t z0 = 0;
-            HIP_TRY(hipMemcpyAsync(qoff_dev, &z0, 8, hipMemcpyHostToDevice, s));
+            piece_rp[0] = 0;
+            piece_rp[1] = len;
+            piece_rp[2] = 0;
+            HIP_TRY(hipMemcpyAsync(rp_dev, piece_rp.data(), 16, hipMemcpyHostToDevice, s));
+            HIP_TRY(hipMemcpyAsync(qoff_dev, piece_rp.data() + 2, 8, hipMemcpyHostToDevice, s));
+            HIP_TRY(hipStreamSynchronize(s));
             HIP_TRY(hipMemcpyAsync(col_dev, G.col + ea + off, 4 * len,
                                    hipMemcpyHostToDevice, s));
             if (G.wt)

@@ -358,6 +358,7 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
     }
     for (uint32_t t = threadIdx.x; t < len; t += kBlock) {
       ctx.perm[s + t] = sval[t];
+      if (mat) ctx.keys[s + t] = skey[t];  // sorted keys stay with their payload
       if (t > 0 && skey[t] != skey[t - 1]) ctx.flags[s + t] = 1;
     }
     __syncthreads();
@@ -404,6 +405,7 @@ __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx) {
     const unsigned long long prev = __shfl_up(key, 1, kWave);
     if (lane < len) {
       ctx.perm[s + lane] = v;
+      if (mat) ctx.keys[s + lane] = key;  // sorted keys stay with their payload
       if (lane > 0 && key != prev) ctx.flags[s + lane] = 1;
     }
   }

@@ -81,17 +81,50 @@ def _gpu():
         lib = ctypes.CDLL(path)
         u64, u32, vp, i32 = ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_int
         lib.gen_rmat_gpu.argtypes = [i32, u32, u64, u32, u32, u32, u64, u64, u32, u32,
-                                     vp, vp, vp]
+                                     u32, u32, vp, vp, vp]
         lib.gen_rmat_gpu.restype = i32
-        lib.gen_chunglu_gpu.argtypes = [i32, u32, u64, vp, vp, u64, u64, u32, u32, vp,
-                                        vp, vp]
+        lib.gen_chunglu_gpu.argtypes = [i32, u32, u64, vp, vp, u64, u64, u32, u32, u32,
+                                        u32, vp, vp, vp]
         lib.gen_chunglu_gpu.restype = i32
+        lib.gen_host_alloc.argtypes = [u64]
+        lib.gen_host_alloc.restype = vp
+        lib.gen_host_free.argtypes = [vp]
+        lib.gen_host_free.restype = None
         _GPU = lib
     return _GPU
 
 
 def _ptr(a):
     return a.ctypes.data_as(ctypes.c_void_p)
+
+
+class _PinnedOwner:
+    def __init__(self, ptr):
+        self.ptr = ptr
+
+    def __del__(self):
+        if self.ptr and _GPU is not None:
+            _GPU.gen_host_free(self.ptr)
+            self.ptr = None
+
+
+def pinned_empty(count, dtype):
+    """A torch tensor of 'count' elements in pinned host memory of exactly
+    that size (torch's own pinned allocator rounds up to powers of two)."""
+    import torch
+    np_dtype = {torch.int32: np.int32, torch.int64: np.int64,
+                torch.uint8: np.uint8}[dtype]
+    nbytes = max(int(count), 1) * np.dtype(np_dtype).itemsize
+    ptr = _gpu().gen_host_alloc(nbytes)
+    if not ptr:
+        raise MemoryError(f"hipHostMalloc({nbytes}) failed")
+    buf = (ctypes.c_char * nbytes).from_address(ptr)
+    # the buffer object frees the allocation when the last view of it dies:
+    # numpy keeps the buffer alive, torch keeps the numpy array alive
+    buf._wl_owner = _PinnedOwner(ptr)
+    arr = np.frombuffer(buf, dtype=np_dtype, count=max(int(count), 1))
+    t = torch.from_numpy(arr)
+    return t if count else t[:0]
 
 
 def csr_from_keys(keys, n, name=""):
@@ -174,9 +207,9 @@ def chung_lu(n=4_000_000, samples=64_000_000, gamma=2.1, seed=0, device="cpu"):
     dal = torch.from_numpy(alias.view(np.int32)).to(device)
     nbits = max(1, int(np.ceil(np.log2(n))))
 
-    def emit(phase, shift, nbk, arr, keys, stream):
+    def emit(phase, shift, nbk, blo, bhi, arr, keys, stream):
         return _gpu().gen_chunglu_gpu(phase, n, seed, dthr.data_ptr(), dal.data_ptr(),
-                                      0, samples, shift, nbk, arr, keys, stream)
+                                      0, samples, shift, nbk, blo, bhi, arr, keys, stream)
     return _gpu_build(n, nbits, 2 * samples, emit, name, device)
 
 
@@ -187,9 +220,12 @@ def rmat_thresholds(abcd):
 
 
 def rmat(scale=27, edge_factor=16, abcd=(0.57, 0.19, 0.19, 0.05), seed=0,
-         device="cpu"):
+         device="cpu", host_out=False):
     """R-MAT, edge_factor * 2^scale samples, seeded vertex bijection, self-loops
-    dropped, symmetrised, deduplicated."""
+    dropped, symmetrised, deduplicated.  device='cuda' generates on the GPU;
+    with host_out=True the CSR is returned in pinned host memory and the
+    device never holds more than a group of buckets (for graphs larger than
+    HBM)."""
     n = 1 << scale
     samples = edge_factor * n
     ta, tab, tabc = rmat_thresholds(abcd)
@@ -199,50 +235,76 @@ def rmat(scale=27, edge_factor=16, abcd=(0.57, 0.19, 0.19, 0.05), seed=0,
         _cpu().gen_rmat_keys_cpu(scale, 0, samples, seed, ta, tab, tabc, _ptr(keys))
         return csr_from_keys(keys, n, name)
 
-    def emit(phase, shift, nbk, arr, keys, stream):
+    def emit(phase, shift, nbk, blo, bhi, arr, keys, stream):
         return _gpu().gen_rmat_gpu(phase, scale, seed, ta, tab, tabc, 0, samples, shift,
-                                   nbk, arr, keys, stream)
-    return _gpu_build(n, scale, 2 * samples, emit, name, device)
+                                   nbk, blo, bhi, arr, keys, stream)
+    return _gpu_build(n, scale, 2 * samples, emit, name, device, host_out)
 
 
-def _gpu_build(n, nbits, max_keys, emit, name, device):
-    """Bucketed generation on the GPU: count, scatter, then per bucket sort +
-    unique + row counts (torch ops).  Returns a CSR of torch tensors on
-    'device' with row_ptr int64 (uint64 values) and col int32 (uint32 values)."""
+def _gpu_build(n, nbits, max_keys, emit, name, device, host_out=False,
+               group_keys=1 << 31):
+    """Bucketed generation on the GPU: count, then per group of buckets
+    scatter + per bucket sort + unique + row counts (torch ops).  Returns a
+    CSR with row_ptr int64 (uint64 values) and col int32 (uint32 values), on
+    'device' or, with host_out, in pinned host memory."""
     import torch
     bbits = _bucket_plan(nbits, max_keys)
     nbk = 1 << bbits
     shift = nbits - bbits
     stream = torch.cuda.current_stream(device).cuda_stream
     counts = torch.zeros(nbk, dtype=torch.int64, device=device)
-    if emit(0, shift, nbk, counts.data_ptr(), 0, stream) != 0:
+    if emit(0, shift, nbk, 0, nbk, counts.data_ptr(), 0, stream) != 0:
         raise RuntimeError("graph generator count pass failed")
-    offs = torch.zeros(nbk + 1, dtype=torch.int64, device=device)
-    offs[1:] = torch.cumsum(counts, 0)
-    total = int(offs[-1].item())
-    keys = torch.empty(max(total, 1), dtype=torch.int64, device=device)
-    cursor = offs[:-1].clone()
-    if emit(1, shift, nbk, cursor.data_ptr(), keys.data_ptr(), stream) != 0:
-        raise RuntimeError("graph generator scatter pass failed")
-    offs_h = offs.cpu().tolist()
+    cnt_h = counts.cpu().tolist()
+    total = sum(cnt_h)
+    if not host_out:
+        group_keys = max(total, 1)
     rows_per = 1 << shift
     row_cnt = torch.zeros(n, dtype=torch.int64, device=device)
+    if host_out:
+        col_out = pinned_empty(total, torch.int32)
     cols = []
-    for b in range(nbk):
-        seg = keys[offs_h[b]:offs_h[b + 1]]
-        if seg.numel() == 0:
-            continue
-        seg = torch.sort(seg).values
-        seg = torch.unique_consecutive(seg)
-        u = seg >> 32
-        lo = b * rows_per
-        hi = min(n, lo + rows_per)
-        row_cnt[lo:hi] = torch.bincount(u - lo, minlength=hi - lo)
-        cols.append((seg & 0xFFFFFFFF).to(torch.int32))
-        del seg, u
-    del keys
-    col = torch.cat(cols) if cols else torch.empty(0, dtype=torch.int32, device=device)
-    del cols
+    pos = 0
+    b0 = 0
+    while b0 < nbk:
+        b1, gk = b0, 0
+        while b1 < nbk and (b1 == b0 or gk + cnt_h[b1] <= group_keys):
+            gk += cnt_h[b1]
+            b1 += 1
+        keys = torch.empty(max(gk, 1), dtype=torch.int64, device=device)
+        cur = [0] * nbk
+        acc = 0
+        for b in range(b0, b1):
+            cur[b] = acc
+            acc += cnt_h[b]
+        cursor = torch.tensor(cur, dtype=torch.int64, device=device)
+        if emit(1, shift, nbk, b0, b1, cursor.data_ptr(), keys.data_ptr(), stream) != 0:
+            raise RuntimeError("graph generator scatter pass failed")
+        for b in range(b0, b1):
+            seg = keys[cur[b]:cur[b] + cnt_h[b]]
+            if seg.numel() == 0:
+                continue
+            seg = torch.sort(seg).values
+            seg = torch.unique_consecutive(seg)
+            u = seg >> 32
+            lo = b * rows_per
+            hi = min(n, lo + rows_per)
+            row_cnt[lo:hi] = torch.bincount(u - lo, minlength=hi - lo)
+            c = (seg & 0xFFFFFFFF).to(torch.int32)
+            if host_out:
+                col_out[pos:pos + c.numel()].copy_(c)
+            else:
+                cols.append(c)
+            pos += c.numel()
+            del seg, u, c
+        del keys
+        b0 = b1
     rp = torch.zeros(n + 1, dtype=torch.int64, device=device)
     rp[1:] = torch.cumsum(row_cnt, 0)
+    if host_out:
+        rp_h = pinned_empty(n + 1, torch.int64)
+        rp_h.copy_(rp)
+        return CSR(n, rp_h, col_out[:pos], None, name)
+    col = torch.cat(cols) if cols else torch.empty(0, dtype=torch.int32, device=device)
+    del cols
     return CSR(n, rp, col, None, name)

@@ -61,6 +61,7 @@ constexpr int kPer = 8;
 
 __global__ void __launch_bounds__(kB) k_scatter(Src S, uint64_t s0, uint64_t cnt,
                                                 uint32_t shift, uint32_t nbk,
+                                                uint32_t blo, uint32_t bhi,
                                                 unsigned long long* cursor,
                                                 uint64_t* keys) {
   __shared__ uint32_t lcnt[kMaxBuckets];
@@ -77,12 +78,12 @@ __global__ void __launch_bounds__(kB) k_scatter(Src S, uint64_t s0, uint64_t cnt
       const uint64_t q = base + (uint64_t)i * kB + threadIdx.x;
       uint64_t u = 0, v = 0;
       bool ok = q < cnt && draw(S, s0 + q, &u, &v);
-      key[2 * i] = ok ? ((u << 32) | v) : ~0ull;
-      key[2 * i + 1] = ok ? ((v << 32) | u) : ~0ull;
-      if (ok) {
-        slot[2 * i] = atomicAdd(&lcnt[u >> shift], 1u);
-        slot[2 * i + 1] = atomicAdd(&lcnt[v >> shift], 1u);
-      }
+      const bool oku = ok && (u >> shift) >= blo && (u >> shift) < bhi;
+      const bool okv = ok && (v >> shift) >= blo && (v >> shift) < bhi;
+      key[2 * i] = oku ? ((u << 32) | v) : ~0ull;
+      key[2 * i + 1] = okv ? ((v << 32) | u) : ~0ull;
+      if (oku) slot[2 * i] = atomicAdd(&lcnt[u >> shift], 1u);
+      if (okv) slot[2 * i + 1] = atomicAdd(&lcnt[v >> shift], 1u);
     }
     __syncthreads();
     for (uint32_t b = threadIdx.x; b < nbk; b += kB)
@@ -124,7 +125,8 @@ Src make_chunglu(uint32_t n, uint64_t seed, const uint64_t* thr,
 }
 
 int launch(const Src& S, int phase, uint64_t s0, uint64_t cnt, uint32_t shift,
-           uint32_t nbk, unsigned long long* arr, uint64_t* keys, void* stream) {
+           uint32_t nbk, uint32_t blo, uint32_t bhi, unsigned long long* arr,
+           uint64_t* keys, void* stream) {
   if (nbk == 0 || nbk > kMaxBuckets) return -1;
   uint64_t blocks = (cnt + kB - 1) / kB;
   if (blocks > 16384) blocks = 16384;
@@ -135,7 +137,7 @@ int launch(const Src& S, int phase, uint64_t s0, uint64_t cnt, uint32_t shift,
                        shift, nbk, arr);
   else
     hipLaunchKernelGGL(k_scatter, dim3((uint32_t)blocks), dim3(kB), 0, st, S, s0,
-                       cnt, shift, nbk, arr, keys);
+                       cnt, shift, nbk, blo, bhi, arr, keys);
   return hipGetLastError() == hipSuccess ? 0 : -2;
 }
 
@@ -144,21 +146,33 @@ int launch(const Src& S, int phase, uint64_t s0, uint64_t cnt, uint32_t shift,
 extern "C" {
 
 // phase 0: counts[b] += number of keys with source bucket b (u >> shift);
-// phase 1: keys[cursor[b]++] = key for every key of bucket b.
+// phase 1: keys[cursor[b]++] = key for every key of a bucket b in
+// [blo, bhi) (keys of other buckets are skipped).
 int gen_rmat_gpu(int phase, uint32_t scale, uint64_t seed, uint32_t ta,
                  uint32_t tab, uint32_t tabc, uint64_t s0, uint64_t cnt,
-                 uint32_t shift, uint32_t nbk, unsigned long long* arr,
-                 uint64_t* keys, void* stream) {
+                 uint32_t shift, uint32_t nbk, uint32_t blo, uint32_t bhi,
+                 unsigned long long* arr, uint64_t* keys, void* stream) {
   return launch(make_rmat(scale, seed, ta, tab, tabc), phase, s0, cnt, shift, nbk,
-                arr, keys, stream);
+                blo, bhi, arr, keys, stream);
 }
 
 int gen_chunglu_gpu(int phase, uint32_t n, uint64_t seed, const uint64_t* thr,
                     const uint32_t* alias, uint64_t s0, uint64_t cnt,
-                    uint32_t shift, uint32_t nbk, unsigned long long* arr,
-                    uint64_t* keys, void* stream) {
-  return launch(make_chunglu(n, seed, thr, alias), phase, s0, cnt, shift, nbk, arr,
-                keys, stream);
+                    uint32_t shift, uint32_t nbk, uint32_t blo, uint32_t bhi,
+                    unsigned long long* arr, uint64_t* keys, void* stream) {
+  return launch(make_chunglu(n, seed, thr, alias), phase, s0, cnt, shift, nbk, blo,
+                bhi, arr, keys, stream);
+}
+
+// Pinned host memory of exactly 'bytes' (the caller frees it).
+void* gen_host_alloc(uint64_t bytes) {
+  void* p = nullptr;
+  if (hipHostMalloc(&p, bytes ? bytes : 8, hipHostMallocDefault) != hipSuccess) return nullptr;
+  return p;
+}
+
+void gen_host_free(void* p) {
+  if (p) (void)hipHostFree(p);
 }
 
 }  // extern "C"

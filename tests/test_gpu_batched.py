@@ -117,3 +117,27 @@ def test_budget_errors():
     # cap 0 = the largest that fits: still a valid, stable result
     c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, None, 0, 0, ws=ws)
     assert oracle.is_stable(g0.row_ptr, g0.col, None, c.numpy().view(np.uint32))
+
+
+def test_medium_rmat_explicit_cap():
+    g = inputs.rmat(18, 16, seed=3)
+    print("rmat18 explicit cap", flush=True)
+    got, k, r, outer, coarsest = _check(g.row_ptr, g.col, mb=g.nnz // 6)
+
+
+def test_medium_rmat_tight_budget_auto_cap():
+    # R-MAT scale 18 in pinned host memory with a workspace far smaller than
+    # one in-core run needs: several batches, cap chosen by the library.
+    g0 = inputs.rmat(18, 16, seed=3)
+    g = _host_graph(g0.row_ptr, g0.col)
+    ws = wl.workspace(wl.wl_batched_workspace_size(g, g.nnz // 6))
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, None, 0, 0, ws=ws)
+    got = c.numpy().view(np.uint32)
+    print(f"rmat18 auto cap: k={k} rounds={r} outer={outer} coarsest={coarsest}", flush=True)
+    assert oracle.is_stable(g0.row_ptr, g0.col, None, got)
+    ref = oracle.first_occurrence(oracle.stable_coloring(g0.row_ptr, g0.col)[0])[0]
+    S = ref
+    for blk in np.unique(got)[:2000]:
+        assert len(np.unique(S[got == blk])) == 1  # finer than or equal to coarsest
+    if coarsest:
+        assert np.array_equal(got, ref)
