@@ -59,6 +59,7 @@ extern "C" {
 #define WL_EMAXROUNDS (-4)  /* round cap reached before stability          */
 #define WL_ENOTSTABLE (-5)  /* wl_verify_stable: colouring is not stable   */
 #define WL_EHIP (-6)        /* a HIP runtime call failed                   */
+#define WL_ENOMEM (-7)      /* a host allocation of the library failed     */
 
 /* CSR adjacency.  Exactly one of row_ptr32 / row_ptr64 is non-NULL; it has
  * n+1 entries, row_ptr[0] == 0 and row_ptr[n] == nnz.  col_idx has nnz
@@ -123,10 +124,13 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
  * memory; only one batch of entries is on the device at a time.  Each batch
  * runs Algorithm 1 with the nodes outside it frozen as singletons; the
  * quotient graphs between outer iterations are built on the device, chunk by
- * chunk, and kept in pinned host memory that this call allocates and frees
- * (at most the size of the input's edge arrays).  Needs n < 2^30.
- *   g_host      host CSR (pinned memory recommended: batches are copied
- *               host-to-device asynchronously).
+ * chunk, and kept in pageable host memory that this call allocates and frees
+ * (at most 8 bytes per entry of the input, plus 8 bytes per node, for each
+ * of the two quotients alive at a time).  Needs n < 2^30.
+ *   g_host      host CSR, pageable or page-locked.  Page-locked arrays are
+ *               copied to the device by DMA directly; pageable ones (and the
+ *               library's quotients) through two page-locked staging buffers
+ *               of 64 MiB that the call allocates.
  *   init_host   host labels or NULL (trivial partition).
  *   max_batch_entries  cap M_b on entries per batch; 0 = the largest cap the
  *               workspace allows.  Batches are contiguous CSR entry ranges
@@ -139,7 +143,8 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
  *   iterations), coarsest_out (1 when the last outer iteration had a single
  *   batch, which makes the result the coarsest stable colouring; 0 when the
  *   contraction stopped at a fixed point with several batches).
- * Errors: WL_EINVAL, WL_EBUDGET, WL_EOVERFLOW, WL_EMAXROUNDS, WL_EHIP. */
+ * Errors: WL_EINVAL, WL_EBUDGET, WL_EOVERFLOW, WL_EMAXROUNDS, WL_ENOMEM,
+ * WL_EHIP. */
 int wl_stable_coloring_batched(const wl_csr *g_host, const uint32_t *init_host,
                                uint64_t seed, uint64_t max_batch_entries,
                                uint32_t *color_out_host, uint32_t *k_out,

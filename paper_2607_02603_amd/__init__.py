@@ -24,8 +24,9 @@ WL_EOVERFLOW = -3
 WL_EMAXROUNDS = -4
 WL_ENOTSTABLE = -5
 WL_EHIP = -6
+WL_ENOMEM = -7
 _NAMES = {-1: "WL_EINVAL", -2: "WL_EBUDGET", -3: "WL_EOVERFLOW",
-          -4: "WL_EMAXROUNDS", -5: "WL_ENOTSTABLE", -6: "WL_EHIP"}
+          -4: "WL_EMAXROUNDS", -5: "WL_ENOTSTABLE", -6: "WL_EHIP", -7: "WL_ENOMEM"}
 
 EXPORTED = ["wl_workspace_size", "wl_batched_workspace_size", "wl_refine_round",
             "wl_stable_coloring", "wl_stable_coloring_batched", "wl_verify_stable",

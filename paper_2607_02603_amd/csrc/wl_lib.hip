@@ -7,7 +7,12 @@
 // never allocates: every buffer is carved from the caller's workspace.
 #include <hip/hip_runtime.h>
 
+#include <sched.h>
+
 #include <algorithm>
+#include <memory>
+#include <new>
+#include <thread>
 #include <utility>
 #include <vector>
 #include <cstdarg>
@@ -571,7 +576,7 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
 // ---------------------------------------------------------------------------
 
 // The current graph G_t in host memory (the caller's arrays for t = 0, the
-// library's pinned quotient arrays afterwards).
+// library's quotient arrays afterwards).
 struct HostGraph {
   uint64_t n = 0, m = 0;
   const uint32_t* rp32 = nullptr;
@@ -686,27 +691,159 @@ uint64_t max_inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts)
   return mx;
 }
 
-struct PinnedBuf {
-  void* p = nullptr;
-  ~PinnedBuf() { if (p) (void)hipHostFree(p); }
+// Host array owned by the library (pageable: the quotient graphs of the outer
+// iterations can be far larger than the page-locked memory a process may hold).
+struct HostBuf {
+  std::unique_ptr<uint8_t[]> p;
   int alloc(uint64_t bytes) {
-    if (p) { (void)hipHostFree(p); p = nullptr; }
-    if (bytes == 0) bytes = 8;
-    hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocDefault);
-    if (e != hipSuccess) return fail(WL_EHIP, "hipHostMalloc(%llu) failed: %s",
-                                     (unsigned long long)bytes, hipGetErrorString(e));
+    p.reset(new (std::nothrow) uint8_t[bytes ? bytes : 8]);
+    if (!p) return fail(WL_ENOMEM, "host allocation of %llu bytes failed",
+                        (unsigned long long)bytes);
     return WL_OK;
   }
+  template <typename T> T* as() const { return (T*)p.get(); }
 };
 
-int copy_rows_h2d(const HostGraph& G, uint64_t r0, uint64_t nrows, uint8_t* stage,
-                  uint64_t* rp_dev, hipStream_t s) {
+bool page_locked(const void* ptr) {
+  hipPointerAttribute_t a;
+  if (hipPointerGetAttributes(&a, ptr) != hipSuccess) {
+    (void)hipGetLastError();  // a pageable pointer is not an error here
+    return false;
+  }
+  return a.type == hipMemoryTypeHost;
+}
+
+// Copies between host memory and the device on one stream.  Page-locked host
+// memory is handed to the DMA engine directly.  Pageable memory goes through
+// two page-locked staging buffers: host threads fill (or drain) one while the
+// DMA engine moves the other.
+class HostCopy {
+ public:
+  static constexpr uint64_t kStage = 64ull << 20;
+  explicit HostCopy(hipStream_t s) : s_(s) {
+    cpu_set_t set;
+    CPU_ZERO(&set);
+    unsigned t = 4;
+    if (sched_getaffinity(0, sizeof(set), &set) == 0) t = (unsigned)CPU_COUNT(&set);
+    threads_ = std::max(1u, std::min(t, 8u));
+  }
+  ~HostCopy() {
+    for (int i = 0; i < 2; ++i) {
+      if (ev_[i]) {
+        (void)hipEventSynchronize(ev_[i]);
+        (void)hipEventDestroy(ev_[i]);
+      }
+      if (buf_[i]) (void)hipHostFree(buf_[i]);
+    }
+  }
+  HostCopy(const HostCopy&) = delete;
+  HostCopy& operator=(const HostCopy&) = delete;
+
+  // Enqueues the copy; the source may be reused once the call returns.
+  int h2d(void* dst, const void* src, uint64_t bytes) {
+    if (bytes == 0) return WL_OK;
+    if (page_locked(src)) {
+      HIP_TRY(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s_));
+      return WL_OK;
+    }
+    if (int r = ensure()) return r;
+    for (uint64_t off = 0; off < bytes; off += kStage) {
+      const uint64_t len = std::min(kStage, bytes - off);
+      HIP_TRY(hipEventSynchronize(ev_[cur_]));
+      par_copy(buf_[cur_], (const uint8_t*)src + off, len);
+      HIP_TRY(hipMemcpyAsync((uint8_t*)dst + off, buf_[cur_], len, hipMemcpyHostToDevice, s_));
+      HIP_TRY(hipEventRecord(ev_[cur_], s_));
+      cur_ ^= 1;
+    }
+    return WL_OK;
+  }
+
+  // Returns once the data is in dst (the stream's earlier work included).
+  int d2h(void* dst, const void* src, uint64_t bytes) {
+    if (bytes == 0) return WL_OK;
+    if (page_locked(dst)) {
+      HIP_TRY(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s_));
+      HIP_TRY(hipStreamSynchronize(s_));
+      return WL_OK;
+    }
+    if (int r = ensure()) return r;
+    int prev = -1;
+    uint64_t prev_off = 0, prev_len = 0;
+    for (uint64_t off = 0; off < bytes; off += kStage) {
+      const uint64_t len = std::min(kStage, bytes - off);
+      const int b = cur_;
+      HIP_TRY(hipEventSynchronize(ev_[b]));
+      HIP_TRY(hipMemcpyAsync(buf_[b], (const uint8_t*)src + off, len, hipMemcpyDeviceToHost,
+                             s_));
+      HIP_TRY(hipEventRecord(ev_[b], s_));
+      if (prev >= 0) {
+        HIP_TRY(hipEventSynchronize(ev_[prev]));
+        par_copy((uint8_t*)dst + prev_off, buf_[prev], prev_len);
+      }
+      prev = b;
+      prev_off = off;
+      prev_len = len;
+      cur_ ^= 1;
+    }
+    HIP_TRY(hipEventSynchronize(ev_[prev]));
+    par_copy((uint8_t*)dst + prev_off, buf_[prev], prev_len);
+    return WL_OK;
+  }
+
+ private:
+  int ensure() {
+    for (int i = 0; i < 2; ++i) {
+      if (buf_[i]) continue;
+      hipError_t e = hipHostMalloc((void**)&buf_[i], kStage, hipHostMallocDefault);
+      if (e != hipSuccess) {
+        buf_[i] = nullptr;
+        (void)hipGetLastError();
+        return fail(WL_ENOMEM, "page-locked staging buffer of %llu bytes: %s",
+                    (unsigned long long)kStage, hipGetErrorString(e));
+      }
+      HIP_TRY(hipEventCreateWithFlags(&ev_[i], hipEventDisableTiming));
+      HIP_TRY(hipEventRecord(ev_[i], s_));
+    }
+    return WL_OK;
+  }
+  void par_copy(void* d, const void* src, uint64_t len) {
+    const unsigned t = len >= (4ull << 20) ? threads_ : 1;
+    if (t <= 1) {
+      memcpy(d, src, len);
+      return;
+    }
+    const uint64_t per = (len + t - 1) / t;
+    std::vector<std::thread> th;
+    try {
+      for (unsigned i = 1; i < t && i * per < len; ++i)
+        th.emplace_back([=] {
+          memcpy((uint8_t*)d + i * per, (const uint8_t*)src + i * per,
+                 std::min(per, len - i * per));
+        });
+    } catch (...) {
+      for (auto& x : th) x.join();
+      memcpy(d, src, len);
+      return;
+    }
+    memcpy(d, src, std::min(per, len));
+    for (auto& x : th) x.join();
+  }
+
+  hipStream_t s_;
+  uint8_t* buf_[2] = {nullptr, nullptr};
+  hipEvent_t ev_[2] = {nullptr, nullptr};
+  int cur_ = 0;
+  unsigned threads_ = 1;
+};
+
+int copy_rows_h2d(HostCopy& hc, const HostGraph& G, uint64_t r0, uint64_t nrows,
+                  uint8_t* stage, uint64_t* rp_dev, hipStream_t s) {
   if (G.rp64) {
-    HIP_TRY(hipMemcpyAsync(stage, G.rp64 + r0, 8 * (nrows + 1), hipMemcpyHostToDevice, s));
+    if (int r = hc.h2d(stage, G.rp64 + r0, 8 * (nrows + 1))) return r;
     hipLaunchKernelGGL(k_rebase_rows<uint64_t>, dim3(grid_for(nrows + 1)), dim3(kBlock), 0,
                        s, (const uint64_t*)stage, rp_dev, (uint32_t)nrows);
   } else {
-    HIP_TRY(hipMemcpyAsync(stage, G.rp32 + r0, 4 * (nrows + 1), hipMemcpyHostToDevice, s));
+    if (int r = hc.h2d(stage, G.rp32 + r0, 4 * (nrows + 1))) return r;
     hipLaunchKernelGGL(k_rebase_rows<uint32_t>, dim3(grid_for(nrows + 1)), dim3(kBlock), 0,
                        s, (const uint32_t*)stage, rp_dev, (uint32_t)nrows);
   }
@@ -716,46 +853,67 @@ int copy_rows_h2d(const HostGraph& G, uint64_t r0, uint64_t nrows, uint8_t* stag
 
 struct QuotientOut {
   std::vector<uint64_t> deg;      // entries per block
-  uint32_t* col = nullptr;        // pinned, capacity cap
+  uint32_t* col = nullptr;        // library host arrays of capacity 'cap'
   uint32_t* wt = nullptr;
   uint64_t m = 0, cap = 0;
 };
 
-// Sorts and reduces the keys of one chunk on the device; appends the
-// distinct (block, target, weight) triples in order (or into 'spill' for a
-// row processed in pieces).
-int quotient_chunk(Session& S, uint64_t nkeys, uint32_t bfirst, QuotientOut& Q,
+// Device buffers of one quotient chunk: the chunk's rows (rebased row
+// pointers, key offsets, columns, weights); after the keys are built the
+// column and weight arrays receive the distinct entries and the offsets the
+// per-block entry counts.
+struct QuotDev {
+  uint64_t* rp;
+  uint64_t* qoff;
+  uint32_t* col;
+  uint32_t* wt;
+  uint32_t* deg() const { return (uint32_t*)qoff; }
+};
+
+// Sorts and reduces the 'nkeys' keys of one chunk on the device.  Whole rows:
+// the distinct (target, weight) entries are appended to Q in key order and
+// the entry counts of the chunk's 'nreps' blocks (ids bfirst ...) added to
+// Q.deg; they may not reach past 'write_end' (the end of the chunk's rows
+// when Q overwrites the graph it is built from).  A row processed in pieces:
+// the entries go to 'spill' with 64-bit weights, merged by the caller.
+int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
+                   uint64_t nreps, uint32_t bfirst, uint64_t write_end, QuotientOut& Q,
                    std::vector<std::pair<uint32_t, uint64_t>>* spill,
-                   std::vector<uint64_t>& hkey, std::vector<uint64_t>& hw) {
-  hipLaunchKernelGGL(k_q_begin, dim3(grid_for(nkeys, kBlock, 4096)), dim3(kBlock), 0, S.s,
-                     S.ctx, (uint32_t)nkeys);
+                   std::vector<uint64_t>& hkey, std::vector<uint64_t>& hw,
+                   std::vector<uint32_t>& hdeg) {
+  hipLaunchKernelGGL(k_q_begin, dim3(grid_for(std::max(nkeys, nreps), kBlock, 4096)),
+                     dim3(kBlock), 0, S.s, S.ctx, (uint32_t)nkeys, D.deg(), (uint32_t)nreps);
   HIP_LAUNCH_CHECK();
   if (int r = S.segmented_sort()) return r;
   hipLaunchKernelGGL(k_q_reduce, dim3(grid_for(nkeys, kBlock, 4096)), dim3(kBlock), 0, S.s,
                      S.ctx, (uint32_t)nkeys);
   HIP_LAUNCH_CHECK();
-  if (int r = S.pull()) return r;
-  const uint32_t nd = S.host.k_new;
-  hkey.resize(nd);
-  hw.resize(nd);
-  HIP_TRY(hipMemcpyAsync(hkey.data(), S.ctx.z, 8ull * nd, hipMemcpyDeviceToHost, S.s));
-  HIP_TRY(hipMemcpyAsync(hw.data(), S.ctx.x, 8ull * nd, hipMemcpyDeviceToHost, S.s));
-  HIP_TRY(hipStreamSynchronize(S.s));
-  const uint64_t mask = (1ull << kQShift) - 1;
-  for (uint32_t d = 0; d < nd; ++d) {
-    const uint64_t brel = hkey[d] >> kQShift, tgt = hkey[d] & mask;
-    if (spill) {
-      spill->push_back({(uint32_t)tgt, hw[d]});
-      continue;
-    }
-    if (hw[d] > 0xFFFFFFFFull)
-      return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
-    if (Q.m >= Q.cap) return fail(WL_EINVAL, "quotient larger than expected");
-    Q.deg[bfirst + brel] += 1;
-    Q.col[Q.m] = (uint32_t)tgt;
-    Q.wt[Q.m] = (uint32_t)hw[d];
-    Q.m++;
+  if (spill) {
+    if (int r = S.pull()) return r;
+    const uint32_t nd = S.host.k_new;
+    hkey.resize(nd);
+    hw.resize(nd);
+    if (int r = hc.d2h(hkey.data(), S.ctx.z, 8ull * nd)) return r;
+    if (int r = hc.d2h(hw.data(), S.ctx.x, 8ull * nd)) return r;
+    const uint64_t mask = (1ull << kQShift) - 1;
+    for (uint32_t d = 0; d < nd; ++d) spill->push_back({(uint32_t)(hkey[d] & mask), hw[d]});
+    return WL_OK;
   }
+  hipLaunchKernelGGL(k_q_emit, dim3(grid_for(nkeys, kBlock, 4096)), dim3(kBlock), 0, S.s,
+                     S.ctx, (uint32_t)nkeys, D.col, D.wt, D.deg());
+  HIP_LAUNCH_CHECK();
+  if (int r = S.pull()) return r;
+  if (S.host.err & kErrQuotientWeight)
+    return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
+  const uint32_t nd = S.host.k_new;
+  if (Q.m + nd > std::min(Q.cap, write_end))
+    return fail(WL_EINVAL, "quotient larger than expected");
+  if (int r = hc.d2h(Q.col + Q.m, D.col, 4ull * nd)) return r;
+  if (int r = hc.d2h(Q.wt + Q.m, D.wt, 4ull * nd)) return r;
+  hdeg.resize(nreps);
+  if (int r = hc.d2h(hdeg.data(), D.deg(), 4ull * nreps)) return r;
+  for (uint64_t b = 0; b < nreps; ++b) Q.deg[bfirst + b] += hdeg[b];
+  Q.m += nd;
   return WL_OK;
 }
 
@@ -779,13 +937,15 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   if (init_host) labels.assign(init_host, init_host + n0);
   std::vector<uint32_t> map0(n0);
   for (uint64_t i = 0; i < n0; ++i) map0[i] = (uint32_t)i;
-  PinnedBuf qrp_buf, qcol_buf, qwt_buf;  // current quotient (G_t, t >= 1)
-  PinnedBuf nrp_buf, ncol_buf, nwt_buf;  // quotient under construction
+  HostBuf qrp_buf, qcol_buf, qwt_buf;  // current quotient (G_t, t >= 1)
+  HostBuf nrp_buf, ncol_buf, nwt_buf;  // G_1 under construction, new row pointers
+  HostCopy hc(s);
   uint64_t rounds = 0;
   uint32_t outer = 0;
   std::vector<uint32_t> key, loc, blk, mapk;
   std::vector<uint8_t> isrep;
   std::vector<uint64_t> hkey, hw;
+  std::vector<uint32_t> hdeg;
   std::vector<uint64_t> piece_rp(3);
 
   for (uint64_t t = 0;; ++t) {
@@ -847,15 +1007,12 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       uint32_t* wt_dev = G.wt ? (uint32_t*)(W + RL.wt) : nullptr;
       uint32_t* lab_dev = labels.empty() ? nullptr : (uint32_t*)(W + RL.lab);
       uint32_t* colors_dev = (uint32_t*)(W + RL.colors);
-      if (int r = copy_rows_h2d(G, r_lo, nl, W + RL.stage, rp_dev, s)) return r;
-      if (ml) {
-        HIP_TRY(hipMemcpyAsync(col_dev, G.col + e0, 4 * ml, hipMemcpyHostToDevice, s));
-        if (wt_dev)
-          HIP_TRY(hipMemcpyAsync(wt_dev, G.wt + e0, 4 * ml, hipMemcpyHostToDevice, s));
-      }
+      if (int r = copy_rows_h2d(hc, G, r_lo, nl, W + RL.stage, rp_dev, s)) return r;
+      if (int r = hc.h2d(col_dev, G.col + e0, 4 * ml)) return r;
+      if (wt_dev)
+        if (int r = hc.h2d(wt_dev, G.wt + e0, 4 * ml)) return r;
       if (lab_dev)
-        HIP_TRY(hipMemcpyAsync(lab_dev, labels.data() + r_lo, 4 * nl,
-                               hipMemcpyHostToDevice, s));
+        if (int r = hc.h2d(lab_dev, labels.data() + r_lo, 4 * nl)) return r;
       wl_csr lg{};
       lg.n = nl;
       lg.nnz = ml;
@@ -882,8 +1039,7 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
                 (unsigned long long)b, (unsigned long long)r_lo, (unsigned long long)r_hi,
                 (unsigned long long)ml, S.host.k, S.host.round);
       loc.resize(nl);
-      HIP_TRY(hipMemcpyAsync(loc.data(), colors_dev, 4 * nl, hipMemcpyDeviceToHost, s));
-      HIP_TRY(hipStreamSynchronize(s));
+      if (int r = hc.d2h(loc.data(), colors_dev, 4 * nl)) return r;
       for (uint64_t i = 0; i < nl; ++i) key[r_lo + i] = (uint32_t)(base + loc[i]);
       base += S.host.k;
     }
@@ -921,20 +1077,33 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       if (isrep[i]) qcap += G.rp(i + 1) - G.rp(i);
     QuotientOut Q;
     Q.deg.assign(nq, 0);
-    if (int r = ncol_buf.alloc(4 * qcap)) return r;
-    if (int r = nwt_buf.alloc(4 * qcap)) return r;
-    Q.col = (uint32_t*)ncol_buf.p;
-    Q.wt = (uint32_t*)nwt_buf.p;
-    Q.cap = qcap;
+    const bool in_place = t > 0;
+    if (in_place) {
+      // G_t is the library's own: G_{t+1} overwrites it.  Block ids follow
+      // their representatives' node order and a block's row is never longer
+      // than its representative's, so every entry is written at or before
+      // the start of the row it comes from, which has been copied by then.
+      Q.col = qcol_buf.as<uint32_t>();
+      Q.wt = qwt_buf.as<uint32_t>();
+      Q.cap = G.m;
+    } else {
+      if (int r = ncol_buf.alloc(4 * qcap)) return r;
+      if (int r = nwt_buf.alloc(4 * qcap)) return r;
+      Q.col = ncol_buf.as<uint32_t>();
+      Q.wt = nwt_buf.as<uint32_t>();
+      Q.cap = qcap;
+    }
     const QuotLayout QL = quot_layout(n, mq);
     uint32_t* blk_dev = (uint32_t*)(W + QL.blk);
     uint8_t* isrep_dev = W + QL.isrep;
-    uint64_t* rp_dev = (uint64_t*)(W + QL.rp);
-    uint64_t* qoff_dev = (uint64_t*)(W + QL.qoff);
-    uint32_t* col_dev = (uint32_t*)(W + QL.col);
-    uint32_t* wt_dev = (uint32_t*)(W + QL.wt);
-    HIP_TRY(hipMemcpyAsync(blk_dev, blk.data(), 4 * n, hipMemcpyHostToDevice, s));
-    HIP_TRY(hipMemcpyAsync(isrep_dev, isrep.data(), n, hipMemcpyHostToDevice, s));
+    const QuotDev D{(uint64_t*)(W + QL.rp), (uint64_t*)(W + QL.qoff), (uint32_t*)(W + QL.col),
+                    (uint32_t*)(W + QL.wt)};
+    uint64_t* rp_dev = D.rp;
+    uint64_t* qoff_dev = D.qoff;
+    uint32_t* col_dev = D.col;
+    uint32_t* wt_dev = D.wt;
+    if (int r = hc.h2d(blk_dev, blk.data(), 4 * n)) return r;
+    if (int r = hc.h2d(isrep_dev, isrep.data(), n)) return r;
     std::vector<uint64_t> qoff;
     uint64_t a = 0;
     while (a < n) {
@@ -959,14 +1128,12 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
             piece_rp[0] = 0;
             piece_rp[1] = len;
             piece_rp[2] = 0;
-            HIP_TRY(hipMemcpyAsync(rp_dev, piece_rp.data(), 16, hipMemcpyHostToDevice, s));
-            HIP_TRY(hipMemcpyAsync(qoff_dev, piece_rp.data() + 2, 8, hipMemcpyHostToDevice, s));
+            if (int r = hc.h2d(rp_dev, piece_rp.data(), 16)) return r;
+            if (int r = hc.h2d(qoff_dev, piece_rp.data() + 2, 8)) return r;
             HIP_TRY(hipStreamSynchronize(s));
-            HIP_TRY(hipMemcpyAsync(col_dev, G.col + ea + off, 4 * len,
-                                   hipMemcpyHostToDevice, s));
+            if (int r = hc.h2d(col_dev, G.col + ea + off, 4 * len)) return r;
             if (G.wt)
-              HIP_TRY(hipMemcpyAsync(wt_dev, G.wt + ea + off, 4 * len,
-                                     hipMemcpyHostToDevice, s));
+              if (int r = hc.h2d(wt_dev, G.wt + ea + off, 4 * len)) return r;
             wl_csr sg{};
             sg.n = len;
             sg.nnz = 0;
@@ -980,7 +1147,9 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
                                col_dev, G.wt ? wt_dev : nullptr, blk_dev, isrep_dev,
                                qoff_dev, 1u, (uint32_t)a, blk[a]);
             HIP_LAUNCH_CHECK();
-            if (int r = quotient_chunk(S, len, blk[a], Q, &spill, hkey, hw)) return r;
+            if (int r = quotient_chunk(S, hc, D, len, 1, blk[a], ea + ent, Q, &spill, hkey, hw,
+                                       hdeg))
+              return r;
           }
           std::sort(spill.begin(), spill.end());
           for (size_t i = 0; i < spill.size();) {
@@ -988,7 +1157,8 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
             uint64_t w = 0;
             while (j < spill.size() && spill[j].first == spill[i].first) w += spill[j++].second;
             if (w > 0xFFFFFFFFull) return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
-            if (Q.m >= Q.cap) return fail(WL_EINVAL, "quotient larger than expected");
+            if (Q.m >= std::min(Q.cap, ea + ent))
+              return fail(WL_EINVAL, "quotient larger than expected");
             Q.deg[blk[a]] += 1;
             Q.col[Q.m] = spill[i].first;
             Q.wt[Q.m] = (uint32_t)w;
@@ -1001,21 +1171,22 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       }
       const uint64_t nrows = bnd - a;
       qoff.resize(nrows);
-      uint64_t run = 0;
+      uint64_t run = 0, nreps = 0;
       uint32_t bfirst = 0xFFFFFFFFu;
       for (uint64_t r = 0; r < nrows; ++r) {
         qoff[r] = run;
         if (isrep[a + r]) {
           if (bfirst == 0xFFFFFFFFu) bfirst = blk[a + r];
           run += G.rp(a + r + 1) - G.rp(a + r);
+          ++nreps;
         }
       }
       if (run > 0) {
-        if (int r = copy_rows_h2d(G, a, nrows, W + QL.stage, rp_dev, s)) return r;
-        HIP_TRY(hipMemcpyAsync(qoff_dev, qoff.data(), 8 * nrows, hipMemcpyHostToDevice, s));
-        HIP_TRY(hipMemcpyAsync(col_dev, G.col + ea, 4 * ent, hipMemcpyHostToDevice, s));
+        if (int r = copy_rows_h2d(hc, G, a, nrows, W + QL.stage, rp_dev, s)) return r;
+        if (int r = hc.h2d(qoff_dev, qoff.data(), 8 * nrows)) return r;
+        if (int r = hc.h2d(col_dev, G.col + ea, 4 * ent)) return r;
         if (G.wt)
-          HIP_TRY(hipMemcpyAsync(wt_dev, G.wt + ea, 4 * ent, hipMemcpyHostToDevice, s));
+          if (int r = hc.h2d(wt_dev, G.wt + ea, 4 * ent)) return r;
         wl_csr sg{};
         sg.n = run;
         sg.nnz = 0;
@@ -1030,13 +1201,15 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
                            G.wt ? wt_dev : nullptr, blk_dev, isrep_dev, qoff_dev,
                            (uint32_t)nrows, (uint32_t)a, bfirst);
         HIP_LAUNCH_CHECK();
-        if (int r = quotient_chunk(S, run, bfirst, Q, nullptr, hkey, hw)) return r;
+        if (int r = quotient_chunk(S, hc, D, run, nreps, bfirst, ea + ent, Q, nullptr, hkey,
+                                   hw, hdeg))
+          return r;
       }
       a = bnd;
     }
     // new row pointers and labels
     if (int r = nrp_buf.alloc(8 * (nq + 1))) return r;
-    uint64_t* qrp = (uint64_t*)nrp_buf.p;
+    uint64_t* qrp = nrp_buf.as<uint64_t>();
     qrp[0] = 0;
     for (uint64_t q = 0; q < nq; ++q) qrp[q + 1] = qrp[q] + Q.deg[q];
     if (!labels.empty()) {
@@ -1046,14 +1219,17 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       labels.swap(nl);
     }
     std::swap(qrp_buf.p, nrp_buf.p);
-    std::swap(qcol_buf.p, ncol_buf.p);
-    std::swap(qwt_buf.p, nwt_buf.p);
+    nrp_buf.p.reset();
+    if (!in_place) {
+      std::swap(qcol_buf.p, ncol_buf.p);
+      std::swap(qwt_buf.p, nwt_buf.p);
+    }
     G.n = nq;
     G.m = Q.m;
     G.rp32 = nullptr;
-    G.rp64 = (const uint64_t*)qrp_buf.p;
-    G.col = (const uint32_t*)qcol_buf.p;
-    G.wt = (const uint32_t*)qwt_buf.p;
+    G.rp64 = qrp_buf.as<const uint64_t>();
+    G.col = qcol_buf.as<const uint32_t>();
+    G.wt = qwt_buf.as<const uint32_t>();
   }
   // final colours: first occurrence over the original nodes
   mapk.assign(n0, 0xFFFFFFFFu);

@@ -50,8 +50,10 @@ __global__ void __launch_bounds__(kBlock) k_q_keys(Ctx ctx, const uint64_t* rp,
   }
 }
 
-// Before the sort: one segment [0, cnt) (k = 1), clear the reduce slots.
-__global__ void __launch_bounds__(kBlock) k_q_begin(Ctx ctx, uint32_t cnt) {
+// Before the sort: one segment [0, cnt) (k = 1), clear the reduce slots and
+// the entry counts of the chunk's blocks.
+__global__ void __launch_bounds__(kBlock) k_q_begin(Ctx ctx, uint32_t cnt, uint32_t* qdeg,
+                                                    uint32_t nblocks) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctx.st->k = 1;
     ctx.st->done = 0;
@@ -60,6 +62,8 @@ __global__ void __launch_bounds__(kBlock) k_q_begin(Ctx ctx, uint32_t cnt) {
   }
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < cnt; i += gridDim.x * kBlock)
     ctx.x[i] = 0;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < nblocks; i += gridDim.x * kBlock)
+    qdeg[i] = 0;
 }
 
 // After the sort and the scan: distinct keys and their summed weights.
@@ -69,6 +73,26 @@ __global__ void __launch_bounds__(kBlock) k_q_reduce(Ctx ctx, uint32_t cnt) {
     const uint32_t id = ctx.ids[p];
     atomicAdd(&qw[id], (unsigned long long)ctx.perm[p]);
     if (ctx.flags[p]) ctx.z[id] = ctx.keys[p];
+  }
+}
+
+constexpr uint32_t kErrQuotientWeight = 8u;  // DevState::err bit
+
+// The distinct entries in key order (block, then target) as column and weight
+// arrays, and the number of entries of every block.  Weights are reduced to
+// 32 bits; a larger sum sets an error bit.
+__global__ void __launch_bounds__(kBlock) k_q_emit(Ctx ctx, uint32_t cnt, uint32_t* qcol,
+                                                   uint32_t* qwt, uint32_t* qdeg) {
+  const uint32_t nd = min(ctx.st->k_new, cnt);
+  const unsigned long long* qw = (const unsigned long long*)ctx.x;
+  const uint64_t mask = (1ull << kQShift) - 1;
+  for (uint32_t d = blockIdx.x * kBlock + threadIdx.x; d < nd; d += gridDim.x * kBlock) {
+    const uint64_t key = ctx.z[d];
+    const uint64_t w = qw[d];
+    if (w > 0xFFFFFFFFull) atomicOr(&ctx.st->err, kErrQuotientWeight);
+    qcol[d] = (uint32_t)(key & mask);
+    qwt[d] = (uint32_t)w;
+    atomicAdd(&qdeg[key >> kQShift], 1u);
   }
 }
 

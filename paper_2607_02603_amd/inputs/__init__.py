@@ -261,8 +261,6 @@ def _gpu_build(n, nbits, max_keys, emit, name, device, host_out=False,
         group_keys = max(total, 1)
     rows_per = 1 << shift
     row_cnt = torch.zeros(n, dtype=torch.int64, device=device)
-    if host_out:
-        col_out = pinned_empty(total, torch.int32)
     cols = []
     pos = 0
     b0 = 0
@@ -291,10 +289,7 @@ def _gpu_build(n, nbits, max_keys, emit, name, device, host_out=False,
             hi = min(n, lo + rows_per)
             row_cnt[lo:hi] = torch.bincount(u - lo, minlength=hi - lo)
             c = (seg & 0xFFFFFFFF).to(torch.int32)
-            if host_out:
-                col_out[pos:pos + c.numel()].copy_(c)
-            else:
-                cols.append(c)
+            cols.append(c)
             pos += c.numel()
             del seg, u, c
         del keys
@@ -302,9 +297,18 @@ def _gpu_build(n, nbits, max_keys, emit, name, device, host_out=False,
     rp = torch.zeros(n + 1, dtype=torch.int64, device=device)
     rp[1:] = torch.cumsum(row_cnt, 0)
     if host_out:
+        # page-locked memory is capped per process: take exactly nnz entries
+        del row_cnt
         rp_h = pinned_empty(n + 1, torch.int64)
         rp_h.copy_(rp)
-        return CSR(n, rp_h, col_out[:pos], None, name)
+        del rp
+        col_h = pinned_empty(pos, torch.int32)
+        at = 0
+        for c in cols:
+            col_h[at:at + c.numel()].copy_(c)
+            at += c.numel()
+        del cols
+        return CSR(n, rp_h, col_h, None, name)
     col = torch.cat(cols) if cols else torch.empty(0, dtype=torch.int32, device=device)
     del cols
     return CSR(n, rp, col, None, name)

@@ -167,7 +167,10 @@ int gen_chunglu_gpu(int phase, uint32_t n, uint64_t seed, const uint64_t* thr,
 // Pinned host memory of exactly 'bytes' (the caller frees it).
 void* gen_host_alloc(uint64_t bytes) {
   void* p = nullptr;
-  if (hipHostMalloc(&p, bytes ? bytes : 8, hipHostMallocDefault) != hipSuccess) return nullptr;
+  if (hipHostMalloc(&p, bytes ? bytes : 8, hipHostMallocDefault) != hipSuccess) {
+    (void)hipGetLastError();  // leave no error behind for the next HIP call
+    return nullptr;
+  }
   return p;
 }
 

@@ -15,15 +15,17 @@ from paper_2607_02603_amd import inputs
 pytestmark = pytest.mark.gpu
 
 
-def _host_graph(rp, col, wt=None):
+def _host_graph(rp, col, wt=None, pinned=True):
     n = len(rp) - 1
     g = wl.Graph.from_numpy(n, rp, col, wt, device=None)
+    if not pinned:
+        return g
     return wl.Graph(n, g.row_ptr.pin_memory(), g.col_idx.pin_memory(),
                     None if g.weight is None else g.weight.pin_memory())
 
 
-def _check(rp, col, wt=None, init=None, mb=8, seed=0):
-    g = _host_graph(rp, col, wt)
+def _check(rp, col, wt=None, init=None, mb=8, seed=0, pinned=True):
+    g = _host_graph(rp, col, wt, pinned)
     init_t = None if init is None else torch.from_numpy(np.asarray(init, np.uint32).view(np.int32))
     c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, init_t, seed, mb)
     got = c.numpy().view(np.uint32)
@@ -123,6 +125,27 @@ def test_medium_rmat_explicit_cap():
     g = inputs.rmat(18, 16, seed=3)
     print("rmat18 explicit cap", flush=True)
     got, k, r, outer, coarsest = _check(g.row_ptr, g.col, mb=g.nnz // 6)
+
+
+@pytest.mark.parametrize("mb", [5, 64, 10**9])
+def test_pageable_host_graph(mb):
+    # the same graphs from pageable host memory (copied through the library's
+    # page-locked staging buffers) give the oracle's result
+    g = inputs.rmat(9, 8, seed=1)
+    _check(g.row_ptr, g.col, mb=mb, pinned=False)
+    rng = random.Random(mb)
+    n = 300
+    edges = [(rng.randrange(n), rng.randrange(n)) for _ in range(2000)]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    wt = np.array([rng.randint(1, 4) for _ in range(col.size)], np.uint32)
+    _check(rp, col, wt, mb=mb, pinned=False)
+
+
+def test_medium_rmat_pageable_explicit_cap():
+    # several outer iterations with quotients larger than one staging buffer
+    g = inputs.rmat(18, 16, seed=5)
+    print("rmat18 pageable explicit cap", flush=True)
+    _check(g.row_ptr, g.col, mb=g.nnz // 5, pinned=False)
 
 
 def test_medium_rmat_tight_budget_auto_cap():
