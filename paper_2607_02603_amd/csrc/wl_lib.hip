@@ -295,57 +295,111 @@ __global__ void __launch_bounds__(kBlock) k_place_colors(Ctx ctx) {
 // One call's device session.
 // ---------------------------------------------------------------------------
 
+constexpr uint32_t kHostRounds = 8;
+constexpr int kAsyncPassesDefault = 2;
+
+int env_int(const char* name, int lo, int hi, int dflt) {
+  const char* v = getenv(name);
+  if (!v || !*v) return dflt;
+  const int x = atoi(v);
+  return x < lo ? lo : (x > hi ? hi : x);
+}
+
 struct Session {
   Layout L;
   Ctx ctx;
+  // Rounds driven from the host before device-driven groups start, and radix
+  // passes a device-driven round runs before it halts for the host.  Both
+  // can be set for testing (WL_HOST_ROUNDS, WL_ASYNC_PASSES).
+  uint32_t host_rounds_first = kHostRounds;
+  int async_passes = kAsyncPassesDefault;
   hipStream_t s;
   bool rp64;
   bool weighted;
   DevState host;      // last copy of the device state
   DevState init_src;  // source of the initial state copy
   uint32_t nscan;
-  // diagnostics
+  // diagnostics: SpMV launches bracketed by events, folded in at the next
+  // read-back (a launch queued for a round that never ran is dropped)
+  struct TimedSpmv {
+    hipEvent_t a, b;
+    uint32_t round;  // the round it belongs to
+    bool always;     // launched by a host-driven round: it ran
+    bool uniform;
+  };
   int sflags = 0;
-  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
-  bool spmv_pending = false;
-  bool pending_uniform = false;
+  hipEvent_t call_ev[2] = {nullptr, nullptr};
+  std::vector<hipEvent_t> ev_pool;
+  size_t ev_used = 0;
+  std::vector<TimedSpmv> timed;
   wl_stats stats{};
 
   ~Session() {
-    for (hipEvent_t& e : ev)
+    for (hipEvent_t& e : call_ev)
       if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t& e : ev_pool) (void)hipEventDestroy(e);
   }
 
   int stats_begin() {
     sflags = g_stats_flags;
     stats = wl_stats{};
     if (sflags & WL_STATS_TIME) {
-      for (hipEvent_t& e : ev) HIP_TRY(hipEventCreate(&e));
-      HIP_TRY(hipEventRecord(ev[2], s));
+      for (hipEvent_t& e : call_ev) HIP_TRY(hipEventCreate(&e));
+      HIP_TRY(hipEventRecord(call_ev[0], s));
     }
     return WL_OK;
   }
 
-  // after a synchronising pull: fold the timed SpMV launch in
-  int stats_collect() {
-    if ((sflags & WL_STATS_TIME) && spmv_pending) {
-      float ms = 0;
-      HIP_TRY(hipEventElapsedTime(&ms, ev[0], ev[1]));
-      if (pending_uniform)
-        stats.uniform_ms += ms;
-      else
-        stats.spmv_ms += ms;
-      spmv_pending = false;
+  hipEvent_t next_event() {
+    if (ev_used == ev_pool.size()) {
+      hipEvent_t e = nullptr;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      ev_pool.push_back(e);
     }
+    return ev_pool[ev_used++];
+  }
+
+  // Brackets the launches issued by 'launch' with events when timing is on;
+  // launches are counted when the round is known to have run.
+  template <typename F>
+  void timed_spmv(uint32_t round, bool always, bool uniform, F&& launch) {
+    TimedSpmv t{nullptr, nullptr, round, always, uniform};
+    if (sflags & WL_STATS_TIME) {
+      t.a = next_event();
+      t.b = next_event();
+    }
+    if (t.a && t.b) (void)hipEventRecord(t.a, s);
+    launch();
+    if (t.a && t.b) (void)hipEventRecord(t.b, s);
+    timed.push_back(t);
+  }
+
+  // after a synchronising pull
+  int stats_collect() {
+    const uint32_t ran = host.round + (host.done == kHalted ? 1u : 0u);
+    for (const TimedSpmv& t : timed) {
+      if (!t.always && t.round >= ran) continue;
+      float ms = 0;
+      if (t.a && t.b) HIP_TRY(hipEventElapsedTime(&ms, t.a, t.b));
+      if (t.uniform) {
+        stats.uniform_ms += ms;
+        stats.uniform_launches++;
+      } else {
+        stats.spmv_ms += ms;
+        stats.spmv_launches++;
+      }
+    }
+    timed.clear();
+    ev_used = 0;
     return WL_OK;
   }
 
   int stats_end() {
     if (sflags & WL_STATS_TIME) {
-      HIP_TRY(hipEventRecord(ev[3], s));
-      HIP_TRY(hipEventSynchronize(ev[3]));
+      HIP_TRY(hipEventRecord(call_ev[1], s));
+      HIP_TRY(hipEventSynchronize(call_ev[1]));
       float ms = 0;
-      HIP_TRY(hipEventElapsedTime(&ms, ev[2], ev[3]));
+      HIP_TRY(hipEventElapsedTime(&ms, call_ev[0], call_ev[1]));
       stats.call_ms = ms;
     }
     if (int r = pull()) return r;
@@ -440,32 +494,24 @@ struct Session {
     g.b1 = g.b2 + (h.bin_cnt[1] ? grid_for(h.bin_cnt[1], kBlock / 16) : 0);
     g.b0 = g.b1 + (h.bin_cnt[0] ? grid_for(h.bin_cnt[0], kBlock / 4) : 0);
     if (g.b0 == 0) return;
-    const int mode = h.k <= 255 ? kGather8 : (h.k <= kTableMax ? kGather16 : kGatherX);
+    const int mode = gather_mode(h.k);
     if (!uniform)
       hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock),
                          0, s, ctx, mode);
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
                          dim3(kBlock), 0, s, ctx);
-    if (sflags & WL_STATS_TIME) (void)hipEventRecord(ev[0], s);
-    if (uniform)
-      hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
-                         dim3(kBlock), 0, s, ctx);
-    else if (mode == kGather8)
-      spmv_launch<RP, W, kGather8>(g);
-    else if (mode == kGather16)
-      spmv_launch<RP, W, kGather16>(g);
-    else
-      spmv_launch<RP, W, kGatherX>(g);
-    if (sflags & WL_STATS_TIME) {
-      (void)hipEventRecord(ev[1], s);
-      spmv_pending = true;
-      pending_uniform = uniform;
-    }
-    if (uniform)
-      stats.uniform_launches++;
-    else
-      stats.spmv_launches++;
+    timed_spmv(h.round, true, uniform, [&] {
+      if (uniform)
+        hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
+                           dim3(kBlock), 0, s, ctx);
+      else if (mode == kGather8)
+        spmv_launch<RP, W, kGather8>(g);
+      else if (mode == kGather16)
+        spmv_launch<RP, W, kGather16>(g);
+      else
+        spmv_launch<RP, W, kGatherX>(g);
+    });
   }
 
   void spmv() {
@@ -476,14 +522,42 @@ struct Session {
     }
   }
 
+  // SpMV of a round launched without reading the state back: the gather
+  // mode is chosen on the device, there is no single-colour shortcut.
+  template <typename RP, bool W>
+  void spmv_async_t(uint32_t round) {
+    const DevState& h = host;
+    SpmvGrid g;
+    g.heavy = h.n_chunks ? grid_for(h.n_chunks, kBlock / kWave) : 0;
+    g.b2 = g.heavy + (h.bin_cnt[2] ? grid_for(h.bin_cnt[2], kBlock / 64) : 0);
+    g.b1 = g.b2 + (h.bin_cnt[1] ? grid_for(h.bin_cnt[1], kBlock / 16) : 0);
+    g.b0 = g.b1 + (h.bin_cnt[0] ? grid_for(h.bin_cnt[0], kBlock / 4) : 0);
+    if (g.b0 == 0) return;
+    hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
+                       ctx, -1);
+    if (sflags & WL_STATS_WORK)
+      hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
+                         dim3(kBlock), 0, s, ctx);
+    timed_spmv(round, false, false, [&] {
+      hipLaunchKernelGGL((k_spmv_dyn<RP, W>), dim3(g.b0), dim3(kBlock), 0, s, ctx, g);
+    });
+  }
+
+  void spmv_async(uint32_t round) {
+    if (rp64) {
+      if (weighted) spmv_async_t<uint64_t, true>(round);
+      else spmv_async_t<uint64_t, false>(round);
+    } else {
+      if (weighted) spmv_async_t<uint32_t, true>(round);
+      else spmv_async_t<uint32_t, false>(round);
+    }
+  }
+
   // Relabel by (c, z) for the current grouping; count_round = 0 for the
   // canonicalisation of the initial labels.
   int relabel(int count_round) {
     if (int r = segmented_sort()) return r;
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
-    hipLaunchKernelGGL(k_cstart, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_scatter_colors, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_round_end, dim3(1), dim3(1), 0, s, ctx, count_round);
+    relabel_tail(count_round);
     HIP_LAUNCH_CHECK();
     return pull();
   }
@@ -499,18 +573,15 @@ struct Session {
                        0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
-    for (int pass = 0; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
-      hipLaunchKernelGGL(k_big_tiles, dim3(1), dim3(kBlock), 0, s, ctx, pass);
-      if (pass == 0 && !ctx.keys_mat)
-        hipLaunchKernelGGL(k_big_gather, dim3(2048), dim3(kBlock), 0, s, ctx);
-      hipLaunchKernelGGL(k_big_clear,
-                         dim3(grid_for((uint64_t)host.n_big[pass & 1] * kRadix)),
-                         dim3(kBlock), 0, s, ctx, pass);
-      hipLaunchKernelGGL(k_big_hist, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
-      hipLaunchKernelGGL(k_big_scan, dim3(std::min<uint32_t>(host.n_big[pass & 1], 4096)),
-                         dim3(kBlock), 0, s, ctx, pass);
-      hipLaunchKernelGGL(k_big_scatter, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
-      hipLaunchKernelGGL(k_big_copyback, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+    return finish_sort(0);
+  }
+
+  // Radix passes from 'pass0' on while big segments are left (read back after
+  // every pass), then the small sorts and the rank scan.
+  int finish_sort(int pass0) {
+    for (int pass = pass0; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
+      radix_pass(pass, grid_for((uint64_t)host.n_big[pass & 1] * kRadix),
+                 std::min<uint32_t>(host.n_big[pass & 1], 4096));
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
     }
@@ -520,11 +591,66 @@ struct Session {
     if (host.n_small)
       hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
                          dim3(kBlock), 0, s, ctx);
+    rank_scan();
+    HIP_LAUNCH_CHECK();
+    return WL_OK;
+  }
+
+  void radix_pass(int pass, uint32_t clear_grid, uint32_t scan_grid) {
+    hipLaunchKernelGGL(k_big_tiles, dim3(1), dim3(kBlock), 0, s, ctx, pass);
+    if (pass == 0 && !ctx.keys_mat)
+      hipLaunchKernelGGL(k_big_gather, dim3(2048), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_big_clear, dim3(clear_grid), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_hist, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_scan, dim3(scan_grid), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_scatter, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_copyback, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+  }
+
+  void rank_scan() {
     hipLaunchKernelGGL(k_scan_part, dim3(nscan), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
     hipLaunchKernelGGL(k_scan_final, dim3(nscan), dim3(kBlock), 0, s, ctx);
+  }
+
+  void relabel_tail(int count_round) {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_cstart, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_scatter_colors, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_round_end, dim3(1), dim3(1), 0, s, ctx, count_round);
+  }
+
+  // One whole round launched without reading anything back.  Every grid is
+  // fixed for the call and every count comes from the device state; at most
+  // async_passes radix passes run, and a round that needs more halts the
+  // device before its small sorts (finish_halted completes it).
+  void round_async(uint32_t round) {
+    hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
+    spmv_async(round);
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_fill_u8, dim3(gn), dim3(kBlock), 0, s, ctx, ctx.flags,
+                       (uint64_t)L.n, (uint8_t)0);
+    hipLaunchKernelGGL(k_segments, dim3(gn), dim3(kBlock), 0, s, ctx);
+    for (int pass = 0; pass < async_passes; ++pass) radix_pass(pass, 1024, 1024);
+    hipLaunchKernelGGL(k_passes_check, dim3(1), dim3(1), 0, s, ctx, async_passes);
+    hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 2048)),
+                       dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_small_sort, dim3(grid_for(L.n / (kTinyMax + 1), 1, 2048)),
+                       dim3(kBlock), 0, s, ctx);
+    rank_scan();
+    relabel_tail(1);
+  }
+
+  // The device halted in a round after async_passes radix passes: clear the
+  // halt and finish that round with host-driven passes.
+  int finish_halted() {
+    hipLaunchKernelGGL(k_resume, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
-    return WL_OK;
+    if (int r = pull()) return r;
+    if (int r = finish_sort(async_passes)) return r;
+    relabel_tail(1);
+    HIP_LAUNCH_CHECK();
+    return pull();
   }
 
   // Algorithm 1 to completion on the session's graph, from labels on the
@@ -539,8 +665,24 @@ struct Session {
       if (int r = relabel(0)) return r;
     }
     if (int r = build_schedule()) return r;
+    // The first rounds are driven from the host (each reads its counts
+    // back); after that, rounds go to the device in groups of 'ahead' with
+    // one read-back per group.  Rounds queued past the last one find the
+    // state done and return at once.
+    uint32_t host_rounds = 0, ahead = 8;
     while (!host.done) {
-      if (int r = round()) return r;
+      if (host_rounds < host_rounds_first) {
+        if (int r = round()) return r;
+        ++host_rounds;
+        continue;
+      }
+      const uint32_t base = host.round;
+      for (uint32_t i = 0; i < ahead; ++i) round_async(base + i);
+      HIP_LAUNCH_CHECK();
+      if (int r = pull()) return r;
+      if (host.done == kHalted)
+        if (int r = finish_halted()) return r;
+      ahead = std::min<uint32_t>(ahead * 2, 64);
     }
     return WL_OK;
   }
@@ -568,6 +710,8 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
   S.rp64 = g->row_ptr64 != nullptr;
   S.weighted = g->weight != nullptr;
   S.nscan = scan_blocks(g->n);
+  S.host_rounds_first = (uint32_t)env_int("WL_HOST_ROUNDS", 0, 1 << 30, (int)kHostRounds);
+  S.async_passes = env_int("WL_ASYNC_PASSES", 0, kPasses, kAsyncPassesDefault);
   return WL_OK;
 }
 

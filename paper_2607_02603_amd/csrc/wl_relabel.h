@@ -103,7 +103,11 @@ __global__ void __launch_bounds__(kBlock) k_big_tiles(Ctx ctx, int pass) {
   if (st->done) return;
   const int cur = pass & 1;
   const uint32_t nb = st->n_big[cur];
-  if (nb == 0) return;
+  if (nb == 0) {
+    // nothing left: the other list must not be taken for a later pass
+    if (threadIdx.x == 0) st->n_big[cur ^ 1] = 0;
+    return;
+  }
   const uint2* L = big_list(ctx, cur);
   __shared__ uint32_t sh[kBlock / kWave];
   uint32_t carry = 0;
@@ -487,6 +491,19 @@ __global__ void __launch_bounds__(kBlock) k_scatter_colors(Ctx ctx) {
     ctx.c[v] = id;
     ctx.act[v] = (ctx.cstart[id + 1] - ctx.cstart[id]) >= 2 ? 1 : 0;
   }
+}
+
+// After the radix passes launched without a read-back: if big segments are
+// left, halt (done = 3) before the small sorts; the host finishes the round.
+constexpr uint32_t kHalted = 3;
+__global__ void k_passes_check(Ctx ctx, int passes) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  if (st->n_big[passes & 1] > 0) st->done = kHalted;
+}
+
+__global__ void k_resume(Ctx ctx) {
+  if (ctx.st->done == kHalted) ctx.st->done = 0;
 }
 
 __global__ void k_round_end(Ctx ctx, int count_round) {

@@ -190,6 +190,10 @@ __global__ void __launch_bounds__(kBlock) k_heavy_fill(Ctx ctx) {
 // table of k values stays in cache.
 enum GatherMode { kGatherX = 0, kGather16 = 1, kGather8 = 2 };
 
+__host__ __device__ __forceinline__ int gather_mode(uint32_t k) {
+  return k <= 255 ? kGather8 : (k <= kTableMax ? kGather16 : kGatherX);
+}
+
 template <int M>
 __device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j,
                                                  uint64_t rkey) {
@@ -284,8 +288,7 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
 }
 
 template <typename RP, bool W, int M>
-__global__ void __launch_bounds__(kBlock) k_spmv(Ctx ctx, SpmvGrid g) {
-  if (ctx.st->done) return;
+__device__ __forceinline__ void spmv_body(const Ctx& ctx, const SpmvGrid& g) {
   const uint64_t rkey = ctx.batch ? round_key(ctx.st->seed, ctx.st->round) : 0;
   const uint32_t b = blockIdx.x;
   if (b < g.heavy)
@@ -296,6 +299,26 @@ __global__ void __launch_bounds__(kBlock) k_spmv(Ctx ctx, SpmvGrid g) {
     spmv_rows<16, 4, RP, W, M>(ctx, 1, b - g.b2, g.b1 - g.b2, rkey);
   else
     spmv_rows<4, 2, RP, W, M>(ctx, 0, b - g.b1, g.b0 - g.b1, rkey);
+}
+
+template <typename RP, bool W, int M>
+__global__ void __launch_bounds__(kBlock) k_spmv(Ctx ctx, SpmvGrid g) {
+  if (ctx.st->done) return;
+  spmv_body<RP, W, M>(ctx, g);
+}
+
+// The same with the gather mode taken from the colour count on the device
+// (rounds launched without reading the state back).
+template <typename RP, bool W>
+__global__ void __launch_bounds__(kBlock) k_spmv_dyn(Ctx ctx, SpmvGrid g) {
+  if (ctx.st->done) return;
+  const int mode = gather_mode(ctx.st->k);
+  if (mode == kGather8)
+    spmv_body<RP, W, kGather8>(ctx, g);
+  else if (mode == kGather16)
+    spmv_body<RP, W, kGather16>(ctx, g);
+  else
+    spmv_body<RP, W, kGatherX>(ctx, g);
 }
 
 // One colour and unit weights: every x_j is the same w, so
@@ -312,9 +335,11 @@ __global__ void __launch_bounds__(kBlock) k_spmv_uniform(Ctx ctx) {
 
 // Per-round random values for the gather: compact colour array plus the
 // table of the k colour values (k <= 65535), or x per node otherwise.
+// mode < 0: chosen from the colour count on the device.
 __global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
   if (ctx.st->done) return;
   const uint32_t k = ctx.st->k;
+  if (mode < 0) mode = gather_mode(k);
   const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
   const uint32_t tid = blockIdx.x * kBlock + threadIdx.x;
   const uint32_t stride = gridDim.x * kBlock;
