@@ -271,7 +271,9 @@ static int cmp_sig(const void *a, const void *b)
     return (li > lj) - (li < lj);
 }
 
-/* One classic round: c_out = dense rank of the signatures; returns k'. */
+/* One classic round: c_out = dense rank of the signatures; returns k'.
+ * Signature terms whose weight sum is 0 are dropped (Definition "Stable
+ * Coloring" compares a_{i,B}, which is 0 for an unreached block too). */
 uint32_t orc_classic_round(uint64_t n, const uint64_t *row_ptr,
                            const uint32_t *col, const uint32_t *weight,
                            const uint32_t *c, uint32_t *c_out)
@@ -303,7 +305,13 @@ uint32_t orc_classic_round(uint64_t n, const uint64_t *row_ptr,
             else
                 s[u++] = s[t];
         }
-        len[i] = u;
+        /* a block reached with total weight 0 is the same as a block not
+         * reached: the definition compares the sums a_{i,B} only */
+        uint64_t kept = 0;
+        for (uint64_t t = 0; t < u; ++t)
+            if (s[t].wsum != 0)
+                s[kept++] = s[t];
+        len[i] = kept;
     }
     /* pack (in place, moving left only) */
     sig_ptr[0] = 0;

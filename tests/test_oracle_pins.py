@@ -148,6 +148,25 @@ def test_bruteforce_random_small(trial):
     assert ra == rb
 
 
+@pytest.mark.parametrize("trial", range(20))
+def test_bruteforce_zero_weight_entries(trial):
+    # an entry of weight 0 adds nothing to a_{i,B} (Definition "Stable
+    # Coloring"): both oracles must treat it as absent, as brute force does
+    rng = random.Random(5000 + trial)
+    n = rng.randint(2, 7)
+    rp, col, _ = _random_graph(rng, n, trial % 2 == 1, False, trial % 3 == 0, False)
+    wt = np.array([rng.choice([0, 0, 1, 2]) for _ in range(col.size)], np.uint32)
+    A = bf.dense_matrix(rp, col, wt)
+    truth = bf.coarsest_stable_partition(A)
+    ca, ka, ra, _, st = oracle.stable_coloring(rp, col, wt, None, seed=trial)
+    cb, kb, rb, _, stb = oracle.classic_coloring(rp, col, wt, None)
+    assert st == 0 and stb == 0
+    assert bf.partition_of(ca) == truth
+    assert bf.partition_of(cb) == truth
+    assert ka == kb and ra == rb
+    assert oracle.is_stable(rp, col, wt, ca)
+
+
 def test_bruteforce_n9_sample():
     rng = random.Random(99)
     for _ in range(3):
