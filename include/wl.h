@@ -76,7 +76,7 @@ typedef struct wl_csr {
 } wl_csr;
 
 /* Workspace (device bytes) needed by the in-core entry points
- * (wl_refine_round, wl_stable_coloring, wl_verify_stable) for graph g.
+ * (wl_refine_round, wl_stable_coloring) for graph g.
  * Only g->n and g->nnz are read; the pointers may be NULL.
  * Returns WL_EINVAL for a NULL argument, WL_EOVERFLOW for n >= 2^32. */
 int wl_workspace_size(const wl_csr *g, uint64_t *bytes_out);
@@ -152,10 +152,23 @@ int wl_stable_coloring_batched(const wl_csr *g_host, const uint32_t *init_host,
                                int *coarsest_out, void *workspace,
                                uint64_t ws_bytes, void *stream);
 
-/* Exact stability certificate (Definition "Stable Coloring"): WL_OK when
- * every two nodes of each colour class have equal total out-weight into
- * every class, WL_ENOTSTABLE otherwise.  Deterministic (no randomness).
- *   g      device CSR;  color  device, n entries, each < k;  k <= n. */
+/* Exact stability certificate (Definition "Stable Coloring", Section 3):
+ * WL_OK when every two nodes of each colour class have equal total
+ * out-weight into every class, WL_ENOTSTABLE otherwise.  Deterministic (no
+ * randomness).  An entry of weight 0 adds nothing to a total, so it is the
+ * same as a missing entry.  Applied to the output of Algorithm 1 it turns
+ * the probabilistic guarantee of Theorem 1 into a certainty: every colouring
+ * Algorithm 1 produces is at least as coarse as the coarsest stable colouring
+ * refining its start, so one that passes this check is exactly that one.
+ *   g          device CSR.
+ *   color      device, n entries, each < k (ids need not all be used).
+ *   k          1 <= k <= n (any k when n == 0).
+ *   workspace  device, 256-byte aligned, >= wl_verify_workspace_size(g)
+ *              bytes (4 bytes per entry, 8 for weighted graphs, plus about
+ *              17 bytes per node); its contents are scratch.
+ * Errors: WL_EINVAL (NULL pointers, k out of range, a colour >= k), WL_EBUDGET,
+ * WL_EHIP. */
+int wl_verify_workspace_size(const wl_csr *g, uint64_t *bytes_out);
 int wl_verify_stable(const wl_csr *g, const uint32_t *color, uint32_t k,
                      void *workspace, uint64_t ws_bytes, void *stream);
 

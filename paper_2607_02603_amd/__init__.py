@@ -29,7 +29,8 @@ _NAMES = {-1: "WL_EINVAL", -2: "WL_EBUDGET", -3: "WL_EOVERFLOW",
           -4: "WL_EMAXROUNDS", -5: "WL_ENOTSTABLE", -6: "WL_EHIP", -7: "WL_ENOMEM"}
 
 EXPORTED = ["wl_workspace_size", "wl_batched_workspace_size", "wl_refine_round",
-            "wl_stable_coloring", "wl_stable_coloring_batched", "wl_verify_stable",
+            "wl_stable_coloring", "wl_stable_coloring_batched", "wl_verify_workspace_size",
+            "wl_verify_stable",
             "wl_stats_enable", "wl_stats_get", "wl_last_error"]
 
 WL_STATS_TIME = 1
@@ -79,6 +80,7 @@ def lib():
                                          u64, vp]
         L.wl_stable_coloring_batched.argtypes = [P(WlCsr), vp, u64, u64, vp, P(u32),
                                                  P(u32), P(u32), P(i32), vp, u64, vp]
+        L.wl_verify_workspace_size.argtypes = [P(WlCsr), P(u64)]
         L.wl_verify_stable.argtypes = [P(WlCsr), vp, u32, vp, u64, vp]
         L.wl_stats_enable.argtypes = [i32]
         L.wl_stats_get.argtypes = [P(WlStats)]
@@ -240,9 +242,17 @@ def wl_stable_coloring_batched(g_host, init_host=None, seed=0, max_batch_entries
     return out, int(k.value), int(r.value), int(o.value), bool(co.value)
 
 
+def wl_verify_workspace_size(g):
+    out = ctypes.c_uint64(0)
+    s = g.csr()
+    _check(lib().wl_verify_workspace_size(ctypes.byref(s), ctypes.byref(out)))
+    return int(out.value)
+
+
 def wl_verify_stable(g, color, k, ws=None, stream=None):
     """True if the colouring is stable (exact certificate), else False."""
-    ws = _ws(g, ws)
+    if ws is None:
+        ws = workspace(wl_verify_workspace_size(g), g.device)
     s = g.csr()
     code = lib().wl_verify_stable(ctypes.byref(s), _ptr(color), k, _ptr(ws), ws.numel(),
                                   _stream(stream))

@@ -25,6 +25,7 @@
 #include "wl_relabel.h"
 #include "wl_spmv.h"
 #include "wl_quotient.h"
+#include "wl_verify.h"
 
 using namespace wl;
 
@@ -1389,6 +1390,91 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   return WL_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Exact stability certificate (Definition "Stable Coloring").
+// ---------------------------------------------------------------------------
+
+struct VerLayout {
+  uint64_t st, rep, multi, mid, hub, hub_off, keys, total;
+};
+
+VerLayout ver_layout(uint64_t n, uint64_t nnz, bool weighted) {
+  VerLayout L{};
+  uint64_t o = 0;
+  auto take = [&](uint64_t b) { uint64_t at = o; o = align_up(o + b); return at; };
+  L.st = take(sizeof(VerState));
+  L.rep = take(4 * n);
+  L.multi = take(n);
+  L.mid = take(4 * n);
+  L.hub = take(4 * n);
+  L.hub_off = take(4 * (n + 1));
+  L.keys = take((weighted ? 8 : 4) * nnz);
+  L.total = o;
+  return L;
+}
+
+template <typename K>
+int verify_run(const wl_csr* g, const uint32_t* color, uint32_t k, uint8_t* ws,
+               const VerLayout& L, hipStream_t s) {
+  VerCtx<K> v{};
+  v.n = (uint32_t)g->n;
+  v.k = k;
+  v.rp32 = g->row_ptr32;
+  v.rp64 = g->row_ptr64;
+  v.col = g->col_idx;
+  v.wgt = g->weight;
+  v.color = color;
+  v.st = (VerState*)(ws + L.st);
+  v.rep = (uint32_t*)(ws + L.rep);
+  v.multi = ws + L.multi;
+  v.mid = (uint32_t*)(ws + L.mid);
+  v.hub = (uint32_t*)(ws + L.hub);
+  v.hub_off = (uint32_t*)(ws + L.hub_off);
+  v.keys = (K*)(ws + L.keys);
+  VerState h{};
+  auto pull = [&]() -> int {
+    HIP_TRY(hipMemcpyAsync(&h, v.st, sizeof(VerState), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    return WL_OK;
+  };
+  const uint32_t gn = grid_for(v.n, kBlock, 4096);
+  hipLaunchKernelGGL(k_v_clear<K>, dim3(grid_for(k, kBlock, 4096)), dim3(kBlock), 0, s, v);
+  hipLaunchKernelGGL(k_v_rep<K>, dim3(gn), dim3(kBlock), 0, s, v);
+  HIP_LAUNCH_CHECK();
+  if (int r = pull()) return r;
+  if (h.err & kVErrColor) return fail(WL_EINVAL, "a colour is >= k");
+  hipLaunchKernelGGL(k_v_multi<K>, dim3(gn), dim3(kBlock), 0, s, v);
+  hipLaunchKernelGGL(k_v_bin<K>, dim3(gn), dim3(kBlock), 0, s, v);
+  hipLaunchKernelGGL(k_v_sort_wave<K>, dim3(grid_for(v.n, kBlock / kWave, 8192)),
+                     dim3(kBlock), 0, s, v);
+  HIP_LAUNCH_CHECK();
+  if (int r = pull()) return r;
+  if (h.n_mid)
+    hipLaunchKernelGGL(k_v_sort_mid<K>, dim3(std::min<uint32_t>(h.n_mid, 4096)),
+                       dim3(kBlock), 0, s, v);
+  if (h.n_hub) {
+    hipLaunchKernelGGL(k_v_hub_plan<K>, dim3(1), dim3(kBlock), 0, s, v);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    const uint32_t gc = std::min<uint32_t>(h.n_hub_chunks, 8192);
+    hipLaunchKernelGGL(k_v_hub_sort_chunks<K>, dim3(gc), dim3(kBlock), 0, s, v);
+    for (uint64_t kk = 2ull * kVChunk; kk <= h.max_pow; kk <<= 1) {
+      hipLaunchKernelGGL(k_v_hub_step<K>, dim3(gc), dim3(kBlock), 0, s, v, kk, kk, 1);
+      for (uint64_t j = kk >> 2; j >= kVChunk; j >>= 1)
+        hipLaunchKernelGGL(k_v_hub_step<K>, dim3(gc), dim3(kBlock), 0, s, v, kk, j, 0);
+      hipLaunchKernelGGL(k_v_hub_finish<K>, dim3(gc), dim3(kBlock), 0, s, v, kk);
+    }
+  }
+  if constexpr (sizeof(K) == 4)
+    hipLaunchKernelGGL(k_v_compare, dim3(grid_for(v.n, kBlock / 16, 8192)), dim3(kBlock), 0,
+                       s, v);
+  else
+    hipLaunchKernelGGL(k_v_compare_w, dim3(gn), dim3(kBlock), 0, s, v);
+  HIP_LAUNCH_CHECK();
+  if (int r = pull()) return r;
+  return (h.err & kVErrMismatch) ? fail(WL_ENOTSTABLE, "the colouring is not stable") : WL_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -1526,10 +1612,35 @@ int wl_stable_coloring_batched(const wl_csr* g_host, const uint32_t* init_host,
                      (hipStream_t)stream);
 }
 
+int wl_verify_workspace_size(const wl_csr* g, uint64_t* bytes_out) {
+  g_err[0] = 0;
+  if (!g || !bytes_out) return fail(WL_EINVAL, "NULL argument");
+  if (g->n >= (1ull << 32)) return fail(WL_EOVERFLOW, "n does not fit 32 bits");
+  *bytes_out = ver_layout(g->n, g->nnz, g->weight != nullptr).total;
+  return WL_OK;
+}
+
 int wl_verify_stable(const wl_csr* g, const uint32_t* color, uint32_t k,
                      void* workspace, uint64_t ws_bytes, void* stream) {
-  (void)g; (void)color; (void)k; (void)workspace; (void)ws_bytes; (void)stream;
-  return fail(WL_EINVAL, "stability certificate is not available in this build");
+  g_err[0] = 0;
+  if (int r = check_graph(g)) return r;
+  if (g->n == 0) return WL_OK;
+  if (!color) return fail(WL_EINVAL, "color is NULL");
+  if (k == 0 || k > g->n) return fail(WL_EINVAL, "k = %u must be in [1, n]", k);
+  if (g->nnz > 0 && g->weight == nullptr && g->col_idx == nullptr)
+    return fail(WL_EINVAL, "col_idx is NULL");
+  const VerLayout L = ver_layout(g->n, g->nnz, g->weight != nullptr);
+  if (!workspace) return fail(WL_EINVAL, "workspace is NULL");
+  if ((uintptr_t)workspace % kAlign)
+    return fail(WL_EINVAL, "workspace must be %llu-byte aligned", (unsigned long long)kAlign);
+  if (ws_bytes < L.total)
+    return fail(WL_EBUDGET, "workspace has %llu bytes, %llu needed",
+                (unsigned long long)ws_bytes, (unsigned long long)L.total);
+  hipStream_t s = (hipStream_t)stream;
+  if (int r = check_nnz_device(g, s)) return r;
+  if (g->weight)
+    return verify_run<uint64_t>(g, color, k, (uint8_t*)workspace, L, s);
+  return verify_run<uint32_t>(g, color, k, (uint8_t*)workspace, L, s);
 }
 
 }  // extern "C"

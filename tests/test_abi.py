@@ -63,6 +63,21 @@ def test_workspace_size_host_only():
     assert 40 * 100000 < out.value < 120 * 100000 + 64 * 5000000 // 2048 * 1024
 
 
+def test_verify_workspace_size_host_only():
+    _ensure_built()
+    L = wl.lib()
+    out = ctypes.c_uint64(0)
+    assert L.wl_verify_workspace_size(None, ctypes.byref(out)) == wl.WL_EINVAL
+    s = _csr(1000, 5000)
+    assert L.wl_verify_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    unweighted = out.value
+    # 4 bytes per entry (sorted neighbour colours) plus per-node arrays
+    assert 4 * 5000 + 13 * 1000 <= unweighted < 4 * 5000 + 40 * 1000
+    s.weight = 8
+    assert L.wl_verify_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    assert out.value >= unweighted + 4 * 5000 - 256  # alignment of the regions
+
+
 def test_host_side_errors():
     _ensure_built()
     L = wl.lib()
