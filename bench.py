@@ -129,8 +129,8 @@ def make_graph(name, device):
         rp = g.row_ptr
         if g.nnz < 2**31 and name != "rmat27":
             rp = rp.to(torch.int32)
-        return wl.Graph(g.n, rp, g.col), g
-    return wl.Graph.from_numpy(g.n, g.row_ptr, g.col, device=device), g
+        return wl.Graph(g.n, rp, g.col, symmetric=True), g
+    return wl.Graph.from_numpy(g.n, g.row_ptr, g.col, device=device, symmetric=True), g
 
 
 def cpu_baseline(dg, seconds_target=15.0):

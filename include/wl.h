@@ -38,7 +38,9 @@
  *   - Preconditions checked on the host: n < 2^32, nnz consistent with the
  *     row pointer, non-NULL pointers where required.  Set the environment
  *     variable WL_VALIDATE=1 to also check, on the device, that row pointers
- *     are non-decreasing and every column index is < n (costs one pass).
+ *     are non-decreasing and every column index is < n (costs one pass), and
+ *     for a graph flagged WL_CSR_SYMMETRIC that the multisets of entries
+ *     (i, j) and (j, i) agree (compared through sums of 64-bit hashes).
  *   - Row sums of the weights must stay below p (true for every graph with
  *     uint32 weights and fewer than 2^29 entries per row, and preserved by
  *     quotients).
@@ -65,7 +67,19 @@ extern "C" {
  * n+1 entries, row_ptr[0] == 0 and row_ptr[n] == nnz.  col_idx has nnz
  * entries, each < n.  weight is NULL (every entry weighs 1) or has nnz
  * entries (a_ij in N_0; weighted graphs arise as quotients).  Whether the
- * pointers are device or host memory is stated per entry point. */
+ * pointers are device or host memory is stated per entry point.
+ * flags: WL_CSR_SYMMETRIC states that A equals its transpose (every entry
+ * (i, j) has a matching entry (j, i), multiplicities included), as for the
+ * CSR of an undirected graph stored in both directions.  For an unweighted
+ * symmetric graph with fewer than 2^32 entries the in-core entry points may
+ * then compute A w by routing each row's value to its neighbours through
+ * LDS-sized bins (streaming passes) instead of one random read per entry;
+ * this needs the larger workspace wl_workspace_size() reports for such a
+ * graph (about 8 bytes more per entry) and is skipped when the workspace is
+ * smaller.  A graph flagged symmetric that is not is reported as WL_EINVAL
+ * when the library notices (it checks the entry counts per bin of rows;
+ * results are defined only for correctly flagged graphs). */
+#define WL_CSR_SYMMETRIC 1ull
 typedef struct wl_csr {
     uint64_t n;
     uint64_t nnz;
@@ -73,11 +87,13 @@ typedef struct wl_csr {
     const uint64_t *row_ptr64;
     const uint32_t *col_idx;
     const uint32_t *weight;
+    uint64_t flags;
 } wl_csr;
 
 /* Workspace (device bytes) needed by the in-core entry points
  * (wl_refine_round, wl_stable_coloring) for graph g.
- * Only g->n and g->nnz are read; the pointers may be NULL.
+ * Only g->n, g->nnz, g->flags and whether g->weight is NULL are read; the
+ * pointers may be NULL otherwise.
  * Returns WL_EINVAL for a NULL argument, WL_EOVERFLOW for n >= 2^32. */
 int wl_workspace_size(const wl_csr *g, uint64_t *bytes_out);
 

@@ -54,10 +54,14 @@ class WlStats(ctypes.Structure):
         return {f: getattr(self, f) for f, _ in self._fields_}
 
 
+WL_CSR_SYMMETRIC = 1
+
+
 class WlCsr(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint64), ("nnz", ctypes.c_uint64),
                 ("row_ptr32", ctypes.c_void_p), ("row_ptr64", ctypes.c_void_p),
-                ("col_idx", ctypes.c_void_p), ("weight", ctypes.c_void_p)]
+                ("col_idx", ctypes.c_void_p), ("weight", ctypes.c_void_p),
+                ("flags", ctypes.c_uint64)]
 
 
 _LIB = None
@@ -109,11 +113,13 @@ class Graph:
     """CSR adjacency whose arrays live in torch tensors (device or host).
 
     row_ptr: int32/int64 tensor of n+1 entries (values read as uint32/uint64);
-    col_idx: int32 tensor (uint32 values); weight: None or int32 (uint32).
+    col_idx: int32 tensor (uint32 values); weight: None or int32 (uint32);
+    symmetric: the caller states that A equals its transpose (WL_CSR_SYMMETRIC).
     """
 
-    def __init__(self, n, row_ptr, col_idx, weight=None):
+    def __init__(self, n, row_ptr, col_idx, weight=None, symmetric=False):
         self.n = int(n)
+        self.symmetric = bool(symmetric)
         self.row_ptr = row_ptr.contiguous()
         self.col_idx = col_idx.contiguous()
         self.weight = None if weight is None else weight.contiguous()
@@ -143,10 +149,11 @@ class Graph:
         s.row_ptr64 = rp if self.row_ptr.dtype == torch.int64 else None
         s.col_idx = self.col_idx.data_ptr() if self.nnz else None
         s.weight = None if self.weight is None else self.weight.data_ptr()
+        s.flags = WL_CSR_SYMMETRIC if self.symmetric else 0
         return s
 
     @classmethod
-    def from_numpy(cls, n, row_ptr, col, weight=None, device="cuda"):
+    def from_numpy(cls, n, row_ptr, col, weight=None, device="cuda", symmetric=False):
         import numpy as np
         rp = np.ascontiguousarray(row_ptr)
         if rp.dtype in (np.uint64, np.int64):
@@ -159,7 +166,7 @@ class Graph:
         if device is not None:
             rp_t, col_t = rp_t.to(device), col_t.to(device)
             w_t = None if w_t is None else w_t.to(device)
-        return cls(n, rp_t, col_t, w_t)
+        return cls(n, rp_t, col_t, w_t, symmetric)
 
 
 def wl_workspace_size(g):

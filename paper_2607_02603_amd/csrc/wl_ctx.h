@@ -50,6 +50,8 @@ struct DevState {
   unsigned long long work_rows;     // diagnostics: rows the SpMV computed
   unsigned long long work_entries;  // diagnostics: entries it gathered
   unsigned long long work_uniform;  // diagnostics: rows of the 1-colour path
+  unsigned long long act_entries;   // entries of the rows whose image is needed
+  unsigned long long sym_hash[2];   // validation: hashes of (i, j) and (j, i)
 };
 
 struct HeavyChunk {

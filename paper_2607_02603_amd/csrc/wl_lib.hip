@@ -24,6 +24,7 @@
 #include "wl_ctx.h"
 #include "wl_relabel.h"
 #include "wl_spmv.h"
+#include "wl_push.h"
 #include "wl_quotient.h"
 #include "wl_verify.h"
 
@@ -115,6 +116,69 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_c16 = take(2 * n);
   L.total = o;
   return L;
+}
+
+// Workspace of the propagation-blocking image (symmetric unweighted graphs
+// with fewer than 2^32 entries), placed after the in-core layout.  Offsets
+// are relative to its start.
+struct PbLayout {
+  bool ok = false;
+  uint32_t levels = 0, shift1 = 0, nb1 = 0, nfine = 0, fbits = 0;
+  uint64_t ntiles1 = 0;
+  uint64_t cnt = 0, bstart1 = 0, bstartf = 0, rec1 = 0, rec2 = 0, table = 0, gsum = 0,
+           tile_row = 0, tile2_off = 0, cur2 = 0, slice_off = 0, mslice_off = 0, mlist = 0,
+           part = 0;
+  uint64_t total = 0;
+};
+
+PbLayout make_pb_layout(uint64_t n, uint64_t nnz) {
+  PbLayout P{};
+  if (n == 0 || nnz == 0 || nnz >= (1ull << 32) || n >= (1ull << 32) - (1ull << 16)) return P;
+  const uint64_t nf = (n + kPbFineRows - 1) >> kPbFineShift;
+  P.nfine = (uint32_t)nf;
+  if (nf <= kPbMaxBins) {
+    P.levels = 1;
+    P.shift1 = kPbFineShift;
+  } else {
+    uint32_t fb = 0;
+    while (((nf + (1ull << fb) - 1) >> fb) > kPbMaxBins) ++fb;
+    if ((1u << fb) > kPbMaxFine) return P;  // pass 2 splits a coarse bin at most this far
+    P.levels = 2;
+    P.fbits = fb;
+    P.shift1 = kPbFineShift + fb;
+  }
+  P.nb1 = (uint32_t)((n + (1ull << P.shift1) - 1) >> P.shift1);
+  P.ntiles1 = (nnz + kPbTile - 1) / kPbTile;
+  // slices of the bins cut into several: each holds more than kPbSlice
+  // records, so together fewer than 2 * nnz / kPbSlice
+  const uint64_t mslots = 2 * ((nnz + kPbSlice - 1) / kPbSlice) + 1;
+  uint64_t o = 0;
+  auto take = [&](uint64_t bytes) {
+    uint64_t at = o;
+    o = align_up(o + bytes);
+    return at;
+  };
+  P.cnt = take(sizeof(PbCounts));
+  P.bstart1 = take(8ull * (P.nb1 + 1));
+  P.bstartf = take(8 * (nf + 1));
+  P.rec1 = take(P.levels == 2 ? 4 * nnz : 0);
+  P.rec2 = take(4 * nnz);
+  P.table = take(4 * P.ntiles1 * P.nb1);
+  P.gsum = take(4ull * kPbGroups * P.nb1);
+  P.tile_row = take(4 * P.ntiles1);
+  P.tile2_off = take(4ull * (P.nb1 + 1));
+  P.cur2 = take(8 * nf);
+  P.slice_off = take(4 * (nf + 1));
+  P.mslice_off = take(4 * (nf + 1));
+  P.mlist = take(4 * nf);
+  P.part = take(8ull * kPbFineRows * mslots);
+  P.total = o;
+  P.ok = true;
+  return P;
+}
+
+bool wants_pb(const wl_csr* g) {
+  return (g->flags & WL_CSR_SYMMETRIC) && g->weight == nullptr;
 }
 
 Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
@@ -227,6 +291,25 @@ __global__ void __launch_bounds__(kBlock) k_validate(Ctx ctx) {
     if (ctx.col[e] >= ctx.n) atomicOr(&ctx.st->err, 2u);
 }
 
+// Symmetry of a graph flagged WL_CSR_SYMMETRIC (validation only): the sums
+// over all entries of a 64-bit hash of (row, column) and of (column, row)
+// agree exactly when the two multisets of entries are equal, up to a hash
+// collision.
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_validate_sym(Ctx ctx) {
+  const RP* rp = rowptr<RP>(ctx);
+  unsigned long long f = 0, b = 0;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n; i += gridDim.x * kBlock)
+    for (uint64_t e = rp[i]; e < rp[i + 1]; ++e) {
+      const uint64_t j = ctx.col[e];
+      const uint64_t w = ctx.wgt ? ctx.wgt[e] : 1u;
+      f += mix64(mix64(((uint64_t)i << 32) | j) + w);
+      b += mix64(mix64((j << 32) | i) + w);
+    }
+  atomicAdd(&ctx.st->sym_hash[0], f);
+  atomicAdd(&ctx.st->sym_hash[1], b);
+}
+
 __global__ void __launch_bounds__(kBlock) k_check_colors(Ctx ctx,
                                                          const uint32_t* col,
                                                          uint32_t k) {
@@ -317,6 +400,17 @@ struct Session {
   hipStream_t s;
   bool rp64;
   bool weighted;
+  // Propagation blocking (symmetric graphs): available when the workspace
+  // holds its layout; planned at its first use; stopped for the rest of the
+  // call once fewer than half of the entries feed rows whose image is needed
+  // (that fraction never grows).  WL_PB=0 turns it off, WL_PB=force uses it
+  // in every round it can serve (for testing).
+  PbLayout P;
+  PbCtx pb{};
+  PbCounts pbc{};
+  bool pb_avail = false, pb_planned = false, pb_stop = false;
+  bool sym_flag = false;
+  int pb_mode = 1;
   DevState host;      // last copy of the device state
   DevState init_src;  // source of the initial state copy
   uint32_t nscan;
@@ -448,6 +542,16 @@ struct Session {
     if (int r = pull()) return r;
     if (host.err & 1u) return fail(WL_EINVAL, "row_ptr is not non-decreasing");
     if (host.err & 2u) return fail(WL_EINVAL, "a column index is >= n");
+    if (sym_flag) {
+      if (rp64)
+        hipLaunchKernelGGL(k_validate_sym<uint64_t>, dim3(grid_for(L.n)), dim3(kBlock), 0, s, ctx);
+      else
+        hipLaunchKernelGGL(k_validate_sym<uint32_t>, dim3(grid_for(L.n)), dim3(kBlock), 0, s, ctx);
+      HIP_LAUNCH_CHECK();
+      if (int r = pull()) return r;
+      if (host.sym_hash[0] != host.sym_hash[1])
+        return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
+    }
     return WL_OK;
   }
 
@@ -485,23 +589,109 @@ struct Session {
     hipLaunchKernelGGL((k_spmv<RP, W, M>), dim3(g.b0), dim3(kBlock), 0, s, ctx, g);
   }
 
+  // Plan of the propagation-blocking image (once per call).
+  template <typename RP>
+  int pb_plan() {
+    hipLaunchKernelGGL(k_pb_bin_starts<RP>, dim3(grid_for(P.nfine + 1)), dim3(kBlock), 0, s,
+                       ctx, pb);
+    hipLaunchKernelGGL(k_pb_tile_rows<RP>, dim3(grid_for(L.n, kBlock, 8192)), dim3(kBlock), 0, s,
+                       ctx, pb);
+    hipLaunchKernelGGL(k_pb_hist1, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 4096)),
+                       dim3(kPbThreads), 0, s, ctx, pb);
+    hipLaunchKernelGGL(k_pb_colsum, dim3(kPbGroups), dim3(kPbThreads), 0, s, pb);
+    hipLaunchKernelGGL(k_pb_colscan<RP>, dim3(1), dim3(kPbThreads), 0, s, ctx, pb);
+    hipLaunchKernelGGL(k_pb_colapply, dim3(kPbGroups), dim3(kPbThreads), 0, s, pb);
+    hipLaunchKernelGGL(k_pb_lists<RP>, dim3(1), dim3(kPbThreads), 0, s, ctx, pb);
+    HIP_LAUNCH_CHECK();
+    HIP_TRY(hipMemcpyAsync(&pbc, pb.cnt, sizeof(PbCounts), hipMemcpyDeviceToHost, s));
+    if (int r = pull()) return r;
+    if (host.err & kErrNotSymmetric)
+      return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
+    pb_planned = true;
+    return WL_OK;
+  }
+
+  // Whether this round's image goes through propagation blocking: the colour
+  // must fit next to the destination in a 32-bit record, and (unless forced)
+  // the graph must be large and at least half of its entries must feed rows
+  // whose image is needed.
+  template <typename RP>
+  int pb_wanted(bool* use) {
+    *use = false;
+    if (!pb_avail || pb_stop || host.k < 2) return WL_OK;
+    const uint32_t cbits = 32 - (uint32_t)__builtin_clz(host.k - 1);
+    if (P.shift1 + cbits > 32) return WL_OK;
+    if (pb_mode == 1) {
+      if (L.nnz < kPbMinEntries) {
+        pb_stop = true;
+        return WL_OK;
+      }
+      hipLaunchKernelGGL(k_count_active<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
+                         s, ctx);
+      HIP_LAUNCH_CHECK();
+      if (int r = pull()) return r;
+      if (host.act_entries * 2 < L.nnz) {
+        pb_stop = true;
+        return WL_OK;
+      }
+    }
+    pb.cbits = cbits;
+    *use = true;
+    return WL_OK;
+  }
+
+  template <typename RP>
+  int pb_round() {
+    if (!pb_planned)
+      if (int r = pb_plan<RP>()) return r;
+    if (sflags & WL_STATS_WORK)
+      hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
+                         ctx, 1);
+    timed_spmv(host.round, true, false, [&] {
+      hipLaunchKernelGGL(k_pb_scatter1<RP>, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 2048)),
+                         dim3(kPbThreads), 0, s, ctx, pb);
+      if (P.levels == 2) {
+        hipLaunchKernelGGL(k_pb_cursors, dim3(grid_for(P.nfine)), dim3(kBlock), 0, s, ctx,
+                           pb);
+        hipLaunchKernelGGL(k_pb_scatter2, dim3(std::max<uint32_t>(1, std::min<uint32_t>(pbc.ntiles2, 2048))),
+                           dim3(kPbThreads), 0, s, ctx, pb);
+      }
+      const dim3 ga(std::max<uint32_t>(1, std::min<uint32_t>(pbc.nslices, 2048)));
+      if (host.k <= kPbTableMax)
+        hipLaunchKernelGGL((k_pb_accum<RP, true>), ga, dim3(kPbAccThreads), 0, s, ctx, pb);
+      else
+        hipLaunchKernelGGL((k_pb_accum<RP, false>), ga, dim3(kPbAccThreads), 0, s, ctx, pb);
+      if (pbc.nmulti)
+        hipLaunchKernelGGL(k_pb_combine,
+                           dim3(grid_for((uint64_t)pbc.nmulti * kPbFineRows, kBlock, 8192)),
+                           dim3(kBlock), 0, s, ctx, pb);
+    });
+    HIP_LAUNCH_CHECK();
+    return WL_OK;
+  }
+
   template <typename RP, bool W>
-  void spmv_t() {
+  int spmv_t() {
     const DevState& h = host;
     const bool uniform = !W && h.k == 1 && !ctx.batch;
+    if (!W && !uniform && !ctx.batch) {
+      bool use = false;
+      if (int r = pb_wanted<RP>(&use)) return r;
+      if (use) return pb_round<RP>();
+    }
     SpmvGrid g;
     g.heavy = h.n_chunks ? grid_for(h.n_chunks, kBlock / kWave) : 0;
     g.b2 = g.heavy + (h.bin_cnt[2] ? grid_for(h.bin_cnt[2], kBlock / 64) : 0);
     g.b1 = g.b2 + (h.bin_cnt[1] ? grid_for(h.bin_cnt[1], kBlock / 16) : 0);
     g.b0 = g.b1 + (h.bin_cnt[0] ? grid_for(h.bin_cnt[0], kBlock / 4) : 0);
-    if (g.b0 == 0) return;
+    if (g.b0 == 0) return WL_OK;
     const int mode = gather_mode(h.k);
     if (!uniform)
       hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock),
                          0, s, ctx, mode);
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
-                         dim3(kBlock), 0, s, ctx);
+                         dim3(kBlock), 0, s, ctx, 0);
     timed_spmv(h.round, true, uniform, [&] {
       if (uniform)
         hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
@@ -513,14 +703,12 @@ struct Session {
       else
         spmv_launch<RP, W, kGatherX>(g);
     });
+    return WL_OK;
   }
 
-  void spmv() {
-    if (rp64) {
-      if (weighted) spmv_t<uint64_t, true>(); else spmv_t<uint64_t, false>();
-    } else {
-      if (weighted) spmv_t<uint32_t, true>(); else spmv_t<uint32_t, false>();
-    }
+  int spmv() {
+    if (rp64) return weighted ? spmv_t<uint64_t, true>() : spmv_t<uint64_t, false>();
+    return weighted ? spmv_t<uint32_t, true>() : spmv_t<uint32_t, false>();
   }
 
   // SpMV of a round launched without reading the state back: the gather
@@ -538,7 +726,7 @@ struct Session {
                        ctx, -1);
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
-                         dim3(kBlock), 0, s, ctx);
+                         dim3(kBlock), 0, s, ctx, 0);
     timed_spmv(round, false, false, [&] {
       hipLaunchKernelGGL((k_spmv_dyn<RP, W>), dim3(g.b0), dim3(kBlock), 0, s, ctx, g);
     });
@@ -690,9 +878,12 @@ struct Session {
 
   int round() {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
-    spmv();
+    if (int r = spmv()) return r;
     HIP_LAUNCH_CHECK();
-    return relabel(1);
+    if (int r = relabel(1)) return r;
+    if (host.err & kErrNotSymmetric)
+      return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
+    return WL_OK;
   }
 };
 
@@ -713,6 +904,40 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
   S.nscan = scan_blocks(g->n);
   S.host_rounds_first = (uint32_t)env_int("WL_HOST_ROUNDS", 0, 1 << 30, (int)kHostRounds);
   S.async_passes = env_int("WL_ASYNC_PASSES", 0, kPasses, kAsyncPassesDefault);
+  {
+    const char* m = getenv("WL_PB");
+    S.pb_mode = !m ? 1 : (strcmp(m, "0") == 0 ? 0 : (strcmp(m, "force") == 0 ? 2 : 1));
+  }
+  S.sym_flag = (g->flags & WL_CSR_SYMMETRIC) != 0;
+  if (wants_pb(g) && S.pb_mode != 0) {
+    S.P = make_pb_layout(g->n, g->nnz);
+    // pass 1 reads the column indices 16 bytes at a time
+    if (S.P.ok && ws_bytes >= S.L.total + S.P.total && (uintptr_t)g->col_idx % 16 == 0) {
+      uint8_t* B = (uint8_t*)ws + S.L.total;
+      PbCtx& p = S.pb;
+      p.levels = S.P.levels;
+      p.shift1 = S.P.shift1;
+      p.nb1 = S.P.nb1;
+      p.nfine = S.P.nfine;
+      p.fbits = S.P.fbits;
+      p.ntiles1 = S.P.ntiles1;
+      p.cnt = (PbCounts*)(B + S.P.cnt);
+      p.bstart1 = (uint64_t*)(B + S.P.bstart1);
+      p.bstartf = (uint64_t*)(B + S.P.bstartf);
+      p.rec1 = (uint32_t*)(B + S.P.rec1);
+      p.rec2 = (uint32_t*)(B + S.P.rec2);
+      p.table = (uint32_t*)(B + S.P.table);
+      p.gsum = (uint32_t*)(B + S.P.gsum);
+      p.tile_row = (uint32_t*)(B + S.P.tile_row);
+      p.tile2_off = (uint32_t*)(B + S.P.tile2_off);
+      p.cur2 = (unsigned long long*)(B + S.P.cur2);
+      p.slice_off = (uint32_t*)(B + S.P.slice_off);
+      p.mslice_off = (uint32_t*)(B + S.P.mslice_off);
+      p.mlist = (uint32_t*)(B + S.P.mlist);
+      p.part = (uint64_t*)(B + S.P.part);
+      S.pb_avail = true;
+    }
+  }
   return WL_OK;
 }
 
@@ -1501,7 +1726,12 @@ int wl_workspace_size(const wl_csr* g, uint64_t* bytes_out) {
   g_err[0] = 0;
   if (!g || !bytes_out) return fail(WL_EINVAL, "NULL argument");
   if (g->n >= (1ull << 32)) return fail(WL_EOVERFLOW, "n does not fit 32 bits");
-  *bytes_out = make_layout(g->n, g->nnz).total;
+  uint64_t bytes = make_layout(g->n, g->nnz).total;
+  if (wants_pb(g)) {
+    const PbLayout P = make_pb_layout(g->n, g->nnz);
+    if (P.ok) bytes += P.total;
+  }
+  *bytes_out = bytes;
   return WL_OK;
 }
 

@@ -1,0 +1,618 @@
+// Step "z = A w" of Algorithm 1 for a symmetric A by propagation blocking.
+//
+// The gathering SpMV reads one value per entry at a random node, which costs
+// a whole cache line per entry on graphs whose node order has no locality.
+// When A is symmetric, the rows that hold node j are exactly the entries of
+// row j, so every row can instead send its colour to its neighbours, and the
+// traffic can be made sequential by routing the messages through bins of
+// destination rows:
+//   pass 1  stream the CSR entries in order; each tile of kPbTile entries
+//           turns them into records (destination row inside its bin, colour
+//           of the source row), counting-sorts them by bin in LDS and writes
+//           one run per bin, at an offset computed once per call;
+//   pass 2  only when there are more than kPbMaxBins fine bins: pass 1 used
+//           coarse bins of 2^fbits fine bins each; every coarse bin is split
+//           into its fine bins the same way (run offsets from atomics);
+//   pass 3  one workgroup per fine bin of kPbFineRows rows, or per slice of
+//           at most kPbSlice records of a larger one, adds W(colour) of its
+//           records into per-row accumulators in LDS; single-slice bins
+//           write z, the partial sums of the others are added by a last
+//           kernel.
+// For symmetric A, the records bound for rows [a, b) number rp[b] - rp[a],
+// so every bin occupies the entry range of its rows in the CSR layout.  The
+// accumulators are exact (two 64-bit sums of the 32-bit halves of canonical
+// residues per row) and every sum is reduced mod p at the end, so the image
+// does not depend on the order in which records arrive.
+#pragma once
+#include "wl_spmv.h"
+
+namespace wl {
+
+constexpr int kPbFineShift = 13;
+constexpr uint32_t kPbFineRows = 1u << kPbFineShift;  // rows per fine bin
+constexpr uint32_t kPbMaxBins = 256;                  // bins of pass 1
+constexpr uint32_t kPbMaxFine = 512;                  // fine bins per coarse bin
+constexpr uint32_t kPbTile = 8192;                    // entries per pass-1 tile
+constexpr uint32_t kPbTile2 = 8192;                   // records per pass-2 tile
+constexpr uint32_t kPbSlice = 1u << 20;               // records per pass-3 item
+constexpr int kPbThreads = 256;                       // pass 1 and 2
+constexpr int kPbAccThreads = 1024;                   // pass 3
+constexpr uint32_t kPbGroups = 1024;                  // groups of the table scan
+constexpr uint32_t kPbPerThread = kPbTile / kPbThreads;
+constexpr uint32_t kErrNotSymmetric = 16u;  // DevState::err bit
+constexpr uint64_t kPbMinEntries = 1ull << 22;  // smaller graphs stay in cache
+
+// Device-side counts of the plan (read by the host once per call).
+struct PbCounts {
+  uint32_t ntiles2;   // pass-2 tiles
+  uint32_t nslices;   // pass-3 work items
+  uint32_t nmulti;    // fine bins with several slices
+  uint32_t mslices;   // slices of those bins
+};
+
+struct PbCtx {
+  uint32_t levels;     // 1: pass 1 writes fine bins; 2: coarse bins, then pass 2
+  uint32_t shift1;     // log2 of the rows of a pass-1 bin
+  uint32_t nb1;        // pass-1 bins
+  uint32_t nfine;      // fine bins
+  uint32_t fbits;      // log2 of the fine bins per coarse bin (levels == 2)
+  uint32_t cbits;      // bits of the colour in a record
+  uint64_t ntiles1;    // pass-1 tiles
+  uint64_t* bstart1;   // nb1 + 1: first entry of the rows of each pass-1 bin
+  uint64_t* bstartf;   // nfine + 1: the same for the fine bins
+  uint32_t* rec1;      // pass-1 records (coarse bins; levels == 2)
+  uint32_t* rec2;      // fine-bin records
+  uint32_t* table;     // ntiles1 x nb1: start of each tile's run inside its bin
+  uint32_t* gsum;      // kPbGroups x nb1: scan scratch
+  uint32_t* tile_row;  // ntiles1: row that holds the first entry of each tile
+  uint32_t* tile2_off; // nb1 + 1: pass-2 tiles before each coarse bin
+  unsigned long long* cur2;  // nfine: write cursors of pass 2
+  uint32_t* slice_off;       // nfine + 1: pass-3 items before each fine bin
+  uint32_t* mslice_off;      // nfine + 1: partial-sum slots before each bin
+  uint32_t* mlist;           // fine bins with several slices
+  uint64_t* part;            // partial images, kPbFineRows per slot
+  PbCounts* cnt;
+};
+
+template <typename RP>
+__device__ __forceinline__ uint64_t rp_at(const Ctx& c, uint64_t i) {
+  return (uint64_t)rowptr<RP>(c)[i];
+}
+
+// Start of the entry range of the rows [b << shift, ...) (clamped to n).
+template <typename RP>
+__device__ __forceinline__ uint64_t bin_start(const Ctx& c, uint64_t b, uint32_t shift) {
+  const uint64_t r = b << shift;
+  return rp_at<RP>(c, r < c.n ? r : c.n);
+}
+
+// Exclusive scan over a block of kPbThreads (or kPbAccThreads) threads.
+template <int T>
+__device__ __forceinline__ uint32_t pb_block_scan(uint32_t v, uint32_t* sh, uint32_t* total) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const uint32_t inc = wave_incl_scan(v);
+  if (lane == kWave - 1) sh[wid] = inc;
+  __syncthreads();
+  uint32_t base = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < T / kWave; ++w) {
+    const uint32_t s = sh[w];
+    if (w < wid) base += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return base + inc - v;
+}
+
+// ---------------------------------------------------------------------------
+// Plan (once per call; depends on the graph only)
+// ---------------------------------------------------------------------------
+
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_pb_bin_starts(Ctx ctx, PbCtx pb) {
+  for (uint32_t b = blockIdx.x * kBlock + threadIdx.x; b <= pb.nfine; b += gridDim.x * kBlock) {
+    pb.bstartf[b] = bin_start<RP>(ctx, b, kPbFineShift);
+    if (b <= pb.nb1) pb.bstart1[b] = bin_start<RP>(ctx, b, pb.shift1);
+  }
+}
+
+// tile_row[t] = the row holding entry t * kPbTile.
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_pb_tile_rows(Ctx ctx, PbCtx pb) {
+  for (uint32_t r = blockIdx.x * kBlock + threadIdx.x; r < ctx.n; r += gridDim.x * kBlock) {
+    const uint64_t b = rp_at<RP>(ctx, r), e = rp_at<RP>(ctx, r + 1);
+    if (e <= b) continue;
+    for (uint64_t t = (b + kPbTile - 1) / kPbTile; t * kPbTile < e; ++t) pb.tile_row[t] = r;
+  }
+}
+
+// Records of every pass-1 tile per bin.
+__global__ void __launch_bounds__(kPbThreads) k_pb_hist1(Ctx ctx, PbCtx pb) {
+  __shared__ uint32_t h[kPbMaxBins];
+  for (uint64_t t = blockIdx.x; t < pb.ntiles1; t += gridDim.x) {
+    for (uint32_t b = threadIdx.x; b < pb.nb1; b += kPbThreads) h[b] = 0;
+    __syncthreads();
+    const uint64_t e0 = t * kPbTile, e1 = min(ctx.nnz, e0 + kPbTile);
+    uint32_t v[kPbTile / kPbThreads];
+#pragma unroll
+    for (uint32_t k = 0; k < kPbTile / kPbThreads; ++k) {
+      const uint64_t e = e0 + k * kPbThreads + threadIdx.x;
+      v[k] = e < e1 ? ctx.col[e] : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (uint32_t k = 0; k < kPbTile / kPbThreads; ++k)
+      if (v[k] != 0xFFFFFFFFu) atomicAdd(&h[v[k] >> pb.shift1], 1u);
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < pb.nb1; b += kPbThreads) pb.table[t * pb.nb1 + b] = h[b];
+    __syncthreads();
+  }
+}
+
+__device__ __forceinline__ void pb_group_range(const PbCtx& pb, uint32_t g, uint64_t* lo,
+                                               uint64_t* hi) {
+  const uint64_t per = (pb.ntiles1 + kPbGroups - 1) / kPbGroups;
+  *lo = min(pb.ntiles1, (uint64_t)g * per);
+  *hi = min(pb.ntiles1, *lo + per);
+}
+
+// Column sums of the table per group of tiles.
+__global__ void __launch_bounds__(kPbThreads) k_pb_colsum(PbCtx pb) {
+  const uint32_t b = threadIdx.x;
+  if (b >= pb.nb1) return;
+  uint64_t lo, hi;
+  pb_group_range(pb, blockIdx.x, &lo, &hi);
+  uint32_t s = 0;
+  for (uint64_t t = lo; t < hi; ++t) s += pb.table[t * pb.nb1 + b];
+  pb.gsum[blockIdx.x * pb.nb1 + b] = s;
+}
+
+// Exclusive scan of the group sums per bin.  The records bound for a bin
+// must fill exactly the entry range of its rows, which holds for a
+// symmetric A; a mismatch proves A is not symmetric and sets an error bit
+// (no record is written then).
+template <typename RP>
+__global__ void __launch_bounds__(kPbThreads) k_pb_colscan(Ctx ctx, PbCtx pb) {
+  const uint32_t b = threadIdx.x;
+  if (b >= pb.nb1) return;
+  uint64_t run = 0;
+  for (uint32_t g = 0; g < kPbGroups; ++g) {
+    const uint32_t v = pb.gsum[g * pb.nb1 + b];
+    pb.gsum[g * pb.nb1 + b] = (uint32_t)run;
+    run += v;
+  }
+  if (run != pb.bstart1[b + 1] - pb.bstart1[b]) atomicOr(&ctx.st->err, kErrNotSymmetric);
+}
+
+// table[t][b] = records of bin b in tiles before t (offset inside the bin).
+__global__ void __launch_bounds__(kPbThreads) k_pb_colapply(PbCtx pb) {
+  const uint32_t b = threadIdx.x;
+  if (b >= pb.nb1) return;
+  uint64_t lo, hi;
+  pb_group_range(pb, blockIdx.x, &lo, &hi);
+  uint32_t run = pb.gsum[blockIdx.x * pb.nb1 + b];
+  for (uint64_t t = lo; t < hi; ++t) {
+    const uint32_t v = pb.table[t * pb.nb1 + b];
+    pb.table[t * pb.nb1 + b] = run;
+    run += v;
+  }
+}
+
+// One block: pass-2 tiles per coarse bin, pass-3 slices per fine bin, and
+// the list of fine bins with several slices.
+template <typename RP>
+__global__ void __launch_bounds__(kPbThreads) k_pb_lists(Ctx ctx, PbCtx pb) {
+  __shared__ uint32_t sh[kPbThreads / kWave];
+  uint32_t carry = 0;
+  if (pb.levels == 2) {
+    for (uint32_t base = 0; base < pb.nb1; base += kPbThreads) {
+      const uint32_t b = base + threadIdx.x;
+      uint32_t nt = 0;
+      if (b < pb.nb1) {
+        const uint64_t sz = pb.bstart1[b + 1] - pb.bstart1[b];
+        nt = (uint32_t)((sz + kPbTile2 - 1) / kPbTile2);
+      }
+      uint32_t tot;
+      const uint32_t ex = pb_block_scan<kPbThreads>(nt, sh, &tot);
+      if (b < pb.nb1) pb.tile2_off[b] = carry + ex;
+      carry += tot;
+    }
+    if (threadIdx.x == 0) {
+      pb.tile2_off[pb.nb1] = carry;
+      pb.cnt->ntiles2 = carry;
+    }
+  }
+  uint32_t sc = 0, mc = 0, nm = 0;
+  for (uint32_t base = 0; base < pb.nfine; base += kPbThreads) {
+    const uint32_t f = base + threadIdx.x;
+    uint32_t ns = 0;
+    if (f < pb.nfine) {
+      const uint64_t sz = pb.bstartf[f + 1] - pb.bstartf[f];
+      ns = sz <= kPbSlice ? 1u : (uint32_t)((sz + kPbSlice - 1) / kPbSlice);
+    }
+    uint32_t tot, mtot, ntot;
+    const uint32_t ex = pb_block_scan<kPbThreads>(ns, sh, &tot);
+    const uint32_t mex = pb_block_scan<kPbThreads>(ns > 1 ? ns : 0u, sh, &mtot);
+    const uint32_t nex = pb_block_scan<kPbThreads>(ns > 1 ? 1u : 0u, sh, &ntot);
+    if (f < pb.nfine) {
+      pb.slice_off[f] = sc + ex;
+      pb.mslice_off[f] = mc + mex;
+      if (ns > 1) pb.mlist[nm + nex] = f;
+    }
+    sc += tot;
+    mc += mtot;
+    nm += ntot;
+  }
+  if (threadIdx.x == 0) {
+    pb.slice_off[pb.nfine] = sc;
+    pb.mslice_off[pb.nfine] = mc;
+    pb.cnt->nslices = sc;
+    pb.cnt->nmulti = nm;
+    pb.cnt->mslices = mc;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 1: CSR entries -> records in pass-1 bins
+// ---------------------------------------------------------------------------
+
+template <typename RP>
+__global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
+  if (ctx.st->done) return;
+  __shared__ __align__(16) uint32_t buf[kPbTile];  // colour+1 at row starts, colours, records
+  __shared__ uint8_t sbin[kPbTile];                // bin of each staged record
+  __shared__ uint32_t hist[kPbMaxBins];
+  __shared__ uint32_t base[kPbMaxBins];
+  __shared__ uint64_t dst[kPbMaxBins];  // output position of the tile's run per bin
+  __shared__ uint32_t wlast[kPbThreads / kWave];
+  __shared__ uint32_t sh[kPbThreads / kWave];
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const uint32_t mask1 = (1u << pb.shift1) - 1;
+  uint32_t* out = pb.levels == 2 ? pb.rec1 : pb.rec2;
+  const uint4* col4 = (const uint4*)ctx.col;
+  // rows of the next tile, loaded one tile ahead
+  uint32_t j0n = 0, jendn = 0;
+  if (blockIdx.x < pb.ntiles1) {
+    j0n = pb.tile_row[blockIdx.x];
+    jendn = blockIdx.x + 1 < pb.ntiles1 ? pb.tile_row[blockIdx.x + 1] : ctx.n - 1;
+  }
+  for (uint64_t t = blockIdx.x; t < pb.ntiles1; t += gridDim.x) {
+    const uint64_t e0 = t * kPbTile, e1 = min(ctx.nnz, e0 + kPbTile);
+    const uint32_t cnt = (uint32_t)(e1 - e0);
+    const uint32_t j0 = j0n, jend = jendn;
+    // everything the tile reads from memory is requested first: its column
+    // indices (4 consecutive entries per load; slot (k, u) holds entry
+    // 4 * (k * kPbThreads + threadIdx.x) + u), its run offsets, the first
+    // row's colour and one row start per thread
+    uint32_t cix[kPbPerThread];
+    if (cnt == kPbTile) {
+#pragma unroll
+      for (uint32_t k = 0; k < kPbPerThread / 4; ++k) {
+        const uint4 v = col4[(e0 >> 2) + k * kPbThreads + threadIdx.x];
+        cix[4 * k] = v.x;
+        cix[4 * k + 1] = v.y;
+        cix[4 * k + 2] = v.z;
+        cix[4 * k + 3] = v.w;
+      }
+    } else {
+#pragma unroll
+      for (uint32_t k = 0; k < kPbPerThread / 4; ++k)
+#pragma unroll
+        for (uint32_t u = 0; u < 4; ++u) {
+          const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
+          cix[4 * k + u] = q < cnt ? ctx.col[e0 + q] : 0u;
+        }
+    }
+    uint64_t my_dst = 0;
+    if (threadIdx.x < pb.nb1) my_dst = pb.bstart1[threadIdx.x] + pb.table[t * pb.nb1 + threadIdx.x];
+    const uint32_t c_first = ctx.c[j0];
+    const uint32_t r_mine = j0 + 1 + threadIdx.x;
+    uint64_t rb = 0, re = 0;
+    uint32_t rc = 0;
+    if (r_mine <= jend) {
+      rb = rp_at<RP>(ctx, r_mine);
+      re = rp_at<RP>(ctx, r_mine + 1);
+      rc = ctx.c[r_mine];
+    }
+    {
+      const uint64_t tn = t + gridDim.x;
+      if (tn < pb.ntiles1) {
+        j0n = pb.tile_row[tn];
+        jendn = tn + 1 < pb.ntiles1 ? pb.tile_row[tn + 1] : ctx.n - 1;
+      }
+    }
+    for (uint32_t q = threadIdx.x; q < kPbTile; q += kPbThreads) buf[q] = 0;
+    if (threadIdx.x < pb.nb1) {
+      hist[threadIdx.x] = 0;
+      dst[threadIdx.x] = my_dst;
+    }
+    __syncthreads();
+    // colour + 1 at the first entry of every row that starts in the tile
+    if (r_mine <= jend && rb < e1 && re > rb) buf[rb - e0] = rc + 1;
+    for (uint32_t r = r_mine + kPbThreads; r <= jend; r += kPbThreads) {
+      const uint64_t b = rp_at<RP>(ctx, r);
+      if (b < e1 && rp_at<RP>(ctx, r + 1) > b) buf[b - e0] = ctx.c[r] + 1;
+    }
+    __syncthreads();
+    // every entry takes the value of the last row start at or before it,
+    // minus one: per segment of 64 entries, the highest marked lane at or
+    // below each lane (a ballot) supplies the value, else the carry
+    constexpr uint32_t per_wave = kPbTile / (kPbThreads / kWave);
+    const uint32_t w0 = wid * per_wave;
+    const unsigned long long le_mask = ~0ull >> (kWave - 1 - lane);  // lanes <= lane
+    {
+      uint32_t last = 0;
+      for (uint32_t q = 0; q < per_wave; q += kWave) {
+        const uint32_t v = buf[w0 + q + lane];
+        const unsigned long long m = __ballot(v != 0);
+        if (m) last = __shfl(v, 63 - __builtin_clzll(m), kWave);
+      }
+      if (lane == 0) wlast[wid] = last;
+    }
+    __syncthreads();
+    uint32_t carry = c_first + 1;
+    for (int w = 0; w < wid; ++w)
+      if (wlast[w]) carry = wlast[w];
+    for (uint32_t q = 0; q < per_wave; q += kWave) {
+      const uint32_t v = buf[w0 + q + lane];
+      const unsigned long long m = __ballot(v != 0);
+      const unsigned long long mine = m & le_mask;
+      const int src = mine ? 63 - __builtin_clzll(mine) : 0;
+      const uint32_t got = __shfl(v, src, kWave);
+      buf[w0 + q + lane] = (mine ? got : carry) - 1;
+      if (m) carry = __shfl(v, 63 - __builtin_clzll(m), kWave);
+    }
+    __syncthreads();
+    // records and their bins, counted per bin
+    uint32_t bin[kPbPerThread];
+#pragma unroll
+    for (uint32_t k = 0; k < kPbPerThread / 4; ++k) {
+      const uint4 cv = *(const uint4*)&buf[4 * (k * kPbThreads + threadIdx.x)];
+      const uint32_t colour[4] = {cv.x, cv.y, cv.z, cv.w};
+#pragma unroll
+      for (uint32_t u = 0; u < 4; ++u) {
+        const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
+        const uint32_t x = 4 * k + u;
+        bin[x] = 0xFFFFFFFFu;
+        if (q < cnt) {
+          const uint32_t i = cix[x];
+          bin[x] = i >> pb.shift1;
+          cix[x] = ((i & mask1) << pb.cbits) | colour[u];  // the record
+          atomicAdd(&hist[bin[x]], 1u);
+        }
+      }
+    }
+    __syncthreads();
+    {
+      // nb1 <= kPbMaxBins == kPbThreads: one bin per thread
+      const uint32_t b = threadIdx.x;
+      const uint32_t h = b < pb.nb1 ? hist[b] : 0u;
+      uint32_t tot;
+      const uint32_t ex = pb_block_scan<kPbThreads>(h, sh, &tot);
+      if (b < pb.nb1) {
+        base[b] = ex;
+        hist[b] = 0;
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (uint32_t x = 0; x < kPbPerThread; ++x)
+      if (bin[x] != 0xFFFFFFFFu) {
+        const uint32_t slot = base[bin[x]] + atomicAdd(&hist[bin[x]], 1u);
+        buf[slot] = cix[x];
+        sbin[slot] = (uint8_t)bin[x];
+      }
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < cnt; q += kPbThreads) {
+      const uint32_t b = sbin[q];
+      out[dst[b] + (q - base[b])] = buf[q];
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2: coarse bins -> fine bins
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(kBlock) k_pb_cursors(Ctx ctx, PbCtx pb) {
+  if (ctx.st->done) return;
+  for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < pb.nfine; f += gridDim.x * kBlock)
+    pb.cur2[f] = pb.bstartf[f];
+}
+
+__global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
+  if (ctx.st->done) return;
+  __shared__ uint32_t buf[kPbTile2];
+  __shared__ uint16_t sbin[kPbTile2];
+  __shared__ uint32_t hist[kPbMaxFine];
+  __shared__ uint32_t base[kPbMaxFine];
+  __shared__ unsigned long long dst[kPbMaxFine];
+  __shared__ uint32_t sh[kPbThreads / kWave];
+  const uint32_t nf = 1u << pb.fbits;
+  const uint32_t cmask = (1u << pb.cbits) - 1;
+  const uint32_t ntiles = pb.cnt->ntiles2;
+  constexpr uint32_t kPer = kPbTile2 / kPbThreads;
+  for (uint32_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    uint32_t lo = 0, hi = pb.nb1 - 1;  // coarse bin: last b with tile2_off[b] <= t
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) >> 1;
+      if (pb.tile2_off[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const uint32_t cb = lo;
+    const uint64_t rend = pb.bstart1[cb + 1];
+    const uint64_t a = pb.bstart1[cb] + (uint64_t)(t - pb.tile2_off[cb]) * kPbTile2;
+    const uint32_t cnt = (uint32_t)(min(rend, a + kPbTile2) - a);
+    uint32_t rec[kPer];
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k) {
+      const uint32_t q = k * kPbThreads + threadIdx.x;
+      rec[k] = q < cnt ? pb.rec1[a + q] : 0u;
+    }
+    for (uint32_t b = threadIdx.x; b < nf; b += kPbThreads) hist[b] = 0;
+    __syncthreads();
+    // the fine bin is (local >> kPbFineShift) of the coarse record
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k)
+      if (k * kPbThreads + threadIdx.x < cnt)
+        atomicAdd(&hist[(rec[k] >> pb.cbits) >> kPbFineShift], 1u);
+    __syncthreads();
+    uint32_t carry = 0;
+    for (uint32_t b0 = 0; b0 < nf; b0 += kPbThreads) {
+      const uint32_t b = b0 + threadIdx.x;
+      const uint32_t h = b < nf ? hist[b] : 0u;
+      uint32_t tot;
+      const uint32_t ex = pb_block_scan<kPbThreads>(h, sh, &tot);
+      if (b < nf) {
+        base[b] = carry + ex;
+        unsigned long long d = 0;
+        if (h) {
+          // a fine bin receives exactly the entry count of its rows when A
+          // is symmetric; more proves it is not, and nothing is written
+          const uint64_t fb = ((uint64_t)cb << pb.fbits) + b;
+          d = atomicAdd(&pb.cur2[fb], (unsigned long long)h);
+          if (d + h > pb.bstartf[fb + 1]) {
+            atomicOr(&ctx.st->err, kErrNotSymmetric);
+            d = ~0ull;
+          }
+        }
+        dst[b] = d;
+        hist[b] = 0;
+      }
+      carry += tot;
+    }
+    __syncthreads();
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k)
+      if (k * kPbThreads + threadIdx.x < cnt) {
+        const uint32_t local = rec[k] >> pb.cbits;
+        const uint32_t b = local >> kPbFineShift;
+        const uint32_t slot = base[b] + atomicAdd(&hist[b], 1u);
+        buf[slot] = ((local & (kPbFineRows - 1)) << pb.cbits) | (rec[k] & cmask);
+        sbin[slot] = (uint16_t)b;
+      }
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < cnt; q += kPbThreads) {
+      const uint32_t b = sbin[q];
+      if (dst[b] != ~0ull) pb.rec2[dst[b] + (q - base[b])] = buf[q];
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 3: records of a fine bin -> z
+// ---------------------------------------------------------------------------
+
+// value = lo + hi * 2^32 (mod p), lo, hi < 2^64
+__device__ __forceinline__ uint64_t pb_reduce(uint64_t lo, uint64_t hi) {
+  const uint64_t h = fold61(hi);
+  // h * 2^32 = (h mod 2^29) * 2^32 + (h >> 29) * 2^61, and 2^61 = 1 (mod p)
+  const uint64_t t2 = ((h & 0x1FFFFFFFull) << 32) + (h >> 29);
+  return addp(fold61(t2), fold61(lo));
+}
+
+// TBL: the k colour values sit in LDS (k <= kPbTableMax), else each record's
+// value is computed from its colour.
+constexpr uint32_t kPbTableMax = 4096;
+
+template <typename RP, bool TBL>
+__global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
+  if (ctx.st->done) return;
+  __shared__ unsigned long long acc_lo[kPbFineRows];
+  __shared__ unsigned long long acc_hi[kPbFineRows];
+  __shared__ uint64_t wtab[TBL ? kPbTableMax : 1];
+  constexpr uint32_t kU = 16;  // records per thread per step, loaded together
+  const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
+  const uint32_t cmask = (1u << pb.cbits) - 1;
+  const uint32_t nitems = pb.cnt->nslices;
+  if (TBL) {
+    const uint32_t k = ctx.st->k;
+    for (uint32_t b = threadIdx.x; b < k; b += kPbAccThreads) wtab[b] = color_weight(key, b);
+  }
+  for (uint32_t t = blockIdx.x; t < nitems; t += gridDim.x) {
+    uint32_t lo = 0, hi = pb.nfine - 1;  // fine bin: last f with slice_off[f] <= t
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) >> 1;
+      if (pb.slice_off[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const uint32_t f = lo;
+    const uint32_t q = t - pb.slice_off[f];
+    const uint32_t ns = pb.slice_off[f + 1] - pb.slice_off[f];
+    const uint64_t b1 = pb.bstartf[f + 1];
+    const uint64_t a = pb.bstartf[f] + (uint64_t)q * kPbSlice;
+    const uint64_t e = ns == 1 ? b1 : min(b1, a + kPbSlice);
+    for (uint32_t r = threadIdx.x; r < kPbFineRows; r += kPbAccThreads) {
+      acc_lo[r] = 0;
+      acc_hi[r] = 0;
+    }
+    __syncthreads();
+    for (uint64_t p0 = a; p0 < e; p0 += kU * kPbAccThreads) {
+      uint32_t rv[kU];
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        const uint64_t p = p0 + u * kPbAccThreads + threadIdx.x;
+        rv[u] = p < e ? pb.rec2[p] : 0u;
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        const bool ok = p0 + u * kPbAccThreads + threadIdx.x < e;
+        const uint32_t local = (rv[u] >> pb.cbits) & (kPbFineRows - 1);
+        const uint64_t w =
+            ok ? (TBL ? wtab[rv[u] & cmask] : color_weight(key, rv[u] & cmask)) : 0ull;
+        uint64_t wl = w & 0xFFFFFFFFull, wh = w >> 32;
+        const uint32_t l0 = __shfl(local, 0, kWave);
+        if (__all(!ok || local == l0)) {
+          // the whole wave feeds one row (rows of high degree): add in
+          // registers first
+#pragma unroll
+          for (int off = kWave / 2; off > 0; off >>= 1) {
+            wl += __shfl_xor(wl, off, kWave);
+            wh += __shfl_xor(wh, off, kWave);
+          }
+          if (lane_id() == 0 && (wl | wh)) {
+            atomicAdd(&acc_lo[l0], (unsigned long long)wl);
+            atomicAdd(&acc_hi[l0], (unsigned long long)wh);
+          }
+        } else if (ok) {
+          atomicAdd(&acc_lo[local], (unsigned long long)wl);
+          atomicAdd(&acc_hi[local], (unsigned long long)wh);
+        }
+      }
+    }
+    __syncthreads();
+    const uint64_t row0 = (uint64_t)f << kPbFineShift;
+    const uint32_t nrows = (uint32_t)min((uint64_t)kPbFineRows, (uint64_t)ctx.n - row0);
+    if (ns == 1) {
+      for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
+        if (ctx.act[row0 + r]) ctx.z[row0 + r] = pb_reduce(acc_lo[r], acc_hi[r]);
+    } else {
+      uint64_t* part = pb.part + (uint64_t)(pb.mslice_off[f] + q) * kPbFineRows;
+      for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
+        part[r] = pb_reduce(acc_lo[r], acc_hi[r]);
+    }
+    __syncthreads();
+  }
+}
+
+// Bins with several slices: z = sum of the partial images.
+__global__ void __launch_bounds__(kBlock) k_pb_combine(Ctx ctx, PbCtx pb) {
+  if (ctx.st->done) return;
+  const uint32_t nm = pb.cnt->nmulti;
+  const uint64_t total = (uint64_t)nm * kPbFineRows;
+  for (uint64_t x = blockIdx.x * (uint64_t)kBlock + threadIdx.x; x < total;
+       x += (uint64_t)gridDim.x * kBlock) {
+    const uint32_t f = pb.mlist[x >> kPbFineShift];
+    const uint32_t r = (uint32_t)(x & (kPbFineRows - 1));
+    const uint64_t row = ((uint64_t)f << kPbFineShift) + r;
+    if (row >= ctx.n || !ctx.act[row]) continue;
+    const uint32_t s0 = pb.mslice_off[f], s1 = pb.mslice_off[f + 1];
+    uint64_t z = 0;
+    for (uint32_t s = s0; s < s1; ++s) z = addp(z, pb.part[(uint64_t)s * kPbFineRows + r]);
+    ctx.z[row] = z;
+  }
+}
+
+}  // namespace wl

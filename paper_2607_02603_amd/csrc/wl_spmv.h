@@ -354,16 +354,17 @@ __global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
     for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c8[i] = (uint8_t)ctx.c[i];
 }
 
-// Diagnostics: rows and entries the next SpMV launch will read.
+// Diagnostics: rows and entries the next SpMV launch will read (all of them
+// when 'all' is set: the propagation-blocking image reads every entry).
 template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx) {
+__global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx, int all) {
   if (ctx.st->done) return;
   const RP* rp = rowptr<RP>(ctx);
   const bool uniform = !ctx.weighted && ctx.st->k == 1;
   unsigned long long rows = 0, ents = 0;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
        i += gridDim.x * kBlock)
-    if (ctx.act[i]) {
+    if (all || ctx.act[i]) {
       rows += 1;
       ents += rp[i + 1] - rp[i];
     }
@@ -386,6 +387,24 @@ __global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx) {
       atomicAdd(&ctx.st->work_entries, se[0]);
     }
   }
+}
+
+// Entries of the rows whose image is needed this round, added to
+// st->act_entries (cleared by k_round_begin).
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_count_active(Ctx ctx) {
+  const RP* rp = rowptr<RP>(ctx);
+  unsigned long long ents = 0;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n; i += gridDim.x * kBlock)
+    if (ctx.act[i]) ents += rp[i + 1] - rp[i];
+  __shared__ unsigned long long se[kBlock];
+  se[threadIdx.x] = ents;
+  __syncthreads();
+  for (int o = kBlock / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) se[threadIdx.x] += se[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && se[0]) atomicAdd(&ctx.st->act_entries, se[0]);
 }
 
 }  // namespace wl

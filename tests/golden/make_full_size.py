@@ -1,0 +1,99 @@
+"""Writes the expected results of the full-size workloads from the CPU oracle.
+
+    python tests/golden/make_full_size.py chunglu rmat27
+
+For each workload: the seeded graph from the shared input generators (built on
+the GPU, which produces byte-identical CSRs to the CPU build of the same
+generators), then Algorithm 1 run by the oracle round by round from the
+trivial partition with seed 0.  Stored per workload in
+tests/golden/full_<name>.json: n, nnz, a checksum of the CSR, the colour
+count after every round, the round count, the final colour count, the SHA-256
+of the final colour array (uint32 little-endian) and the colours of 4096
+seeded sample nodes.  Nothing here calls the HIP library.
+"""
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(os.path.dirname(HERE))
+sys.path.insert(0, ROOT)
+
+import oracle  # noqa: E402
+from paper_2607_02603_amd import inputs  # noqa: E402
+
+WORKLOADS = {
+    "chunglu": "Chung-Lu n=4e6, 64e6 sampled pairs, exponent 2.1, seed 0",
+    "rmat27": "R-MAT scale 27, edge factor 16, (0.57,0.19,0.19,0.05), symmetrised+dedup, seed 0",
+}
+
+
+def say(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+
+
+def build(name):
+    import torch
+    dev = torch.device("cuda:0")
+    g = inputs.chung_lu(device=dev) if name == "chunglu" else inputs.rmat(27, 16, device=dev)
+    torch.cuda.synchronize()
+    rp = g.row_ptr.cpu().numpy().view(np.uint64)
+    col = g.col.cpu().numpy().view(np.uint32)
+    del g
+    torch.cuda.empty_cache()
+    return rp, col
+
+
+def csr_checksum(rp, col):
+    """(sum of col[e] * (e + 1), sum of row_ptr) mod 2^64, computed in chunks."""
+    acc = np.uint64(0)
+    step = 1 << 27
+    with np.errstate(over="ignore"):
+        for a in range(0, col.size, step):
+            c = col[a:a + step].astype(np.uint64)
+            idx = np.arange(a + 1, a + 1 + c.size, dtype=np.uint64)
+            acc = acc + np.sum(c * idx, dtype=np.uint64)
+        rsum = np.sum(rp, dtype=np.uint64)
+    return [int(acc), int(rsum)]
+
+
+def run(name):
+    say(f"{name}: generating")
+    rp, col = build(name)
+    n = rp.size - 1
+    say(f"{name}: n={n} nnz={col.size}")
+    c, k = oracle.canonicalize(None, n)
+    hist = []
+    r = 0
+    while True:
+        t0 = time.time()
+        c2, k2, _ = oracle.refine_round(rp, col, None, c, k, 0, r)
+        r += 1
+        hist.append(k2)
+        say(f"{name}: round {r - 1}: {k} -> {k2} colours ({time.time() - t0:.1f} s)")
+        c = c2
+        if k2 == k:
+            break
+        k = k2
+    rng = np.random.default_rng(12345)
+    sample = np.sort(rng.choice(n, size=min(n, 4096), replace=False)).astype(np.int64)
+    out = {
+        "workload": WORKLOADS[name], "seed": 0, "n": int(n), "nnz": int(col.size),
+        "csr_checksum": csr_checksum(rp, col), "k_per_round": hist, "rounds": r,
+        "colours": int(k), "sha256": hashlib.sha256(c.astype("<u4").tobytes()).hexdigest(),
+        "sample_nodes": sample.tolist(), "sample_colours": c[sample].astype(int).tolist(),
+        "written_by": "tests/golden/make_full_size.py (oracle/ only)",
+    }
+    path = os.path.join(HERE, f"full_{name}.json")
+    with open(path, "w") as f:
+        json.dump(out, f)
+    say(f"{name}: wrote {path}: colours={k} rounds={r}")
+
+
+if __name__ == "__main__":
+    for nm in sys.argv[1:] or list(WORKLOADS):
+        run(nm)

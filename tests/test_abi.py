@@ -63,6 +63,22 @@ def test_workspace_size_host_only():
     assert 40 * 100000 < out.value < 120 * 100000 + 64 * 5000000 // 2048 * 1024
 
 
+def test_symmetric_flag_adds_the_binned_image_workspace():
+    _ensure_built()
+    L = wl.lib()
+    out = ctypes.c_uint64(0)
+    s = _csr(100000, 5000000)
+    assert L.wl_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    plain = out.value
+    s.flags = wl.WL_CSR_SYMMETRIC
+    assert L.wl_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    # 4 bytes per entry of records (one scatter pass at this size) plus tables
+    assert plain + 4 * 5000000 <= out.value < plain + 6 * 5000000
+    s.weight = 8  # weighted graphs never take that path
+    assert L.wl_workspace_size(ctypes.byref(s), ctypes.byref(out)) == wl.WL_OK
+    assert out.value == plain
+
+
 def test_verify_workspace_size_host_only():
     _ensure_built()
     L = wl.lib()

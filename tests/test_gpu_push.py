@@ -1,0 +1,188 @@
+"""GPU parity of the propagation-blocking image (symmetric graphs flagged
+WL_CSR_SYMMETRIC): with WL_PB=force every round it can serve goes through
+it, on graphs of every shape (isolated nodes, self-loops, multi-edges, rows
+of high degree, bins cut into several slices, two scatter passes); results
+must equal the oracle bit for bit.  Also: graphs wrongly flagged symmetric
+are rejected, never written out of bounds."""
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_02603_amd as wl
+from oracle import bruteforce as bf
+from paper_2607_02603_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+@pytest.fixture
+def force_pb(monkeypatch):
+    monkeypatch.setenv("WL_PB", "force")
+
+
+def _sym_graph(rp, col, rp64=False):
+    n = len(rp) - 1
+    rp = np.asarray(rp, dtype=np.uint64)
+    if not rp64:
+        rp = rp.astype(np.uint32)
+    return wl.Graph.from_numpy(n, rp, col, None, device="cuda", symmetric=True)
+
+
+def _exact(rp, col, seed=0, rp64=False, init=None):
+    g = _sym_graph(rp, col, rp64)
+    init_t = None
+    if init is not None:
+        init_t = torch.from_numpy(np.asarray(init, np.uint32).view(np.int32)).cuda()
+    c, k, r = wl.wl_stable_coloring(g, init_t, seed)
+    got = c.cpu().numpy().view(np.uint32)
+    ref, kr, rr, _, st = oracle.stable_coloring(rp, col, None, init, seed)
+    assert st == 0
+    assert (k, r) == (kr, rr)
+    assert np.array_equal(got, ref)
+    return k, r
+
+
+def _symmetric_edges(rng, n, m, loops=False, multi=False):
+    edges = []
+    for _ in range(m):
+        u, v = rng.randrange(n), rng.randrange(n)
+        if u == v and not loops:
+            continue
+        edges.append((u, v))
+        if multi and rng.random() < 0.2:
+            edges.append((u, v))
+    # both directions (a self-loop once); keep multiplicities
+    entries = []
+    for u, v in edges:
+        entries.append((u, v))
+        if u != v:
+            entries.append((v, u))
+    entries.sort()
+    rp = np.zeros(n + 1, np.uint64)
+    for u, _ in entries:
+        rp[u + 1] += 1
+    rp = np.cumsum(rp).astype(np.uint64)
+    col = np.array([v for _, v in entries], np.uint32)
+    return rp, col
+
+
+@pytest.mark.parametrize("trial", range(12))
+def test_random_symmetric_graphs(force_pb, trial):
+    rng = random.Random(700 + trial)
+    n = rng.choice([1, 2, 5, 300, 8191, 8192, 8193, 20000, 60000])
+    m = rng.randint(0, 4 * n)
+    rp, col = _symmetric_edges(rng, n, m, loops=trial % 3 == 0, multi=trial % 4 == 1)
+    _say(f"trial {trial}: n={n} nnz={col.size}")
+    init = None
+    if trial % 5 == 2:
+        init = np.array([rng.randrange(4) for _ in range(n)], np.uint32)
+    _exact(rp, col, seed=trial, rp64=trial % 2 == 0, init=init)
+
+
+def test_configs_small(force_pb):
+    g = inputs.er_graph()
+    assert _exact(g.row_ptr, g.col) == (19993, 4)
+    g = inputs.grid_graph(64)
+    assert _exact(g.row_ptr, g.col) == (528, 32)
+    g = inputs.rmat(14, 16, seed=2)
+    _exact(g.row_ptr, g.col, seed=3)
+    g = inputs.chung_lu(50000, 400000, seed=1)
+    _exact(g.row_ptr, g.col, seed=1)
+
+
+def test_star_multi_slice_bin(force_pb):
+    # a hub of 1.3e6 neighbours: its fine bin holds more records than one
+    # slice, and most waves feed that one row
+    leaves = 1_300_000
+    rng = random.Random(4)
+    extra = [(rng.randrange(1, leaves + 1), rng.randrange(1, leaves + 1)) for _ in range(200000)]
+    u = np.concatenate([np.zeros(leaves, np.uint64), np.array([a for a, _ in extra], np.uint64)])
+    v = np.concatenate([np.arange(1, leaves + 1, dtype=np.uint64),
+                        np.array([b for _, b in extra], np.uint64)])
+    g = inputs.csr_from_edges(leaves + 1, u, v)
+    _say(f"star: n={g.n} nnz={g.nnz}")
+    _exact(g.row_ptr, g.col, seed=6)
+
+
+def test_two_scatter_passes(force_pb):
+    # more than 512 fine bins of 8192 rows: coarse bins, then fine bins
+    g = inputs.er_graph(4_400_000, 3_000_000, seed=3)
+    _say(f"er 4.4e6: nnz={g.nnz}")
+    _exact(g.row_ptr, g.col, seed=2)
+
+
+def test_refine_round_each_round(force_pb):
+    g = inputs.rmat(13, 8, seed=1)
+    dg = _sym_graph(g.row_ptr, g.col)
+    c, k = oracle.canonicalize(None, g.n)
+    r = 0
+    while True:
+        cin = torch.from_numpy(c.view(np.int32)).cuda()
+        cout, kg = wl.wl_refine_round(dg, cin, k, 17, r)
+        c2, k2, _ = oracle.refine_round(g.row_ptr, g.col, None, c, k, 17, r)
+        assert kg == k2
+        assert np.array_equal(cout.cpu().numpy().view(np.uint32), c2)
+        r += 1
+        if k2 == k:
+            break
+        c, k = c2, k2
+
+
+def test_stats_count_every_entry(force_pb):
+    g = inputs.rmat(12, 16, seed=0)
+    dg = _sym_graph(g.row_ptr, g.col)
+    wl.wl_stats_enable(wl.WL_STATS_WORK)
+    try:
+        wl.wl_refine_round(dg, torch.zeros(g.n, dtype=torch.int32, device="cuda"), 1, 0, 0)
+        _, k1 = wl.wl_refine_round(dg, torch.zeros(g.n, dtype=torch.int32, device="cuda"), 1, 0, 0)
+        c1 = torch.from_numpy(oracle.refine_round(g.row_ptr, g.col, None,
+                                                  np.zeros(g.n, np.uint32), 1, 0, 0)[0]
+                              .view(np.int32)).cuda()
+        wl.wl_refine_round(dg, c1, k1, 0, 1)
+        st = wl.wl_stats_get()
+    finally:
+        wl.wl_stats_enable(0)
+    assert st["spmv_entries"] == g.nnz and st["spmv_rows"] == g.n
+
+
+def test_wrongly_flagged_graph_is_rejected(force_pb, monkeypatch):
+    # directed star over three fine bins: the row counts of bin 0 cannot
+    # match the records bound for it
+    n = 20000
+    rp = np.zeros(n + 1, np.uint64)
+    rp[1:] = n - 1
+    col = np.arange(1, n, dtype=np.uint32)
+    g = _sym_graph(rp, col)
+    with pytest.raises(wl.WlError) as e:
+        wl.wl_stable_coloring(g)
+    assert e.value.code == wl.WL_EINVAL
+    # one bin only: the counts agree, the validation pass catches it
+    n = 100
+    rp = np.zeros(n + 1, np.uint64)
+    rp[1:] = n - 1
+    col = np.arange(1, n, dtype=np.uint32)
+    g = _sym_graph(rp, col)
+    monkeypatch.setenv("WL_VALIDATE", "1")
+    with pytest.raises(wl.WlError) as e:
+        wl.wl_stable_coloring(g)
+    assert e.value.code == wl.WL_EINVAL
+    # a symmetric graph passes the validation
+    gg = inputs.er_graph(3000, 9000, seed=4)
+    _exact(gg.row_ptr, gg.col)
+
+
+def test_auto_mode_matches_pull(monkeypatch):
+    # default policy on a graph above the size threshold, against the
+    # gathering path and the oracle
+    g = inputs.rmat(17, 16, seed=5)
+    _say(f"rmat17: nnz={g.nnz}")
+    k, r = _exact(g.row_ptr, g.col, seed=1)
+    monkeypatch.setenv("WL_PB", "0")
+    assert _exact(g.row_ptr, g.col, seed=1) == (k, r)
