@@ -45,7 +45,15 @@ struct DevState {
   uint32_t bin_start[kNumBins];
   uint32_t n_tiny;      // entries in the tiny-segment list (<= 64 nodes)
   uint32_t dense;       // 1 if the colours in use are exactly [0, k)
-  uint32_t pad[3];
+  uint32_t n_live;      // live classes (wl_live.h) of the current round
+  uint32_t nl;          // their members
+  uint32_t n_live2;     // the same for the next round
+  uint32_t nl2;
+  uint32_t nsub;        // sub-classes of the live classes after the sort
+  uint32_t nosplit;     // 1 when no live class split in this round
+  uint32_t n_split;     // live classes that split
+  uint32_t split_any;   // 1 when some live class split in this round
+  uint32_t shift_big;   // 1 when the splits need the per-colour shift table
   uint64_t seed;
   unsigned long long work_rows;     // diagnostics: rows the SpMV computed
   unsigned long long work_entries;  // diagnostics: entries it gathered
@@ -78,7 +86,7 @@ struct Ctx {
   const uint32_t* wgt;
   DevState* st;
   uint32_t* c;         // colours, node order
-  uint64_t* x;         // per-node random value of the round
+  uint64_t* x;         // scratch of the quotient phase (8 bytes per node)
   uint64_t* wtab;      // per-colour random values (k <= 65535)
   uint16_t* c16;       // compact colours (k <= 65535)
   uint8_t* c8;         // compact colours (k <= 255)
@@ -115,6 +123,26 @@ struct Ctx {
   int batch;
   uint32_t ext_lo;
   int keys_mat;        // segment keys are already in 'keys' (no gather of z)
+  // Live classes of the incremental rounds (wl_live.h).  Several of these
+  // share memory with buffers of the full relabel that those rounds do not
+  // use (see make_ctx).
+  uint32_t* lperm;     // members of the live classes, class after class
+  uint32_t* lperm2;
+  uint32_t* qcls;      // live class of every position of lperm
+  uint32_t* qcls2;
+  uint32_t* lcold;     // colour of each live class
+  uint32_t* loff;      // its first position in lperm
+  uint32_t* llen;      // its size
+  uint32_t* lcold2;
+  uint32_t* loff2;
+  uint32_t* llen2;
+  uint32_t* gstart;    // per sub-class: first position
+  uint32_t* gend;      // one past its last position
+  uint8_t* gnz;        // 1 if it holds a non-empty row
+  uint32_t* gl;        // per sub-class (or class): live flag, then its index
+  uint32_t* go;        // size, then its first position
+  uint2* split;        // (old colour, extra sub-classes) of the classes that split
+  uint32_t* shift;     // per colour: extra sub-classes below it (many splits)
 };
 
 }  // namespace wl

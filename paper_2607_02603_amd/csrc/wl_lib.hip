@@ -23,6 +23,7 @@
 #include "../../include/wl.h"
 #include "wl_ctx.h"
 #include "wl_relabel.h"
+#include "wl_live.h"
 #include "wl_spmv.h"
 #include "wl_push.h"
 #include "wl_quotient.h"
@@ -68,7 +69,7 @@ struct Layout {
   uint64_t off_st, off_x, off_z, off_keys, off_keys_tmp, off_perm, off_perm_tmp,
       off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
-      off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16;
+      off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2];
   uint64_t total;
 };
 
@@ -106,7 +107,7 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_bmin = take(8ull * L.max_big * kRadix);
   L.off_bmax = take(8ull * L.max_big * kRadix);
   L.off_bcur = take(4ull * L.max_big * kRadix);
-  L.off_scan = take(4ull * kScanBlocks);
+  L.off_scan = take(8ull * kScanBlocks);
   L.off_rows = take(4 * n);
   L.off_binpart = take(4ull * kNumBins * kScanBlocks);
   L.off_chunks = take(sizeof(HeavyChunk) * (uint64_t)L.max_chunks);
@@ -114,6 +115,10 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_hcnt = take(4ull * L.max_heavy);
   L.off_wtab = take(8ull * std::min<uint64_t>(n, kTableMax));
   L.off_c16 = take(2 * n);
+  L.off_qcls2 = take(4 * n);
+  // live classes have >= 2 members: at most n / 2 of them, three words each
+  L.off_lcls[0] = take(12ull * (n / 2 + 1));
+  L.off_lcls[1] = take(12ull * (n / 2 + 1));
   L.total = o;
   return L;
 }
@@ -219,6 +224,34 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.wtab = (uint64_t*)(ws + L.off_wtab);
   c.c16 = (uint16_t*)(ws + L.off_c16);
   c.c8 = ws + L.off_c16;
+  // Live-class state.  The incremental rounds do not use the full relabel's
+  // grouping (perm, cstart), its flags, x, or keys_tmp/tiny_list outside the
+  // sort, so those regions are shared:
+  //   lperm = perm, lperm2 = perm_tmp (the sort's scratch, written after it),
+  //   qcls = cstart, gnz = flags, gl/go = x, gstart/gend = keys_tmp,
+  //   split = tiny_list, shift = keys (written after the last read of keys).
+  c.lperm = c.perm;
+  c.lperm2 = c.perm_tmp;
+  c.qcls = c.cstart;
+  c.qcls2 = (uint32_t*)(ws + L.off_qcls2);
+  {
+    const uint64_t m = L.n / 2 + 1;
+    uint32_t* a = (uint32_t*)(ws + L.off_lcls[0]);
+    uint32_t* b = (uint32_t*)(ws + L.off_lcls[1]);
+    c.lcold = a;
+    c.loff = a + m;
+    c.llen = a + 2 * m;
+    c.lcold2 = b;
+    c.loff2 = b + m;
+    c.llen2 = b + 2 * m;
+  }
+  c.gnz = c.flags;
+  c.gl = (uint32_t*)c.x;
+  c.go = (uint32_t*)c.x + L.n;
+  c.gstart = (uint32_t*)c.keys_tmp;
+  c.gend = (uint32_t*)c.keys_tmp + L.n;
+  c.split = c.tiny_list;
+  c.shift = (uint32_t*)c.keys;
   c.weighted = g->weight != nullptr;
   {
     const char* nt = getenv("WL_NT_STREAM");
@@ -322,6 +355,7 @@ __global__ void __launch_bounds__(kBlock) k_iota_zero(Ctx ctx) {
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
        i += gridDim.x * kBlock) {
     ctx.perm[i] = i;
+    ctx.ids[i] = 0;
     ctx.c[i] = 0;
     ctx.act[i] = ctx.n >= 2 ? 1 : 0;
   }
@@ -686,7 +720,7 @@ struct Session {
     g.b0 = g.b1 + (h.bin_cnt[0] ? grid_for(h.bin_cnt[0], kBlock / 4) : 0);
     if (g.b0 == 0) return WL_OK;
     const int mode = gather_mode(h.k);
-    if (!uniform)
+    if (!uniform && mode != kGatherC)
       hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock),
                          0, s, ctx, mode);
     if (sflags & WL_STATS_WORK)
@@ -701,7 +735,7 @@ struct Session {
       else if (mode == kGather16)
         spmv_launch<RP, W, kGather16>(g);
       else
-        spmv_launch<RP, W, kGatherX>(g);
+        spmv_launch<RP, W, kGatherC>(g);
     });
     return WL_OK;
   }
@@ -762,12 +796,13 @@ struct Session {
                        0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
-    return finish_sort(0);
+    return finish_sort(0, true);
   }
 
   // Radix passes from 'pass0' on while big segments are left (read back after
-  // every pass), then the small sorts and the rank scan.
-  int finish_sort(int pass0) {
+  // every pass), then the small sorts and, for the full relabel, the rank
+  // scan.
+  int finish_sort(int pass0, bool full) {
     for (int pass = pass0; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
       radix_pass(pass, grid_for((uint64_t)host.n_big[pass & 1] * kRadix),
                  std::min<uint32_t>(host.n_big[pass & 1], 4096));
@@ -780,7 +815,7 @@ struct Session {
     if (host.n_small)
       hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
                          dim3(kBlock), 0, s, ctx);
-    rank_scan();
+    if (full) rank_scan();
     HIP_LAUNCH_CHECK();
     return WL_OK;
   }
@@ -809,25 +844,107 @@ struct Session {
     hipLaunchKernelGGL(k_round_end, dim3(1), dim3(1), 0, s, ctx, count_round);
   }
 
-  // One whole round launched without reading anything back.  Every grid is
-  // fixed for the call and every count comes from the device state; at most
-  // async_passes radix passes run, and a round that needs more halts the
-  // device before its small sorts (finish_halted completes it).
-  void round_async(uint32_t round) {
+  // Exclusive scan of a (and b) over *lenp entries; totals to tot_a / tot_b.
+  // Runs only when *run_if != 0 (run_if NULL: always).
+  void xscan(const uint32_t* run_if, const uint32_t* lenp, uint32_t* a, uint32_t* b,
+             uint32_t* tot_a, uint32_t* tot_b) {
+    hipLaunchKernelGGL(k_xscan_part, dim3(nscan), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
+                       b, ctx.scan_part);
+    hipLaunchKernelGGL(k_xscan_top, dim3(1), dim3(kBlock), 0, s, ctx.st, run_if, ctx.scan_part,
+                       nscan, tot_a, tot_b);
+    hipLaunchKernelGGL(k_xscan_final, dim3(nscan), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
+                       b, ctx.scan_part);
+  }
+
+  // Live classes from the grouping of the canonical start (perm, cstart, ids
+  // = colour of every position, host.k colours).  Once per call.
+  int build_live() {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    const uint32_t k = host.k;
+    DevState* st = ctx.st;
+    hipLaunchKernelGGL(k_fill_u8, dim3(grid_for(k, kBlock, 4096)), dim3(kBlock), 0, s, ctx,
+                       ctx.gnz, (uint64_t)k, (uint8_t)0);
+    if (rp64)
+      hipLaunchKernelGGL(k_live_class_nz<uint64_t>, dim3(gn), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_live_class_nz<uint32_t>, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_class_vals, dim3(grid_for(k, kBlock, 4096)), dim3(kBlock), 0, s,
+                       ctx);
+    xscan(nullptr, &st->k, ctx.gl, ctx.go, &st->n_live2, &st->nl2);
+    if (rp64)
+      hipLaunchKernelGGL(k_live_build<uint64_t>, dim3(gn), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_live_build<uint32_t>, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_commit, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_adopt, dim3(1), dim3(1), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    return WL_OK;
+  }
+
+  // Image keys of the live classes and their sort lists.
+  void live_head() {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_segments, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)),
+                       dim3(kBlock), 0, s, ctx);
+  }
+
+  // After the sort: sub-classes, new colours of every node, next live
+  // classes, end of the round.
+  void live_tail() {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    DevState* st = ctx.st;
+    hipLaunchKernelGGL(k_live_scan_part, dim3(nscan), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
+    hipLaunchKernelGGL(k_live_scan_final, dim3(nscan), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_nz0, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_subs, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_splits, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)), dim3(kBlock),
+                       0, s, ctx);
+    xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2);
+    hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx);
+    hipLaunchKernelGGL(k_shift_clear, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_shift_scatter, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)),
+                       dim3(kBlock), 0, s, ctx);
+    xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr);
+    hipLaunchKernelGGL(k_shift_apply, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_emit, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_commit, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
+  }
+
+  // One round of the incremental relabel driven from the host (counts read
+  // back to size the sorts).
+  int round_live() {
+    hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
+    if (int r = spmv()) return r;
+    live_head();
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    if (int r = finish_sort(0, false)) return r;
+    live_tail();
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    if (host.err & kErrNotSymmetric)
+      return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
+    return WL_OK;
+  }
+
+  // The same launched without reading anything back: grids are fixed for the
+  // call and counts come from the device state; at most async_passes radix
+  // passes run, and a round that needs more halts the device before its
+  // small sorts (finish_halted completes it).
+  void round_live_async(uint32_t round) {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
     spmv_async(round);
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
-    hipLaunchKernelGGL(k_fill_u8, dim3(gn), dim3(kBlock), 0, s, ctx, ctx.flags,
-                       (uint64_t)L.n, (uint8_t)0);
-    hipLaunchKernelGGL(k_segments, dim3(gn), dim3(kBlock), 0, s, ctx);
+    live_head();
     for (int pass = 0; pass < async_passes; ++pass) radix_pass(pass, 1024, 1024);
     hipLaunchKernelGGL(k_passes_check, dim3(1), dim3(1), 0, s, ctx, async_passes);
     hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 2048)),
                        dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_small_sort, dim3(grid_for(L.n / (kTinyMax + 1), 1, 2048)),
                        dim3(kBlock), 0, s, ctx);
-    rank_scan();
-    relabel_tail(1);
+    live_tail();
   }
 
   // The device halted in a round after async_passes radix passes: clear the
@@ -836,8 +953,8 @@ struct Session {
     hipLaunchKernelGGL(k_resume, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
-    if (int r = finish_sort(async_passes)) return r;
-    relabel_tail(1);
+    if (int r = finish_sort(async_passes, false)) return r;
+    live_tail();
     HIP_LAUNCH_CHECK();
     return pull();
   }
@@ -854,6 +971,8 @@ struct Session {
       if (int r = relabel(0)) return r;
     }
     if (int r = build_schedule()) return r;
+    if (int r = build_live()) return r;
+    ctx.keys_mat = 1;
     // The first rounds are driven from the host (each reads its counts
     // back); after that, rounds go to the device in groups of 'ahead' with
     // one read-back per group.  Rounds queued past the last one find the
@@ -861,16 +980,18 @@ struct Session {
     uint32_t host_rounds = 0, ahead = 8;
     while (!host.done) {
       if (host_rounds < host_rounds_first) {
-        if (int r = round()) return r;
+        if (int r = round_live()) return r;
         ++host_rounds;
         continue;
       }
       const uint32_t base = host.round;
-      for (uint32_t i = 0; i < ahead; ++i) round_async(base + i);
+      for (uint32_t i = 0; i < ahead; ++i) round_live_async(base + i);
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
       if (host.done == kHalted)
         if (int r = finish_halted()) return r;
+      if (host.err & kErrNotSymmetric)
+        return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
       ahead = std::min<uint32_t>(ahead * 2, 64);
     }
     return WL_OK;

@@ -1,0 +1,531 @@
+// Relabel step of Algorithm 1 (Section 4.1) restricted to the classes that
+// can still split.
+//
+// New colour of node i = rank of (c_i, z_i) among the distinct pairs in
+// lexicographic order.  Colours are dense ranks, so a class b that splits
+// into s sub-classes (sorted by z) receives the ids
+//     b + shift(b), ..., b + shift(b) + s - 1,
+// where shift(b) counts the extra sub-classes created by the classes before
+// b, and a class that does not split keeps b + shift(b).  A class can only
+// split when it has two or more members and one of them has a non-empty row
+// (an empty row has z = 0 in every round), so only such "live" classes are
+// sorted; everything else just moves by shift.
+//
+// State kept between rounds (device):
+//   L      live classes in colour order: old colour lcold[j], members at
+//          lperm[loff[j] .. loff[j] + llen[j]); qcls[q] = class of position q.
+//   act    1 for a node of a live class whose row is non-empty (the SpMV
+//          computes z only there; every other member of a live class has
+//          key 0).
+// One round after the image:
+//   load      keys[q] = z of lperm[q] (0 for act = 0)
+//   sort      segmented sort of the keys inside every live class (the MSD
+//             radix / LDS / wave sorts of wl_relabel.h, keys materialised)
+//   scan      flags at sub-class starts (class start, or key change); their
+//             inclusive scan R gives the sub-class index g = R - 1 and the
+//             new colour lcold[j] + g - j; sub-class extents and whether a
+//             sub-class holds a non-empty row
+//   shift     classes that split (old colour, extra sub-classes) -> shift(b)
+//             for every colour, applied to every node
+//   emit      members of live classes get their exact new colour; live
+//             sub-classes (>= 2 members, a non-empty row) form the next L.
+// Every kernel reads its counts from the device state, so a round can be
+// queued without reading anything back.
+#pragma once
+#include "wl_relabel.h"
+
+namespace wl {
+
+constexpr uint32_t kShiftLds = 4096;  // splits searched in LDS; more use a table
+
+// ---------------------------------------------------------------------------
+// Generic exclusive scan of one or two u32 arrays in place, length read from
+// device memory, totals written to device memory.  Three launches:
+// part (kScanBlocks blocks), top (one block), final (kScanBlocks blocks).
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void xscan_range(uint32_t len, uint32_t b, uint32_t nblk,
+                                            uint32_t* lo, uint32_t* hi) {
+  const uint32_t per = ((len + nblk - 1) / nblk + kBlock - 1) / kBlock * kBlock;
+  *lo = min(len, b * per);
+  *hi = min(len, *lo + per);
+}
+
+// 'run_if' (device, may be NULL): the scan runs only when *run_if != 0.
+__global__ void __launch_bounds__(kBlock) k_xscan_part(const DevState* st, const uint32_t* run_if,
+                                                       const uint32_t* lenp, const uint32_t* a,
+                                                       const uint32_t* b, uint32_t* part) {
+  if (st->done || (run_if && !*run_if)) return;
+  uint32_t lo, hi;
+  xscan_range(*lenp, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t sa = 0, sb = 0;
+  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+    sa += a[i];
+    if (b) sb += b[i];
+  }
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t ta, tb = 0;
+  block_excl_scan(sa, sh, &ta);
+  if (b) block_excl_scan(sb, sh, &tb);
+  if (threadIdx.x == 0) {
+    part[blockIdx.x] = ta;
+    part[gridDim.x + blockIdx.x] = tb;
+  }
+}
+
+// One block: exclusive scan of the block sums; totals to *tot_a / *tot_b.
+__global__ void __launch_bounds__(kBlock) k_xscan_top(const DevState* st, const uint32_t* run_if,
+                                                      uint32_t* part, uint32_t nblk,
+                                                      uint32_t* tot_a, uint32_t* tot_b) {
+  if (st->done || (run_if && !*run_if)) return;
+  __shared__ uint32_t sh[kBlock / kWave];
+  for (int which = 0; which < 2; ++which) {
+    uint32_t* p = part + which * nblk;
+    uint32_t carry = 0;
+    for (uint32_t base = 0; base < nblk; base += kBlock) {
+      const uint32_t i = base + threadIdx.x;
+      const uint32_t v = i < nblk ? p[i] : 0;
+      uint32_t tot;
+      const uint32_t ex = block_excl_scan(v, sh, &tot);
+      if (i < nblk) p[i] = carry + ex;
+      carry += tot;
+    }
+    uint32_t* dst = which ? tot_b : tot_a;
+    if (threadIdx.x == 0 && dst) *dst = carry;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_xscan_final(const DevState* st, const uint32_t* run_if,
+                                                        const uint32_t* lenp, uint32_t* a,
+                                                        uint32_t* b, const uint32_t* part) {
+  if (st->done || (run_if && !*run_if)) return;
+  uint32_t lo, hi;
+  xscan_range(*lenp, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t ra = part[blockIdx.x], rb = part[gridDim.x + blockIdx.x];
+  __shared__ uint32_t sh[kBlock / kWave];
+  for (uint32_t base = lo; base < hi; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t va = i < hi ? a[i] : 0;
+    uint32_t ta;
+    const uint32_t ea = block_excl_scan(va, sh, &ta);
+    if (i < hi) a[i] = ra + ea;
+    ra += ta;
+    if (b) {
+      const uint32_t vb = i < hi ? b[i] : 0;
+      uint32_t tb;
+      const uint32_t eb = block_excl_scan(vb, sh, &tb);
+      if (i < hi) b[i] = rb + eb;
+      rb += tb;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Set-up of the live classes from a grouping (perm, cstart, ids = colour of
+// every position), once per call after the canonical start.
+// ---------------------------------------------------------------------------
+
+template <typename RP>
+__device__ __forceinline__ bool row_nonempty(const Ctx& ctx, uint32_t v) {
+  const RP* rp = rowptr<RP>(ctx);
+  return rp[v + 1] > rp[v];
+}
+
+// gnz[b] = 1 if class b has a member with a non-empty row (gnz cleared for
+// b < k by the caller).
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_live_class_nz(Ctx ctx) {
+  for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n; p += gridDim.x * kBlock)
+    if (row_nonempty<RP>(ctx, ctx.perm[p])) ctx.gnz[ctx.ids[p]] = 1;
+}
+
+__device__ __forceinline__ bool class_live(const Ctx& ctx, uint32_t b) {
+  return ctx.cstart[b + 1] - ctx.cstart[b] >= 2 && ctx.gnz[b];
+}
+
+// gl[b] = 1, go[b] = size for live classes b < k, else 0 (scanned next).
+__global__ void __launch_bounds__(kBlock) k_live_class_vals(Ctx ctx) {
+  const uint32_t k = ctx.st->k;
+  for (uint32_t b = blockIdx.x * kBlock + threadIdx.x; b < k; b += gridDim.x * kBlock) {
+    const bool live = class_live(ctx, b);
+    ctx.gl[b] = live ? 1u : 0u;
+    ctx.go[b] = live ? ctx.cstart[b + 1] - ctx.cstart[b] : 0u;
+  }
+}
+
+// Members of the live classes in colour order (into the '2' buffers, made
+// current by k_live_commit), act for every node.
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_live_build(Ctx ctx) {
+  for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n; p += gridDim.x * kBlock) {
+    const uint32_t b = ctx.ids[p], v = ctx.perm[p];
+    const bool live = class_live(ctx, b);
+    ctx.act[v] = live && row_nonempty<RP>(ctx, v) ? 1 : 0;
+    if (!live) continue;
+    const uint32_t s = ctx.cstart[b];
+    const uint32_t j = ctx.gl[b], q = ctx.go[b] + (p - s);
+    ctx.lperm2[q] = v;
+    ctx.qcls2[q] = j;
+    if (p == s) {
+      ctx.lcold2[j] = b;
+      ctx.loff2[j] = ctx.go[b];
+      ctx.llen2[j] = ctx.cstart[b + 1] - s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// One round
+// ---------------------------------------------------------------------------
+
+__global__ void __launch_bounds__(kBlock) k_live_load(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t nl = st->nl;
+  for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
+    const uint32_t v = ctx.lperm[q];
+    ctx.keys[q] = ctx.act[v] ? ctx.z[v] : 0ull;
+  }
+}
+
+// Sort work lists of the live classes (every one has >= 2 members); keys are
+// materialised in 'keys'.
+__global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  __shared__ uint32_t sh[kBlock / kWave];
+  __shared__ uint32_t base_sh;
+  const uint32_t nlive = st->n_live;
+  const uint32_t stride = gridDim.x * kBlock;
+  for (uint32_t j0 = blockIdx.x * kBlock; j0 < nlive; j0 += stride) {
+    const uint32_t j = j0 + threadIdx.x;
+    uint32_t s = 0, len = 0;
+    if (j < nlive) {
+      s = ctx.loff[j];
+      len = ctx.llen[j];
+    }
+    const bool tiny = len >= 2 && len <= kTinyMax;
+    const bool small = len > kTinyMax && len <= kSmallMax;
+    const bool big = len > kSmallMax;
+    const uint32_t t = block_append(tiny, &st->n_tiny, sh, &base_sh);
+    if (tiny) ctx.tiny_list[t] = make_uint2(s, len | kMatBit);
+    const uint32_t a = block_append(small, &st->n_small, sh, &base_sh);
+    if (small) ctx.small_list[a] = make_uint2(s, len | kMatBit);
+    const uint32_t b = block_append(big, &st->n_big[0], sh, &base_sh);
+    if (big) ctx.big_list0[b] = make_uint2(s, len);
+  }
+}
+
+// A sub-class starts at q: first position of a class, or a key change.
+__device__ __forceinline__ uint32_t live_flag(const Ctx& ctx, uint32_t q) {
+  return (q == 0 || ctx.qcls[q] != ctx.qcls[q - 1] || ctx.keys[q] != ctx.keys[q - 1]) ? 1u
+                                                                                      : 0u;
+}
+
+__global__ void __launch_bounds__(kBlock) k_live_scan_part(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done) return;
+  uint32_t lo, hi;
+  xscan_range(st->nl, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t s = 0;
+  for (uint32_t q = lo + threadIdx.x; q < hi; q += kBlock) s += live_flag(ctx, q);
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t tot;
+  block_excl_scan(s, sh, &tot);
+  if (threadIdx.x == 0) ctx.scan_part[blockIdx.x] = tot;
+}
+
+// One block: block offsets; nsub = sub-classes of the live classes,
+// k_new = k + nsub - n_live; nosplit when no class split.
+__global__ void __launch_bounds__(kBlock) k_live_scan_top(Ctx ctx, uint32_t nblk) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nblk; base += kBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t v = i < nblk ? ctx.scan_part[i] : 0;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(v, sh, &tot);
+    if (i < nblk) ctx.scan_part[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) {
+    st->nsub = carry;
+    st->k_new = st->k + carry - st->n_live;
+    st->nosplit = carry == st->n_live ? 1u : 0u;
+    st->split_any = 1u - st->nosplit;
+    st->shift_big = 0;
+  }
+}
+
+// ids[q] = sub-class of q; per sub-class g: first position, end, and whether
+// its key is non-zero (then it holds a non-empty row).
+__global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t nl = st->nl;
+  uint32_t lo, hi;
+  xscan_range(nl, blockIdx.x, gridDim.x, &lo, &hi);
+  uint32_t run = ctx.scan_part[blockIdx.x];
+  __shared__ uint32_t sh[kBlock / kWave];
+  for (uint32_t base = lo; base < hi; base += kBlock) {
+    const uint32_t q = base + threadIdx.x;
+    const uint32_t f = q < hi ? live_flag(ctx, q) : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(f, sh, &tot);
+    if (q < hi) {
+      const uint32_t g = run + ex + f - 1;
+      ctx.ids[q] = g;
+      if (f) {
+        ctx.gstart[g] = q;
+        ctx.gnz[g] = ctx.keys[q] != 0 ? 1 : 0;
+      }
+      if (q + 1 == nl || live_flag(ctx, q + 1)) ctx.gend[g] = q + 1;
+    }
+    run += tot;
+  }
+}
+
+// Sub-classes with key 0 hold a non-empty row if one of their members is
+// active (a non-empty row whose image happens to be 0).
+__global__ void __launch_bounds__(kBlock) k_live_nz0(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t nl = st->nl;
+  for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock)
+    if (ctx.keys[q] == 0 && ctx.act[ctx.lperm[q]]) ctx.gnz[ctx.ids[q]] = 1;
+}
+
+__device__ __forceinline__ bool sub_live(const Ctx& ctx, uint32_t g) {
+  return ctx.gend[g] - ctx.gstart[g] >= 2 && ctx.gnz[g];
+}
+
+// gl[g] = 1, go[g] = size for the live sub-classes (scanned next).
+__global__ void __launch_bounds__(kBlock) k_live_subs(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t ns = st->nsub;
+  for (uint32_t g = blockIdx.x * kBlock + threadIdx.x; g < ns; g += gridDim.x * kBlock) {
+    const bool live = sub_live(ctx, g);
+    ctx.gl[g] = live ? 1u : 0u;
+    ctx.go[g] = live ? ctx.gend[g] - ctx.gstart[g] : 0u;
+  }
+}
+
+// Classes that split: (old colour, extra sub-classes), in any order.
+__global__ void __launch_bounds__(kBlock) k_live_splits(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  __shared__ uint32_t sh[kBlock / kWave];
+  __shared__ uint32_t base_sh;
+  const uint32_t nlive = st->n_live;
+  const uint32_t stride = gridDim.x * kBlock;
+  for (uint32_t j0 = blockIdx.x * kBlock; j0 < nlive; j0 += stride) {
+    const uint32_t j = j0 + threadIdx.x;
+    uint32_t extra = 0;
+    if (j < nlive) {
+      const uint32_t s = ctx.loff[j];
+      extra = ctx.ids[s + ctx.llen[j] - 1] - ctx.ids[s];
+    }
+    const uint32_t at = block_append(extra > 0, &st->n_split, sh, &base_sh);
+    if (extra > 0) ctx.split[at] = make_uint2(ctx.lcold[j], extra);
+  }
+}
+
+// One block of 1024 threads: with at most kShiftLds splits, sort them by old
+// colour and replace the extras by their inclusive prefix sums.
+constexpr int kShiftThreads = 1024;
+__global__ void __launch_bounds__(kShiftThreads) k_shift_sort(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t S = st->n_split;
+  if (S > kShiftLds) {
+    if (threadIdx.x == 0) ctx.st->shift_big = 1;
+    return;
+  }
+  if (S == 0) return;
+  __shared__ uint32_t key[kShiftLds];
+  __shared__ uint32_t val[kShiftLds];
+  __shared__ uint32_t wsum[kShiftThreads / kWave];
+  uint32_t P = 1;
+  while (P < S) P <<= 1;
+  for (uint32_t t = threadIdx.x; t < P; t += kShiftThreads) {
+    if (t < S) {
+      const uint2 e = ctx.split[t];
+      key[t] = e.x;
+      val[t] = e.y;
+    } else {
+      key[t] = 0xFFFFFFFFu;
+      val[t] = 0;
+    }
+  }
+  __syncthreads();
+  for (uint32_t kk = 2; kk <= P; kk <<= 1)
+    for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+      for (uint32_t i = threadIdx.x; i < P; i += kShiftThreads) {
+        const uint32_t l = i ^ j;
+        if (l > i) {
+          const bool asc = (i & kk) == 0;
+          const uint32_t a = key[i], b = key[l];
+          if ((a > b) == asc) {
+            key[i] = b;
+            key[l] = a;
+            const uint32_t tv = val[i];
+            val[i] = val[l];
+            val[l] = tv;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  // inclusive scan of val[0..S): each thread owns a run of consecutive items
+  constexpr uint32_t kPer = kShiftLds / kShiftThreads;
+  const uint32_t t0 = threadIdx.x * kPer;
+  uint32_t loc = 0;
+#pragma unroll
+  for (uint32_t u = 0; u < kPer; ++u) loc += (t0 + u < S) ? val[t0 + u] : 0u;
+  const int lane = lane_id(), wid = threadIdx.x / kWave;
+  const uint32_t inc = wave_incl_scan(loc);
+  if (lane == kWave - 1) wsum[wid] = inc;
+  __syncthreads();
+  uint32_t run = inc - loc;
+  for (int w = 0; w < wid; ++w) run += wsum[w];
+#pragma unroll
+  for (uint32_t u = 0; u < kPer; ++u)
+    if (t0 + u < S) {
+      run += val[t0 + u];
+      ctx.split[t0 + u] = make_uint2(key[t0 + u], run);
+    }
+}
+
+// More than kShiftLds splits: shift table over all colours, shift[b] =
+// extras of the split classes below b (delta at the split colours, then an
+// exclusive scan).
+__global__ void __launch_bounds__(kBlock) k_shift_clear(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || !st->shift_big) return;
+  const uint32_t k = st->k;
+  for (uint32_t b = blockIdx.x * kBlock + threadIdx.x; b < k; b += gridDim.x * kBlock)
+    ctx.shift[b] = 0;
+}
+
+__global__ void __launch_bounds__(kBlock) k_shift_scatter(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || !st->shift_big) return;
+  const uint32_t S = st->n_split;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < S; i += gridDim.x * kBlock) {
+    const uint2 e = ctx.split[i];
+    ctx.shift[e.x] = e.y;
+  }
+}
+
+// New colour of every node: b + shift(b).  Members of the classes that
+// split are rewritten by k_live_emit afterwards.
+__global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t S = st->n_split;
+  const uint32_t n = ctx.n;
+  if (st->shift_big) {
+    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+      const uint32_t b = ctx.c[i];
+      const uint32_t sft = ctx.shift[b];
+      if (sft) ctx.c[i] = b + sft;
+    }
+    return;
+  }
+  __shared__ uint32_t scol[kShiftLds];
+  __shared__ uint32_t scum[kShiftLds];
+  for (uint32_t t = threadIdx.x; t < S; t += kBlock) {
+    const uint2 e = ctx.split[t];
+    scol[t] = e.x;
+    scum[t] = e.y;
+  }
+  __syncthreads();
+  const uint32_t first = scol[0];
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    const uint32_t b = ctx.c[i];
+    if (b <= first) continue;
+    // last split colour < b
+    uint32_t lo = 0, hi = S - 1;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) >> 1;
+      if (scol[mid] < b) lo = mid; else hi = mid - 1;
+    }
+    ctx.c[i] = b + scum[lo];
+  }
+}
+
+// Exact new colours of the members of live classes, act of those whose
+// sub-class is no longer live, and the next live classes ('2' buffers).
+__global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t nl = st->nl;
+  for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
+    const uint32_t v = ctx.lperm[q];
+    const uint32_t j = ctx.qcls[q];
+    const uint32_t g = ctx.ids[q];
+    const uint32_t id = ctx.lcold[j] + g - j;
+    ctx.c[v] = id;
+    const uint32_t gs = ctx.gstart[g];
+    const uint32_t len = ctx.gend[g] - gs;
+    if (!(len >= 2 && ctx.gnz[g])) {
+      if (ctx.act[v]) ctx.act[v] = 0;
+      continue;
+    }
+    const uint32_t jn = ctx.gl[g], off = ctx.go[g];
+    ctx.lperm2[off + (q - gs)] = v;
+    ctx.qcls2[off + (q - gs)] = jn;
+    if (q == gs) {
+      ctx.lcold2[jn] = id;
+      ctx.loff2[jn] = off;
+      ctx.llen2[jn] = len;
+    }
+  }
+}
+
+// The '2' buffers become current (their counts n_live2, nl2 are taken over
+// by k_round_end / k_live_adopt).
+__global__ void __launch_bounds__(kBlock) k_live_commit(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done || st->nosplit) return;
+  const uint32_t nl = st->nl2, nlive = st->n_live2;
+  const uint32_t tid = blockIdx.x * kBlock + threadIdx.x, stride = gridDim.x * kBlock;
+  for (uint32_t q = tid; q < nl; q += stride) {
+    ctx.lperm[q] = ctx.lperm2[q];
+    ctx.qcls[q] = ctx.qcls2[q];
+  }
+  for (uint32_t j = tid; j < nlive; j += stride) {
+    ctx.lcold[j] = ctx.lcold2[j];
+    ctx.loff[j] = ctx.loff2[j];
+    ctx.llen[j] = ctx.llen2[j];
+  }
+}
+
+// After the set-up: the live counts take effect.
+__global__ void k_live_adopt(Ctx ctx) {
+  DevState* st = ctx.st;
+  st->n_live = st->n_live2;
+  st->nl = st->nl2;
+}
+
+// End of a live round: colour count, round counter, termination, and the new
+// live counts.
+__global__ void k_live_round_end(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t kn = st->k_new;
+  st->round += 1;
+  if (kn == st->k) {
+    st->done = 1;
+  } else {
+    if (st->round >= st->max_rounds) st->done = 2;
+    st->n_live = st->n_live2;
+    st->nl = st->nl2;
+  }
+  st->k = kn;
+}
+
+}  // namespace wl

@@ -36,6 +36,7 @@ __global__ void k_round_begin(Ctx ctx) {
   st->n_big[1] = 0;
   st->n_tiles = 0;
   st->act_entries = 0;
+  st->n_split = 0;
 }
 
 __global__ void __launch_bounds__(kBlock) k_fill_u8(Ctx ctx, uint8_t* p,

@@ -183,15 +183,15 @@ __global__ void __launch_bounds__(kBlock) k_heavy_fill(Ctx ctx) {
 // ---------------------------------------------------------------------------
 
 // Where the SpMV reads the random value of a neighbour j:
-//   kGatherX   x[j]                      (any number of colours)
+//   kGatherC   W(c[j]) computed from the colour (any number of colours)
 //   kGather16  tbl[c16[j]], c16 = colour  (k <= 65535: 2 bytes per node)
 //   kGather8   tbl[c8[j]],  c8  = colour  (k <= 255:   1 byte per node)
 // The compact colour arrays shrink the randomly gathered footprint 4-8x; the
 // table of k values stays in cache.
-enum GatherMode { kGatherX = 0, kGather16 = 1, kGather8 = 2 };
+enum GatherMode { kGatherC = 0, kGather16 = 1, kGather8 = 2 };
 
 __host__ __device__ __forceinline__ int gather_mode(uint32_t k) {
-  return k <= 255 ? kGather8 : (k <= kTableMax ? kGather16 : kGatherX);
+  return k <= 255 ? kGather8 : (k <= kTableMax ? kGather16 : kGatherC);
 }
 
 template <int M>
@@ -204,7 +204,7 @@ __device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j,
   }
   if (M == kGather16) return ctx.wtab[ctx.c16[j]];
   if (M == kGather8) return ctx.wtab[ctx.c8[j]];
-  return ctx.x[j];
+  return color_weight(rkey, ctx.c[j]);
 }
 
 template <int U, bool W, int M>
@@ -289,7 +289,7 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
 
 template <typename RP, bool W, int M>
 __device__ __forceinline__ void spmv_body(const Ctx& ctx, const SpmvGrid& g) {
-  const uint64_t rkey = ctx.batch ? round_key(ctx.st->seed, ctx.st->round) : 0;
+  const uint64_t rkey = round_key(ctx.st->seed, ctx.st->round);
   const uint32_t b = blockIdx.x;
   if (b < g.heavy)
     spmv_heavy<W, M>(ctx, b, g.heavy, rkey);
@@ -318,7 +318,7 @@ __global__ void __launch_bounds__(kBlock) k_spmv_dyn(Ctx ctx, SpmvGrid g) {
   else if (mode == kGather16)
     spmv_body<RP, W, kGather16>(ctx, g);
   else
-    spmv_body<RP, W, kGatherX>(ctx, g);
+    spmv_body<RP, W, kGatherC>(ctx, g);
 }
 
 // One colour and unit weights: every x_j is the same w, so
@@ -334,7 +334,8 @@ __global__ void __launch_bounds__(kBlock) k_spmv_uniform(Ctx ctx) {
 }
 
 // Per-round random values for the gather: compact colour array plus the
-// table of the k colour values (k <= 65535), or x per node otherwise.
+// table of the k colour values (k <= 65535); with more colours the SpMV
+// computes each value from the neighbour's colour.
 // mode < 0: chosen from the colour count on the device.
 __global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
   if (ctx.st->done) return;
@@ -343,10 +344,7 @@ __global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
   const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
   const uint32_t tid = blockIdx.x * kBlock + threadIdx.x;
   const uint32_t stride = gridDim.x * kBlock;
-  if (mode == kGatherX) {
-    for (uint32_t i = tid; i < ctx.n; i += stride) ctx.x[i] = color_weight(key, ctx.c[i]);
-    return;
-  }
+  if (mode == kGatherC) return;
   for (uint32_t b = tid; b < k; b += stride) ctx.wtab[b] = color_weight(key, b);
   if (mode == kGather16)
     for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c16[i] = (uint16_t)ctx.c[i];
