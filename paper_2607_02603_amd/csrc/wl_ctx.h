@@ -54,6 +54,8 @@ struct DevState {
   uint32_t n_split;     // live classes that split
   uint32_t split_any;   // 1 when some live class split in this round
   uint32_t shift_big;   // 1 when the splits need the per-colour shift table
+  uint32_t lbin_cnt[kNumBins];    // live rows per length bin (this round)
+  uint32_t lbin_start[kNumBins];
   uint64_t seed;
   unsigned long long work_rows;     // diagnostics: rows the SpMV computed
   unsigned long long work_entries;  // diagnostics: entries it gathered
@@ -143,6 +145,8 @@ struct Ctx {
   uint32_t* go;        // size, then its first position
   uint2* split;        // (old colour, extra sub-classes) of the classes that split
   uint32_t* shift;     // per colour: extra sub-classes below it (many splits)
+  uint32_t* lrows;     // live rows of the SpMV by length bin (positions of lperm)
+  uint8_t* lsplit;     // per live class: 1 if it split in this round
 };
 
 }  // namespace wl

@@ -252,6 +252,8 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.gend = (uint32_t*)c.keys_tmp + L.n;
   c.split = c.tiny_list;
   c.shift = (uint32_t*)c.keys;
+  c.lrows = c.qcls2;  // consumed by the SpMV before k_live_emit writes qcls2
+  c.lsplit = c.c8;    // written after the SpMV has read the compact colours
   c.weighted = g->weight != nullptr;
   {
     const char* nt = getenv("WL_NT_STREAM");
@@ -441,6 +443,7 @@ struct Session {
   // in every round it can serve (for testing).
   PbLayout P;
   PbCtx pb{};
+  SpmvGrid live_grid{};
   PbCounts pbc{};
   bool pb_avail = false, pb_planned = false, pb_stop = false;
   bool sym_flag = false;
@@ -745,35 +748,81 @@ struct Session {
     return weighted ? spmv_t<uint32_t, true>() : spmv_t<uint32_t, false>();
   }
 
-  // SpMV of a round launched without reading the state back: the gather
-  // mode is chosen on the device, there is no single-colour shortcut.
+  // Image of a live round.  The one-colour and propagation-blocking images
+  // write z in node order, then loaded into the sort keys; otherwise the
+  // rows of the live classes are binned and their images go to the keys
+  // directly.
   template <typename RP, bool W>
-  void spmv_async_t(uint32_t round) {
+  int spmv_live_t() {
     const DevState& h = host;
-    SpmvGrid g;
-    g.heavy = h.n_chunks ? grid_for(h.n_chunks, kBlock / kWave) : 0;
-    g.b2 = g.heavy + (h.bin_cnt[2] ? grid_for(h.bin_cnt[2], kBlock / 64) : 0);
-    g.b1 = g.b2 + (h.bin_cnt[1] ? grid_for(h.bin_cnt[1], kBlock / 16) : 0);
-    g.b0 = g.b1 + (h.bin_cnt[0] ? grid_for(h.bin_cnt[0], kBlock / 4) : 0);
-    if (g.b0 == 0) return;
+    const bool uniform = !W && h.k == 1 && !ctx.batch;
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    if (!W && !uniform && !ctx.batch) {
+      bool use = false;
+      if (int r = pb_wanted<RP>(&use)) return r;
+      if (use) {
+        if (int r = pb_round<RP>()) return r;
+        hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
+        return WL_OK;
+      }
+    }
+    if (uniform) {
+      if (sflags & WL_STATS_WORK)
+        hipLaunchKernelGGL(k_count_work<RP>, dim3(gn), dim3(kBlock), 0, s, ctx, 0);
+      timed_spmv(h.round, true, true, [&] {
+        hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
+                           dim3(kBlock), 0, s, ctx);
+      });
+      hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
+      return WL_OK;
+    }
+    live_gather<RP, W>(h.round, true);
+    return WL_OK;
+  }
+
+  int spmv_live() {
+    if (rp64) return weighted ? spmv_live_t<uint64_t, true>() : spmv_live_t<uint64_t, false>();
+    return weighted ? spmv_live_t<uint32_t, true>() : spmv_live_t<uint32_t, false>();
+  }
+
+  // Gathering image of the live rows; every count comes from the device.
+  template <typename RP, bool W>
+  void live_gather(uint32_t round, bool always) {
+    hipLaunchKernelGGL(k_lbins_count<RP>, dim3(nscan), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_lbins_scan, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
+    hipLaunchKernelGGL(k_lbins_fill<RP>, dim3(nscan), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
                        ctx, -1);
     if (sflags & WL_STATS_WORK)
-      hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
-                         dim3(kBlock), 0, s, ctx, 0);
-    timed_spmv(round, false, false, [&] {
-      hipLaunchKernelGGL((k_spmv_dyn<RP, W>), dim3(g.b0), dim3(kBlock), 0, s, ctx, g);
+      hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
+                         s, ctx, 0);
+    timed_spmv(round, always, false, [&] {
+      hipLaunchKernelGGL((k_spmv_live<RP, W>), dim3(live_grid.b0), dim3(kBlock), 0, s, ctx,
+                         live_grid);
     });
+    if (live_grid.heavy)
+      hipLaunchKernelGGL(k_live_heavy_fix, dim3(grid_for(host.bin_cnt[3], kBlock, 1024)),
+                         dim3(kBlock), 0, s, ctx);
   }
 
-  void spmv_async(uint32_t round) {
+  void spmv_live_async(uint32_t round) {
     if (rp64) {
-      if (weighted) spmv_async_t<uint64_t, true>(round);
-      else spmv_async_t<uint64_t, false>(round);
+      if (weighted) live_gather<uint64_t, true>(round, false);
+      else live_gather<uint64_t, false>(round, false);
     } else {
-      if (weighted) spmv_async_t<uint32_t, true>(round);
-      else spmv_async_t<uint32_t, false>(round);
+      if (weighted) live_gather<uint32_t, true>(round, false);
+      else live_gather<uint32_t, false>(round, false);
     }
+  }
+
+  // Fixed grid of the live SpMV: the static heavy chunks, then groups for
+  // bins 2, 1, 0 that stride over the per-round counts.
+  void plan_live_grid() {
+    const uint64_t n = L.n;
+    live_grid.heavy = host.n_chunks ? grid_for(host.n_chunks, kBlock / kWave) : 0;
+    live_grid.b2 = live_grid.heavy + grid_for(n, kBlock / 64, 512);
+    live_grid.b1 = live_grid.b2 + grid_for(n, kBlock / 16, 1024);
+    live_grid.b0 = live_grid.b1 + grid_for(n, kBlock / 4, 2048);
   }
 
   // Relabel by (c, z) for the current grouping; count_round = 0 for the
@@ -881,10 +930,8 @@ struct Session {
     return WL_OK;
   }
 
-  // Image keys of the live classes and their sort lists.
-  void live_head() {
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
-    hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
+  // Sort lists of the live classes.
+  void live_segments() {
     hipLaunchKernelGGL(k_live_segments, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)),
                        dim3(kBlock), 0, s, ctx);
   }
@@ -917,8 +964,8 @@ struct Session {
   // back to size the sorts).
   int round_live() {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
-    if (int r = spmv()) return r;
-    live_head();
+    if (int r = spmv_live()) return r;
+    live_segments();
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (int r = finish_sort(0, false)) return r;
@@ -936,8 +983,8 @@ struct Session {
   // small sorts (finish_halted completes it).
   void round_live_async(uint32_t round) {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
-    spmv_async(round);
-    live_head();
+    spmv_live_async(round);
+    live_segments();
     for (int pass = 0; pass < async_passes; ++pass) radix_pass(pass, 1024, 1024);
     hipLaunchKernelGGL(k_passes_check, dim3(1), dim3(1), 0, s, ctx, async_passes);
     hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 2048)),
@@ -973,6 +1020,7 @@ struct Session {
     if (int r = build_schedule()) return r;
     if (int r = build_live()) return r;
     ctx.keys_mat = 1;
+    plan_live_grid();
     // The first rounds are driven from the host (each reads its counts
     // back); after that, rounds go to the device in groups of 'ahead' with
     // one read-back per group.  Rounds queued past the last one find the

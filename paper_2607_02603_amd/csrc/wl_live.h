@@ -330,6 +330,7 @@ __global__ void __launch_bounds__(kBlock) k_live_splits(Ctx ctx) {
     }
     const uint32_t at = block_append(extra > 0, &st->n_split, sh, &base_sh);
     if (extra > 0) ctx.split[at] = make_uint2(ctx.lcold[j], extra);
+    if (j < nlive) ctx.lsplit[j] = extra > 0 ? 1 : 0;
   }
 }
 
@@ -421,39 +422,60 @@ __global__ void __launch_bounds__(kBlock) k_shift_scatter(Ctx ctx) {
 }
 
 // New colour of every node: b + shift(b).  Members of the classes that
-// split are rewritten by k_live_emit afterwards.
+// split are rewritten by k_live_emit afterwards.  Four nodes per thread and
+// step (16-byte accesses when the colour array allows).
+__device__ __forceinline__ uint32_t shift_lds(const uint32_t* scol, const uint32_t* scum,
+                                              uint32_t S, uint32_t b) {
+  // b > scol[0]: last split colour < b
+  uint32_t lo = 0, hi = S - 1;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi + 1) >> 1;
+    if (scol[mid] < b) lo = mid; else hi = mid - 1;
+  }
+  return scum[lo];
+}
+
 __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
   const uint32_t S = st->n_split;
   const uint32_t n = ctx.n;
-  if (st->shift_big) {
-    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-      const uint32_t b = ctx.c[i];
-      const uint32_t sft = ctx.shift[b];
-      if (sft) ctx.c[i] = b + sft;
-    }
-    return;
-  }
+  const bool big = st->shift_big != 0;
   __shared__ uint32_t scol[kShiftLds];
   __shared__ uint32_t scum[kShiftLds];
-  for (uint32_t t = threadIdx.x; t < S; t += kBlock) {
-    const uint2 e = ctx.split[t];
-    scol[t] = e.x;
-    scum[t] = e.y;
-  }
-  __syncthreads();
-  const uint32_t first = scol[0];
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
-    const uint32_t b = ctx.c[i];
-    if (b <= first) continue;
-    // last split colour < b
-    uint32_t lo = 0, hi = S - 1;
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi + 1) >> 1;
-      if (scol[mid] < b) lo = mid; else hi = mid - 1;
+  if (!big) {
+    for (uint32_t t = threadIdx.x; t < S; t += kBlock) {
+      const uint2 e = ctx.split[t];
+      scol[t] = e.x;
+      scum[t] = e.y;
     }
-    ctx.c[i] = b + scum[lo];
+    __syncthreads();
+  }
+  const uint32_t first = big ? 0u : scol[0];
+  auto moved = [&](uint32_t b) -> uint32_t {
+    if (big) return b + ctx.shift[b];
+    return b <= first ? b : b + shift_lds(scol, scum, S, b);
+  };
+  const uint32_t tid = blockIdx.x * kBlock + threadIdx.x, stride = gridDim.x * kBlock;
+  uint32_t done4 = 0;
+  if (((uintptr_t)ctx.c & 15) == 0) {
+    uint4* c4 = (uint4*)ctx.c;
+    const uint32_t n4 = n / 4;
+    for (uint32_t i = tid; i < n4; i += stride) {
+      const uint4 a = c4[i];
+      uint4 r;
+      r.x = moved(a.x);
+      r.y = moved(a.y);
+      r.z = moved(a.z);
+      r.w = moved(a.w);
+      if (r.x != a.x || r.y != a.y || r.z != a.z || r.w != a.w) c4[i] = r;
+    }
+    done4 = n4 * 4;
+  }
+  for (uint32_t i = done4 + tid; i < n; i += stride) {
+    const uint32_t b = ctx.c[i];
+    const uint32_t r = moved(b);
+    if (r != b) ctx.c[i] = r;
   }
 }
 
@@ -468,10 +490,13 @@ __global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
     const uint32_t j = ctx.qcls[q];
     const uint32_t g = ctx.ids[q];
     const uint32_t id = ctx.lcold[j] + g - j;
-    ctx.c[v] = id;
     const uint32_t gs = ctx.gstart[g];
     const uint32_t len = ctx.gend[g] - gs;
-    if (!(len >= 2 && ctx.gnz[g])) {
+    // a class that did not split: its colour was moved by k_shift_apply and
+    // it stays live (it has an active member)
+    const bool split = ctx.lsplit[j] != 0;
+    if (split) ctx.c[v] = id;
+    if (split && !(len >= 2 && ctx.gnz[g])) {
       if (ctx.act[v]) ctx.act[v] = 0;
       continue;
     }
