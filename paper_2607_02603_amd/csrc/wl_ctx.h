@@ -56,6 +56,8 @@ struct DevState {
   uint32_t shift_big;   // 1 when the splits need the per-colour shift table
   uint32_t lbin_cnt[kNumBins];    // live rows per length bin (this round)
   uint32_t lbin_start[kNumBins];
+  uint32_t max_deg;     // largest row length (saturated at 2^32 - 1)
+  uint32_t deg_nd;      // distinct row lengths (one-colour round)
   uint64_t seed;
   unsigned long long work_rows;     // diagnostics: rows the SpMV computed
   unsigned long long work_entries;  // diagnostics: entries it gathered

@@ -1,0 +1,262 @@
+// The round of Algorithm 1 (Section 4.1) that starts from a single colour on
+// an unweighted graph, done without sorting the nodes.
+//
+// With one colour every neighbour carries the same random value w, so the
+// image is z_i = deg_i * w (mod p) and the new colour of node i is the rank
+// of deg_i * w among the distinct values d * w over the degrees d present
+// (equal degrees give equal values; for w != 0 distinct degrees below p give
+// distinct values, and the ranks are taken over the values themselves, so
+// w = 0 is handled as well).  The work is a degree histogram, a sort of the
+// distinct degrees' values (at most kDegRanks of them, in one workgroup), and
+// a counting placement of the nodes of the new live classes, class after
+// class, into the member list of the incremental rounds (wl_live.h).
+// A graph with more distinct values than kDegRanks takes the general path.
+#pragma once
+#include "wl_live.h"
+
+namespace wl {
+
+constexpr uint32_t kDegRanks = 4096;  // distinct degrees handled in one workgroup
+constexpr uint32_t kDegLds = 2048;    // degrees counted in LDS (larger: global atomics)
+constexpr int kDegThreads = 1024;
+
+// Scratch of the degree round (carved from the 'keys' region, 8 bytes per
+// node: the degree table takes max_deg + 1 words, the rest sits behind it).
+struct DegScratch {
+  uint32_t* dcount;  // max_deg + 1: nodes per degree, then rank | live bit
+  uint32_t* dlist;   // kDegRanks: present degrees (unordered)
+  uint32_t* roff;    // kDegRanks: first member-list position of each rank
+  uint32_t* rcur;    // kDegRanks: placement cursors
+  uint32_t* rj;      // kDegRanks: live class index of each rank
+  uint32_t* nd;      // number of present degrees (DevState::deg_nd)
+};
+
+constexpr uint32_t kDegLive = 0x80000000u;
+
+__device__ __forceinline__ uint32_t degree_of(const Ctx& ctx, uint32_t i, bool rp64) {
+  return rp64 ? (uint32_t)(ctx.rp64[i + 1] - ctx.rp64[i]) : ctx.rp32[i + 1] - ctx.rp32[i];
+}
+
+__global__ void __launch_bounds__(kBlock) k_deg_clear(Ctx ctx, DegScratch d, uint32_t maxd) {
+  for (uint32_t x = blockIdx.x * kBlock + threadIdx.x; x <= maxd; x += gridDim.x * kBlock)
+    d.dcount[x] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *d.nd = 0;
+}
+
+// Nodes per degree.
+template <bool RP64>
+__global__ void __launch_bounds__(kBlock) k_deg_hist(Ctx ctx, DegScratch d) {
+  __shared__ uint32_t h[kDegLds];
+  for (uint32_t x = threadIdx.x; x < kDegLds; x += kBlock) h[x] = 0;
+  __syncthreads();
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n; i += gridDim.x * kBlock) {
+    const uint32_t g = degree_of(ctx, i, RP64);
+    if (g < kDegLds)
+      atomicAdd(&h[g], 1u);
+    else
+      atomicAdd(&d.dcount[g], 1u);
+  }
+  __syncthreads();
+  for (uint32_t x = threadIdx.x; x < kDegLds; x += kBlock)
+    if (h[x]) atomicAdd(&d.dcount[x], h[x]);
+}
+
+// Present degrees, unordered (at most kDegRanks are kept; *nd counts all).
+__global__ void __launch_bounds__(kBlock) k_deg_list(Ctx ctx, DegScratch d, uint32_t maxd) {
+  __shared__ uint32_t sh[kBlock / kWave];
+  __shared__ uint32_t base_sh;
+  for (uint32_t x0 = blockIdx.x * kBlock; x0 <= maxd; x0 += gridDim.x * kBlock) {
+    const uint32_t x = x0 + threadIdx.x;
+    const bool present = x <= maxd && d.dcount[x] != 0;
+    const uint32_t at = block_append(present, d.nd, sh, &base_sh);
+    if (present && at < kDegRanks) d.dlist[at] = x;
+  }
+}
+
+// One workgroup: values d * w of the present degrees, sorted; rank of every
+// degree = number of distinct smaller values; per rank its node count and
+// whether it forms a live class (>= 2 nodes, a non-empty row); live classes
+// numbered in rank order with their member-list offsets.  Writes the next
+// round's live class table and counts, k_new and nosplit.
+__global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d) {
+  DevState* st = ctx.st;
+  const uint32_t D = *d.nd;
+  if (D > kDegRanks) return;  // the host takes the general path
+  __shared__ unsigned long long key[kDegRanks];
+  __shared__ uint32_t deg[kDegRanks];
+  __shared__ uint32_t rk[kDegRanks];    // rank of sorted slot t
+  __shared__ uint32_t wsum[kDegThreads / kWave];
+  __shared__ uint32_t wsum2[kDegThreads / kWave];
+  const uint64_t w = color_weight(round_key(st->seed, st->round), 0);
+  uint32_t P = 1;
+  while (P < D) P <<= 1;
+  for (uint32_t t = threadIdx.x; t < P; t += kDegThreads) {
+    if (t < D) {
+      const uint32_t g = d.dlist[t];
+      deg[t] = g;
+      key[t] = mulp(fold61(g), w);
+    } else {
+      deg[t] = 0xFFFFFFFFu;
+      key[t] = ~0ull;
+    }
+  }
+  __syncthreads();
+  for (uint32_t kk = 2; kk <= P; kk <<= 1)
+    for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+      for (uint32_t i = threadIdx.x; i < P; i += kDegThreads) {
+        const uint32_t l = i ^ j;
+        if (l > i) {
+          const bool asc = (i & kk) == 0;
+          const unsigned long long a = key[i], b = key[l];
+          // ties broken by degree so the order is total
+          const bool gt = a > b || (a == b && deg[i] > deg[l]);
+          if (gt == asc) {
+            key[i] = b;
+            key[l] = a;
+            const uint32_t tv = deg[i];
+            deg[i] = deg[l];
+            deg[l] = tv;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  // rank of slot t = distinct keys before it (block scan of "new key" flags)
+  constexpr uint32_t kPer = kDegRanks / kDegThreads;
+  const uint32_t t0 = threadIdx.x * kPer;
+  const int lane = lane_id(), wid = threadIdx.x / kWave;
+  {
+    uint32_t loc = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u) {
+      const uint32_t t = t0 + u;
+      if (t < D && (t == 0 || key[t] != key[t - 1])) ++loc;
+    }
+    const uint32_t inc = wave_incl_scan(loc);
+    if (lane == kWave - 1) wsum[wid] = inc;
+    __syncthreads();
+    uint32_t run = inc - loc;
+    for (int x = 0; x < wid; ++x) run += wsum[x];
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u) {
+      const uint32_t t = t0 + u;
+      if (t < D) {
+        if (t == 0 || key[t] != key[t - 1]) ++run;
+        rk[t] = run - 1;
+      }
+    }
+  }
+  __syncthreads();
+  // per rank (at its first slot): size and liveness, summed over the slots
+  // that share it (several degrees share a rank only when w = 0)
+  {
+    uint32_t cnt_loc = 0, live_loc = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u) {
+      const uint32_t t = t0 + u;
+      if (t < D && (t == 0 || rk[t] != rk[t - 1])) {
+        uint32_t size = 0;
+        bool nonnull = false;
+        for (uint32_t s = t; s < D && rk[s] == rk[t]; ++s) {
+          size += d.dcount[deg[s]];
+          nonnull = nonnull || deg[s] > 0;
+        }
+        const bool live = size >= 2 && nonnull;
+        // stash size and liveness in the rank table entry of the first slot
+        d.roff[rk[t]] = live ? size : 0u;
+        cnt_loc += live ? size : 0u;
+        live_loc += live ? 1u : 0u;
+      }
+    }
+    __syncthreads();
+    const uint32_t inc = wave_incl_scan(cnt_loc);
+    const uint32_t inc2 = wave_incl_scan(live_loc);
+    if (lane == kWave - 1) {
+      wsum[wid] = inc;
+      wsum2[wid] = inc2;
+    }
+    __syncthreads();
+    uint32_t off = inc - cnt_loc, jn = inc2 - live_loc;
+    uint32_t tot = 0, totj = 0;
+    for (int x = 0; x < kDegThreads / kWave; ++x) {
+      if (x < wid) {
+        off += wsum[x];
+        jn += wsum2[x];
+      }
+      tot += wsum[x];
+      totj += wsum2[x];
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u) {
+      const uint32_t t = t0 + u;
+      if (t < D && (t == 0 || rk[t] != rk[t - 1])) {
+        const uint32_t r = rk[t];
+        const uint32_t size = d.roff[r];
+        const bool live = size != 0;
+        d.rj[r] = live ? jn : 0xFFFFFFFFu;
+        d.roff[r] = off;
+        d.rcur[r] = off;
+        if (live) {
+          ctx.lcold2[jn] = r;
+          ctx.loff2[jn] = off;
+          ctx.llen2[jn] = size;
+        }
+        off += size;
+        jn += live ? 1u : 0u;
+      }
+    }
+    if (threadIdx.x == 0) {
+      const uint32_t k_new = D ? rk[D - 1] + 1 : 0;
+      st->n_live2 = totj;
+      st->nl2 = tot;
+      st->k_new = k_new;
+      st->nosplit = k_new == st->k ? 1u : 0u;
+      st->split_any = 1u - st->nosplit;
+    }
+  }
+  __syncthreads();
+  // degree table -> rank | live bit
+  for (uint32_t t = threadIdx.x; t < D; t += kDegThreads) {
+    const uint32_t r = rk[t];
+    d.dcount[deg[t]] = r | (d.rj[r] != 0xFFFFFFFFu ? kDegLive : 0u);
+  }
+}
+
+// New colour of every node; members of live classes placed class after
+// class into the '2' member list (counting placement: one cursor reservation
+// per block and rank), act for every node.
+template <bool RP64>
+__global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
+  const DevState* st = ctx.st;
+  if (*d.nd > kDegRanks || st->nosplit) return;
+  __shared__ uint32_t lc[kDegRanks];
+  const uint32_t K = st->k_new;
+  const uint32_t n = ctx.n;
+  const uint32_t per = ((n + gridDim.x - 1) / gridDim.x + kBlock - 1) / kBlock * kBlock;
+  const uint32_t lo = min(n, blockIdx.x * per), hi = min(n, lo + per);
+  for (uint32_t r = threadIdx.x; r < K; r += kBlock) lc[r] = 0;
+  __syncthreads();
+  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+    const uint32_t e = d.dcount[degree_of(ctx, i, RP64)];
+    if (e & kDegLive) atomicAdd(&lc[e & ~kDegLive], 1u);
+  }
+  __syncthreads();
+  for (uint32_t r = threadIdx.x; r < K; r += kBlock)
+    if (lc[r]) lc[r] = atomicAdd(&d.rcur[r], lc[r]);
+  __syncthreads();
+  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+    const uint32_t g = degree_of(ctx, i, RP64);
+    const uint32_t e = d.dcount[g];
+    const uint32_t r = e & ~kDegLive;
+    ctx.c[i] = r;
+    const bool live = (e & kDegLive) != 0;
+    ctx.act[i] = live && g > 0 ? 1 : 0;
+    if (live) {
+      const uint32_t q = atomicAdd(&lc[r], 1u);
+      ctx.lperm2[q] = i;
+      ctx.qcls2[q] = d.rj[r];
+    }
+  }
+}
+
+}  // namespace wl

@@ -13,6 +13,7 @@
 #include <memory>
 #include <new>
 #include <thread>
+#include <type_traits>
 #include <utility>
 #include <vector>
 #include <cstdarg>
@@ -24,6 +25,7 @@
 #include "wl_ctx.h"
 #include "wl_relabel.h"
 #include "wl_live.h"
+#include "wl_degree.h"
 #include "wl_spmv.h"
 #include "wl_push.h"
 #include "wl_quotient.h"
@@ -130,8 +132,8 @@ struct PbLayout {
   bool ok = false;
   uint32_t levels = 0, shift1 = 0, nb1 = 0, nfine = 0, fbits = 0;
   uint64_t ntiles1 = 0;
-  uint64_t cnt = 0, bstart1 = 0, bstartf = 0, rec1 = 0, rec2 = 0, table = 0, gsum = 0,
-           tile_row = 0, tile2_off = 0, cur2 = 0, slice_off = 0, mslice_off = 0, mlist = 0,
+  uint64_t cnt = 0, bstart1 = 0, bstartf = 0, rec1 = 0, rec2 = 0, tile_row = 0,
+           tile2_off = 0, cur1 = 0, cur2 = 0, slice_off = 0, mslice_off = 0, mlist = 0,
            part = 0;
   uint64_t total = 0;
 };
@@ -168,10 +170,9 @@ PbLayout make_pb_layout(uint64_t n, uint64_t nnz) {
   P.bstartf = take(8 * (nf + 1));
   P.rec1 = take(P.levels == 2 ? 4 * nnz : 0);
   P.rec2 = take(4 * nnz);
-  P.table = take(4 * P.ntiles1 * P.nb1);
-  P.gsum = take(4ull * kPbGroups * P.nb1);
   P.tile_row = take(4 * P.ntiles1);
   P.tile2_off = take(4ull * (P.nb1 + 1));
+  P.cur1 = take(8ull * P.nb1);
   P.cur2 = take(8 * nf);
   P.slice_off = take(4 * (nf + 1));
   P.mslice_off = take(4 * (nf + 1));
@@ -444,6 +445,9 @@ struct Session {
   PbLayout P;
   PbCtx pb{};
   SpmvGrid live_grid{};
+  // The one-colour round by degree histogram (WL_DEGREE_ROUND=0 turns it off,
+  // for testing the general path).
+  bool deg_mode = true;
   PbCounts pbc{};
   bool pb_avail = false, pb_planned = false, pb_stop = false;
   bool sym_flag = false;
@@ -633,17 +637,10 @@ struct Session {
                        ctx, pb);
     hipLaunchKernelGGL(k_pb_tile_rows<RP>, dim3(grid_for(L.n, kBlock, 8192)), dim3(kBlock), 0, s,
                        ctx, pb);
-    hipLaunchKernelGGL(k_pb_hist1, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 4096)),
-                       dim3(kPbThreads), 0, s, ctx, pb);
-    hipLaunchKernelGGL(k_pb_colsum, dim3(kPbGroups), dim3(kPbThreads), 0, s, pb);
-    hipLaunchKernelGGL(k_pb_colscan<RP>, dim3(1), dim3(kPbThreads), 0, s, ctx, pb);
-    hipLaunchKernelGGL(k_pb_colapply, dim3(kPbGroups), dim3(kPbThreads), 0, s, pb);
     hipLaunchKernelGGL(k_pb_lists<RP>, dim3(1), dim3(kPbThreads), 0, s, ctx, pb);
     HIP_LAUNCH_CHECK();
     HIP_TRY(hipMemcpyAsync(&pbc, pb.cnt, sizeof(PbCounts), hipMemcpyDeviceToHost, s));
     if (int r = pull()) return r;
-    if (host.err & kErrNotSymmetric)
-      return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
     pb_planned = true;
     return WL_OK;
   }
@@ -684,12 +681,11 @@ struct Session {
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
                          ctx, 1);
+    hipLaunchKernelGGL(k_pb_cursors, dim3(grid_for(P.nfine)), dim3(kBlock), 0, s, ctx, pb);
     timed_spmv(host.round, true, false, [&] {
       hipLaunchKernelGGL(k_pb_scatter1<RP>, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 2048)),
                          dim3(kPbThreads), 0, s, ctx, pb);
       if (P.levels == 2) {
-        hipLaunchKernelGGL(k_pb_cursors, dim3(grid_for(P.nfine)), dim3(kBlock), 0, s, ctx,
-                           pb);
         hipLaunchKernelGGL(k_pb_scatter2, dim3(std::max<uint32_t>(1, std::min<uint32_t>(pbc.ntiles2, 2048))),
                            dim3(kPbThreads), 0, s, ctx, pb);
       }
@@ -960,10 +956,63 @@ struct Session {
     hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
   }
 
+  // The one-colour round of an unweighted graph without a sort
+  // (wl_degree.h).  *handled is false when the graph has more distinct
+  // degrees than one workgroup ranks; the caller then runs the general round.
+  template <bool RP64>
+  int degree_round(bool* handled) {
+    *handled = false;
+    const uint32_t maxd = host.max_deg;
+    DegScratch d;
+    uint32_t* base = (uint32_t*)ctx.keys_tmp;
+    d.dcount = base;
+    d.dlist = base + (uint64_t)maxd + 1;
+    d.roff = d.dlist + kDegRanks;
+    d.rcur = d.roff + kDegRanks;
+    d.rj = d.rcur + kDegRanks;
+    d.nd = &ctx.st->deg_nd;
+    const uint32_t gd = grid_for((uint64_t)maxd + 1, kBlock, 4096);
+    using RPT = typename std::conditional<RP64, uint64_t, uint32_t>::type;
+    if (sflags & WL_STATS_WORK)
+      hipLaunchKernelGGL(k_count_work<RPT>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
+                         s, ctx, 0);
+    timed_spmv(host.round, true, true, [&] {
+      hipLaunchKernelGGL(k_deg_clear, dim3(gd), dim3(kBlock), 0, s, ctx, d, maxd);
+      hipLaunchKernelGGL(k_deg_hist<RP64>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
+                         s, ctx, d);
+    });
+    hipLaunchKernelGGL(k_deg_list, dim3(gd), dim3(kBlock), 0, s, ctx, d, maxd);
+    hipLaunchKernelGGL(k_deg_ranks, dim3(1), dim3(kDegThreads), 0, s, ctx, d);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    if (host.deg_nd > kDegRanks) return WL_OK;
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_deg_place<RP64>, dim3(grid_for(L.n, kBlock, 2048)), dim3(kBlock), 0, s,
+                       ctx, d);
+    hipLaunchKernelGGL(k_live_commit, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    *handled = true;
+    return WL_OK;
+  }
+
+  // Whether the degree round's table and lists fit the scratch it uses (the
+  // keys_tmp region, two words per node).
+  bool degree_round_fits() const {
+    const uint64_t words = (uint64_t)host.max_deg + 1 + 4ull * kDegRanks;
+    return host.max_deg < 0x7FFFFFFFu && words <= 2 * L.n;
+  }
+
   // One round of the incremental relabel driven from the host (counts read
   // back to size the sorts).
   int round_live() {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
+    if (host.k == 1 && !weighted && !ctx.batch && degree_round_fits() && deg_mode) {
+      bool handled = false;
+      if (int r = rp64 ? degree_round<true>(&handled) : degree_round<false>(&handled)) return r;
+      if (handled) return WL_OK;
+    }
     if (int r = spmv_live()) return r;
     live_segments();
     HIP_LAUNCH_CHECK();
@@ -1078,6 +1127,7 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
     S.pb_mode = !m ? 1 : (strcmp(m, "0") == 0 ? 0 : (strcmp(m, "force") == 0 ? 2 : 1));
   }
   S.sym_flag = (g->flags & WL_CSR_SYMMETRIC) != 0;
+  S.deg_mode = env_int("WL_DEGREE_ROUND", 0, 1, 1) != 0;
   if (wants_pb(g) && S.pb_mode != 0) {
     S.P = make_pb_layout(g->n, g->nnz);
     // pass 1 reads the column indices 16 bytes at a time
@@ -1095,10 +1145,9 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
       p.bstartf = (uint64_t*)(B + S.P.bstartf);
       p.rec1 = (uint32_t*)(B + S.P.rec1);
       p.rec2 = (uint32_t*)(B + S.P.rec2);
-      p.table = (uint32_t*)(B + S.P.table);
-      p.gsum = (uint32_t*)(B + S.P.gsum);
       p.tile_row = (uint32_t*)(B + S.P.tile_row);
       p.tile2_off = (uint32_t*)(B + S.P.tile2_off);
+      p.cur1 = (unsigned long long*)(B + S.P.cur1);
       p.cur2 = (unsigned long long*)(B + S.P.cur2);
       p.slice_off = (uint32_t*)(B + S.P.slice_off);
       p.mslice_off = (uint32_t*)(B + S.P.mslice_off);

@@ -9,7 +9,7 @@
 //   pass 1  stream the CSR entries in order; each tile of kPbTile entries
 //           turns them into records (destination row inside its bin, colour
 //           of the source row), counting-sorts them by bin in LDS and writes
-//           one run per bin, at an offset computed once per call;
+//           one run per bin, reserved with an atomic on the bin's cursor;
 //   pass 2  only when there are more than kPbMaxBins fine bins: pass 1 used
 //           coarse bins of 2^fbits fine bins each; every coarse bin is split
 //           into its fine bins the same way (run offsets from atomics);
@@ -37,7 +37,6 @@ constexpr uint32_t kPbTile2 = 8192;                   // records per pass-2 tile
 constexpr uint32_t kPbSlice = 1u << 20;               // records per pass-3 item
 constexpr int kPbThreads = 256;                       // pass 1 and 2
 constexpr int kPbAccThreads = 1024;                   // pass 3
-constexpr uint32_t kPbGroups = 1024;                  // groups of the table scan
 constexpr uint32_t kPbPerThread = kPbTile / kPbThreads;
 constexpr uint32_t kErrNotSymmetric = 16u;  // DevState::err bit
 constexpr uint64_t kPbMinEntries = 1ull << 22;  // smaller graphs stay in cache
@@ -62,11 +61,10 @@ struct PbCtx {
   uint64_t* bstartf;   // nfine + 1: the same for the fine bins
   uint32_t* rec1;      // pass-1 records (coarse bins; levels == 2)
   uint32_t* rec2;      // fine-bin records
-  uint32_t* table;     // ntiles1 x nb1: start of each tile's run inside its bin
-  uint32_t* gsum;      // kPbGroups x nb1: scan scratch
   uint32_t* tile_row;  // ntiles1: row that holds the first entry of each tile
   uint32_t* tile2_off; // nb1 + 1: pass-2 tiles before each coarse bin
-  unsigned long long* cur2;  // nfine: write cursors of pass 2
+  unsigned long long* cur1;  // nb1: write cursors of pass 1 (levels == 2)
+  unsigned long long* cur2;  // nfine: write cursors of the fine bins
   uint32_t* slice_off;       // nfine + 1: pass-3 items before each fine bin
   uint32_t* mslice_off;      // nfine + 1: partial-sum slots before each bin
   uint32_t* mlist;           // fine bins with several slices
@@ -128,77 +126,6 @@ __global__ void __launch_bounds__(kBlock) k_pb_tile_rows(Ctx ctx, PbCtx pb) {
   }
 }
 
-// Records of every pass-1 tile per bin.
-__global__ void __launch_bounds__(kPbThreads) k_pb_hist1(Ctx ctx, PbCtx pb) {
-  __shared__ uint32_t h[kPbMaxBins];
-  for (uint64_t t = blockIdx.x; t < pb.ntiles1; t += gridDim.x) {
-    for (uint32_t b = threadIdx.x; b < pb.nb1; b += kPbThreads) h[b] = 0;
-    __syncthreads();
-    const uint64_t e0 = t * kPbTile, e1 = min(ctx.nnz, e0 + kPbTile);
-    uint32_t v[kPbTile / kPbThreads];
-#pragma unroll
-    for (uint32_t k = 0; k < kPbTile / kPbThreads; ++k) {
-      const uint64_t e = e0 + k * kPbThreads + threadIdx.x;
-      v[k] = e < e1 ? ctx.col[e] : 0xFFFFFFFFu;
-    }
-#pragma unroll
-    for (uint32_t k = 0; k < kPbTile / kPbThreads; ++k)
-      if (v[k] != 0xFFFFFFFFu) atomicAdd(&h[v[k] >> pb.shift1], 1u);
-    __syncthreads();
-    for (uint32_t b = threadIdx.x; b < pb.nb1; b += kPbThreads) pb.table[t * pb.nb1 + b] = h[b];
-    __syncthreads();
-  }
-}
-
-__device__ __forceinline__ void pb_group_range(const PbCtx& pb, uint32_t g, uint64_t* lo,
-                                               uint64_t* hi) {
-  const uint64_t per = (pb.ntiles1 + kPbGroups - 1) / kPbGroups;
-  *lo = min(pb.ntiles1, (uint64_t)g * per);
-  *hi = min(pb.ntiles1, *lo + per);
-}
-
-// Column sums of the table per group of tiles.
-__global__ void __launch_bounds__(kPbThreads) k_pb_colsum(PbCtx pb) {
-  const uint32_t b = threadIdx.x;
-  if (b >= pb.nb1) return;
-  uint64_t lo, hi;
-  pb_group_range(pb, blockIdx.x, &lo, &hi);
-  uint32_t s = 0;
-  for (uint64_t t = lo; t < hi; ++t) s += pb.table[t * pb.nb1 + b];
-  pb.gsum[blockIdx.x * pb.nb1 + b] = s;
-}
-
-// Exclusive scan of the group sums per bin.  The records bound for a bin
-// must fill exactly the entry range of its rows, which holds for a
-// symmetric A; a mismatch proves A is not symmetric and sets an error bit
-// (no record is written then).
-template <typename RP>
-__global__ void __launch_bounds__(kPbThreads) k_pb_colscan(Ctx ctx, PbCtx pb) {
-  const uint32_t b = threadIdx.x;
-  if (b >= pb.nb1) return;
-  uint64_t run = 0;
-  for (uint32_t g = 0; g < kPbGroups; ++g) {
-    const uint32_t v = pb.gsum[g * pb.nb1 + b];
-    pb.gsum[g * pb.nb1 + b] = (uint32_t)run;
-    run += v;
-  }
-  if (run != pb.bstart1[b + 1] - pb.bstart1[b]) atomicOr(&ctx.st->err, kErrNotSymmetric);
-}
-
-// table[t][b] = records of bin b in tiles before t (offset inside the bin).
-__global__ void __launch_bounds__(kPbThreads) k_pb_colapply(PbCtx pb) {
-  const uint32_t b = threadIdx.x;
-  if (b >= pb.nb1) return;
-  uint64_t lo, hi;
-  pb_group_range(pb, blockIdx.x, &lo, &hi);
-  uint32_t run = pb.gsum[blockIdx.x * pb.nb1 + b];
-  for (uint64_t t = lo; t < hi; ++t) {
-    const uint32_t v = pb.table[t * pb.nb1 + b];
-    pb.table[t * pb.nb1 + b] = run;
-    run += v;
-  }
-}
-
 // One block: pass-2 tiles per coarse bin, pass-3 slices per fine bin, and
 // the list of fine bins with several slices.
 template <typename RP>
@@ -257,39 +184,57 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_lists(Ctx ctx, PbCtx pb) {
 // Pass 1: CSR entries -> records in pass-1 bins
 // ---------------------------------------------------------------------------
 
+// Exclusive "last non-zero" scan across the lanes of a wave: for each lane,
+// the last non-zero value held by a lower lane (0 if none).
+__device__ __forceinline__ uint32_t wave_last_nonzero_excl(uint32_t v, uint32_t* incl) {
+  const int lane = lane_id();
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const uint32_t o = __shfl_up(x, off, kWave);
+    if (lane >= off && x == 0) x = o;
+  }
+  *incl = x;
+  const uint32_t ex = __shfl_up(x, 1, kWave);
+  return lane == 0 ? 0u : ex;
+}
+
+// Each tile of kPbTile entries: the colour of every entry's row (row starts
+// marked in LDS, then each thread fills forward over 32 consecutive entries
+// with a carry from the threads before it), records binned in LDS, one run
+// per bin reserved with an atomic on the bin's cursor and written out.  A
+// bin whose runs would pass its end proves A is not symmetric: the run is
+// not written and an error bit is set (every later pass then stops).
 template <typename RP>
 __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
   if (ctx.st->done) return;
-  __shared__ __align__(16) uint32_t buf[kPbTile];  // colour+1 at row starts, colours, records
+  __shared__ __align__(16) uint32_t buf[kPbTile];  // row marks, colours, records
   __shared__ uint8_t sbin[kPbTile];                // bin of each staged record
   __shared__ uint32_t hist[kPbMaxBins];
   __shared__ uint32_t base[kPbMaxBins];
-  __shared__ uint64_t dst[kPbMaxBins];  // output position of the tile's run per bin
+  __shared__ long long dd[kPbMaxBins];  // output index of staged slot q: dd[bin] + q
   __shared__ uint32_t wlast[kPbThreads / kWave];
   __shared__ uint32_t sh[kPbThreads / kWave];
-  const int lane = lane_id();
+  constexpr long long kSkip = -(1ll << 62);
+  constexpr uint32_t kRun = kPbTile / kPbThreads;  // entries per thread
   const int wid = threadIdx.x / kWave;
   const uint32_t mask1 = (1u << pb.shift1) - 1;
-  uint32_t* out = pb.levels == 2 ? pb.rec1 : pb.rec2;
+  const bool two = pb.levels == 2;
+  uint32_t* out = two ? pb.rec1 : pb.rec2;
+  unsigned long long* cur = two ? pb.cur1 : pb.cur2;
+  const uint64_t* bstart = two ? pb.bstart1 : pb.bstartf;
   const uint4* col4 = (const uint4*)ctx.col;
-  // rows of the next tile, loaded one tile ahead
-  uint32_t j0n = 0, jendn = 0;
-  if (blockIdx.x < pb.ntiles1) {
-    j0n = pb.tile_row[blockIdx.x];
-    jendn = blockIdx.x + 1 < pb.ntiles1 ? pb.tile_row[blockIdx.x + 1] : ctx.n - 1;
-  }
   for (uint64_t t = blockIdx.x; t < pb.ntiles1; t += gridDim.x) {
     const uint64_t e0 = t * kPbTile, e1 = min(ctx.nnz, e0 + kPbTile);
     const uint32_t cnt = (uint32_t)(e1 - e0);
-    const uint32_t j0 = j0n, jend = jendn;
-    // everything the tile reads from memory is requested first: its column
-    // indices (4 consecutive entries per load; slot (k, u) holds entry
-    // 4 * (k * kPbThreads + threadIdx.x) + u), its run offsets, the first
-    // row's colour and one row start per thread
-    uint32_t cix[kPbPerThread];
+    const uint32_t j0 = pb.tile_row[t];
+    const uint32_t jend = t + 1 < pb.ntiles1 ? pb.tile_row[t + 1] : ctx.n - 1;
+    // column indices, 4 consecutive entries per load: slot (k, u) holds
+    // entry 4 * (k * kPbThreads + threadIdx.x) + u
+    uint32_t cix[kRun];
     if (cnt == kPbTile) {
 #pragma unroll
-      for (uint32_t k = 0; k < kPbPerThread / 4; ++k) {
+      for (uint32_t k = 0; k < kRun / 4; ++k) {
         const uint4 v = col4[(e0 >> 2) + k * kPbThreads + threadIdx.x];
         cix[4 * k] = v.x;
         cix[4 * k + 1] = v.y;
@@ -298,86 +243,74 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
       }
     } else {
 #pragma unroll
-      for (uint32_t k = 0; k < kPbPerThread / 4; ++k)
+      for (uint32_t k = 0; k < kRun / 4; ++k)
 #pragma unroll
         for (uint32_t u = 0; u < 4; ++u) {
           const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
           cix[4 * k + u] = q < cnt ? ctx.col[e0 + q] : 0u;
         }
     }
-    uint64_t my_dst = 0;
-    if (threadIdx.x < pb.nb1) my_dst = pb.bstart1[threadIdx.x] + pb.table[t * pb.nb1 + threadIdx.x];
     const uint32_t c_first = ctx.c[j0];
-    const uint32_t r_mine = j0 + 1 + threadIdx.x;
-    uint64_t rb = 0, re = 0;
-    uint32_t rc = 0;
-    if (r_mine <= jend) {
-      rb = rp_at<RP>(ctx, r_mine);
-      re = rp_at<RP>(ctx, r_mine + 1);
-      rc = ctx.c[r_mine];
-    }
-    {
-      const uint64_t tn = t + gridDim.x;
-      if (tn < pb.ntiles1) {
-        j0n = pb.tile_row[tn];
-        jendn = tn + 1 < pb.ntiles1 ? pb.tile_row[tn + 1] : ctx.n - 1;
-      }
-    }
-    for (uint32_t q = threadIdx.x; q < kPbTile; q += kPbThreads) buf[q] = 0;
-    if (threadIdx.x < pb.nb1) {
-      hist[threadIdx.x] = 0;
-      dst[threadIdx.x] = my_dst;
-    }
+    const uint4 z4 = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (uint32_t k = 0; k < kRun / 4; ++k) ((uint4*)buf)[k * kPbThreads + threadIdx.x] = z4;
+    if (threadIdx.x < kPbMaxBins) hist[threadIdx.x] = 0;
     __syncthreads();
-    // colour + 1 at the first entry of every row that starts in the tile
-    if (r_mine <= jend && rb < e1 && re > rb) buf[rb - e0] = rc + 1;
-    for (uint32_t r = r_mine + kPbThreads; r <= jend; r += kPbThreads) {
+    // colour + 1 at the first entry of every non-empty row starting in the tile
+    for (uint32_t r = j0 + 1 + threadIdx.x; r <= jend; r += kPbThreads) {
       const uint64_t b = rp_at<RP>(ctx, r);
       if (b < e1 && rp_at<RP>(ctx, r + 1) > b) buf[b - e0] = ctx.c[r] + 1;
     }
     __syncthreads();
-    // every entry takes the value of the last row start at or before it,
-    // minus one: per segment of 64 entries, the highest marked lane at or
-    // below each lane (a ballot) supplies the value, else the carry
-    constexpr uint32_t per_wave = kPbTile / (kPbThreads / kWave);
-    const uint32_t w0 = wid * per_wave;
-    const unsigned long long le_mask = ~0ull >> (kWave - 1 - lane);  // lanes <= lane
+    // fill forward: thread i owns entries [kRun * i, kRun * (i + 1))
     {
+      uint4 v[kRun / 4];
       uint32_t last = 0;
-      for (uint32_t q = 0; q < per_wave; q += kWave) {
-        const uint32_t v = buf[w0 + q + lane];
-        const unsigned long long m = __ballot(v != 0);
-        if (m) last = __shfl(v, 63 - __builtin_clzll(m), kWave);
+#pragma unroll
+      for (uint32_t k = 0; k < kRun / 4; ++k) {
+        v[k] = ((const uint4*)buf)[threadIdx.x * (kRun / 4) + k];
+        if (v[k].x) last = v[k].x;
+        if (v[k].y) last = v[k].y;
+        if (v[k].z) last = v[k].z;
+        if (v[k].w) last = v[k].w;
       }
-      if (lane == 0) wlast[wid] = last;
-    }
-    __syncthreads();
-    uint32_t carry = c_first + 1;
-    for (int w = 0; w < wid; ++w)
-      if (wlast[w]) carry = wlast[w];
-    for (uint32_t q = 0; q < per_wave; q += kWave) {
-      const uint32_t v = buf[w0 + q + lane];
-      const unsigned long long m = __ballot(v != 0);
-      const unsigned long long mine = m & le_mask;
-      const int src = mine ? 63 - __builtin_clzll(mine) : 0;
-      const uint32_t got = __shfl(v, src, kWave);
-      buf[w0 + q + lane] = (mine ? got : carry) - 1;
-      if (m) carry = __shfl(v, 63 - __builtin_clzll(m), kWave);
+      uint32_t incl;
+      uint32_t carry = wave_last_nonzero_excl(last, &incl);
+      if (lane_id() == kWave - 1) wlast[wid] = incl;
+      __syncthreads();
+      if (!carry) {
+        carry = c_first + 1;
+        for (int w = 0; w < wid; ++w)
+          if (wlast[w]) carry = wlast[w];
+      }
+#pragma unroll
+      for (uint32_t k = 0; k < kRun / 4; ++k) {
+        if (v[k].x) carry = v[k].x;
+        v[k].x = carry - 1;
+        if (v[k].y) carry = v[k].y;
+        v[k].y = carry - 1;
+        if (v[k].z) carry = v[k].z;
+        v[k].z = carry - 1;
+        if (v[k].w) carry = v[k].w;
+        v[k].w = carry - 1;
+        ((uint4*)buf)[threadIdx.x * (kRun / 4) + k] = v[k];
+      }
     }
     __syncthreads();
     // records and their bins, counted per bin
-    uint32_t bin[kPbPerThread];
+    uint32_t bin[kRun];
 #pragma unroll
-    for (uint32_t k = 0; k < kPbPerThread / 4; ++k) {
-      const uint4 cv = *(const uint4*)&buf[4 * (k * kPbThreads + threadIdx.x)];
+    for (uint32_t k = 0; k < kRun / 4; ++k) {
+      const uint4 cv = ((const uint4*)buf)[k * kPbThreads + threadIdx.x];
       const uint32_t colour[4] = {cv.x, cv.y, cv.z, cv.w};
 #pragma unroll
       for (uint32_t u = 0; u < 4; ++u) {
         const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
         const uint32_t x = 4 * k + u;
         bin[x] = 0xFFFFFFFFu;
-        if (q < cnt) {
-          const uint32_t i = cix[x];
+        const uint32_t i = cix[x];
+        if (q < cnt && i >= ctx.n) atomicOr(&ctx.st->err, kErrNotSymmetric);  // invalid column
+        if (q < cnt && i < ctx.n) {
           bin[x] = i >> pb.shift1;
           cix[x] = ((i & mask1) << pb.cbits) | colour[u];  // the record
           atomicAdd(&hist[bin[x]], 1u);
@@ -385,29 +318,38 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
       }
     }
     __syncthreads();
-    {
-      // nb1 <= kPbMaxBins == kPbThreads: one bin per thread
-      const uint32_t b = threadIdx.x;
-      const uint32_t h = b < pb.nb1 ? hist[b] : 0u;
-      uint32_t tot;
-      const uint32_t ex = pb_block_scan<kPbThreads>(h, sh, &tot);
-      if (b < pb.nb1) {
-        base[b] = ex;
-        hist[b] = 0;
-      }
-      __syncthreads();
+    // run offsets inside the tile; one cursor reservation per bin (its
+    // result is first needed after the staging below)
+    const uint32_t b = threadIdx.x;
+    const uint32_t h = b < pb.nb1 ? hist[b] : 0u;
+    uint32_t tot;
+    const uint32_t ex = pb_block_scan<kPbThreads>(h, sh, &tot);
+    unsigned long long d = 0;
+    if (h) d = atomicAdd(&cur[b], (unsigned long long)h);
+    if (b < pb.nb1) {
+      base[b] = ex;
+      hist[b] = 0;
     }
+    __syncthreads();
 #pragma unroll
-    for (uint32_t x = 0; x < kPbPerThread; ++x)
+    for (uint32_t x = 0; x < kRun; ++x)
       if (bin[x] != 0xFFFFFFFFu) {
         const uint32_t slot = base[bin[x]] + atomicAdd(&hist[bin[x]], 1u);
         buf[slot] = cix[x];
         sbin[slot] = (uint8_t)bin[x];
       }
+    if (h) {
+      if (d + h > bstart[b + 1]) {
+        atomicOr(&ctx.st->err, kErrNotSymmetric);
+        dd[b] = kSkip;
+      } else {
+        dd[b] = (long long)d - (long long)ex;
+      }
+    }
     __syncthreads();
     for (uint32_t q = threadIdx.x; q < cnt; q += kPbThreads) {
-      const uint32_t b = sbin[q];
-      out[dst[b] + (q - base[b])] = buf[q];
+      const long long o = dd[sbin[q]];
+      if (o != kSkip) out[o + q] = buf[q];
     }
     __syncthreads();
   }
@@ -417,14 +359,17 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
 // Pass 2: coarse bins -> fine bins
 // ---------------------------------------------------------------------------
 
+// Write cursors of both passes: the first entry of every bin.
 __global__ void __launch_bounds__(kBlock) k_pb_cursors(Ctx ctx, PbCtx pb) {
   if (ctx.st->done) return;
-  for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < pb.nfine; f += gridDim.x * kBlock)
+  for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < pb.nfine; f += gridDim.x * kBlock) {
     pb.cur2[f] = pb.bstartf[f];
+    if (f < pb.nb1) pb.cur1[f] = pb.bstart1[f];
+  }
 }
 
 __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
-  if (ctx.st->done) return;
+  if (ctx.st->done || (ctx.st->err & kErrNotSymmetric)) return;
   __shared__ uint32_t buf[kPbTile2];
   __shared__ uint16_t sbin[kPbTile2];
   __shared__ uint32_t hist[kPbMaxFine];
@@ -520,7 +465,7 @@ constexpr uint32_t kPbTableMax = 4096;
 
 template <typename RP, bool TBL>
 __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
-  if (ctx.st->done) return;
+  if (ctx.st->done || (ctx.st->err & kErrNotSymmetric)) return;
   __shared__ unsigned long long acc_lo[kPbFineRows];
   __shared__ unsigned long long acc_hi[kPbFineRows];
   __shared__ uint64_t wtab[TBL ? kPbTableMax : 1];
@@ -599,7 +544,7 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
 
 // Bins with several slices: z = sum of the partial images.
 __global__ void __launch_bounds__(kBlock) k_pb_combine(Ctx ctx, PbCtx pb) {
-  if (ctx.st->done) return;
+  if (ctx.st->done || (ctx.st->err & kErrNotSymmetric)) return;
   const uint32_t nm = pb.cnt->nmulti;
   const uint64_t total = (uint64_t)nm * kPbFineRows;
   for (uint64_t x = blockIdx.x * (uint64_t)kBlock + threadIdx.x; x < total;

@@ -36,16 +36,22 @@ __global__ void __launch_bounds__(kBlock) k_bins_count(Ctx ctx) {
   const uint32_t per = (n + gridDim.x - 1) / gridDim.x;
   const uint32_t lo = min(n, blockIdx.x * per), hi = min(n, lo + per);
   uint32_t cnt[kNumBins] = {0, 0, 0, 0};
+  uint64_t mx = 0;
   for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
-    int b = row_bin((uint64_t)(rp[i + 1] - rp[i]));
-    cnt[b]++;
+    const uint64_t len = (uint64_t)(rp[i + 1] - rp[i]);
+    cnt[row_bin(len)]++;
+    mx = len > mx ? len : mx;
   }
   __shared__ uint32_t sh[kNumBins];
+  __shared__ uint32_t smx;
   if (threadIdx.x < kNumBins) sh[threadIdx.x] = 0;
+  if (threadIdx.x == 0) smx = 0;
   __syncthreads();
   for (int b = 0; b < kNumBins; ++b)
     if (cnt[b]) atomicAdd(&sh[b], cnt[b]);
+  atomicMax(&smx, (uint32_t)(mx < 0xFFFFFFFFull ? mx : 0xFFFFFFFFull));
   __syncthreads();
+  if (threadIdx.x == 0 && smx) atomicMax(&ctx.st->max_deg, smx);
   if (threadIdx.x < kNumBins)
     ctx.bin_part[threadIdx.x * gridDim.x + blockIdx.x] = sh[threadIdx.x];
 }
