@@ -37,4 +37,18 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* sh,
   return base + inc - v;
 }
 
+// Appends 'want' items to a device list: one atomic per block, slots
+// handed out by a block scan (order inside the list is irrelevant).
+// Contains __syncthreads(); every thread of the block must call it.
+__device__ __forceinline__ uint32_t block_append(bool want, uint32_t* counter,
+                                                 uint32_t* sh, uint32_t* base_sh) {
+  uint32_t tot;
+  const uint32_t ex = block_excl_scan(want ? 1u : 0u, sh, &tot);
+  if (threadIdx.x == 0) *base_sh = tot ? atomicAdd(counter, tot) : 0u;
+  __syncthreads();
+  const uint32_t at = *base_sh + ex;
+  __syncthreads();
+  return at;
+}
+
 }  // namespace wl

@@ -54,10 +54,10 @@ struct DevState {
   uint32_t n_split;     // live classes that split
   uint32_t split_any;   // 1 when some live class split in this round
   uint32_t shift_big;   // 1 when the splits need the per-colour shift table
-  uint32_t lbin_cnt[kNumBins];    // live rows per length bin (this round)
-  uint32_t lbin_start[kNumBins];
   uint32_t max_deg;     // largest row length (saturated at 2^32 - 1)
   uint32_t deg_nd;      // distinct row lengths (one-colour round)
+  uint32_t n_mid;       // live rows queued for one wave each (this round)
+  uint32_t n_hlive;     // live heavy rows (this round)
   uint64_t seed;
   unsigned long long work_rows;     // diagnostics: rows the SpMV computed
   unsigned long long work_entries;  // diagnostics: entries it gathered
@@ -100,7 +100,7 @@ struct Ctx {
   uint64_t* keys;      // z in position order (big segments)
   uint64_t* keys_tmp;
   uint8_t* flags;      // 1 where a new (colour, z) group starts
-  uint8_t* act;        // 1 if the node's class has >= 2 members
+  uint8_t* act;        // 1 if the node's row needs an image (see wl_live.h)
   uint32_t* ids;       // inclusive scan of flags minus one
   uint32_t* cstart;    // class c occupies perm[cstart[c] .. cstart[c+1])
   uint2* small_list;   // (start, len | kMatBit), 64 < len <= kSmallMax
@@ -147,7 +147,12 @@ struct Ctx {
   uint32_t* go;        // size, then its first position
   uint2* split;        // (old colour, extra sub-classes) of the classes that split
   uint32_t* shift;     // per colour: extra sub-classes below it (many splits)
-  uint32_t* lrows;     // live rows of the SpMV by length bin (positions of lperm)
+  uint64_t* rs;        // per position of lperm: first entry of its node's row
+  uint64_t* rs2;
+  uint32_t* rl;        // and the row's length
+  uint32_t* rl2;
+  uint32_t* midq;      // positions whose rows get one wave each (this round)
+  uint32_t* hq;        // positions with heavy rows (this round)
   uint8_t* lsplit;     // per live class: 1 if it split in this round
 };
 

@@ -245,6 +245,7 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
     if (lc[r]) lc[r] = atomicAdd(&d.rcur[r], lc[r]);
   __syncthreads();
   for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+    const uint64_t r0 = RP64 ? ctx.rp64[i] : ctx.rp32[i];
     const uint32_t g = degree_of(ctx, i, RP64);
     const uint32_t e = d.dcount[g];
     const uint32_t r = e & ~kDegLive;
@@ -255,6 +256,8 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
       const uint32_t q = atomicAdd(&lc[r], 1u);
       ctx.lperm2[q] = i;
       ctx.qcls2[q] = d.rj[r];
+      ctx.rs2[q] = r0;
+      ctx.rl2[q] = g;
     }
   }
 }

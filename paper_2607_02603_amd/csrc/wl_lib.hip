@@ -71,7 +71,8 @@ struct Layout {
   uint64_t off_st, off_x, off_z, off_keys, off_keys_tmp, off_perm, off_perm_tmp,
       off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
-      off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2];
+      off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2],
+      off_rs[2], off_rl[2], off_hq, off_lperm;
   uint64_t total;
 };
 
@@ -121,6 +122,12 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   // live classes have >= 2 members: at most n / 2 of them, three words each
   L.off_lcls[0] = take(12ull * (n / 2 + 1));
   L.off_lcls[1] = take(12ull * (n / 2 + 1));
+  L.off_rs[0] = take(8 * n);
+  L.off_rs[1] = take(8 * n);
+  L.off_rl[0] = take(4 * n);
+  L.off_rl[1] = take(4 * n);
+  L.off_hq = take(4ull * L.max_heavy);
+  L.off_lperm = take(4 * n);
   L.total = o;
   return L;
 }
@@ -228,10 +235,11 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   // Live-class state.  The incremental rounds do not use the full relabel's
   // grouping (perm, cstart), its flags, x, or keys_tmp/tiny_list outside the
   // sort, so those regions are shared:
-  //   lperm = perm, lperm2 = perm_tmp (the sort's scratch, written after it),
-  //   qcls = cstart, gnz = flags, gl/go = x, gstart/gend = keys_tmp,
-  //   split = tiny_list, shift = keys (written after the last read of keys).
-  c.lperm = c.perm;
+  //   perm = the sort's payload (original positions), lperm2 = perm_tmp
+  //   (the sort's scratch, written after it), qcls = cstart, gnz = flags,
+  //   gl/go = x, gstart/gend = keys_tmp, split = tiny_list, shift = keys
+  //   (written after the last read of keys).
+  c.lperm = (uint32_t*)(ws + L.off_lperm);
   c.lperm2 = c.perm_tmp;
   c.qcls = c.cstart;
   c.qcls2 = (uint32_t*)(ws + L.off_qcls2);
@@ -253,7 +261,12 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.gend = (uint32_t*)c.keys_tmp + L.n;
   c.split = c.tiny_list;
   c.shift = (uint32_t*)c.keys;
-  c.lrows = c.qcls2;  // consumed by the SpMV before k_live_emit writes qcls2
+  c.rs = (uint64_t*)(ws + L.off_rs[0]);
+  c.rs2 = (uint64_t*)(ws + L.off_rs[1]);
+  c.rl = (uint32_t*)(ws + L.off_rl[0]);
+  c.rl2 = (uint32_t*)(ws + L.off_rl[1]);
+  c.midq = c.qcls2;  // consumed by the SpMV before k_live_emit writes qcls2
+  c.hq = (uint32_t*)(ws + L.off_hq);
   c.lsplit = c.c8;    // written after the SpMV has read the compact colours
   c.weighted = g->weight != nullptr;
   {
@@ -444,7 +457,8 @@ struct Session {
   // in every round it can serve (for testing).
   PbLayout P;
   PbCtx pb{};
-  SpmvGrid live_grid{};
+  uint32_t live_heavy = 0, live_mid = 0;  // blocks of k_spmv_mid
+  bool live_mode = false;                  // incremental rounds (run_rsc)
   // The one-colour round by degree histogram (WL_DEGREE_ROUND=0 turns it off,
   // for testing the general path).
   bool deg_mode = true;
@@ -660,8 +674,12 @@ struct Session {
         pb_stop = true;
         return WL_OK;
       }
-      hipLaunchKernelGGL(k_count_active<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
-                         s, ctx);
+      if (live_mode)
+        hipLaunchKernelGGL(k_live_count, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
+                           ctx, 0);
+      else
+        hipLaunchKernelGGL(k_count_active<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock),
+                           0, s, ctx);
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
       if (host.act_entries * 2 < L.nnz) {
@@ -772,7 +790,7 @@ struct Session {
       hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
       return WL_OK;
     }
-    live_gather<RP, W>(h.round, true);
+    live_gather<W>(h.round, true);
     return WL_OK;
   }
 
@@ -782,43 +800,35 @@ struct Session {
   }
 
   // Gathering image of the live rows; every count comes from the device.
-  template <typename RP, bool W>
+  template <bool W>
   void live_gather(uint32_t round, bool always) {
-    hipLaunchKernelGGL(k_lbins_count<RP>, dim3(nscan), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_lbins_scan, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
-    hipLaunchKernelGGL(k_lbins_fill<RP>, dim3(nscan), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
-                       ctx, -1);
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, ctx, -1);
     if (sflags & WL_STATS_WORK)
-      hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
-                         s, ctx, 0);
+      hipLaunchKernelGGL(k_live_count, dim3(gn), dim3(kBlock), 0, s, ctx, 1);
     timed_spmv(round, always, false, [&] {
-      hipLaunchKernelGGL((k_spmv_live<RP, W>), dim3(live_grid.b0), dim3(kBlock), 0, s, ctx,
-                         live_grid);
+      hipLaunchKernelGGL(k_spmv_q<W>, dim3(grid_for(L.n, kBlock, 8192)), dim3(kBlock), 0, s,
+                         ctx);
+      hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + live_mid), dim3(kBlock), 0, s, ctx,
+                         live_heavy);
     });
-    if (live_grid.heavy)
+    if (live_heavy)
       hipLaunchKernelGGL(k_live_heavy_fix, dim3(grid_for(host.bin_cnt[3], kBlock, 1024)),
                          dim3(kBlock), 0, s, ctx);
   }
 
   void spmv_live_async(uint32_t round) {
-    if (rp64) {
-      if (weighted) live_gather<uint64_t, true>(round, false);
-      else live_gather<uint64_t, false>(round, false);
-    } else {
-      if (weighted) live_gather<uint32_t, true>(round, false);
-      else live_gather<uint32_t, false>(round, false);
-    }
+    if (weighted)
+      live_gather<true>(round, false);
+    else
+      live_gather<false>(round, false);
   }
 
-  // Fixed grid of the live SpMV: the static heavy chunks, then groups for
-  // bins 2, 1, 0 that stride over the per-round counts.
+  // Blocks of k_spmv_mid: the static heavy chunks, then waves for the rows
+  // queued per round.
   void plan_live_grid() {
-    const uint64_t n = L.n;
-    live_grid.heavy = host.n_chunks ? grid_for(host.n_chunks, kBlock / kWave) : 0;
-    live_grid.b2 = live_grid.heavy + grid_for(n, kBlock / 64, 512);
-    live_grid.b1 = live_grid.b2 + grid_for(n, kBlock / 16, 1024);
-    live_grid.b0 = live_grid.b1 + grid_for(n, kBlock / 4, 2048);
+    live_heavy = host.n_chunks ? grid_for(host.n_chunks, kBlock / kWave) : 0;
+    live_mid = grid_for(L.n, kBlock / kWave, 2048);
   }
 
   // Relabel by (c, z) for the current grouping; count_round = 0 for the
@@ -1069,6 +1079,7 @@ struct Session {
     if (int r = build_schedule()) return r;
     if (int r = build_live()) return r;
     ctx.keys_mat = 1;
+    live_mode = true;
     plan_live_grid();
     // The first rounds are driven from the host (each reads its counts
     // back); after that, rounds go to the device in groups of 'ahead' with

@@ -14,11 +14,16 @@
 // State kept between rounds (device):
 //   L      live classes in colour order: old colour lcold[j], members at
 //          lperm[loff[j] .. loff[j] + llen[j]); qcls[q] = class of position q.
-//   act    1 for a node of a live class whose row is non-empty (the SpMV
-//          computes z only there; every other member of a live class has
-//          key 0).
+//          The sort permutes keys with the original positions (perm), so
+//          after it position q holds the key of member lperm[perm[q]].
+//   rs, rl first entry and length of the row of every position's node (an
+//          empty row has key 0; the image is computed only for the others).
+//   act    rows longer than kHeavyChunk use the static heavy chunks, which
+//          check act: it is 1 exactly for the nodes of live classes with a
+//          non-empty row (kept up to date for heavy rows only after the
+//          first live round).
 // One round after the image:
-//   load      keys[q] = z of lperm[q] (0 for act = 0)
+//   load      keys[q] = z of lperm[q] (0 for an empty row)
 //   sort      segmented sort of the keys inside every live class (the MSD
 //             radix / LDS / wave sorts of wl_relabel.h, keys materialised)
 //   scan      flags at sub-class starts (class start, or key change); their
@@ -157,15 +162,19 @@ __global__ void __launch_bounds__(kBlock) k_live_class_vals(Ctx ctx) {
 // current by k_live_commit), act for every node.
 template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_live_build(Ctx ctx) {
+  const RP* rp = rowptr<RP>(ctx);
   for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n; p += gridDim.x * kBlock) {
     const uint32_t b = ctx.ids[p], v = ctx.perm[p];
     const bool live = class_live(ctx, b);
-    ctx.act[v] = live && row_nonempty<RP>(ctx, v) ? 1 : 0;
+    const uint64_t r0 = rp[v], r1 = rp[v + 1];
+    ctx.act[v] = live && r1 > r0 ? 1 : 0;
     if (!live) continue;
     const uint32_t s = ctx.cstart[b];
     const uint32_t j = ctx.gl[b], q = ctx.go[b] + (p - s);
     ctx.lperm2[q] = v;
     ctx.qcls2[q] = j;
+    ctx.rs2[q] = r0;
+    ctx.rl2[q] = (uint32_t)(r1 - r0);
     if (p == s) {
       ctx.lcold2[j] = b;
       ctx.loff2[j] = ctx.go[b];
@@ -183,8 +192,8 @@ __global__ void __launch_bounds__(kBlock) k_live_load(Ctx ctx) {
   if (st->done) return;
   const uint32_t nl = st->nl;
   for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
-    const uint32_t v = ctx.lperm[q];
-    ctx.keys[q] = ctx.act[v] ? ctx.z[v] : 0ull;
+    ctx.keys[q] = ctx.rl[q] ? ctx.z[ctx.lperm[q]] : 0ull;
+    ctx.perm[q] = q;  // sort payload: original position
   }
 }
 
@@ -287,14 +296,14 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
   }
 }
 
-// Sub-classes with key 0 hold a non-empty row if one of their members is
-// active (a non-empty row whose image happens to be 0).
+// Sub-classes with key 0 hold a non-empty row if one of their members has
+// one (whose image happens to be 0).
 __global__ void __launch_bounds__(kBlock) k_live_nz0(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
   const uint32_t nl = st->nl;
   for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock)
-    if (ctx.keys[q] == 0 && ctx.act[ctx.lperm[q]]) ctx.gnz[ctx.ids[q]] = 1;
+    if (ctx.keys[q] == 0 && ctx.rl[ctx.perm[q]]) ctx.gnz[ctx.ids[q]] = 1;
 }
 
 __device__ __forceinline__ bool sub_live(const Ctx& ctx, uint32_t g) {
@@ -479,14 +488,16 @@ __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
   }
 }
 
-// Exact new colours of the members of live classes, act of those whose
-// sub-class is no longer live, and the next live classes ('2' buffers).
+// Exact new colours of the members of live classes, act of the heavy rows
+// whose sub-class is no longer live, and the next live classes ('2'
+// buffers).
 __global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
   const uint32_t nl = st->nl;
   for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
-    const uint32_t v = ctx.lperm[q];
+    const uint32_t o = ctx.perm[q];  // original position of the key now at q
+    const uint32_t v = ctx.lperm[o];
     const uint32_t j = ctx.qcls[q];
     const uint32_t g = ctx.ids[q];
     const uint32_t id = ctx.lcold[j] + g - j;
@@ -497,12 +508,15 @@ __global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
     const bool split = ctx.lsplit[j] != 0;
     if (split) ctx.c[v] = id;
     if (split && !(len >= 2 && ctx.gnz[g])) {
-      if (ctx.act[v]) ctx.act[v] = 0;
+      if (ctx.rl[o] > kHeavyChunk) ctx.act[v] = 0;
       continue;
     }
     const uint32_t jn = ctx.gl[g], off = ctx.go[g];
-    ctx.lperm2[off + (q - gs)] = v;
-    ctx.qcls2[off + (q - gs)] = jn;
+    const uint32_t q2 = off + (q - gs);
+    ctx.lperm2[q2] = v;
+    ctx.qcls2[q2] = jn;
+    ctx.rs2[q2] = ctx.rs[o];
+    ctx.rl2[q2] = ctx.rl[o];
     if (q == gs) {
       ctx.lcold2[jn] = id;
       ctx.loff2[jn] = off;
@@ -521,6 +535,8 @@ __global__ void __launch_bounds__(kBlock) k_live_commit(Ctx ctx) {
   for (uint32_t q = tid; q < nl; q += stride) {
     ctx.lperm[q] = ctx.lperm2[q];
     ctx.qcls[q] = ctx.qcls2[q];
+    ctx.rs[q] = ctx.rs2[q];
+    ctx.rl[q] = ctx.rl2[q];
   }
   for (uint32_t j = tid; j < nlive; j += stride) {
     ctx.lcold[j] = ctx.lcold2[j];

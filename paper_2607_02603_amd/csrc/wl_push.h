@@ -84,7 +84,7 @@ __device__ __forceinline__ uint64_t bin_start(const Ctx& c, uint64_t b, uint32_t
   return rp_at<RP>(c, r < c.n ? r : c.n);
 }
 
-// Exclusive scan over a block of kPbThreads (or kPbAccThreads) threads.
+// Exclusive scan over a block of kPbThreads threads.
 template <int T>
 __device__ __forceinline__ uint32_t pb_block_scan(uint32_t v, uint32_t* sh, uint32_t* total) {
   const int lane = lane_id();
@@ -181,43 +181,98 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_lists(Ctx ctx, PbCtx pb) {
 }
 
 // ---------------------------------------------------------------------------
+// Passes 1 and 2 share the staging scheme: every record of a tile gets its
+// rank inside its bin from an LDS atomic, the bins' run offsets come from a
+// block scan and one cursor reservation per bin and tile, the records are
+// staged in bin order in LDS and written out four consecutive slots per
+// thread (staged slot s of bin b goes to dd[b] + s).
+// ---------------------------------------------------------------------------
+
+constexpr long long kPbSkip = -(1ll << 62);  // dd of a run that is not written
+
+template <typename BT>
+__device__ __forceinline__ void pb_write_out(const uint32_t* buf, const BT* sbin,
+                                             const long long* dd, uint32_t cnt,
+                                             uint32_t* out) {
+  for (uint32_t s = 4 * threadIdx.x; s < cnt; s += 4 * kPbThreads) {
+    const uint4 v = *(const uint4*)&buf[s];
+    const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
+    BT b[4];
+    if (sizeof(BT) == 1) {
+      const uint32_t w = *(const uint32_t*)&sbin[s];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) b[u] = (BT)((w >> (8 * u)) & 0xFF);
+    } else {
+      const uint2 w = *(const uint2*)&sbin[s];
+      b[0] = (BT)(w.x & 0xFFFF);
+      b[1] = (BT)(w.x >> 16);
+      b[2] = (BT)(w.y & 0xFFFF);
+      b[3] = (BT)(w.y >> 16);
+    }
+    BT last = b[0];
+    long long o = dd[last];
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u)
+      if (s + u < cnt) {
+        if (b[u] != last) {
+          last = b[u];
+          o = dd[last];
+        }
+        if (o != kPbSkip) out[o + s + u] = vv[u];
+      }
+  }
+}
+
+// Run offsets of a tile: hist[b] (records of bin b in the tile) becomes its
+// exclusive prefix; one cursor reservation per non-empty bin; dd[b] = output
+// index of staged slot 0 of bin b, or kPbSkip when the run would pass the
+// bin's end (A is not symmetric: error bit, run dropped).  Bins
+// [0, nbins) over the block's threads.  Contains __syncthreads().
+__device__ __forceinline__ void pb_reserve(const Ctx& ctx, uint32_t* hist, long long* dd,
+                                           uint32_t* sh, uint32_t nbins,
+                                           unsigned long long* cur, const uint64_t* bstart) {
+  uint32_t carry = 0;
+  for (uint32_t b0 = 0; b0 < nbins; b0 += kPbThreads) {
+    const uint32_t b = b0 + threadIdx.x;
+    const uint32_t h = b < nbins ? hist[b] : 0u;
+    uint32_t tot;
+    const uint32_t ex = carry + pb_block_scan<kPbThreads>(h, sh, &tot);
+    if (h) {
+      const unsigned long long d = atomicAdd(&cur[b], (unsigned long long)h);
+      if (d + h > bstart[b + 1]) {
+        atomicOr(&ctx.st->err, kErrNotSymmetric);
+        dd[b] = kPbSkip;
+      } else {
+        dd[b] = (long long)d - (long long)ex;
+      }
+    }
+    if (b < nbins) hist[b] = ex;
+    carry += tot;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Pass 1: CSR entries -> records in pass-1 bins
 // ---------------------------------------------------------------------------
 
-// Exclusive "last non-zero" scan across the lanes of a wave: for each lane,
-// the last non-zero value held by a lower lane (0 if none).
-__device__ __forceinline__ uint32_t wave_last_nonzero_excl(uint32_t v, uint32_t* incl) {
-  const int lane = lane_id();
-  uint32_t x = v;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t o = __shfl_up(x, off, kWave);
-    if (lane >= off && x == 0) x = o;
-  }
-  *incl = x;
-  const uint32_t ex = __shfl_up(x, 1, kWave);
-  return lane == 0 ? 0u : ex;
-}
-
 // Each tile of kPbTile entries: the colour of every entry's row (row starts
-// marked in LDS, then each thread fills forward over 32 consecutive entries
-// with a carry from the threads before it), records binned in LDS, one run
-// per bin reserved with an atomic on the bin's cursor and written out.  A
-// bin whose runs would pass its end proves A is not symmetric: the run is
-// not written and an error bit is set (every later pass then stops).
+// marked in LDS; a block-wide "last mark at or before" scan in entry order,
+// one ballot and one lane permute per 4 x 64 entries), then the records are
+// staged by bin and written out (pb_reserve, pb_write_out).
 template <typename RP>
 __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
   if (ctx.st->done) return;
-  __shared__ __align__(16) uint32_t buf[kPbTile];  // row marks, colours, records
-  __shared__ uint8_t sbin[kPbTile];                // bin of each staged record
-  __shared__ uint32_t hist[kPbMaxBins];
-  __shared__ uint32_t base[kPbMaxBins];
-  __shared__ long long dd[kPbMaxBins];  // output index of staged slot q: dd[bin] + q
-  __shared__ uint32_t wlast[kPbThreads / kWave];
-  __shared__ uint32_t sh[kPbThreads / kWave];
-  constexpr long long kSkip = -(1ll << 62);
   constexpr uint32_t kRun = kPbTile / kPbThreads;  // entries per thread
-  const int wid = threadIdx.x / kWave;
+  constexpr uint32_t kGroups = kRun / 4;           // loads of 4 entries per thread
+  constexpr int kWaves = kPbThreads / kWave;
+  __shared__ __align__(16) uint32_t buf[kPbTile];  // row marks, then staged records
+  __shared__ __align__(16) uint8_t sbin[kPbTile];  // bin of each staged record
+  __shared__ uint32_t hist[kPbMaxBins];
+  __shared__ long long dd[kPbMaxBins];
+  __shared__ uint32_t wtot[kGroups][kWaves];
+  __shared__ uint32_t sh[kWaves];
+  const int lane = lane_id(), wid = threadIdx.x / kWave;
+  const unsigned long long lt_mask = (1ull << lane) - 1;
   const uint32_t mask1 = (1u << pb.shift1) - 1;
   const bool two = pb.levels == 2;
   uint32_t* out = two ? pb.rec1 : pb.rec2;
@@ -229,12 +284,11 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
     const uint32_t cnt = (uint32_t)(e1 - e0);
     const uint32_t j0 = pb.tile_row[t];
     const uint32_t jend = t + 1 < pb.ntiles1 ? pb.tile_row[t + 1] : ctx.n - 1;
-    // column indices, 4 consecutive entries per load: slot (k, u) holds
-    // entry 4 * (k * kPbThreads + threadIdx.x) + u
+    // column indices: slot (k, u) holds entry 4 * (k * kPbThreads + threadIdx.x) + u
     uint32_t cix[kRun];
     if (cnt == kPbTile) {
 #pragma unroll
-      for (uint32_t k = 0; k < kRun / 4; ++k) {
+      for (uint32_t k = 0; k < kGroups; ++k) {
         const uint4 v = col4[(e0 >> 2) + k * kPbThreads + threadIdx.x];
         cix[4 * k] = v.x;
         cix[4 * k + 1] = v.y;
@@ -243,7 +297,7 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
       }
     } else {
 #pragma unroll
-      for (uint32_t k = 0; k < kRun / 4; ++k)
+      for (uint32_t k = 0; k < kGroups; ++k)
 #pragma unroll
         for (uint32_t u = 0; u < 4; ++u) {
           const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
@@ -253,8 +307,8 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
     const uint32_t c_first = ctx.c[j0];
     const uint4 z4 = make_uint4(0, 0, 0, 0);
 #pragma unroll
-    for (uint32_t k = 0; k < kRun / 4; ++k) ((uint4*)buf)[k * kPbThreads + threadIdx.x] = z4;
-    if (threadIdx.x < kPbMaxBins) hist[threadIdx.x] = 0;
+    for (uint32_t k = 0; k < kGroups; ++k) ((uint4*)buf)[k * kPbThreads + threadIdx.x] = z4;
+    for (uint32_t b = threadIdx.x; b < kPbMaxBins; b += kPbThreads) hist[b] = 0;
     __syncthreads();
     // colour + 1 at the first entry of every non-empty row starting in the tile
     for (uint32_t r = j0 + 1 + threadIdx.x; r <= jend; r += kPbThreads) {
@@ -262,95 +316,79 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
       if (b < e1 && rp_at<RP>(ctx, r + 1) > b) buf[b - e0] = ctx.c[r] + 1;
     }
     __syncthreads();
-    // fill forward: thread i owns entries [kRun * i, kRun * (i + 1))
-    {
-      uint4 v[kRun / 4];
-      uint32_t last = 0;
+    // entry order is (k, thread, u): per k, the last mark of every group of
+    // 4, the last mark of the lower lanes (ballot + permute), the waves'
+    // totals through LDS
+    uint4 mk[kGroups];
+    uint32_t ex[kGroups];
 #pragma unroll
-      for (uint32_t k = 0; k < kRun / 4; ++k) {
-        v[k] = ((const uint4*)buf)[threadIdx.x * (kRun / 4) + k];
-        if (v[k].x) last = v[k].x;
-        if (v[k].y) last = v[k].y;
-        if (v[k].z) last = v[k].z;
-        if (v[k].w) last = v[k].w;
-      }
-      uint32_t incl;
-      uint32_t carry = wave_last_nonzero_excl(last, &incl);
-      if (lane_id() == kWave - 1) wlast[wid] = incl;
-      __syncthreads();
-      if (!carry) {
-        carry = c_first + 1;
-        for (int w = 0; w < wid; ++w)
-          if (wlast[w]) carry = wlast[w];
-      }
-#pragma unroll
-      for (uint32_t k = 0; k < kRun / 4; ++k) {
-        if (v[k].x) carry = v[k].x;
-        v[k].x = carry - 1;
-        if (v[k].y) carry = v[k].y;
-        v[k].y = carry - 1;
-        if (v[k].z) carry = v[k].z;
-        v[k].z = carry - 1;
-        if (v[k].w) carry = v[k].w;
-        v[k].w = carry - 1;
-        ((uint4*)buf)[threadIdx.x * (kRun / 4) + k] = v[k];
+    for (uint32_t k = 0; k < kGroups; ++k) {
+      mk[k] = ((const uint4*)buf)[k * kPbThreads + threadIdx.x];
+      const uint32_t g = mk[k].w ? mk[k].w : (mk[k].z ? mk[k].z : (mk[k].y ? mk[k].y : mk[k].x));
+      const unsigned long long m = __ballot(g != 0);
+      const unsigned long long below = m & lt_mask;
+      const uint32_t v = __shfl(g, below ? 63 - __builtin_clzll(below) : lane, kWave);
+      ex[k] = below ? v : 0u;
+      if (m) {
+        const uint32_t tot = __shfl(g, 63 - __builtin_clzll(m), kWave);
+        if (lane == 0) wtot[k][wid] = tot;
+      } else if (lane == 0) {
+        wtot[k][wid] = 0;
       }
     }
     __syncthreads();
-    // records and their bins, counted per bin
-    uint32_t bin[kRun];
+    uint32_t running = c_first + 1;  // last mark of every group before (k, wave)
 #pragma unroll
-    for (uint32_t k = 0; k < kRun / 4; ++k) {
-      const uint4 cv = ((const uint4*)buf)[k * kPbThreads + threadIdx.x];
-      const uint32_t colour[4] = {cv.x, cv.y, cv.z, cv.w};
+    for (uint32_t k = 0; k < kGroups; ++k) {
+      uint32_t before = running;
+      for (int w = 0; w < kWaves; ++w) {
+        const uint32_t x = wtot[k][w];
+        if (x) {
+          if (w < wid) before = x;
+          running = x;
+        }
+      }
+      uint32_t c = ex[k] ? ex[k] : before;
+      uint32_t mv[4] = {mk[k].x, mk[k].y, mk[k].z, mk[k].w};
+#pragma unroll
+      for (uint32_t u = 0; u < 4; ++u) {
+        if (mv[u]) c = mv[u];
+        const uint32_t i = cix[4 * k + u];
+        cix[4 * k + u] = ((i & mask1) << pb.cbits) | (c - 1);  // the record
+        mv[u] = i >> pb.shift1;                                  // its bin
+      }
+      mk[k] = make_uint4(mv[0], mv[1], mv[2], mv[3]);
+    }
+    // ranks inside the bins: packed (bin << 16 | rank), or ~0 for no record
+    uint32_t pk[kRun];
+#pragma unroll
+    for (uint32_t k = 0; k < kGroups; ++k) {
+      const uint32_t bv[4] = {mk[k].x, mk[k].y, mk[k].z, mk[k].w};
 #pragma unroll
       for (uint32_t u = 0; u < 4; ++u) {
         const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
-        const uint32_t x = 4 * k + u;
-        bin[x] = 0xFFFFFFFFu;
-        const uint32_t i = cix[x];
-        if (q < cnt && i >= ctx.n) atomicOr(&ctx.st->err, kErrNotSymmetric);  // invalid column
-        if (q < cnt && i < ctx.n) {
-          bin[x] = i >> pb.shift1;
-          cix[x] = ((i & mask1) << pb.cbits) | colour[u];  // the record
-          atomicAdd(&hist[bin[x]], 1u);
+        pk[4 * k + u] = 0xFFFFFFFFu;
+        if (q < cnt) {
+          if (bv[u] < pb.nb1)
+            pk[4 * k + u] = (bv[u] << 16) | atomicAdd(&hist[bv[u]], 1u);
+          else  // a column >= n
+            atomicOr(&ctx.st->err, kErrNotSymmetric);
         }
       }
     }
     __syncthreads();
-    // run offsets inside the tile; one cursor reservation per bin (its
-    // result is first needed after the staging below)
-    const uint32_t b = threadIdx.x;
-    const uint32_t h = b < pb.nb1 ? hist[b] : 0u;
-    uint32_t tot;
-    const uint32_t ex = pb_block_scan<kPbThreads>(h, sh, &tot);
-    unsigned long long d = 0;
-    if (h) d = atomicAdd(&cur[b], (unsigned long long)h);
-    if (b < pb.nb1) {
-      base[b] = ex;
-      hist[b] = 0;
-    }
+    pb_reserve(ctx, hist, dd, sh, pb.nb1, cur, bstart);
     __syncthreads();
 #pragma unroll
     for (uint32_t x = 0; x < kRun; ++x)
-      if (bin[x] != 0xFFFFFFFFu) {
-        const uint32_t slot = base[bin[x]] + atomicAdd(&hist[bin[x]], 1u);
+      if (pk[x] != 0xFFFFFFFFu) {
+        const uint32_t b = pk[x] >> 16;
+        const uint32_t slot = hist[b] + (pk[x] & 0xFFFF);
         buf[slot] = cix[x];
-        sbin[slot] = (uint8_t)bin[x];
+        sbin[slot] = (uint8_t)b;
       }
-    if (h) {
-      if (d + h > bstart[b + 1]) {
-        atomicOr(&ctx.st->err, kErrNotSymmetric);
-        dd[b] = kSkip;
-      } else {
-        dd[b] = (long long)d - (long long)ex;
-      }
-    }
     __syncthreads();
-    for (uint32_t q = threadIdx.x; q < cnt; q += kPbThreads) {
-      const long long o = dd[sbin[q]];
-      if (o != kSkip) out[o + q] = buf[q];
-    }
+    pb_write_out<uint8_t>(buf, sbin, dd, cnt, out);
     __syncthreads();
   }
 }
@@ -359,7 +397,6 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
 // Pass 2: coarse bins -> fine bins
 // ---------------------------------------------------------------------------
 
-// Write cursors of both passes: the first entry of every bin.
 __global__ void __launch_bounds__(kBlock) k_pb_cursors(Ctx ctx, PbCtx pb) {
   if (ctx.st->done) return;
   for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < pb.nfine; f += gridDim.x * kBlock) {
@@ -370,79 +407,80 @@ __global__ void __launch_bounds__(kBlock) k_pb_cursors(Ctx ctx, PbCtx pb) {
 
 __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
   if (ctx.st->done || (ctx.st->err & kErrNotSymmetric)) return;
-  __shared__ uint32_t buf[kPbTile2];
-  __shared__ uint16_t sbin[kPbTile2];
+  __shared__ __align__(16) uint32_t buf[kPbTile2];
+  __shared__ __align__(16) uint16_t sbin[kPbTile2];
   __shared__ uint32_t hist[kPbMaxFine];
-  __shared__ uint32_t base[kPbMaxFine];
-  __shared__ unsigned long long dst[kPbMaxFine];
+  __shared__ long long dd[kPbMaxFine];
   __shared__ uint32_t sh[kPbThreads / kWave];
   const uint32_t nf = 1u << pb.fbits;
   const uint32_t cmask = (1u << pb.cbits) - 1;
   const uint32_t ntiles = pb.cnt->ntiles2;
   constexpr uint32_t kPer = kPbTile2 / kPbThreads;
-  for (uint32_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    uint32_t lo = 0, hi = pb.nb1 - 1;  // coarse bin: last b with tile2_off[b] <= t
+  // tile t: coarse bin, first record, record count
+  auto tile_of = [&](uint32_t t, uint32_t* cbo, uint64_t* ao, uint32_t* cnto) {
+    uint32_t lo = 0, hi = pb.nb1 - 1;  // last b with tile2_off[b] <= t
     while (lo < hi) {
       const uint32_t mid = (lo + hi + 1) >> 1;
       if (pb.tile2_off[mid] <= t) lo = mid; else hi = mid - 1;
     }
-    const uint32_t cb = lo;
-    const uint64_t rend = pb.bstart1[cb + 1];
-    const uint64_t a = pb.bstart1[cb] + (uint64_t)(t - pb.tile2_off[cb]) * kPbTile2;
-    const uint32_t cnt = (uint32_t)(min(rend, a + kPbTile2) - a);
-    uint32_t rec[kPer];
+    *cbo = lo;
+    *ao = pb.bstart1[lo] + (uint64_t)(t - pb.tile2_off[lo]) * kPbTile2;
+    *cnto = (uint32_t)(min(pb.bstart1[lo + 1], *ao + kPbTile2) - *ao);
+  };
+  // records of the next tile are loaded while the current one is processed
+  uint32_t nxt[kPer];
+  uint32_t ncb = 0, ncnt = 0;
+  uint64_t na = 0;
+  if (blockIdx.x < ntiles) {
+    tile_of(blockIdx.x, &ncb, &na, &ncnt);
 #pragma unroll
     for (uint32_t k = 0; k < kPer; ++k) {
       const uint32_t q = k * kPbThreads + threadIdx.x;
-      rec[k] = q < cnt ? pb.rec1[a + q] : 0u;
+      nxt[k] = q < ncnt ? pb.rec1[na + q] : 0u;
     }
+  }
+  for (uint32_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const uint32_t cb = ncb, cnt = ncnt;
+    uint32_t rec[kPer];
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k) rec[k] = nxt[k];
+    if (t + gridDim.x < ntiles) {
+      tile_of(t + gridDim.x, &ncb, &na, &ncnt);
+#pragma unroll
+      for (uint32_t k = 0; k < kPer; ++k) {
+        const uint32_t q = k * kPbThreads + threadIdx.x;
+        nxt[k] = q < ncnt ? pb.rec1[na + q] : 0u;
+      }
+    }
+    const uint32_t nfb = min(nf, pb.nfine - (cb << pb.fbits));  // fine bins of this coarse bin
     for (uint32_t b = threadIdx.x; b < nf; b += kPbThreads) hist[b] = 0;
     __syncthreads();
-    // the fine bin is (local >> kPbFineShift) of the coarse record
+    // fine bin = (local >> kPbFineShift) of the coarse record; packed rank
+    uint32_t pk[kPer];
 #pragma unroll
-    for (uint32_t k = 0; k < kPer; ++k)
-      if (k * kPbThreads + threadIdx.x < cnt)
-        atomicAdd(&hist[(rec[k] >> pb.cbits) >> kPbFineShift], 1u);
-    __syncthreads();
-    uint32_t carry = 0;
-    for (uint32_t b0 = 0; b0 < nf; b0 += kPbThreads) {
-      const uint32_t b = b0 + threadIdx.x;
-      const uint32_t h = b < nf ? hist[b] : 0u;
-      uint32_t tot;
-      const uint32_t ex = pb_block_scan<kPbThreads>(h, sh, &tot);
-      if (b < nf) {
-        base[b] = carry + ex;
-        unsigned long long d = 0;
-        if (h) {
-          // a fine bin receives exactly the entry count of its rows when A
-          // is symmetric; more proves it is not, and nothing is written
-          const uint64_t fb = ((uint64_t)cb << pb.fbits) + b;
-          d = atomicAdd(&pb.cur2[fb], (unsigned long long)h);
-          if (d + h > pb.bstartf[fb + 1]) {
-            atomicOr(&ctx.st->err, kErrNotSymmetric);
-            d = ~0ull;
-          }
-        }
-        dst[b] = d;
-        hist[b] = 0;
-      }
-      carry += tot;
-    }
-    __syncthreads();
-#pragma unroll
-    for (uint32_t k = 0; k < kPer; ++k)
+    for (uint32_t k = 0; k < kPer; ++k) {
+      pk[k] = 0xFFFFFFFFu;
       if (k * kPbThreads + threadIdx.x < cnt) {
         const uint32_t local = rec[k] >> pb.cbits;
-        const uint32_t b = local >> kPbFineShift;
-        const uint32_t slot = base[b] + atomicAdd(&hist[b], 1u);
-        buf[slot] = ((local & (kPbFineRows - 1)) << pb.cbits) | (rec[k] & cmask);
+        const uint32_t b = min(local >> kPbFineShift, nfb - 1);
+        pk[k] = (b << 16) | atomicAdd(&hist[b], 1u);
+        rec[k] = ((local & (kPbFineRows - 1)) << pb.cbits) | (rec[k] & cmask);
+      }
+    }
+    __syncthreads();
+    pb_reserve(ctx, hist, dd, sh, nfb, pb.cur2 + ((uint64_t)cb << pb.fbits),
+               pb.bstartf + ((uint64_t)cb << pb.fbits));
+    __syncthreads();
+#pragma unroll
+    for (uint32_t k = 0; k < kPer; ++k)
+      if (pk[k] != 0xFFFFFFFFu) {
+        const uint32_t b = pk[k] >> 16;
+        const uint32_t slot = hist[b] + (pk[k] & 0xFFFF);
+        buf[slot] = rec[k];
         sbin[slot] = (uint16_t)b;
       }
     __syncthreads();
-    for (uint32_t q = threadIdx.x; q < cnt; q += kPbThreads) {
-      const uint32_t b = sbin[q];
-      if (dst[b] != ~0ull) pb.rec2[dst[b] + (q - base[b])] = buf[q];
-    }
+    pb_write_out<uint16_t>(buf, sbin, dd, cnt, pb.rec2);
     __syncthreads();
   }
 }
@@ -451,23 +489,29 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
 // Pass 3: records of a fine bin -> z
 // ---------------------------------------------------------------------------
 
-// value = lo + hi * 2^32 (mod p), lo, hi < 2^64
-__device__ __forceinline__ uint64_t pb_reduce(uint64_t lo, uint64_t hi) {
-  const uint64_t h = fold61(hi);
-  // h * 2^32 = (h mod 2^29) * 2^32 + (h >> 29) * 2^61, and 2^61 = 1 (mod p)
-  const uint64_t t2 = ((h & 0x1FFFFFFFull) << 32) + (h >> 29);
-  return addp(fold61(t2), fold61(lo));
+// value = acc + carries * 2^64 (mod p); 2^64 = 8 (mod p)
+__device__ __forceinline__ uint64_t pb_reduce(uint64_t acc, uint32_t carries) {
+  return addp(fold61(acc), fold61((uint64_t)carries << 3));
 }
 
 // TBL: the k colour values sit in LDS (k <= kPbTableMax), else each record's
 // value is computed from its colour.
 constexpr uint32_t kPbTableMax = 4096;
 
+// Per row an exact sum: a 64-bit accumulator (one atomic per record, whose
+// returned old value shows a wrap past 2^64) and a count of such wraps.
+__device__ __forceinline__ void pb_acc_add(unsigned long long* acc, uint32_t* wraps,
+                                           uint32_t r, uint64_t v, uint32_t extra) {
+  const unsigned long long old = atomicAdd(&acc[r], (unsigned long long)v);
+  const uint32_t w = extra + (old + v < old ? 1u : 0u);
+  if (w) atomicAdd(&wraps[r], w);
+}
+
 template <typename RP, bool TBL>
 __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
   if (ctx.st->done || (ctx.st->err & kErrNotSymmetric)) return;
-  __shared__ unsigned long long acc_lo[kPbFineRows];
-  __shared__ unsigned long long acc_hi[kPbFineRows];
+  __shared__ unsigned long long acc[kPbFineRows];
+  __shared__ uint32_t wraps[kPbFineRows];
   __shared__ uint64_t wtab[TBL ? kPbTableMax : 1];
   constexpr uint32_t kU = 16;  // records per thread per step, loaded together
   const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
@@ -490,16 +534,28 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
     const uint64_t a = pb.bstartf[f] + (uint64_t)q * kPbSlice;
     const uint64_t e = ns == 1 ? b1 : min(b1, a + kPbSlice);
     for (uint32_t r = threadIdx.x; r < kPbFineRows; r += kPbAccThreads) {
-      acc_lo[r] = 0;
-      acc_hi[r] = 0;
+      acc[r] = 0;
+      wraps[r] = 0;
     }
     __syncthreads();
+    uint32_t nxt[kU];
+#pragma unroll
+    for (uint32_t u = 0; u < kU; ++u) {
+      const uint64_t p = a + u * kPbAccThreads + threadIdx.x;
+      nxt[u] = p < e ? pb.rec2[p] : 0u;
+    }
     for (uint64_t p0 = a; p0 < e; p0 += kU * kPbAccThreads) {
       uint32_t rv[kU];
 #pragma unroll
-      for (uint32_t u = 0; u < kU; ++u) {
-        const uint64_t p = p0 + u * kPbAccThreads + threadIdx.x;
-        rv[u] = p < e ? pb.rec2[p] : 0u;
+      for (uint32_t u = 0; u < kU; ++u) rv[u] = nxt[u];
+      // the next step's records are loaded while these are added
+      const uint64_t p1 = p0 + kU * kPbAccThreads;
+      if (p1 < e) {
+#pragma unroll
+        for (uint32_t u = 0; u < kU; ++u) {
+          const uint64_t p = p1 + u * kPbAccThreads + threadIdx.x;
+          nxt[u] = p < e ? pb.rec2[p] : 0u;
+        }
       }
 #pragma unroll
       for (uint32_t u = 0; u < kU; ++u) {
@@ -507,23 +563,24 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
         const uint32_t local = (rv[u] >> pb.cbits) & (kPbFineRows - 1);
         const uint64_t w =
             ok ? (TBL ? wtab[rv[u] & cmask] : color_weight(key, rv[u] & cmask)) : 0ull;
-        uint64_t wl = w & 0xFFFFFFFFull, wh = w >> 32;
         const uint32_t l0 = __shfl(local, 0, kWave);
         if (__all(!ok || local == l0)) {
-          // the whole wave feeds one row (rows of high degree): add in
-          // registers first
+          // the whole wave feeds one row (rows of high degree): add the 64
+          // values exactly (low and high 32-bit halves) in registers first
+          uint64_t sl = w & 0xFFFFFFFFull, sh2 = w >> 32;
 #pragma unroll
           for (int off = kWave / 2; off > 0; off >>= 1) {
-            wl += __shfl_xor(wl, off, kWave);
-            wh += __shfl_xor(wh, off, kWave);
+            sl += __shfl_xor(sl, off, kWave);
+            sh2 += __shfl_xor(sh2, off, kWave);
           }
-          if (lane_id() == 0 && (wl | wh)) {
-            atomicAdd(&acc_lo[l0], (unsigned long long)wl);
-            atomicAdd(&acc_hi[l0], (unsigned long long)wh);
+          if (lane_id() == 0 && (sl | sh2)) {
+            // sl + sh2 * 2^32 as (64-bit part, multiples of 2^64)
+            const uint64_t v = sl + (sh2 << 32);
+            const uint32_t hi64 = (uint32_t)(sh2 >> 32) + (v < sl ? 1u : 0u);
+            pb_acc_add(acc, wraps, l0, v, hi64);
           }
         } else if (ok) {
-          atomicAdd(&acc_lo[local], (unsigned long long)wl);
-          atomicAdd(&acc_hi[local], (unsigned long long)wh);
+          pb_acc_add(acc, wraps, local, w, 0);
         }
       }
     }
@@ -532,11 +589,11 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
     const uint32_t nrows = (uint32_t)min((uint64_t)kPbFineRows, (uint64_t)ctx.n - row0);
     if (ns == 1) {
       for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
-        if (ctx.act[row0 + r]) ctx.z[row0 + r] = pb_reduce(acc_lo[r], acc_hi[r]);
+        ctx.z[row0 + r] = pb_reduce(acc[r], wraps[r]);
     } else {
       uint64_t* part = pb.part + (uint64_t)(pb.mslice_off[f] + q) * kPbFineRows;
       for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
-        part[r] = pb_reduce(acc_lo[r], acc_hi[r]);
+        part[r] = pb_reduce(acc[r], wraps[r]);
     }
     __syncthreads();
   }
@@ -552,7 +609,7 @@ __global__ void __launch_bounds__(kBlock) k_pb_combine(Ctx ctx, PbCtx pb) {
     const uint32_t f = pb.mlist[x >> kPbFineShift];
     const uint32_t r = (uint32_t)(x & (kPbFineRows - 1));
     const uint64_t row = ((uint64_t)f << kPbFineShift) + r;
-    if (row >= ctx.n || !ctx.act[row]) continue;
+    if (row >= ctx.n) continue;
     const uint32_t s0 = pb.mslice_off[f], s1 = pb.mslice_off[f + 1];
     uint64_t z = 0;
     for (uint32_t s = s0; s < s1; ++s) z = addp(z, pb.part[(uint64_t)s * kPbFineRows + r]);

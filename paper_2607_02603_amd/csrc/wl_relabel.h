@@ -37,6 +37,8 @@ __global__ void k_round_begin(Ctx ctx) {
   st->n_tiles = 0;
   st->act_entries = 0;
   st->n_split = 0;
+  st->n_mid = 0;
+  st->n_hlive = 0;
 }
 
 __global__ void __launch_bounds__(kBlock) k_fill_u8(Ctx ctx, uint8_t* p,
@@ -45,20 +47,6 @@ __global__ void __launch_bounds__(kBlock) k_fill_u8(Ctx ctx, uint8_t* p,
   for (uint64_t i = blockIdx.x * (uint64_t)kBlock + threadIdx.x; i < cnt;
        i += (uint64_t)gridDim.x * kBlock)
     p[i] = v;
-}
-
-// Appends 'want' items to a device list: one atomic per block, slots
-// handed out by a block scan (order inside the list is irrelevant).
-// Contains __syncthreads(); every thread of the block must call it.
-__device__ __forceinline__ uint32_t block_append(bool want, uint32_t* counter,
-                                                 uint32_t* sh, uint32_t* base_sh) {
-  uint32_t tot;
-  const uint32_t ex = block_excl_scan(want ? 1u : 0u, sh, &tot);
-  if (threadIdx.x == 0) *base_sh = tot ? atomicAdd(counter, tot) : 0u;
-  __syncthreads();
-  const uint32_t at = *base_sh + ex;
-  __syncthreads();
-  return at;
 }
 
 // One entry per class: flag its first position, queue it if it has >= 2

@@ -236,34 +236,24 @@ __device__ __forceinline__ void accumulate(const Ctx& ctx, Acc96& a, uint64_t e0
   for (int u = 0; u < U; ++u) acc_add(a, v[u]);
 }
 
-// LIVE: the rows are the members of the live classes, listed by position q
-// of lperm (every one active), and the image goes to keys[q]; otherwise the
-// static bins of all rows, skipping inactive ones, image to z[row].
-template <int G, int U, typename RP, bool W, int M, bool LIVE>
+template <int G, int U, typename RP, bool W, int M>
 __device__ __forceinline__ void spmv_rows(const Ctx& ctx, int bin, uint32_t bid,
                                           uint32_t nblk, uint64_t rkey) {
   const RP* rp = rowptr<RP>(ctx);
-  const uint32_t cnt = LIVE ? ctx.st->lbin_cnt[bin] : ctx.st->bin_cnt[bin];
-  const uint32_t* list =
-      LIVE ? ctx.lrows + ctx.st->lbin_start[bin] : ctx.rows + ctx.st->bin_start[bin];
+  const uint32_t cnt = ctx.st->bin_cnt[bin];
+  const uint32_t* list = ctx.rows + ctx.st->bin_start[bin];
   const uint32_t sub = threadIdx.x % G;
   const uint32_t gpb = kBlock / G;
   const uint32_t ngroups = nblk * gpb;
   for (uint32_t t = bid * gpb + threadIdx.x / G; t < cnt; t += ngroups) {
-    const uint32_t item = list[t];
-    const uint32_t row = LIVE ? ctx.lperm[item] : item;
-    if (!LIVE && !ctx.act[row]) continue;
+    const uint32_t row = list[t];
+    if (!ctx.act[row]) continue;
     const uint64_t beg = rp[row], end = rp[row + 1];
     Acc96 a{0, 0};
     for (uint64_t e0 = beg + sub; e0 < end; e0 += (uint64_t)G * U)
       accumulate<U, W, M>(ctx, a, e0, end, G, rkey);
     const uint64_t r = group_sum_p<G>(acc_reduce(a));
-    if (sub == 0) {
-      if (LIVE)
-        ctx.keys[item] = r;
-      else
-        ctx.z[row] = r;
-    }
+    if (sub == 0) ctx.z[row] = r;
   }
 }
 
@@ -303,140 +293,173 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
   }
 }
 
-template <typename RP, bool W, int M, bool LIVE>
+template <typename RP, bool W, int M>
 __device__ __forceinline__ void spmv_body(const Ctx& ctx, const SpmvGrid& g) {
   const uint64_t rkey = round_key(ctx.st->seed, ctx.st->round);
   const uint32_t b = blockIdx.x;
   if (b < g.heavy)
     spmv_heavy<W, M>(ctx, b, g.heavy, rkey);
   else if (b < g.b2)
-    spmv_rows<64, 4, RP, W, M, LIVE>(ctx, 2, b - g.heavy, g.b2 - g.heavy, rkey);
+    spmv_rows<64, 4, RP, W, M>(ctx, 2, b - g.heavy, g.b2 - g.heavy, rkey);
   else if (b < g.b1)
-    spmv_rows<16, 4, RP, W, M, LIVE>(ctx, 1, b - g.b2, g.b1 - g.b2, rkey);
+    spmv_rows<16, 4, RP, W, M>(ctx, 1, b - g.b2, g.b1 - g.b2, rkey);
   else
-    spmv_rows<4, 2, RP, W, M, LIVE>(ctx, 0, b - g.b1, g.b0 - g.b1, rkey);
+    spmv_rows<4, 2, RP, W, M>(ctx, 0, b - g.b1, g.b0 - g.b1, rkey);
 }
 
 template <typename RP, bool W, int M>
 __global__ void __launch_bounds__(kBlock) k_spmv(Ctx ctx, SpmvGrid g) {
   if (ctx.st->done) return;
-  spmv_body<RP, W, M, false>(ctx, g);
+  spmv_body<RP, W, M>(ctx, g);
 }
 
-// Rows of the live classes (bins built by k_lbins_*), gather mode taken from
-// the colour count on the device, so the launch needs no read-back.  Heavy
-// rows go through the static chunks (which write z; k_live_heavy_fix moves
-// their images to keys).
-template <typename RP, bool W>
-__global__ void __launch_bounds__(kBlock) k_spmv_live(Ctx ctx, SpmvGrid g) {
+// ---------------------------------------------------------------------------
+// Image of the live rows, by position q of lperm: the row of position q
+// starts at rs[q] and has rl[q] entries (kept with the member list, so no
+// per-node lookups).  Rows of at most kShortRow entries take one lane each;
+// longer ones are queued for one wave each (k_spmv_mid), and rows longer
+// than kHeavyChunk go through the static heavy chunks (which write z;
+// k_live_heavy_fix moves those images to the keys).  Empty rows have key 0.
+// ---------------------------------------------------------------------------
+
+constexpr uint32_t kShortRow = 16;
+
+template <bool W, int M>
+__device__ __forceinline__ void spmv_q_body(const Ctx& ctx) {
+  DevState* st = ctx.st;
+  const uint64_t rkey = round_key(st->seed, st->round);
+  const uint32_t nl = st->nl;
+  __shared__ uint32_t sh[kBlock / kWave];
+  __shared__ uint32_t base_sh;
+  for (uint32_t q0 = blockIdx.x * kBlock; q0 < nl; q0 += gridDim.x * kBlock) {
+    const uint32_t q = q0 + threadIdx.x;
+    uint32_t len = 0;
+    uint64_t beg = 0;
+    if (q < nl) {
+      len = ctx.rl[q];
+      beg = ctx.rs[q];
+      ctx.perm[q] = q;  // sort payload: original position
+    }
+    const bool heavy = len > kHeavyChunk;
+    const bool mid = len > kShortRow && !heavy;
+    const uint32_t am = block_append(mid, &st->n_mid, sh, &base_sh);
+    if (mid) ctx.midq[am] = q;
+    const uint32_t ah = block_append(heavy, &st->n_hlive, sh, &base_sh);
+    if (heavy) ctx.hq[ah] = q;
+    if (q < nl && !mid && !heavy) {
+      Acc96 a{0, 0};
+      for (uint32_t t0 = 0; t0 < len; t0 += 4) {
+        uint32_t j[4];
+        bool ok[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          ok[u] = t0 + u < len;
+          j[u] = ok[u] ? ctx.col[beg + t0 + u] : 0u;
+        }
+        uint64_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          v[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
+          if (W && ok[u]) v[u] = mul_small_fold(ctx.wgt[beg + t0 + u], v[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc_add(a, v[u]);
+      }
+      ctx.keys[q] = acc_reduce(a);
+    }
+  }
+}
+
+template <bool W>
+__global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx) {
   if (ctx.st->done) return;
   const int mode = gather_mode(ctx.st->k);
   if (mode == kGather8)
-    spmv_body<RP, W, kGather8, true>(ctx, g);
+    spmv_q_body<W, kGather8>(ctx);
   else if (mode == kGather16)
-    spmv_body<RP, W, kGather16, true>(ctx, g);
+    spmv_q_body<W, kGather16>(ctx);
   else
-    spmv_body<RP, W, kGatherC, true>(ctx, g);
+    spmv_q_body<W, kGatherC>(ctx);
 }
 
-// ---------------------------------------------------------------------------
-// Per-round bins of the live rows: positions q of lperm whose node is active,
-// by row length (bins 0-2 as in the static schedule, bin 3 = heavy rows).
-// Positions of inactive nodes get key 0 here.  Block ranges of count and
-// fill are the same.
-// ---------------------------------------------------------------------------
-
-__device__ __forceinline__ void lbins_range(uint32_t nl, uint32_t* lo, uint32_t* hi) {
-  const uint32_t per = ((nl + gridDim.x - 1) / gridDim.x + kBlock - 1) / kBlock * kBlock;
-  *lo = min(nl, blockIdx.x * per);
-  *hi = min(nl, *lo + per);
-}
-
-template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_lbins_count(Ctx ctx) {
-  const DevState* st = ctx.st;
-  if (st->done) return;
-  const RP* rp = rowptr<RP>(ctx);
-  uint32_t lo, hi;
-  lbins_range(st->nl, &lo, &hi);
-  uint32_t cnt[kNumBins] = {0, 0, 0, 0};
-  for (uint32_t q = lo + threadIdx.x; q < hi; q += kBlock) {
-    const uint32_t v = ctx.lperm[q];
-    if (ctx.act[v])
-      cnt[row_bin((uint64_t)(rp[v + 1] - rp[v]))]++;
-    else
-      ctx.keys[q] = 0;
+// Blocks [0, heavy): the static heavy chunks (rows whose act flag is set);
+// the rest: one wave per queued row.
+template <bool W, int M>
+__device__ __forceinline__ void spmv_mid_body(const Ctx& ctx, uint32_t heavy) {
+  const uint64_t rkey = round_key(ctx.st->seed, ctx.st->round);
+  if (blockIdx.x < heavy) {
+    spmv_heavy<W, M>(ctx, blockIdx.x, heavy, rkey);
+    return;
   }
-  __shared__ uint32_t sh[kNumBins];
-  if (threadIdx.x < kNumBins) sh[threadIdx.x] = 0;
-  __syncthreads();
-  for (int b = 0; b < kNumBins; ++b)
-    if (cnt[b]) atomicAdd(&sh[b], cnt[b]);
-  __syncthreads();
-  if (threadIdx.x < kNumBins)
-    ctx.bin_part[threadIdx.x * gridDim.x + blockIdx.x] = sh[threadIdx.x];
-}
-
-__global__ void __launch_bounds__(kBlock) k_lbins_scan(Ctx ctx, uint32_t nblk) {
-  DevState* st = ctx.st;
-  if (st->done) return;
-  __shared__ uint32_t sh[kBlock / kWave];
-  uint32_t start = 0;
-  for (int b = 0; b < kNumBins; ++b) {
-    uint32_t carry = 0;
-    uint32_t* part = ctx.bin_part + b * nblk;
-    for (uint32_t base = 0; base < nblk; base += kBlock) {
-      const uint32_t i = base + threadIdx.x;
-      const uint32_t v = i < nblk ? part[i] : 0;
-      uint32_t tot;
-      const uint32_t ex = block_excl_scan(v, sh, &tot);
-      if (i < nblk) part[i] = carry + ex;
-      carry += tot;
-    }
-    if (threadIdx.x == 0) {
-      st->lbin_cnt[b] = carry;
-      st->lbin_start[b] = start;
-    }
-    start += carry;
+  const uint32_t cnt = ctx.st->n_mid;
+  const uint32_t lane = lane_id();
+  const uint32_t nwaves = (gridDim.x - heavy) * (kBlock / kWave);
+  for (uint32_t t = (blockIdx.x - heavy) * (kBlock / kWave) + threadIdx.x / kWave; t < cnt;
+       t += nwaves) {
+    const uint32_t q = ctx.midq[t];
+    const uint64_t beg = ctx.rs[q], end = beg + ctx.rl[q];
+    Acc96 a{0, 0};
+    for (uint64_t e0 = beg + lane; e0 < end; e0 += (uint64_t)kWave * 4)
+      accumulate<4, W, M>(ctx, a, e0, end, kWave, rkey);
+    const uint64_t r = group_sum_p<kWave>(acc_reduce(a));
+    if (lane == 0) ctx.keys[q] = r;
   }
 }
 
-template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_lbins_fill(Ctx ctx) {
-  const DevState* st = ctx.st;
-  if (st->done) return;
-  const RP* rp = rowptr<RP>(ctx);
-  uint32_t lo, hi;
-  lbins_range(st->nl, &lo, &hi);
-  __shared__ uint32_t sh[kBlock / kWave];
-  uint32_t run[kNumBins];
-  for (int b = 0; b < kNumBins; ++b)
-    run[b] = st->lbin_start[b] + ctx.bin_part[b * gridDim.x + blockIdx.x];
-  for (uint32_t base = lo; base < hi; base += kBlock) {
-    const uint32_t q = base + threadIdx.x;
-    int mybin = -1;
-    if (q < hi) {
-      const uint32_t v = ctx.lperm[q];
-      if (ctx.act[v]) mybin = row_bin((uint64_t)(rp[v + 1] - rp[v]));
-    }
-    for (int b = 0; b < kNumBins; ++b) {
-      uint32_t tot;
-      const uint32_t ex = block_excl_scan(mybin == b ? 1u : 0u, sh, &tot);
-      if (mybin == b) ctx.lrows[run[b] + ex] = q;
-      run[b] += tot;
-    }
-  }
+template <bool W>
+__global__ void __launch_bounds__(kBlock) k_spmv_mid(Ctx ctx, uint32_t heavy) {
+  if (ctx.st->done) return;
+  const int mode = gather_mode(ctx.st->k);
+  if (mode == kGather8)
+    spmv_mid_body<W, kGather8>(ctx, heavy);
+  else if (mode == kGather16)
+    spmv_mid_body<W, kGather16>(ctx, heavy);
+  else
+    spmv_mid_body<W, kGatherC>(ctx, heavy);
 }
 
 // Heavy live rows: their images (written to z by the chunks) into keys.
 __global__ void __launch_bounds__(kBlock) k_live_heavy_fix(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done) return;
-  const uint32_t cnt = st->lbin_cnt[3];
-  const uint32_t* list = ctx.lrows + st->lbin_start[3];
+  const uint32_t cnt = st->n_hlive;
   for (uint32_t t = blockIdx.x * kBlock + threadIdx.x; t < cnt; t += gridDim.x * kBlock) {
-    const uint32_t q = list[t];
+    const uint32_t q = ctx.hq[t];
     ctx.keys[q] = ctx.z[ctx.lperm[q]];
+  }
+}
+
+// Rows and entries of the live rows (diagnostics, and the choice of the
+// propagation-blocking image): st->act_entries, and with 'work' the
+// diagnostic counters.
+__global__ void __launch_bounds__(kBlock) k_live_count(Ctx ctx, int work) {
+  const DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t nl = st->nl;
+  unsigned long long rows = 0, ents = 0;
+  for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
+    const uint32_t l = ctx.rl[q];
+    rows += l ? 1 : 0;
+    ents += l;
+  }
+  __shared__ unsigned long long sr[kBlock], se[kBlock];
+  sr[threadIdx.x] = rows;
+  se[threadIdx.x] = ents;
+  __syncthreads();
+  for (int o = kBlock / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) {
+      sr[threadIdx.x] += sr[threadIdx.x + o];
+      se[threadIdx.x] += se[threadIdx.x + o];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0 && se[0]) {
+    if (work) {
+      atomicAdd(&ctx.st->work_rows, sr[0]);
+      atomicAdd(&ctx.st->work_entries, se[0]);
+    } else {
+      atomicAdd(&ctx.st->act_entries, se[0]);
+    }
   }
 }
 
@@ -449,7 +472,7 @@ __global__ void __launch_bounds__(kBlock) k_spmv_uniform(Ctx ctx) {
   const uint64_t w0 = color_weight(round_key(ctx.st->seed, ctx.st->round), 0);
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
        i += gridDim.x * kBlock)
-    if (ctx.act[i]) ctx.z[i] = mulp(fold61(rp[i + 1] - rp[i]), w0);
+    ctx.z[i] = mulp(fold61(rp[i + 1] - rp[i]), w0);
 }
 
 // Per-round random values for the gather: compact colour array plus the
