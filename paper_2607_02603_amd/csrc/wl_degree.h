@@ -76,8 +76,8 @@ __global__ void __launch_bounds__(kBlock) k_deg_list(Ctx ctx, DegScratch d, uint
 // One workgroup: values d * w of the present degrees, sorted; rank of every
 // degree = number of distinct smaller values; per rank its node count and
 // whether it forms a live class (>= 2 nodes, a non-empty row); live classes
-// numbered in rank order with their member-list offsets.  Writes the next
-// round's live class table and counts, k_new and nosplit.
+// numbered in rank order with their member-list offsets.  Writes the live
+// class table (in place) and the next round's counts, k_new and nosplit.
 __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d) {
   DevState* st = ctx.st;
   const uint32_t D = *d.nd;
@@ -197,9 +197,9 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
         d.roff[r] = off;
         d.rcur[r] = off;
         if (live) {
-          ctx.lcold2[jn] = r;
-          ctx.loff2[jn] = off;
-          ctx.llen2[jn] = size;
+          ctx.lcold[jn] = r;
+          ctx.loff[jn] = off;
+          ctx.llen[jn] = size;
         }
         off += size;
         jn += live ? 1u : 0u;
@@ -223,8 +223,9 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
 }
 
 // New colour of every node; members of live classes placed class after
-// class into the '2' member list (counting placement: one cursor reservation
-// per block and rank), act for every node.
+// class into the member list (counting placement: one cursor reservation per
+// block and rank), act for every node.  Nothing of the live state is read in
+// this round, so the lists are written in place.
 template <bool RP64>
 __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
   const DevState* st = ctx.st;
@@ -254,10 +255,10 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
     ctx.act[i] = live && g > 0 ? 1 : 0;
     if (live) {
       const uint32_t q = atomicAdd(&lc[r], 1u);
-      ctx.lperm2[q] = i;
-      ctx.qcls2[q] = d.rj[r];
-      ctx.rs2[q] = r0;
-      ctx.rl2[q] = g;
+      ctx.lperm[q] = i;
+      ctx.qcls[q] = d.rj[r];
+      ctx.rs[q] = r0;
+      ctx.rl[q] = g;
     }
   }
 }

@@ -459,6 +459,7 @@ struct Session {
   PbCtx pb{};
   uint32_t live_heavy = 0, live_mid = 0;  // blocks of k_spmv_mid
   bool live_mode = false;                  // incremental rounds (run_rsc)
+  bool live_built = false;                 // live classes set up
   // The one-colour round by degree histogram (WL_DEGREE_ROUND=0 turns it off,
   // for testing the general path).
   bool deg_mode = true;
@@ -611,17 +612,24 @@ struct Session {
   }
 
   // SpMV schedule (row bins and heavy chunks); once per call.
-  int build_schedule() {
+  int build_schedule(bool heavy_only = false) {
     const uint32_t nb = scan_blocks(L.n);
     if (rp64)
       hipLaunchKernelGGL(k_bins_count<uint64_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
     else
       hipLaunchKernelGGL(k_bins_count<uint32_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_bins_scan, dim3(1), dim3(kBlock), 0, s, ctx, nb);
-    if (rp64)
-      hipLaunchKernelGGL(k_bins_fill<uint64_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
-    else
-      hipLaunchKernelGGL(k_bins_fill<uint32_t>, dim3(nb), dim3(kBlock), 0, s, ctx);
+    if (rp64) {
+      if (heavy_only)
+        hipLaunchKernelGGL((k_bins_fill<uint64_t, true>), dim3(nb), dim3(kBlock), 0, s, ctx);
+      else
+        hipLaunchKernelGGL((k_bins_fill<uint64_t, false>), dim3(nb), dim3(kBlock), 0, s, ctx);
+    } else {
+      if (heavy_only)
+        hipLaunchKernelGGL((k_bins_fill<uint32_t, true>), dim3(nb), dim3(kBlock), 0, s, ctx);
+      else
+        hipLaunchKernelGGL((k_bins_fill<uint32_t, false>), dim3(nb), dim3(kBlock), 0, s, ctx);
+    }
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     const uint32_t nh = host.bin_cnt[3];
@@ -803,13 +811,14 @@ struct Session {
   template <bool W>
   void live_gather(uint32_t round, bool always) {
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    const uint32_t gl = live_grid();
     hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, ctx, -1);
     if (sflags & WL_STATS_WORK)
-      hipLaunchKernelGGL(k_live_count, dim3(gn), dim3(kBlock), 0, s, ctx, 1);
+      hipLaunchKernelGGL(k_live_count, dim3(gl), dim3(kBlock), 0, s, ctx, 1);
+    const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
     timed_spmv(round, always, false, [&] {
-      hipLaunchKernelGGL(k_spmv_q<W>, dim3(grid_for(L.n, kBlock, 8192)), dim3(kBlock), 0, s,
-                         ctx);
-      hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + live_mid), dim3(kBlock), 0, s, ctx,
+      hipLaunchKernelGGL(k_spmv_q<W>, dim3(gl), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
                          live_heavy);
     });
     if (live_heavy)
@@ -902,12 +911,12 @@ struct Session {
   // Exclusive scan of a (and b) over *lenp entries; totals to tot_a / tot_b.
   // Runs only when *run_if != 0 (run_if NULL: always).
   void xscan(const uint32_t* run_if, const uint32_t* lenp, uint32_t* a, uint32_t* b,
-             uint32_t* tot_a, uint32_t* tot_b) {
-    hipLaunchKernelGGL(k_xscan_part, dim3(nscan), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
+             uint32_t* tot_a, uint32_t* tot_b, uint32_t nblk) {
+    hipLaunchKernelGGL(k_xscan_part, dim3(nblk), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
                        b, ctx.scan_part);
     hipLaunchKernelGGL(k_xscan_top, dim3(1), dim3(kBlock), 0, s, ctx.st, run_if, ctx.scan_part,
-                       nscan, tot_a, tot_b);
-    hipLaunchKernelGGL(k_xscan_final, dim3(nscan), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
+                       nblk, tot_a, tot_b);
+    hipLaunchKernelGGL(k_xscan_final, dim3(nblk), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
                        b, ctx.scan_part);
   }
 
@@ -925,7 +934,7 @@ struct Session {
       hipLaunchKernelGGL(k_live_class_nz<uint32_t>, dim3(gn), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_class_vals, dim3(grid_for(k, kBlock, 4096)), dim3(kBlock), 0, s,
                        ctx);
-    xscan(nullptr, &st->k, ctx.gl, ctx.go, &st->n_live2, &st->nl2);
+    xscan(nullptr, &st->k, ctx.gl, ctx.go, &st->n_live2, &st->nl2, nscan);
     if (rp64)
       hipLaunchKernelGGL(k_live_build<uint64_t>, dim3(gn), dim3(kBlock), 0, s, ctx);
     else
@@ -933,36 +942,41 @@ struct Session {
     hipLaunchKernelGGL(k_live_commit, dim3(gn), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_adopt, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
-    return WL_OK;
+    return pull();
   }
 
   // Sort lists of the live classes.
   void live_segments() {
-    hipLaunchKernelGGL(k_live_segments, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)),
+    hipLaunchKernelGGL(k_live_segments, dim3(grid_for(host.n_live, kBlock, 4096)),
                        dim3(kBlock), 0, s, ctx);
   }
+
+  // Grids of the kernels over the live positions: sized from the last count
+  // read back (the live set only shrinks, so it bounds every later round).
+  uint32_t live_grid() const { return grid_for(host.nl, kBlock, 4096); }
+  uint32_t live_scan_blocks() const { return scan_blocks(host.nl); }
 
   // After the sort: sub-classes, new colours of every node, next live
   // classes, end of the round.
   void live_tail() {
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    const uint32_t gl = live_grid(), ns = live_scan_blocks();
+    const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
     DevState* st = ctx.st;
-    hipLaunchKernelGGL(k_live_scan_part, dim3(nscan), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, nscan);
-    hipLaunchKernelGGL(k_live_scan_final, dim3(nscan), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_nz0, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_subs, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_splits, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)), dim3(kBlock),
-                       0, s, ctx);
-    xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2);
+    hipLaunchKernelGGL(k_live_scan_part, dim3(ns), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, ns);
+    hipLaunchKernelGGL(k_live_scan_final, dim3(ns), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_nz0, dim3(gl), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_subs, dim3(gl), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_splits, dim3(gc), dim3(kBlock), 0, s, ctx);
+    xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
     hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx);
     hipLaunchKernelGGL(k_shift_clear, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_shift_scatter, dim3(grid_for(L.n / 2 + 1, kBlock, 4096)),
-                       dim3(kBlock), 0, s, ctx);
-    xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr);
+    hipLaunchKernelGGL(k_shift_scatter, dim3(gc), dim3(kBlock), 0, s, ctx);
+    xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr, nscan);
     hipLaunchKernelGGL(k_shift_apply, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_emit, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_commit, dim3(gn), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_emit, dim3(gl), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_commit, dim3(gl), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
   }
 
@@ -996,10 +1010,8 @@ struct Session {
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (host.deg_nd > kDegRanks) return WL_OK;
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
     hipLaunchKernelGGL(k_deg_place<RP64>, dim3(grid_for(L.n, kBlock, 2048)), dim3(kBlock), 0, s,
                        ctx, d);
-    hipLaunchKernelGGL(k_live_commit, dim3(gn), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
@@ -1016,12 +1028,23 @@ struct Session {
 
   // One round of the incremental relabel driven from the host (counts read
   // back to size the sorts).
+  bool degree_round_applies() const {
+    return host.k == 1 && !weighted && !ctx.batch && deg_mode && degree_round_fits();
+  }
+
   int round_live() {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
-    if (host.k == 1 && !weighted && !ctx.batch && degree_round_fits() && deg_mode) {
+    if (degree_round_applies()) {
       bool handled = false;
       if (int r = rp64 ? degree_round<true>(&handled) : degree_round<false>(&handled)) return r;
-      if (handled) return WL_OK;
+      if (handled) {
+        live_built = true;
+        return WL_OK;
+      }
+    }
+    if (!live_built) {
+      if (int r = build_live()) return r;
+      live_built = true;
     }
     if (int r = spmv_live()) return r;
     live_segments();
@@ -1076,8 +1099,13 @@ struct Session {
       HIP_LAUNCH_CHECK();
       if (int r = relabel(0)) return r;
     }
-    if (int r = build_schedule()) return r;
-    if (int r = build_live()) return r;
+    if (int r = build_schedule(true)) return r;
+    // The live classes come from the grouping above, unless the first round
+    // is the one-colour degree round, which builds them itself.
+    if (!degree_round_applies()) {
+      if (int r = build_live()) return r;
+      live_built = true;
+    }
     ctx.keys_mat = 1;
     live_mode = true;
     plan_live_grid();
@@ -1091,6 +1119,10 @@ struct Session {
         if (int r = round_live()) return r;
         ++host_rounds;
         continue;
+      }
+      if (!live_built) {
+        if (int r = build_live()) return r;
+        live_built = true;
       }
       const uint32_t base = host.round;
       for (uint32_t i = 0; i < ahead; ++i) round_live_async(base + i);

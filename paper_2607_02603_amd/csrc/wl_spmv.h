@@ -79,7 +79,9 @@ __global__ void __launch_bounds__(kBlock) k_bins_scan(Ctx ctx, uint32_t nblk) {
   }
 }
 
-template <typename RP>
+// HEAVY: only the heavy rows' list (bin 3) is written (the incremental
+// rounds use nothing else of the static schedule).
+template <typename RP, bool HEAVY>
 __global__ void __launch_bounds__(kBlock) k_bins_fill(Ctx ctx) {
   const RP* rp = rowptr<RP>(ctx);
   const uint32_t n = ctx.n;
@@ -93,7 +95,7 @@ __global__ void __launch_bounds__(kBlock) k_bins_fill(Ctx ctx) {
     uint32_t i = base + threadIdx.x;
     int mybin = -1;
     if (i < hi) mybin = row_bin((uint64_t)(rp[i + 1] - rp[i]));
-    for (int b = 0; b < kNumBins; ++b) {
+    for (int b = HEAVY ? 3 : 0; b < kNumBins; ++b) {
       uint32_t tot;
       uint32_t ex = block_excl_scan(mybin == b ? 1u : 0u, sh, &tot);
       if (mybin == b) ctx.rows[run[b] + ex] = i;
