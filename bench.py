@@ -8,7 +8,10 @@ uint64 row pointers, generated on the GPU from seed 0.
 
 Prints one JSON line: GTEPS per refinement round (directed CSR entries x
 rounds / time-to-stable), time-to-stable in ms_per_step, the roofline of the
-dominant kernel and the CPU oracle timed on a bounded sample.
+dominant image launch (the step "z = A w" of a round; on R-MAT scale 27 the
+propagation-blocking image of the full round) and the CPU oracle timed on a
+bounded sample.  The roofline's HBM traffic comes from the rocprofv3 counter
+summary under profiles/ when it was taken on the current kernel source.
 """
 import argparse
 import json
@@ -133,6 +136,41 @@ def make_graph(name, device):
     return wl.Graph.from_numpy(g.n, g.row_ptr, g.col, device=device, symmetric=True), g
 
 
+KINDS = ("gather", "pb", "uniform")
+KIND_KERNELS = {
+    "pb": "k_pb_scatter1+k_pb_scatter2+k_pb_accum (propagation-blocking image, one launch "
+          "= its three passes)",
+    "gather": "k_spmv_q+k_spmv_mid (gathering image of the live rows)",
+    "uniform": "k_deg_hist (one-colour round)",
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pb_image_rmat27_traffic.json")
+
+
+def image_roofline(work, kind_ms, rp_bytes, workload):
+    """Roofline of the dominant image kind (largest device time per step):
+    algorithmic bytes per launch (12 B per entry read: 4 B column index and
+    the 8 B value of its colour; per row the row pointer and the 8 B image)
+    over its average launch time from the library's HIP events."""
+    ms = {kd: sum(m[kd] for m in kind_ms) / len(kind_ms) for kd in KINDS}
+    kd = max(KINDS, key=lambda x: ms[x])
+    w = work[kd]
+    launches = max(1, w["launches"])
+    bytes_per_launch = (12 * w["entries"] + (rp_bytes + 8) * w["rows"]) / launches
+    avg_s = ms[kd] / 1e3 / launches
+    achieved = bytes_per_launch / avg_s / 1e9 if avg_s > 0 else 0.0
+    traffic = None
+    if kd == "pb" and workload == "rmat27" and os.path.exists(TRAFFIC_FILE):
+        from paper_2607_02603_amd import profsum
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        if t.get("source_sha256") == profsum.source_hash():
+            traffic = t["traffic_bytes_per_launch"]
+    return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": KIND_KERNELS[kd],
+            "launches_per_step": launches, "avg_launch_ms": avg_s * 1e3,
+            "bytes_per_launch": bytes_per_launch}
+
+
 def cpu_baseline(dg, seconds_target=15.0):
     """The CPU oracle (one randomized round: image + relabel) on a bounded
     sample of the same graph: the first rows of the CSR, with a pseudo-random
@@ -206,14 +244,14 @@ def main():
     for i in range(args.warmup):
         _, k, rounds = wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
         log(f"warmup {i}: colours={k} rounds={rounds}")
-    # untimed run: work of every SpMV launch (rows, gathered entries)
+    # untimed run: work of every image launch (rows, entries read)
     wl.wl_stats_enable(wl.WL_STATS_TIME | wl.WL_STATS_WORK)
     wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
     work = wl.wl_stats_get()
-    # timed runs: HIP events around every SpMV launch on the library's stream
+    # timed runs: HIP events around every image launch on the library's stream
     wl.wl_stats_enable(wl.WL_STATS_TIME)
     torch.cuda.synchronize()
-    times, spmv_ms = [], []
+    times, kind_ms = [], []
     for i in range(args.steps):
         torch.cuda.synchronize()
         t1 = time.perf_counter()
@@ -221,24 +259,14 @@ def main():
         torch.cuda.synchronize()
         times.append(time.perf_counter() - t1)
         st = wl.wl_stats_get()
-        spmv_ms.append(st["spmv_ms"])
-        log(f"step {i}: {times[-1] * 1e3:.2f} ms colours={k} rounds={rounds} "
-            f"spmv {st['spmv_ms']:.2f} ms in {st['spmv_launches']} launches")
+        kind_ms.append({kd: st[kd]["ms"] for kd in KINDS})
+        log(f"step {i}: {times[-1] * 1e3:.2f} ms colours={k} rounds={rounds} image ms: "
+            + ", ".join(f"{kd} {st[kd]['ms']:.2f} ({st[kd]['launches']})" for kd in KINDS))
     wl.wl_stats_enable(0)
     step_s = sum(times) / len(times)
     gteps = dg.nnz * rounds / step_s / 1e9
-    # Algorithmic bytes of the SpMV kernel: 4 B column index + 8 B gathered
-    # value per entry, row pointer + 8 B image per row.
     rp_bytes = 8 if dg.row_ptr.dtype == torch.int64 else 4
-    spmv_bytes = 12 * work["spmv_entries"] + (rp_bytes + 8) * work["spmv_rows"]
-    spmv_s = sum(spmv_ms) / len(spmv_ms) / 1e3
-    launches = max(1, work["spmv_launches"])
-    achieved = spmv_bytes / spmv_s / 1e9 if spmv_s > 0 else 0.0
-    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                "kernel": "k_spmv", "launches_per_step": launches,
-                "avg_launch_ms": spmv_s * 1e3 / launches,
-                "bytes_per_launch": spmv_bytes / launches}
+    roofline = image_roofline(work, kind_ms, rp_bytes, args.workload)
     model_bytes = (12 * dg.nnz + (36 + rp_bytes) * dg.n) * rounds
     cpu = None
     if not args.no_cpu_baseline:
@@ -261,7 +289,8 @@ def main():
         "config": {"workload": WORKLOADS[args.workload]["desc"], "n": dg.n,
                    "nnz": dg.nnz, "colours": k, "rounds": rounds,
                    "time_to_stable_ms": step_s * 1e3,
-                   "spmv_ms_per_step": spmv_s * 1e3,
+                   "image_ms_per_step": {kd: sum(m[kd] for m in kind_ms) / len(kind_ms)
+                                         for kd in KINDS},
                    "model_round_bytes_frac": model_bytes / step_s / 1e9 / HBM_PEAK_GBS},
         "roofline": roofline,
         "cpu_baseline": cpu,

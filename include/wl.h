@@ -193,26 +193,32 @@ const char *wl_last_error(void);
 
 /* Diagnostics (instrumentation of this library, not part of the method).
  * wl_stats_enable(flags) turns them on for the calling thread:
- *   WL_STATS_TIME  record HIP events on 'stream' around every SpMV launch
- *                  and around the whole call;
+ *   WL_STATS_TIME  record HIP events on 'stream' around every image launch
+ *                  (step "z = A w" of a round) and around the whole call;
  *   WL_STATS_WORK  also count, with one extra reduction kernel per round,
- *                  the rows and CSR entries the SpMV launches read (this
+ *                  the rows and CSR entries each image launch reads (this
  *                  adds device work: use it in an untimed run).
+ * The image of a round is one of three kinds: 'gather' (a row reads its
+ * neighbours' values), 'pb' (propagation blocking on a symmetric graph: its
+ * passes count as one launch) or 'uniform' (rounds with a single colour).
  * wl_stats_get() returns the figures of the last in-core call on this thread.
  * Both return WL_OK, or WL_EINVAL for a NULL pointer / unknown flag. */
 #define WL_STATS_TIME 1
 #define WL_STATS_WORK 2
+typedef struct wl_stats_kind {
+    uint32_t launches;         /* image launches of this kind               */
+    uint32_t pad;
+    double ms;                 /* their summed device time (WL_STATS_TIME)  */
+    uint64_t rows;             /* rows whose image they computed (WORK)     */
+    uint64_t entries;          /* CSR entries they read (WORK)              */
+} wl_stats_kind;
 typedef struct wl_stats {
     uint32_t rounds;           /* rounds of the last call                   */
-    uint32_t spmv_launches;    /* launches of the gathering SpMV kernel     */
-    double spmv_ms;            /* their summed device time (WL_STATS_TIME)  */
-    double call_ms;            /* device time of the whole call             */
-    uint64_t spmv_rows;        /* rows whose image it computed (WORK)       */
-    uint64_t spmv_entries;     /* CSR entries it gathered (WORK)            */
-    uint32_t uniform_launches; /* launches of the one-colour kernel         */
     uint32_t pad;
-    double uniform_ms;         /* their summed device time                  */
-    uint64_t uniform_rows;     /* rows they computed (WORK)                 */
+    double call_ms;            /* device time of the whole call             */
+    wl_stats_kind gather;
+    wl_stats_kind pb;
+    wl_stats_kind uniform;
 } wl_stats;
 int wl_stats_enable(int flags);
 int wl_stats_get(wl_stats *out);

@@ -43,15 +43,24 @@ class WlError(RuntimeError):
         self.code = code
 
 
-class WlStats(ctypes.Structure):
-    _fields_ = [("rounds", ctypes.c_uint32), ("spmv_launches", ctypes.c_uint32),
-                ("spmv_ms", ctypes.c_double), ("call_ms", ctypes.c_double),
-                ("spmv_rows", ctypes.c_uint64), ("spmv_entries", ctypes.c_uint64),
-                ("uniform_launches", ctypes.c_uint32), ("pad", ctypes.c_uint32),
-                ("uniform_ms", ctypes.c_double), ("uniform_rows", ctypes.c_uint64)]
+class WlStatsKind(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_uint32), ("pad", ctypes.c_uint32),
+                ("ms", ctypes.c_double), ("rows", ctypes.c_uint64),
+                ("entries", ctypes.c_uint64)]
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_}
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "pad"}
+
+
+class WlStats(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_uint32), ("pad", ctypes.c_uint32),
+                ("call_ms", ctypes.c_double), ("gather", WlStatsKind),
+                ("pb", WlStatsKind), ("uniform", WlStatsKind)]
+
+    def as_dict(self):
+        return {"rounds": self.rounds, "call_ms": self.call_ms,
+                "gather": self.gather.as_dict(), "pb": self.pb.as_dict(),
+                "uniform": self.uniform.as_dict()}
 
 
 WL_CSR_SYMMETRIC = 1
@@ -275,7 +284,9 @@ def wl_stats_enable(flags):
 
 
 def wl_stats_get():
-    """Diagnostics of the last in-core call on this thread, as a dict."""
+    """Diagnostics of the last in-core call on this thread, as a dict:
+    rounds, call_ms and, per image kind ('gather', 'pb', 'uniform'), the
+    launches, their summed ms, and the rows and entries they read."""
     st = WlStats()
     _check(lib().wl_stats_get(ctypes.byref(st)))
     return st.as_dict()

@@ -20,6 +20,10 @@ constexpr int kNumBins = 4;                // row-length bins of the SpMV
 constexpr int kScanBlocks = 1024;          // blocks of the device-wide scans
 constexpr uint32_t kTableMax = 65535;      // largest k of the compact gathers
 
+// Kinds of image launches (diagnostics): gathering SpMV, propagation
+// blocking, one-colour rounds.
+constexpr int kImgGather = 0, kImgPb = 1, kImgUniform = 2;
+
 // Row-length bins of the SpMV: lanes per row.
 //   bin 0: len <= 8        4 lanes
 //   bin 1: len <= 64      16 lanes
@@ -59,9 +63,7 @@ struct DevState {
   uint32_t n_mid;       // live rows queued for one wave each (this round)
   uint32_t n_hlive;     // live heavy rows (this round)
   uint64_t seed;
-  unsigned long long work_rows;     // diagnostics: rows the SpMV computed
-  unsigned long long work_entries;  // diagnostics: entries it gathered
-  unsigned long long work_uniform;  // diagnostics: rows of the 1-colour path
+  unsigned long long work[3][2];    // diagnostics: rows, entries per image kind
   unsigned long long act_entries;   // entries of the rows whose image is needed
   unsigned long long sym_hash[2];   // validation: hashes of (i, j) and (j, i)
 };

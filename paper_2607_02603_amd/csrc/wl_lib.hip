@@ -476,7 +476,7 @@ struct Session {
     hipEvent_t a, b;
     uint32_t round;  // the round it belongs to
     bool always;     // launched by a host-driven round: it ran
-    bool uniform;
+    int kind;        // kImgGather, kImgPb, kImgUniform
   };
   int sflags = 0;
   hipEvent_t call_ev[2] = {nullptr, nullptr};
@@ -513,8 +513,8 @@ struct Session {
   // Brackets the launches issued by 'launch' with events when timing is on;
   // launches are counted when the round is known to have run.
   template <typename F>
-  void timed_spmv(uint32_t round, bool always, bool uniform, F&& launch) {
-    TimedSpmv t{nullptr, nullptr, round, always, uniform};
+  void timed_spmv(uint32_t round, bool always, int kind, F&& launch) {
+    TimedSpmv t{nullptr, nullptr, round, always, kind};
     if (sflags & WL_STATS_TIME) {
       t.a = next_event();
       t.b = next_event();
@@ -532,13 +532,10 @@ struct Session {
       if (!t.always && t.round >= ran) continue;
       float ms = 0;
       if (t.a && t.b) HIP_TRY(hipEventElapsedTime(&ms, t.a, t.b));
-      if (t.uniform) {
-        stats.uniform_ms += ms;
-        stats.uniform_launches++;
-      } else {
-        stats.spmv_ms += ms;
-        stats.spmv_launches++;
-      }
+      wl_stats_kind& sk = t.kind == kImgPb ? stats.pb
+                          : (t.kind == kImgUniform ? stats.uniform : stats.gather);
+      sk.ms += ms;
+      sk.launches++;
     }
     timed.clear();
     ev_used = 0;
@@ -555,9 +552,12 @@ struct Session {
     }
     if (int r = pull()) return r;
     stats.rounds = host.round;
-    stats.spmv_rows = host.work_rows;
-    stats.spmv_entries = host.work_entries;
-    stats.uniform_rows = host.work_uniform;
+    stats.gather.rows = host.work[kImgGather][0];
+    stats.gather.entries = host.work[kImgGather][1];
+    stats.pb.rows = host.work[kImgPb][0];
+    stats.pb.entries = host.work[kImgPb][1];
+    stats.uniform.rows = host.work[kImgUniform][0];
+    stats.uniform.entries = host.work[kImgUniform][1];
     g_stats = stats;
     return WL_OK;
   }
@@ -706,9 +706,9 @@ struct Session {
       if (int r = pb_plan<RP>()) return r;
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
-                         ctx, 1);
+                         ctx, kImgPb, 1);
     hipLaunchKernelGGL(k_pb_cursors, dim3(grid_for(P.nfine)), dim3(kBlock), 0, s, ctx, pb);
-    timed_spmv(host.round, true, false, [&] {
+    timed_spmv(host.round, true, kImgPb, [&] {
       hipLaunchKernelGGL(k_pb_scatter1<RP>, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 2048)),
                          dim3(kPbThreads), 0, s, ctx, pb);
       if (P.levels == 2) {
@@ -750,8 +750,8 @@ struct Session {
                          0, s, ctx, mode);
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RP>, dim3(grid_for(L.n, kBlock, 4096)),
-                         dim3(kBlock), 0, s, ctx, 0);
-    timed_spmv(h.round, true, uniform, [&] {
+                         dim3(kBlock), 0, s, ctx, uniform ? kImgUniform : kImgGather, 0);
+    timed_spmv(h.round, true, uniform ? kImgUniform : kImgGather, [&] {
       if (uniform)
         hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
                            dim3(kBlock), 0, s, ctx);
@@ -790,8 +790,8 @@ struct Session {
     }
     if (uniform) {
       if (sflags & WL_STATS_WORK)
-        hipLaunchKernelGGL(k_count_work<RP>, dim3(gn), dim3(kBlock), 0, s, ctx, 0);
-      timed_spmv(h.round, true, true, [&] {
+        hipLaunchKernelGGL(k_count_work<RP>, dim3(gn), dim3(kBlock), 0, s, ctx, kImgUniform, 1);
+      timed_spmv(h.round, true, kImgUniform, [&] {
         hipLaunchKernelGGL(k_spmv_uniform<RP>, dim3(grid_for(L.n, kBlock, 8192)),
                            dim3(kBlock), 0, s, ctx);
       });
@@ -816,7 +816,7 @@ struct Session {
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_live_count, dim3(gl), dim3(kBlock), 0, s, ctx, 1);
     const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
-    timed_spmv(round, always, false, [&] {
+    timed_spmv(round, always, kImgGather, [&] {
       hipLaunchKernelGGL(k_spmv_q<W>, dim3(gl), dim3(kBlock), 0, s, ctx);
       hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
                          live_heavy);
@@ -999,8 +999,8 @@ struct Session {
     using RPT = typename std::conditional<RP64, uint64_t, uint32_t>::type;
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_count_work<RPT>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
-                         s, ctx, 0);
-    timed_spmv(host.round, true, true, [&] {
+                         s, ctx, kImgUniform, 1);
+    timed_spmv(host.round, true, kImgUniform, [&] {
       hipLaunchKernelGGL(k_deg_clear, dim3(gd), dim3(kBlock), 0, s, ctx, d, maxd);
       hipLaunchKernelGGL(k_deg_hist<RP64>, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0,
                          s, ctx, d);

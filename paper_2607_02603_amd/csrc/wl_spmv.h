@@ -457,8 +457,8 @@ __global__ void __launch_bounds__(kBlock) k_live_count(Ctx ctx, int work) {
   }
   if (threadIdx.x == 0 && se[0]) {
     if (work) {
-      atomicAdd(&ctx.st->work_rows, sr[0]);
-      atomicAdd(&ctx.st->work_entries, se[0]);
+      atomicAdd(&ctx.st->work[kImgGather][0], sr[0]);
+      atomicAdd(&ctx.st->work[kImgGather][1], se[0]);
     } else {
       atomicAdd(&ctx.st->act_entries, se[0]);
     }
@@ -496,13 +496,13 @@ __global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
     for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c8[i] = (uint8_t)ctx.c[i];
 }
 
-// Diagnostics: rows and entries the next SpMV launch will read (all of them
-// when 'all' is set: the propagation-blocking image reads every entry).
+// Diagnostics: rows and entries the next image launch of 'kind' reads (all
+// of them when 'all' is set: the propagation-blocking image reads every
+// entry); otherwise the rows with act set.
 template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx, int all) {
+__global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx, int kind, int all) {
   if (ctx.st->done) return;
   const RP* rp = rowptr<RP>(ctx);
-  const bool uniform = !ctx.weighted && ctx.st->k == 1;
   unsigned long long rows = 0, ents = 0;
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
        i += gridDim.x * kBlock)
@@ -522,14 +522,11 @@ __global__ void __launch_bounds__(kBlock) k_count_work(Ctx ctx, int all) {
     __syncthreads();
   }
   if (threadIdx.x == 0 && sr[0]) {
-    if (uniform) {
-      atomicAdd(&ctx.st->work_uniform, sr[0]);
-    } else {
-      atomicAdd(&ctx.st->work_rows, sr[0]);
-      atomicAdd(&ctx.st->work_entries, se[0]);
-    }
+    atomicAdd(&ctx.st->work[kind][0], sr[0]);
+    atomicAdd(&ctx.st->work[kind][1], se[0]);
   }
 }
+
 
 // Entries of the rows whose image is needed this round, added to
 // st->act_entries (cleared by k_round_begin).

@@ -149,7 +149,7 @@ def test_stats_count_every_entry(force_pb):
         st = wl.wl_stats_get()
     finally:
         wl.wl_stats_enable(0)
-    assert st["spmv_entries"] == g.nnz and st["spmv_rows"] == g.n
+    assert st["pb"]["entries"] == g.nnz and st["pb"]["rows"] == g.n
 
 
 def test_wrongly_flagged_graph_is_rejected(force_pb, monkeypatch):
