@@ -102,7 +102,8 @@ struct Ctx {
   uint64_t* keys;      // z in position order (big segments)
   uint64_t* keys_tmp;
   uint8_t* flags;      // 1 where a new (colour, z) group starts
-  uint8_t* act;        // 1 if the node's row needs an image (see wl_live.h)
+  uint8_t* act;        // 1 if the node's row needs an image (full relabel); in the
+                       // incremental rounds: 1 for heavy rows of live classes
   uint32_t* ids;       // inclusive scan of flags minus one
   uint32_t* cstart;    // class c occupies perm[cstart[c] .. cstart[c+1])
   uint2* small_list;   // (start, len | kMatBit), 64 < len <= kSmallMax
@@ -156,6 +157,7 @@ struct Ctx {
   uint32_t* midq;      // positions whose rows get one wave each (this round)
   uint32_t* hq;        // positions with heavy rows (this round)
   uint8_t* lsplit;     // per live class: 1 if it split in this round
+  uint8_t* bsame;      // per big segment of a radix pass: 1 if all its keys are equal
 };
 
 }  // namespace wl

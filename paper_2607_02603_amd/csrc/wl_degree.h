@@ -224,8 +224,8 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
 
 // New colour of every node; members of live classes placed class after
 // class into the member list (counting placement: one cursor reservation per
-// block and rank), act for every node.  Nothing of the live state is read in
-// this round, so the lists are written in place.
+// block and rank).  Nothing of the live state is read in this round, so the
+// lists are written in place.
 template <bool RP64>
 __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
   const DevState* st = ctx.st;
@@ -252,7 +252,6 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
     const uint32_t r = e & ~kDegLive;
     ctx.c[i] = r;
     const bool live = (e & kDegLive) != 0;
-    ctx.act[i] = live && g > 0 ? 1 : 0;
     if (live) {
       const uint32_t q = atomicAdd(&lc[r], 1u);
       ctx.lperm[q] = i;

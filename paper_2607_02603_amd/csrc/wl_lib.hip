@@ -72,7 +72,7 @@ struct Layout {
       off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
       off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2],
-      off_rs[2], off_rl[2], off_hq, off_lperm;
+      off_rs[2], off_rl[2], off_hq, off_bsame;
   uint64_t total;
 };
 
@@ -127,7 +127,7 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_rl[0] = take(4 * n);
   L.off_rl[1] = take(4 * n);
   L.off_hq = take(4ull * L.max_heavy);
-  L.off_lperm = take(4 * n);
+  L.off_bsame = take(L.max_big + 1);
   L.total = o;
   return L;
 }
@@ -235,11 +235,11 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   // Live-class state.  The incremental rounds do not use the full relabel's
   // grouping (perm, cstart), its flags, x, or keys_tmp/tiny_list outside the
   // sort, so those regions are shared:
-  //   perm = the sort's payload (original positions), lperm2 = perm_tmp
-  //   (the sort's scratch, written after it), qcls = cstart, gnz = flags,
-  //   gl/go = x, gstart/gend = keys_tmp, split = tiny_list, shift = keys
-  //   (written after the last read of keys).
-  c.lperm = (uint32_t*)(ws + L.off_lperm);
+  //   lperm = perm (the sort's payload), lperm2 = perm_tmp (the sort's
+  //   scratch, written after it), qcls = cstart, gnz = flags, gl/go = x,
+  //   gstart/gend = keys_tmp, split = tiny_list, shift = keys (written after
+  //   the last read of keys).
+  c.lperm = c.perm;
   c.lperm2 = c.perm_tmp;
   c.qcls = c.cstart;
   c.qcls2 = (uint32_t*)(ws + L.off_qcls2);
@@ -267,6 +267,7 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.rl2 = (uint32_t*)(ws + L.off_rl[1]);
   c.midq = c.qcls2;  // consumed by the SpMV before k_live_emit writes qcls2
   c.hq = (uint32_t*)(ws + L.off_hq);
+  c.bsame = ws + L.off_bsame;
   c.lsplit = c.c8;    // written after the SpMV has read the compact colours
   c.weighted = g->weight != nullptr;
   {
@@ -818,6 +819,11 @@ struct Session {
     const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
     timed_spmv(round, always, kImgGather, [&] {
       hipLaunchKernelGGL(k_spmv_q<W>, dim3(gl), dim3(kBlock), 0, s, ctx);
+      if (live_heavy) {
+        const uint32_t gh = grid_for(host.bin_cnt[3], kBlock, 1024);
+        hipLaunchKernelGGL(k_heavy_clear, dim3(gh), dim3(kBlock), 0, s, ctx);
+        hipLaunchKernelGGL(k_heavy_set, dim3(gh), dim3(kBlock), 0, s, ctx);
+      }
       hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
                          live_heavy);
     });
@@ -966,7 +972,10 @@ struct Session {
     hipLaunchKernelGGL(k_live_scan_part, dim3(ns), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, ns);
     hipLaunchKernelGGL(k_live_scan_final, dim3(ns), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_nz0, dim3(gl), dim3(kBlock), 0, s, ctx);
+    if (rp64)
+      hipLaunchKernelGGL(k_live_nz0<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_live_nz0<uint32_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_subs, dim3(gl), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_splits, dim3(gc), dim3(kBlock), 0, s, ctx);
     xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
@@ -975,7 +984,10 @@ struct Session {
     hipLaunchKernelGGL(k_shift_scatter, dim3(gc), dim3(kBlock), 0, s, ctx);
     xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr, nscan);
     hipLaunchKernelGGL(k_shift_apply, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_emit, dim3(gl), dim3(kBlock), 0, s, ctx);
+    if (rp64)
+      hipLaunchKernelGGL(k_live_emit<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_live_emit<uint32_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_commit, dim3(gl), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
   }

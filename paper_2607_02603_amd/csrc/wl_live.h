@@ -14,14 +14,14 @@
 // State kept between rounds (device):
 //   L      live classes in colour order: old colour lcold[j], members at
 //          lperm[loff[j] .. loff[j] + llen[j]); qcls[q] = class of position q.
-//          The sort permutes keys with the original positions (perm), so
-//          after it position q holds the key of member lperm[perm[q]].
+//          The sort permutes lperm with the keys.  A class that does not
+//          split is not moved (the sorts leave classes of equal keys alone),
+//          so rs/rl stay valid by position for it; the members of classes
+//          that split take them from the row pointers.
 //   rs, rl first entry and length of the row of every position's node (an
 //          empty row has key 0; the image is computed only for the others).
 //   act    rows longer than kHeavyChunk use the static heavy chunks, which
-//          check act: it is 1 exactly for the nodes of live classes with a
-//          non-empty row (kept up to date for heavy rows only after the
-//          first live round).
+//          check act; every round sets it for the heavy rows of live classes.
 // One round after the image:
 //   load      keys[q] = z of lperm[q] (0 for an empty row)
 //   sort      segmented sort of the keys inside every live class (the MSD
@@ -158,17 +158,16 @@ __global__ void __launch_bounds__(kBlock) k_live_class_vals(Ctx ctx) {
   }
 }
 
-// Members of the live classes in colour order (into the '2' buffers, made
-// current by k_live_commit), act for every node.
+// Members of the live classes in colour order, with their row spans (into
+// the '2' buffers, made current by k_live_commit).
 template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_live_build(Ctx ctx) {
   const RP* rp = rowptr<RP>(ctx);
   for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n; p += gridDim.x * kBlock) {
     const uint32_t b = ctx.ids[p], v = ctx.perm[p];
     const bool live = class_live(ctx, b);
-    const uint64_t r0 = rp[v], r1 = rp[v + 1];
-    ctx.act[v] = live && r1 > r0 ? 1 : 0;
     if (!live) continue;
+    const uint64_t r0 = rp[v], r1 = rp[v + 1];
     const uint32_t s = ctx.cstart[b];
     const uint32_t j = ctx.gl[b], q = ctx.go[b] + (p - s);
     ctx.lperm2[q] = v;
@@ -193,7 +192,6 @@ __global__ void __launch_bounds__(kBlock) k_live_load(Ctx ctx) {
   const uint32_t nl = st->nl;
   for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
     ctx.keys[q] = ctx.rl[q] ? ctx.z[ctx.lperm[q]] : 0ull;
-    ctx.perm[q] = q;  // sort payload: original position
   }
 }
 
@@ -298,12 +296,13 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
 
 // Sub-classes with key 0 hold a non-empty row if one of their members has
 // one (whose image happens to be 0).
+template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_live_nz0(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
   const uint32_t nl = st->nl;
   for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock)
-    if (ctx.keys[q] == 0 && ctx.rl[ctx.perm[q]]) ctx.gnz[ctx.ids[q]] = 1;
+    if (ctx.keys[q] == 0 && row_nonempty<RP>(ctx, ctx.lperm[q])) ctx.gnz[ctx.ids[q]] = 1;
 }
 
 __device__ __forceinline__ bool sub_live(const Ctx& ctx, uint32_t g) {
@@ -488,35 +487,40 @@ __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
   }
 }
 
-// Exact new colours of the members of live classes, act of the heavy rows
-// whose sub-class is no longer live, and the next live classes ('2'
-// buffers).
+// Exact new colours of the members of classes that split, and the next live
+// classes ('2' buffers).
+template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
+  const RP* rp = rowptr<RP>(ctx);
   const uint32_t nl = st->nl;
   for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock) {
-    const uint32_t o = ctx.perm[q];  // original position of the key now at q
-    const uint32_t v = ctx.lperm[o];
+    const uint32_t v = ctx.lperm[q];
     const uint32_t j = ctx.qcls[q];
     const uint32_t g = ctx.ids[q];
     const uint32_t id = ctx.lcold[j] + g - j;
     const uint32_t gs = ctx.gstart[g];
     const uint32_t len = ctx.gend[g] - gs;
-    // a class that did not split: its colour was moved by k_shift_apply and
-    // it stays live (it has an active member)
-    const bool split = ctx.lsplit[j] != 0;
-    if (split) ctx.c[v] = id;
-    if (split && !(len >= 2 && ctx.gnz[g])) {
-      if (ctx.rl[o] > kHeavyChunk) ctx.act[v] = 0;
-      continue;
+    uint64_t r0;
+    uint32_t rlen;
+    if (ctx.lsplit[j]) {
+      ctx.c[v] = id;
+      if (!(len >= 2 && ctx.gnz[g])) continue;
+      r0 = rp[v];
+      rlen = (uint32_t)(rp[v + 1] - r0);
+    } else {
+      // a class that did not split: its colour was moved by k_shift_apply,
+      // it stays live (it has a non-empty row) and was not reordered
+      r0 = ctx.rs[q];
+      rlen = ctx.rl[q];
     }
     const uint32_t jn = ctx.gl[g], off = ctx.go[g];
     const uint32_t q2 = off + (q - gs);
     ctx.lperm2[q2] = v;
     ctx.qcls2[q2] = jn;
-    ctx.rs2[q2] = ctx.rs[o];
-    ctx.rl2[q2] = ctx.rl[o];
+    ctx.rs2[q2] = r0;
+    ctx.rl2[q2] = rlen;
     if (q == gs) {
       ctx.lcold2[jn] = id;
       ctx.loff2[jn] = off;

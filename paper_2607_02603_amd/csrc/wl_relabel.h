@@ -223,6 +223,13 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
     uint32_t tot;
     const uint32_t off = block_excl_scan(h, sh, &tot);
     ctx.bcur[g] = off;
+    // every key of the segment equal (one bucket, min == max): its elements
+    // are not moved.  Exactly one thread decides (the bucket holding all of
+    // them, or bucket 0 when none does).
+    const bool all_here = h == s.y;
+    const bool none_full = __syncthreads_or(all_here) == 0;
+    if (all_here) ctx.bsame[sgi] = ctx.bmin[g] == ctx.bmax[g] ? 1 : 0;
+    else if (none_full && threadIdx.x == 0) ctx.bsame[sgi] = 0;
     if (h) {
       const uint32_t pos = s.x + off;
       ctx.flags[pos] = 1;
@@ -254,6 +261,7 @@ __global__ void __launch_bounds__(kBlock) k_big_scatter(Ctx ctx, int pass) {
   __shared__ uint32_t lbase[kRadix];
   for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
     TileRange r = tile_range(ctx, cur, nb, t);
+    if (ctx.bsame[r.seg]) continue;  // uniform across the block
     lcnt[threadIdx.x] = 0;
     __syncthreads();
     uint32_t slot[kTilePerThread];
@@ -291,6 +299,7 @@ __global__ void __launch_bounds__(kBlock) k_big_copyback(Ctx ctx, int pass) {
   if (nb == 0) return;
   for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
     TileRange r = tile_range(ctx, cur, nb, t);
+    if (ctx.bsame[r.seg]) continue;
     for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
       ctx.keys[p] = ctx.keys_tmp[p];
       ctx.perm[p] = ctx.perm_tmp[p];

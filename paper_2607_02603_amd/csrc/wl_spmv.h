@@ -340,7 +340,6 @@ __device__ __forceinline__ void spmv_q_body(const Ctx& ctx) {
     if (q < nl) {
       len = ctx.rl[q];
       beg = ctx.rs[q];
-      ctx.perm[q] = q;  // sort payload: original position
     }
     const bool heavy = len > kHeavyChunk;
     const bool mid = len > kShortRow && !heavy;
@@ -384,8 +383,8 @@ __global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx) {
     spmv_q_body<W, kGatherC>(ctx);
 }
 
-// Blocks [0, heavy): the static heavy chunks (rows whose act flag is set);
-// the rest: one wave per queued row.
+// Blocks [0, heavy): the static heavy chunks (rows whose act flag is set by
+// k_heavy_set); the rest: one wave per queued row.
 template <bool W, int M>
 __device__ __forceinline__ void spmv_mid_body(const Ctx& ctx, uint32_t heavy) {
   const uint64_t rkey = round_key(ctx.st->seed, ctx.st->round);
@@ -418,6 +417,25 @@ __global__ void __launch_bounds__(kBlock) k_spmv_mid(Ctx ctx, uint32_t heavy) {
     spmv_mid_body<W, kGather16>(ctx, heavy);
   else
     spmv_mid_body<W, kGatherC>(ctx, heavy);
+}
+
+// act of the heavy rows for the static chunks: 0 for every heavy row, then 1
+// for those of live classes (listed by k_spmv_q).
+__global__ void __launch_bounds__(kBlock) k_heavy_clear(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t nh = st->bin_cnt[3];
+  const uint32_t* list = ctx.rows + st->bin_start[3];
+  for (uint32_t t = blockIdx.x * kBlock + threadIdx.x; t < nh; t += gridDim.x * kBlock)
+    ctx.act[list[t]] = 0;
+}
+
+__global__ void __launch_bounds__(kBlock) k_heavy_set(Ctx ctx) {
+  const DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t cnt = st->n_hlive;
+  for (uint32_t t = blockIdx.x * kBlock + threadIdx.x; t < cnt; t += gridDim.x * kBlock)
+    ctx.act[ctx.lperm[ctx.hq[t]]] = 1;
 }
 
 // Heavy live rows: their images (written to z by the chunks) into keys.
