@@ -136,6 +136,46 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
                        uint32_t *k_out, uint32_t *rounds_out, void *workspace,
                        uint64_t ws_bytes, void *stream);
 
+/* Algorithm 1 (Section 4.1) for a graph whose edge arrays stay in host
+ * memory.  Each round, the rows whose image is needed (those of colour
+ * classes with two or more members) are packed by host threads into
+ * page-locked staging buffers and copied to the device in chunks of at most
+ * 64M entries, on a copy stream of the library's own, while the device
+ * computes the images of the previous chunk; the colours, images and the
+ * relabel stay in the workspace.  The rounds, seeds and colour ids are those
+ * of wl_stable_coloring: for the same graph, labels and seed both return
+ * the same colours, colour count and round count.
+ *   g_host      host CSR (pageable or page-locked), n < 2^31.
+ *   init_host   host labels or NULL (trivial partition).
+ *   color_out_host  host, n entries: raw rank ids as from wl_stable_coloring.
+ *   workspace   device, 256-byte aligned.  wl_streamed_workspace_size()
+ *               gives the size with full chunks (about 69 bytes per node
+ *               plus two chunks); a smaller one, down to chunks of 4096
+ *               entries, is accepted.  Its contents are scratch.
+ * The call also allocates about 2 x 13 bytes (17 weighted) per chunk entry
+ * of page-locked host memory, plus 5 bytes per node, freed on return.
+ * Errors: WL_EINVAL, WL_EBUDGET, WL_EOVERFLOW, WL_EMAXROUNDS, WL_ENOMEM,
+ * WL_EHIP. */
+int wl_streamed_workspace_size(const wl_csr *g, uint64_t *bytes_out);
+int wl_stable_coloring_streamed(const wl_csr *g_host, const uint32_t *init_host,
+                                uint64_t seed, uint32_t max_rounds,
+                                uint32_t *color_out_host, uint32_t *k_out,
+                                uint32_t *rounds_out, void *workspace,
+                                uint64_t ws_bytes, void *stream);
+
+/* Options of wl_stable_coloring_batched.
+ * WL_BATCHED_EXACT: when the contraction stops with several batches (the
+ *   fixed point of Algorithm 2, or WL_BATCHED_EARLY_STOP), finish with
+ *   Algorithm 1 on the last graph (the streamed rounds of
+ *   wl_stable_coloring_streamed, from the labels that graph's nodes carry).
+ *   A quotient keeps every stable colouring of the graph it contracts
+ *   (Definition "Quotient Graph"), so the lifted result is the coarsest
+ *   stable colouring refining the labels, as in-core; coarsest_out is 1.
+ * WL_BATCHED_EARLY_STOP: the termination used in Section 5.4: stop the
+ *   outer loop as soon as the next iteration would not have fewer batches. */
+#define WL_BATCHED_EXACT 1u
+#define WL_BATCHED_EARLY_STOP 2u
+
 /* Algorithm 2 (Section 4.2) for graphs whose edge arrays stay in host
  * memory; only one batch of entries is on the device at a time.  Each batch
  * runs Algorithm 1 with the nodes outside it frozen as singletons; the
@@ -155,16 +195,21 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
  *   color_out_host  host, n entries: first-occurrence canonical colours
  *               (node 0 gets 0, each new colour the next id), so equal
  *               partitions give equal arrays.
- *   k_out, rounds_out (sum over all batch runs), outer_out (outer
- *   iterations), coarsest_out (1 when the last outer iteration had a single
- *   batch, which makes the result the coarsest stable colouring; 0 when the
- *   contraction stopped at a fixed point with several batches).
- * Errors: WL_EINVAL, WL_EBUDGET, WL_EOVERFLOW, WL_EMAXROUNDS, WL_ENOMEM,
- * WL_EHIP. */
+ *   options     0, or WL_BATCHED_EXACT and / or WL_BATCHED_EARLY_STOP.
+ *   k_out, rounds_out (sum over all batch runs and the exact finish),
+ *   outer_out (outer iterations), coarsest_out (1 when the last outer
+ *   iteration had a single batch or the exact finish ran, which makes the
+ *   result the coarsest stable colouring; 0 when the contraction stopped
+ *   with several batches).
+ * The exact finish needs the workspace of wl_stable_coloring_streamed for
+ * the graph it runs on, at least with chunks of 4096 entries.
+ * Errors: WL_EINVAL (also unknown option bits), WL_EBUDGET, WL_EOVERFLOW,
+ * WL_EMAXROUNDS, WL_ENOMEM, WL_EHIP. */
 int wl_stable_coloring_batched(const wl_csr *g_host, const uint32_t *init_host,
                                uint64_t seed, uint64_t max_batch_entries,
-                               uint32_t *color_out_host, uint32_t *k_out,
-                               uint32_t *rounds_out, uint32_t *outer_out,
+                               uint32_t options, uint32_t *color_out_host,
+                               uint32_t *k_out, uint32_t *rounds_out,
+                               uint32_t *outer_out,
                                int *coarsest_out, void *workspace,
                                uint64_t ws_bytes, void *stream);
 

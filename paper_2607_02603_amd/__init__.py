@@ -29,12 +29,15 @@ _NAMES = {-1: "WL_EINVAL", -2: "WL_EBUDGET", -3: "WL_EOVERFLOW",
           -4: "WL_EMAXROUNDS", -5: "WL_ENOTSTABLE", -6: "WL_EHIP", -7: "WL_ENOMEM"}
 
 EXPORTED = ["wl_workspace_size", "wl_batched_workspace_size", "wl_refine_round",
-            "wl_stable_coloring", "wl_stable_coloring_batched", "wl_verify_workspace_size",
-            "wl_verify_stable",
+            "wl_stable_coloring", "wl_stable_coloring_batched", "wl_streamed_workspace_size",
+            "wl_stable_coloring_streamed", "wl_verify_workspace_size", "wl_verify_stable",
             "wl_stats_enable", "wl_stats_get", "wl_last_error"]
 
 WL_STATS_TIME = 1
 WL_STATS_WORK = 2
+
+WL_BATCHED_EXACT = 1
+WL_BATCHED_EARLY_STOP = 2
 
 
 class WlError(RuntimeError):
@@ -91,8 +94,11 @@ def lib():
         L.wl_refine_round.argtypes = [P(WlCsr), vp, u32, u64, u32, vp, P(u32), vp, u64, vp]
         L.wl_stable_coloring.argtypes = [P(WlCsr), vp, u64, u32, vp, P(u32), P(u32), vp,
                                          u64, vp]
-        L.wl_stable_coloring_batched.argtypes = [P(WlCsr), vp, u64, u64, vp, P(u32),
+        L.wl_stable_coloring_batched.argtypes = [P(WlCsr), vp, u64, u64, u32, vp, P(u32),
                                                  P(u32), P(u32), P(i32), vp, u64, vp]
+        L.wl_streamed_workspace_size.argtypes = [P(WlCsr), P(u64)]
+        L.wl_stable_coloring_streamed.argtypes = [P(WlCsr), vp, u64, u32, vp, P(u32), P(u32),
+                                                  vp, u64, vp]
         L.wl_verify_workspace_size.argtypes = [P(WlCsr), P(u64)]
         L.wl_verify_stable.argtypes = [P(WlCsr), vp, u32, vp, u64, vp]
         L.wl_stats_enable.argtypes = [i32]
@@ -240,22 +246,51 @@ def wl_stable_coloring(g, init_color=None, seed=0, max_rounds=0, color_out=None,
 
 
 def wl_stable_coloring_batched(g_host, init_host=None, seed=0, max_batch_entries=0,
-                               ws=None, ws_bytes=None, device="cuda", stream=None):
+                               ws=None, ws_bytes=None, device="cuda", stream=None,
+                               options=0):
     """Algorithm 2.  g_host: Graph with host tensors (pinned recommended).
+    options: WL_BATCHED_EXACT and / or WL_BATCHED_EARLY_STOP.
     Returns (colors (host int32), k, rounds, outer, coarsest)."""
     if ws is None:
         cap = min(max_batch_entries, max(g_host.nnz, 1)) if max_batch_entries else 0
         nb = ws_bytes or wl_batched_workspace_size(g_host, cap)
+        if options & WL_BATCHED_EXACT and not ws_bytes:
+            nb = max(nb, wl_streamed_workspace_size(g_host))
         ws = workspace(nb, device)
     out = torch.empty(g_host.n, dtype=torch.int32)
     k, r, o = ctypes.c_uint32(0), ctypes.c_uint32(0), ctypes.c_uint32(0)
     co = ctypes.c_int(0)
     s = g_host.csr()
     _check(lib().wl_stable_coloring_batched(
-        ctypes.byref(s), _ptr(init_host), seed, max_batch_entries, _ptr(out),
+        ctypes.byref(s), _ptr(init_host), seed, max_batch_entries, options, _ptr(out),
         ctypes.byref(k), ctypes.byref(r), ctypes.byref(o), ctypes.byref(co), _ptr(ws),
         ws.numel(), _stream(stream)))
     return out, int(k.value), int(r.value), int(o.value), bool(co.value)
+
+
+def wl_streamed_workspace_size(g):
+    out = ctypes.c_uint64(0)
+    s = g.csr()
+    _check(lib().wl_streamed_workspace_size(ctypes.byref(s), ctypes.byref(out)))
+    return int(out.value)
+
+
+def wl_stable_coloring_streamed(g_host, init_host=None, seed=0, max_rounds=0, ws=None,
+                                ws_bytes=None, device="cuda", stream=None,
+                                allow_max_rounds=False):
+    """Algorithm 1 with the entries in host memory (streamed image).
+    Returns (colors (host int32), k, rounds); same ids as wl_stable_coloring."""
+    if ws is None:
+        ws = workspace(ws_bytes or wl_streamed_workspace_size(g_host), device)
+    out = torch.empty(g_host.n, dtype=torch.int32)
+    k, r = ctypes.c_uint32(0), ctypes.c_uint32(0)
+    s = g_host.csr()
+    code = lib().wl_stable_coloring_streamed(
+        ctypes.byref(s), _ptr(init_host), seed, max_rounds, _ptr(out), ctypes.byref(k),
+        ctypes.byref(r), _ptr(ws), ws.numel(), _stream(stream))
+    if not (allow_max_rounds and code == WL_EMAXROUNDS):
+        _check(code)
+    return out, int(k.value), int(r.value)
 
 
 def wl_verify_workspace_size(g):

@@ -10,6 +10,9 @@
 #include <sched.h>
 
 #include <algorithm>
+#include <condition_variable>
+#include <functional>
+#include <mutex>
 #include <memory>
 #include <new>
 #include <thread>
@@ -22,10 +25,12 @@
 #include <cstring>
 
 #include "../../include/wl.h"
+#include "wl_host.h"
 #include "wl_ctx.h"
 #include "wl_relabel.h"
 #include "wl_live.h"
 #include "wl_degree.h"
+#include "wl_stream.h"
 #include "wl_spmv.h"
 #include "wl_push.h"
 #include "wl_quotient.h"
@@ -65,6 +70,8 @@ constexpr uint64_t kAlign = 256;
 uint64_t align_up(uint64_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 // Sizes of every workspace region for a graph with n nodes, nnz entries.
+// in_core = false: a session whose image is computed elsewhere (the streamed
+// rounds), without the SpMV schedule and the live-class state.
 struct Layout {
   uint64_t n, nnz;
   uint32_t max_small, max_big, max_chunks, max_heavy;
@@ -76,8 +83,9 @@ struct Layout {
   uint64_t total;
 };
 
-Layout make_layout(uint64_t n, uint64_t nnz) {
+Layout make_layout(uint64_t n, uint64_t nnz, bool in_core = true) {
   Layout L{};
+  const uint64_t nc = in_core ? n : 0;
   L.n = n;
   L.nnz = nnz;
   L.max_small = (uint32_t)(n / 2 + 1);
@@ -111,22 +119,22 @@ Layout make_layout(uint64_t n, uint64_t nnz) {
   L.off_bmax = take(8ull * L.max_big * kRadix);
   L.off_bcur = take(4ull * L.max_big * kRadix);
   L.off_scan = take(8ull * kScanBlocks);
-  L.off_rows = take(4 * n);
+  L.off_rows = take(4 * nc);
   L.off_binpart = take(4ull * kNumBins * kScanBlocks);
-  L.off_chunks = take(sizeof(HeavyChunk) * (uint64_t)L.max_chunks);
-  L.off_hacc = take(16ull * L.max_heavy);
-  L.off_hcnt = take(4ull * L.max_heavy);
+  L.off_chunks = take(in_core ? sizeof(HeavyChunk) * (uint64_t)L.max_chunks : 0);
+  L.off_hacc = take(in_core ? 16ull * L.max_heavy : 0);
+  L.off_hcnt = take(in_core ? 4ull * L.max_heavy : 0);
   L.off_wtab = take(8ull * std::min<uint64_t>(n, kTableMax));
   L.off_c16 = take(2 * n);
-  L.off_qcls2 = take(4 * n);
+  L.off_qcls2 = take(4 * nc);
   // live classes have >= 2 members: at most n / 2 of them, three words each
-  L.off_lcls[0] = take(12ull * (n / 2 + 1));
-  L.off_lcls[1] = take(12ull * (n / 2 + 1));
-  L.off_rs[0] = take(8 * n);
-  L.off_rs[1] = take(8 * n);
-  L.off_rl[0] = take(4 * n);
-  L.off_rl[1] = take(4 * n);
-  L.off_hq = take(4ull * L.max_heavy);
+  L.off_lcls[0] = take(in_core ? 12ull * (n / 2 + 1) : 0);
+  L.off_lcls[1] = take(in_core ? 12ull * (n / 2 + 1) : 0);
+  L.off_rs[0] = take(8 * nc);
+  L.off_rs[1] = take(8 * nc);
+  L.off_rl[0] = take(4 * nc);
+  L.off_rl[1] = take(4 * nc);
+  L.off_hq = take(in_core ? 4ull * L.max_heavy : 0);
   L.off_bsame = take(L.max_big + 1);
   L.total = o;
   return L;
@@ -1161,8 +1169,8 @@ struct Session {
 };
 
 int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
-                 uint64_t ws_bytes, void* stream) {
-  S.L = make_layout(g->n, g->nnz);
+                 uint64_t ws_bytes, void* stream, bool in_core = true) {
+  S.L = make_layout(g->n, g->nnz, in_core);
   if (!ws) return fail(WL_EINVAL, "workspace is NULL");
   if ((uintptr_t)ws % kAlign)
     return fail(WL_EINVAL, "workspace must be %llu-byte aligned",
@@ -1220,23 +1228,6 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
 
 // The current graph G_t in host memory (the caller's arrays for t = 0, the
 // library's quotient arrays afterwards).
-struct HostGraph {
-  uint64_t n = 0, m = 0;
-  const uint32_t* rp32 = nullptr;
-  const uint64_t* rp64 = nullptr;
-  const uint32_t* col = nullptr;
-  const uint32_t* wt = nullptr;
-  uint64_t rp(uint64_t i) const { return rp64 ? rp64[i] : (uint64_t)rp32[i]; }
-  // first row i in [0, n] with rp(i) >= v
-  uint64_t lower_row(uint64_t v) const {
-    uint64_t lo = 0, hi = n;
-    while (lo < hi) {
-      uint64_t mid = (lo + hi) / 2;
-      if (rp(mid) < v) lo = mid + 1; else hi = mid;
-    }
-    return lo;
-  }
-};
 
 // Device workspace of the refinement phase: a batch's local CSR and labels
 // plus the in-core state for up to n0 rows and mb entries.
@@ -1560,11 +1551,275 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
   return WL_OK;
 }
 
+
+// ---------------------------------------------------------------------------
+// Algorithm 1 with the entries in host memory: the image of every round is
+// streamed through the device chunk by chunk (wl_stream.h); the node state
+// and the relabel stay on the device.
+// ---------------------------------------------------------------------------
+
+
+// Page-locked host memory owned by the library.
+struct PinnedBuf {
+  uint8_t* p = nullptr;
+  ~PinnedBuf() { release(); }
+  void release() {
+    if (p) (void)hipHostFree(p);
+    p = nullptr;
+  }
+  // false when the allocation is refused (page-locked memory is limited)
+  bool try_alloc(uint64_t bytes) {
+    release();
+    if (hipHostMalloc((void**)&p, bytes ? bytes : 8, hipHostMallocDefault) != hipSuccess) {
+      p = nullptr;
+      (void)hipGetLastError();
+      return false;
+    }
+    return true;
+  }
+};
+
+constexpr uint64_t kStreamMaxChunk = 64ull << 20;  // entries per chunk
+constexpr uint64_t kStreamMinStage = 1ull << 16;   // smallest staged chunk (entries)
+
+
+// One chunk's arrays (device slot, or host staging without 'part').
+struct StreamSlot {
+  uint64_t node, off, col, wt, part, fold, total;
+};
+StreamSlot stream_slot(uint64_t mc, bool weighted, bool device) {
+  StreamSlot L{};
+  uint64_t o = 0;
+  auto take = [&](uint64_t b) { uint64_t at = o; o = align_up(o + b); return at; };
+  const uint64_t sc = stream_segs(mc);
+  L.node = take(4 * sc);
+  L.off = take(8 * (sc + 1));
+  L.col = take(4 * mc);
+  L.wt = take(weighted ? 4 * mc : 0);
+  L.part = take(device ? 8 * sc : 0);
+  L.fold = take(16 * stream_folds(mc));
+  L.total = o;
+  return L;
+}
+
+struct StreamLayout {
+  uint64_t core, core_bytes, colors, slot[2], total;
+  StreamSlot sl;
+};
+StreamLayout stream_layout(uint64_t n, uint64_t mc, bool weighted) {
+  StreamLayout L{};
+  uint64_t o = 0;
+  auto take = [&](uint64_t b) { uint64_t at = o; o = align_up(o + b); return at; };
+  L.core_bytes = make_layout(n, 0, false).total;
+  L.core = take(L.core_bytes);
+  L.colors = take(4 * n);
+  L.sl = stream_slot(mc, weighted, true);
+  L.slot[0] = take(L.sl.total);
+  L.slot[1] = take(L.sl.total);
+  L.total = o;
+  return L;
+}
+
+uint64_t stream_chunk_cap(const HostGraph& G) {
+  return std::min<uint64_t>(kStreamMaxChunk, std::max<uint64_t>(G.m, 1));
+}
+
+// Events and the copy stream of the streamed rounds.
+struct StreamRes {
+  hipStream_t cs = nullptr;
+  hipEvent_t copied[2] = {nullptr, nullptr}, computed[2] = {nullptr, nullptr};
+  ~StreamRes() {
+    if (cs) (void)hipStreamSynchronize(cs);
+    for (int i = 0; i < 2; ++i) {
+      if (copied[i]) (void)hipEventDestroy(copied[i]);
+      if (computed[i]) (void)hipEventDestroy(computed[i]);
+    }
+    if (cs) (void)hipStreamDestroy(cs);
+  }
+};
+
+// Algorithm 1 on the host graph G from its labels (or the trivial
+// partition).  Colours (raw rank ids, as in the in-core path) to color_host;
+// *done_out: 1 stable, 2 round cap reached.
+int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
+                 uint32_t max_rounds, uint8_t* W, uint64_t ws_bytes, hipStream_t s,
+                 uint32_t* color_host, uint32_t* k_out, uint32_t* rounds_out, int* done_out) {
+  const uint64_t n = G.n;
+  const bool weighted = G.wt != nullptr;
+  const uint64_t mc = largest_fitting(
+      [&](uint64_t c) { return stream_layout(n, c, weighted).total; }, ws_bytes,
+      stream_chunk_cap(G));
+  if (mc < std::min<uint64_t>(kSegMax, std::max<uint64_t>(G.m, 1)))
+    return fail(WL_EBUDGET, "workspace of %llu bytes holds no chunk of %u entries",
+                (unsigned long long)ws_bytes, kSegMax);
+  const StreamLayout SL = stream_layout(n, mc, weighted);
+  uint32_t* colors_dev = (uint32_t*)(W + SL.colors);
+  wl_csr vg{};
+  vg.n = n;
+  Session S;
+  if (int r = open_session(S, &vg, colors_dev, W + SL.core, SL.core_bytes, s, false)) return r;
+  const uint32_t cap = max_rounds ? max_rounds : (uint32_t)std::min<uint64_t>(n + 1, 0xFFFFFFFFull);
+  if (int r = S.init_state(seed, 1, 0, cap, 1)) return r;
+  if (int r = S.stats_begin()) return r;
+
+  HostPool pool;
+  const unsigned T = pool.size();
+  // page-locked staging for two chunks; the chunk shrinks when that much
+  // page-locked memory is refused (the device slots keep their size)
+  PinnedBuf stage[2];
+  uint64_t mcs = mc;
+  for (;;) {
+    const uint64_t bytes = stream_slot(mcs, weighted, false).total;
+    if (stage[0].try_alloc(bytes) && stage[1].try_alloc(bytes)) break;
+    stage[0].release();
+    stage[1].release();
+    if (mcs <= std::min(kStreamMinStage, mc))
+      return fail(WL_ENOMEM, "no page-locked staging of %llu bytes",
+                  (unsigned long long)bytes);
+    mcs = std::max(std::min(kStreamMinStage, mc), mcs / 2);
+  }
+  const StreamSlot HS = stream_slot(mcs, weighted, false);
+  const uint64_t sc = stream_segs(mcs);
+  std::vector<uint8_t> act_h;
+  std::vector<uint32_t> deg_h;
+  StreamRes R;
+  HIP_TRY(hipStreamCreateWithFlags(&R.cs, hipStreamNonBlocking));
+  for (int i = 0; i < 2; ++i) {
+    HIP_TRY(hipEventCreateWithFlags(&R.copied[i], hipEventDisableTiming));
+    HIP_TRY(hipEventCreateWithFlags(&R.computed[i], hipEventDisableTiming));
+    HIP_TRY(hipEventRecord(R.copied[i], R.cs));
+    HIP_TRY(hipEventRecord(R.computed[i], s));
+  }
+  HostCopy hc(s);
+
+  const uint32_t gn = grid_for(n, kBlock, 4096);
+  hipLaunchKernelGGL(k_iota_zero, dim3(gn), dim3(kBlock), 0, s, S.ctx);
+  HIP_LAUNCH_CHECK();
+  if (labels) {
+    uint32_t* lab_dev = (uint32_t*)S.ctx.x;
+    if (int r = hc.h2d(lab_dev, labels, 4 * n)) return r;
+    hipLaunchKernelGGL(k_labels_to_z, dim3(gn), dim3(kBlock), 0, s, S.ctx, lab_dev);
+    HIP_LAUNCH_CHECK();
+    if (int r = S.relabel(0)) return r;
+  }
+
+  StreamPlan plan;
+  auto node_lo = [&](unsigned t) { return n * t / T; };
+
+  while (!S.host.done) {
+    hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, S.ctx);
+    HIP_LAUNCH_CHECK();
+    bool uniform = S.host.k == 1 && !weighted;
+    if (uniform) {
+      // z_i = deg_i * w: the degrees only
+      deg_h.resize(n);
+      std::vector<uint8_t> big(T, 0);
+      uint32_t* deg = deg_h.data();
+      pool.run([&](unsigned t) {
+        for (uint64_t i = node_lo(t); i < node_lo(t + 1); ++i) {
+          const uint64_t d = G.rp(i + 1) - G.rp(i);
+          if (d > 0xFFFFFFFFull) big[t] = 1;
+          deg[i] = (uint32_t)d;
+        }
+      });
+      for (unsigned t = 0; t < T; ++t) uniform = uniform && !big[t];
+      if (uniform) {
+        uint32_t* deg_dev = (uint32_t*)S.ctx.keys_tmp;
+        if (int r = hc.h2d(deg_dev, deg, 4 * n)) return r;
+        hipLaunchKernelGGL(k_stream_uniform, dim3(gn), dim3(kBlock), 0, s, S.ctx, deg_dev);
+        HIP_LAUNCH_CHECK();
+      }
+    }
+    if (!uniform) {
+      act_h.resize(n);
+      hipLaunchKernelGGL(k_zero_u64, dim3(grid_for(n, kBlock, 4096)), dim3(kBlock), 0, s,
+                         S.ctx.z, n);
+      hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, S.ctx, -1);
+      HIP_LAUNCH_CHECK();
+      if (int r = hc.d2h(act_h.data(), S.ctx.act, n)) return r;
+      plan.build(pool, G, act_h.data());
+      uint64_t a = 0;
+      int slot = 0;
+      while (a < plan.ns) {
+        const uint64_t b = plan.chunk_end(a, mcs, sc);
+        const uint64_t len = plan.entry_of(b) - plan.entry_of(a), nseg = b - a;
+        HIP_TRY(hipEventSynchronize(R.copied[slot]));
+        uint8_t* H = stage[slot].p;
+        uint32_t* hnode = (uint32_t*)(H + HS.node);
+        uint64_t* hoff = (uint64_t*)(H + HS.off);
+        uint32_t* hcol = (uint32_t*)(H + HS.col);
+        uint32_t* hwt = (uint32_t*)(H + HS.wt);
+        StreamFold* hfold = (StreamFold*)(H + HS.fold);
+        const int64_t nfs = plan.pack(pool, G, a, b, hnode, hoff, hcol, weighted ? hwt : nullptr,
+                                      hfold, stream_folds(mcs));
+        if (nfs < 0) return fail(WL_EINVAL, "chunk plan exceeds its fold table");
+        const uint64_t nf = (uint64_t)nfs;
+        uint8_t* D = W + SL.slot[slot];
+        HIP_TRY(hipStreamWaitEvent(R.cs, R.computed[slot], 0));
+        HIP_TRY(hipMemcpyAsync(D + SL.sl.node, hnode, 4 * nseg, hipMemcpyHostToDevice, R.cs));
+        HIP_TRY(hipMemcpyAsync(D + SL.sl.off, hoff, 8 * (nseg + 1), hipMemcpyHostToDevice, R.cs));
+        HIP_TRY(hipMemcpyAsync(D + SL.sl.col, hcol, 4 * len, hipMemcpyHostToDevice, R.cs));
+        if (weighted)
+          HIP_TRY(hipMemcpyAsync(D + SL.sl.wt, hwt, 4 * len, hipMemcpyHostToDevice, R.cs));
+        if (nf)
+          HIP_TRY(hipMemcpyAsync(D + SL.sl.fold, hfold, 16 * nf, hipMemcpyHostToDevice, R.cs));
+        HIP_TRY(hipEventRecord(R.copied[slot], R.cs));
+        HIP_TRY(hipStreamWaitEvent(s, R.copied[slot], 0));
+        StreamChunk ch;
+        ch.node = (const uint32_t*)(D + SL.sl.node);
+        ch.off = (const uint64_t*)(D + SL.sl.off);
+        ch.col = (const uint32_t*)(D + SL.sl.col);
+        ch.wt = weighted ? (const uint32_t*)(D + SL.sl.wt) : nullptr;
+        ch.part = (uint64_t*)(D + SL.sl.part);
+        ch.fold = (const StreamFold*)(D + SL.sl.fold);
+        ch.nseg = (uint32_t)nseg;
+        ch.nfold = (uint32_t)nf;
+        const uint32_t gs = grid_for(nseg, kBlock / kWave, 16384);
+        if (weighted)
+          hipLaunchKernelGGL(k_stream_seg<true>, dim3(gs), dim3(kBlock), 0, s, S.ctx, ch);
+        else
+          hipLaunchKernelGGL(k_stream_seg<false>, dim3(gs), dim3(kBlock), 0, s, S.ctx, ch);
+        if (nf)
+          hipLaunchKernelGGL(k_stream_fold, dim3(grid_for(nf, kBlock, 1024)), dim3(kBlock), 0,
+                             s, S.ctx, ch);
+        HIP_LAUNCH_CHECK();
+        HIP_TRY(hipEventRecord(R.computed[slot], s));
+        a = b;
+        slot ^= 1;
+      }
+    }
+    if (int r = S.relabel(1)) return r;
+  }
+  if (int r = S.stats_end()) return r;
+  if (int r = hc.d2h(color_host, colors_dev, 4 * n)) return r;
+  *k_out = S.host.k;
+  *rounds_out = S.host.round;
+  *done_out = (int)S.host.done;
+  return WL_OK;
+}
+
+// Final colours of the original nodes: the colour of the node of Gf each
+// maps to, numbered by first occurrence.
+void canonical_colours(const std::vector<uint32_t>& map0, const uint32_t* col_f, uint64_t nf,
+                       uint32_t* color_out, uint32_t* k_out) {
+  std::vector<uint32_t> slot(nf, 0xFFFFFFFFu);
+  uint32_t k = 0;
+  for (uint64_t v = 0; v < map0.size(); ++v) {
+    const uint32_t c = col_f ? col_f[map0[v]] : map0[v];
+    uint32_t& sl = slot[c];
+    if (sl == 0xFFFFFFFFu) sl = k++;
+    color_out[v] = sl;
+  }
+  *k_out = k;
+}
+
 int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
-                uint64_t max_batch, uint32_t* color_out, uint32_t* k_out,
+                uint64_t max_batch, uint32_t options, uint32_t* color_out, uint32_t* k_out,
                 uint32_t* rounds_out, uint32_t* outer_out, int* coarsest_out,
                 void* ws, uint64_t ws_bytes, hipStream_t s) {
   const uint64_t n0 = g->n;
+  const bool exact = (options & WL_BATCHED_EXACT) != 0;
+  const bool early = (options & WL_BATCHED_EARLY_STOP) != 0;
   uint8_t* W = (uint8_t*)ws;
   const char* tr = getenv("WL_TRACE_BATCHED");
   const bool trace = tr && tr[0] == '1';
@@ -1591,19 +1846,16 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   std::vector<uint32_t> hdeg;
   std::vector<uint64_t> piece_rp(3);
 
-  for (uint64_t t = 0;; ++t) {
-    const uint64_t n = G.n;
-    // ---- batch cap: the caller's, or the largest whose batches fit
-    const uint64_t mall = std::max<uint64_t>(G.m, 1);  // a cap >= nnz is one batch
-    uint64_t mb;
-    std::vector<uint64_t> starts;
+  // batch cap for graph G: the caller's, or the largest whose batches fit
+  auto plan_batches = [&](const HostGraph& Gp, uint64_t* mb_out,
+                          std::vector<uint64_t>* starts_out) -> int {
+    const uint64_t mall = std::max<uint64_t>(Gp.m, 1);  // a cap >= nnz is one batch
     if (max_batch) {
-      mb = std::min(max_batch, mall);
-      starts = cut_batches(G, mb);
+      *mb_out = std::min(max_batch, mall);
     } else {
       auto fits = [&](uint64_t cap) {
-        const std::vector<uint64_t> st = cut_batches(G, cap);
-        return refine_layout(max_inner_rows(G, st), cap).total <= ws_bytes;
+        const std::vector<uint64_t> st = cut_batches(Gp, cap);
+        return refine_layout(max_inner_rows(Gp, st), cap).total <= ws_bytes;
       };
       uint64_t lo = 0, hi = std::min(mall, ws_bytes / 8);
       while (lo < hi) {
@@ -1613,9 +1865,37 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       if (lo == 0)
         return fail(WL_EBUDGET, "workspace of %llu bytes holds no batch",
                     (unsigned long long)ws_bytes);
-      mb = lo;
-      starts = cut_batches(G, mb);
+      *mb_out = lo;
     }
+    *starts_out = cut_batches(Gp, *mb_out);
+    return WL_OK;
+  };
+  // Algorithm 1 on Gf with its entries streamed from host memory; the
+  // result, lifted through map0, is the final colouring
+  auto finish_exact = [&](const HostGraph& Gf) -> int {
+    std::vector<uint32_t> col_f(Gf.n);
+    uint32_t kf = 0, rf = 0;
+    int done = 0;
+    if (int r = streamed_run(Gf, labels.empty() ? nullptr : labels.data(), seed, 0, W,
+                             ws_bytes, s, col_f.data(), &kf, &rf, &done))
+      return r;
+    if (done == 2) return fail(WL_EMAXROUNDS, "streamed refinement did not stabilise");
+    rounds += rf;
+    if (trace)
+      fprintf(stderr, "[wl batched] exact finish on n=%llu m=%llu: colours %u rounds %u\n",
+              (unsigned long long)Gf.n, (unsigned long long)Gf.m, kf, rf);
+    canonical_colours(map0, col_f.data(), Gf.n, color_out, k_out);
+    *rounds_out = (uint32_t)std::min<uint64_t>(rounds, 0xFFFFFFFFull);
+    *outer_out = outer;
+    *coarsest_out = 1;
+    return WL_OK;
+  };
+  uint64_t mb = 0;
+  std::vector<uint64_t> starts;
+  if (int r = plan_batches(G, &mb, &starts)) return r;
+
+  for (uint64_t t = 0;; ++t) {
+    const uint64_t n = G.n;
     const uint64_t nb = starts.size() - 1;
     const uint64_t rows_cap = max_inner_rows(G, starts);
     const RefineLayout RL = refine_layout(rows_cap, mb);
@@ -1705,11 +1985,13 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       }
     }
     ++outer;
-    for (uint64_t v = 0; v < n0; ++v) map0[v] = blk[map0[v]];
     const uint64_t nq = next;
     if (trace)
       fprintf(stderr, "[wl batched] t=%llu merged blocks=%llu rounds so far=%llu\n",
               (unsigned long long)t, (unsigned long long)nq, (unsigned long long)rounds);
+    // fixed point with several batches: the exact finish runs on G_t itself
+    if (nb > 1 && nq == n && exact) return finish_exact(G);
+    for (uint64_t v = 0; v < n0; ++v) map0[v] = blk[map0[v]];
     if (nb == 1 || nq == n) {
       *coarsest_out = (nb == 1) ? 1 : 0;
       break;
@@ -1873,16 +2155,17 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     G.rp64 = qrp_buf.as<const uint64_t>();
     G.col = qcol_buf.as<const uint32_t>();
     G.wt = qwt_buf.as<const uint32_t>();
+    if (int r = plan_batches(G, &mb, &starts)) return r;
+    // Section 5.4's termination: stop when the next iteration would not
+    // have fewer batches
+    if (early && starts.size() - 1 >= nb) {
+      if (exact) return finish_exact(G);
+      *coarsest_out = 0;
+      break;
+    }
   }
   // final colours: first occurrence over the original nodes
-  mapk.assign(n0, 0xFFFFFFFFu);
-  uint32_t k = 0;
-  for (uint64_t v = 0; v < n0; ++v) {
-    uint32_t& slot = mapk[map0[v]];
-    if (slot == 0xFFFFFFFFu) slot = k++;
-    color_out[v] = slot;
-  }
-  *k_out = k;
+  canonical_colours(map0, nullptr, G.n, color_out, k_out);
   *rounds_out = (uint32_t)std::min<uint64_t>(rounds, 0xFFFFFFFFull);
   *outer_out = outer;
   return WL_OK;
@@ -2088,7 +2371,7 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
 }
 
 int wl_stable_coloring_batched(const wl_csr* g_host, const uint32_t* init_host,
-                               uint64_t seed, uint64_t max_batch_entries,
+                               uint64_t seed, uint64_t max_batch_entries, uint32_t options,
                                uint32_t* color_out_host, uint32_t* k_out,
                                uint32_t* rounds_out, uint32_t* outer_out,
                                int* coarsest_out, void* workspace, uint64_t ws_bytes,
@@ -2110,9 +2393,55 @@ int wl_stable_coloring_batched(const wl_csr* g_host, const uint32_t* init_host,
   const uint64_t last = g_host->row_ptr64 ? g_host->row_ptr64[g_host->n]
                                           : g_host->row_ptr32[g_host->n];
   if (last != g_host->nnz) return fail(WL_EINVAL, "row_ptr[n] != nnz");
-  return batched_run(g_host, init_host, seed, max_batch_entries, color_out_host, k_out,
+  if (options & ~(WL_BATCHED_EXACT | WL_BATCHED_EARLY_STOP))
+    return fail(WL_EINVAL, "unknown option bits 0x%x", options);
+  return batched_run(g_host, init_host, seed, max_batch_entries, options, color_out_host, k_out,
                      rounds_out, outer_out, coarsest_out, workspace, ws_bytes,
                      (hipStream_t)stream);
+}
+
+int wl_streamed_workspace_size(const wl_csr* g, uint64_t* bytes_out) {
+  g_err[0] = 0;
+  if (!g || !bytes_out) return fail(WL_EINVAL, "NULL argument");
+  if (g->n >= (1ull << 31)) return fail(WL_EOVERFLOW, "the streamed path needs n < 2^31");
+  HostGraph G;
+  G.n = g->n;
+  G.m = g->nnz;
+  *bytes_out = stream_layout(g->n, stream_chunk_cap(G), g->weight != nullptr).total;
+  return WL_OK;
+}
+
+int wl_stable_coloring_streamed(const wl_csr* g_host, const uint32_t* init_host, uint64_t seed,
+                                uint32_t max_rounds, uint32_t* color_out_host, uint32_t* k_out,
+                                uint32_t* rounds_out, void* workspace, uint64_t ws_bytes,
+                                void* stream) {
+  g_err[0] = 0;
+  if (int r = check_graph(g_host)) return r;
+  if (!k_out || !rounds_out) return fail(WL_EINVAL, "output scalar is NULL");
+  *k_out = 0;
+  *rounds_out = 0;
+  if (g_host->n >= (1ull << 31)) return fail(WL_EOVERFLOW, "the streamed path needs n < 2^31");
+  if (g_host->n == 0) return WL_OK;
+  if (!color_out_host) return fail(WL_EINVAL, "color_out_host is NULL");
+  if (!workspace) return fail(WL_EINVAL, "workspace is NULL");
+  if ((uintptr_t)workspace % kAlign) return fail(WL_EINVAL, "workspace must be 256-byte aligned");
+  HostGraph G;
+  G.n = g_host->n;
+  G.m = g_host->nnz;
+  G.rp32 = g_host->row_ptr32;
+  G.rp64 = g_host->row_ptr64;
+  G.col = g_host->col_idx;
+  G.wt = g_host->weight;
+  if (G.rp(0) != 0 || G.rp(G.n) != G.m) return fail(WL_EINVAL, "row_ptr[0] != 0 or row_ptr[n] != nnz");
+  for (uint64_t i = 0; i < G.n; ++i)
+    if (G.rp(i + 1) < G.rp(i)) return fail(WL_EINVAL, "row_ptr is not non-decreasing");
+  if (G.m > 0 && !G.col) return fail(WL_EINVAL, "col_idx is NULL");
+  int done = 0;
+  if (int r = streamed_run(G, init_host, seed, max_rounds, (uint8_t*)workspace, ws_bytes,
+                           (hipStream_t)stream, color_out_host, k_out, rounds_out, &done))
+    return r;
+  if (done == 2) return fail(WL_EMAXROUNDS, "no stable colouring after %u rounds", *rounds_out);
+  return WL_OK;
 }
 
 int wl_verify_workspace_size(const wl_csr* g, uint64_t* bytes_out) {

@@ -1,0 +1,207 @@
+"""GPU parity of Algorithm 1 with the entries in host memory
+(wl_stable_coloring_streamed) against the oracle: identical raw colour ids,
+colour count and round count, as for the in-core path; and of the exact
+finish of Algorithm 2 (WL_BATCHED_EXACT), whose result must be the coarsest
+stable colouring, numbered by first occurrence."""
+import ctypes
+import random
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_02603_amd as wl
+from oracle import bruteforce as bf
+from paper_2607_02603_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _host_graph(rp, col, wt=None, pinned=True):
+    n = len(rp) - 1
+    g = wl.Graph.from_numpy(n, np.asarray(rp, np.uint64), col, wt, device=None)
+    if not pinned:
+        return g
+    return wl.Graph(n, g.row_ptr.pin_memory(), g.col_idx.pin_memory(),
+                    None if g.weight is None else g.weight.pin_memory())
+
+
+def _ws_for_chunk(n, entries, weighted):
+    """Workspace whose chunks hold 'entries' entries (the size reported for
+    a graph of n nodes with that many entries)."""
+    s = wl.WlCsr()
+    s.n = n
+    s.nnz = entries
+    s.weight = 8 if weighted else None
+    out = ctypes.c_uint64(0)
+    assert wl.lib().wl_streamed_workspace_size(ctypes.byref(s), ctypes.byref(out)) == 0
+    return int(out.value)
+
+
+def _init_t(init):
+    if init is None:
+        return None
+    return torch.from_numpy(np.asarray(init, np.uint32).view(np.int32))
+
+
+def _check(rp, col, wt=None, init=None, seed=0, chunk=None, pinned=True, max_rounds=0):
+    g = _host_graph(rp, col, wt, pinned)
+    ws_bytes = None if chunk is None else _ws_for_chunk(g.n, chunk, wt is not None)
+    c, k, r = wl.wl_stable_coloring_streamed(g, _init_t(init), seed, max_rounds,
+                                             ws_bytes=ws_bytes, allow_max_rounds=True)
+    co, ko, ro, _, st = oracle.stable_coloring(rp, col, wt, init, seed, max_rounds)
+    got = c.numpy().view(np.uint32)
+    assert (k, r) == (ko, ro)
+    assert np.array_equal(got, co)
+    return got, k, r, st
+
+
+@pytest.mark.parametrize("name", ["er", "rmat", "grid", "chunglu"])
+def test_small_graphs_full_chunks(name):
+    g = {"er": lambda: inputs.er_graph(3000, 12000, seed=2),
+         "rmat": lambda: inputs.rmat(11, 8, seed=4),
+         "grid": lambda: inputs.grid_graph(17, 23),
+         "chunglu": lambda: inputs.chung_lu(5000, 40000, seed=3)}[name]()
+    print(f"streamed {name} n={g.n} nnz={g.nnz}", flush=True)
+    got, k, r, st = _check(g.row_ptr, g.col, seed=7)
+    assert st == 0
+
+
+@pytest.mark.parametrize("chunk", [4096, 5000, 20000])
+def test_small_chunks_cut_rows(chunk):
+    # hubs longer than a segment (4096 entries) and than a chunk: their
+    # partial sums are folded, some across chunk boundaries
+    rng = random.Random(chunk)
+    n = 3000
+    edges = [(0, 1 + rng.randrange(n - 1)) for _ in range(15000)]
+    edges += [(1, 2 + rng.randrange(n - 2)) for _ in range(9000)]
+    edges += [(rng.randrange(n), rng.randrange(n)) for _ in range(12000)]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    print(f"cut rows chunk={chunk} nnz={col.size}", flush=True)
+    _check(rp, col, seed=chunk, chunk=chunk)
+    wt = np.array([rng.randint(1, 7) for _ in range(col.size)], np.uint32)
+    init = np.array([rng.choice([2, 5, 11]) for _ in range(n)], np.uint32)
+    _check(rp, col, wt, init, seed=3, chunk=chunk)
+
+
+def test_rmat_many_chunks_pageable():
+    g = inputs.rmat(14, 16, seed=9)
+    print(f"rmat14 nnz={g.nnz}", flush=True)
+    _check(g.row_ptr, g.col, seed=1, chunk=50000, pinned=False)
+    _check(g.row_ptr, g.col, seed=1, chunk=50000, pinned=True)
+
+
+def test_equals_in_core_call():
+    g0 = inputs.rmat(12, 8, seed=2)
+    gd = wl.Graph.from_numpy(g0.n, g0.row_ptr, g0.col, None, device="cuda")
+    ci, ki, ri = wl.wl_stable_coloring(gd, None, 5)
+    got, k, r, _ = _check(g0.row_ptr, g0.col, seed=5, chunk=30000)
+    assert (k, r) == (ki, ri)
+    assert np.array_equal(got, ci.cpu().numpy().view(np.uint32))
+
+
+@pytest.mark.parametrize("trial", range(4))
+def test_random_weighted_directed(trial):
+    rng = random.Random(90 + trial)
+    n = rng.randint(5, 400)
+    edges = [(rng.randrange(n), rng.randrange(n)) for _ in range(rng.randint(n, 8 * n))]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    wt = np.array([rng.randint(1, 9) for _ in range(col.size)], np.uint32)
+    init = np.array([rng.choice([1, 4]) for _ in range(n)], np.uint32) if trial % 2 else None
+    _check(rp, col, wt, init, seed=trial, chunk=4096)
+
+
+def test_edge_cases():
+    for n in (1, 2, 7):
+        rp = np.zeros(n + 1, np.uint64)
+        _check(rp, np.zeros(0, np.uint32))
+    # a round cap that stops early
+    g = inputs.grid_graph(9, 9)
+    got, k, r, st = _check(g.row_ptr, g.col, max_rounds=2)
+    assert st != 0 and r == 2
+    # n = 0
+    g = _host_graph(np.zeros(1, np.uint64), np.zeros(0, np.uint32))
+    c, k, r = wl.wl_stable_coloring_streamed(g, None, 0)
+    assert (k, r) == (0, 0)
+
+
+def test_budget_error():
+    g0 = inputs.rmat(9, 4, seed=1)
+    g = _host_graph(g0.row_ptr, g0.col)
+    small = _ws_for_chunk(g.n, 100, False)
+    with pytest.raises(wl.WlError) as e:
+        wl.wl_stable_coloring_streamed(g, None, 0, ws_bytes=small)
+    assert e.value.code == wl.WL_EBUDGET
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 2 with the exact finish
+# ---------------------------------------------------------------------------
+
+def _coarsest(rp, col, wt=None, init=None):
+    return oracle.first_occurrence(oracle.stable_coloring(rp, col, wt, init, 0)[0])[0]
+
+
+def _batched_exact(rp, col, wt=None, init=None, mb=8, options=wl.WL_BATCHED_EXACT,
+                   pinned=True):
+    g = _host_graph(rp, col, wt, pinned)
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, _init_t(init), 0, mb,
+                                                             options=options)
+    got = c.numpy().view(np.uint32)
+    ref = _coarsest(rp, col, wt, init)
+    assert coarsest
+    assert np.array_equal(got, ref)
+    assert k == int(ref.max()) + 1
+    return outer
+
+
+def test_exact_finish_at_fixed_point():
+    # the grid stops at a fixed point with several batches (case ii); the
+    # exact finish recovers the coarsest colouring
+    g = inputs.grid_graph(6, 7)
+    _, _, _, outer, coarsest = wl.wl_stable_coloring_batched(_host_graph(g.row_ptr, g.col),
+                                                             None, 0, 12)
+    assert not coarsest
+    _batched_exact(g.row_ptr, g.col, mb=12)
+
+
+@pytest.mark.parametrize("options", [wl.WL_BATCHED_EXACT,
+                                     wl.WL_BATCHED_EXACT | wl.WL_BATCHED_EARLY_STOP])
+@pytest.mark.parametrize("mb", [3, 40, 300])
+def test_exact_rmat_caps(options, mb):
+    g = inputs.rmat(10, 6, seed=6)
+    _batched_exact(g.row_ptr, g.col, mb=mb, options=options)
+
+
+@pytest.mark.parametrize("trial", range(4))
+def test_exact_weighted_labels(trial):
+    rng = random.Random(70 + trial)
+    n = rng.randint(20, 300)
+    edges = [(rng.randrange(n), rng.randrange(n)) for _ in range(rng.randint(n, 6 * n))]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    wt = np.array([rng.randint(1, 5) for _ in range(col.size)], np.uint32)
+    init = np.array([rng.choice([3, 9]) for _ in range(n)], np.uint32) if trial % 2 else None
+    _batched_exact(rp, col, wt, init, mb=17, pinned=bool(trial % 2),
+                   options=wl.WL_BATCHED_EXACT | (wl.WL_BATCHED_EARLY_STOP * (trial // 2)))
+
+
+def test_early_stop_without_exact():
+    # the early stop alone still gives a stable colouring that refines the
+    # coarsest one
+    g = inputs.rmat(10, 6, seed=6)
+    hg = _host_graph(g.row_ptr, g.col)
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(
+        hg, None, 0, 40, options=wl.WL_BATCHED_EARLY_STOP)
+    got = c.numpy().view(np.uint32)
+    assert oracle.is_stable(g.row_ptr, g.col, None, got)
+    ref = _coarsest(g.row_ptr, g.col)
+    for b in np.unique(got):
+        assert len(np.unique(ref[got == b])) == 1
+
+
+def test_unknown_option_rejected():
+    g = inputs.rmat(8, 4, seed=1)
+    with pytest.raises(wl.WlError) as e:
+        wl.wl_stable_coloring_batched(_host_graph(g.row_ptr, g.col), None, 0, 40, options=8)
+    assert e.value.code == wl.WL_EINVAL
