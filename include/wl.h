@@ -246,6 +246,9 @@ const char *wl_last_error(void);
  * The image of a round is one of three kinds: 'gather' (a row reads its
  * neighbours' values), 'pb' (propagation blocking on a symmetric graph: its
  * passes count as one launch) or 'uniform' (rounds with a single colour).
+ * With WL_GRAPH=1 in the environment, the rounds that run without a
+ * read-back are replayed from a HIP graph: their image launches are counted
+ * but not timed, so 'ms' then covers the host-driven rounds only.
  * wl_stats_get() returns the figures of the last in-core call on this thread.
  * Both return WL_OK, or WL_EINVAL for a NULL pointer / unknown flag. */
 #define WL_STATS_TIME 1

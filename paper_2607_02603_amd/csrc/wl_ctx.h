@@ -62,6 +62,7 @@ struct DevState {
   uint32_t deg_nd;      // distinct row lengths (one-colour round)
   uint32_t n_mid;       // live rows queued for one wave each (this round)
   uint32_t n_hlive;     // live heavy rows (this round)
+  uint32_t prep_round;  // the round whose gather tables the round end prepares
   uint64_t seed;
   unsigned long long work[3][2];    // diagnostics: rows, entries per image kind
   unsigned long long act_entries;   // entries of the rows whose image is needed
@@ -158,6 +159,9 @@ struct Ctx {
   uint32_t* hq;        // positions with heavy rows (this round)
   uint8_t* lsplit;     // per live class: 1 if it split in this round
   uint8_t* bsame;      // per big segment of a radix pass: 1 if all its keys are equal
+  uint8_t* nz0f;       // per sub-class: a member with key 0 has a non-empty row
+                       // (set by k_live_scan_final, consumed and cleared by
+                       // k_live_subs_splits; NULL outside in-core sessions)
 };
 
 }  // namespace wl

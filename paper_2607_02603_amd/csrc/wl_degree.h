@@ -212,6 +212,7 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
       st->k_new = k_new;
       st->nosplit = k_new == st->k ? 1u : 0u;
       st->split_any = 1u - st->nosplit;
+      st->prep_round = st->round + 1;
     }
   }
   __syncthreads();

@@ -75,17 +75,19 @@ uint64_t align_up(uint64_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
   uint64_t n, nnz;
   uint32_t max_small, max_big, max_chunks, max_heavy;
+  bool in_core;
   uint64_t off_st, off_x, off_z, off_keys, off_keys_tmp, off_perm, off_perm_tmp,
       off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
       off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2],
-      off_rs[2], off_rl[2], off_hq, off_bsame;
+      off_rs[2], off_rl[2], off_hq, off_bsame, off_nz0f;
   uint64_t total;
 };
 
 Layout make_layout(uint64_t n, uint64_t nnz, bool in_core = true) {
   Layout L{};
   const uint64_t nc = in_core ? n : 0;
+  L.in_core = in_core;
   L.n = n;
   L.nnz = nnz;
   L.max_small = (uint32_t)(n / 2 + 1);
@@ -136,6 +138,7 @@ Layout make_layout(uint64_t n, uint64_t nnz, bool in_core = true) {
   L.off_rl[1] = take(4 * nc);
   L.off_hq = take(in_core ? 4ull * L.max_heavy : 0);
   L.off_bsame = take(L.max_big + 1);
+  L.off_nz0f = take(in_core ? n + 1 : 0);
   L.total = o;
   return L;
 }
@@ -196,6 +199,25 @@ PbLayout make_pb_layout(uint64_t n, uint64_t nnz) {
   P.total = o;
   P.ok = true;
   return P;
+}
+
+// The Ctx of a live round whose current lists are the other buffer set: the
+// '2' arrays become current and the current ones receive the next round's
+// lists (so no copy is needed between rounds).  lperm is the sort's payload,
+// so perm and perm_tmp swap with it; the per-round wave queue lives in the
+// buffer that is not current.
+Ctx swapped_live(const Ctx& c) {
+  Ctx x = c;
+  std::swap(x.perm, x.perm_tmp);
+  std::swap(x.lperm, x.lperm2);
+  std::swap(x.qcls, x.qcls2);
+  x.midq = x.qcls2;
+  std::swap(x.lcold, x.lcold2);
+  std::swap(x.loff, x.loff2);
+  std::swap(x.llen, x.llen2);
+  std::swap(x.rs, x.rs2);
+  std::swap(x.rl, x.rl2);
+  return x;
 }
 
 bool wants_pb(const wl_csr* g) {
@@ -276,6 +298,7 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.midq = c.qcls2;  // consumed by the SpMV before k_live_emit writes qcls2
   c.hq = (uint32_t*)(ws + L.off_hq);
   c.bsame = ws + L.off_bsame;
+  c.nz0f = L.in_core ? ws + L.off_nz0f : nullptr;
   c.lsplit = c.c8;    // written after the SpMV has read the compact colours
   c.weighted = g->weight != nullptr;
   {
@@ -383,6 +406,7 @@ __global__ void __launch_bounds__(kBlock) k_iota_zero(Ctx ctx) {
     ctx.ids[i] = 0;
     ctx.c[i] = 0;
     ctx.act[i] = ctx.n >= 2 ? 1 : 0;
+    if (ctx.nz0f) ctx.nz0f[i] = 0;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctx.cstart[0] = 0;
@@ -456,6 +480,13 @@ struct Session {
   // can be set for testing (WL_HOST_ROUNDS, WL_ASYNC_PASSES).
   uint32_t host_rounds_first = kHostRounds;
   int async_passes = kAsyncPassesDefault;
+  int passes_seen = 0;      // most radix passes a host-driven sort needed
+  // Live rounds alternate between two buffer sets: round r reads the set
+  // (r - live_r0) & 1 and writes the other; ctx0 has set 0 current.
+  Ctx ctx0{};
+  uint32_t live_r0 = 0;
+  bool next_async = false;  // the round after this host-driven one is device-driven
+  bool hist_clean = false;  // radix histograms cleared (first pass of the call)
   hipStream_t s;
   bool rp64;
   bool weighted;
@@ -494,10 +525,24 @@ struct Session {
   std::vector<TimedSpmv> timed;
   wl_stats stats{};
 
+  // WL_GRAPH=1: device-driven rounds replayed from a HIP graph of two rounds
+  // (one per buffer-set parity of its first round), captured on a stream of
+  // the session's own.  Off by default: on the 1024 x 1024 grid (512 rounds)
+  // replay took 277 ms against 132 ms for the same kernels launched on the
+  // stream.
+  bool use_graph = false;
+  bool capturing = false;
+  hipStream_t cap_stream = nullptr;
+  hipGraphExec_t gexec[2] = {nullptr, nullptr};
+  int gexec_ap[2] = {-1, -1};  // radix passes per round when captured
+
   ~Session() {
     for (hipEvent_t& e : call_ev)
       if (e) (void)hipEventDestroy(e);
     for (hipEvent_t& e : ev_pool) (void)hipEventDestroy(e);
+    for (hipGraphExec_t& g : gexec)
+      if (g) (void)hipGraphExecDestroy(g);
+    if (cap_stream) (void)hipStreamDestroy(cap_stream);
   }
 
   int stats_begin() {
@@ -523,6 +568,10 @@ struct Session {
   // launches are counted when the round is known to have run.
   template <typename F>
   void timed_spmv(uint32_t round, bool always, int kind, F&& launch) {
+    if (capturing) {  // replayed launches are not timed
+      launch();
+      return;
+    }
     TimedSpmv t{nullptr, nullptr, round, always, kind};
     if (sflags & WL_STATS_TIME) {
       t.a = next_event();
@@ -818,10 +867,12 @@ struct Session {
 
   // Gathering image of the live rows; every count comes from the device.
   template <bool W>
+  // always: a host-driven round, which prepares its gather tables itself; a
+  // device-driven round finds them prepared by the previous round's end.
   void live_gather(uint32_t round, bool always) {
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
     const uint32_t gl = live_grid();
-    hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, ctx, -1);
+    if (always) hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, ctx, -1);
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_live_count, dim3(gl), dim3(kBlock), 0, s, ctx, 1);
     const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
@@ -881,15 +932,16 @@ struct Session {
   // every pass), then the small sorts and, for the full relabel, the rank
   // scan.
   int finish_sort(int pass0, bool full) {
-    for (int pass = pass0; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
-      radix_pass(pass, grid_for((uint64_t)host.n_big[pass & 1] * kRadix),
-                 std::min<uint32_t>(host.n_big[pass & 1], 4096));
+    int pass = pass0;
+    for (; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
+      radix_pass(pass, std::min<uint32_t>(host.n_big[pass & 1], 4096));
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
     }
+    passes_seen = std::max(passes_seen, pass);
     if (host.n_tiny)
       hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(host.n_tiny, kBlock / kWave, 8192)),
-                         dim3(kBlock), 0, s, ctx);
+                         dim3(kBlock), 0, s, ctx, -1);
     if (host.n_small)
       hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
                          dim3(kBlock), 0, s, ctx);
@@ -898,11 +950,17 @@ struct Session {
     return WL_OK;
   }
 
-  void radix_pass(int pass, uint32_t clear_grid, uint32_t scan_grid) {
+  void radix_pass(int pass, uint32_t scan_grid) {
     hipLaunchKernelGGL(k_big_tiles, dim3(1), dim3(kBlock), 0, s, ctx, pass);
     if (pass == 0 && !ctx.keys_mat)
       hipLaunchKernelGGL(k_big_gather, dim3(2048), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_big_clear, dim3(clear_grid), dim3(kBlock), 0, s, ctx, pass);
+    // the first pass of the call clears the histograms over their whole
+    // capacity; k_big_scan keeps them cleared after that
+    if (!hist_clean) {
+      hipLaunchKernelGGL(k_big_clear, dim3(grid_for((uint64_t)L.max_big * kRadix, kBlock, 4096)),
+                         dim3(kBlock), 0, s, ctx);
+      hist_clean = true;
+    }
     hipLaunchKernelGGL(k_big_hist, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
     hipLaunchKernelGGL(k_big_scan, dim3(scan_grid), dim3(kBlock), 0, s, ctx, pass);
     hipLaunchKernelGGL(k_big_scatter, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
@@ -972,20 +1030,20 @@ struct Session {
 
   // After the sort: sub-classes, new colours of every node, next live
   // classes, end of the round.
-  void live_tail() {
+  // prep: the round end also prepares the next round's gather tables (the
+  // next round is device-driven).
+  void live_tail(bool prep) {
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
     const uint32_t gl = live_grid(), ns = live_scan_blocks();
     const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
     DevState* st = ctx.st;
     hipLaunchKernelGGL(k_live_scan_part, dim3(ns), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, ns);
-    hipLaunchKernelGGL(k_live_scan_final, dim3(ns), dim3(kBlock), 0, s, ctx);
     if (rp64)
-      hipLaunchKernelGGL(k_live_nz0<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_live_scan_final<uint64_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
     else
-      hipLaunchKernelGGL(k_live_nz0<uint32_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_subs, dim3(gl), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_splits, dim3(gc), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_live_scan_final<uint32_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_subs_splits, dim3(std::max(gl, gc)), dim3(kBlock), 0, s, ctx);
     xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
     hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx);
     hipLaunchKernelGGL(k_shift_clear, dim3(gn), dim3(kBlock), 0, s, ctx);
@@ -996,8 +1054,8 @@ struct Session {
       hipLaunchKernelGGL(k_live_emit<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
     else
       hipLaunchKernelGGL(k_live_emit<uint32_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_commit, dim3(gl), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_round_end, dim3(prep ? gn : 1), dim3(kBlock), 0, s, ctx,
+                       prep ? 1 : 0);
   }
 
   // The one-colour round of an unweighted graph without a sort
@@ -1032,7 +1090,8 @@ struct Session {
     if (host.deg_nd > kDegRanks) return WL_OK;
     hipLaunchKernelGGL(k_deg_place<RP64>, dim3(grid_for(L.n, kBlock, 2048)), dim3(kBlock), 0, s,
                        ctx, d);
-    hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
+    hipLaunchKernelGGL(k_live_round_end, dim3(next_async ? grid_for(L.n, kBlock, 4096) : 1),
+                       dim3(kBlock), 0, s, ctx, next_async ? 1 : 0);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     *handled = true;
@@ -1052,26 +1111,46 @@ struct Session {
     return host.k == 1 && !weighted && !ctx.batch && deg_mode && degree_round_fits();
   }
 
-  int round_live() {
+  void use_round_ctx(uint32_t round) {
+    ctx = ((round - live_r0) & 1) ? swapped_live(ctx0) : ctx0;
+  }
+
+  // Builds the live classes into buffer set 0 for the coming round, whose
+  // counters and gather tables it also sets.
+  int build_live_now() {
+    ctx = ctx0;
+    if (int r = build_live()) return r;
+    live_built = true;
+    live_r0 = host.round;
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
+    hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
+                       ctx, -1);
+    HIP_LAUNCH_CHECK();
+    return WL_OK;
+  }
+
+  int round_live() {
     if (degree_round_applies()) {
+      ctx = ctx0;
+      hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
       bool handled = false;
       if (int r = rp64 ? degree_round<true>(&handled) : degree_round<false>(&handled)) return r;
       if (handled) {
         live_built = true;
+        live_r0 = host.round;
         return WL_OK;
       }
     }
-    if (!live_built) {
-      if (int r = build_live()) return r;
-      live_built = true;
-    }
+    if (!live_built)
+      if (int r = build_live_now()) return r;
+    use_round_ctx(host.round);
+    hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
     if (int r = spmv_live()) return r;
     live_segments();
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (int r = finish_sort(0, false)) return r;
-    live_tail();
+    live_tail(next_async);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (host.err & kErrNotSymmetric)
@@ -1079,31 +1158,94 @@ struct Session {
     return WL_OK;
   }
 
+  // Radix passes launched per device-driven round: as many as the rounds so
+  // far needed (at least one), at most async_passes.
+  int async_pass_count() const {
+    return std::min(async_passes, std::max(1, passes_seen));
+  }
+
   // The same launched without reading anything back: grids are fixed for the
-  // call and counts come from the device state; at most async_passes radix
-  // passes run, and a round that needs more halts the device before its
-  // small sorts (finish_halted completes it).
+  // call and counts come from the device state; the per-round counters and
+  // gather tables were set by the previous round's end.  A round that needs
+  // more radix passes than it launches halts the device before its small
+  // sorts (finish_halted completes it).
   void round_live_async(uint32_t round) {
-    hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
+    use_round_ctx(round);
     spmv_live_async(round);
     live_segments();
-    for (int pass = 0; pass < async_passes; ++pass) radix_pass(pass, 1024, 1024);
-    hipLaunchKernelGGL(k_passes_check, dim3(1), dim3(1), 0, s, ctx, async_passes);
-    hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 2048)),
+    const int ap = async_pass_count();
+    for (int pass = 0; pass < ap; ++pass) radix_pass(pass, 1024);
+    // the small sorts' grids: enough blocks to fill the device, the segments
+    // taken in grid-stride loops
+    hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 1024)),
+                       dim3(kBlock), 0, s, ctx, ap);
+    hipLaunchKernelGGL(k_small_sort, dim3(grid_for(L.n / (kTinyMax + 1), 1, 1024)),
                        dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_small_sort, dim3(grid_for(L.n / (kTinyMax + 1), 1, 2048)),
-                       dim3(kBlock), 0, s, ctx);
-    live_tail();
+    live_tail(true);
+  }
+
+  // The graph of rounds r, r + 1 for a first round of parity p = (r -
+  // live_r0) & 1, (re)captured when the radix pass count changed.  The
+  // grids are those of the capture; the live set only shrinks, so they stay
+  // large enough.
+  int ensure_graph(int p, uint32_t r) {
+    const int ap = async_pass_count();
+    if (gexec[p] && gexec_ap[p] == ap) return WL_OK;
+    if (gexec[p]) {
+      HIP_TRY(hipGraphExecDestroy(gexec[p]));
+      gexec[p] = nullptr;
+    }
+    if (!cap_stream) HIP_TRY(hipStreamCreateWithFlags(&cap_stream, hipStreamNonBlocking));
+    const hipStream_t s0 = s;
+    s = cap_stream;
+    capturing = true;
+    hipGraph_t g = nullptr;
+    hipError_t e = hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal);
+    if (e == hipSuccess) {
+      round_live_async(r);
+      round_live_async(r + 1);
+      e = hipStreamEndCapture(s, &g);
+    }
+    s = s0;
+    capturing = false;
+    if (e != hipSuccess)
+      return fail(WL_EHIP, "graph capture of the rounds failed: %s", hipGetErrorString(e));
+    e = hipGraphInstantiate(&gexec[p], g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) {
+      gexec[p] = nullptr;
+      return fail(WL_EHIP, "graph instantiation failed: %s", hipGetErrorString(e));
+    }
+    gexec_ap[p] = ap;
+    return WL_OK;
+  }
+
+  // Queues rounds base .. base + count - 1 (count even) without a read-back.
+  int launch_async_rounds(uint32_t base, uint32_t count) {
+    if (!use_graph) {
+      for (uint32_t i = 0; i < count; ++i) round_live_async(base + i);
+      HIP_LAUNCH_CHECK();
+      return WL_OK;
+    }
+    const int p = (int)((base - live_r0) & 1);
+    if (int r = ensure_graph(p, base)) return r;
+    for (uint32_t i = 0; i < count; i += 2) HIP_TRY(hipGraphLaunch(gexec[p], s));
+    // each replayed round has one gathering image launch: counted when the
+    // round ran, without a time
+    for (uint32_t i = 0; i < count; ++i)
+      timed.push_back(TimedSpmv{nullptr, nullptr, base + i, false, kImgGather});
+    return WL_OK;
   }
 
   // The device halted in a round after async_passes radix passes: clear the
   // halt and finish that round with host-driven passes.
   int finish_halted() {
+    use_round_ctx(host.round);
     hipLaunchKernelGGL(k_resume, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
-    if (int r = finish_sort(async_passes, false)) return r;
-    live_tail();
+    if (int r = finish_sort(async_pass_count(), false)) return r;
+    live_tail(true);
     HIP_LAUNCH_CHECK();
     return pull();
   }
@@ -1120,13 +1262,12 @@ struct Session {
       if (int r = relabel(0)) return r;
     }
     if (int r = build_schedule(true)) return r;
+    ctx.keys_mat = 1;
+    ctx0 = ctx;
     // The live classes come from the grouping above, unless the first round
     // is the one-colour degree round, which builds them itself.
-    if (!degree_round_applies()) {
-      if (int r = build_live()) return r;
-      live_built = true;
-    }
-    ctx.keys_mat = 1;
+    if (!degree_round_applies())
+      if (int r = build_live_now()) return r;
     live_mode = true;
     plan_live_grid();
     // The first rounds are driven from the host (each reads its counts
@@ -1136,17 +1277,14 @@ struct Session {
     uint32_t host_rounds = 0, ahead = 8;
     while (!host.done) {
       if (host_rounds < host_rounds_first) {
+        next_async = host_rounds + 1 >= host_rounds_first;
         if (int r = round_live()) return r;
         ++host_rounds;
         continue;
       }
-      if (!live_built) {
-        if (int r = build_live()) return r;
-        live_built = true;
-      }
-      const uint32_t base = host.round;
-      for (uint32_t i = 0; i < ahead; ++i) round_live_async(base + i);
-      HIP_LAUNCH_CHECK();
+      if (!live_built)
+        if (int r = build_live_now()) return r;
+      if (int r = launch_async_rounds(host.round, ahead)) return r;
       if (int r = pull()) return r;
       if (host.done == kHalted)
         if (int r = finish_halted()) return r;
@@ -1191,6 +1329,7 @@ int open_session(Session& S, const wl_csr* g, uint32_t* colors, void* ws,
   }
   S.sym_flag = (g->flags & WL_CSR_SYMMETRIC) != 0;
   S.deg_mode = env_int("WL_DEGREE_ROUND", 0, 1, 1) != 0;
+  S.use_graph = env_int("WL_GRAPH", 0, 1, 0) != 0;
   if (wants_pb(g) && S.pb_mode != 0) {
     S.P = make_pb_layout(g->n, g->nnz);
     // pass 1 reads the column indices 16 bytes at a time

@@ -38,6 +38,7 @@
 // queued without reading anything back.
 #pragma once
 #include "wl_relabel.h"
+#include "wl_spmv.h"
 
 namespace wl {
 
@@ -243,7 +244,8 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_part(Ctx ctx) {
 }
 
 // One block: block offsets; nsub = sub-classes of the live classes,
-// k_new = k + nsub - n_live; nosplit when no class split.
+// k_new = k + nsub - n_live; nosplit when no class split; the round whose
+// gather tables the round end prepares.
 __global__ void __launch_bounds__(kBlock) k_live_scan_top(Ctx ctx, uint32_t nblk) {
   DevState* st = ctx.st;
   if (st->done) return;
@@ -263,11 +265,14 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_top(Ctx ctx, uint32_t nblk
     st->nosplit = carry == st->n_live ? 1u : 0u;
     st->split_any = 1u - st->nosplit;
     st->shift_big = 0;
+    st->prep_round = st->round + 1;
   }
 }
 
 // ids[q] = sub-class of q; per sub-class g: first position, end, and whether
-// its key is non-zero (then it holds a non-empty row).
+// it holds a non-empty row: its key is non-zero (gnz), or a member with key
+// 0 has one (its image happens to be 0; nz0f).
+template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
   const DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
@@ -288,47 +293,36 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
         ctx.gstart[g] = q;
         ctx.gnz[g] = ctx.keys[q] != 0 ? 1 : 0;
       }
+      if (ctx.keys[q] == 0 && row_nonempty<RP>(ctx, ctx.lperm[q])) ctx.nz0f[g] = 1;
       if (q + 1 == nl || live_flag(ctx, q + 1)) ctx.gend[g] = q + 1;
     }
     run += tot;
   }
 }
 
-// Sub-classes with key 0 hold a non-empty row if one of their members has
-// one (whose image happens to be 0).
-template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_live_nz0(Ctx ctx) {
-  const DevState* st = ctx.st;
-  if (st->done || st->nosplit) return;
-  const uint32_t nl = st->nl;
-  for (uint32_t q = blockIdx.x * kBlock + threadIdx.x; q < nl; q += gridDim.x * kBlock)
-    if (ctx.keys[q] == 0 && row_nonempty<RP>(ctx, ctx.lperm[q])) ctx.gnz[ctx.ids[q]] = 1;
-}
-
-__device__ __forceinline__ bool sub_live(const Ctx& ctx, uint32_t g) {
-  return ctx.gend[g] - ctx.gstart[g] >= 2 && ctx.gnz[g];
-}
-
-// gl[g] = 1, go[g] = size for the live sub-classes (scanned next).
-__global__ void __launch_bounds__(kBlock) k_live_subs(Ctx ctx) {
-  const DevState* st = ctx.st;
-  if (st->done || st->nosplit) return;
-  const uint32_t ns = st->nsub;
-  for (uint32_t g = blockIdx.x * kBlock + threadIdx.x; g < ns; g += gridDim.x * kBlock) {
-    const bool live = sub_live(ctx, g);
-    ctx.gl[g] = live ? 1u : 0u;
-    ctx.go[g] = live ? ctx.gend[g] - ctx.gstart[g] : 0u;
-  }
-}
-
-// Classes that split: (old colour, extra sub-classes), in any order.
-__global__ void __launch_bounds__(kBlock) k_live_splits(Ctx ctx) {
+// The live sub-classes (gl[g] = 1, go[g] = size; scanned next), with the
+// key-0 flags folded into gnz; and the classes that split: (old colour,
+// extra sub-classes), in any order.
+__global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
+  const uint32_t stride = gridDim.x * kBlock;
+  const uint32_t ns = st->nsub;
+  for (uint32_t g = blockIdx.x * kBlock + threadIdx.x; g < ns; g += stride) {
+    bool nz = ctx.gnz[g] != 0;
+    if (ctx.nz0f[g]) {
+      ctx.nz0f[g] = 0;
+      ctx.gnz[g] = 1;
+      nz = true;
+    }
+    const uint32_t len = ctx.gend[g] - ctx.gstart[g];
+    const bool live = len >= 2 && nz;
+    ctx.gl[g] = live ? 1u : 0u;
+    ctx.go[g] = live ? len : 0u;
+  }
   __shared__ uint32_t sh[kBlock / kWave];
   __shared__ uint32_t base_sh;
   const uint32_t nlive = st->n_live;
-  const uint32_t stride = gridDim.x * kBlock;
   for (uint32_t j0 = blockIdx.x * kBlock; j0 < nlive; j0 += stride) {
     const uint32_t j = j0 + threadIdx.x;
     uint32_t extra = 0;
@@ -556,14 +550,22 @@ __global__ void k_live_adopt(Ctx ctx) {
   st->nl = st->nl2;
 }
 
-// End of a live round: colour count, round counter, termination, and the new
-// live counts.
-__global__ void k_live_round_end(Ctx ctx) {
+// End of a live round.  Every block prepares the next round's gather tables
+// (prep = 0 when the next round prepares its own; the colours are final
+// here, the next colour count is k_new and the round is prep_round, fields
+// this kernel does not change); block 0 sets the colour count, round
+// counter, termination and new live counts and clears the per-round
+// counters.  No argument depends on the round, so the launch can be
+// replayed.
+__global__ void __launch_bounds__(kBlock) k_live_round_end(Ctx ctx, int prep) {
   DevState* st = ctx.st;
   if (st->done) return;
   const uint32_t kn = st->k_new;
+  if (prep && !st->nosplit)
+    gather_prep_body(ctx, gather_mode(kn), kn, round_key(st->seed, st->prep_round));
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
   st->round += 1;
-  if (kn == st->k) {
+  if (st->nosplit) {
     st->done = 1;
   } else {
     if (st->round >= st->max_rounds) st->done = 2;
@@ -571,6 +573,15 @@ __global__ void k_live_round_end(Ctx ctx) {
     st->nl = st->nl2;
   }
   st->k = kn;
+  st->n_small = 0;
+  st->n_tiny = 0;
+  st->n_big[0] = 0;
+  st->n_big[1] = 0;
+  st->n_tiles = 0;
+  st->act_entries = 0;
+  st->n_split = 0;
+  st->n_mid = 0;
+  st->n_hlive = 0;
 }
 
 }  // namespace wl

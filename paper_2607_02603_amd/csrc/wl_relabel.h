@@ -21,6 +21,10 @@
 
 namespace wl {
 
+// DevState::done of a device-driven round that stopped for the host to finish
+// its radix passes (k_resume clears it).
+constexpr uint32_t kHalted = 3;
+
 __device__ __forceinline__ uint32_t digit_of(uint64_t key, int pass) {
   const int hi = 61 - kRadixBits * pass;
   const int lo = hi > kRadixBits ? hi - kRadixBits : 0;
@@ -159,20 +163,22 @@ __global__ void __launch_bounds__(kBlock) k_big_gather(Ctx ctx) {
   }
 }
 
-__global__ void __launch_bounds__(kBlock) k_big_clear(Ctx ctx, int pass) {
-  DevState* st = ctx.st;
-  if (st->done) return;
-  const uint32_t nb = st->n_big[pass & 1];
-  const uint32_t tot = nb * kRadix;
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < tot;
-       i += gridDim.x * kBlock) {
+// Clears the radix histograms over their whole capacity (max_big segments),
+// whatever the state: once per call, before its first radix pass.  From
+// then on every k_big_scan clears what it consumed, so each pass finds them
+// cleared however many segments it has.
+__global__ void __launch_bounds__(kBlock) k_big_clear(Ctx ctx) {
+  const uint64_t tot = (uint64_t)ctx.max_big * kRadix;
+  for (uint64_t i = blockIdx.x * (uint64_t)kBlock + threadIdx.x; i < tot;
+       i += (uint64_t)gridDim.x * kBlock) {
     ctx.bhist[i] = 0;
     ctx.bmin[i] = ~0ull;
     ctx.bmax[i] = 0;
   }
 }
 
-// Histogram of the pass digit per (segment, bucket), with min/max key.
+// Histogram of the pass digit per (segment, bucket), with min/max key, into
+// arrays that k_big_clear and k_big_scan keep cleared.
 __global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
   DevState* st = ctx.st;
   if (st->done) return;
@@ -220,6 +226,11 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
     const uint2 s = L[sgi];
     const uint32_t g = sgi * kRadix + threadIdx.x;
     const uint32_t h = ctx.bhist[g];
+    const unsigned long long bmn = ctx.bmin[g], bmx = ctx.bmax[g];
+    // the histogram is consumed here: leave it cleared for the next pass
+    ctx.bhist[g] = 0;
+    ctx.bmin[g] = ~0ull;
+    ctx.bmax[g] = 0;
     uint32_t tot;
     const uint32_t off = block_excl_scan(h, sh, &tot);
     ctx.bcur[g] = off;
@@ -228,12 +239,12 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
     // them, or bucket 0 when none does).
     const bool all_here = h == s.y;
     const bool none_full = __syncthreads_or(all_here) == 0;
-    if (all_here) ctx.bsame[sgi] = ctx.bmin[g] == ctx.bmax[g] ? 1 : 0;
+    if (all_here) ctx.bsame[sgi] = bmn == bmx ? 1 : 0;
     else if (none_full && threadIdx.x == 0) ctx.bsame[sgi] = 0;
     if (h) {
       const uint32_t pos = s.x + off;
       ctx.flags[pos] = 1;
-      if (h >= 2 && ctx.bmin[g] != ctx.bmax[g]) {
+      if (h >= 2 && bmn != bmx) {
         if (h <= kTinyMax) {
           uint32_t idx = atomicAdd(&st->n_tiny, 1u);
           ctx.tiny_list[idx] = make_uint2(pos, h | kMatBit);
@@ -371,9 +382,16 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
 // One wave per tiny segment (<= 64 nodes): bitonic sort of (z, node) across
 // the lanes with shuffles, flags where z changes.  Skipped when all images of
 // the segment are equal.
-__global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx) {
+// check_passes >= 0: first halt the device (done = kHalted) if big segments
+// are left after that many radix passes; the blocks that still run sort
+// their segments, which the host-driven completion sorts again (a sort of
+// sorted keys changes nothing).
+__global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes) {
   DevState* st = ctx.st;
   if (st->done) return;
+  if (check_passes >= 0 && blockIdx.x == 0 && threadIdx.x == 0 &&
+      st->n_big[check_passes & 1] > 0)
+    st->done = kHalted;
   const uint32_t nt = st->n_tiny;
   const uint32_t lane = lane_id();
   const uint32_t nwaves = gridDim.x * (kBlock / kWave);
@@ -492,15 +510,7 @@ __global__ void __launch_bounds__(kBlock) k_scatter_colors(Ctx ctx) {
   }
 }
 
-// After the radix passes launched without a read-back: if big segments are
-// left, halt (done = 3) before the small sorts; the host finishes the round.
-constexpr uint32_t kHalted = 3;
-__global__ void k_passes_check(Ctx ctx, int passes) {
-  DevState* st = ctx.st;
-  if (st->done) return;
-  if (st->n_big[passes & 1] > 0) st->done = kHalted;
-}
-
+// Clears the halt of a device-driven round before the host finishes it.
 __global__ void k_resume(Ctx ctx) {
   if (ctx.st->done == kHalted) ctx.st->done = 0;
 }

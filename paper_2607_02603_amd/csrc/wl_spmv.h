@@ -499,11 +499,8 @@ __global__ void __launch_bounds__(kBlock) k_spmv_uniform(Ctx ctx) {
 // table of the k colour values (k <= 65535); with more colours the SpMV
 // computes each value from the neighbour's colour.
 // mode < 0: chosen from the colour count on the device.
-__global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
-  if (ctx.st->done) return;
-  const uint32_t k = ctx.st->k;
-  if (mode < 0) mode = gather_mode(k);
-  const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
+__device__ __forceinline__ void gather_prep_body(const Ctx& ctx, int mode, uint32_t k,
+                                                 uint64_t key) {
   const uint32_t tid = blockIdx.x * kBlock + threadIdx.x;
   const uint32_t stride = gridDim.x * kBlock;
   if (mode == kGatherC) return;
@@ -512,6 +509,13 @@ __global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
     for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c16[i] = (uint16_t)ctx.c[i];
   else
     for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c8[i] = (uint8_t)ctx.c[i];
+}
+
+__global__ void __launch_bounds__(kBlock) k_gather_prep(Ctx ctx, int mode) {
+  if (ctx.st->done) return;
+  const uint32_t k = ctx.st->k;
+  gather_prep_body(ctx, mode < 0 ? gather_mode(k) : mode, k,
+                   round_key(ctx.st->seed, ctx.st->round));
 }
 
 // Diagnostics: rows and entries the next image launch of 'kind' reads (all

@@ -4,8 +4,9 @@ give exactly the oracle's colours, colour count and round count.
 WL_HOST_ROUNDS sets how many rounds are host-driven before the groups start
 (0: every round is device-driven) and WL_ASYNC_PASSES how many radix passes a
 device-driven round runs before it halts for the host to finish it (0: every
-round with a class of more than 2048 nodes halts).  Both are read at every
-call, so the cases below switch them per call.
+round with a class of more than 2048 nodes halts).  WL_GRAPH=1 replays the
+device-driven rounds from a captured HIP graph.  All are read at every call,
+so the cases below switch them per call.
 """
 import os
 import random
@@ -26,11 +27,12 @@ SETTINGS = [(0, 0), (0, 1), (0, 2), (3, 0), (3, 2)]
 
 @pytest.fixture
 def knobs():
-    saved = {k: os.environ.get(k) for k in ("WL_HOST_ROUNDS", "WL_ASYNC_PASSES")}
+    saved = {k: os.environ.get(k) for k in ("WL_HOST_ROUNDS", "WL_ASYNC_PASSES", "WL_GRAPH")}
 
-    def set_(host_rounds, passes):
+    def set_(host_rounds, passes, graph=0):
         os.environ["WL_HOST_ROUNDS"] = str(host_rounds)
         os.environ["WL_ASYNC_PASSES"] = str(passes)
+        os.environ["WL_GRAPH"] = str(graph)
 
     yield set_
     for k, v in saved.items():
@@ -98,6 +100,21 @@ def test_big_classes_and_paths(knobs, host_rounds, passes):
     rp, col = _heavy_graph()
     print(f"heavy host_rounds={host_rounds} passes={passes}", flush=True)
     _same_as_oracle(rp, col, seed=3)
+
+
+@pytest.mark.parametrize("host_rounds,passes", [(0, 0), (0, 1), (3, 2)])
+def test_graph_replay(knobs, host_rounds, passes):
+    # the device-driven rounds replayed from the captured two-round graphs,
+    # with halts (passes 0, 1) that change the parity of the next group
+    knobs(host_rounds, passes, graph=1)
+    g = inputs.grid_graph(100)
+    print(f"graph replay grid100 host_rounds={host_rounds} passes={passes}", flush=True)
+    assert _same_as_oracle(g.row_ptr, g.col, seed=1) == (1275, 50, 0)
+    rp, col = _heavy_graph()
+    _same_as_oracle(rp, col, seed=3)
+    for cap in (7, 20):
+        k, r, st = _same_as_oracle(g.row_ptr, g.col, seed=2, max_rounds=cap)
+        assert r == cap and st == 1
 
 
 @pytest.mark.parametrize("trial", range(8))
