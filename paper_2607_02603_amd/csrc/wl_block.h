@@ -51,4 +51,21 @@ __device__ __forceinline__ uint32_t block_append(bool want, uint32_t* counter,
   return at;
 }
 
+// Lanes of the wave that are active and hold the same key as this lane
+// (0 for an inactive lane); one pass per distinct key among the active
+// lanes.  Every lane of the calling control flow must call it.
+__device__ __forceinline__ unsigned long long wave_peers(uint32_t key, bool active) {
+  unsigned long long todo = __ballot(active);
+  unsigned long long mine = 0;
+  while (todo) {
+    const int leader = __ffsll((long long)todo) - 1;
+    const uint32_t lk = __shfl(key, leader, kWave);
+    const bool same = active && key == lk;
+    const unsigned long long m = __ballot(same);
+    if (same) mine = m;
+    todo &= ~m;
+  }
+  return mine;
+}
+
 }  // namespace wl

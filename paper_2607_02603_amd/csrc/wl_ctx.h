@@ -9,6 +9,7 @@ namespace wl {
 constexpr int kBlock = 256;          // threads per workgroup (4 waves)
 constexpr uint32_t kSmallMax = 2048; // class/bucket size sorted in LDS
 constexpr uint32_t kTinyMax = 64;    // class/bucket size sorted in one wave
+constexpr uint32_t kPicoMax = 8;     // ... sorted by 8 lanes (kept at the back of the tiny list)
 constexpr uint32_t kTile = 4096;     // elements per tile in the MSD passes
 constexpr uint32_t kTilePerThread = kTile / kBlock;
 constexpr int kRadixBits = 8;
@@ -63,6 +64,7 @@ struct DevState {
   uint32_t n_mid;       // live rows queued for one wave each (this round)
   uint32_t n_hlive;     // live heavy rows (this round)
   uint32_t prep_round;  // the round whose gather tables the round end prepares
+  uint32_t n_pico;      // segments of <= kPicoMax nodes (this round)
   uint64_t seed;
   unsigned long long work[3][2];    // diagnostics: rows, entries per image kind
   unsigned long long act_entries;   // entries of the rows whose image is needed

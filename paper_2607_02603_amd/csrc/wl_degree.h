@@ -26,7 +26,6 @@ struct DegScratch {
   uint32_t* dcount;  // max_deg + 1: nodes per degree, then rank | live bit
   uint32_t* dlist;   // kDegRanks: present degrees (unordered)
   uint32_t* roff;    // kDegRanks: first member-list position of each rank
-  uint32_t* rcur;    // kDegRanks: placement cursors
   uint32_t* rj;      // kDegRanks: live class index of each rank
   uint32_t* nd;      // number of present degrees (DevState::deg_nd)
 };
@@ -195,7 +194,6 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
         const bool live = size != 0;
         d.rj[r] = live ? jn : 0xFFFFFFFFu;
         d.roff[r] = off;
-        d.rcur[r] = off;
         if (live) {
           ctx.lcold[jn] = r;
           ctx.loff[jn] = off;
@@ -223,19 +221,25 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
   }
 }
 
-// New colour of every node; members of live classes placed class after
-// class into the member list (counting placement: one cursor reservation per
-// block and rank).  Nothing of the live state is read in this round, so the
-// lists are written in place.
+// Placement of the nodes of the live classes, class after class, as a
+// counting sort over blocks: every block counts its nodes per rank (a
+// column of the rank x block matrix m), each rank's row is scanned into
+// offsets from the rank's first position, and every block places its nodes
+// from its own offsets.  No block contends with another for a cursor.
+__device__ __forceinline__ void deg_block_range(uint32_t n, uint32_t* lo, uint32_t* hi) {
+  const uint32_t per = ((n + gridDim.x - 1) / gridDim.x + kBlock - 1) / kBlock * kBlock;
+  *lo = min(n, blockIdx.x * per);
+  *hi = min(n, *lo + per);
+}
+
 template <bool RP64>
-__global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
+__global__ void __launch_bounds__(kBlock) k_deg_count(Ctx ctx, DegScratch d, uint32_t* m) {
   const DevState* st = ctx.st;
   if (*d.nd > kDegRanks || st->nosplit) return;
   __shared__ uint32_t lc[kDegRanks];
-  const uint32_t K = st->k_new;
-  const uint32_t n = ctx.n;
-  const uint32_t per = ((n + gridDim.x - 1) / gridDim.x + kBlock - 1) / kBlock * kBlock;
-  const uint32_t lo = min(n, blockIdx.x * per), hi = min(n, lo + per);
+  const uint32_t K = st->k_new, nblk = gridDim.x;
+  uint32_t lo, hi;
+  deg_block_range(ctx.n, &lo, &hi);
   for (uint32_t r = threadIdx.x; r < K; r += kBlock) lc[r] = 0;
   __syncthreads();
   for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
@@ -243,9 +247,45 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
     if (e & kDegLive) atomicAdd(&lc[e & ~kDegLive], 1u);
   }
   __syncthreads();
-  for (uint32_t r = threadIdx.x; r < K; r += kBlock)
-    if (lc[r]) lc[r] = atomicAdd(&d.rcur[r], lc[r]);
+  for (uint32_t r = threadIdx.x; r < K; r += kBlock) m[(uint64_t)r * nblk + blockIdx.x] = lc[r];
+}
+
+// One block per rank: its row of m becomes the first member-list position
+// of each block's nodes of that rank.
+__global__ void __launch_bounds__(kBlock) k_deg_rowscan(Ctx ctx, DegScratch d, uint32_t* m,
+                                                        uint32_t nblk) {
+  const DevState* st = ctx.st;
+  if (*d.nd > kDegRanks || st->nosplit) return;
+  const uint32_t K = st->k_new;
+  __shared__ uint32_t sh[kBlock / kWave];
+  for (uint32_t r = blockIdx.x; r < K; r += gridDim.x) {
+    uint32_t* row = m + (uint64_t)r * nblk;
+    uint32_t carry = d.roff[r];
+    for (uint32_t b0 = 0; b0 < nblk; b0 += kBlock) {
+      const uint32_t b = b0 + threadIdx.x;
+      const uint32_t v = b < nblk ? row[b] : 0u;
+      uint32_t tot;
+      const uint32_t ex = block_excl_scan(v, sh, &tot);
+      if (b < nblk) row[b] = carry + ex;
+      carry += tot;
+    }
+  }
+}
+
+// New colour of every node; members of live classes placed from their
+// block's offsets.  Nothing of the live state is read in this round, so the
+// lists are written in place.
+template <bool RP64>
+__global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d, const uint32_t* m) {
+  const DevState* st = ctx.st;
+  if (*d.nd > kDegRanks || st->nosplit) return;
+  __shared__ uint32_t lc[kDegRanks];
+  const uint32_t K = st->k_new, nblk = gridDim.x;
+  uint32_t lo, hi;
+  deg_block_range(ctx.n, &lo, &hi);
+  for (uint32_t r = threadIdx.x; r < K; r += kBlock) lc[r] = m[(uint64_t)r * nblk + blockIdx.x];
   __syncthreads();
+  const uint32_t lane = lane_id();
   for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
     const uint64_t r0 = RP64 ? ctx.rp64[i] : ctx.rp32[i];
     const uint32_t g = degree_of(ctx, i, RP64);
@@ -253,8 +293,15 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d) {
     const uint32_t r = e & ~kDegLive;
     ctx.c[i] = r;
     const bool live = (e & kDegLive) != 0;
+    // slots: one LDS atomic per rank present in the wave, ranks of the lanes
+    // inside it by their position
+    const unsigned long long peers = wave_peers(r, live);
+    const int ldr = live ? __ffsll((long long)peers) - 1 : (int)lane;
+    uint32_t b = 0;
+    if (live && (int)lane == ldr) b = atomicAdd(&lc[r], (uint32_t)__popcll(peers));
+    b = __shfl(b, ldr, kWave);
     if (live) {
-      const uint32_t q = atomicAdd(&lc[r], 1u);
+      const uint32_t q = b + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
       ctx.lperm[q] = i;
       ctx.qcls[q] = d.rj[r];
       ctx.rs[q] = r0;

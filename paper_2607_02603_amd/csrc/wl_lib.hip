@@ -942,6 +942,9 @@ struct Session {
     if (host.n_tiny)
       hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(host.n_tiny, kBlock / kWave, 8192)),
                          dim3(kBlock), 0, s, ctx, -1);
+    if (host.n_pico)
+      hipLaunchKernelGGL(k_pico_sort, dim3(grid_for(host.n_pico, kBlock / 8, 8192)),
+                         dim3(kBlock), 0, s, ctx);
     if (host.n_small)
       hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
                          dim3(kBlock), 0, s, ctx);
@@ -1049,7 +1052,9 @@ struct Session {
     hipLaunchKernelGGL(k_shift_clear, dim3(gn), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_shift_scatter, dim3(gc), dim3(kBlock), 0, s, ctx);
     xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr, nscan);
-    hipLaunchKernelGGL(k_shift_apply, dim3(gn), dim3(kBlock), 0, s, ctx);
+    // each block loads the split list into LDS: a capped grid loads it fewer times
+    hipLaunchKernelGGL(k_shift_apply, dim3(std::min<uint32_t>(gn, 1024)), dim3(kBlock), 0, s,
+                       ctx);
     if (rp64)
       hipLaunchKernelGGL(k_live_emit<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
     else
@@ -1070,8 +1075,7 @@ struct Session {
     d.dcount = base;
     d.dlist = base + (uint64_t)maxd + 1;
     d.roff = d.dlist + kDegRanks;
-    d.rcur = d.roff + kDegRanks;
-    d.rj = d.rcur + kDegRanks;
+    d.rj = d.roff + kDegRanks;
     d.nd = &ctx.st->deg_nd;
     const uint32_t gd = grid_for((uint64_t)maxd + 1, kBlock, 4096);
     using RPT = typename std::conditional<RP64, uint64_t, uint32_t>::type;
@@ -1088,8 +1092,16 @@ struct Session {
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (host.deg_nd > kDegRanks) return WL_OK;
-    hipLaunchKernelGGL(k_deg_place<RP64>, dim3(grid_for(L.n, kBlock, 2048)), dim3(kBlock), 0, s,
-                       ctx, d);
+    // the rank x block matrix of the placement lives in x (2n words): at
+    // most 1024 blocks, fewer when there are many ranks
+    const uint64_t K = std::max<uint32_t>(host.k_new, 1);
+    const uint32_t nblk = (uint32_t)std::max<uint64_t>(
+        1, std::min<uint64_t>({1024, grid_for(L.n, kBlock), 2 * L.n / K}));
+    uint32_t* m = (uint32_t*)ctx.x;
+    hipLaunchKernelGGL(k_deg_count<RP64>, dim3(nblk), dim3(kBlock), 0, s, ctx, d, m);
+    hipLaunchKernelGGL(k_deg_rowscan, dim3((uint32_t)std::min<uint64_t>(K, 4096)), dim3(kBlock), 0,
+                       s, ctx, d, m, nblk);
+    hipLaunchKernelGGL(k_deg_place<RP64>, dim3(nblk), dim3(kBlock), 0, s, ctx, d, m);
     hipLaunchKernelGGL(k_live_round_end, dim3(next_async ? grid_for(L.n, kBlock, 4096) : 1),
                        dim3(kBlock), 0, s, ctx, next_async ? 1 : 0);
     HIP_LAUNCH_CHECK();
@@ -1101,7 +1113,7 @@ struct Session {
   // Whether the degree round's table and lists fit the scratch it uses (the
   // keys_tmp region, two words per node).
   bool degree_round_fits() const {
-    const uint64_t words = (uint64_t)host.max_deg + 1 + 4ull * kDegRanks;
+    const uint64_t words = (uint64_t)host.max_deg + 1 + 3ull * kDegRanks;
     return host.max_deg < 0x7FFFFFFFu && words <= 2 * L.n;
   }
 
@@ -1179,6 +1191,8 @@ struct Session {
     // taken in grid-stride loops
     hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 1024)),
                        dim3(kBlock), 0, s, ctx, ap);
+    hipLaunchKernelGGL(k_pico_sort, dim3(grid_for(L.n / 2, kBlock / 8, 1024)), dim3(kBlock), 0,
+                       s, ctx);
     hipLaunchKernelGGL(k_small_sort, dim3(grid_for(L.n / (kTinyMax + 1), 1, 1024)),
                        dim3(kBlock), 0, s, ctx);
     live_tail(true);

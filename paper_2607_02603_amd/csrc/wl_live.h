@@ -212,9 +212,12 @@ __global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
       s = ctx.loff[j];
       len = ctx.llen[j];
     }
-    const bool tiny = len >= 2 && len <= kTinyMax;
+    const bool pico = len >= 2 && len <= kPicoMax;
+    const bool tiny = len > kPicoMax && len <= kTinyMax;
     const bool small = len > kTinyMax && len <= kSmallMax;
     const bool big = len > kSmallMax;
+    const uint32_t pp = block_append(pico, &st->n_pico, sh, &base_sh);
+    if (pico) ctx.tiny_list[ctx.max_small - 1 - pp] = make_uint2(s, len | kMatBit);
     const uint32_t t = block_append(tiny, &st->n_tiny, sh, &base_sh);
     if (tiny) ctx.tiny_list[t] = make_uint2(s, len | kMatBit);
     const uint32_t a = block_append(small, &st->n_small, sh, &base_sh);
@@ -575,6 +578,7 @@ __global__ void __launch_bounds__(kBlock) k_live_round_end(Ctx ctx, int prep) {
   st->k = kn;
   st->n_small = 0;
   st->n_tiny = 0;
+  st->n_pico = 0;
   st->n_big[0] = 0;
   st->n_big[1] = 0;
   st->n_tiles = 0;

@@ -36,6 +36,7 @@ __global__ void k_round_begin(Ctx ctx) {
   if (st->done) return;
   st->n_small = 0;
   st->n_tiny = 0;
+  st->n_pico = 0;
   st->n_big[0] = 0;
   st->n_big[1] = 0;
   st->n_tiles = 0;
@@ -71,10 +72,13 @@ __global__ void __launch_bounds__(kBlock) k_segments(Ctx ctx) {
       len = e > s ? e - s : 0;
       if (len) ctx.flags[s] = 1;
     }
-    const bool tiny = len >= 2 && len <= kTinyMax;
+    const bool pico = len >= 2 && len <= kPicoMax;
+    const bool tiny = len > kPicoMax && len <= kTinyMax;
     const bool small = len > kTinyMax && len <= kSmallMax;
     const bool big = len > kSmallMax;
     const uint32_t mat = ctx.keys_mat ? kMatBit : 0u;
+    const uint32_t pp = block_append(pico, &st->n_pico, sh, &base_sh);
+    if (pico) ctx.tiny_list[ctx.max_small - 1 - pp] = make_uint2(s, len | mat);
     const uint32_t t = block_append(tiny, &st->n_tiny, sh, &base_sh);
     if (tiny) ctx.tiny_list[t] = make_uint2(s, len | mat);
     const uint32_t a = block_append(small, &st->n_small, sh, &base_sh);
@@ -245,7 +249,10 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
       const uint32_t pos = s.x + off;
       ctx.flags[pos] = 1;
       if (h >= 2 && bmn != bmx) {
-        if (h <= kTinyMax) {
+        if (h <= kPicoMax) {
+          uint32_t idx = atomicAdd(&st->n_pico, 1u);
+          ctx.tiny_list[ctx.max_small - 1 - idx] = make_uint2(pos, h | kMatBit);
+        } else if (h <= kTinyMax) {
           uint32_t idx = atomicAdd(&st->n_tiny, 1u);
           ctx.tiny_list[idx] = make_uint2(pos, h | kMatBit);
         } else if (h <= kSmallMax) {
@@ -428,6 +435,60 @@ __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes)
       ctx.perm[s + lane] = v;
       if (mat) ctx.keys[s + lane] = key;  // sorted keys stay with their payload
       if (lane > 0 && key != prev) ctx.flags[s + lane] = 1;
+    }
+  }
+}
+
+// Segments of at most kPicoMax nodes, listed from the back of the tiny
+// list: eight per wave, eight lanes each, with the tiny sort's bitonic
+// network cut to eight elements.  Skipped when all keys of a segment agree.
+__global__ void __launch_bounds__(kBlock) k_pico_sort(Ctx ctx) {
+  DevState* st = ctx.st;
+  if (st->done) return;
+  const uint32_t np = st->n_pico;
+  const uint32_t lane = lane_id(), sub = lane & 7u, g0 = lane & ~7u;
+  const uint32_t nwaves = gridDim.x * (kBlock / kWave);
+  // loop bounds are the same for the whole wave (the shuffles need every lane)
+  for (uint32_t base = (blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * 8; base < np;
+       base += nwaves * 8) {
+    const uint32_t si = base + (lane >> 3);
+    uint32_t s = 0, len = 0;
+    bool mat = false;
+    if (si < np) {
+      const uint2 sg = ctx.tiny_list[ctx.max_small - 1 - si];
+      s = sg.x;
+      len = sg.y & ~kMatBit;
+      mat = (sg.y & kMatBit) != 0;
+    }
+    unsigned long long key = ~0ull;
+    uint32_t v = 0;
+    if (sub < len) {
+      v = ctx.perm[s + sub];
+      key = mat ? ctx.keys[s + sub] : ctx.z[v];
+    }
+    const unsigned long long first = __shfl(key, (int)g0, kWave);
+    const unsigned long long dm = __ballot(sub < len && key != first);
+    const bool differ = ((dm >> g0) & 0xFFull) != 0;
+#pragma unroll
+    for (uint32_t kk = 2; kk <= 8; kk <<= 1) {
+#pragma unroll
+      for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+        const unsigned long long pk = __shfl_xor(key, (int)j, kWave);
+        const uint32_t pv = __shfl_xor(v, (int)j, kWave);
+        const bool up = (sub & kk) == 0;
+        const bool lower = (sub & j) == 0;
+        const bool take = (lower == up) ? (pk < key) : (pk > key);
+        if (take) {
+          key = pk;
+          v = pv;
+        }
+      }
+    }
+    const unsigned long long prev = __shfl_up(key, 1, kWave);
+    if (differ && sub < len) {
+      ctx.perm[s + sub] = v;
+      if (mat) ctx.keys[s + sub] = key;
+      if (sub > 0 && key != prev) ctx.flags[s + sub] = 1;
     }
   }
 }

@@ -164,3 +164,16 @@ def test_medium_rmat_tight_budget_auto_cap():
         assert len(np.unique(S[got == blk])) == 1  # finer than or equal to coarsest
     if coarsest:
         assert np.array_equal(got, ref)
+
+
+def test_rmat20_several_outer_iterations():
+    # R-MAT scale 20 (31M entries) under a cap of a fifth of the entries:
+    # several batches with heavy rows and several outer iterations; the same
+    # result twice
+    g = inputs.rmat(20, 16, seed=3)
+    mb = g.nnz // 5
+    print(f"rmat20 mb={mb}", flush=True)
+    got, k, r, outer, coarsest = _check(g.row_ptr, g.col, mb=mb)
+    assert outer >= 2
+    again = wl.wl_stable_coloring_batched(_host_graph(g.row_ptr, g.col), None, 0, mb)
+    assert np.array_equal(again[0].numpy().view(np.uint32), got)
