@@ -197,12 +197,33 @@ __global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
     mn[threadIdx.x] = ~0ull;
     mx[threadIdx.x] = 0;
     __syncthreads();
+    // runs of one digit among a thread's keys are counted in registers and
+    // added with one set of atomics (classes with few distinct keys give
+    // long runs; the LDS atomics of a wave would all hit one bucket)
+    uint32_t rd = 0xFFFFFFFFu, rc = 0;
+    unsigned long long rmn = ~0ull, rmx = 0;
     for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
       const uint64_t key = ctx.keys[p];
       const uint32_t d = digit_of(key, pass);
-      atomicAdd(&cnt[d], 1u);
-      atomicMin(&mn[d], (unsigned long long)key);
-      atomicMax(&mx[d], (unsigned long long)key);
+      if (d != rd) {
+        if (rc) {
+          atomicAdd(&cnt[rd], rc);
+          atomicMin(&mn[rd], rmn);
+          atomicMax(&mx[rd], rmx);
+        }
+        rd = d;
+        rc = 0;
+        rmn = ~0ull;
+        rmx = 0;
+      }
+      ++rc;
+      rmn = key < rmn ? key : rmn;
+      rmx = key > rmx ? key : rmx;
+    }
+    if (rc) {
+      atomicAdd(&cnt[rd], rc);
+      atomicMin(&mn[rd], rmn);
+      atomicMax(&mx[rd], rmx);
     }
     __syncthreads();
     const uint32_t b = threadIdx.x;
