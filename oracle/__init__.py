@@ -25,6 +25,11 @@ _LIB = None
 P61 = (1 << 61) - 1
 GAMMA = 0x9E3779B97F4A7C15
 
+# Arithmetic of the image step (argument q): F_p with p = 2^61 - 1, or the
+# ring Z/2^64 of Section 4.1 (Algorithm 1 with precision q = 64).
+FP = 0
+RING64 = 64
+
 
 def _lib():
     global _LIB
@@ -44,16 +49,27 @@ def _lib():
         lib.orc_round_key.argtypes = [u64, u64]
         lib.orc_weight.restype = u64
         lib.orc_weight.argtypes = [u64, u64, u64]
+        lib.orc_weight_q.restype = u64
+        lib.orc_weight_q.argtypes = [u64, u64, u64, u32]
+        lib.orc_ring_preconditions.restype = ctypes.c_int
+        lib.orc_ring_preconditions.argtypes = [u64, vp, vp]
         lib.orc_canonicalize.restype = u32
         lib.orc_canonicalize.argtypes = [u64, vp, vp]
         lib.orc_image.restype = None
         lib.orc_image.argtypes = [u64, vp, vp, vp, vp, u32, u64, u64, vp]
+        lib.orc_image_q.restype = ctypes.c_int
+        lib.orc_image_q.argtypes = [u64, vp, vp, vp, vp, u32, u64, u64, vp, u32]
         lib.orc_relabel.restype = u32
         lib.orc_relabel.argtypes = [u64, vp, vp, vp]
         lib.orc_refine_round.restype = u32
         lib.orc_refine_round.argtypes = [u64, vp, vp, vp, vp, u32, u64, u64, vp, vp]
+        lib.orc_refine_round_q.restype = u32
+        lib.orc_refine_round_q.argtypes = [u64, vp, vp, vp, vp, u32, u64, u64, vp, vp, u32]
         lib.orc_stable_coloring.restype = ctypes.c_int
         lib.orc_stable_coloring.argtypes = [u64, vp, vp, vp, vp, u64, u32, vp, vp, vp, vp]
+        lib.orc_stable_coloring_q.restype = ctypes.c_int
+        lib.orc_stable_coloring_q.argtypes = [u64, vp, vp, vp, vp, u64, u32, vp, vp, vp, vp,
+                                              u32]
         lib.orc_classic_round.restype = u32
         lib.orc_classic_round.argtypes = [u64, vp, vp, vp, vp, vp]
         lib.orc_classic_coloring.restype = ctypes.c_int
@@ -67,6 +83,9 @@ def _lib():
         lib.orc_batched_coloring.restype = ctypes.c_int
         lib.orc_batched_coloring.argtypes = [u64, vp, vp, vp, vp, u64, u64, u32,
                                              vp, vp, vp, vp, vp]
+        lib.orc_batched_coloring_q.restype = ctypes.c_int
+        lib.orc_batched_coloring_q.argtypes = [u64, vp, vp, vp, vp, u64, u64, u32,
+                                               vp, vp, vp, vp, vp, u32]
         _LIB = lib
     return _LIB
 
@@ -98,9 +117,18 @@ def round_key(seed, r):
     return int(_lib().orc_round_key(seed, r))
 
 
-def weight(seed, r, color):
-    """W(seed, r, b): random value of colour b in round r (Algorithm 1)."""
-    return int(_lib().orc_weight(seed, r, color))
+def weight(seed, r, color, q=FP):
+    """W(seed, r, b): random value of colour b in round r (Algorithm 1), in
+    F_p (q = FP) or Z/2^64 (q = RING64)."""
+    return int(_lib().orc_weight_q(seed, r, color, q))
+
+
+def ring_preconditions(row_ptr, weight_=None):
+    """Theorem 1's preconditions for Z/2^64: n <= 2^32 and every row sum
+    of A at most 2^32."""
+    rp = np.ascontiguousarray(row_ptr, dtype=np.uint64)
+    wt = None if weight_ is None else np.ascontiguousarray(weight_, dtype=np.uint32)
+    return bool(_lib().orc_ring_preconditions(rp.size - 1, _p(rp), _p(wt)))
 
 
 # ---------------------------------------------------------------------------
@@ -118,13 +146,16 @@ def canonicalize(labels, n=None):
     return out, int(k)
 
 
-def image(row_ptr, col, weight_, colors, k, seed, r):
-    """z = A w (mod p) with w_j = W(seed, r, c_j) (Algorithm 1)."""
+def image(row_ptr, col, weight_, colors, k, seed, r, q=FP):
+    """z = A w with w_j = W(seed, r, c_j) (Algorithm 1), mod p (q = FP) or
+    mod 2^64 (q = RING64)."""
     rp, cl, wt = _csr(row_ptr, col, weight_)
     c = np.ascontiguousarray(colors, dtype=np.uint32)
     n = rp.size - 1
     z = np.empty(n, dtype=np.uint64)
-    _lib().orc_image(n, _p(rp), _p(cl), _p(wt), _p(c), k, seed, r, _p(z))
+    st = _lib().orc_image_q(n, _p(rp), _p(cl), _p(wt), _p(c), k, seed, r, _p(z), q)
+    if st != 0:
+        raise ValueError(f"orc_image_q failed ({st})")
     return z
 
 
@@ -137,23 +168,26 @@ def relabel(colors, z):
     return out, int(k)
 
 
-def refine_round(row_ptr, col, weight_, colors, k, seed, r):
+def refine_round(row_ptr, col, weight_, colors, k, seed, r, q=FP):
     """One round of Algorithm 1.  Returns (new colours, k', z)."""
     rp, cl, wt = _csr(row_ptr, col, weight_)
     c = np.ascontiguousarray(colors, dtype=np.uint32)
     n = rp.size - 1
     out = np.empty(n, dtype=np.uint32)
     z = np.empty(n, dtype=np.uint64)
-    k2 = _lib().orc_refine_round(n, _p(rp), _p(cl), _p(wt), _p(c), k, seed, r,
-                                 _p(out), _p(z))
+    k2 = _lib().orc_refine_round_q(n, _p(rp), _p(cl), _p(wt), _p(c), k, seed, r,
+                                   _p(out), _p(z), q)
+    if n and k2 == 0:
+        raise ValueError("orc_refine_round_q: the image step failed")
     return out, int(k2), z
 
 
-def stable_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_rounds=0):
-    """Algorithm 1 to completion.
+def stable_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_rounds=0, q=FP):
+    """Algorithm 1 to completion, in F_p (q = FP) or Z/2^64 (q = RING64).
 
     Returns (colours, k, rounds, k_per_round, status); status 0 = stable,
-    1 = round cap reached.
+    1 = round cap reached, 3 = q = RING64 and Theorem 1's preconditions
+    fail (nothing computed), 4 = an image step failed.
     """
     rp, cl, wt = _csr(row_ptr, col, weight_)
     n = rp.size - 1
@@ -163,9 +197,9 @@ def stable_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_rounds=0)
     hist = np.zeros(max(cap, 1), dtype=np.uint32)
     k = ctypes.c_uint32(0)
     rounds = ctypes.c_uint32(0)
-    st = _lib().orc_stable_coloring(n, _p(rp), _p(cl), _p(wt), _p(lab), seed, cap,
-                                    _p(out), ctypes.byref(k), ctypes.byref(rounds),
-                                    _p(hist))
+    st = _lib().orc_stable_coloring_q(n, _p(rp), _p(cl), _p(wt), _p(lab), seed, cap,
+                                      _p(out), ctypes.byref(k), ctypes.byref(rounds),
+                                      _p(hist), q)
     return out, int(k.value), int(rounds.value), hist[: rounds.value].copy(), int(st)
 
 
@@ -228,8 +262,9 @@ def batch_cut(row_ptr, max_batch):
 
 
 def batched_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_batch=1,
-                     max_rounds=0):
-    """Algorithm 2 with the readings of the oracle source.
+                     max_rounds=0, q=FP):
+    """Algorithm 2 with the readings of the oracle source, in F_p (q = FP)
+    or Z/2^64 (q = RING64).
 
     Returns (first-occurrence colours, k, rounds, outer iterations,
     coarsest flag, status).
@@ -243,9 +278,9 @@ def batched_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_batch=1,
     rounds = ctypes.c_uint32(0)
     outer = ctypes.c_uint32(0)
     coarsest = ctypes.c_int(0)
-    st = _lib().orc_batched_coloring(n, _p(rp), _p(cl), _p(wt), _p(lab), seed,
-                                     max_batch, cap, _p(out), ctypes.byref(k),
-                                     ctypes.byref(rounds), ctypes.byref(outer),
-                                     ctypes.byref(coarsest))
+    st = _lib().orc_batched_coloring_q(n, _p(rp), _p(cl), _p(wt), _p(lab), seed,
+                                       max_batch, cap, _p(out), ctypes.byref(k),
+                                       ctypes.byref(rounds), ctypes.byref(outer),
+                                       ctypes.byref(coarsest), q)
     return (out, int(k.value), int(rounds.value), int(outer.value),
             bool(coarsest.value), int(st))

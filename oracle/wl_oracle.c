@@ -18,13 +18,25 @@
  *
  * Readings where the paper leaves a choice open (each is listed in the design
  * notes of the repository):
- *   - arithmetic is the prime field F_p, p = 2^61 - 1, instead of the ring
- *     Z/2^64 of Section 4.1 (a nonzero linear form over a field vanishes on a
- *     uniform probe with probability exactly 1/p, so the paper's resampling
- *     "until |H| distinct values" step of Algorithm 1 is not needed);
+ *   - two arithmetics for the image z = A w, chosen by the argument q of the
+ *     *_q functions:
+ *       q = 0  (ORC_FP, the default): the prime field F_p, p = 2^61 - 1, in
+ *              place of the ring of Section 4.1 (a nonzero linear form over a
+ *              field vanishes on a uniform probe with probability exactly
+ *              1/p, so the resampling step "until |H| distinct values" of
+ *              Algorithm 1 is not needed and not done);
+ *       q = 64 (ORC_RING64): the ring R = Z/2^64 of Section 4.1 and
+ *              Algorithm 1 with precision q = 64: unsigned 64-bit values,
+ *              sums and products taken modulo 2^64.  The resampling step is
+ *              kept as a check: the k values of a round must be pairwise
+ *              distinct.  They always are (the SplitMix64 output function is
+ *              a bijection of 64-bit words and the k stream states are
+ *              distinct), so one draw suffices.  Theorem 1's preconditions,
+ *              n <= 2^32 and every row sum <= 2^32, are checked first;
  *   - the per-colour random value of colour b in round r is
  *     W(seed, r, b) = (b+1)-th output of a SplitMix64 stream whose state is
- *     K(seed, r) = mix(mix(seed + g) + (r+1) g), reduced mod p
+ *     K(seed, r) = mix(mix(seed + g) + (r+1) g), reduced mod p in F_p and
+ *     taken as it is in Z/2^64
  *     (SplitMix64: Steele, Lea, Flood, OOPSLA 2014; the paper's appendix
  *     seeds its generator with SplitMix64 as well);
  *   - the new colour of node i is the rank of the pair (c_i, z_i) among the
@@ -68,10 +80,43 @@ uint64_t orc_round_key(uint64_t seed, uint64_t round)
     return orc_splitmix_nth(s1, round + 1);
 }
 
+#define ORC_FP 0     /* arithmetic in F_p, p = 2^61 - 1 */
+#define ORC_RING64 64 /* arithmetic in Z/2^64 (Algorithm 1, q = 64) */
+
 /* Random value of colour b in round r (Algorithm 1: one value per block). */
+uint64_t orc_weight_q(uint64_t seed, uint64_t round, uint64_t color, uint32_t q)
+{
+    uint64_t v = orc_splitmix_nth(orc_round_key(seed, round), color + 1);
+    return q == ORC_RING64 ? v : v % ORC_P;
+}
+
 uint64_t orc_weight(uint64_t seed, uint64_t round, uint64_t color)
 {
-    return orc_splitmix_nth(orc_round_key(seed, round), color + 1) % ORC_P;
+    return orc_weight_q(seed, round, color, ORC_FP);
+}
+
+static int cmp_u64(const void *a, const void *b)
+{
+    uint64_t x = *(const uint64_t *)a, y = *(const uint64_t *)b;
+    return (x > y) - (x < y);
+}
+
+/* Theorem 1's preconditions for Z/2^q: n <= 2^(q/2) and every row sum of A
+ * at most 2^(q/2).  Returns 1 when they hold (q = 64). */
+int orc_ring_preconditions(uint64_t n, const uint64_t *row_ptr,
+                           const uint32_t *weight)
+{
+    const u128 lim = (u128)1 << 32;
+    if (n > (uint64_t)lim)
+        return 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        u128 s = 0;
+        for (uint64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e)
+            s += weight ? weight[e] : 1;
+        if (s > lim)
+            return 0;
+    }
+    return 1;
 }
 
 /* ------------------------------------------------------------------------- */
@@ -134,15 +179,34 @@ static int cmp_pair(const void *a, const void *b)
     return (x->z > y->z) - (x->z < y->z);
 }
 
-/* z = A w mod p where w_j = W(seed, round, c_j).  A is CSR (row_ptr has n+1
- * entries; weight == NULL means every stored entry has weight 1). */
-void orc_image(uint64_t n, const uint64_t *row_ptr, const uint32_t *col,
-               const uint32_t *weight, const uint32_t *c, uint32_t k,
-               uint64_t seed, uint64_t round, uint64_t *z)
+/* z = A w where w_j = W(seed, round, c_j), in F_p (q = 0) or in Z/2^64
+ * (q = 64).  A is CSR (row_ptr has n+1 entries; weight == NULL means every
+ * stored entry has weight 1).  The sums are exact in 128 bits and reduced
+ * once.  Returns 0, -1 if (q = 64) the k values are not pairwise distinct
+ * (the repeat-until condition of Algorithm 1; it does not happen, see the
+ * header), -2 for an unknown q. */
+int orc_image_q(uint64_t n, const uint64_t *row_ptr, const uint32_t *col,
+                const uint32_t *weight, const uint32_t *c, uint32_t k,
+                uint64_t seed, uint64_t round, uint64_t *z, uint32_t q)
 {
+    if (q != ORC_FP && q != ORC_RING64)
+        return -2;
     uint64_t *w = (uint64_t *)malloc((k ? k : 1) * sizeof(uint64_t));
     for (uint32_t b = 0; b < k; ++b)
-        w[b] = orc_weight(seed, round, b);
+        w[b] = orc_weight_q(seed, round, b, q);
+    if (q == ORC_RING64 && k > 1) {
+        uint64_t *s = (uint64_t *)malloc(k * sizeof(uint64_t));
+        memcpy(s, w, k * sizeof(uint64_t));
+        qsort(s, k, sizeof(uint64_t), cmp_u64);
+        int dup = 0;
+        for (uint32_t b = 1; b < k; ++b)
+            dup |= s[b] == s[b - 1];
+        free(s);
+        if (dup) {
+            free(w);
+            return -1;
+        }
+    }
 #pragma omp parallel for schedule(dynamic, 1024)
     for (int64_t i = 0; i < (int64_t)n; ++i) {
         u128 acc = 0;
@@ -150,9 +214,17 @@ void orc_image(uint64_t n, const uint64_t *row_ptr, const uint32_t *col,
             uint64_t a = weight ? weight[e] : 1;
             acc += (u128)a * w[c[col[e]]];
         }
-        z[i] = (uint64_t)(acc % ORC_P);
+        z[i] = q == ORC_RING64 ? (uint64_t)acc : (uint64_t)(acc % ORC_P);
     }
     free(w);
+    return 0;
+}
+
+void orc_image(uint64_t n, const uint64_t *row_ptr, const uint32_t *col,
+               const uint32_t *weight, const uint32_t *c, uint32_t k,
+               uint64_t seed, uint64_t round, uint64_t *z)
+{
+    orc_image_q(n, row_ptr, col, weight, c, k, seed, round, z, ORC_FP);
 }
 
 /* New colour = rank of (c_i, z_i) among distinct pairs, lexicographic. */
@@ -178,33 +250,49 @@ uint32_t orc_relabel(uint64_t n, const uint32_t *c, const uint64_t *z,
     return (uint32_t)(rank + 1);
 }
 
-/* One full round; returns k'.  z may be NULL (scratch is allocated then). */
-uint32_t orc_refine_round(uint64_t n, const uint64_t *row_ptr,
-                          const uint32_t *col, const uint32_t *weight,
-                          const uint32_t *c_in, uint32_t k_in, uint64_t seed,
-                          uint64_t round, uint32_t *c_out, uint64_t *z_out)
+/* One full round; returns k' (0 if the image step failed, see orc_image_q).
+ * z may be NULL (scratch is allocated then). */
+uint32_t orc_refine_round_q(uint64_t n, const uint64_t *row_ptr,
+                            const uint32_t *col, const uint32_t *weight,
+                            const uint32_t *c_in, uint32_t k_in, uint64_t seed,
+                            uint64_t round, uint32_t *c_out, uint64_t *z_out,
+                            uint32_t q)
 {
     if (n == 0)
         return 0;
     uint64_t *z = z_out ? z_out : (uint64_t *)malloc(n * sizeof(uint64_t));
-    orc_image(n, row_ptr, col, weight, c_in, k_in, seed, round, z);
-    uint32_t k = orc_relabel(n, c_in, z, c_out);
+    uint32_t k = 0;
+    if (orc_image_q(n, row_ptr, col, weight, c_in, k_in, seed, round, z, q) == 0)
+        k = orc_relabel(n, c_in, z, c_out);
     if (!z_out)
         free(z);
     return k;
 }
 
+uint32_t orc_refine_round(uint64_t n, const uint64_t *row_ptr,
+                          const uint32_t *col, const uint32_t *weight,
+                          const uint32_t *c_in, uint32_t k_in, uint64_t seed,
+                          uint64_t round, uint32_t *c_out, uint64_t *z_out)
+{
+    return orc_refine_round_q(n, row_ptr, col, weight, c_in, k_in, seed, round,
+                              c_out, z_out, ORC_FP);
+}
+
 /* Algorithm 1 to completion.  Returns 0 on success, 1 if max_rounds was hit
- * (then c_out holds the last round's colours).  k_hist (may be NULL) receives
- * the colour count after each round (capacity max_rounds). */
-int orc_stable_coloring(uint64_t n, const uint64_t *row_ptr,
-                        const uint32_t *col, const uint32_t *weight,
-                        const uint32_t *init, uint64_t seed,
-                        uint32_t max_rounds, uint32_t *c_out, uint32_t *k_out,
-                        uint32_t *rounds_out, uint32_t *k_hist)
+ * (then c_out holds the last round's colours), 3 if q = 64 and Theorem 1's
+ * preconditions fail (nothing is computed), 4 if an image step failed.
+ * k_hist (may be NULL) receives the colour count after each round (capacity
+ * max_rounds). */
+int orc_stable_coloring_q(uint64_t n, const uint64_t *row_ptr,
+                          const uint32_t *col, const uint32_t *weight,
+                          const uint32_t *init, uint64_t seed,
+                          uint32_t max_rounds, uint32_t *c_out, uint32_t *k_out,
+                          uint32_t *rounds_out, uint32_t *k_hist, uint32_t q)
 {
     *k_out = 0;
     *rounds_out = 0;
+    if (q == ORC_RING64 && !orc_ring_preconditions(n, row_ptr, weight))
+        return 3;
     if (n == 0)
         return 0;
     uint32_t *c = (uint32_t *)malloc(n * sizeof(uint32_t));
@@ -212,8 +300,12 @@ int orc_stable_coloring(uint64_t n, const uint64_t *row_ptr,
     int status = 1;
     uint32_t r = 0;
     while (r < max_rounds) {
-        uint32_t k2 = orc_refine_round(n, row_ptr, col, weight, c, k, seed, r,
-                                       c_out, NULL);
+        uint32_t k2 = orc_refine_round_q(n, row_ptr, col, weight, c, k, seed, r,
+                                         c_out, NULL, q);
+        if (k2 == 0) {
+            status = 4;
+            break;
+        }
         if (k_hist)
             k_hist[r] = k2;
         ++r;
@@ -229,6 +321,16 @@ int orc_stable_coloring(uint64_t n, const uint64_t *row_ptr,
     *rounds_out = r;
     free(c);
     return status;
+}
+
+int orc_stable_coloring(uint64_t n, const uint64_t *row_ptr,
+                        const uint32_t *col, const uint32_t *weight,
+                        const uint32_t *init, uint64_t seed,
+                        uint32_t max_rounds, uint32_t *c_out, uint32_t *k_out,
+                        uint32_t *rounds_out, uint32_t *k_hist)
+{
+    return orc_stable_coloring_q(n, row_ptr, col, weight, init, seed, max_rounds,
+                                 c_out, k_out, rounds_out, k_hist, ORC_FP);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -470,18 +572,24 @@ uint64_t orc_batch_cut(uint64_t n, const uint64_t *row_ptr, uint64_t max_batch,
     return nb;
 }
 
-int orc_batched_coloring(uint64_t n0, const uint64_t *row_ptr0,
-                         const uint32_t *col0, const uint32_t *weight0,
-                         const uint32_t *init, uint64_t seed,
-                         uint64_t max_batch, uint32_t max_rounds,
-                         uint32_t *c_out, uint32_t *k_out,
-                         uint32_t *rounds_out, uint32_t *outer_out,
-                         int *coarsest_out)
+/* Returns 0, 1 (a batch hit max_rounds), 2 (a quotient weight overflowed),
+ * 3 (q = 64 and Theorem 1's preconditions fail; a quotient row sums the
+ * same entries as its representative's row, so checking the input covers
+ * every quotient) or 4 (an image step failed). */
+int orc_batched_coloring_q(uint64_t n0, const uint64_t *row_ptr0,
+                           const uint32_t *col0, const uint32_t *weight0,
+                           const uint32_t *init, uint64_t seed,
+                           uint64_t max_batch, uint32_t max_rounds,
+                           uint32_t *c_out, uint32_t *k_out,
+                           uint32_t *rounds_out, uint32_t *outer_out,
+                           int *coarsest_out, uint32_t q)
 {
     *k_out = 0;
     *rounds_out = 0;
     *outer_out = 0;
     *coarsest_out = 1;
+    if (q == ORC_RING64 && !orc_ring_preconditions(n0, row_ptr0, weight0))
+        return 3;
     if (n0 == 0)
         return 0;
     /* current graph (owned copies) */
@@ -568,10 +676,12 @@ int orc_batched_coloring(uint64_t n0, const uint64_t *row_ptr0,
             }
             uint32_t kb = 0, rb = 0;
             uint64_t s_tb = orc_splitmix_nth(seed, (t << 32) + b + 1);
-            int st = orc_stable_coloring(n, brp, col + s, wt + s, lab, s_tb,
-                                         max_rounds, hout, &kb, &rb, NULL);
+            int st = orc_stable_coloring_q(n, brp, col + s, wt + s, lab, s_tb,
+                                           max_rounds, hout, &kb, &rb, NULL, q);
             rounds_total += rb;
-            if (st)
+            if (st == 4)
+                status = 4;
+            else if (st && status != 4)
                 status = 1;
             for (uint64_t i = 0; i < n; ++i)
                 if (owner[i] == (int64_t)b)
@@ -678,4 +788,17 @@ int orc_batched_coloring(uint64_t n0, const uint64_t *row_ptr0,
     free(wt);
     free(label);
     return status;
+}
+
+int orc_batched_coloring(uint64_t n0, const uint64_t *row_ptr0,
+                         const uint32_t *col0, const uint32_t *weight0,
+                         const uint32_t *init, uint64_t seed,
+                         uint64_t max_batch, uint32_t max_rounds,
+                         uint32_t *c_out, uint32_t *k_out,
+                         uint32_t *rounds_out, uint32_t *outer_out,
+                         int *coarsest_out)
+{
+    return orc_batched_coloring_q(n0, row_ptr0, col0, weight0, init, seed,
+                                  max_batch, max_rounds, c_out, k_out,
+                                  rounds_out, outer_out, coarsest_out, ORC_FP);
 }
