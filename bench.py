@@ -36,6 +36,10 @@ WORKLOADS = {
                          "under a 32 GiB device workspace"),
 }
 
+# Arithmetic of the image step (--arith): the prime field of the default
+# path, or the ring of Section 4.1 (Algorithm 1 with precision q = 64).
+ARITH = {"fp": (0, "F_p, p = 2^61 - 1"), "ring64": (64, "Z/2^64")}
+
 # How the out-of-core workload is refined (--batched-mode):
 #   plain        Algorithm 2 as printed (outer loop to its fixed point)
 #   exact        Algorithm 2, then the exact finish (Algorithm 1 streamed)
@@ -127,7 +131,7 @@ def bench_batched(args):
         "ms_per_step": step_s * 1e3, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "u64", "data": "synthetic",
         "config": {"workload": WORKLOADS["rmat28b"]["desc"] + ", " + BATCHED_MODES[mode],
-                   "mode": mode, "n": g.n, "nnz": g.nnz,
+                   "mode": mode, "arithmetic": ARITH[args.arith][1], "n": g.n, "nnz": g.nnz,
                    "colours": k, "rounds_summed_over_batches": rounds,
                    "outer_iterations": outer, "coarsest": coarsest,
                    "time_to_stable_ms": step_s * 1e3, "check": check},
@@ -172,7 +176,7 @@ KIND_KERNELS = {
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pb_image_rmat27_traffic.json")
 
 
-def image_roofline(work, kind_ms, rp_bytes, workload):
+def image_roofline(work, kind_ms, rp_bytes, workload, arith="fp"):
     """Roofline of the dominant image kind (largest device time per step):
     algorithmic bytes per launch (12 B per entry read: 4 B column index and
     the 8 B value of its colour; per row the row pointer and the 8 B image)
@@ -185,7 +189,7 @@ def image_roofline(work, kind_ms, rp_bytes, workload):
     avg_s = ms[kd] / 1e3 / launches
     achieved = bytes_per_launch / avg_s / 1e9 if avg_s > 0 else 0.0
     traffic = None
-    if kd == "pb" and workload == "rmat27" and os.path.exists(TRAFFIC_FILE):
+    if kd == "pb" and workload == "rmat27" and arith == "fp" and os.path.exists(TRAFFIC_FILE):
         from paper_2607_02603_amd import profsum
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -197,7 +201,7 @@ def image_roofline(work, kind_ms, rp_bytes, workload):
             "bytes_per_launch": bytes_per_launch}
 
 
-def cpu_baseline(dg, seconds_target=15.0):
+def cpu_baseline(dg, seconds_target=15.0, q=0):
     """The CPU oracle (one randomized round: image + relabel) on a bounded
     sample of the same graph: the first rows of the CSR, with a pseudo-random
     colouring of 2^20 colours.  Returns GTEPS of the sample."""
@@ -215,7 +219,7 @@ def cpu_baseline(dg, seconds_target=15.0):
         col = dg.col_idx[:m_s].cpu().numpy().view(np.uint32)
         sub_rp = rp[: rows + 1].copy()
         t0 = time.perf_counter()
-        z = oracle.image(sub_rp, col, None, colors, 1 << 20, 0, 1)
+        z = oracle.image(sub_rp, col, None, colors, 1 << 20, 0, 1, q)
         oracle.relabel(colors[:rows], z)
         dt = time.perf_counter() - t0
         best = (rows, m_s, dt)
@@ -238,6 +242,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="rmat27", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--arith", default="fp", choices=sorted(ARITH),
+                    help="arithmetic of the image step: F_p (default) or Z/2^64")
     ap.add_argument("--batched-mode", default="streamed", choices=sorted(BATCHED_MODES),
                     help="how the out-of-core workload (rmat28b) is refined")
     ap.add_argument("--verify", action="store_true",
@@ -251,10 +257,11 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
+    import paper_2607_02603_amd as wl
+    wl.wl_set_precision(ARITH[args.arith][0])
     if args.workload == "rmat28b":
         return bench_batched(args)
     import torch
-    import paper_2607_02603_amd as wl
     dev = torch.device("cuda:0")
     if args.copy_probe:
         src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
@@ -294,11 +301,11 @@ def main():
     step_s = sum(times) / len(times)
     gteps = dg.nnz * rounds / step_s / 1e9
     rp_bytes = 8 if dg.row_ptr.dtype == torch.int64 else 4
-    roofline = image_roofline(work, kind_ms, rp_bytes, args.workload)
+    roofline = image_roofline(work, kind_ms, rp_bytes, args.workload, args.arith)
     model_bytes = (12 * dg.nnz + (36 + rp_bytes) * dg.n) * rounds
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(dg)
+        cpu = cpu_baseline(dg, q=ARITH[args.arith][0])
         log(f"cpu baseline: {cpu}")
     out = {
         "metric": "GTEPS per refinement round (directed CSR entries x rounds / "
@@ -315,6 +322,7 @@ def main():
         "dtype": "u64",
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.workload]["desc"], "n": dg.n,
+                   "arithmetic": ARITH[args.arith][1],
                    "nnz": dg.nnz, "colours": k, "rounds": rounds,
                    "time_to_stable_ms": step_s * 1e3,
                    "image_ms_per_step": {kd: sum(m[kd] for m in kind_ms) / len(kind_ms)

@@ -12,10 +12,12 @@
  *     as singletons (Eq. batch-init), merge (Eq. merge), contract to the
  *     quotient graph (Definition "Quotient Graph", Eq. sc) and repeat.
  *
- * Arithmetic: exact modular arithmetic in F_p, p = 2^61 - 1.  The random
+ * Arithmetic: exact modular arithmetic in F_p, p = 2^61 - 1 (the default),
+ * or in the ring Z/2^64 of Section 4.1 (wl_set_precision).  The random
  * value of colour b in round r is W(seed, r, b): the (b+1)-th output of a
  * SplitMix64 stream whose state is mix(mix(seed + g) + (r+1) g), reduced
- * mod p (g = 0x9E3779B97F4A7C15, mix = the SplitMix64 output function).
+ * mod p in F_p and taken as it is in Z/2^64 (g = 0x9E3779B97F4A7C15, mix =
+ * the SplitMix64 output function).
  * New colour of node i = rank of the pair (c_i, z_i) among all distinct pairs
  * in lexicographic order.  Rounds repeat until the colour count does not
  * change; the round that confirms this is counted.
@@ -43,7 +45,7 @@
  *     (i, j) and (j, i) agree (compared through sums of 64-bit hashes).
  *   - Row sums of the weights must stay below p (true for every graph with
  *     uint32 weights and fewer than 2^29 entries per row, and preserved by
- *     quotients).
+ *     quotients); in Z/2^64 they must be at most 2^32 (checked).
  */
 #ifndef WL_H
 #define WL_H
@@ -57,7 +59,8 @@ extern "C" {
 #define WL_OK 0
 #define WL_EINVAL (-1)      /* malformed arguments or graph                */
 #define WL_EBUDGET (-2)     /* workspace smaller than required             */
-#define WL_EOVERFLOW (-3)   /* n >= 2^32, or a quotient weight overflowed  */
+#define WL_EOVERFLOW (-3)   /* n >= 2^32, a quotient weight overflowed, or
+                               a row sum above 2^32 in Z/2^64             */
 #define WL_EMAXROUNDS (-4)  /* round cap reached before stability          */
 #define WL_ENOTSTABLE (-5)  /* wl_verify_stable: colouring is not stable   */
 #define WL_EHIP (-6)        /* a HIP runtime call failed                   */
@@ -162,6 +165,29 @@ int wl_stable_coloring_streamed(const wl_csr *g_host, const uint32_t *init_host,
                                 uint32_t *color_out_host, uint32_t *k_out,
                                 uint32_t *rounds_out, void *workspace,
                                 uint64_t ws_bytes, void *stream);
+
+/* Arithmetic of the image z = A w for the calls that this thread makes
+ * after it (wl_refine_round, wl_stable_coloring, wl_stable_coloring_streamed,
+ * wl_stable_coloring_batched).  q is the precision parameter of Algorithm 1
+ * (Section 4.1):
+ *   WL_PRECISION_FP (0, the default): the prime field F_p, p = 2^61 - 1.
+ *   WL_PRECISION_RING64 (64): the ring R = Z/2^64, as in the paper: values,
+ *     sums and products wrap at 2^64.  The k values of a round are pairwise
+ *     distinct by construction (distinct stream positions of a bijective
+ *     output function), so Algorithm 1's resampling until |H| distinct values
+ *     never draws again.  Theorem 1 holds for n <= 2^32 and row sums at most
+ *     2^32: the calls check the row sums (on the device for device graphs,
+ *     one pass over the weights or row pointers; on the host for host
+ *     graphs) and return WL_EOVERFLOW above the bound.
+ * In both, node i's new colour is the rank of (c_i, z_i).  Both return the
+ * coarsest stable colouring with high probability (Theorem 1), so their
+ * partitions agree; the raw colour ids (ranks of different z) differ.
+ * wl_set_precision returns WL_EINVAL for another q; wl_get_precision gives
+ * the current one. */
+#define WL_PRECISION_FP 0u
+#define WL_PRECISION_RING64 64u
+int wl_set_precision(uint32_t q);
+int wl_get_precision(uint32_t *q);
 
 /* Options of wl_stable_coloring_batched.
  * WL_BATCHED_EXACT: when the contraction stops with several batches (the

@@ -31,13 +31,17 @@ _NAMES = {-1: "WL_EINVAL", -2: "WL_EBUDGET", -3: "WL_EOVERFLOW",
 EXPORTED = ["wl_workspace_size", "wl_batched_workspace_size", "wl_refine_round",
             "wl_stable_coloring", "wl_stable_coloring_batched", "wl_streamed_workspace_size",
             "wl_stable_coloring_streamed", "wl_verify_workspace_size", "wl_verify_stable",
-            "wl_stats_enable", "wl_stats_get", "wl_last_error"]
+            "wl_stats_enable", "wl_stats_get", "wl_set_precision", "wl_get_precision",
+            "wl_last_error"]
 
 WL_STATS_TIME = 1
 WL_STATS_WORK = 2
 
 WL_BATCHED_EXACT = 1
 WL_BATCHED_EARLY_STOP = 2
+
+WL_PRECISION_FP = 0
+WL_PRECISION_RING64 = 64
 
 
 class WlError(RuntimeError):
@@ -103,6 +107,8 @@ def lib():
         L.wl_verify_stable.argtypes = [P(WlCsr), vp, u32, vp, u64, vp]
         L.wl_stats_enable.argtypes = [i32]
         L.wl_stats_get.argtypes = [P(WlStats)]
+        L.wl_set_precision.argtypes = [u32]
+        L.wl_get_precision.argtypes = [P(u32)]
         L.wl_last_error.restype = ctypes.c_char_p
         for f in EXPORTED[:-1]:
             getattr(L, f).restype = i32
@@ -311,6 +317,38 @@ def wl_verify_stable(g, color, k, ws=None, stream=None):
         return False
     _check(code)
     return True
+
+
+def wl_set_precision(q):
+    """Arithmetic of the image step for this thread's later calls:
+    WL_PRECISION_FP (0, F_p with p = 2^61 - 1) or WL_PRECISION_RING64 (64,
+    the ring Z/2^64 of Algorithm 1 with q = 64)."""
+    _check(lib().wl_set_precision(q))
+
+
+def wl_get_precision():
+    out = ctypes.c_uint32(0)
+    _check(lib().wl_get_precision(ctypes.byref(out)))
+    return int(out.value)
+
+
+class precision:
+    """Context manager: ``with precision(WL_PRECISION_RING64): ...`` runs the
+    block's calls (on this thread) in that arithmetic and restores the
+    previous one."""
+
+    def __init__(self, q):
+        self.q = q
+        self.prev = None
+
+    def __enter__(self):
+        self.prev = wl_get_precision()
+        wl_set_precision(self.q)
+        return self
+
+    def __exit__(self, *exc):
+        wl_set_precision(self.prev)
+        return False
 
 
 def wl_stats_enable(flags):

@@ -126,6 +126,7 @@ struct Ctx {
   uint32_t* hcnt;            // finished chunks per heavy row
   uint32_t max_small, max_big, max_chunks, max_heavy;
   int weighted;
+  uint32_t ring;       // 0: image in F_p (p = 2^61 - 1); 1: in Z/2^64 (wl_device.h)
   int nt_stream;       // stream col_idx with non-temporal loads
   // Batch mode (Algorithm 2): the rows are nodes [ext_lo, ext_lo + n) of a
   // larger graph; a column outside that range is a node frozen as its own

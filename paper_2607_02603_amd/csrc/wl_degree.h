@@ -86,14 +86,14 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
   __shared__ uint32_t rk[kDegRanks];    // rank of sorted slot t
   __shared__ uint32_t wsum[kDegThreads / kWave];
   __shared__ uint32_t wsum2[kDegThreads / kWave];
-  const uint64_t w = color_weight(round_key(st->seed, st->round), 0);
+  const uint64_t w = color_weight(round_key(st->seed, st->round), 0, ctx.ring);
   uint32_t P = 1;
   while (P < D) P <<= 1;
   for (uint32_t t = threadIdx.x; t < P; t += kDegThreads) {
     if (t < D) {
       const uint32_t g = d.dlist[t];
       deg[t] = g;
-      key[t] = mulp(fold61(g), w);
+      key[t] = mul_int_q(g, w, ctx.ring);
     } else {
       deg[t] = 0xFFFFFFFFu;
       key[t] = ~0ull;
@@ -147,7 +147,9 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
   }
   __syncthreads();
   // per rank (at its first slot): size and liveness, summed over the slots
-  // that share it (several degrees share a rank only when w = 0)
+  // that share it (several degrees share a rank only when their values d * w
+  // coincide: when w = 0 in F_p; in Z/2^64 when 2^64 divides (d - d') w,
+  // which for degrees below 2^32 needs more than 32 trailing zero bits in w)
   {
     uint32_t cnt_loc = 0, live_loc = 0;
 #pragma unroll

@@ -1,5 +1,6 @@
 // Device-side helpers for the gfx950 kernels: arithmetic in F_p with
-// p = 2^61 - 1, the SplitMix64 weight generator, and wave64 primitives.
+// p = 2^61 - 1 or in the ring Z/2^64, the SplitMix64 weight generator, and
+// wave64 primitives.
 //
 // Method: randomized stable colouring (Algorithm 1, Section 4.1 of "Scaling
 // Weisfeiler-Leman Expressiveness Analysis to Massive Graphs with GPUs").
@@ -78,15 +79,47 @@ __device__ __forceinline__ uint64_t round_key(uint64_t seed, uint32_t r) {
   return mix64(s1 + ((uint64_t)r + 1) * kGamma);
 }
 
-// Random value of colour c: (c+1)-th output of the round's stream, mod p.
-__device__ __forceinline__ uint64_t color_weight(uint64_t key, uint32_t c) {
-  return fold61(mix64(key + ((uint64_t)c + 1) * kGamma));
+// Random value of colour c: (c+1)-th output of the round's stream, reduced
+// mod p, or taken as it is in Z/2^64 (ring != 0).  The outputs for distinct
+// c are distinct: the states key + (c+1) g differ (g is odd) and the output
+// function is a bijection of 64-bit words.
+__device__ __forceinline__ uint64_t color_weight(uint64_t key, uint32_t c, uint32_t ring) {
+  const uint64_t m = mix64(key + ((uint64_t)c + 1) * kGamma);
+  return ring ? m : fold61(m);
 }
 
 // Same stream, 64-bit colour id (ids >= 2^32 name the frozen singleton
 // classes of nodes outside a batch).
-__device__ __forceinline__ uint64_t color_weight64(uint64_t key, uint64_t c) {
-  return fold61(mix64(key + (c + 1) * kGamma));
+__device__ __forceinline__ uint64_t color_weight64(uint64_t key, uint64_t c, uint32_t ring) {
+  const uint64_t m = mix64(key + (c + 1) * kGamma);
+  return ring ? m : fold61(m);
+}
+
+// ---------------------------------------------------------------------------
+// The two arithmetics of the image z = A w.  ring == 0: F_p as above; the
+// values are canonical residues.  ring != 0: Z/2^64 (Algorithm 1 with
+// precision q = 64): values, sums and products wrap at 2^64.  An Acc96 sum
+// holds the exact sum's low 64 bits in 'lo', which is its value in Z/2^64.
+// 'ring' is the same for every thread of a launch.
+// ---------------------------------------------------------------------------
+
+// a * x for a weight a < 2^32: mod p folded to < 2^62 for x < 2^61, or mod 2^64.
+__device__ __forceinline__ uint64_t mul_small_q(uint32_t a, uint64_t x, uint32_t ring) {
+  return ring ? (uint64_t)a * x : mul_small_fold(a, x);
+}
+
+// Value of an accumulated sum: canonical residue, or the sum mod 2^64.
+__device__ __forceinline__ uint64_t acc_value(const Acc96& a, uint32_t ring) {
+  return ring ? a.lo : acc_reduce(a);
+}
+
+__device__ __forceinline__ uint64_t add_q(uint64_t a, uint64_t b, uint32_t ring) {
+  return ring ? a + b : addp(a, b);
+}
+
+// d * w for an integer d < 2^61 (a degree) and a value w.
+__device__ __forceinline__ uint64_t mul_int_q(uint64_t d, uint64_t w, uint32_t ring) {
+  return ring ? d * w : mulp(fold61(d), w);
 }
 
 // ---------------------------------------------------------------------------
@@ -96,12 +129,13 @@ __device__ __forceinline__ uint64_t color_weight64(uint64_t key, uint64_t c) {
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 template <int G>
-__device__ __forceinline__ uint64_t group_sum_p(uint64_t v) {
-  // Sum of canonical residues over aligned groups of G lanes (G | 64).
+__device__ __forceinline__ uint64_t group_sum_q(uint64_t v, uint32_t ring) {
+  // Sum over aligned groups of G lanes (G | 64) of canonical residues, or
+  // of values mod 2^64.
 #pragma unroll
   for (int off = G / 2; off > 0; off >>= 1) {
     uint64_t o = __shfl_xor(v, off, kWave);
-    v = addp(v, o);
+    v = add_q(v, o, ring);
   }
   return v;
 }

@@ -111,6 +111,30 @@ class HostPool {
   bool stop_ = false;
 };
 
+// Theorem 1's precondition for arithmetic mod 2^64: every row sum of G at
+// most 2^32 (the row length for an unweighted G).
+inline bool ring_row_sums_ok(HostPool& pool, const HostGraph& G) {
+  const unsigned T = pool.size();
+  std::vector<uint8_t> bad(T, 0);
+  pool.run([&](unsigned t) {
+    for (uint64_t i = G.n * t / T; i < G.n * (t + 1) / T; ++i) {
+      const uint64_t beg = G.rp(i), end = G.rp(i + 1);
+      uint64_t sum = end - beg;
+      if (G.wt) {
+        sum = 0;
+        for (uint64_t e = beg; e < end && sum <= (1ull << 32); ++e) sum += G.wt[e];
+      }
+      if (sum > (1ull << 32)) {
+        bad[t] = 1;
+        return;
+      }
+    }
+  });
+  for (unsigned t = 0; t < T; ++t)
+    if (bad[t]) return false;
+  return true;
+}
+
 // A cut row's share of one chunk: its segments [first, first + count) of the
 // chunk, the node, and whether z already holds the sum of earlier chunks.
 struct StreamFold {

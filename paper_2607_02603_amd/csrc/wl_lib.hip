@@ -43,6 +43,9 @@ namespace {
 thread_local char g_err[512] = "";
 thread_local int g_stats_flags = 0;
 thread_local wl_stats g_stats{};
+// Arithmetic of the image step on this thread (wl_set_precision): 0 = F_p,
+// 1 = Z/2^64.
+thread_local uint32_t g_ring = 0;
 
 int fail(int code, const char* fmt, ...) {
   va_list ap;
@@ -226,6 +229,7 @@ bool wants_pb(const wl_csr* g) {
 
 Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   Ctx c{};
+  c.ring = g_ring;
   c.n = (uint32_t)L.n;
   c.nnz = L.nnz;
   c.rp32 = g->row_ptr32;
@@ -389,6 +393,28 @@ __global__ void __launch_bounds__(kBlock) k_validate_sym(Ctx ctx) {
     }
   atomicAdd(&ctx.st->sym_hash[0], f);
   atomicAdd(&ctx.st->sym_hash[1], b);
+}
+
+// Theorem 1's precondition for Z/2^64: every row sum of A at most 2^32.  One
+// wave per row (the weights of a long row are summed by its 64 lanes); sets
+// error bit 8 on a row above the bound.
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_ring_rows(Ctx ctx) {
+  const RP* rp = rowptr<RP>(ctx);
+  const uint32_t lane = lane_id();
+  const uint64_t nw = (uint64_t)gridDim.x * (kBlock / kWave);
+  for (uint64_t i = blockIdx.x * (uint64_t)(kBlock / kWave) + threadIdx.x / kWave; i < ctx.n;
+       i += nw) {
+    const uint64_t beg = rp[i], end = rp[i + 1];
+    uint64_t sum = 0;
+    if (ctx.wgt) {
+      for (uint64_t e = beg + lane; e < end; e += kWave) sum += ctx.wgt[e];
+      for (int off = kWave / 2; off > 0; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+    } else {
+      sum = end - beg;
+    }
+    if (lane == 0 && sum > (1ull << 32)) atomicOr(&ctx.st->err, 8u);
+  }
 }
 
 __global__ void __launch_bounds__(kBlock) k_check_colors(Ctx ctx,
@@ -669,6 +695,41 @@ struct Session {
     return WL_OK;
   }
 
+  // In Z/2^64, Theorem 1's bound on the row sums (n < 2^32 holds already).
+  int check_ring() {
+    if (!ctx.ring) return WL_OK;
+    const uint32_t g = grid_for(L.n, kBlock / kWave, 4096);
+    if (rp64)
+      hipLaunchKernelGGL(k_ring_rows<uint64_t>, dim3(g), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_ring_rows<uint32_t>, dim3(g), dim3(kBlock), 0, s, ctx);
+    HIP_LAUNCH_CHECK();
+    if (int r = pull()) return r;
+    if (host.err & 8u)
+      return fail(WL_EOVERFLOW, "a row sum exceeds 2^32, the bound of arithmetic mod 2^64");
+    return WL_OK;
+  }
+
+  // The sorting networks, with the tie-aware key order in Z/2^64.
+  void tiny_sort(uint32_t grid, int check_passes) {
+    if (ctx.ring)
+      hipLaunchKernelGGL(k_tiny_sort<true>, dim3(grid), dim3(kBlock), 0, s, ctx, check_passes);
+    else
+      hipLaunchKernelGGL(k_tiny_sort<false>, dim3(grid), dim3(kBlock), 0, s, ctx, check_passes);
+  }
+  void pico_sort(uint32_t grid) {
+    if (ctx.ring)
+      hipLaunchKernelGGL(k_pico_sort<true>, dim3(grid), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_pico_sort<false>, dim3(grid), dim3(kBlock), 0, s, ctx);
+  }
+  void small_sort(uint32_t grid) {
+    if (ctx.ring)
+      hipLaunchKernelGGL(k_small_sort<true>, dim3(grid), dim3(kBlock), 0, s, ctx);
+    else
+      hipLaunchKernelGGL(k_small_sort<false>, dim3(grid), dim3(kBlock), 0, s, ctx);
+  }
+
   // SpMV schedule (row bins and heavy chunks); once per call.
   int build_schedule(bool heavy_only = false) {
     const uint32_t nb = scan_blocks(L.n);
@@ -939,15 +1000,9 @@ struct Session {
       if (int r = pull()) return r;
     }
     passes_seen = std::max(passes_seen, pass);
-    if (host.n_tiny)
-      hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(host.n_tiny, kBlock / kWave, 8192)),
-                         dim3(kBlock), 0, s, ctx, -1);
-    if (host.n_pico)
-      hipLaunchKernelGGL(k_pico_sort, dim3(grid_for(host.n_pico, kBlock / 8, 8192)),
-                         dim3(kBlock), 0, s, ctx);
-    if (host.n_small)
-      hipLaunchKernelGGL(k_small_sort, dim3(std::min<uint32_t>(host.n_small, 4096)),
-                         dim3(kBlock), 0, s, ctx);
+    if (host.n_tiny) tiny_sort(grid_for(host.n_tiny, kBlock / kWave, 8192), -1);
+    if (host.n_pico) pico_sort(grid_for(host.n_pico, kBlock / 8, 8192));
+    if (host.n_small) small_sort(std::min<uint32_t>(host.n_small, 4096));
     if (full) rank_scan();
     HIP_LAUNCH_CHECK();
     return WL_OK;
@@ -1189,12 +1244,9 @@ struct Session {
     for (int pass = 0; pass < ap; ++pass) radix_pass(pass, 1024);
     // the small sorts' grids: enough blocks to fill the device, the segments
     // taken in grid-stride loops
-    hipLaunchKernelGGL(k_tiny_sort, dim3(grid_for(L.n / 2, kBlock / kWave, 1024)),
-                       dim3(kBlock), 0, s, ctx, ap);
-    hipLaunchKernelGGL(k_pico_sort, dim3(grid_for(L.n / 2, kBlock / 8, 1024)), dim3(kBlock), 0,
-                       s, ctx);
-    hipLaunchKernelGGL(k_small_sort, dim3(grid_for(L.n / (kTinyMax + 1), 1, 1024)),
-                       dim3(kBlock), 0, s, ctx);
+    tiny_sort(grid_for(L.n / 2, kBlock / kWave, 1024), ap);
+    pico_sort(grid_for(L.n / 2, kBlock / 8, 1024));
+    small_sort(grid_for(L.n / (kTinyMax + 1), 1, 1024));
     live_tail(true);
   }
 
@@ -2419,6 +2471,21 @@ extern "C" {
 
 const char* wl_last_error(void) { return g_err; }
 
+int wl_set_precision(uint32_t q) {
+  g_err[0] = 0;
+  if (q != WL_PRECISION_FP && q != WL_PRECISION_RING64)
+    return fail(WL_EINVAL, "precision %u: use 0 (F_p) or 64 (Z/2^64)", q);
+  g_ring = q == WL_PRECISION_RING64 ? 1u : 0u;
+  return WL_OK;
+}
+
+int wl_get_precision(uint32_t* q) {
+  g_err[0] = 0;
+  if (!q) return fail(WL_EINVAL, "NULL argument");
+  *q = g_ring ? WL_PRECISION_RING64 : WL_PRECISION_FP;
+  return WL_OK;
+}
+
 int wl_stats_enable(int flags) {
   if (flags & ~(WL_STATS_TIME | WL_STATS_WORK)) return fail(WL_EINVAL, "unknown flag");
   g_stats_flags = flags;
@@ -2474,6 +2541,7 @@ int wl_refine_round(const wl_csr* g, const uint32_t* color_in, uint32_t k_in,
   if (int r = check_nnz_device(g, S.s)) return r;
   if (int r = S.init_state(seed, k_in, round, round + 1, 0)) return r;
   if (int r = S.validate_device()) return r;
+  if (int r = S.check_ring()) return r;
   const uint32_t gn = grid_for(g->n, kBlock, 4096);
   hipLaunchKernelGGL(k_check_colors, dim3(gn), dim3(kBlock), 0, S.s, S.ctx, color_in,
                      k_in);
@@ -2513,6 +2581,7 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
   const uint32_t cap = max_rounds ? max_rounds : (uint32_t)std::min<uint64_t>(g->n + 1, 0xFFFFFFFFull);
   if (int r = S.init_state(seed, 1, 0, cap, 1)) return r;
   if (int r = S.validate_device()) return r;
+  if (int r = S.check_ring()) return r;
   if (int r = S.stats_begin()) return r;
   if (int r = S.run_rsc(init_color)) return r;
   if (int r = S.stats_end()) return r;
@@ -2548,6 +2617,19 @@ int wl_stable_coloring_batched(const wl_csr* g_host, const uint32_t* init_host,
   if (last != g_host->nnz) return fail(WL_EINVAL, "row_ptr[n] != nnz");
   if (options & ~(WL_BATCHED_EXACT | WL_BATCHED_EARLY_STOP))
     return fail(WL_EINVAL, "unknown option bits 0x%x", options);
+  if (g_ring) {
+    // a quotient row sums the entries of its representative's row, so the
+    // input's bound holds for every quotient
+    HostGraph G;
+    G.n = g_host->n;
+    G.m = g_host->nnz;
+    G.rp32 = g_host->row_ptr32;
+    G.rp64 = g_host->row_ptr64;
+    G.wt = g_host->weight;
+    HostPool pool;
+    if (!ring_row_sums_ok(pool, G))
+      return fail(WL_EOVERFLOW, "a row sum exceeds 2^32, the bound of arithmetic mod 2^64");
+  }
   return batched_run(g_host, init_host, seed, max_batch_entries, options, color_out_host, k_out,
                      rounds_out, outer_out, coarsest_out, workspace, ws_bytes,
                      (hipStream_t)stream);
@@ -2589,6 +2671,11 @@ int wl_stable_coloring_streamed(const wl_csr* g_host, const uint32_t* init_host,
   for (uint64_t i = 0; i < G.n; ++i)
     if (G.rp(i + 1) < G.rp(i)) return fail(WL_EINVAL, "row_ptr is not non-decreasing");
   if (G.m > 0 && !G.col) return fail(WL_EINVAL, "col_idx is NULL");
+  if (g_ring) {
+    HostPool pool;
+    if (!ring_row_sums_ok(pool, G))
+      return fail(WL_EOVERFLOW, "a row sum exceeds 2^32, the bound of arithmetic mod 2^64");
+  }
   int done = 0;
   if (int r = streamed_run(G, init_host, seed, max_rounds, (uint8_t*)workspace, ws_bytes,
                            (hipStream_t)stream, color_out_host, k_out, rounds_out, &done))

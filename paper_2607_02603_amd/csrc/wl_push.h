@@ -489,9 +489,9 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
 // Pass 3: records of a fine bin -> z
 // ---------------------------------------------------------------------------
 
-// value = acc + carries * 2^64 (mod p); 2^64 = 8 (mod p)
-__device__ __forceinline__ uint64_t pb_reduce(uint64_t acc, uint32_t carries) {
-  return addp(fold61(acc), fold61((uint64_t)carries << 3));
+// value = acc + carries * 2^64: mod p (2^64 = 8 mod p), or acc in Z/2^64
+__device__ __forceinline__ uint64_t pb_reduce(uint64_t acc, uint32_t carries, uint32_t ring) {
+  return ring ? acc : addp(fold61(acc), fold61((uint64_t)carries << 3));
 }
 
 // TBL: the k colour values sit in LDS (k <= kPbTableMax), else each record's
@@ -499,10 +499,13 @@ __device__ __forceinline__ uint64_t pb_reduce(uint64_t acc, uint32_t carries) {
 constexpr uint32_t kPbTableMax = 4096;
 
 // Per row an exact sum: a 64-bit accumulator (one atomic per record, whose
-// returned old value shows a wrap past 2^64) and a count of such wraps.
+// returned old value shows a wrap past 2^64) and a count of such wraps.  In
+// Z/2^64 the wraps are dropped (the accumulator is the sum mod 2^64).
 __device__ __forceinline__ void pb_acc_add(unsigned long long* acc, uint32_t* wraps,
-                                           uint32_t r, uint64_t v, uint32_t extra) {
+                                           uint32_t r, uint64_t v, uint32_t extra,
+                                           uint32_t ring) {
   const unsigned long long old = atomicAdd(&acc[r], (unsigned long long)v);
+  if (ring) return;
   const uint32_t w = extra + (old + v < old ? 1u : 0u);
   if (w) atomicAdd(&wraps[r], w);
 }
@@ -519,7 +522,8 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
   const uint32_t nitems = pb.cnt->nslices;
   if (TBL) {
     const uint32_t k = ctx.st->k;
-    for (uint32_t b = threadIdx.x; b < k; b += kPbAccThreads) wtab[b] = color_weight(key, b);
+    for (uint32_t b = threadIdx.x; b < k; b += kPbAccThreads)
+      wtab[b] = color_weight(key, b, ctx.ring);
   }
   for (uint32_t t = blockIdx.x; t < nitems; t += gridDim.x) {
     uint32_t lo = 0, hi = pb.nfine - 1;  // fine bin: last f with slice_off[f] <= t
@@ -562,7 +566,8 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
         const bool ok = p0 + u * kPbAccThreads + threadIdx.x < e;
         const uint32_t local = (rv[u] >> pb.cbits) & (kPbFineRows - 1);
         const uint64_t w =
-            ok ? (TBL ? wtab[rv[u] & cmask] : color_weight(key, rv[u] & cmask)) : 0ull;
+            ok ? (TBL ? wtab[rv[u] & cmask] : color_weight(key, rv[u] & cmask, ctx.ring))
+               : 0ull;
         const uint32_t l0 = __shfl(local, 0, kWave);
         if (__all(!ok || local == l0)) {
           // the whole wave feeds one row (rows of high degree): add the 64
@@ -577,10 +582,10 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
             // sl + sh2 * 2^32 as (64-bit part, multiples of 2^64)
             const uint64_t v = sl + (sh2 << 32);
             const uint32_t hi64 = (uint32_t)(sh2 >> 32) + (v < sl ? 1u : 0u);
-            pb_acc_add(acc, wraps, l0, v, hi64);
+            pb_acc_add(acc, wraps, l0, v, hi64, ctx.ring);
           }
         } else if (ok) {
-          pb_acc_add(acc, wraps, local, w, 0);
+          pb_acc_add(acc, wraps, local, w, 0, ctx.ring);
         }
       }
     }
@@ -589,11 +594,11 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
     const uint32_t nrows = (uint32_t)min((uint64_t)kPbFineRows, (uint64_t)ctx.n - row0);
     if (ns == 1) {
       for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
-        ctx.z[row0 + r] = pb_reduce(acc[r], wraps[r]);
+        ctx.z[row0 + r] = pb_reduce(acc[r], wraps[r], ctx.ring);
     } else {
       uint64_t* part = pb.part + (uint64_t)(pb.mslice_off[f] + q) * kPbFineRows;
       for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
-        part[r] = pb_reduce(acc[r], wraps[r]);
+        part[r] = pb_reduce(acc[r], wraps[r], ctx.ring);
     }
     __syncthreads();
   }
@@ -612,7 +617,8 @@ __global__ void __launch_bounds__(kBlock) k_pb_combine(Ctx ctx, PbCtx pb) {
     if (row >= ctx.n) continue;
     const uint32_t s0 = pb.mslice_off[f], s1 = pb.mslice_off[f + 1];
     uint64_t z = 0;
-    for (uint32_t s = s0; s < s1; ++s) z = addp(z, pb.part[(uint64_t)s * kPbFineRows + r]);
+    for (uint32_t s = s0; s < s1; ++s)
+      z = add_q(z, pb.part[(uint64_t)s * kPbFineRows + r], ctx.ring);
     ctx.z[row] = z;
   }
 }

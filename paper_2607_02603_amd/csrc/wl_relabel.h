@@ -25,8 +25,10 @@ namespace wl {
 // its radix passes (k_resume clears it).
 constexpr uint32_t kHalted = 3;
 
-__device__ __forceinline__ uint32_t digit_of(uint64_t key, int pass) {
-  const int hi = 61 - kRadixBits * pass;
+// Digit of a radix pass: 8-bit digits from the top of the key (61-bit
+// residues of F_p, or 64-bit values of Z/2^64), the last one shorter for F_p.
+__device__ __forceinline__ uint32_t digit_of(uint64_t key, int pass, uint32_t ring) {
+  const int hi = (ring ? 64 : 61) - kRadixBits * pass;
   const int lo = hi > kRadixBits ? hi - kRadixBits : 0;
   return (uint32_t)((key >> lo) & ((1ull << (hi - lo)) - 1));
 }
@@ -204,7 +206,7 @@ __global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
     unsigned long long rmn = ~0ull, rmx = 0;
     for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
       const uint64_t key = ctx.keys[p];
-      const uint32_t d = digit_of(key, pass);
+      const uint32_t d = digit_of(key, pass, ctx.ring);
       if (d != rd) {
         if (rc) {
           atomicAdd(&cnt[rd], rc);
@@ -309,7 +311,7 @@ __global__ void __launch_bounds__(kBlock) k_big_scatter(Ctx ctx, int pass) {
     for (uint32_t q = 0; q < kTilePerThread; ++q) {
       const uint32_t p = r.beg + q * kBlock + threadIdx.x;
       if (p < r.end) {
-        dg[q] = digit_of(ctx.keys[p], pass);
+        dg[q] = digit_of(ctx.keys[p], pass, ctx.ring);
         slot[q] = atomicAdd(&lcnt[dg[q]], 1u);
       }
     }
@@ -346,8 +348,20 @@ __global__ void __launch_bounds__(kBlock) k_big_copyback(Ctx ctx, int pass) {
   }
 }
 
+// Order of the sorting networks below.  Padding slots carry the largest key
+// ~0 and node 0xFFFFFFFF (no node has that id).  In F_p no key reaches ~0,
+// so keys alone decide (TIE = false).  In Z/2^64 a key may equal ~0: then
+// (key, node) pairs are compared (TIE = true), which keeps every padding slot
+// behind every node.
+template <bool TIE>
+__device__ __forceinline__ bool key_less(unsigned long long a, uint32_t va,
+                                         unsigned long long b, uint32_t vb) {
+  return a < b || (TIE && a == b && va < vb);
+}
+
 // One workgroup per small segment: bitonic sort of (z, node) in LDS, then
 // flags where z changes.
+template <bool TIE>
 __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
@@ -367,7 +381,7 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
         sval[t] = v;
         skey[t] = mat ? ctx.keys[s + t] : ctx.z[v];
       } else {
-        sval[t] = 0;
+        sval[t] = 0xFFFFFFFFu;
         skey[t] = ~0ull;
       }
     }
@@ -386,7 +400,7 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
           if (l > i) {
             const bool asc = (i & kk) == 0;
             const unsigned long long a = skey[i], b = skey[l];
-            if ((a > b) == asc) {
+            if (key_less<TIE>(b, sval[l], a, sval[i]) == asc) {
               skey[i] = b;
               skey[l] = a;
               const uint32_t tv = sval[i];
@@ -414,6 +428,7 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
 // are left after that many radix passes; the blocks that still run sort
 // their segments, which the host-driven completion sorts again (a sort of
 // sorted keys changes nothing).
+template <bool TIE>
 __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes) {
   DevState* st = ctx.st;
   if (st->done) return;
@@ -429,7 +444,7 @@ __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes)
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
     const bool mat = (sg.y & kMatBit) != 0;
     unsigned long long key = ~0ull;
-    uint32_t v = 0;
+    uint32_t v = 0xFFFFFFFFu;
     if (lane < len) {
       v = ctx.perm[s + lane];
       key = mat ? ctx.keys[s + lane] : ctx.z[v];
@@ -444,7 +459,8 @@ __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes)
         const uint32_t pv = __shfl_xor(v, (int)j, kWave);
         const bool up = (lane & kk) == 0;
         const bool lower = (lane & j) == 0;
-        const bool take = (lower == up) ? (pk < key) : (pk > key);
+        const bool take =
+            (lower == up) ? key_less<TIE>(pk, pv, key, v) : key_less<TIE>(key, v, pk, pv);
         if (take) {
           key = pk;
           v = pv;
@@ -463,6 +479,7 @@ __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes)
 // Segments of at most kPicoMax nodes, listed from the back of the tiny
 // list: eight per wave, eight lanes each, with the tiny sort's bitonic
 // network cut to eight elements.  Skipped when all keys of a segment agree.
+template <bool TIE>
 __global__ void __launch_bounds__(kBlock) k_pico_sort(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
@@ -482,7 +499,7 @@ __global__ void __launch_bounds__(kBlock) k_pico_sort(Ctx ctx) {
       mat = (sg.y & kMatBit) != 0;
     }
     unsigned long long key = ~0ull;
-    uint32_t v = 0;
+    uint32_t v = 0xFFFFFFFFu;
     if (sub < len) {
       v = ctx.perm[s + sub];
       key = mat ? ctx.keys[s + sub] : ctx.z[v];
@@ -498,7 +515,8 @@ __global__ void __launch_bounds__(kBlock) k_pico_sort(Ctx ctx) {
         const uint32_t pv = __shfl_xor(v, (int)j, kWave);
         const bool up = (sub & kk) == 0;
         const bool lower = (sub & j) == 0;
-        const bool take = (lower == up) ? (pk < key) : (pk > key);
+        const bool take =
+            (lower == up) ? key_less<TIE>(pk, pv, key, v) : key_less<TIE>(key, v, pk, pv);
         if (take) {
           key = pk;
           v = pv;

@@ -207,12 +207,12 @@ __device__ __forceinline__ uint64_t gather_value(const Ctx& ctx, uint32_t j,
                                                  uint64_t rkey) {
   if (ctx.batch) {
     const uint32_t jl = j - ctx.ext_lo;
-    if (jl >= ctx.n) return color_weight64(rkey, (1ull << 32) + j);
+    if (jl >= ctx.n) return color_weight64(rkey, (1ull << 32) + j, ctx.ring);
     j = jl;
   }
   if (M == kGather16) return ctx.wtab[ctx.c16[j]];
   if (M == kGather8) return ctx.wtab[ctx.c8[j]];
-  return color_weight(rkey, ctx.c[j]);
+  return color_weight(rkey, ctx.c[j], ctx.ring);
 }
 
 template <int U, bool W, int M>
@@ -232,7 +232,7 @@ __device__ __forceinline__ void accumulate(const Ctx& ctx, Acc96& a, uint64_t e0
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     v[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
-    if (W && ok[u]) v[u] = mul_small_fold(ctx.wgt[e0 + (uint64_t)u * stride], v[u]);
+    if (W && ok[u]) v[u] = mul_small_q(ctx.wgt[e0 + (uint64_t)u * stride], v[u], ctx.ring);
   }
 #pragma unroll
   for (int u = 0; u < U; ++u) acc_add(a, v[u]);
@@ -254,7 +254,7 @@ __device__ __forceinline__ void spmv_rows(const Ctx& ctx, int bin, uint32_t bid,
     Acc96 a{0, 0};
     for (uint64_t e0 = beg + sub; e0 < end; e0 += (uint64_t)G * U)
       accumulate<U, W, M>(ctx, a, e0, end, G, rkey);
-    const uint64_t r = group_sum_p<G>(acc_reduce(a));
+    const uint64_t r = group_sum_q<G>(acc_value(a, ctx.ring), ctx.ring);
     if (sub == 0) ctx.z[row] = r;
   }
 }
@@ -273,10 +273,10 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
     const uint64_t end = ch.beg + ch.len;
     for (uint64_t e0 = ch.beg + lane; e0 < end; e0 += (uint64_t)kWave * 4)
       accumulate<4, W, M>(ctx, a, e0, end, kWave, rkey);
-    const uint64_t r = group_sum_p<kWave>(acc_reduce(a));
+    const uint64_t r = group_sum_q<kWave>(acc_value(a, ctx.ring), ctx.ring);
     if (lane == 0) {
       // Partial sums of the row's chunks meet in two 64-bit accumulators
-      // (low and high 32-bit halves of canonical residues); the chunk that
+      // (low and high 32-bit halves of the chunk values); the chunk that
       // finishes last folds them into z and resets them for the next round.
       atomicAdd(&ctx.hacc[2 * ch.h], (unsigned long long)(r & 0xFFFFFFFFull));
       atomicAdd(&ctx.hacc[2 * ch.h + 1], (unsigned long long)(r >> 32));
@@ -285,11 +285,16 @@ __device__ __forceinline__ void spmv_heavy(const Ctx& ctx, uint32_t bid,
       if (seen == ch.nc - 1) {
         __threadfence();
         const uint64_t lo = atomicExch(&ctx.hacc[2 * ch.h], 0ull);
-        const uint64_t hi = fold61(atomicExch(&ctx.hacc[2 * ch.h + 1], 0ull));
+        const uint64_t hs = atomicExch(&ctx.hacc[2 * ch.h + 1], 0ull);
         atomicExch(&ctx.hcnt[ch.h], 0u);
-        // hi * 2^32 = (hi mod 2^29) * 2^32 + (hi >> 29) * 2^61, 2^61 = 1.
-        const uint64_t t2 = ((hi & 0x1FFFFFFFull) << 32) + (hi >> 29);
-        ctx.z[ch.row] = addp(fold61(t2), fold61(lo));
+        if (ctx.ring) {
+          ctx.z[ch.row] = lo + (hs << 32);  // mod 2^64
+        } else {
+          // hi * 2^32 = (hi mod 2^29) * 2^32 + (hi >> 29) * 2^61, 2^61 = 1.
+          const uint64_t hi = fold61(hs);
+          const uint64_t t2 = ((hi & 0x1FFFFFFFull) << 32) + (hi >> 29);
+          ctx.z[ch.row] = addp(fold61(t2), fold61(lo));
+        }
       }
     }
   }
@@ -361,12 +366,12 @@ __device__ __forceinline__ void spmv_q_body(const Ctx& ctx) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           v[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
-          if (W && ok[u]) v[u] = mul_small_fold(ctx.wgt[beg + t0 + u], v[u]);
+          if (W && ok[u]) v[u] = mul_small_q(ctx.wgt[beg + t0 + u], v[u], ctx.ring);
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) acc_add(a, v[u]);
       }
-      ctx.keys[q] = acc_reduce(a);
+      ctx.keys[q] = acc_value(a, ctx.ring);
     }
   }
 }
@@ -402,7 +407,7 @@ __device__ __forceinline__ void spmv_mid_body(const Ctx& ctx, uint32_t heavy) {
     Acc96 a{0, 0};
     for (uint64_t e0 = beg + lane; e0 < end; e0 += (uint64_t)kWave * 4)
       accumulate<4, W, M>(ctx, a, e0, end, kWave, rkey);
-    const uint64_t r = group_sum_p<kWave>(acc_reduce(a));
+    const uint64_t r = group_sum_q<kWave>(acc_value(a, ctx.ring), ctx.ring);
     if (lane == 0) ctx.keys[q] = r;
   }
 }
@@ -484,15 +489,15 @@ __global__ void __launch_bounds__(kBlock) k_live_count(Ctx ctx, int work) {
 }
 
 // One colour and unit weights: every x_j is the same w, so
-// z_i = deg_i * w (mod p) exactly, without touching col_idx.
+// z_i = deg_i * w exactly, without touching col_idx.
 template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_spmv_uniform(Ctx ctx) {
   if (ctx.st->done) return;
   const RP* rp = rowptr<RP>(ctx);
-  const uint64_t w0 = color_weight(round_key(ctx.st->seed, ctx.st->round), 0);
+  const uint64_t w0 = color_weight(round_key(ctx.st->seed, ctx.st->round), 0, ctx.ring);
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
        i += gridDim.x * kBlock)
-    ctx.z[i] = mulp(fold61(rp[i + 1] - rp[i]), w0);
+    ctx.z[i] = mul_int_q(rp[i + 1] - rp[i], w0, ctx.ring);
 }
 
 // Per-round random values for the gather: compact colour array plus the
@@ -504,7 +509,7 @@ __device__ __forceinline__ void gather_prep_body(const Ctx& ctx, int mode, uint3
   const uint32_t tid = blockIdx.x * kBlock + threadIdx.x;
   const uint32_t stride = gridDim.x * kBlock;
   if (mode == kGatherC) return;
-  for (uint32_t b = tid; b < k; b += stride) ctx.wtab[b] = color_weight(key, b);
+  for (uint32_t b = tid; b < k; b += stride) ctx.wtab[b] = color_weight(key, b, ctx.ring);
   if (mode == kGather16)
     for (uint32_t i = tid; i < ctx.n; i += stride) ctx.c16[i] = (uint16_t)ctx.c[i];
   else

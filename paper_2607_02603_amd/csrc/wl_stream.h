@@ -45,12 +45,12 @@ __device__ __forceinline__ void stream_seg_body(const Ctx& ctx, const StreamChun
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         v[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
-        if (W && ok[u]) v[u] = mul_small_fold(ch.wt[e0 + (uint64_t)u * kWave], v[u]);
+        if (W && ok[u]) v[u] = mul_small_q(ch.wt[e0 + (uint64_t)u * kWave], v[u], ctx.ring);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) acc_add(a, v[u]);
     }
-    const uint64_t r = group_sum_p<kWave>(acc_reduce(a));
+    const uint64_t r = group_sum_q<kWave>(acc_value(a, ctx.ring), ctx.ring);
     if (lane == 0) {
       const uint32_t nd = ch.node[t];
       if (nd & kSegPartial)
@@ -80,7 +80,7 @@ __global__ void __launch_bounds__(kBlock) k_stream_fold(Ctx ctx, StreamChunk ch)
   for (uint32_t f = blockIdx.x * kBlock + threadIdx.x; f < ch.nfold; f += gridDim.x * kBlock) {
     const StreamFold d = ch.fold[f];
     uint64_t s = d.add ? ctx.z[d.node] : 0ull;
-    for (uint32_t t = 0; t < d.count; ++t) s = addp(s, ch.part[d.first + t]);
+    for (uint32_t t = 0; t < d.count; ++t) s = add_q(s, ch.part[d.first + t], ctx.ring);
     ctx.z[d.node] = s;
   }
 }
@@ -88,9 +88,9 @@ __global__ void __launch_bounds__(kBlock) k_stream_fold(Ctx ctx, StreamChunk ch)
 // One colour, unit weights: z_i = deg_i * w without the entries.
 __global__ void __launch_bounds__(kBlock) k_stream_uniform(Ctx ctx, const uint32_t* deg) {
   if (ctx.st->done) return;
-  const uint64_t w0 = color_weight(round_key(ctx.st->seed, ctx.st->round), 0);
+  const uint64_t w0 = color_weight(round_key(ctx.st->seed, ctx.st->round), 0, ctx.ring);
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n; i += gridDim.x * kBlock)
-    ctx.z[i] = mulp(fold61(deg[i]), w0);
+    ctx.z[i] = mul_int_q(deg[i], w0, ctx.ring);
 }
 
 __global__ void __launch_bounds__(kBlock) k_zero_u64(uint64_t* p, uint64_t n) {

@@ -134,3 +134,22 @@ def test_binding_refuses_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(wl, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         wl.lib()
+
+
+def test_precision_setter_is_per_thread_and_checked():
+    # host-only calls: no device is touched
+    import threading
+    assert wl.wl_get_precision() == wl.WL_PRECISION_FP
+    with wl.precision(wl.WL_PRECISION_RING64):
+        assert wl.wl_get_precision() == 64
+        seen = []
+        t = threading.Thread(target=lambda: seen.append(wl.wl_get_precision()))
+        t.start()
+        t.join()
+        assert seen == [wl.WL_PRECISION_FP]  # another thread keeps its own
+    assert wl.wl_get_precision() == wl.WL_PRECISION_FP
+    for bad in (1, 32, 63, 65, 128):
+        with pytest.raises(wl.WlError) as e:
+            wl.wl_set_precision(bad)
+        assert e.value.code == wl.WL_EINVAL
+    assert wl.wl_get_precision() == wl.WL_PRECISION_FP

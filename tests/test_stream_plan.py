@@ -39,3 +39,14 @@ def test_stream_packing(checker, args):
     print(r.stdout, r.stderr)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "bad=0" in r.stdout
+
+
+def test_ring_row_sum_bound(tmp_path):
+    # Theorem 1's bound for arithmetic mod 2^64 as checked on the host paths
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not available")
+    out = str(tmp_path / "ring_rows_check")
+    src = os.path.join(HERE, "host", "ring_rows_check.cpp")
+    subprocess.run(["g++", "-std=c++17", "-O1", "-pthread", src, "-o", out], check=True)
+    r = subprocess.run([out], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stdout + r.stderr
