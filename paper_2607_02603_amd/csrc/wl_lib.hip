@@ -396,24 +396,43 @@ __global__ void __launch_bounds__(kBlock) k_validate_sym(Ctx ctx) {
 }
 
 // Theorem 1's precondition for Z/2^64: every row sum of A at most 2^32.  One
-// wave per row (the weights of a long row are summed by its 64 lanes); sets
-// error bit 8 on a row above the bound.
+// thread per row (its length, or the sum of at most 64 weights); the rows
+// with more weights are summed by all 64 lanes of the wave, one after the
+// other.  Sets error bit 8 on a row above the bound.
 template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_ring_rows(Ctx ctx) {
   const RP* rp = rowptr<RP>(ctx);
   const uint32_t lane = lane_id();
-  const uint64_t nw = (uint64_t)gridDim.x * (kBlock / kWave);
-  for (uint64_t i = blockIdx.x * (uint64_t)(kBlock / kWave) + threadIdx.x / kWave; i < ctx.n;
-       i += nw) {
-    const uint64_t beg = rp[i], end = rp[i + 1];
-    uint64_t sum = 0;
-    if (ctx.wgt) {
-      for (uint64_t e = beg + lane; e < end; e += kWave) sum += ctx.wgt[e];
-      for (int off = kWave / 2; off > 0; off >>= 1) sum += __shfl_xor(sum, off, kWave);
-    } else {
-      sum = end - beg;
+  const uint64_t lim = 1ull << 32;
+  // 'base' is the same for all lanes of a wave, so every lane runs every
+  // iteration (the shuffles below need the whole wave)
+  for (uint64_t base = blockIdx.x * (uint64_t)kBlock + threadIdx.x - lane; base < ctx.n;
+       base += (uint64_t)gridDim.x * kBlock) {
+    const uint64_t i = base + lane;
+    uint64_t beg = 0, end = 0;
+    if (i < ctx.n) {
+      beg = rp[i];
+      end = rp[i + 1];
     }
-    if (lane == 0 && sum > (1ull << 32)) atomicOr(&ctx.st->err, 8u);
+    bool over = false, wide = false;
+    if (!ctx.wgt) {
+      over = end - beg > lim;
+    } else if (end - beg <= (uint64_t)kWave) {
+      uint64_t sum = 0;
+      for (uint64_t e = beg; e < end; ++e) sum += ctx.wgt[e];
+      over = sum > lim;
+    } else {
+      wide = true;
+    }
+    for (uint64_t m = __ballot(wide); m; m &= m - 1) {
+      const int l = __builtin_ctzll(m);
+      const uint64_t b = __shfl(beg, l, kWave), e = __shfl(end, l, kWave);
+      uint64_t sum = 0;
+      for (uint64_t x = b + lane; x < e; x += kWave) sum += ctx.wgt[x];
+      for (int off = kWave / 2; off > 0; off >>= 1) sum += __shfl_xor(sum, off, kWave);
+      if (sum > lim) over = true;
+    }
+    if (over) atomicOr(&ctx.st->err, 8u);
   }
 }
 
@@ -698,7 +717,7 @@ struct Session {
   // In Z/2^64, Theorem 1's bound on the row sums (n < 2^32 holds already).
   int check_ring() {
     if (!ctx.ring) return WL_OK;
-    const uint32_t g = grid_for(L.n, kBlock / kWave, 4096);
+    const uint32_t g = grid_for(L.n, kBlock, 4096);
     if (rp64)
       hipLaunchKernelGGL(k_ring_rows<uint64_t>, dim3(g), dim3(kBlock), 0, s, ctx);
     else

@@ -334,6 +334,18 @@ def test_row_sum_bound_every_path():
     with pytest.raises(wl.WlError) as e:
         wl.wl_stable_coloring_batched(_host_graph(rp, col, bad), None, 0, 2)
     assert e.value.code == wl.WL_EOVERFLOW
+    # a row of 100 weights (summed by a whole wave) at and above the bound
+    n = 101
+    rp = np.array([0, 100] + [100] * (n - 1), np.uint64)
+    col = np.arange(1, 101, dtype=np.uint32)
+    wide = np.full(100, 1 << 25, np.uint32)
+    wide[0] = (1 << 32) - 99 * (1 << 25)
+    assert int(wide.astype(np.uint64).sum()) == 1 << 32
+    _exact(rp, col, wide, classic=False)
+    wide[1] += 1
+    with pytest.raises(wl.WlError) as e:
+        wl.wl_stable_coloring(_dev_graph(rp, col, wide), None, 0)
+    assert e.value.code == wl.WL_EOVERFLOW
     # F_p has no such bound
     with wl.precision(wl.WL_PRECISION_FP):
         c, k, r = wl.wl_stable_coloring(_dev_graph(rp, col, bad), None, 0)
