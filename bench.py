@@ -140,6 +140,72 @@ def bench_batched(args):
     print(json.dumps(out), flush=True)
 
 
+STUDY_GRAPHS = {
+    "rmat20": "R-MAT scale 20, edge factor 16, undirected (social-like)",
+    "rmat20dir": "R-MAT scale 20, edge factor 16, directed (web-like: skewed out- and "
+                 "in-degrees, many nodes without out-edges)",
+    "chunglu1m": "Chung-Lu n=1e6, 16e6 sampled pairs, exponent 2.1, undirected",
+    "rmat22": "R-MAT scale 22, edge factor 16, undirected",
+}
+
+
+def study_reduction(args):
+    """Reduction quality of Algorithm 2 (Section 5, Table 1's layout) on
+    synthetic graphs: colours as a fraction of n for N_b = 1, 2, 4 batches
+    (cap M_b = ceil(m / N_b)), with the outer loop run to its fixed point
+    and with the early stop of Section 5.4, against the coarsest colouring
+    (Algorithm 1 in core).  Prints one JSON line with a row per run."""
+    import numpy as np
+    import torch
+    import paper_2607_02603_amd as wl
+    from paper_2607_02603_amd import inputs
+    dev = torch.device("cuda:0")
+    gens = {
+        "rmat20": lambda: inputs.rmat(20, 16),
+        "rmat20dir": lambda: inputs.rmat(20, 16, directed=True),
+        "chunglu1m": lambda: inputs.chung_lu(1_000_000, 16_000_000),
+        "rmat22": lambda: inputs.rmat(22, 16),
+    }
+    rows = []
+    for name, gen in gens.items():
+        t0 = time.perf_counter()
+        g = gen()
+        rp = np.asarray(g.row_ptr, np.uint64)
+        hg = wl.Graph.from_numpy(g.n, rp, g.col, None, device=None)
+        hg = wl.Graph(g.n, hg.row_ptr.pin_memory(), hg.col_idx.pin_memory(), None)
+        dg = wl.Graph.from_numpy(g.n, rp, g.col, None, device=dev)
+        log(f"{name}: n={g.n} nnz={g.nnz} built in {time.perf_counter() - t0:.1f}s")
+        _, k_star, r_star = wl.wl_stable_coloring(dg, None, 0)
+        torch.cuda.synchronize()
+        del dg
+        for nb in (1, 2, 4):
+            mb = -(-g.nnz // nb)
+            for mode, opt in (("fixed point", 0), ("early stop", wl.WL_BATCHED_EARLY_STOP)):
+                if nb == 1 and opt:
+                    continue
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                _, k, r, outer, coarsest = wl.wl_stable_coloring_batched(hg, None, 0, mb,
+                                                                         options=opt)
+                torch.cuda.synchronize()
+                dt = time.perf_counter() - t1
+                row = {"graph": STUDY_GRAPHS[name], "n": g.n, "nnz": g.nnz, "N_b": nb,
+                       "M_b": mb, "outer_loop": mode, "colours": k,
+                       "colours_pct_of_n": 100.0 * k / g.n,
+                       "coarsest_colours": k_star,
+                       "excess_pct_over_coarsest": 100.0 * (k - k_star) / k_star,
+                       "outer_iterations": outer, "rounds": r, "coarsest": coarsest,
+                       "seconds": dt}
+                rows.append(row)
+                log(f"  N_b={nb} {mode:11s}: colours {k} ({row['colours_pct_of_n']:.2f}% of n,"
+                    f" +{row['excess_pct_over_coarsest']:.3f}% over {k_star}), outer {outer},"
+                    f" coarsest {coarsest}, {dt:.2f}s")
+        del hg, g
+    print(json.dumps({"study": "reduction quality of Algorithm 2 on synthetic graphs",
+                      "arithmetic": ARITH[args.arith][1], "seed": 0, "rows": rows}),
+          flush=True)
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -248,6 +314,9 @@ def main():
                     help="how the out-of-core workload (rmat28b) is refined")
     ap.add_argument("--verify", action="store_true",
                     help="rmat28b: also run the in-core colouring and compare")
+    ap.add_argument("--study", choices=["reduction"],
+                    help="instead of the benchmark: the reduction-quality study of "
+                         "Algorithm 2 (N_b = 1, 2, 4) on synthetic graphs")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 1 GiB device-to-device (a plain copy kernel of "
                          "known size, to calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -259,6 +328,8 @@ def main():
 
     import paper_2607_02603_amd as wl
     wl.wl_set_precision(ARITH[args.arith][0])
+    if args.study == "reduction":
+        return study_reduction(args)
     if args.workload == "rmat28b":
         return bench_batched(args)
     import torch

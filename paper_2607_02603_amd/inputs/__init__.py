@@ -220,20 +220,26 @@ def rmat_thresholds(abcd):
 
 
 def rmat(scale=27, edge_factor=16, abcd=(0.57, 0.19, 0.19, 0.05), seed=0,
-         device="cpu", host_out=False):
+         device="cpu", host_out=False, directed=False):
     """R-MAT, edge_factor * 2^scale samples, seeded vertex bijection, self-loops
     dropped, symmetrised, deduplicated.  device='cuda' generates on the GPU;
     with host_out=True the CSR is returned in pinned host memory and the
     device never holds more than a group of buckets (for graphs larger than
-    HBM)."""
+    HBM).  directed=True (host generation only) keeps each sample as the one
+    entry u -> v, as for a web graph: out- and in-degrees are both skewed and
+    many nodes have no out-edge."""
     n = 1 << scale
     samples = edge_factor * n
     ta, tab, tabc = rmat_thresholds(abcd)
-    name = f"rmat_s{scale}_ef{edge_factor}_s{seed}"
+    name = f"rmat_s{scale}_ef{edge_factor}_s{seed}" + ("_dir" if directed else "")
     if device == "cpu":
         keys = np.empty(2 * samples, dtype=np.uint64)
         _cpu().gen_rmat_keys_cpu(scale, 0, samples, seed, ta, tab, tabc, _ptr(keys))
+        if directed:
+            keys = keys[0::2]  # the entry u -> v of every sample (see gen_cpu.c)
         return csr_from_keys(keys, n, name)
+    if directed:
+        raise ValueError("directed R-MAT is generated on the host only")
 
     def emit(phase, shift, nbk, blo, bhi, arr, keys, stream):
         return _gpu().gen_rmat_gpu(phase, scale, seed, ta, tab, tabc, 0, samples, shift,

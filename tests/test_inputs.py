@@ -85,3 +85,21 @@ def test_alias_table_probabilities():
     est = q.copy()
     np.add.at(est, alias, (1.0 / n) - q)
     assert np.allclose(est, p, atol=1e-9)
+
+
+def test_rmat_directed_is_the_forward_half():
+    # the directed graph holds one entry u -> v per sample; its symmetrisation
+    # is the undirected R-MAT of the same seed
+    gd = inputs.rmat(10, 8, seed=3, directed=True)
+    gu = inputs.rmat(10, 8, seed=3)
+    rp = np.asarray(gd.row_ptr, np.int64)
+    u = np.repeat(np.arange(gd.n), np.diff(rp))
+    v = gd.col.astype(np.int64)
+    assert np.all(u != v)
+    both = np.unique(np.concatenate([u * gd.n + v, v * gd.n + u]))
+    rpu = np.asarray(gu.row_ptr, np.int64)
+    uu = np.repeat(np.arange(gu.n), np.diff(rpu))
+    assert np.array_equal(both, np.unique(uu * gu.n + gu.col.astype(np.int64)))
+    # not symmetric, and many nodes without out-edges
+    assert gd.nnz < gu.nnz
+    assert (np.diff(rp) == 0).sum() > (np.diff(rpu) == 0).sum()
