@@ -472,10 +472,18 @@ __global__ void __launch_bounds__(kBlock) k_count_colors(Ctx ctx, uint32_t k) {
        i += gridDim.x * kBlock)
     ctx.ids[i] = 0;
 }
+// Class sizes of a given colouring.  The lanes of a wave that share a colour
+// add their count with one atomic (a colouring with few classes would
+// otherwise put most atomics of the device on one address).
 __global__ void __launch_bounds__(kBlock) k_hist_colors(Ctx ctx) {
+  const uint32_t lane = lane_id();
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
-       i += gridDim.x * kBlock)
-    atomicAdd(&ctx.ids[ctx.c[i]], 1u);
+       i += gridDim.x * kBlock) {
+    const uint32_t c = ctx.c[i];
+    const unsigned long long peers = wave_peers(c, true);
+    if ((int)lane == __ffsll((long long)peers) - 1)
+      atomicAdd(&ctx.ids[c], (uint32_t)__popcll(peers));
+  }
 }
 // One block: cstart = exclusive scan of ids[0..k]; ids becomes the cursor.
 __global__ void __launch_bounds__(kBlock) k_scan_colors(Ctx ctx, uint32_t k) {
@@ -493,11 +501,18 @@ __global__ void __launch_bounds__(kBlock) k_scan_colors(Ctx ctx, uint32_t k) {
     carry += tot;
   }
 }
+// Nodes grouped by colour: one cursor reservation per colour present in a
+// wave, the lanes' slots by their position among its peers.
 __global__ void __launch_bounds__(kBlock) k_place_colors(Ctx ctx) {
+  const uint32_t lane = lane_id();
   for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n;
        i += gridDim.x * kBlock) {
     const uint32_t c = ctx.c[i];
-    const uint32_t at = atomicAdd(&ctx.ids[c], 1u);
+    const unsigned long long peers = wave_peers(c, true);
+    const int ldr = __ffsll((long long)peers) - 1;
+    uint32_t at = 0;
+    if ((int)lane == ldr) at = atomicAdd(&ctx.ids[c], (uint32_t)__popcll(peers));
+    at = __shfl(at, ldr, kWave) + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
     ctx.perm[at] = i;
     ctx.act[i] = (ctx.cstart[c + 1] - ctx.cstart[c]) >= 2 ? 1 : 0;
   }
