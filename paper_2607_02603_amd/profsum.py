@@ -100,11 +100,26 @@ def traffic(fetch_db, write_db, kernels):
             for k in kernels:
                 if s.startswith(k):
                     kib[k] += c.get(counter, 0.0)
+        # the whole call: every library kernel, summed per kernel name
+        per = {}
+        for n, c in lib:
+            s = _short(n)
+            per[s] = per.get(s, 0.0) + c.get(counter, 0.0) * 1024.0 * scale
         res[which] = {"counter": counter, "kib": kib, "copy_kib": copy[0], "scale": scale,
-                      "bytes": sum(kib.values()) * 1024.0 * scale}
+                      "bytes": sum(kib.values()) * 1024.0 * scale,
+                      "call_bytes": sum(per.values()), "call_per_kernel": per}
+    per_kernel = {}
+    for which in ("fetch", "write"):
+        for k, v in res[which].pop("call_per_kernel").items():
+            per_kernel[k] = per_kernel.get(k, 0.0) + v
+    top = dict(sorted(per_kernel.items(), key=lambda kv: -kv[1])[:20])
     return {"kernels": kernels, "source": os.path.relpath(PB_SOURCE, os.path.dirname(_HERE)),
             "source_sha256": source_hash(), "fetch": res["fetch"], "write": res["write"],
-            "traffic_bytes_per_launch": res["fetch"]["bytes"] + res["write"]["bytes"]}
+            "traffic_bytes_per_launch": res["fetch"]["bytes"] + res["write"]["bytes"],
+            "call": {"note": "all library kernels of the last call (fetch + write, scaled "
+                             "like the image's); informational, not tied to the hash above",
+                     "bytes": res["fetch"]["call_bytes"] + res["write"]["call_bytes"],
+                     "top_kernels_bytes": top}}
 
 
 def main(argv):
