@@ -9,7 +9,9 @@
 #include <cstdint>
 #include <cstring>
 #include <functional>
+#include <memory>
 #include <mutex>
+#include <new>
 #include <thread>
 #include <vector>
 
@@ -135,6 +137,42 @@ inline bool ring_row_sums_ok(HostPool& pool, const HostGraph& G) {
   return true;
 }
 
+// Growable array that is not value-initialised: a fresh allocation is first
+// touched by the threads that fill it, and every slot read later has been
+// written.  reserve() returns false when the allocation fails.
+template <typename T>
+struct RawBuf {
+  std::unique_ptr<T[]> p;
+  uint64_t cap = 0;
+  bool reserve(uint64_t n) {
+    if (n <= cap) return true;
+    p.reset(new (std::nothrow) T[n]);
+    cap = p ? n : 0;
+    return p != nullptr;
+  }
+  T& operator[](uint64_t i) { return p[i]; }
+  const T& operator[](uint64_t i) const { return p[i]; }
+  const T* data() const { return p.get(); }
+};
+
+// f(i) for every i in [lo, hi) with act[i] != 0, reading act eight bytes at
+// a time (the active rows of late rounds are few).
+template <typename F>
+inline void for_active(const uint8_t* act, uint64_t lo, uint64_t hi, F&& f) {
+  uint64_t i = lo;
+  for (; i + 8 <= hi; i += 8) {
+    uint64_t w;
+    memcpy(&w, act + i, 8);
+    while (w) {
+      const int b = __builtin_ctzll(w) >> 3;
+      f(i + (uint64_t)b);
+      w &= ~(0xFFull << (8 * b));
+    }
+  }
+  for (; i < hi; ++i)
+    if (act[i]) f(i);
+}
+
 // A cut row's share of one chunk: its segments [first, first + count) of the
 // chunk, the node, and whether z already holds the sum of earlier chunks.
 struct StreamFold {
@@ -152,24 +190,25 @@ inline uint64_t stream_folds(uint64_t mc) { return mc / kSegMax + 2; }
 // entries.  Segments are numbered over the round; seg0[r] / ent0[r] are the
 // first segment and the first packed entry of live row r.
 struct StreamPlan {
-  std::vector<uint32_t> rows;
-  std::vector<uint64_t> seg0, ent0;
+  RawBuf<uint32_t> rows;
+  RawBuf<uint64_t> seg0, ent0;
   uint64_t nr = 0, ns = 0, ne = 0;
 
-  void build(HostPool& pool, const HostGraph& G, const uint8_t* act) {
+  // false when the host arrays cannot be allocated
+  bool build(HostPool& pool, const HostGraph& G, const uint8_t* act) {
     const unsigned T = pool.size();
     const uint64_t n = G.n;
     std::vector<uint64_t> tc(T + 1, 0), ts(T + 1, 0), te(T + 1, 0);
     auto lo = [&](unsigned t) { return n * t / T; };
     pool.run([&](unsigned t) {
       uint64_t c = 0, sg = 0, en = 0;
-      for (uint64_t i = lo(t); i < lo(t + 1); ++i) {
+      for_active(act, lo(t), lo(t + 1), [&](uint64_t i) {
         const uint64_t d = G.rp(i + 1) - G.rp(i);
-        if (!act[i] || d == 0) continue;
+        if (d == 0) return;
         ++c;
         sg += (d + kSegMax - 1) / kSegMax;
         en += d;
-      }
+      });
       tc[t + 1] = c;
       ts[t + 1] = sg;
       te[t + 1] = en;
@@ -182,29 +221,31 @@ struct StreamPlan {
     nr = tc[T];
     ns = ts[T];
     ne = te[T];
-    rows.resize(nr);
-    seg0.resize(nr + 1);
-    ent0.resize(nr + 1);
+    if (!rows.reserve(nr + 1) || !seg0.reserve(nr + 1) || !ent0.reserve(nr + 1)) {
+      nr = ns = ne = 0;
+      return false;
+    }
     pool.run([&](unsigned t) {
       uint64_t c = tc[t], sg = ts[t], en = te[t];
-      for (uint64_t i = lo(t); i < lo(t + 1); ++i) {
+      for_active(act, lo(t), lo(t + 1), [&](uint64_t i) {
         const uint64_t d = G.rp(i + 1) - G.rp(i);
-        if (!act[i] || d == 0) continue;
+        if (d == 0) return;
         rows[c] = (uint32_t)i;
         seg0[c] = sg;
         ent0[c] = en;
         ++c;
         sg += (d + kSegMax - 1) / kSegMax;
         en += d;
-      }
+      });
     });
     seg0[nr] = ns;
     ent0[nr] = ne;
+    return true;
   }
 
   // live row holding segment g < ns
   uint64_t row_of(uint64_t g) const {
-    return (uint64_t)(std::upper_bound(seg0.begin(), seg0.begin() + nr, g) - seg0.begin()) - 1;
+    return (uint64_t)(std::upper_bound(seg0.data(), seg0.data() + nr, g) - seg0.data()) - 1;
   }
   // packed entry where segment g starts (ne for g >= ns)
   uint64_t entry_of(uint64_t g) const {

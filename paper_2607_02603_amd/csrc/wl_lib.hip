@@ -10,6 +10,7 @@
 #include <sched.h>
 
 #include <algorithm>
+#include <chrono>
 #include <condition_variable>
 #include <functional>
 #include <mutex>
@@ -1885,6 +1886,13 @@ int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
                  uint32_t* color_host, uint32_t* k_out, uint32_t* rounds_out, int* done_out) {
   const uint64_t n = G.n;
   const bool weighted = G.wt != nullptr;
+  const char* trs = getenv("WL_TRACE_STREAMED");
+  const bool trace = trs && trs[0] == '1';
+  using clk = std::chrono::steady_clock;
+  auto ms_since = [](clk::time_point t) {
+    return std::chrono::duration<double, std::milli>(clk::now() - t).count();
+  };
+  const clk::time_point t_call = clk::now();
   const uint64_t mc = largest_fitting(
       [&](uint64_t c) { return stream_layout(n, c, weighted).total; }, ws_bytes,
       stream_chunk_cap(G));
@@ -1919,8 +1927,11 @@ int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
   }
   const StreamSlot HS = stream_slot(mcs, weighted, false);
   const uint64_t sc = stream_segs(mcs);
+  if (trace)
+    fprintf(stderr, "[wl streamed] n=%llu m=%llu chunk=%llu staged=%llu set-up %.1f ms\n",
+            (unsigned long long)n, (unsigned long long)G.m, (unsigned long long)mc,
+            (unsigned long long)mcs, ms_since(t_call));
   std::vector<uint8_t> act_h;
-  std::vector<uint32_t> deg_h;
   StreamRes R;
   HIP_TRY(hipStreamCreateWithFlags(&R.cs, hipStreamNonBlocking));
   for (int i = 0; i < 2; ++i) {
@@ -1943,28 +1954,74 @@ int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
   }
 
   StreamPlan plan;
-  auto node_lo = [&](unsigned t) { return n * t / T; };
+  // Once all chunks of a round fit in the workspace beyond its layout, they
+  // are copied there instead of to the two slots and kept: the rows a later
+  // round needs are among them (a class never grows back), and the image of
+  // a row that is no longer needed is not used.
+  bool resident = false;
+  std::vector<StreamChunk> res_chunks;
+  const uint64_t keep_begin = align_up(SL.total);
+  const uint64_t keep_bytes = ws_bytes > keep_begin ? ws_bytes - keep_begin : 0;
+  // a kept chunk's arrays, packed: node, off, col, wt, part, fold
+  auto kept_layout = [&](uint64_t nseg, uint64_t len, uint64_t nf, uint64_t o[6]) {
+    uint64_t at = 0;
+    const uint64_t sz[6] = {4 * nseg, 8 * (nseg + 1), 4 * len, weighted ? 4 * len : 0, 8 * nseg,
+                            16 * nf};
+    for (int i = 0; i < 6; ++i) {
+      o[i] = at;
+      at = align_up(at + sz[i]);
+    }
+    return at;
+  };
+  auto launch_chunk = [&](const StreamChunk& ch) -> int {
+    const uint32_t gs = grid_for(ch.nseg, kBlock / kWave, 16384);
+    if (weighted)
+      hipLaunchKernelGGL(k_stream_seg<true>, dim3(gs), dim3(kBlock), 0, s, S.ctx, ch);
+    else
+      hipLaunchKernelGGL(k_stream_seg<false>, dim3(gs), dim3(kBlock), 0, s, S.ctx, ch);
+    if (ch.nfold)
+      hipLaunchKernelGGL(k_stream_fold, dim3(grid_for(ch.nfold, kBlock, 1024)), dim3(kBlock), 0,
+                         s, S.ctx, ch);
+    HIP_LAUNCH_CHECK();
+    return WL_OK;
+  };
 
   while (!S.host.done) {
+    const clk::time_point t_round = clk::now();
+    double pack_ms = 0, wait_ms = 0, act_ms = 0, plan_ms = 0, relabel_ms = 0;
+    uint64_t chunks = 0;
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, S.ctx);
     HIP_LAUNCH_CHECK();
     bool uniform = S.host.k == 1 && !weighted;
     if (uniform) {
-      // z_i = deg_i * w: the degrees only
-      deg_h.resize(n);
+      // z_i = deg_i * w: the degrees only, computed by host threads straight
+      // into the two page-locked staging buffers and copied chunk by chunk
+      uint32_t* deg_dev = (uint32_t*)S.ctx.keys_tmp;
+      const uint64_t per = HS.total / 4;  // degrees per staging buffer
       std::vector<uint8_t> big(T, 0);
-      uint32_t* deg = deg_h.data();
-      pool.run([&](unsigned t) {
-        for (uint64_t i = node_lo(t); i < node_lo(t + 1); ++i) {
-          const uint64_t d = G.rp(i + 1) - G.rp(i);
-          if (d > 0xFFFFFFFFull) big[t] = 1;
-          deg[i] = (uint32_t)d;
-        }
-      });
+      int slot = 0;
+      // the copies overwrite scratch that earlier work on s may still use
+      HIP_TRY(hipEventRecord(R.computed[0], s));
+      HIP_TRY(hipStreamWaitEvent(R.cs, R.computed[0], 0));
+      for (uint64_t r0 = 0; r0 < n; r0 += per) {
+        const uint64_t nr = std::min(per, n - r0);
+        HIP_TRY(hipEventSynchronize(R.copied[slot]));
+        uint32_t* deg = (uint32_t*)stage[slot].p;
+        pool.run([&](unsigned t) {
+          for (uint64_t i = nr * t / T; i < nr * (t + 1) / T; ++i) {
+            const uint64_t d = G.rp(r0 + i + 1) - G.rp(r0 + i);
+            if (d > 0xFFFFFFFFull) big[t] = 1;
+            deg[i] = (uint32_t)d;
+          }
+        });
+        HIP_TRY(hipMemcpyAsync(deg_dev + r0, deg, 4 * nr, hipMemcpyHostToDevice, R.cs));
+        HIP_TRY(hipEventRecord(R.copied[slot], R.cs));
+        slot ^= 1;
+      }
+      HIP_TRY(hipStreamWaitEvent(s, R.copied[slot ^ 1], 0));
+      HIP_TRY(hipStreamWaitEvent(s, R.copied[slot], 0));
       for (unsigned t = 0; t < T; ++t) uniform = uniform && !big[t];
       if (uniform) {
-        uint32_t* deg_dev = (uint32_t*)S.ctx.keys_tmp;
-        if (int r = hc.h2d(deg_dev, deg, 4 * n)) return r;
         hipLaunchKernelGGL(k_stream_uniform, dim3(gn), dim3(kBlock), 0, s, S.ctx, deg_dev);
         HIP_LAUNCH_CHECK();
       }
@@ -1975,14 +2032,36 @@ int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
                          S.ctx.z, n);
       hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, S.ctx, -1);
       HIP_LAUNCH_CHECK();
+    }
+    if (!uniform && resident) {
+      for (const StreamChunk& ch : res_chunks)
+        if (int r = launch_chunk(ch)) return r;
+    } else if (!uniform) {
+      clk::time_point t0 = clk::now();
       if (int r = hc.d2h(act_h.data(), S.ctx.act, n)) return r;
-      plan.build(pool, G, act_h.data());
+      act_ms = ms_since(t0);
+      t0 = clk::now();
+      if (!plan.build(pool, G, act_h.data()))
+        return fail(WL_ENOMEM, "host arrays for the plan of %llu rows",
+                    (unsigned long long)n);
+      plan_ms = ms_since(t0);
+      // keep this round's chunks if they all fit (a bound of their bytes)
+      uint64_t nchunks = 0;
+      for (uint64_t a = 0; a < plan.ns; a = plan.chunk_end(a, mcs, sc)) ++nchunks;
+      const uint64_t bound = 20 * plan.ns + (weighted ? 8 : 4) * plan.ne +
+                             nchunks * (8 + 16 * stream_folds(mcs) + 6 * kAlign);
+      const bool keep = plan.ns > 0 && bound <= keep_bytes;
+      uint64_t keep_off = keep_begin;
       uint64_t a = 0;
       int slot = 0;
       while (a < plan.ns) {
         const uint64_t b = plan.chunk_end(a, mcs, sc);
         const uint64_t len = plan.entry_of(b) - plan.entry_of(a), nseg = b - a;
+        clk::time_point t0 = clk::now();
         HIP_TRY(hipEventSynchronize(R.copied[slot]));
+        wait_ms += ms_since(t0);
+        t0 = clk::now();
+        ++chunks;
         uint8_t* H = stage[slot].p;
         uint32_t* hnode = (uint32_t*)(H + HS.node);
         uint64_t* hoff = (uint64_t*)(H + HS.off);
@@ -1992,45 +2071,65 @@ int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
         const int64_t nfs = plan.pack(pool, G, a, b, hnode, hoff, hcol, weighted ? hwt : nullptr,
                                       hfold, stream_folds(mcs));
         if (nfs < 0) return fail(WL_EINVAL, "chunk plan exceeds its fold table");
+        pack_ms += ms_since(t0);
         const uint64_t nf = (uint64_t)nfs;
-        uint8_t* D = W + SL.slot[slot];
-        HIP_TRY(hipStreamWaitEvent(R.cs, R.computed[slot], 0));
-        HIP_TRY(hipMemcpyAsync(D + SL.sl.node, hnode, 4 * nseg, hipMemcpyHostToDevice, R.cs));
-        HIP_TRY(hipMemcpyAsync(D + SL.sl.off, hoff, 8 * (nseg + 1), hipMemcpyHostToDevice, R.cs));
-        HIP_TRY(hipMemcpyAsync(D + SL.sl.col, hcol, 4 * len, hipMemcpyHostToDevice, R.cs));
+        uint8_t* D;
+        uint64_t o[6] = {SL.sl.node, SL.sl.off, SL.sl.col, SL.sl.wt, SL.sl.part, SL.sl.fold};
+        if (keep) {
+          D = W + keep_off;
+          const uint64_t tot = kept_layout(nseg, len, nf, o);
+          if (keep_off + tot > keep_begin + keep_bytes)
+            return fail(WL_EINVAL, "kept chunks exceed their bound");
+          keep_off += tot;
+        } else {
+          D = W + SL.slot[slot];
+          HIP_TRY(hipStreamWaitEvent(R.cs, R.computed[slot], 0));
+        }
+        HIP_TRY(hipMemcpyAsync(D + o[0], hnode, 4 * nseg, hipMemcpyHostToDevice, R.cs));
+        HIP_TRY(hipMemcpyAsync(D + o[1], hoff, 8 * (nseg + 1), hipMemcpyHostToDevice, R.cs));
+        HIP_TRY(hipMemcpyAsync(D + o[2], hcol, 4 * len, hipMemcpyHostToDevice, R.cs));
         if (weighted)
-          HIP_TRY(hipMemcpyAsync(D + SL.sl.wt, hwt, 4 * len, hipMemcpyHostToDevice, R.cs));
-        if (nf)
-          HIP_TRY(hipMemcpyAsync(D + SL.sl.fold, hfold, 16 * nf, hipMemcpyHostToDevice, R.cs));
+          HIP_TRY(hipMemcpyAsync(D + o[3], hwt, 4 * len, hipMemcpyHostToDevice, R.cs));
+        if (nf) HIP_TRY(hipMemcpyAsync(D + o[5], hfold, 16 * nf, hipMemcpyHostToDevice, R.cs));
         HIP_TRY(hipEventRecord(R.copied[slot], R.cs));
         HIP_TRY(hipStreamWaitEvent(s, R.copied[slot], 0));
         StreamChunk ch;
-        ch.node = (const uint32_t*)(D + SL.sl.node);
-        ch.off = (const uint64_t*)(D + SL.sl.off);
-        ch.col = (const uint32_t*)(D + SL.sl.col);
-        ch.wt = weighted ? (const uint32_t*)(D + SL.sl.wt) : nullptr;
-        ch.part = (uint64_t*)(D + SL.sl.part);
-        ch.fold = (const StreamFold*)(D + SL.sl.fold);
+        ch.node = (const uint32_t*)(D + o[0]);
+        ch.off = (const uint64_t*)(D + o[1]);
+        ch.col = (const uint32_t*)(D + o[2]);
+        ch.wt = weighted ? (const uint32_t*)(D + o[3]) : nullptr;
+        ch.part = (uint64_t*)(D + o[4]);
+        ch.fold = (const StreamFold*)(D + o[5]);
         ch.nseg = (uint32_t)nseg;
         ch.nfold = (uint32_t)nf;
-        const uint32_t gs = grid_for(nseg, kBlock / kWave, 16384);
-        if (weighted)
-          hipLaunchKernelGGL(k_stream_seg<true>, dim3(gs), dim3(kBlock), 0, s, S.ctx, ch);
-        else
-          hipLaunchKernelGGL(k_stream_seg<false>, dim3(gs), dim3(kBlock), 0, s, S.ctx, ch);
-        if (nf)
-          hipLaunchKernelGGL(k_stream_fold, dim3(grid_for(nf, kBlock, 1024)), dim3(kBlock), 0,
-                             s, S.ctx, ch);
-        HIP_LAUNCH_CHECK();
+        if (int r = launch_chunk(ch)) return r;
         HIP_TRY(hipEventRecord(R.computed[slot], s));
+        if (keep) res_chunks.push_back(ch);
         a = b;
         slot ^= 1;
       }
+      resident = keep;
     }
-    if (int r = S.relabel(1)) return r;
+    if (trace) {
+      HIP_TRY(hipStreamSynchronize(s));
+      const clk::time_point t0 = clk::now();
+      if (int r = S.relabel(1)) return r;
+      relabel_ms = ms_since(t0);
+    } else if (int r = S.relabel(1)) {
+      return r;
+    }
+    if (trace)
+      fprintf(stderr, "[wl streamed] round %u: %s rows %llu entries %llu chunks %llu, "
+              "act %.1f ms, plan %.1f ms, packing %.1f ms, waiting for copies %.1f ms, "
+              "relabel %.1f ms, round %.1f ms, colours %u\n",
+              S.host.round, uniform ? "degrees," : (resident && !chunks ? "resident chunk," : ""),
+              uniform ? 0ull : (unsigned long long)plan.nr,
+              uniform ? 0ull : (unsigned long long)plan.ne, (unsigned long long)chunks, act_ms,
+              plan_ms, pack_ms, wait_ms, relabel_ms, ms_since(t_round), S.host.k);
   }
   if (int r = S.stats_end()) return r;
   if (int r = hc.d2h(color_host, colors_dev, 4 * n)) return r;
+  if (trace) fprintf(stderr, "[wl streamed] call %.1f ms\n", ms_since(t_call));
   *k_out = S.host.k;
   *rounds_out = S.host.round;
   *done_out = (int)S.host.done;

@@ -33,62 +33,73 @@ int main(int argc, char** argv) {
     col[e] = (uint32_t)(rng() % n);
     if (weighted) wt[e] = (uint32_t)(1 + rng() % 9);
   }
-  std::vector<uint8_t> act(n);
-  for (uint64_t i = 0; i < n; ++i) act[i] = (int)(rng() % 100) < act_pct;
-  HostGraph G;
-  G.n = n;
-  G.m = m;
-  G.rp64 = rp.data();
-  G.col = col.data();
-  G.wt = weighted ? wt.data() : nullptr;
   HostPool pool;
-  StreamPlan P;
-  P.build(pool, G, act.data());
-  const uint64_t sc = stream_segs(mc), fc = stream_folds(mc);
-  std::vector<uint32_t> node(sc), hc(mc), hw(mc);
-  std::vector<uint64_t> off(sc + 1), part(sc), got(n, 0);
-  std::vector<StreamFold> fold(fc);
-  uint64_t a = 0, chunks = 0, cut = 0;
-  while (a < P.ns) {
-    const uint64_t b = P.chunk_end(a, mc, sc);
-    if (b <= a || b - a > sc) return printf("bad chunk end\n"), 1;
-    const int64_t nf = P.pack(pool, G, a, b, node.data(), off.data(), hc.data(),
-                              weighted ? hw.data() : nullptr, fold.data(), fc);
-    if (nf < 0) return printf("fold table overflow\n"), 1;
-    const uint64_t nseg = b - a;
-    if (off[0] != 0 || off[nseg] > mc) return printf("bad chunk length\n"), 1;
-    for (uint64_t t = 0; t < nseg; ++t) {
-      if (off[t + 1] <= off[t] || off[t + 1] - off[t] > kSegMax) return printf("bad segment\n"), 1;
-      uint64_t s = 0;
-      for (uint64_t e = off[t]; e < off[t + 1]; ++e) s += (uint64_t)hc[e] * (weighted ? hw[e] : 1);
-      if (node[t] & kSegPartial) {
-        part[t] = s;
-        ++cut;
-      } else {
-        if ((node[t] & ~kSegPartial) >= n) return printf("bad node\n"), 1;
-        got[node[t]] = s;
-      }
-    }
-    for (int64_t f = 0; f < nf; ++f) {
-      const StreamFold d = fold[f];
-      if ((uint64_t)d.first + d.count > nseg || d.node >= n) return printf("bad fold\n"), 1;
-      uint64_t s = d.add ? got[d.node] : 0;
-      for (uint32_t t = 0; t < d.count; ++t) s += part[d.first + t];
-      got[d.node] = s;
-    }
-    a = b;
-    ++chunks;
-  }
+  StreamPlan P;  // rebuilt for every pattern: its arrays shrink and grow
   uint64_t bad = 0;
-  for (uint64_t i = 0; i < n; ++i) {
-    uint64_t s = 0;
-    if (act[i])
-      for (uint64_t e = rp[i]; e < rp[i + 1]; ++e) s += (uint64_t)col[e] * (weighted ? wt[e] : 1);
-    bad += s != got[i];
+  // the act percentage given, a third of it, then every row
+  for (int pass = 0; pass < 3; ++pass) {
+    const int pct = pass == 0 ? act_pct : (pass == 1 ? act_pct / 3 : 100);
+    std::vector<uint8_t> act(n);
+    for (uint64_t i = 0; i < n; ++i) act[i] = (int)(rng() % 100) < pct;
+    HostGraph G;
+    G.n = n;
+    G.m = m;
+    G.rp64 = rp.data();
+    G.col = col.data();
+    G.wt = weighted ? wt.data() : nullptr;
+    if (!P.build(pool, G, act.data())) return printf("plan allocation failed\n"), 1;
+    const uint64_t sc = stream_segs(mc), fc = stream_folds(mc);
+    std::vector<uint32_t> node(sc), hc(mc), hw(mc);
+    std::vector<uint64_t> off(sc + 1), part(sc), got(n, 0);
+    std::vector<StreamFold> fold(fc);
+    uint64_t a = 0, chunks = 0, cut = 0;
+    while (a < P.ns) {
+      const uint64_t b = P.chunk_end(a, mc, sc);
+      if (b <= a || b - a > sc) return printf("bad chunk end\n"), 1;
+      const int64_t nf = P.pack(pool, G, a, b, node.data(), off.data(), hc.data(),
+                                weighted ? hw.data() : nullptr, fold.data(), fc);
+      if (nf < 0) return printf("fold table overflow\n"), 1;
+      const uint64_t nseg = b - a;
+      if (off[0] != 0 || off[nseg] > mc) return printf("bad chunk length\n"), 1;
+      for (uint64_t t = 0; t < nseg; ++t) {
+        if (off[t + 1] <= off[t] || off[t + 1] - off[t] > kSegMax)
+          return printf("bad segment\n"), 1;
+        uint64_t s = 0;
+        for (uint64_t e = off[t]; e < off[t + 1]; ++e)
+          s += (uint64_t)hc[e] * (weighted ? hw[e] : 1);
+        if (node[t] & kSegPartial) {
+          part[t] = s;
+          ++cut;
+        } else {
+          if ((node[t] & ~kSegPartial) >= n) return printf("bad node\n"), 1;
+          got[node[t]] = s;
+        }
+      }
+      for (int64_t f = 0; f < nf; ++f) {
+        const StreamFold d = fold[f];
+        if ((uint64_t)d.first + d.count > nseg || d.node >= n) return printf("bad fold\n"), 1;
+        uint64_t s = d.add ? got[d.node] : 0;
+        for (uint32_t t = 0; t < d.count; ++t) s += part[d.first + t];
+        got[d.node] = s;
+      }
+      a = b;
+      ++chunks;
+    }
+    uint64_t bad_p = 0, rows = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+      uint64_t s = 0;
+      if (act[i])
+        for (uint64_t e = rp[i]; e < rp[i + 1]; ++e) s += (uint64_t)col[e] * (weighted ? wt[e] : 1);
+      bad_p += s != got[i];
+      rows += act[i] && rp[i + 1] > rp[i];
+    }
+    if (rows != P.nr) return printf("row count %llu, plan %llu\n", (unsigned long long)rows,
+                                    (unsigned long long)P.nr), 1;
+    printf("act %d%%: n=%llu m=%llu rows=%llu segments=%llu chunks=%llu cut=%llu bad=%llu\n",
+           pct, (unsigned long long)n, (unsigned long long)m, (unsigned long long)P.nr,
+           (unsigned long long)P.ns, (unsigned long long)chunks, (unsigned long long)cut,
+           (unsigned long long)bad_p);
+    bad += bad_p;
   }
-  printf("n=%llu m=%llu rows=%llu segments=%llu chunks=%llu cut=%llu bad=%llu\n",
-         (unsigned long long)n, (unsigned long long)m, (unsigned long long)P.nr,
-         (unsigned long long)P.ns, (unsigned long long)chunks, (unsigned long long)cut,
-         (unsigned long long)bad);
   return bad ? 1 : 0;
 }

@@ -85,6 +85,27 @@ def test_small_chunks_cut_rows(chunk):
     _check(rp, col, wt, init, seed=3, chunk=chunk)
 
 
+@pytest.mark.parametrize("extra", [0, 64 << 20])
+def test_kept_chunks_with_cut_rows(extra):
+    # with room beyond the layout the rows of a round are kept on the device
+    # in several chunks (rows cut across chunk ends included) and reused by
+    # the later rounds; without it every round streams its chunks again
+    rng = random.Random(31)
+    n = 4000
+    edges = [(0, 1 + rng.randrange(n - 1)) for _ in range(20000)]
+    edges += [(2, 3 + rng.randrange(n - 3)) for _ in range(7000)]
+    edges += [(rng.randrange(n), rng.randrange(n)) for _ in range(30000)]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    wt = np.array([rng.randint(1, 5) for _ in range(col.size)], np.uint32)
+    for w in (None, wt):
+        g = _host_graph(rp, col, w)
+        ws = _ws_for_chunk(n, 6000, w is not None) + extra
+        c, k, r = wl.wl_stable_coloring_streamed(g, None, 8, ws_bytes=ws)
+        co, ko, ro, _, st = oracle.stable_coloring(rp, col, w, None, 8)
+        assert st == 0 and (k, r) == (ko, ro) and r >= 3
+        assert np.array_equal(c.numpy().view(np.uint32), co)
+
+
 def test_rmat_many_chunks_pageable():
     g = inputs.rmat(14, 16, seed=9)
     print(f"rmat14 nnz={g.nnz}", flush=True)
