@@ -396,10 +396,12 @@ __global__ void __launch_bounds__(kBlock) k_validate_sym(Ctx ctx) {
   atomicAdd(&ctx.st->sym_hash[1], b);
 }
 
+constexpr uint32_t kErrRowSum = 32u;  // DevState::err bit: a row sum above 2^32 (ring)
+
 // Theorem 1's precondition for Z/2^64: every row sum of A at most 2^32.  One
 // thread per row (its length, or the sum of at most 64 weights); the rows
 // with more weights are summed by all 64 lanes of the wave, one after the
-// other.  Sets error bit 8 on a row above the bound.
+// other.  Sets kErrRowSum on a row above the bound.
 template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_ring_rows(Ctx ctx) {
   const RP* rp = rowptr<RP>(ctx);
@@ -433,7 +435,7 @@ __global__ void __launch_bounds__(kBlock) k_ring_rows(Ctx ctx) {
       for (int off = kWave / 2; off > 0; off >>= 1) sum += __shfl_xor(sum, off, kWave);
       if (sum > lim) over = true;
     }
-    if (over) atomicOr(&ctx.st->err, 8u);
+    if (over) atomicOr(&ctx.st->err, kErrRowSum);
   }
 }
 
@@ -740,7 +742,7 @@ struct Session {
       hipLaunchKernelGGL(k_ring_rows<uint32_t>, dim3(g), dim3(kBlock), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
-    if (host.err & 8u)
+    if (host.err & kErrRowSum)
       return fail(WL_EOVERFLOW, "a row sum exceeds 2^32, the bound of arithmetic mod 2^64");
     return WL_OK;
   }
@@ -1754,9 +1756,23 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
                    uint64_t nreps, uint32_t bfirst, uint64_t write_end, QuotientOut& Q,
                    std::vector<std::pair<uint32_t, uint64_t>>* spill,
                    std::vector<uint64_t>& hkey, std::vector<uint64_t>& hw,
-                   std::vector<uint32_t>& hdeg) {
+                   std::vector<uint32_t>& hdeg, const std::vector<uint32_t>* seg = nullptr,
+                   double* tm = nullptr) {
+  // tm (diagnostics): adds the ms until the device's part is done, then the
+  // ms of the copies out
+  using clk = std::chrono::steady_clock;
+  clk::time_point t0 = clk::now();
+  // seg: key offsets of the chunk's non-empty rows and nkeys (one segment
+  // each), or none (one segment)
+  const uint64_t nseg = seg ? seg->size() - 1 : 0;
+  if (nseg) {
+    if (nseg > nkeys) return fail(WL_EINVAL, "more row segments than keys");
+    if (int r = hc.h2d(S.ctx.cstart, seg->data(), 4 * (nseg + 1))) return r;
+    S.host.k = (uint32_t)nseg;
+  }
   hipLaunchKernelGGL(k_q_begin, dim3(grid_for(std::max(nkeys, nreps), kBlock, 4096)),
-                     dim3(kBlock), 0, S.s, S.ctx, (uint32_t)nkeys, D.deg(), (uint32_t)nreps);
+                     dim3(kBlock), 0, S.s, S.ctx, (uint32_t)nkeys, D.deg(), (uint32_t)nreps,
+                     (uint32_t)nseg);
   HIP_LAUNCH_CHECK();
   if (int r = S.segmented_sort()) return r;
   hipLaunchKernelGGL(k_q_reduce, dim3(grid_for(nkeys, kBlock, 4096)), dim3(kBlock), 0, S.s,
@@ -1777,6 +1793,10 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
                      S.ctx, (uint32_t)nkeys, D.col, D.wt, D.deg());
   HIP_LAUNCH_CHECK();
   if (int r = S.pull()) return r;
+  if (tm) {
+    tm[0] += std::chrono::duration<double, std::milli>(clk::now() - t0).count();
+    t0 = clk::now();
+  }
   if (S.host.err & kErrQuotientWeight)
     return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
   const uint32_t nd = S.host.k_new;
@@ -1788,6 +1808,7 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
   if (int r = hc.d2h(hdeg.data(), D.deg(), 4ull * nreps)) return r;
   for (uint64_t b = 0; b < nreps; ++b) Q.deg[bfirst + b] += hdeg[b];
   Q.m += nd;
+  if (tm) tm[1] += std::chrono::duration<double, std::milli>(clk::now() - t0).count();
   return WL_OK;
 }
 
@@ -2161,6 +2182,11 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   uint8_t* W = (uint8_t*)ws;
   const char* tr = getenv("WL_TRACE_BATCHED");
   const bool trace = tr && tr[0] == '1';
+  using clk = std::chrono::steady_clock;
+  auto ms_since = [](clk::time_point t) {
+    return std::chrono::duration<double, std::milli>(clk::now() - t).count();
+  };
+  clk::time_point t_phase = clk::now();
 
   HostGraph G;
   G.n = n0;
@@ -2247,9 +2273,11 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     if (mq == 0) return fail(WL_EBUDGET, "workspace too small for the quotient phase");
     if (trace)
       fprintf(stderr, "[wl batched] t=%llu n=%llu m=%llu cap=%llu batches=%llu rows_cap=%llu "
-              "quotient_chunk=%llu\n", (unsigned long long)t, (unsigned long long)n,
-              (unsigned long long)G.m, (unsigned long long)mb, (unsigned long long)nb,
-              (unsigned long long)rows_cap, (unsigned long long)mq);
+              "quotient_chunk=%llu (%.1f ms since the last line)\n", (unsigned long long)t,
+              (unsigned long long)n, (unsigned long long)G.m, (unsigned long long)mb,
+              (unsigned long long)nb, (unsigned long long)rows_cap, (unsigned long long)mq,
+              ms_since(t_phase));
+    if (trace) t_phase = clk::now();
     // ---- refinement of every batch (Eq. batch-init), merge keys (Eq. merge)
     key.assign(n, 0xFFFFFFFFu);
     uint64_t base = 0;
@@ -2296,9 +2324,11 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       if (S.host.done == 2) return fail(WL_EMAXROUNDS, "batch refinement did not stabilise");
       rounds += S.host.round;
       if (trace)
-        fprintf(stderr, "[wl batched]   batch %llu rows [%llu, %llu) entries %llu colours %u rounds %u\n",
+        fprintf(stderr, "[wl batched]   batch %llu rows [%llu, %llu) entries %llu colours %u "
+              "rounds %u (%.1f ms since the last line)\n",
                 (unsigned long long)b, (unsigned long long)r_lo, (unsigned long long)r_hi,
-                (unsigned long long)ml, S.host.k, S.host.round);
+                (unsigned long long)ml, S.host.k, S.host.round, ms_since(t_phase));
+    if (trace) t_phase = clk::now();
       loc.resize(nl);
       if (int r = hc.d2h(loc.data(), colors_dev, 4 * nl)) return r;
       for (uint64_t i = 0; i < nl; ++i) key[r_lo + i] = (uint32_t)(base + loc[i]);
@@ -2325,8 +2355,10 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     ++outer;
     const uint64_t nq = next;
     if (trace)
-      fprintf(stderr, "[wl batched] t=%llu merged blocks=%llu rounds so far=%llu\n",
-              (unsigned long long)t, (unsigned long long)nq, (unsigned long long)rounds);
+      fprintf(stderr, "[wl batched] t=%llu merged blocks=%llu rounds so far=%llu (merge %.1f ms)\n",
+              (unsigned long long)t, (unsigned long long)nq, (unsigned long long)rounds,
+              ms_since(t_phase));
+    if (trace) t_phase = clk::now();
     // fixed point with several batches: the exact finish runs on G_t itself
     if (nb > 1 && nq == n && exact) return finish_exact(G);
     for (uint64_t v = 0; v < n0; ++v) map0[v] = blk[map0[v]];
@@ -2368,6 +2400,9 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     if (int r = hc.h2d(blk_dev, blk.data(), 4 * n)) return r;
     if (int r = hc.h2d(isrep_dev, isrep.data(), n)) return r;
     std::vector<uint64_t> qoff;
+    std::vector<uint32_t> qseg;
+    double q_in_ms = 0, q_dev_ms = 0, q_tm[2] = {0, 0};
+    uint64_t q_chunks = 0;
     uint64_t a = 0;
     while (a < n) {
       // rows [a, bnd) with at most mq entries, at least one row
@@ -2406,7 +2441,8 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
               return r;
             S.ctx.keys_mat = 1;
             if (int r = S.init_state(0, 1, 0, 1, 1)) return r;
-            hipLaunchKernelGGL(k_q_keys, dim3(1), dim3(kBlock), 0, s, S.ctx, rp_dev,
+            hipLaunchKernelGGL(k_q_keys, dim3(grid_for(len, kBlock, 8192)), dim3(kBlock), 0, s,
+                               S.ctx, rp_dev,
                                col_dev, G.wt ? wt_dev : nullptr, blk_dev, isrep_dev,
                                qoff_dev, 1u, (uint32_t)a, blk[a]);
             HIP_LAUNCH_CHECK();
@@ -2434,22 +2470,33 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       }
       const uint64_t nrows = bnd - a;
       qoff.resize(nrows);
+      qseg.clear();
       uint64_t run = 0, nreps = 0;
       uint32_t bfirst = 0xFFFFFFFFu;
       for (uint64_t r = 0; r < nrows; ++r) {
         qoff[r] = run;
         if (isrep[a + r]) {
           if (bfirst == 0xFFFFFFFFu) bfirst = blk[a + r];
-          run += G.rp(a + r + 1) - G.rp(a + r);
+          const uint64_t d = G.rp(a + r + 1) - G.rp(a + r);
+          if (d) qseg.push_back((uint32_t)run);
+          run += d;
           ++nreps;
         }
       }
+      qseg.push_back((uint32_t)run);
       if (run > 0) {
+        clk::time_point tq = clk::now();
+        ++q_chunks;
         if (int r = copy_rows_h2d(hc, G, a, nrows, W + QL.stage, rp_dev, s)) return r;
         if (int r = hc.h2d(qoff_dev, qoff.data(), 8 * nrows)) return r;
         if (int r = hc.h2d(col_dev, G.col + ea, 4 * ent)) return r;
         if (G.wt)
           if (int r = hc.h2d(wt_dev, G.wt + ea, 4 * ent)) return r;
+        if (trace) {
+          HIP_TRY(hipStreamSynchronize(s));
+          q_in_ms += ms_since(tq);
+          tq = clk::now();
+        }
         wl_csr sg{};
         sg.n = run;
         sg.nnz = 0;
@@ -2459,16 +2506,24 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
           return r;
         S.ctx.keys_mat = 1;
         if (int r = S.init_state(0, 1, 0, 1, 1)) return r;
-        hipLaunchKernelGGL(k_q_keys, dim3(grid_for(nrows, kBlock / kWave, 8192)),
+        hipLaunchKernelGGL(k_q_keys, dim3(grid_for(ent, kBlock, 8192)),
                            dim3(kBlock), 0, s, S.ctx, rp_dev, col_dev,
                            G.wt ? wt_dev : nullptr, blk_dev, isrep_dev, qoff_dev,
                            (uint32_t)nrows, (uint32_t)a, bfirst);
         HIP_LAUNCH_CHECK();
         if (int r = quotient_chunk(S, hc, D, run, nreps, bfirst, ea + ent, Q, nullptr, hkey,
-                                   hw, hdeg))
+                                   hw, hdeg, &qseg, trace ? q_tm : nullptr))
           return r;
+        if (trace) q_dev_ms += ms_since(tq);
       }
       a = bnd;
+    }
+    if (trace) {
+      fprintf(stderr, "[wl batched] t=%llu quotient: %llu chunks, copies in %.1f ms, device "
+              "and copies out %.1f ms (device %.1f, out %.1f), %.1f ms since the last line\n",
+              (unsigned long long)t, (unsigned long long)q_chunks, q_in_ms, q_dev_ms, q_tm[0],
+              q_tm[1], ms_since(t_phase));
+      t_phase = clk::now();
     }
     // new row pointers and labels
     if (int r = nrp_buf.alloc(8 * (nq + 1))) return r;

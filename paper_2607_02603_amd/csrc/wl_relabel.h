@@ -368,7 +368,7 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
   const uint32_t ns = st->n_small;
   __shared__ unsigned long long skey[kSmallMax];
   __shared__ uint32_t sval[kSmallMax];
-  __shared__ int differ;
+  __shared__ int differ, unsorted;
   for (uint32_t si = blockIdx.x; si < ns; si += gridDim.x) {
     const uint2 sg = ctx.small_list[si];
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
@@ -386,13 +386,25 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
       }
     }
     __syncthreads();
-    // all images equal: nothing splits, nothing to reorder
-    if (threadIdx.x == 0) differ = 0;
+    // all images equal: nothing splits, nothing to reorder; already in
+    // order (the rows of a quotient): only the flags
+    if (threadIdx.x == 0) {
+      differ = 0;
+      unsorted = 0;
+    }
     __syncthreads();
-    for (uint32_t t = threadIdx.x; t < len; t += kBlock)
+    for (uint32_t t = threadIdx.x; t < len; t += kBlock) {
       if (skey[t] != skey[0]) differ = 1;
+      if (t + 1 < len && key_less<TIE>(skey[t + 1], sval[t + 1], skey[t], sval[t])) unsorted = 1;
+    }
     __syncthreads();
     if (!differ) continue;
+    if (!unsorted) {
+      for (uint32_t t = threadIdx.x + 1; t < len; t += kBlock)
+        if (skey[t] != skey[t - 1]) ctx.flags[s + t] = 1;
+      __syncthreads();
+      continue;
+    }
     for (uint32_t kk = 2; kk <= P; kk <<= 1) {
       for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
         for (uint32_t i = threadIdx.x; i < P; i += kBlock) {
