@@ -173,6 +173,59 @@ inline void for_active(const uint8_t* act, uint64_t lo, uint64_t hi, F&& f) {
     if (act[i]) f(i);
 }
 
+// Merged partition of Algorithm 2 (Eq. merge) numbered by first occurrence
+// in node order: a node whose key is kNoKey (a boundary node) is a block of
+// its own, nodes sharing a key form one block.  Writes blk[i] (block of node
+// i) and isrep[i] (1 for the first node of its block) and returns the
+// number of blocks.  first (nkeys entries) is scratch.
+constexpr uint32_t kNoKey = 0xFFFFFFFFu;
+
+inline uint64_t merge_blocks(HostPool& pool, const uint32_t* key, uint64_t n, uint64_t nkeys,
+                             uint32_t* first, uint32_t* blk, uint8_t* isrep) {
+  const unsigned T = pool.size();
+  auto lo = [&](unsigned t) { return n * t / T; };
+  pool.run([&](unsigned t) {
+    for (uint64_t k = nkeys * t / T; k < nkeys * (t + 1) / T; ++k) first[k] = kNoKey;
+  });
+  // first node of every key (a key's nodes rarely span two threads' ranges)
+  pool.run([&](unsigned t) {
+    for (uint64_t i = lo(t); i < lo(t + 1); ++i) {
+      const uint32_t kk = key[i];
+      if (kk == kNoKey) continue;
+      uint32_t cur = __atomic_load_n(&first[kk], __ATOMIC_RELAXED);
+      while ((uint32_t)i < cur &&
+             !__atomic_compare_exchange_n(&first[kk], &cur, (uint32_t)i, true, __ATOMIC_RELAXED,
+                                          __ATOMIC_RELAXED)) {
+      }
+    }
+  });
+  std::vector<uint64_t> cnt(T + 1, 0);
+  pool.run([&](unsigned t) {
+    uint64_t c = 0;
+    for (uint64_t i = lo(t); i < lo(t + 1); ++i) {
+      const uint32_t kk = key[i];
+      c += kk == kNoKey || first[kk] == (uint32_t)i;
+    }
+    cnt[t + 1] = c;
+  });
+  for (unsigned t = 0; t < T; ++t) cnt[t + 1] += cnt[t];
+  pool.run([&](unsigned t) {
+    uint64_t id = cnt[t];
+    for (uint64_t i = lo(t); i < lo(t + 1); ++i) {
+      const uint32_t kk = key[i];
+      const bool fresh = kk == kNoKey || first[kk] == (uint32_t)i;
+      isrep[i] = fresh ? 1 : 0;
+      if (fresh) blk[i] = (uint32_t)id++;
+    }
+  });
+  // the other nodes take the block of their key's first node
+  pool.run([&](unsigned t) {
+    for (uint64_t i = lo(t); i < lo(t + 1); ++i)
+      if (!isrep[i]) blk[i] = blk[first[key[i]]];
+  });
+  return cnt[T];
+}
+
 // A cut row's share of one chunk: its segments [first, first + count) of the
 // chunk, the node, and whether z already holds the sum of earlier chunks.
 struct StreamFold {

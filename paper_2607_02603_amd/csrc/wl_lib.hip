@@ -2204,8 +2204,10 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   HostCopy hc(s);
   uint64_t rounds = 0;
   uint32_t outer = 0;
-  std::vector<uint32_t> key, loc, blk, mapk;
-  std::vector<uint8_t> isrep;
+  std::vector<uint32_t> key, loc;
+  RawBuf<uint32_t> blk, mapk;
+  RawBuf<uint8_t> isrep;
+  HostPool pool;
   std::vector<uint64_t> hkey, hw;
   std::vector<uint32_t> hdeg;
   std::vector<uint64_t> piece_rp(3);
@@ -2279,7 +2281,11 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
               ms_since(t_phase));
     if (trace) t_phase = clk::now();
     // ---- refinement of every batch (Eq. batch-init), merge keys (Eq. merge)
-    key.assign(n, 0xFFFFFFFFu);
+    key.resize(n);
+    pool.run([&](unsigned th) {
+      std::fill(key.begin() + n * th / pool.size(), key.begin() + n * (th + 1) / pool.size(),
+                kNoKey);
+    });
     uint64_t base = 0;
     for (uint64_t b = 0; b < nb; ++b) {
       uint64_t r_lo, r_hi;
@@ -2335,25 +2341,12 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
       base += S.host.k;
     }
     // ---- merged partition: first-occurrence ids; boundary nodes singletons
-    mapk.assign(base, 0xFFFFFFFFu);
-    blk.resize(n);
-    isrep.assign(n, 0);
-    uint32_t next = 0;
-    for (uint64_t i = 0; i < n; ++i) {
-      const uint32_t kk = key[i];
-      if (kk == 0xFFFFFFFFu) {
-        isrep[i] = 1;
-        blk[i] = next++;
-      } else {
-        if (mapk[kk] == 0xFFFFFFFFu) {
-          mapk[kk] = next++;
-          isrep[i] = 1;
-        }
-        blk[i] = mapk[kk];
-      }
-    }
+    if (!mapk.reserve(base) || !blk.reserve(n) || !isrep.reserve(n))
+      return fail(WL_ENOMEM, "host arrays of the merged partition (%llu nodes)",
+                  (unsigned long long)n);
+    const uint64_t nq = merge_blocks(pool, key.data(), n, base, mapk.p.get(), blk.p.get(),
+                                     isrep.p.get());
     ++outer;
-    const uint64_t nq = next;
     if (trace)
       fprintf(stderr, "[wl batched] t=%llu merged blocks=%llu rounds so far=%llu (merge %.1f ms)\n",
               (unsigned long long)t, (unsigned long long)nq, (unsigned long long)rounds,
@@ -2361,15 +2354,24 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     if (trace) t_phase = clk::now();
     // fixed point with several batches: the exact finish runs on G_t itself
     if (nb > 1 && nq == n && exact) return finish_exact(G);
-    for (uint64_t v = 0; v < n0; ++v) map0[v] = blk[map0[v]];
+    pool.run([&](unsigned th) {
+      for (uint64_t v = n0 * th / pool.size(); v < n0 * (th + 1) / pool.size(); ++v)
+        map0[v] = blk[map0[v]];
+    });
     if (nb == 1 || nq == n) {
       *coarsest_out = (nb == 1) ? 1 : 0;
       break;
     }
     // ---- quotient graph (Definition "Quotient Graph"), on the device
+    std::vector<uint64_t> qcap_t(pool.size(), 0);
+    pool.run([&](unsigned th) {
+      uint64_t c = 0;
+      for (uint64_t i = n * th / pool.size(); i < n * (th + 1) / pool.size(); ++i)
+        if (isrep[i]) c += G.rp(i + 1) - G.rp(i);
+      qcap_t[th] = c;
+    });
     uint64_t qcap = 0;
-    for (uint64_t i = 0; i < n; ++i)
-      if (isrep[i]) qcap += G.rp(i + 1) - G.rp(i);
+    for (uint64_t c : qcap_t) qcap += c;
     QuotientOut Q;
     Q.deg.assign(nq, 0);
     const bool in_place = t > 0;

@@ -50,3 +50,29 @@ def test_ring_row_sum_bound(tmp_path):
     subprocess.run(["g++", "-std=c++17", "-O1", "-pthread", src, "-o", out], check=True)
     r = subprocess.run([out], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0, r.stdout + r.stderr
+
+
+@pytest.mark.parametrize("args", [
+    # n, keys, spread over the array, % boundary nodes, seed
+    (100000, 30000, 0, 5, 1),
+    (100000, 30000, 1, 5, 2),
+    (257, 40, 1, 50, 3),
+    (1000, 1, 1, 0, 4),      # one key: one block
+    (1000, 10, 0, 100, 5),   # no key at all: every node a block
+    (0, 0, 0, 0, 6),
+])
+def test_merge_blocks(tmp_path, args):
+    # Algorithm 2's merged partition (Eq. merge) numbered by first
+    # occurrence, computed by host threads, against the sequential definition
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not available")
+    out = str(tmp_path / "merge_check")
+    src = os.path.join(HERE, "host", "merge_check.cpp")
+    base = ["g++", "-std=c++17", "-O1", "-g", "-pthread", src, "-o", out]
+    r = subprocess.run(base[:4] + ["-fsanitize=address"] + base[4:], capture_output=True)
+    if r.returncode != 0:
+        subprocess.run(base, check=True)
+    r = subprocess.run([out] + [str(a) for a in args], capture_output=True, text=True,
+                       timeout=120)
+    print(r.stdout, r.stderr)
+    assert r.returncode == 0, r.stdout + r.stderr
