@@ -12,8 +12,10 @@
 #include <algorithm>
 #include <chrono>
 #include <condition_variable>
+#include <deque>
 #include <functional>
 #include <mutex>
+#include <string>
 #include <memory>
 #include <new>
 #include <thread>
@@ -1493,8 +1495,10 @@ RefineLayout refine_layout(uint64_t n0, uint64_t mb) {
 
 // Device workspace of the quotient phase: block of every node, representative
 // flags, a chunk of rows (mq entries) and the sort state for mq keys.
+// Two sets of a chunk's input arrays: the rows of the next chunk are copied
+// into one while the device reduces the current chunk from the other.
 struct QuotLayout {
-  uint64_t blk, isrep, stage, rp, qoff, col, wt, core, total;
+  uint64_t blk, isrep, stage[2], rp[2], qoff[2], col[2], wt[2], core, total;
 };
 QuotLayout quot_layout(uint64_t n0, uint64_t mq) {
   QuotLayout L{};
@@ -1502,11 +1506,13 @@ QuotLayout quot_layout(uint64_t n0, uint64_t mq) {
   auto take = [&](uint64_t b) { uint64_t at = o; o = align_up(o + b); return at; };
   L.blk = take(4 * n0);
   L.isrep = take(n0 + 1);
-  L.stage = take(8 * (n0 + 1));
-  L.rp = take(8 * (n0 + 1));
-  L.qoff = take(8 * (n0 + 1));
-  L.col = take(4 * mq);
-  L.wt = take(4 * mq);
+  for (int i = 0; i < 2; ++i) {
+    L.stage[i] = take(8 * (n0 + 1));
+    L.rp[i] = take(8 * (n0 + 1));
+    L.qoff[i] = take(8 * (n0 + 1));
+    L.col[i] = take(4 * mq);
+    L.wt[i] = take(4 * mq);
+  }
   L.core = take(make_layout(mq, 0).total);
   L.total = o;
   return L;
@@ -1622,7 +1628,12 @@ class HostCopy {
       HIP_TRY(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s_));
       return WL_OK;
     }
-    if (int r = ensure()) return r;
+    if (!ensure()) {
+      // no page-locked staging: the runtime copies from pageable memory
+      HIP_TRY(hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s_));
+      HIP_TRY(hipStreamSynchronize(s_));
+      return WL_OK;
+    }
     for (uint64_t off = 0; off < bytes; off += kStage) {
       const uint64_t len = std::min(kStage, bytes - off);
       HIP_TRY(hipEventSynchronize(ev_[cur_]));
@@ -1642,7 +1653,11 @@ class HostCopy {
       HIP_TRY(hipStreamSynchronize(s_));
       return WL_OK;
     }
-    if (int r = ensure()) return r;
+    if (!ensure()) {
+      HIP_TRY(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToHost, s_));
+      HIP_TRY(hipStreamSynchronize(s_));
+      return WL_OK;
+    }
     int prev = -1;
     uint64_t prev_off = 0, prev_len = 0;
     for (uint64_t off = 0; off < bytes; off += kStage) {
@@ -1667,20 +1682,30 @@ class HostCopy {
   }
 
  private:
-  int ensure() {
+  // true when the two staging buffers exist; false (for good) when the
+  // page-locked memory is refused, and the copies go without them
+  bool ensure() {
+    if (direct_) return false;
     for (int i = 0; i < 2; ++i) {
       if (buf_[i]) continue;
-      hipError_t e = hipHostMalloc((void**)&buf_[i], kStage, hipHostMallocDefault);
-      if (e != hipSuccess) {
-        buf_[i] = nullptr;
+      if (hipHostMalloc((void**)&buf_[i], kStage, hipHostMallocDefault) != hipSuccess ||
+          hipEventCreateWithFlags(&ev_[i], hipEventDisableTiming) != hipSuccess ||
+          hipEventRecord(ev_[i], s_) != hipSuccess) {
         (void)hipGetLastError();
-        return fail(WL_ENOMEM, "page-locked staging buffer of %llu bytes: %s",
-                    (unsigned long long)kStage, hipGetErrorString(e));
+        for (int k = 0; k < 2; ++k) {
+          if (ev_[k]) {
+            (void)hipEventSynchronize(ev_[k]);
+            (void)hipEventDestroy(ev_[k]);
+            ev_[k] = nullptr;
+          }
+          if (buf_[k]) (void)hipHostFree(buf_[k]);
+          buf_[k] = nullptr;
+        }
+        direct_ = true;
+        return false;
       }
-      HIP_TRY(hipEventCreateWithFlags(&ev_[i], hipEventDisableTiming));
-      HIP_TRY(hipEventRecord(ev_[i], s_));
     }
-    return WL_OK;
+    return true;
   }
   void par_copy(void* d, const void* src, uint64_t len) {
     const unsigned t = len >= (4ull << 20) ? threads_ : 1;
@@ -1710,6 +1735,7 @@ class HostCopy {
   hipEvent_t ev_[2] = {nullptr, nullptr};
   int cur_ = 0;
   unsigned threads_ = 1;
+  bool direct_ = false;
 };
 
 int copy_rows_h2d(HostCopy& hc, const HostGraph& G, uint64_t r0, uint64_t nrows,
@@ -1757,7 +1783,7 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
                    std::vector<std::pair<uint32_t, uint64_t>>* spill,
                    std::vector<uint64_t>& hkey, std::vector<uint64_t>& hw,
                    std::vector<uint32_t>& hdeg, const std::vector<uint32_t>* seg = nullptr,
-                   double* tm = nullptr) {
+                   double* tm = nullptr, uint64_t* nd_out = nullptr) {
   // tm (diagnostics): adds the ms until the device's part is done, then the
   // ms of the copies out
   using clk = std::chrono::steady_clock;
@@ -1800,6 +1826,11 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
   if (S.host.err & kErrQuotientWeight)
     return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
   const uint32_t nd = S.host.k_new;
+  if (nd_out) {
+    // the caller copies the chunk's entries out (quotient_chunk_out)
+    *nd_out = nd;
+    return WL_OK;
+  }
   if (Q.m + nd > std::min(Q.cap, write_end))
     return fail(WL_EINVAL, "quotient larger than expected");
   if (int r = hc.d2h(Q.col + Q.m, D.col, 4ull * nd)) return r;
@@ -1812,6 +1843,22 @@ int quotient_chunk(Session& S, HostCopy& hc, const QuotDev& D, uint64_t nkeys,
   return WL_OK;
 }
 
+
+// The copies out of a reduced chunk (its nd distinct entries and the entry
+// counts of its nreps blocks, ids bfirst ...), appended to Q.
+int quotient_chunk_out(HostCopy& hc, const QuotDev& D, uint64_t nd, uint64_t nreps,
+                       uint32_t bfirst, uint64_t write_end, QuotientOut& Q,
+                       std::vector<uint32_t>& hdeg) {
+  if (Q.m + nd > std::min(Q.cap, write_end))
+    return fail(WL_EINVAL, "quotient larger than expected");
+  if (int r = hc.d2h(Q.col + Q.m, D.col, 4ull * nd)) return r;
+  if (int r = hc.d2h(Q.wt + Q.m, D.wt, 4ull * nd)) return r;
+  hdeg.resize(nreps);
+  if (int r = hc.d2h(hdeg.data(), D.deg(), 4ull * nreps)) return r;
+  for (uint64_t b = 0; b < nreps; ++b) Q.deg[bfirst + b] += hdeg[b];
+  Q.m += nd;
+  return WL_OK;
+}
 
 // ---------------------------------------------------------------------------
 // Algorithm 1 with the entries in host memory: the image of every round is
@@ -2202,6 +2249,21 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
   HostBuf qrp_buf, qcol_buf, qwt_buf;  // current quotient (G_t, t >= 1)
   HostBuf nrp_buf, ncol_buf, nwt_buf;  // G_1 under construction, new row pointers
   HostCopy hc(s);
+  // copy streams and staging of the quotient pipeline (kept over the outer
+  // iterations; page-locked memory is not given back and taken again)
+  struct QStreams {
+    hipStream_t in = nullptr, out = nullptr;
+    ~QStreams() {
+      for (hipStream_t x : {in, out})
+        if (x) {
+          (void)hipStreamSynchronize(x);
+          (void)hipStreamDestroy(x);
+        }
+    }
+  } qstr;
+  HIP_TRY(hipStreamCreateWithFlags(&qstr.in, hipStreamNonBlocking));
+  HIP_TRY(hipStreamCreateWithFlags(&qstr.out, hipStreamNonBlocking));
+  HostCopy hc_in(qstr.in), hc_out(qstr.out);
   uint64_t rounds = 0;
   uint32_t outer = 0;
   std::vector<uint32_t> key, loc;
@@ -2393,34 +2455,213 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     const QuotLayout QL = quot_layout(n, mq);
     uint32_t* blk_dev = (uint32_t*)(W + QL.blk);
     uint8_t* isrep_dev = W + QL.isrep;
-    const QuotDev D{(uint64_t*)(W + QL.rp), (uint64_t*)(W + QL.qoff), (uint32_t*)(W + QL.col),
-                    (uint32_t*)(W + QL.wt)};
-    uint64_t* rp_dev = D.rp;
-    uint64_t* qoff_dev = D.qoff;
-    uint32_t* col_dev = D.col;
-    uint32_t* wt_dev = D.wt;
+    const QuotDev Ds[2] = {
+        {(uint64_t*)(W + QL.rp[0]), (uint64_t*)(W + QL.qoff[0]), (uint32_t*)(W + QL.col[0]),
+         (uint32_t*)(W + QL.wt[0])},
+        {(uint64_t*)(W + QL.rp[1]), (uint64_t*)(W + QL.qoff[1]), (uint32_t*)(W + QL.col[1]),
+         (uint32_t*)(W + QL.wt[1])}};
     if (int r = hc.h2d(blk_dev, blk.data(), 4 * n)) return r;
     if (int r = hc.h2d(isrep_dev, isrep.data(), n)) return r;
-    std::vector<uint64_t> qoff;
-    std::vector<uint32_t> qseg;
-    double q_in_ms = 0, q_dev_ms = 0, q_tm[2] = {0, 0};
-    uint64_t q_chunks = 0;
-    uint64_t a = 0;
-    while (a < n) {
-      // rows [a, bnd) with at most mq entries, at least one row
-      uint64_t bnd = a + 1;
+    // chunks: row ranges [a, bnd) of at most mq entries, or one row longer
+    // than that (processed in pieces)
+    struct QChunk {
+      uint64_t a, bnd, ea, ent;
+    };
+    std::vector<QChunk> qch;
+    for (uint64_t a = 0; a < n;) {
       const uint64_t ea = G.rp(a);
-      {
-        uint64_t lo = a + 1, hi = n;  // last row end <= ea + mq
-        while (lo < hi) {
-          uint64_t mid = lo + (hi - lo + 1) / 2;
-          if (G.rp(mid) - ea <= mq) lo = mid; else hi = mid - 1;
-        }
-        bnd = lo;
+      uint64_t lo = a + 1, hi = n;  // last row end <= ea + mq (at least one row)
+      while (lo < hi) {
+        const uint64_t mid = lo + (hi - lo + 1) / 2;
+        if (G.rp(mid) - ea <= mq) lo = mid; else hi = mid - 1;
       }
-      const uint64_t ent = G.rp(bnd) - ea;
+      qch.push_back({a, lo, ea, G.rp(lo) - ea});
+      a = lo;
+    }
+    // Pipeline: a host thread prepares chunk j+1 (its key offsets, and the
+    // copies of its rows into input set (j+1) & 1 on a copy stream of its
+    // own) while this thread reduces chunk j from set j & 1.  A set is
+    // refilled only after the chunk that used it two steps before has been
+    // reduced and copied out.
+    struct QSet {
+      std::vector<uint64_t> qoff;
+      std::vector<uint32_t> qseg;
+      uint64_t run = 0, nreps = 0;
+      uint32_t bfirst = 0;
+    } qs[2];
+    struct QPipe {
+      std::mutex m;
+      std::condition_variable cv;
+      uint64_t prepared = 0, released = 0;
+      bool stop = false;
+      int err = WL_OK;
+      std::string msg;
+      hipStream_t cs = nullptr;
+      hipEvent_t ready[2] = {nullptr, nullptr};
+      std::thread th;
+      ~QPipe() {
+        {
+          std::lock_guard<std::mutex> g(m);
+          stop = true;
+        }
+        cv.notify_all();
+        if (th.joinable()) th.join();
+        if (cs) (void)hipStreamSynchronize(cs);
+        for (auto& e : ready)
+          if (e) (void)hipEventDestroy(e);
+      }
+    } qp;
+    qp.cs = qstr.in;
+    for (auto& e : qp.ready) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    auto prefetch = [&] {
+      HostCopy& hc2 = hc_in;
+      for (uint64_t j = 0; j < qch.size(); ++j) {
+        {
+          std::unique_lock<std::mutex> g(qp.m);
+          qp.cv.wait(g, [&] { return qp.stop || j < 2 || qp.released + 1 >= j; });
+          if (qp.stop) return;
+        }
+        const QChunk& c = qch[j];
+        const int st = (int)(j & 1);
+        QSet& q = qs[st];
+        int rc = WL_OK;
+        if (c.ent <= mq) {
+          const uint64_t nrows = c.bnd - c.a;
+          q.qoff.resize(nrows);
+          q.qseg.clear();
+          q.run = q.nreps = 0;
+          q.bfirst = 0xFFFFFFFFu;
+          for (uint64_t r = 0; r < nrows; ++r) {
+            q.qoff[r] = q.run;
+            if (isrep[c.a + r]) {
+              if (q.bfirst == 0xFFFFFFFFu) q.bfirst = blk[c.a + r];
+              const uint64_t d = G.rp(c.a + r + 1) - G.rp(c.a + r);
+              if (d) q.qseg.push_back((uint32_t)q.run);
+              q.run += d;
+              ++q.nreps;
+            }
+          }
+          q.qseg.push_back((uint32_t)q.run);
+          if (q.run > 0) {
+            const QuotDev& D = Ds[st];
+            rc = copy_rows_h2d(hc2, G, c.a, nrows, W + QL.stage[st], D.rp, qp.cs);
+            if (!rc) rc = hc2.h2d(D.qoff, q.qoff.data(), 8 * nrows);
+            if (!rc) rc = hc2.h2d(D.col, G.col + c.ea, 4 * c.ent);
+            if (!rc && G.wt) rc = hc2.h2d(D.wt, G.wt + c.ea, 4 * c.ent);
+            if (!rc && hipEventRecord(qp.ready[st], qp.cs) != hipSuccess)
+              rc = fail(WL_EHIP, "hipEventRecord failed");
+          }
+        }
+        std::lock_guard<std::mutex> g(qp.m);
+        if (rc) {
+          qp.err = rc;
+          qp.msg = g_err;
+          qp.stop = true;
+        }
+        qp.prepared = j + 1;
+        qp.cv.notify_all();
+        if (rc) return;
+      }
+    };
+    try {
+      qp.th = std::thread(prefetch);
+    } catch (...) {
+      return fail(WL_ENOMEM, "no host thread for the quotient copies");
+    }
+    // A second host thread copies the entries of reduced chunk j out (on a
+    // stream of its own) while this thread reduces chunk j+1; it releases the
+    // chunks' input sets in chunk order.
+    struct QJob {
+      uint64_t j, nd, nreps, write_end;
+      uint32_t bfirst;
+      bool copy;
+    };
+    struct QOut {
+      std::mutex m;
+      std::condition_variable cv;
+      std::deque<QJob> jobs;
+      uint64_t done = 0;
+      bool stop = false;
+      int err = WL_OK;
+      std::string msg;
+      hipStream_t cs = nullptr;
+      std::thread th;
+      ~QOut() {
+        {
+          std::lock_guard<std::mutex> g(m);
+          stop = true;
+        }
+        cv.notify_all();
+        if (th.joinable()) th.join();
+        if (cs) (void)hipStreamSynchronize(cs);
+      }
+    } qo;
+    qo.cs = qstr.out;
+    auto drain = [&] {
+      HostCopy& hc3 = hc_out;
+      std::vector<uint32_t> hdeg3;
+      for (;;) {
+        QJob jb;
+        {
+          std::unique_lock<std::mutex> g(qo.m);
+          qo.cv.wait(g, [&] { return qo.stop || !qo.jobs.empty(); });
+          if (qo.jobs.empty()) return;
+          jb = qo.jobs.front();
+          qo.jobs.pop_front();
+        }
+        int rc = WL_OK;
+        if (jb.copy)
+          rc = quotient_chunk_out(hc3, Ds[jb.j & 1], jb.nd, jb.nreps, jb.bfirst, jb.write_end, Q,
+                                  hdeg3);
+        {
+          std::lock_guard<std::mutex> g(qo.m);
+          if (rc) {
+            qo.err = rc;
+            qo.msg = g_err;
+          }
+          qo.done = jb.j + 1;
+          qo.cv.notify_all();
+        }
+        {
+          std::lock_guard<std::mutex> g(qp.m);
+          qp.released = jb.j + 1;
+          qp.cv.notify_all();
+        }
+        if (rc) return;
+      }
+    };
+    try {
+      qo.th = std::thread(drain);
+    } catch (...) {
+      return fail(WL_ENOMEM, "no host thread for the quotient copies");
+    }
+    auto push_job = [&](const QJob& jb) {
+      std::lock_guard<std::mutex> g(qo.m);
+      qo.jobs.push_back(jb);
+      qo.cv.notify_all();
+    };
+    // waits until the copies out of every chunk before j are done
+    auto wait_out = [&](uint64_t j) -> int {
+      std::unique_lock<std::mutex> g(qo.m);
+      qo.cv.wait(g, [&] { return qo.err != WL_OK || qo.done >= j; });
+      return qo.err;
+    };
+    double q_dev_ms = 0, q_tm[2] = {0, 0};
+    uint64_t q_chunks = 0;
+    for (uint64_t j = 0; j < qch.size(); ++j) {
+      {
+        std::unique_lock<std::mutex> g(qp.m);
+        qp.cv.wait(g, [&] { return qp.err != WL_OK || qp.prepared > j; });
+        if (qp.err != WL_OK) return fail(qp.err, "%s", qp.msg.c_str());
+      }
+      const QChunk& c = qch[j];
+      const int st = (int)(j & 1);
+      const QuotDev& D = Ds[st];
+      const uint64_t a = c.a, ea = c.ea, ent = c.ent;
       if (ent > mq) {
         // a single row longer than the chunk: pieces, merged on the host
+        // (after the copies out of the chunks before it: Q grows in order)
+        if (wait_out(j)) return fail(qo.err, "%s", qo.msg.c_str());
         if (isrep[a]) {
           std::vector<std::pair<uint32_t, uint64_t>> spill;
           for (uint64_t off = 0; off < ent; off += mq) {
@@ -2428,25 +2669,24 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
             piece_rp[0] = 0;
             piece_rp[1] = len;
             piece_rp[2] = 0;
-            if (int r = hc.h2d(rp_dev, piece_rp.data(), 16)) return r;
-            if (int r = hc.h2d(qoff_dev, piece_rp.data() + 2, 8)) return r;
+            if (int r = hc.h2d(D.rp, piece_rp.data(), 16)) return r;
+            if (int r = hc.h2d(D.qoff, piece_rp.data() + 2, 8)) return r;
             HIP_TRY(hipStreamSynchronize(s));
-            if (int r = hc.h2d(col_dev, G.col + ea + off, 4 * len)) return r;
+            if (int r = hc.h2d(D.col, G.col + ea + off, 4 * len)) return r;
             if (G.wt)
-              if (int r = hc.h2d(wt_dev, G.wt + ea + off, 4 * len)) return r;
+              if (int r = hc.h2d(D.wt, G.wt + ea + off, 4 * len)) return r;
             wl_csr sg{};
             sg.n = len;
             sg.nnz = 0;
-            sg.row_ptr64 = rp_dev;
+            sg.row_ptr64 = D.rp;
             Session S;
             if (int r = open_session(S, &sg, nullptr, W + QL.core, QL.total - QL.core, s))
               return r;
             S.ctx.keys_mat = 1;
             if (int r = S.init_state(0, 1, 0, 1, 1)) return r;
             hipLaunchKernelGGL(k_q_keys, dim3(grid_for(len, kBlock, 8192)), dim3(kBlock), 0, s,
-                               S.ctx, rp_dev,
-                               col_dev, G.wt ? wt_dev : nullptr, blk_dev, isrep_dev,
-                               qoff_dev, 1u, (uint32_t)a, blk[a]);
+                               S.ctx, D.rp, D.col, G.wt ? D.wt : nullptr, blk_dev, isrep_dev,
+                               D.qoff, 1u, (uint32_t)a, blk[a]);
             HIP_LAUNCH_CHECK();
             if (int r = quotient_chunk(S, hc, D, len, 1, blk[a], ea + ent, Q, &spill, hkey, hw,
                                        hdeg))
@@ -2454,9 +2694,9 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
           }
           std::sort(spill.begin(), spill.end());
           for (size_t i = 0; i < spill.size();) {
-            size_t j = i;
+            size_t k2 = i;
             uint64_t w = 0;
-            while (j < spill.size() && spill[j].first == spill[i].first) w += spill[j++].second;
+            while (k2 < spill.size() && spill[k2].first == spill[i].first) w += spill[k2++].second;
             if (w > 0xFFFFFFFFull) return fail(WL_EOVERFLOW, "a quotient weight exceeds 2^32 - 1");
             if (Q.m >= std::min(Q.cap, ea + ent))
               return fail(WL_EINVAL, "quotient larger than expected");
@@ -2464,67 +2704,55 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
             Q.col[Q.m] = spill[i].first;
             Q.wt[Q.m] = (uint32_t)w;
             Q.m++;
-            i = j;
+            i = k2;
           }
         }
-        a = a + 1;
-        continue;
-      }
-      const uint64_t nrows = bnd - a;
-      qoff.resize(nrows);
-      qseg.clear();
-      uint64_t run = 0, nreps = 0;
-      uint32_t bfirst = 0xFFFFFFFFu;
-      for (uint64_t r = 0; r < nrows; ++r) {
-        qoff[r] = run;
-        if (isrep[a + r]) {
-          if (bfirst == 0xFFFFFFFFu) bfirst = blk[a + r];
-          const uint64_t d = G.rp(a + r + 1) - G.rp(a + r);
-          if (d) qseg.push_back((uint32_t)run);
-          run += d;
-          ++nreps;
-        }
-      }
-      qseg.push_back((uint32_t)run);
-      if (run > 0) {
+        push_job({j, 0, 0, 0, 0, false});
+      } else if (qs[st].run > 0) {
+        const QSet& q = qs[st];
+        const uint64_t nrows = c.bnd - a;
         clk::time_point tq = clk::now();
         ++q_chunks;
-        if (int r = copy_rows_h2d(hc, G, a, nrows, W + QL.stage, rp_dev, s)) return r;
-        if (int r = hc.h2d(qoff_dev, qoff.data(), 8 * nrows)) return r;
-        if (int r = hc.h2d(col_dev, G.col + ea, 4 * ent)) return r;
-        if (G.wt)
-          if (int r = hc.h2d(wt_dev, G.wt + ea, 4 * ent)) return r;
-        if (trace) {
-          HIP_TRY(hipStreamSynchronize(s));
-          q_in_ms += ms_since(tq);
-          tq = clk::now();
-        }
+        HIP_TRY(hipStreamWaitEvent(s, qp.ready[st], 0));
         wl_csr sg{};
-        sg.n = run;
+        sg.n = q.run;
         sg.nnz = 0;
-        sg.row_ptr64 = rp_dev;
+        sg.row_ptr64 = D.rp;
         Session S;
         if (int r = open_session(S, &sg, nullptr, W + QL.core, QL.total - QL.core, s))
           return r;
         S.ctx.keys_mat = 1;
         if (int r = S.init_state(0, 1, 0, 1, 1)) return r;
         hipLaunchKernelGGL(k_q_keys, dim3(grid_for(ent, kBlock, 8192)),
-                           dim3(kBlock), 0, s, S.ctx, rp_dev, col_dev,
-                           G.wt ? wt_dev : nullptr, blk_dev, isrep_dev, qoff_dev,
-                           (uint32_t)nrows, (uint32_t)a, bfirst);
+                           dim3(kBlock), 0, s, S.ctx, D.rp, D.col,
+                           G.wt ? D.wt : nullptr, blk_dev, isrep_dev, D.qoff,
+                           (uint32_t)nrows, (uint32_t)a, q.bfirst);
         HIP_LAUNCH_CHECK();
-        if (int r = quotient_chunk(S, hc, D, run, nreps, bfirst, ea + ent, Q, nullptr, hkey,
-                                   hw, hdeg, &qseg, trace ? q_tm : nullptr))
+        uint64_t nd = 0;
+        if (int r = quotient_chunk(S, hc, D, q.run, q.nreps, q.bfirst, ea + ent, Q, nullptr,
+                                   hkey, hw, hdeg, &q.qseg, trace ? q_tm : nullptr, &nd))
           return r;
         if (trace) q_dev_ms += ms_since(tq);
+        push_job({j, nd, q.nreps, ea + ent, q.bfirst, true});
+      } else {
+        push_job({j, 0, 0, 0, 0, false});
       }
-      a = bnd;
+      // the device must not start chunk j+1 before the copies out of chunk
+      // j-1 (its input set) are done: the prefetcher waits for that; a
+      // failed copy ends the loop here
+      {
+        std::lock_guard<std::mutex> g(qo.m);
+        if (qo.err != WL_OK) return fail(qo.err, "%s", qo.msg.c_str());
+      }
     }
+    if (wait_out(qch.size())) return fail(qo.err, "%s", qo.msg.c_str());
+    qp.th.join();
+    if (qp.err != WL_OK) return fail(qp.err, "%s", qp.msg.c_str());
     if (trace) {
-      fprintf(stderr, "[wl batched] t=%llu quotient: %llu chunks, copies in %.1f ms, device "
+      fprintf(stderr, "[wl batched] t=%llu quotient: %llu chunks, waiting for copies in, device "
               "and copies out %.1f ms (device %.1f, out %.1f), %.1f ms since the last line\n",
-              (unsigned long long)t, (unsigned long long)q_chunks, q_in_ms, q_dev_ms, q_tm[0],
-              q_tm[1], ms_since(t_phase));
+              (unsigned long long)t, (unsigned long long)q_chunks, q_dev_ms, q_tm[0], q_tm[1],
+              ms_since(t_phase));
       t_phase = clk::now();
     }
     // new row pointers and labels
