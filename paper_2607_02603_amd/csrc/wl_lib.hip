@@ -1603,6 +1603,10 @@ class HostCopy {
  public:
   static constexpr uint64_t kStage = 64ull << 20;
   explicit HostCopy(hipStream_t s) : s_(s) {
+    // WL_HOST_STAGING=0: copy pageable memory without the staging buffers,
+    // as when page-locked memory is refused
+    const char* st = getenv("WL_HOST_STAGING");
+    direct_ = st && st[0] == '0';
     cpu_set_t set;
     CPU_ZERO(&set);
     unsigned t = 4;

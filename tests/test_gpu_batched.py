@@ -177,3 +177,21 @@ def test_rmat20_several_outer_iterations():
     assert outer >= 2
     again = wl.wl_stable_coloring_batched(_host_graph(g.row_ptr, g.col), None, 0, mb)
     assert np.array_equal(again[0].numpy().view(np.uint32), got)
+
+
+def test_pageable_copies_without_staging(monkeypatch):
+    # the copies from and to pageable memory as they run when page-locked
+    # staging is refused (Algorithm 2's batches and quotients, the exact
+    # finish and the streamed rounds)
+    monkeypatch.setenv("WL_HOST_STAGING", "0")
+    g = inputs.rmat(12, 8, seed=5)
+    for mb in (3000, 40000):
+        _check(g.row_ptr, g.col, mb=mb, seed=2, pinned=False)
+    hg = _host_graph(g.row_ptr, g.col, pinned=False)
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(hg, None, 0, 5000,
+                                                             options=wl.WL_BATCHED_EXACT)
+    ref = oracle.first_occurrence(oracle.stable_coloring(g.row_ptr, g.col, None, None, 0)[0])[0]
+    assert coarsest and np.array_equal(c.numpy().view(np.uint32), ref)
+    c, k, r = wl.wl_stable_coloring_streamed(hg, None, 3)
+    co, ko, ro, _, _ = oracle.stable_coloring(g.row_ptr, g.col, None, None, 3)
+    assert (k, r) == (ko, ro) and np.array_equal(c.numpy().view(np.uint32), co)
