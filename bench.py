@@ -206,6 +206,32 @@ def study_reduction(args):
           flush=True)
 
 
+def oracle_timing(args):
+    """The CPU oracle on the configurations it finishes in minutes, on this
+    host's cores: Algorithm 1 (oracle (a)) and classic refinement (oracle
+    (b)) to the stable colouring, whole runs, timed around the call.  The
+    thread count is OMP_NUM_THREADS (the oracle's images are OpenMP loops;
+    its sorts run on one thread).  One JSON line per run."""
+    if args.oracle_threads:
+        os.environ["OMP_NUM_THREADS"] = str(args.oracle_threads)
+    import oracle
+    from paper_2607_02603_amd import inputs
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    cfgs = [("C1 ER n=20000 m=80000", inputs.er_graph, ("a", "b")),
+            ("C2 grid 1024x1024", lambda: inputs.grid_graph(1024), ("a", "b")),
+            ("C3 Chung-Lu n=4e6", inputs.chung_lu, ("a",))]
+    for name, gen, which in cfgs:
+        g = gen()
+        for w in which:
+            f = oracle.stable_coloring if w == "a" else oracle.classic_coloring
+            t0 = time.perf_counter()
+            r = f(g.row_ptr, g.col)
+            dt = time.perf_counter() - t0
+            print(json.dumps({"oracle": w, "config": name, "n": g.n, "nnz": g.nnz,
+                              "colours": r[1], "rounds": r[2], "seconds": dt,
+                              "threads": threads}), flush=True)
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -317,6 +343,10 @@ def main():
     ap.add_argument("--study", choices=["reduction"],
                     help="instead of the benchmark: the reduction-quality study of "
                          "Algorithm 2 (N_b = 1, 2, 4) on synthetic graphs")
+    ap.add_argument("--oracle-timing", action="store_true",
+                    help="instead of the benchmark: time the CPU oracles on C1-C3")
+    ap.add_argument("--oracle-threads", type=int, default=0,
+                    help="--oracle-timing: OMP_NUM_THREADS for the oracle (0: as set)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="first copy 1 GiB device-to-device (a plain copy kernel of "
                          "known size, to calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE)")
@@ -326,6 +356,8 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
+    if args.oracle_timing:
+        return oracle_timing(args)
     import paper_2607_02603_amd as wl
     wl.wl_set_precision(ARITH[args.arith][0])
     if args.study == "reduction":
