@@ -34,6 +34,9 @@ WORKLOADS = {
     "rmat28b": dict(desc="R-MAT scale 28, edge factor 32, (0.57,0.19,0.19,0.05), "
                          "symmetrised+dedup, seed 0, CSR in pinned host memory, "
                          "under a 32 GiB device workspace"),
+    "rmat29s": dict(desc="R-MAT scale 29, edge factor 32, (0.57,0.19,0.19,0.05), "
+                         "symmetrised+dedup, seed 0, CSR in pageable host memory, "
+                         "streamed workspace plus 8 GiB"),
 }
 
 # Arithmetic of the image step (--arith): the prime field of the default
@@ -54,19 +57,31 @@ BATCHED_MODES = {
 
 
 def bench_batched(args):
-    """Algorithm 2 on R-MAT scale 28 held in pinned host memory, 32 GiB of
-    device workspace; optionally checked against the in-core colouring."""
+    """Out of core: R-MAT scale 28 held in pinned host memory under 32 GiB of
+    device workspace (Algorithm 2 or the streamed Algorithm 1), or R-MAT
+    scale 29 (over 3e10 entries) in pageable host memory, streamed, with the
+    workspace that mode asks for; optionally checked against the in-core
+    colouring of the same graph copied to HBM."""
     import torch
     import paper_2607_02603_amd as wl
     from paper_2607_02603_amd import inputs
     dev = torch.device("cuda:0")
+    big = args.workload == "rmat29s"
+    if big and args.batched_mode != "streamed":
+        raise SystemExit("rmat29s runs the streamed mode only")
     t0 = time.perf_counter()
-    g = inputs.rmat(28, 32, device=dev, host_out=True)
+    if big:
+        g = inputs.rmat(29, 32, device=dev, host_out=True, pinned=False)
+    else:
+        g = inputs.rmat(28, 32, device=dev, host_out=True)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    log(f"graph rmat28 (host): n={g.n} nnz={g.nnz} built in {time.perf_counter() - t0:.1f}s")
+    log(f"graph {args.workload} (host): n={g.n} nnz={g.nnz} built in "
+        f"{time.perf_counter() - t0:.1f}s")
     hg = wl.Graph(g.n, g.row_ptr, g.col)
-    ws = wl.workspace(32 << 30, dev)
+    # R-MAT 29: the streamed mode's workspace and 8 GiB more, in which the
+    # rounds after the full one keep their chunks on the device
+    ws = wl.workspace(wl.wl_streamed_workspace_size(hg) + (8 << 30) if big else 32 << 30, dev)
     mode = args.batched_mode
     opts = {"plain": 0, "exact": wl.WL_BATCHED_EXACT,
             "exact-early": wl.WL_BATCHED_EXACT | wl.WL_BATCHED_EARLY_STOP}.get(mode)
@@ -130,7 +145,7 @@ def bench_batched(args):
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": step_s * 1e3, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "u64", "data": "synthetic",
-        "config": {"workload": WORKLOADS["rmat28b"]["desc"] + ", " + BATCHED_MODES[mode],
+        "config": {"workload": WORKLOADS[args.workload]["desc"] + ", " + BATCHED_MODES[mode],
                    "mode": mode, "arithmetic": ARITH[args.arith][1], "n": g.n, "nnz": g.nnz,
                    "colours": k, "rounds_summed_over_batches": rounds,
                    "outer_iterations": outer, "coarsest": coarsest,
@@ -362,7 +377,7 @@ def main():
     wl.wl_set_precision(ARITH[args.arith][0])
     if args.study == "reduction":
         return study_reduction(args)
-    if args.workload == "rmat28b":
+    if args.workload in ("rmat28b", "rmat29s"):
         return bench_batched(args)
     import torch
     dev = torch.device("cuda:0")

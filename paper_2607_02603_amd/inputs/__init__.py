@@ -220,12 +220,14 @@ def rmat_thresholds(abcd):
 
 
 def rmat(scale=27, edge_factor=16, abcd=(0.57, 0.19, 0.19, 0.05), seed=0,
-         device="cpu", host_out=False, directed=False):
+         device="cpu", host_out=False, directed=False, pinned=True):
     """R-MAT, edge_factor * 2^scale samples, seeded vertex bijection, self-loops
     dropped, symmetrised, deduplicated.  device='cuda' generates on the GPU;
     with host_out=True the CSR is returned in pinned host memory and the
     device never holds more than a group of buckets (for graphs larger than
-    HBM).  directed=True (host generation only) keeps each sample as the one
+    HBM; pinned=False puts it in pageable memory instead, for graphs larger
+    than the page-locked memory a process may hold).  directed=True (host
+    generation only) keeps each sample as the one
     entry u -> v, as for a web graph: out- and in-degrees are both skewed and
     many nodes have no out-edge."""
     n = 1 << scale
@@ -244,11 +246,11 @@ def rmat(scale=27, edge_factor=16, abcd=(0.57, 0.19, 0.19, 0.05), seed=0,
     def emit(phase, shift, nbk, blo, bhi, arr, keys, stream):
         return _gpu().gen_rmat_gpu(phase, scale, seed, ta, tab, tabc, 0, samples, shift,
                                    nbk, blo, bhi, arr, keys, stream)
-    return _gpu_build(n, scale, 2 * samples, emit, name, device, host_out)
+    return _gpu_build(n, scale, 2 * samples, emit, name, device, host_out, pinned=pinned)
 
 
 def _gpu_build(n, nbits, max_keys, emit, name, device, host_out=False,
-               group_keys=1 << 31):
+               group_keys=1 << 31, pinned=True):
     """Bucketed generation on the GPU: count, then per group of buckets
     scatter + per bucket sort + unique + row counts (torch ops).  Returns a
     CSR with row_ptr int64 (uint64 values) and col int32 (uint32 values), on
@@ -305,10 +307,11 @@ def _gpu_build(n, nbits, max_keys, emit, name, device, host_out=False,
     if host_out:
         # page-locked memory is capped per process: take exactly nnz entries
         del row_cnt
-        rp_h = pinned_empty(n + 1, torch.int64)
+        alloc = pinned_empty if pinned else (lambda c, dt: torch.empty(c, dtype=dt))
+        rp_h = alloc(n + 1, torch.int64)
         rp_h.copy_(rp)
         del rp
-        col_h = pinned_empty(pos, torch.int32)
+        col_h = alloc(pos, torch.int32)
         at = 0
         for c in cols:
             col_h[at:at + c.numel()].copy_(c)
