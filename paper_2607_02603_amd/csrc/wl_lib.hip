@@ -2567,8 +2567,20 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
         if (rc) return;
       }
     };
+    // a host allocation failing inside the thread ends it with WL_ENOMEM
+    auto prefetch_guarded = [&] {
+      try {
+        prefetch();
+      } catch (...) {
+        std::lock_guard<std::mutex> g(qp.m);
+        qp.err = WL_ENOMEM;
+        qp.msg = "host allocation failed while preparing a quotient chunk";
+        qp.stop = true;
+        qp.cv.notify_all();
+      }
+    };
     try {
-      qp.th = std::thread(prefetch);
+      qp.th = std::thread(prefetch_guarded);
     } catch (...) {
       return fail(WL_ENOMEM, "no host thread for the quotient copies");
     }
@@ -2627,15 +2639,40 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
           qo.cv.notify_all();
         }
         {
+          // a failed copy also stops the preparation and wakes this thread's
+          // partner waiting for the next chunk
           std::lock_guard<std::mutex> g(qp.m);
           qp.released = jb.j + 1;
+          if (rc) {
+            qp.err = rc;
+            qp.msg = g_err;
+            qp.stop = true;
+          }
           qp.cv.notify_all();
         }
         if (rc) return;
       }
     };
+    auto drain_guarded = [&] {
+      try {
+        drain();
+      } catch (...) {
+        const char* msg = "host allocation failed while copying a quotient chunk out";
+        {
+          std::lock_guard<std::mutex> g(qo.m);
+          qo.err = WL_ENOMEM;
+          qo.msg = msg;
+          qo.cv.notify_all();
+        }
+        std::lock_guard<std::mutex> g(qp.m);
+        qp.err = WL_ENOMEM;
+        qp.msg = msg;
+        qp.stop = true;
+        qp.cv.notify_all();
+      }
+    };
     try {
-      qo.th = std::thread(drain);
+      qo.th = std::thread(drain_guarded);
     } catch (...) {
       return fail(WL_ENOMEM, "no host thread for the quotient copies");
     }
