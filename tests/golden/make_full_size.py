@@ -1,6 +1,7 @@
 """Writes the expected results of the full-size workloads from the CPU oracle.
 
     python tests/golden/make_full_size.py chunglu rmat27
+    python tests/golden/make_full_size.py --ring64 rmat27
 
 For each workload: the seeded graph from the shared input generators (built on
 the GPU, which produces byte-identical CSRs to the CPU build of the same
@@ -9,7 +10,9 @@ trivial partition with seed 0.  Stored per workload in
 tests/golden/full_<name>.json: n, nnz, a checksum of the CSR, the colour
 count after every round, the round count, the final colour count, the SHA-256
 of the final colour array (uint32 little-endian) and the colours of 4096
-seeded sample nodes.  Nothing here calls the HIP library.
+seeded sample nodes.  With --ring64 the oracle computes in the ring Z/2^64
+(Algorithm 1 with precision q = 64) and the file is full_<name>_ring64.json.
+Nothing here calls the HIP library.
 """
 import hashlib
 import json
@@ -61,7 +64,7 @@ def csr_checksum(rp, col):
     return [int(acc), int(rsum)]
 
 
-def run(name):
+def run(name, q=0):
     say(f"{name}: generating")
     rp, col = build(name)
     n = rp.size - 1
@@ -71,7 +74,7 @@ def run(name):
     r = 0
     while True:
         t0 = time.time()
-        c2, k2, _ = oracle.refine_round(rp, col, None, c, k, 0, r)
+        c2, k2, _ = oracle.refine_round(rp, col, None, c, k, 0, r, q)
         r += 1
         hist.append(k2)
         say(f"{name}: round {r - 1}: {k} -> {k2} colours ({time.time() - t0:.1f} s)")
@@ -88,12 +91,17 @@ def run(name):
         "sample_nodes": sample.tolist(), "sample_colours": c[sample].astype(int).tolist(),
         "written_by": "tests/golden/make_full_size.py (oracle/ only)",
     }
-    path = os.path.join(HERE, f"full_{name}.json")
+    if q:
+        out["arithmetic"] = "Z/2^64"
+    path = os.path.join(HERE, f"full_{name}{'_ring64' if q else ''}.json")
     with open(path, "w") as f:
         json.dump(out, f)
     say(f"{name}: wrote {path}: colours={k} rounds={r}")
 
 
 if __name__ == "__main__":
-    for nm in sys.argv[1:] or list(WORKLOADS):
-        run(nm)
+    args = sys.argv[1:]
+    q = oracle.RING64 if "--ring64" in args else oracle.FP
+    names = [a for a in args if not a.startswith("--")]
+    for nm in names or list(WORKLOADS):
+        run(nm, q)

@@ -55,3 +55,25 @@ def test_full_size_bit_exact(name):
     assert np.array_equal(host[idx], np.asarray(gold["sample_colours"], np.uint32))
     assert hashlib.sha256(host.astype("<u4").tobytes()).hexdigest() == gold["sha256"]
     assert wl.wl_verify_stable(g, colors, k, ws=ws)
+
+
+def test_full_size_ring64_bit_exact():
+    # R-MAT scale 27 in the ring Z/2^64 (precision q = 64) against the
+    # oracle's results in the same arithmetic; the partition equals F_p's
+    gold = _golden("rmat27_ring64")
+    gold_fp = _golden("rmat27")
+    print("rmat27 ring64: generating", flush=True)
+    g = _graph("rmat27")
+    assert (g.n, g.nnz) == (gold["n"], gold["nnz"])
+    ws = wl.workspace(max(wl.wl_workspace_size(g), wl.wl_verify_workspace_size(g)))
+    with wl.precision(wl.WL_PRECISION_RING64):
+        colors, k, rounds = wl.wl_stable_coloring(g, None, 0, 0, ws=ws)
+    torch.cuda.synchronize()
+    print(f"rmat27 ring64: colours={k} rounds={rounds}", flush=True)
+    assert (k, rounds) == (gold["colours"], gold["rounds"])
+    assert (k, rounds) == (gold_fp["colours"], gold_fp["rounds"])
+    host = colors.cpu().numpy().view(np.uint32)
+    idx = np.asarray(gold["sample_nodes"], np.int64)
+    assert np.array_equal(host[idx], np.asarray(gold["sample_colours"], np.uint32))
+    assert hashlib.sha256(host.astype("<u4").tobytes()).hexdigest() == gold["sha256"]
+    assert wl.wl_verify_stable(g, colors, k, ws=ws)
