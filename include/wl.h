@@ -297,6 +297,24 @@ typedef struct wl_stats {
 int wl_stats_enable(int flags);
 int wl_stats_get(wl_stats *out);
 
+/* Environment variables read by the library (tuning and diagnostics; none
+ * changes a result):
+ *   WL_VALIDATE=1        device checks of the graph (see the conventions).
+ *   WL_PB=0 | force      propagation blocking off, or on whenever possible
+ *                        (default: on when at least half the entries feed
+ *                        rows whose image is needed).
+ *   WL_DEGREE_ROUND=0    no histogram round from one colour.
+ *   WL_HOST_ROUNDS=n     rounds driven from the host before the device-driven
+ *                        ones (default 8).
+ *   WL_ASYNC_PASSES=n    radix passes a device-driven round launches (0-8).
+ *   WL_GRAPH=1           replay the device-driven rounds from a HIP graph.
+ *   WL_NT_STREAM=1       non-temporal loads of the column indices.
+ *   WL_HOST_STAGING=0    copy pageable host memory without page-locked
+ *                        staging buffers (as when they are refused).
+ *   WL_TRACE_STREAMED=1, WL_TRACE_BATCHED=1
+ *                        per-round (per outer iteration) host-side timings
+ *                        of the streamed rounds (of Algorithm 2) on stderr. */
+
 #ifdef __cplusplus
 }
 #endif
