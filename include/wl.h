@@ -154,9 +154,13 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
  *   workspace   device, 256-byte aligned.  wl_streamed_workspace_size()
  *               gives the size with full chunks (about 69 bytes per node
  *               plus two chunks); a smaller one, down to chunks of 4096
- *               entries, is accepted.  Its contents are scratch.
+ *               entries, is accepted.  Room beyond that size is used too:
+ *               once all chunks of a round fit there, they are kept and the
+ *               later rounds need no transfers.  Its contents are scratch.
  * The call also allocates about 2 x 13 bytes (17 weighted) per chunk entry
- * of page-locked host memory, plus 5 bytes per node, freed on return.
+ * of page-locked host memory, and up to about 25 bytes per node of pageable
+ * host memory (the rows a round needs and their segment offsets), freed on
+ * return.
  * Errors: WL_EINVAL, WL_EBUDGET, WL_EOVERFLOW, WL_EMAXROUNDS, WL_ENOMEM,
  * WL_EHIP. */
 int wl_streamed_workspace_size(const wl_csr *g, uint64_t *bytes_out);
