@@ -215,8 +215,11 @@ int wl_get_precision(uint32_t *q);
  * of the two quotients alive at a time).  Needs n < 2^30.
  *   g_host      host CSR, pageable or page-locked.  Page-locked arrays are
  *               copied to the device by DMA directly; pageable ones (and the
- *               library's quotients) through two page-locked staging buffers
- *               of 64 MiB that the call allocates.
+ *               library's quotients) through page-locked staging buffers of
+ *               64 MiB that the call allocates (two per copy stream: the
+ *               quotient's copies in and out run on two host threads and
+ *               streams of their own, overlapped with the device's work;
+ *               without page-locked memory the copies go unstaged).
  *   init_host   host labels or NULL (trivial partition).
  *   max_batch_entries  cap M_b on entries per batch; 0 = the largest cap the
  *               workspace allows.  Batches are contiguous CSR entry ranges
