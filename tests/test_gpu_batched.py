@@ -177,6 +177,15 @@ def test_rmat20_several_outer_iterations():
     assert outer >= 2
     again = wl.wl_stable_coloring_batched(_host_graph(g.row_ptr, g.col), None, 0, mb)
     assert np.array_equal(again[0].numpy().view(np.uint32), got)
+    # with the exact finish, after the fixed point or the early stop: the
+    # coarsest colouring (the quotient pipeline's chunks, then the streamed
+    # rounds on a weighted quotient)
+    ref = oracle.first_occurrence(oracle.stable_coloring(g.row_ptr, g.col, None, None, 0)[0])[0]
+    for opt in (wl.WL_BATCHED_EXACT, wl.WL_BATCHED_EXACT | wl.WL_BATCHED_EARLY_STOP):
+        c, k2, r2, outer2, co = wl.wl_stable_coloring_batched(_host_graph(g.row_ptr, g.col),
+                                                              None, 0, mb, options=opt)
+        print(f"rmat20 options={opt}: outer={outer2} colours={k2}", flush=True)
+        assert co and np.array_equal(c.numpy().view(np.uint32), ref)
 
 
 def test_pageable_copies_without_staging(monkeypatch):
