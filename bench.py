@@ -223,28 +223,34 @@ def study_reduction(args):
 
 def oracle_timing(args):
     """The CPU oracle on the configurations it finishes in minutes, on this
-    host's cores: Algorithm 1 (oracle (a)) and classic refinement (oracle
-    (b)) to the stable colouring, whole runs, timed around the call.  The
-    thread count is OMP_NUM_THREADS (the oracle's images are OpenMP loops;
-    its sorts run on one thread).  One JSON line per run."""
+    host's cores: Algorithm 1 (oracle (a)), classic refinement (oracle (b))
+    and splitter-based refinement (oracle (b'), one thread, no rounds) to
+    the stable colouring, whole runs, timed around the call.  The thread
+    count is OMP_NUM_THREADS (the oracle's images are OpenMP loops; its
+    sorts run on one thread).  One JSON line per run."""
     if args.oracle_threads:
         os.environ["OMP_NUM_THREADS"] = str(args.oracle_threads)
     import oracle
     from paper_2607_02603_amd import inputs
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    cfgs = [("C1 ER n=20000 m=80000", inputs.er_graph, ("a", "b")),
-            ("C2 grid 1024x1024", lambda: inputs.grid_graph(1024), ("a", "b")),
-            ("C3 Chung-Lu n=4e6", inputs.chung_lu, ("a",))]
+    cfgs = [("C1 ER n=20000 m=80000", inputs.er_graph, ("a", "b", "b'")),
+            ("C2 grid 1024x1024", lambda: inputs.grid_graph(1024), ("a", "b", "b'")),
+            ("C3 Chung-Lu n=4e6", inputs.chung_lu, ("a", "b'"))]
     for name, gen, which in cfgs:
         g = gen()
         for w in which:
-            f = oracle.stable_coloring if w == "a" else oracle.classic_coloring
+            f = {"a": oracle.stable_coloring, "b": oracle.classic_coloring,
+                 "b'": oracle.splitter_coloring}[w]
             t0 = time.perf_counter()
             r = f(g.row_ptr, g.col)
             dt = time.perf_counter() - t0
-            print(json.dumps({"oracle": w, "config": name, "n": g.n, "nnz": g.nnz,
-                              "colours": r[1], "rounds": r[2], "seconds": dt,
-                              "threads": threads}), flush=True)
+            rec = {"oracle": w, "config": name, "n": g.n, "nnz": g.nnz, "colours": r[1],
+                   "seconds": dt, "threads": 1 if w == "b'" else threads}
+            if w == "b'":
+                rec["splitter_visits"] = r[2]
+            else:
+                rec["rounds"] = r[2]
+            print(json.dumps(rec), flush=True)
 
 
 def log(msg):

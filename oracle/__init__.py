@@ -74,6 +74,8 @@ def _lib():
         lib.orc_classic_round.argtypes = [u64, vp, vp, vp, vp, vp]
         lib.orc_classic_coloring.restype = ctypes.c_int
         lib.orc_classic_coloring.argtypes = [u64, vp, vp, vp, vp, u32, vp, vp, vp, vp]
+        lib.orc_splitter_coloring.restype = ctypes.c_int
+        lib.orc_splitter_coloring.argtypes = [u64, vp, vp, vp, vp, vp, vp, vp]
         lib.orc_is_stable.restype = ctypes.c_int
         lib.orc_is_stable.argtypes = [u64, vp, vp, vp, vp, u32]
         lib.orc_first_occurrence.restype = u32
@@ -223,6 +225,28 @@ def classic_coloring(row_ptr, col, weight_=None, init=None, max_rounds=0):
     st = _lib().orc_classic_coloring(n, _p(rp), _p(cl), _p(wt), _p(lab), cap, _p(out),
                                      ctypes.byref(k), ctypes.byref(rounds), _p(hist))
     return out, int(k.value), int(rounds.value), hist[: rounds.value].copy(), int(st)
+
+
+def splitter_coloring(row_ptr, col, weight_=None, init=None):
+    """Oracle (b'): the coarsest stable colouring refining ``init`` by
+    splitter-based partition refinement (work list of classes, all parts
+    but a largest listed on a split), the partition-refinement method of
+    the baselines Section 2 discusses.  Exact and deterministic; no rounds.
+
+    Returns (colours with first-occurrence ids, k, splitter visits), where
+    the visits count the transpose entries read, O(m log n).
+    Parity: pinned against brute force, automorphism orbits, closed forms
+    and oracle (b) in ``tests/test_oracle_splitter.py``.
+    """
+    rp, cl, wt = _csr(row_ptr, col, weight_)
+    n = rp.size - 1
+    lab = None if init is None else np.ascontiguousarray(init, dtype=np.uint32)
+    out = np.empty(n, dtype=np.uint32)
+    k = ctypes.c_uint32(0)
+    visits = ctypes.c_uint64(0)
+    _lib().orc_splitter_coloring(n, _p(rp), _p(cl), _p(wt), _p(lab), _p(out),
+                                 ctypes.byref(k), ctypes.byref(visits))
+    return out, int(k.value), int(visits.value)
 
 
 def classic_round(row_ptr, col, weight_, colors):

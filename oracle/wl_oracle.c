@@ -802,3 +802,233 @@ int orc_batched_coloring(uint64_t n0, const uint64_t *row_ptr0,
                                   max_batch, max_rounds, c_out, k_out,
                                   rounds_out, outer_out, coarsest_out, ORC_FP);
 }
+
+/* ------------------------------------------------------------------------- */
+/* Oracle (b'): exact colour refinement by splitters.                          */
+/*                                                                            */
+/* The coarsest stable colouring refining the initial one (Definitions        */
+/* "Stable Coloring" and "Coarsest Stable Coloring", Section 3), computed     */
+/* the way the partition-refinement baselines the paper compares against     */
+/* work (Section 2): a partition is stable exactly when, for every class S    */
+/* (a splitter), all members i of a class C have the same weighted count      */
+/* w(i, S) = sum of A[i][l] over l in S.  A work list holds the classes the   */
+/* partition may not yet be stable against.  Taking S off the list, the       */
+/* counts w(i, S) of every node with an entry into S are summed over the     */
+/* transpose, and every class is split by them (members without such an      */
+/* entry count 0).  When C splits into parts:                                 */
+/*   - if C is on the list, every part is (C keeps its id on its first part); */
+/*   - otherwise every part but one largest is listed: the partition was      */
+/*     stable against C, and w(i, largest) = w(i, C) - sum of the others.     */
+/* This is Hopcroft's "process the smaller half" (Hopcroft 1971), extended    */
+/* to k-way splits of weighted counts by Cardon and Crochemore (1982) and     */
+/* analysed for colour refinement by Berkholz, Bonsma and Grohe (2017): a     */
+/* node lies in a processed splitter O(log n) times, so the entries are      */
+/* visited O(m log n) times.  The touched members of a class are ordered by  */
+/* a comparison sort here, which adds a logarithmic factor to that part.      */
+/* Precondition: every weighted row sum fits in 64 bits (always true for     */
+/* rows of fewer than 2^32 entries of 32-bit weights).                        */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+    uint64_t w;
+    uint32_t node;
+} orc_wnode;
+
+static int cmp_wnode(const void *a, const void *b)
+{
+    const orc_wnode *x = (const orc_wnode *)a, *y = (const orc_wnode *)b;
+    if (x->w != y->w)
+        return x->w < y->w ? -1 : 1;
+    return (x->node > y->node) - (x->node < y->node);
+}
+
+/* Returns 0; c_out gets first-occurrence ids (node 0 has colour 0), k_out
+ * the number of classes, visits_out (may be NULL) the number of transpose
+ * entries read over all splitters. */
+int orc_splitter_coloring(uint64_t n, const uint64_t *row_ptr,
+                          const uint32_t *col, const uint32_t *weight,
+                          const uint32_t *init, uint32_t *c_out,
+                          uint32_t *k_out, uint64_t *visits_out)
+{
+    *k_out = 0;
+    if (visits_out)
+        *visits_out = 0;
+    if (n == 0)
+        return 0;
+    const uint64_t m = row_ptr[n];
+    /* transpose: for column l, the rows i with an entry A[i][l] */
+    uint64_t *tptr = (uint64_t *)calloc(n + 1, sizeof(uint64_t));
+    uint32_t *tsrc = (uint32_t *)malloc((m ? m : 1) * sizeof(uint32_t));
+    uint32_t *twt = weight ? (uint32_t *)malloc((m ? m : 1) * sizeof(uint32_t)) : NULL;
+    for (uint64_t e = 0; e < m; ++e)
+        ++tptr[col[e] + 1];
+    for (uint64_t l = 0; l < n; ++l)
+        tptr[l + 1] += tptr[l];
+    uint64_t *tfill = (uint64_t *)malloc(n * sizeof(uint64_t));
+    memcpy(tfill, tptr, n * sizeof(uint64_t));
+    for (uint64_t i = 0; i < n; ++i)
+        for (uint64_t e = row_ptr[i]; e < row_ptr[i + 1]; ++e) {
+            const uint64_t t = tfill[col[e]]++;
+            tsrc[t] = (uint32_t)i;
+            if (twt)
+                twt[t] = weight[e];
+        }
+    free(tfill);
+
+    /* the partition: members of class c are elem[cbeg[c] .. cend[c]) */
+    uint32_t *cls = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *elem = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *loc = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *cbeg = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *cend = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *cmark = (uint32_t *)calloc(n, sizeof(uint32_t)); /* touched members */
+    uint8_t *listed = (uint8_t *)calloc(n, 1);
+    uint32_t *work = (uint32_t *)malloc(n * sizeof(uint32_t)); /* the work list */
+    uint32_t *touched = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *tclass = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint32_t *members = (uint32_t *)malloc(n * sizeof(uint32_t));
+    uint64_t *cnt = (uint64_t *)calloc(n, sizeof(uint64_t));
+    uint8_t *hit = (uint8_t *)calloc(n, 1);
+    orc_wnode *tail = (orc_wnode *)malloc(n * sizeof(orc_wnode));
+
+    uint32_t k = orc_canonicalize(n, init, cls);
+    for (uint32_t c = 0; c < k; ++c)
+        cbeg[c] = 0;
+    {
+        uint32_t *size = (uint32_t *)calloc(k, sizeof(uint32_t));
+        for (uint64_t i = 0; i < n; ++i)
+            ++size[cls[i]];
+        uint32_t s = 0;
+        for (uint32_t c = 0; c < k; ++c) {
+            cbeg[c] = s;
+            cend[c] = s;
+            s += size[c];
+        }
+        free(size);
+        for (uint64_t i = 0; i < n; ++i) {
+            const uint32_t p = cend[cls[i]]++;
+            elem[p] = (uint32_t)i;
+            loc[i] = p;
+        }
+    }
+    uint32_t nwork = 0;
+    for (uint32_t c = 0; c < k; ++c) {
+        work[nwork++] = c;
+        listed[c] = 1;
+    }
+    uint64_t visits = 0;
+    while (nwork) {
+        const uint32_t s = work[--nwork];
+        listed[s] = 0;
+        /* the splitter's members as they are now */
+        const uint32_t ns = cend[s] - cbeg[s];
+        memcpy(members, elem + cbeg[s], ns * sizeof(uint32_t));
+        uint32_t nt = 0, ntc = 0;
+        for (uint32_t x = 0; x < ns; ++x) {
+            const uint32_t l = members[x];
+            for (uint64_t t = tptr[l]; t < tptr[l + 1]; ++t) {
+                const uint32_t i = tsrc[t];
+                ++visits;
+                if (!hit[i]) {
+                    /* move i to the touched tail of its class */
+                    hit[i] = 1;
+                    touched[nt++] = i;
+                    const uint32_t c = cls[i];
+                    if (cmark[c] == 0)
+                        tclass[ntc++] = c;
+                    const uint32_t dst = cend[c] - 1 - cmark[c]++;
+                    const uint32_t other = elem[dst], src = loc[i];
+                    elem[dst] = i;
+                    loc[i] = dst;
+                    elem[src] = other;
+                    loc[other] = src;
+                }
+                cnt[i] += twt ? twt[t] : 1u;
+            }
+        }
+        for (uint32_t y = 0; y < ntc; ++y) {
+            const uint32_t c = tclass[y];
+            const uint32_t b = cbeg[c], e = cend[c], nm = cmark[c];
+            const uint32_t t0 = e - nm;
+            cmark[c] = 0;
+            for (uint32_t p = t0; p < e; ++p) {
+                tail[p - t0].w = cnt[elem[p]];
+                tail[p - t0].node = elem[p];
+            }
+            qsort(tail, nm, sizeof(orc_wnode), cmp_wnode);
+            for (uint32_t p = t0; p < e; ++p) {
+                elem[p] = tail[p - t0].node;
+                loc[elem[p]] = p;
+            }
+            /* runs of equal counts in position order; the untouched
+             * prefix [b, t0) counts 0, sorts first and is taken as one
+             * run, so the walk costs only the touched members */
+            uint32_t nruns = 0, big = 0, bigsize = 0;
+            uint32_t p = b;
+            while (p < e) {
+                const uint64_t v = p < t0 ? 0 : tail[p - t0].w;
+                uint32_t q = p < t0 ? t0 : p + 1;
+                while (q < e && tail[q - t0].w == v)
+                    ++q;
+                if (q - p > bigsize) {
+                    bigsize = q - p;
+                    big = nruns;
+                }
+                ++nruns;
+                p = q;
+            }
+            if (nruns == 1)
+                continue;
+            const int was_listed = listed[c];
+            uint32_t r = 0;
+            p = b;
+            while (p < e) {
+                const uint64_t v = p < t0 ? 0 : tail[p - t0].w;
+                uint32_t q = p < t0 ? t0 : p + 1;
+                while (q < e && tail[q - t0].w == v)
+                    ++q;
+                uint32_t id = c;
+                if (r == 0) {
+                    cend[c] = q;
+                } else {
+                    id = k++;
+                    cbeg[id] = p;
+                    cend[id] = q;
+                    for (uint32_t z = p; z < q; ++z)
+                        cls[elem[z]] = id;
+                }
+                if ((was_listed || r != big) && !listed[id]) {
+                    work[nwork++] = id;
+                    listed[id] = 1;
+                }
+                ++r;
+                p = q;
+            }
+        }
+        for (uint32_t x = 0; x < nt; ++x) {
+            cnt[touched[x]] = 0;
+            hit[touched[x]] = 0;
+        }
+    }
+    *k_out = orc_first_occurrence(n, cls, c_out);
+    if (visits_out)
+        *visits_out = visits;
+    free(tptr);
+    free(tsrc);
+    free(twt);
+    free(cls);
+    free(elem);
+    free(loc);
+    free(cbeg);
+    free(cend);
+    free(cmark);
+    free(listed);
+    free(work);
+    free(touched);
+    free(tclass);
+    free(members);
+    free(cnt);
+    free(hit);
+    free(tail);
+    return 0;
+}
