@@ -47,6 +47,7 @@
  *   - an empty row gives z_i = 0 (no A + I in the unbatched algorithm).
  */
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -834,6 +835,13 @@ typedef struct {
     uint32_t node;
 } orc_wnode;
 
+/* ORC_PROGRESS=1 in the environment: progress lines on stderr (long runs). */
+static int orc_progress_on(void)
+{
+    const char *s = getenv("ORC_PROGRESS");
+    return s && s[0] == '1';
+}
+
 static int cmp_wnode(const void *a, const void *b)
 {
     const orc_wnode *x = (const orc_wnode *)a, *y = (const orc_wnode *)b;
@@ -874,6 +882,10 @@ int orc_splitter_coloring(uint64_t n, const uint64_t *row_ptr,
                 twt[t] = weight[e];
         }
     free(tfill);
+    const int prog = orc_progress_on();
+    if (prog)
+        fprintf(stderr, "[splitters] transpose built: n=%llu m=%llu\n",
+                (unsigned long long)n, (unsigned long long)m);
 
     /* the partition: members of class c are elem[cbeg[c] .. cend[c]) */
     uint32_t *cls = (uint32_t *)malloc(n * sizeof(uint32_t));
@@ -916,8 +928,9 @@ int orc_splitter_coloring(uint64_t n, const uint64_t *row_ptr,
         work[nwork++] = c;
         listed[c] = 1;
     }
-    uint64_t visits = 0;
+    uint64_t visits = 0, pmark = 0, npop = 0;
     while (nwork) {
+        ++npop;
         const uint32_t s = work[--nwork];
         listed[s] = 0;
         /* the splitter's members as they are now */
@@ -944,6 +957,11 @@ int orc_splitter_coloring(uint64_t n, const uint64_t *row_ptr,
                     loc[other] = src;
                 }
                 cnt[i] += twt ? twt[t] : 1u;
+            }
+            if (prog && (visits >> 30) != pmark) {
+                pmark = visits >> 30;
+                fprintf(stderr, "[splitters] visits %llu, splitters %llu, classes %u, listed %u\n",
+                        (unsigned long long)visits, (unsigned long long)npop, k, nwork);
             }
         }
         for (uint32_t y = 0; y < ntc; ++y) {

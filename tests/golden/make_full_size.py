@@ -2,6 +2,7 @@
 
     python tests/golden/make_full_size.py chunglu rmat27
     python tests/golden/make_full_size.py --ring64 rmat27
+    python tests/golden/make_full_size.py --exact chunglu rmat27
 
 For each workload: the seeded graph from the shared input generators (built on
 the GPU, which produces byte-identical CSRs to the CPU build of the same
@@ -12,6 +13,10 @@ count after every round, the round count, the final colour count, the SHA-256
 of the final colour array (uint32 little-endian) and the colours of 4096
 seeded sample nodes.  With --ring64 the oracle computes in the ring Z/2^64
 (Algorithm 1 with precision q = 64) and the file is full_<name>_ring64.json.
+With --exact the coarsest stable colouring is computed instead by oracle (b'),
+the splitter-based refinement (no rounds, no random weights), and
+full_<name>_exact.json stores its colour count and the SHA-256 of its
+first-occurrence ids (node 0 has colour 0, each new colour the next id).
 Nothing here calls the HIP library.
 """
 import hashlib
@@ -99,9 +104,35 @@ def run(name, q=0):
     say(f"{name}: wrote {path}: colours={k} rounds={r}")
 
 
+def run_exact(name):
+    say(f"{name}: generating")
+    rp, col = build(name)
+    n = rp.size - 1
+    say(f"{name}: n={n} nnz={col.size}; oracle (b') running")
+    os.environ["ORC_PROGRESS"] = "1"
+    t0 = time.time()
+    c, k, visits = oracle.splitter_coloring(rp, col)
+    dt = time.time() - t0
+    say(f"{name}: colours={k} visits={visits} ({dt:.1f} s)")
+    out = {
+        "workload": WORKLOADS[name], "n": int(n), "nnz": int(col.size),
+        "csr_checksum": csr_checksum(rp, col), "colours": int(k),
+        "sha256_first_occurrence": hashlib.sha256(c.astype("<u4").tobytes()).hexdigest(),
+        "splitter_visits": int(visits), "seconds": round(dt, 1),
+        "written_by": "tests/golden/make_full_size.py --exact (oracle/ only: splitter_coloring)",
+    }
+    path = os.path.join(HERE, f"full_{name}_exact.json")
+    with open(path, "w") as f:
+        json.dump(out, f)
+    say(f"{name}: wrote {path}")
+
+
 if __name__ == "__main__":
     args = sys.argv[1:]
     q = oracle.RING64 if "--ring64" in args else oracle.FP
     names = [a for a in args if not a.startswith("--")]
     for nm in names or list(WORKLOADS):
-        run(nm, q)
+        if "--exact" in args:
+            run_exact(nm)
+        else:
+            run(nm, q)

@@ -3,7 +3,8 @@ the configuration the benchmark times (graph generated on the device, one
 wl_stable_coloring call from the trivial partition, seed 0), against the
 oracle's results stored by tests/golden/make_full_size.py: colour count,
 round count, SHA-256 of the whole colour array and sampled colours.  The
-result must also pass the exact stability certificate on the device."""
+result must also pass the exact stability certificate on the device, and
+where oracle (b')'s coarsest colouring is stored, equal it as a partition."""
 import hashlib
 import json
 import os
@@ -12,6 +13,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 import paper_2607_02603_amd as wl
 from paper_2607_02603_amd import inputs
 
@@ -55,6 +57,15 @@ def test_full_size_bit_exact(name):
     assert np.array_equal(host[idx], np.asarray(gold["sample_colours"], np.uint32))
     assert hashlib.sha256(host.astype("<u4").tobytes()).hexdigest() == gold["sha256"]
     assert wl.wl_verify_stable(g, colors, k, ws=ws)
+    # the coarsest stable colouring, from oracle (b') (splitter refinement)
+    path = os.path.join(GOLDEN, f"full_{name}_exact.json")
+    if os.path.exists(path):
+        with open(path) as f:
+            exact = json.load(f)
+        fo = oracle.first_occurrence(host)[0]
+        assert k == exact["colours"]
+        assert hashlib.sha256(fo.astype("<u4").tobytes()).hexdigest() == \
+            exact["sha256_first_occurrence"]
 
 
 def test_full_size_ring64_bit_exact():
