@@ -69,6 +69,12 @@ def bench_batched(args):
     big = args.workload == "rmat29s"
     if big and args.batched_mode != "streamed":
         raise SystemExit("rmat29s runs the streamed mode only")
+    if args.batched_mode in ("exact", "exact-early"):
+        # one exact-early run at this size ended in a host segmentation
+        # fault whose cause is not found; the exact finishes are exercised
+        # at R-MAT scale 26 and below until it is
+        raise SystemExit(f"--batched-mode {args.batched_mode} is switched off for "
+                         f"{args.workload}: an unexplained host fault at this size")
     t0 = time.perf_counter()
     if big:
         g = inputs.rmat(29, 32, device=dev, host_out=True, pinned=False)
