@@ -10,7 +10,10 @@
  *     with the C '%' operator at the end;
  *   - the relabel is a plain qsort of (old color, image) pairs followed by a
  *     walk that hands out ranks;
- *   - classic refinement builds every node's full neighbour-colour multiset.
+ *   - classic refinement builds every node's full neighbour-colour multiset;
+ *   - splitter refinement (oracle (b'), at the end of this file) reaches the
+ *     coarsest stable colouring without rounds or random values, by a work
+ *     list of splitter classes over the transpose.
  *
  * Paper: "Scaling Weisfeiler-Leman Expressiveness Analysis to Massive Graphs
  * with GPUs" (Biondi, Tribastone, Tschaikowski).  Section and equation names
