@@ -56,7 +56,7 @@ def trace_table(db, calls):
 
 def trace_markdown(db, calls, title, command):
     rows, per_call = trace_table(db, calls)
-    out = [f"# {title}", "", "Command (repository root, on the GPU box):", "",
+    out = [f"# {title}", "", "Command (repository root, on the MI355X machine):", "",
            f"    {command}", "",
            f"Library kernels only; the traced program makes {calls} library call(s): "
            f"per-call figures are totals / {calls}.", "",
