@@ -170,3 +170,36 @@ def test_empty_and_single():
     assert c.size == 0 and k == 0 and v == 0
     c, k, v = oracle.splitter_coloring(np.zeros(2, np.uint64), np.zeros(0, np.uint32))
     assert list(c) == [0] and k == 1
+
+
+def test_planted_list_every_part_breaks_the_bound(tmp_path):
+    # the visit bound is what tells "all parts but a largest" from "every
+    # part": a CPU copy of the oracle with the rule changed must exceed it
+    import ctypes
+    import os
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "wl_oracle.c")).read()
+    rule = "if ((was_listed || r != big) && !listed[id])"
+    assert src.count(rule) == 1
+    planted = tmp_path / "planted.c"
+    planted.write_text(src.replace(rule, "if (!listed[id])"))
+    so = tmp_path / "planted.so"
+    subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", str(so), str(planted)],
+                   check=True, capture_output=True)
+    lib = ctypes.CDLL(str(so))
+    n = 1024
+    rp, col = _path(n)
+    rp = np.ascontiguousarray(rp, np.uint64)
+    col = np.ascontiguousarray(col, np.uint32)
+    out = np.empty(n, np.uint32)
+    k, visits = ctypes.c_uint32(0), ctypes.c_uint64(0)
+    vp = ctypes.c_void_p
+    lib.orc_splitter_coloring(ctypes.c_uint64(n), vp(rp.ctypes.data), vp(col.ctypes.data), None,
+                              None, vp(out.ctypes.data), ctypes.byref(k), ctypes.byref(visits))
+    bound = int(rp[-1]) * (math.floor(math.log2(n)) + 2)
+    assert k.value == n // 2  # still the right partition ...
+    assert visits.value > bound  # ... at the cost the bound rules out
+    assert oracle.splitter_coloring(rp, col)[2] <= bound
