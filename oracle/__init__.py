@@ -5,7 +5,8 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 its binding) never imports it, and the two share no code.
 
 Thin ctypes wrapper over ``oracle/wl_oracle.c`` (plain C, 128-bit exact sums,
-qsort-based relabel) plus pure-Python pieces for tiny inputs
+qsort-based relabel; Algorithm 1, classic refinement, splitter-based exact
+refinement and Algorithm 2) plus pure-Python pieces for tiny inputs
 (``oracle.bruteforce``).  Section, equation and algorithm names refer to
 "Scaling Weisfeiler-Leman Expressiveness Analysis to Massive Graphs with
 GPUs".
