@@ -70,11 +70,11 @@ def bench_batched(args):
     if big and args.batched_mode != "streamed":
         raise SystemExit("rmat29s runs the streamed mode only")
     if args.batched_mode in ("exact", "exact-early"):
-        # one exact-early run at this size ended in a host segmentation
-        # fault whose cause is not found; the exact finishes are exercised
-        # at R-MAT scale 26 and below until it is
+        # the library accepts WL_BATCHED_EXACT only up to 2^31 entries, far
+        # below these graphs: say so before building them
         raise SystemExit(f"--batched-mode {args.batched_mode} is switched off for "
-                         f"{args.workload}: an unexplained host fault at this size")
+                         f"{args.workload}: the library's exact finish is limited to "
+                         f"2^31 entries (use --batched-mode streamed)")
     t0 = time.perf_counter()
     if big:
         g = inputs.rmat(29, 32, device=dev, host_out=True, pinned=False)

@@ -27,9 +27,19 @@
  *     stability condition of the paper is on out-weights).  Column order
  *     inside a row does not matter; repeated columns count with
  *     multiplicity.  Self-loops are allowed.
- *   - The caller owns every buffer.  The library allocates no device or host
- *     memory of its own: all scratch space is the caller's 'workspace'
- *     (device memory, 256-byte aligned), sized by wl_workspace_size().
+ *   - The caller owns every buffer it passes.  Device memory: no entry point
+ *     allocates any; all device scratch space is the caller's 'workspace'
+ *     (256-byte aligned), sized by the *_workspace_size() call of each entry
+ *     point.  Host memory: the in-core entry points (wl_refine_round,
+ *     wl_stable_coloring, wl_verify_stable) allocate none beyond a few
+ *     bytes of bookkeeping; the out-of-core ones (wl_stable_coloring_streamed,
+ *     wl_stable_coloring_batched) allocate page-locked staging buffers and
+ *     pageable arrays, stated at each, and free them before returning.
+ *     Streams and events: the in-core entry points create none, except with
+ *     WL_GRAPH=1 in the environment, where a call creates a capture stream
+ *     and HIP graph objects and destroys them before it returns; the
+ *     out-of-core ones create copy streams and events for the call's
+ *     duration.
  *   - All device work is enqueued on 'stream' (a hipStream_t; NULL = the
  *     null stream).  Entry points that return host scalars synchronise that
  *     stream before returning.
@@ -236,6 +246,11 @@ int wl_get_precision(uint32_t *q);
  *   with several batches).
  * The exact finish needs the workspace of wl_stable_coloring_streamed for
  * the graph it runs on, at least with chunks of 4096 entries.
+ * WL_BATCHED_EXACT is accepted only for graphs of at most 2^31 entries, the
+ * largest on which the exact finish has been verified (WL_EINVAL above;
+ * one run on a 1.7e10-entry graph ended in a host fault whose cause has not
+ * been found).  wl_stable_coloring_streamed computes the same colouring
+ * (the coarsest stable one) for larger graphs.
  * Errors: WL_EINVAL (also unknown option bits), WL_EBUDGET, WL_EOVERFLOW,
  * WL_EMAXROUNDS, WL_ENOMEM, WL_EHIP. */
 int wl_stable_coloring_batched(const wl_csr *g_host, const uint32_t *init_host,

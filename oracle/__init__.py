@@ -88,7 +88,7 @@ def _lib():
                                              vp, vp, vp, vp, vp]
         lib.orc_batched_coloring_q.restype = ctypes.c_int
         lib.orc_batched_coloring_q.argtypes = [u64, vp, vp, vp, vp, u64, u64, u32,
-                                               vp, vp, vp, vp, vp, u32]
+                                               vp, vp, vp, vp, vp, u32, ctypes.c_int]
         _LIB = lib
     return _LIB
 
@@ -287,9 +287,11 @@ def batch_cut(row_ptr, max_batch):
 
 
 def batched_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_batch=1,
-                     max_rounds=0, q=FP):
+                     max_rounds=0, q=FP, early_stop=False):
     """Algorithm 2 with the readings of the oracle source, in F_p (q = FP)
-    or Z/2^64 (q = RING64).
+    or Z/2^64 (q = RING64).  early_stop adds Section 5.4's termination: the
+    outer loop ends once the quotient just built would not be cut into fewer
+    batches than the iteration that built it.
 
     Returns (first-occurrence colours, k, rounds, outer iterations,
     coarsest flag, status).
@@ -306,6 +308,6 @@ def batched_coloring(row_ptr, col, weight_=None, init=None, seed=0, max_batch=1,
     st = _lib().orc_batched_coloring_q(n, _p(rp), _p(cl), _p(wt), _p(lab), seed,
                                        max_batch, cap, _p(out), ctypes.byref(k),
                                        ctypes.byref(rounds), ctypes.byref(outer),
-                                       ctypes.byref(coarsest), q)
+                                       ctypes.byref(coarsest), q, int(bool(early_stop)))
     return (out, int(k.value), int(rounds.value), int(outer.value),
             bool(coarsest.value), int(st))

@@ -579,14 +579,21 @@ uint64_t orc_batch_cut(uint64_t n, const uint64_t *row_ptr, uint64_t max_batch,
 /* Returns 0, 1 (a batch hit max_rounds), 2 (a quotient weight overflowed),
  * 3 (q = 64 and Theorem 1's preconditions fail; a quotient row sums the
  * same entries as its representative's row, so checking the input covers
- * every quotient) or 4 (an image step failed). */
+ * every quotient) or 4 (an image step failed).
+ *
+ * early_stop != 0 adds the termination of Section 5.4 ("Feasibility"): once
+ * the quotient of an outer iteration is built, the outer loop ends when that
+ * quotient, cut with the same cap, would not give fewer batches than the
+ * iteration just done (N_b counted as the ranges orc_batch_cut produces).
+ * The colouring returned is then the merged partition of that iteration,
+ * and the coarsest flag is 0 (several batches were used). */
 int orc_batched_coloring_q(uint64_t n0, const uint64_t *row_ptr0,
                            const uint32_t *col0, const uint32_t *weight0,
                            const uint32_t *init, uint64_t seed,
                            uint64_t max_batch, uint32_t max_rounds,
                            uint32_t *c_out, uint32_t *k_out,
                            uint32_t *rounds_out, uint32_t *outer_out,
-                           int *coarsest_out, uint32_t q)
+                           int *coarsest_out, uint32_t q, int early_stop)
 {
     *k_out = 0;
     *rounds_out = 0;
@@ -780,6 +787,12 @@ int orc_batched_coloring_q(uint64_t n0, const uint64_t *row_ptr0,
         free(hout);
         free(brp);
         free(hc);
+        /* Section 5.4: stop when the next iteration would not have fewer
+         * batches (nb > 1 here, else the loop ended above) */
+        if (early_stop && orc_batch_cut(n, rp, max_batch, NULL, 0) >= nb) {
+            *coarsest_out = 0;
+            break;
+        }
     }
     /* final colours: first occurrence over the original nodes */
     uint32_t k = orc_first_occurrence(n0, map, c_out);
@@ -804,7 +817,7 @@ int orc_batched_coloring(uint64_t n0, const uint64_t *row_ptr0,
 {
     return orc_batched_coloring_q(n0, row_ptr0, col0, weight0, init, seed,
                                   max_batch, max_rounds, c_out, k_out,
-                                  rounds_out, outer_out, coarsest_out, ORC_FP);
+                                  rounds_out, outer_out, coarsest_out, ORC_FP, 0);
 }
 
 /* ------------------------------------------------------------------------- */

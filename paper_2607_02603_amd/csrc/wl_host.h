@@ -226,6 +226,161 @@ inline uint64_t merge_blocks(HostPool& pool, const uint32_t* key, uint64_t n, ui
   return cnt[T];
 }
 
+// Largest value v in [0, cap] with total_of(v) <= budget (total_of is
+// non-decreasing), or 0.
+template <typename F>
+inline uint64_t largest_fitting(F total_of, uint64_t budget, uint64_t cap) {
+  uint64_t lo = 0, hi = cap;
+  while (lo < hi) {
+    uint64_t mid = lo + (hi - lo + 1) / 2;
+    if (total_of(mid) <= budget) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// ---------------------------------------------------------------------------
+// Algorithm 2 (Section 4.2), host side: the batch cut, the inner rows of a
+// batch, the chunk plan of the quotient and the final colours.
+// ---------------------------------------------------------------------------
+
+// Greedy batch cut of the entry array: ranges of at most mb >= 1 entries
+// ending at a row boundary, a row longer than mb cut inside (reading of
+// Algorithm 2's "partition E into E_1 .. E_Nb with |E_k| <= M_b").  Returns
+// the starts of the ranges followed by m (at least {0, m}).
+inline std::vector<uint64_t> cut_batches(const HostGraph& G, uint64_t mb) {
+  std::vector<uint64_t> starts;
+  uint64_t s = 0;
+  const uint64_t m = G.m;
+  do {
+    starts.push_back(s);
+    if (m - s <= mb) { s = m; break; }
+    const uint64_t lim = s + mb;
+    // last row boundary <= lim
+    uint64_t lo = 0, hi = G.n;
+    while (lo < hi) {
+      uint64_t mid = lo + (hi - lo + 1) / 2;
+      if (G.rp(mid) <= lim) lo = mid; else hi = mid - 1;
+    }
+    uint64_t e = G.rp(lo);
+    if (e <= s) e = lim;
+    s = e;
+  } while (s < m);
+  starts.push_back(m);
+  return starts;
+}
+
+// Inner rows of batch b (Definition "Inner and boundary nodes"): the rows
+// that start inside it and end inside it; empty rows belong to the batch
+// whose range contains their offset.
+inline void inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts, uint64_t b,
+                       uint64_t* r_lo, uint64_t* r_hi) {
+  const uint64_t nb = starts.size() - 1, eb = starts[b + 1];
+  *r_lo = G.lower_row(starts[b]);
+  *r_hi = (b + 1 == nb) ? G.n : G.lower_row(eb);
+  if (*r_hi > *r_lo && G.rp(*r_hi) > eb) --*r_hi;  // the last row continues
+}
+
+inline uint64_t max_inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts) {
+  uint64_t mx = 0;
+  for (uint64_t b = 0; b + 1 < starts.size(); ++b) {
+    uint64_t lo, hi;
+    inner_rows(G, starts, b, &lo, &hi);
+    if (hi > lo) mx = std::max(mx, hi - lo);
+  }
+  return mx;
+}
+
+// Largest batch cap whose batches fit a device budget: bytes_of(rows, cap)
+// is the workspace a batch of 'rows' inner rows and 'cap' entries needs.
+// Returns 0 when not even a cap of one entry fits.
+template <typename F>
+inline uint64_t fit_batch_cap(const HostGraph& G, uint64_t budget, F bytes_of) {
+  const uint64_t mall = std::max<uint64_t>(G.m, 1);  // a cap >= m is one batch
+  auto fits = [&](uint64_t cap) {
+    const std::vector<uint64_t> st = cut_batches(G, cap);
+    return bytes_of(max_inner_rows(G, st), cap) <= budget;
+  };
+  uint64_t lo = 0, hi = std::min(mall, budget / 8);
+  while (lo < hi) {
+    const uint64_t mid = lo + (hi - lo + 1) / 2;
+    if (fits(mid)) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// A chunk of the quotient phase: rows [a, bnd) holding entries
+// [ea, ea + ent).  ent <= mq, or the chunk is one row longer than mq
+// (processed in pieces).
+struct QChunk {
+  uint64_t a, bnd, ea, ent;
+};
+
+// Row ranges of at most mq >= 1 entries (at least one row each) covering
+// all n rows.
+inline std::vector<QChunk> quotient_chunks(const HostGraph& G, uint64_t mq) {
+  std::vector<QChunk> qch;
+  const uint64_t n = G.n;
+  for (uint64_t a = 0; a < n;) {
+    const uint64_t ea = G.rp(a);
+    uint64_t lo = a + 1, hi = n;  // last row end <= ea + mq (at least one row)
+    while (lo < hi) {
+      const uint64_t mid = lo + (hi - lo + 1) / 2;
+      if (G.rp(mid) - ea <= mq) lo = mid; else hi = mid - 1;
+    }
+    qch.push_back({a, lo, ea, G.rp(lo) - ea});
+    a = lo;
+  }
+  return qch;
+}
+
+// The key plan of one quotient chunk (ent <= mq < 2^32): for each row, the
+// offset of its keys among the chunk's keys (only representatives' rows
+// have keys, Definition "Quotient Graph"); the key offsets where the
+// non-empty representative rows start, followed by the key count; the
+// number of representatives and the block of the first one.
+struct QChunkPrep {
+  std::vector<uint64_t> qoff;
+  std::vector<uint32_t> qseg;
+  uint64_t run = 0, nreps = 0;
+  uint32_t bfirst = 0xFFFFFFFFu;
+};
+
+inline void prep_quotient_chunk(const HostGraph& G, const QChunk& c, const uint8_t* isrep,
+                                const uint32_t* blk, QChunkPrep& q) {
+  const uint64_t nrows = c.bnd - c.a;
+  q.qoff.resize(nrows);
+  q.qseg.clear();
+  q.run = q.nreps = 0;
+  q.bfirst = 0xFFFFFFFFu;
+  for (uint64_t r = 0; r < nrows; ++r) {
+    q.qoff[r] = q.run;
+    if (isrep[c.a + r]) {
+      if (q.bfirst == 0xFFFFFFFFu) q.bfirst = blk[c.a + r];
+      const uint64_t d = G.rp(c.a + r + 1) - G.rp(c.a + r);
+      if (d) q.qseg.push_back((uint32_t)q.run);
+      q.run += d;
+      ++q.nreps;
+    }
+  }
+  q.qseg.push_back((uint32_t)q.run);
+}
+
+// Final colours of the original nodes: the colour of the node of the last
+// graph each maps to (col_f, or the node itself when col_f is NULL),
+// numbered by first occurrence.  Every map0[v] < nf, every col_f[.] < nf.
+inline void canonical_colours(const std::vector<uint32_t>& map0, const uint32_t* col_f,
+                              uint64_t nf, uint32_t* color_out, uint32_t* k_out) {
+  std::vector<uint32_t> slot(nf, 0xFFFFFFFFu);
+  uint32_t k = 0;
+  for (uint64_t v = 0; v < map0.size(); ++v) {
+    const uint32_t c = col_f ? col_f[map0[v]] : map0[v];
+    uint32_t& sl = slot[c];
+    if (sl == 0xFFFFFFFFu) sl = k++;
+    color_out[v] = sl;
+  }
+  *k_out = k;
+}
+
 // A cut row's share of one chunk: its segments [first, first + count) of the
 // chunk, the node, and whether z already holds the sum of earlier chunks.
 struct StreamFold {

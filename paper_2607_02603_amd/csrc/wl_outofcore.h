@@ -53,61 +53,6 @@ QuotLayout quot_layout(uint64_t n0, uint64_t mq) {
   return L;
 }
 
-template <typename F>
-uint64_t largest_fitting(F total_of, uint64_t budget, uint64_t cap) {
-  uint64_t lo = 0, hi = cap;
-  while (lo < hi) {
-    uint64_t mid = lo + (hi - lo + 1) / 2;
-    if (total_of(mid) <= budget) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
-// Greedy batch cut of the entry array: ranges of at most mb entries ending
-// at a row boundary, a row longer than mb cut inside (reading of Algorithm 2).
-std::vector<uint64_t> cut_batches(const HostGraph& G, uint64_t mb) {
-  std::vector<uint64_t> starts;
-  uint64_t s = 0;
-  const uint64_t m = G.m;
-  do {
-    starts.push_back(s);
-    if (m - s <= mb) { s = m; break; }
-    const uint64_t lim = s + mb;
-    // last row boundary <= lim
-    uint64_t lo = 0, hi = G.n;
-    while (lo < hi) {
-      uint64_t mid = lo + (hi - lo + 1) / 2;
-      if (G.rp(mid) <= lim) lo = mid; else hi = mid - 1;
-    }
-    uint64_t e = G.rp(lo);
-    if (e <= s) e = lim;
-    s = e;
-  } while (s < m);
-  starts.push_back(m);
-  return starts;
-}
-
-// Inner rows of batch b (Definition "Inner and boundary nodes"): the rows
-// that start inside it and end inside it; empty rows belong to the batch
-// whose range contains their offset.
-void inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts, uint64_t b,
-                uint64_t* r_lo, uint64_t* r_hi) {
-  const uint64_t nb = starts.size() - 1, eb = starts[b + 1];
-  *r_lo = G.lower_row(starts[b]);
-  *r_hi = (b + 1 == nb) ? G.n : G.lower_row(eb);
-  if (*r_hi > *r_lo && G.rp(*r_hi) > eb) --*r_hi;  // the last row continues
-}
-
-uint64_t max_inner_rows(const HostGraph& G, const std::vector<uint64_t>& starts) {
-  uint64_t mx = 0;
-  for (uint64_t b = 0; b + 1 < starts.size(); ++b) {
-    uint64_t lo, hi;
-    inner_rows(G, starts, b, &lo, &hi);
-    if (hi > lo) mx = std::max(mx, hi - lo);
-  }
-  return mx;
-}
-
 // Host array owned by the library (pageable: the quotient graphs of the outer
 // iterations can be far larger than the page-locked memory a process may hold).
 struct HostBuf {
@@ -743,21 +688,6 @@ int streamed_run(const HostGraph& G, const uint32_t* labels, uint64_t seed,
   return WL_OK;
 }
 
-// Final colours of the original nodes: the colour of the node of Gf each
-// maps to, numbered by first occurrence.
-void canonical_colours(const std::vector<uint32_t>& map0, const uint32_t* col_f, uint64_t nf,
-                       uint32_t* color_out, uint32_t* k_out) {
-  std::vector<uint32_t> slot(nf, 0xFFFFFFFFu);
-  uint32_t k = 0;
-  for (uint64_t v = 0; v < map0.size(); ++v) {
-    const uint32_t c = col_f ? col_f[map0[v]] : map0[v];
-    uint32_t& sl = slot[c];
-    if (sl == 0xFFFFFFFFu) sl = k++;
-    color_out[v] = sl;
-  }
-  *k_out = k;
-}
-
 int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
                 uint64_t max_batch, uint32_t options, uint32_t* color_out, uint32_t* k_out,
                 uint32_t* rounds_out, uint32_t* outer_out, int* coarsest_out,
@@ -820,19 +750,13 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     if (max_batch) {
       *mb_out = std::min(max_batch, mall);
     } else {
-      auto fits = [&](uint64_t cap) {
-        const std::vector<uint64_t> st = cut_batches(Gp, cap);
-        return refine_layout(max_inner_rows(Gp, st), cap).total <= ws_bytes;
-      };
-      uint64_t lo = 0, hi = std::min(mall, ws_bytes / 8);
-      while (lo < hi) {
-        const uint64_t mid = lo + (hi - lo + 1) / 2;
-        if (fits(mid)) lo = mid; else hi = mid - 1;
-      }
-      if (lo == 0)
+      const uint64_t cap = fit_batch_cap(Gp, ws_bytes, [](uint64_t rows, uint64_t c) {
+        return refine_layout(rows, c).total;
+      });
+      if (cap == 0)
         return fail(WL_EBUDGET, "workspace of %llu bytes holds no batch",
                     (unsigned long long)ws_bytes);
-      *mb_out = lo;
+      *mb_out = cap;
     }
     *starts_out = cut_batches(Gp, *mb_out);
     return WL_OK;
@@ -1003,31 +927,13 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
     if (int r = hc.h2d(isrep_dev, isrep.data(), n)) return r;
     // chunks: row ranges [a, bnd) of at most mq entries, or one row longer
     // than that (processed in pieces)
-    struct QChunk {
-      uint64_t a, bnd, ea, ent;
-    };
-    std::vector<QChunk> qch;
-    for (uint64_t a = 0; a < n;) {
-      const uint64_t ea = G.rp(a);
-      uint64_t lo = a + 1, hi = n;  // last row end <= ea + mq (at least one row)
-      while (lo < hi) {
-        const uint64_t mid = lo + (hi - lo + 1) / 2;
-        if (G.rp(mid) - ea <= mq) lo = mid; else hi = mid - 1;
-      }
-      qch.push_back({a, lo, ea, G.rp(lo) - ea});
-      a = lo;
-    }
+    const std::vector<QChunk> qch = quotient_chunks(G, mq);
     // Pipeline: a host thread prepares chunk j+1 (its key offsets, and the
     // copies of its rows into input set (j+1) & 1 on a copy stream of its
     // own) while this thread reduces chunk j from set j & 1.  A set is
     // refilled only after the chunk that used it two steps before has been
     // reduced and copied out.
-    struct QSet {
-      std::vector<uint64_t> qoff;
-      std::vector<uint32_t> qseg;
-      uint64_t run = 0, nreps = 0;
-      uint32_t bfirst = 0;
-    } qs[2];
+    QChunkPrep qs[2];
     struct QPipe {
       std::mutex m;
       std::condition_variable cv;
@@ -1062,25 +968,11 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
         }
         const QChunk& c = qch[j];
         const int st = (int)(j & 1);
-        QSet& q = qs[st];
+        QChunkPrep& q = qs[st];
         int rc = WL_OK;
         if (c.ent <= mq) {
           const uint64_t nrows = c.bnd - c.a;
-          q.qoff.resize(nrows);
-          q.qseg.clear();
-          q.run = q.nreps = 0;
-          q.bfirst = 0xFFFFFFFFu;
-          for (uint64_t r = 0; r < nrows; ++r) {
-            q.qoff[r] = q.run;
-            if (isrep[c.a + r]) {
-              if (q.bfirst == 0xFFFFFFFFu) q.bfirst = blk[c.a + r];
-              const uint64_t d = G.rp(c.a + r + 1) - G.rp(c.a + r);
-              if (d) q.qseg.push_back((uint32_t)q.run);
-              q.run += d;
-              ++q.nreps;
-            }
-          }
-          q.qseg.push_back((uint32_t)q.run);
+          prep_quotient_chunk(G, c, isrep.data(), blk.data(), q);
           if (q.run > 0) {
             const QuotDev& D = Ds[st];
             rc = copy_rows_h2d(hc2, G, c.a, nrows, W + QL.stage[st], D.rp, qp.cs);
@@ -1285,7 +1177,7 @@ int batched_run(const wl_csr* g, const uint32_t* init_host, uint64_t seed,
         }
         push_job({j, 0, 0, 0, 0, false});
       } else if (qs[st].run > 0) {
-        const QSet& q = qs[st];
+        const QChunkPrep& q = qs[st];
         const uint64_t nrows = c.bnd - a;
         clk::time_point tq = clk::now();
         ++q_chunks;

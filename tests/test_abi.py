@@ -153,3 +153,30 @@ def test_precision_setter_is_per_thread_and_checked():
             wl.wl_set_precision(bad)
         assert e.value.code == wl.WL_EINVAL
     assert wl.wl_get_precision() == wl.WL_PRECISION_FP
+
+
+def test_exact_finish_limited_to_verified_size():
+    # WL_BATCHED_EXACT is refused above 2^31 entries before any device work
+    # (a host-side row pointer array is all the check reads)
+    _ensure_built()
+    import numpy as np
+    L = wl.lib()
+    nnz = (1 << 31) + 1
+    rp = np.array([0, nnz, nnz], dtype=np.uint64)
+    s = wl.WlCsr()
+    s.n = 2
+    s.nnz = nnz
+    s.row_ptr32 = None
+    s.row_ptr64 = rp.ctypes.data
+    s.col_idx = 16  # never read before the refusal
+    s.weight = None
+    k, r, o = ctypes.c_uint32(0), ctypes.c_uint32(0), ctypes.c_uint32(0)
+    co = ctypes.c_int(0)
+    out = np.zeros(2, dtype=np.uint32)
+    for opts in (wl.WL_BATCHED_EXACT, wl.WL_BATCHED_EXACT | wl.WL_BATCHED_EARLY_STOP):
+        code = L.wl_stable_coloring_batched(ctypes.byref(s), None, 0, 0, opts,
+                                            ctypes.c_void_p(out.ctypes.data), ctypes.byref(k),
+                                            ctypes.byref(r), ctypes.byref(o), ctypes.byref(co),
+                                            ctypes.c_void_p(256), 1 << 30, None)
+        assert code == wl.WL_EINVAL
+        assert b"2^31" in L.wl_last_error()

@@ -24,12 +24,14 @@ def _host_graph(rp, col, wt=None, pinned=True):
                     None if g.weight is None else g.weight.pin_memory())
 
 
-def _check(rp, col, wt=None, init=None, mb=8, seed=0, pinned=True):
+def _check(rp, col, wt=None, init=None, mb=8, seed=0, pinned=True, early=False):
     g = _host_graph(rp, col, wt, pinned)
     init_t = None if init is None else torch.from_numpy(np.asarray(init, np.uint32).view(np.int32))
-    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, init_t, seed, mb)
+    opts = wl.WL_BATCHED_EARLY_STOP if early else 0
+    c, k, r, outer, coarsest = wl.wl_stable_coloring_batched(g, init_t, seed, mb, options=opts)
     got = c.numpy().view(np.uint32)
-    ref, kr, rr, orr, cr, st = oracle.batched_coloring(rp, col, wt, init, seed, mb)
+    ref, kr, rr, orr, cr, st = oracle.batched_coloring(rp, col, wt, init, seed, mb,
+                                                       early_stop=early)
     assert st == 0
     assert np.array_equal(got, ref)
     assert (k, outer, coarsest) == (kr, orr, cr)
@@ -204,3 +206,51 @@ def test_pageable_copies_without_staging(monkeypatch):
     c, k, r = wl.wl_stable_coloring_streamed(hg, None, 3)
     co, ko, ro, _, _ = oracle.stable_coloring(g.row_ptr, g.col, None, None, 3)
     assert (k, r) == (ko, ro) and np.array_equal(c.numpy().view(np.uint32), co)
+
+
+# Section 5.4's early stop (WL_BATCHED_EARLY_STOP without the exact finish)
+# against the batched oracle with the same rule: colours, colour count,
+# rounds, outer iterations and the coarsest flag.
+
+@pytest.mark.parametrize("seed,mb", [(1, 40), (2, 120), (3, 300), (4, 900), (6, 3)])
+def test_early_stop_rmat(seed, mb):
+    g = inputs.rmat(9, 8, seed=seed)
+    print(f"early stop rmat9 seed={seed} mb={mb}", flush=True)
+    _check(g.row_ptr, g.col, mb=mb, seed=seed, early=True)
+
+
+def test_early_stop_path_with_isolated_nodes():
+    # the rule fires after the first outer iteration (the quotient keeps
+    # every entry); the oracle's pins derive that in closed form
+    L, every, mb = 200, 7, 31
+    order = []
+    p = 0
+    while p < L:
+        for _ in range(min(every, L - p)):
+            order.append(p)
+            p += 1
+        order.append(-1)
+    node = {v: i for i, v in enumerate(order) if v >= 0}
+    rp, col = bf.to_csr(len(order), [(node[i], node[i + 1]) for i in range(L - 1)])
+    got, k, r, outer, coarsest = _check(rp, col, mb=mb, early=True)
+    assert outer == 1 and not coarsest
+
+
+@pytest.mark.parametrize("trial", range(4))
+def test_early_stop_weighted_labels(trial):
+    rng = random.Random(90 + trial)
+    n = rng.randint(50, 400)
+    edges = [(rng.randrange(n), rng.randrange(n)) for _ in range(rng.randint(n, 6 * n))]
+    rp, col = bf.to_csr(n, edges, directed=True)
+    wt = np.array([rng.randint(1, 5) for _ in range(col.size)], np.uint32)
+    init = np.array([rng.choice([3, 9]) for _ in range(n)], np.uint32) if trial % 2 else None
+    for mb in (9, 60, 10**6):
+        _check(rp, col, wt, init, mb=mb, seed=trial, pinned=bool(trial % 2), early=True)
+
+
+def test_early_stop_rmat_larger():
+    # R-MAT scale 14: several batches and outer iterations
+    g = inputs.rmat(14, 8, seed=3)
+    for mb in (20000, 60000):
+        print(f"early stop rmat14 mb={mb}", flush=True)
+        _check(g.row_ptr, g.col, mb=mb, seed=5, early=True)

@@ -165,3 +165,97 @@ def test_batched_weighted_quotient_input():
         truth = bf.partition_of(oracle.stable_coloring(rp, col, wt)[0])
         if coarsest:
             assert bf.partition_of(c) == truth
+
+
+def _path_with_isolated(L, every):
+    """Path 0-1-...-(L-1) on the path nodes, with an isolated node inserted
+    after every 'every' path nodes.  Returns (rp, col, is_path)."""
+    order = []
+    p = 0
+    while p < L:
+        for _ in range(min(every, L - p)):
+            order.append(("p", p))
+            p += 1
+        order.append(("iso", None))
+    n = len(order)
+    node_of_path = {}
+    for v, (kind, idx) in enumerate(order):
+        if kind == "p":
+            node_of_path[idx] = v
+    edges = [(node_of_path[i], node_of_path[i + 1]) for i in range(L - 1)]
+    rp, col = bf.to_csr(n, edges)
+    is_path = np.array([kind == "p" for kind, _ in order])
+    return rp, col, is_path
+
+
+@pytest.mark.parametrize("L,every,mb", [(60, 5, 14), (200, 7, 31), (90, 3, 20)])
+def test_early_stop_fires_after_first_iteration(L, every, mb):
+    """Section 5.4's termination on a path with isolated nodes spread over
+    it.  Rows never exceed the cap, so every node is inner to the batch that
+    holds its row.  Within a batch, the path nodes are pinned by the frozen
+    singletons next to the batch (or by the path's end) and all end up as
+    singletons; the isolated nodes of a batch share z = 0 in every round and
+    form one block.  The quotient therefore keeps every entry, is cut into
+    the same ranges, and the early stop ends the loop after one outer
+    iteration.  Without it, the second iteration merges nothing more (each
+    batch now holds a single isolated block) and ends at the fixed point."""
+    rp, col, is_path = _path_with_isolated(L, every)
+    n = rp.size - 1
+    starts = oracle.batch_cut(rp, mb).astype(np.int64)
+    nb = starts.size - 1
+    assert nb >= 2
+    # batch of every isolated row: the range that holds its start offset
+    iso = np.flatnonzero(~is_path)
+    off = rp.astype(np.int64)[iso]
+    bat = np.minimum(np.searchsorted(starts, off, side="right") - 1, nb - 1)
+    want_k = L + len(set(bat.tolist()))
+    # expected colouring: path nodes singletons, one block per batch of
+    # isolated rows, numbered by first occurrence
+    key = [("p", v) if is_path[v] else ("b", int(bat[np.searchsorted(iso, v)]))
+           for v in range(n)]
+    ids = {}
+    want = np.array([ids.setdefault(kk, len(ids)) for kk in key], np.uint32)
+
+    c, k, r, outer, coarsest, st = oracle.batched_coloring(rp, col, max_batch=mb,
+                                                           early_stop=True)
+    assert st == 0 and outer == 1 and not coarsest
+    assert k == want_k and np.array_equal(c, want)
+    c2, k2, r2, outer2, coarsest2, st2 = oracle.batched_coloring(rp, col, max_batch=mb)
+    assert st2 == 0 and outer2 == 2 and not coarsest2
+    assert np.array_equal(c2, c) and r2 > r
+    assert oracle.is_stable(rp, col, None, c)
+
+
+def test_early_stop_does_not_fire_while_batches_shrink():
+    # 30 disjoint P4s, two per batch: every batch contracts to 2 blocks and
+    # 3 entries, so each quotient needs fewer batches and the loop runs on
+    # to a single batch (case (i)), exactly as without the early stop
+    edges = [(4 * t + i, 4 * t + i + 1) for t in range(30) for i in range(3)]
+    rp, col = bf.to_csr(120, edges)
+    plain = oracle.batched_coloring(rp, col, max_batch=12)
+    early = oracle.batched_coloring(rp, col, max_batch=12, early_stop=True)
+    assert plain[4] and early[4] and plain[3] >= 2
+    assert np.array_equal(plain[0], early[0]) and plain[1:5] == early[1:5]
+
+
+@pytest.mark.parametrize("seed,mb", [(1, 40), (2, 120), (3, 300), (4, 900)])
+def test_early_stop_is_a_prefix_of_the_plain_loop(seed, mb):
+    """The early stop only ends the outer loop sooner: it runs the same
+    iterations as the plain loop up to that point, so its colouring is
+    stable (Theorem 2), is refined into by nothing the plain loop does
+    differently (the plain colouring is a coarsening of it), and equals the
+    plain one whenever both ran the same number of outer iterations."""
+    g = inputs.rmat(9, 8, seed=seed)
+    c, k, r, outer, coarsest, st = oracle.batched_coloring(g.row_ptr, g.col, max_batch=mb,
+                                                           early_stop=True)
+    cp, kp, rp_, outerp, coarsestp, stp = oracle.batched_coloring(g.row_ptr, g.col,
+                                                                  max_batch=mb)
+    assert st == 0 and stp == 0
+    assert 1 <= outer <= outerp and r <= rp_ and k >= kp
+    assert oracle.is_stable(g.row_ptr, g.col, None, c)
+    for blk in range(k):
+        assert len(set(cp[c == blk].tolist())) == 1
+    if outer == outerp:
+        assert np.array_equal(c, cp) and coarsest == coarsestp
+    if coarsest:
+        assert outer == outerp

@@ -76,3 +76,38 @@ def test_merge_blocks(tmp_path, args):
                        timeout=120)
     print(r.stdout, r.stderr)
     assert r.returncode == 0, r.stdout + r.stderr
+
+
+@pytest.fixture(scope="module")
+def c5_checker(tmp_path_factory):
+    if shutil.which("g++") is None:
+        pytest.skip("g++ not available")
+    out = str(tmp_path_factory.mktemp("c5") / "c5_host_check")
+    src = os.path.join(HERE, "host", "c5_host_check.cpp")
+    base = ["g++", "-std=c++17", "-O1", "-g", "-pthread", src, "-o", out]
+    r = subprocess.run(base[:4] + ["-fsanitize=address,undefined",
+                                   "-fno-sanitize-recover=undefined"] + base[4:],
+                       capture_output=True)
+    if r.returncode != 0:
+        subprocess.run(base, check=True)
+    return out
+
+
+@pytest.mark.parametrize("args", [
+    # n, entries, batch cap, quotient chunk, stream chunk, % rows needed, seed
+    (2000000, 90000000, 20000000, 500000, 1000000, 50, 3),    # rows longer than a chunk
+    # more than 2^32 entries: every entry offset, count and chunk plan of
+    # Algorithm 2 and the streamed rounds beyond 32 bits (about 40 s)
+    (1 << 26, 4400000000, 1000000000, 240000000, 1 << 26, 30, 2),
+])
+def test_out_of_core_host_logic_at_scale(c5_checker, args):
+    # The host side of Algorithm 2 after an outer iteration's batches (batch
+    # cut, inner rows, merged partition, quotient chunk plan, Section 5.4's
+    # early-stop test) and of the streamed rounds on the weighted quotient,
+    # under AddressSanitizer and UndefinedBehaviorSanitizer; the entry
+    # arrays are zero-page mappings, so 4.4e9 entries cost no memory.
+    r = subprocess.run([c5_checker] + [str(a) for a in args], capture_output=True, text=True,
+                       timeout=600)
+    print(r.stdout, r.stderr)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.rstrip().endswith("ok")
