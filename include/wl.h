@@ -149,6 +149,31 @@ int wl_stable_coloring(const wl_csr *g, const uint32_t *init_color,
                        uint32_t *k_out, uint32_t *rounds_out, void *workspace,
                        uint64_t ws_bytes, void *stream);
 
+/* Allocation-free variant of wl_stable_coloring, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It computes exactly what
+ * wl_stable_coloring computes (same colours, colour count and rounds, the
+ * same errors) but takes no workspace: its device scratch is a fixed array
+ * of WL_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held from
+ * the library's load until the process ends.  It calls no hipMalloc,
+ * hipFree or other allocating routine, and creates no stream, event or
+ * graph (WL_GRAPH and the wl_stats diagnostics do not apply to it).
+ *   g, init_color, seed, max_rounds, color_out, k_out, rounds_out
+ *               as for wl_stable_coloring (device CSR, device arrays).
+ *   stream      must belong to the current device (WL_EINVAL otherwise).
+ * Limit: graphs whose wl_workspace_size() without WL_CSR_SYMMETRIC exceeds
+ * WL_NOALLOC_SCRATCH_BYTES (about 130 bytes per node plus a few per entry,
+ * so some 400,000 nodes) are refused with WL_EBUDGET before any device work.
+ * Every call on one GPU uses that GPU's one scratch array: calls that
+ * overlap on a GPU (from several threads or streams) race and must be
+ * serialised by the caller.  The array keeps the last call's contents;
+ * each call initialises all of it that it reads. */
+#define WL_NOALLOC_SCRATCH_BYTES (64ull << 20)
+int wl_stable_coloring_noalloc(const wl_csr *g, const uint32_t *init_color,
+                               uint64_t seed, uint32_t max_rounds,
+                               uint32_t *color_out, uint32_t *k_out,
+                               uint32_t *rounds_out, void *stream);
+
 /* Algorithm 1 (Section 4.1) for a graph whose edge arrays stay in host
  * memory.  Each round, the rows whose image is needed (those of colour
  * classes with two or more members) are packed by host threads into

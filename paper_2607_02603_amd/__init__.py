@@ -32,7 +32,9 @@ EXPORTED = ["wl_workspace_size", "wl_batched_workspace_size", "wl_refine_round",
             "wl_stable_coloring", "wl_stable_coloring_batched", "wl_streamed_workspace_size",
             "wl_stable_coloring_streamed", "wl_verify_workspace_size", "wl_verify_stable",
             "wl_stats_enable", "wl_stats_get", "wl_set_precision", "wl_get_precision",
-            "wl_last_error"]
+            "wl_stable_coloring_noalloc", "wl_last_error"]
+
+WL_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 WL_STATS_TIME = 1
 WL_STATS_WORK = 2
@@ -98,6 +100,8 @@ def lib():
         L.wl_refine_round.argtypes = [P(WlCsr), vp, u32, u64, u32, vp, P(u32), vp, u64, vp]
         L.wl_stable_coloring.argtypes = [P(WlCsr), vp, u64, u32, vp, P(u32), P(u32), vp,
                                          u64, vp]
+        L.wl_stable_coloring_noalloc.argtypes = [P(WlCsr), vp, u64, u32, vp, P(u32), P(u32),
+                                                 vp]
         L.wl_stable_coloring_batched.argtypes = [P(WlCsr), vp, u64, u64, u32, vp, P(u32),
                                                  P(u32), P(u32), P(i32), vp, u64, vp]
         L.wl_streamed_workspace_size.argtypes = [P(WlCsr), P(u64)]
@@ -248,6 +252,23 @@ def wl_stable_coloring(g, init_color=None, seed=0, max_rounds=0, color_out=None,
                                     _ptr(ws), ws.numel(), _stream(stream))
     if not (allow_max_rounds and code == WL_EMAXROUNDS):
         _check(code)
+    return color_out, int(k.value), int(r.value)
+
+
+def wl_stable_coloring_noalloc(g, init_color=None, seed=0, max_rounds=0, color_out=None,
+                               stream=None):
+    """Algorithm 1 to completion without a workspace (the library's fixed
+    per-GPU scratch of WL_NOALLOC_SCRATCH_BYTES).  Returns (colors, k,
+    rounds).  Only the output array is allocated here, and only when
+    color_out is None."""
+    if color_out is None:
+        color_out = torch.empty(g.n, dtype=torch.int32, device=g.device)
+    k = ctypes.c_uint32(0)
+    r = ctypes.c_uint32(0)
+    s = g.csr()
+    _check(lib().wl_stable_coloring_noalloc(ctypes.byref(s), _ptr(init_color), seed,
+                                            max_rounds, _ptr(color_out), ctypes.byref(k),
+                                            ctypes.byref(r), _stream(stream)))
     return color_out, int(k.value), int(r.value)
 
 

@@ -1561,6 +1561,37 @@ int verify_run(const wl_csr* g, const uint32_t* color, uint32_t k, uint8_t* ws,
 // C ABI
 // ---------------------------------------------------------------------------
 
+// Device scratch of wl_stable_coloring_noalloc: one array per GPU, held for
+// the life of the process, in place of the caller's workspace.  Host code
+// never passes 'scratch' itself to a kernel or a copy: its device address on
+// the current GPU comes from hipGetSymbolAddress (scratch_address below).
+__device__ __align__(256) uint8_t scratch[WL_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of 'scratch' on the current device, looked up once per
+// device and kept.
+int scratch_address(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(WL_EINVAL, "device %d is beyond the %d devices the scratch table holds", dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(WL_EHIP, "hipGetSymbolAddress gave no address for the scratch");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return WL_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char* wl_last_error(void) { return g_err; }
@@ -1679,6 +1710,51 @@ int wl_stable_coloring(const wl_csr* g, const uint32_t* init_color, uint64_t see
   if (int r = S.stats_begin()) return r;
   if (int r = S.run_rsc(init_color)) return r;
   if (int r = S.stats_end()) return r;
+  *k_out = S.host.k;
+  *rounds_out = S.host.round;
+  if (S.host.done == 2)
+    return fail(WL_EMAXROUNDS, "no stable colouring after %u rounds", S.host.round);
+  return WL_OK;
+}
+
+int wl_stable_coloring_noalloc(const wl_csr* g, const uint32_t* init_color, uint64_t seed,
+                               uint32_t max_rounds, uint32_t* color_out, uint32_t* k_out,
+                               uint32_t* rounds_out, void* stream) {
+  g_err[0] = 0;
+  if (int r = check_graph(g)) return r;
+  if (!k_out || !rounds_out) return fail(WL_EINVAL, "output scalar is NULL");
+  *k_out = 0;
+  *rounds_out = 0;
+  if (g->n == 0) return WL_OK;
+  if (!color_out) return fail(WL_EINVAL, "color_out is NULL");
+  // the in-core layout must fit the scratch (the binned image is used only
+  // when its larger layout fits as well)
+  const uint64_t need = make_layout(g->n, g->nnz).total;
+  if (need > WL_NOALLOC_SCRATCH_BYTES)
+    return fail(WL_EBUDGET,
+                "graph needs %llu bytes of workspace; the fixed scratch holds %llu "
+                "(use wl_stable_coloring with a workspace of that size)",
+                (unsigned long long)need, (unsigned long long)WL_NOALLOC_SCRATCH_BYTES);
+  if (stream) {
+    int sdev = -1, cur = -1;
+    HIP_TRY(hipStreamGetDevice((hipStream_t)stream, &sdev));
+    HIP_TRY(hipGetDevice(&cur));
+    if (sdev != cur)
+      return fail(WL_EINVAL, "the stream belongs to device %d, the current device is %d",
+                  sdev, cur);
+  }
+  void* ws = nullptr;
+  if (int r = scratch_address(&ws)) return r;
+  Session S;
+  if (int r = open_session(S, g, color_out, ws, WL_NOALLOC_SCRATCH_BYTES, stream)) return r;
+  S.use_graph = false;  // no graph objects: nothing is created
+  if (int r = check_nnz_device(g, S.s)) return r;
+  const uint32_t cap = max_rounds ? max_rounds : (uint32_t)std::min<uint64_t>(g->n + 1, 0xFFFFFFFFull);
+  if (int r = S.init_state(seed, 1, 0, cap, 1)) return r;
+  if (int r = S.validate_device()) return r;
+  if (int r = S.check_ring()) return r;
+  if (int r = S.run_rsc(init_color)) return r;
+  if (int r = S.pull()) return r;
   *k_out = S.host.k;
   *rounds_out = S.host.round;
   if (S.host.done == 2)

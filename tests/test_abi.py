@@ -180,3 +180,22 @@ def test_exact_finish_limited_to_verified_size():
                                             ctypes.c_void_p(256), 1 << 30, None)
         assert code == wl.WL_EINVAL
         assert b"2^31" in L.wl_last_error()
+
+
+def test_noalloc_refuses_graphs_beyond_its_scratch():
+    # the size check comes before any device work
+    _ensure_built()
+    L = wl.lib()
+    s = _csr(2_000_000, 0, rp32=False)
+    k, r = ctypes.c_uint32(0), ctypes.c_uint32(0)
+    code = L.wl_stable_coloring_noalloc(ctypes.byref(s), None, 0, 0, ctypes.c_void_p(256),
+                                        ctypes.byref(k), ctypes.byref(r), None)
+    assert code == wl.WL_EBUDGET
+    assert b"scratch" in L.wl_last_error()
+    need = ctypes.c_uint64(0)
+    assert L.wl_workspace_size(ctypes.byref(s), ctypes.byref(need)) == wl.WL_OK
+    assert need.value > wl.WL_NOALLOC_SCRATCH_BYTES
+    # an empty graph needs nothing
+    s = _csr(0, 0)
+    assert L.wl_stable_coloring_noalloc(ctypes.byref(s), None, 0, 0, None, ctypes.byref(k),
+                                        ctypes.byref(r), None) == wl.WL_OK
