@@ -872,7 +872,7 @@ struct Session {
       hipLaunchKernelGGL(k_pb_scatter1<RP>, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 2048)),
                          dim3(kPbThreads), 0, s, ctx, pb);
       if (P.levels == 2) {
-        hipLaunchKernelGGL(k_pb_scatter2, dim3(std::max<uint32_t>(1, std::min<uint32_t>(pbc.ntiles2, 2048))),
+        hipLaunchKernelGGL(k_pb_scatter2, dim3(std::max<uint32_t>(1, pbc.maxtiles2 * P.nb1)),
                            dim3(kPbThreads), 0, s, ctx, pb);
       }
       const dim3 ga(std::max<uint32_t>(1, std::min<uint32_t>(pbc.nslices, 2048)));

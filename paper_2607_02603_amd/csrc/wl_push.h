@@ -12,7 +12,10 @@
 //           one run per bin, reserved with an atomic on the bin's cursor;
 //   pass 2  only when there are more than kPbMaxBins fine bins: pass 1 used
 //           coarse bins of 2^fbits fine bins each; every coarse bin is split
-//           into its fine bins the same way (run offsets from atomics);
+//           into its fine bins the same way (run offsets from atomics), one
+//           tile of kPbTile2 records per workgroup, neighbouring workgroups
+//           on different coarse bins so that their reservations on the
+//           bins' cursors do not queue behind each other;
 //   pass 3  one workgroup per fine bin of kPbFineRows rows, or per slice of
 //           at most kPbSlice records of a larger one, adds W(colour) of its
 //           records into per-row accumulators in LDS; single-slice bins
@@ -33,7 +36,7 @@ constexpr uint32_t kPbFineRows = 1u << kPbFineShift;  // rows per fine bin
 constexpr uint32_t kPbMaxBins = 256;                  // bins of pass 1
 constexpr uint32_t kPbMaxFine = 512;                  // fine bins per coarse bin
 constexpr uint32_t kPbTile = 8192;                    // entries per pass-1 tile
-constexpr uint32_t kPbTile2 = 8192;                   // records per pass-2 tile
+constexpr uint32_t kPbTile2 = 4096;                   // records per pass-2 tile
 constexpr uint32_t kPbSlice = 1u << 20;               // records per pass-3 item
 constexpr int kPbThreads = 256;                       // pass 1 and 2
 constexpr int kPbAccThreads = 1024;                   // pass 3
@@ -47,6 +50,7 @@ struct PbCounts {
   uint32_t nslices;   // pass-3 work items
   uint32_t nmulti;    // fine bins with several slices
   uint32_t mslices;   // slices of those bins
+  uint32_t maxtiles2; // most pass-2 tiles of one coarse bin
 };
 
 struct PbCtx {
@@ -110,6 +114,7 @@ __device__ __forceinline__ uint32_t pb_block_scan(uint32_t v, uint32_t* sh, uint
 
 template <typename RP>
 __global__ void __launch_bounds__(kBlock) k_pb_bin_starts(Ctx ctx, PbCtx pb) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) pb.cnt->maxtiles2 = 0;
   for (uint32_t b = blockIdx.x * kBlock + threadIdx.x; b <= pb.nfine; b += gridDim.x * kBlock) {
     pb.bstartf[b] = bin_start<RP>(ctx, b, kPbFineShift);
     if (b <= pb.nb1) pb.bstart1[b] = bin_start<RP>(ctx, b, pb.shift1);
@@ -144,6 +149,7 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_lists(Ctx ctx, PbCtx pb) {
       const uint32_t ex = pb_block_scan<kPbThreads>(nt, sh, &tot);
       if (b < pb.nb1) pb.tile2_off[b] = carry + ex;
       carry += tot;
+      if (nt) atomicMax(&pb.cnt->maxtiles2, nt);
     }
     if (threadIdx.x == 0) {
       pb.tile2_off[pb.nb1] = carry;
@@ -184,8 +190,9 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_lists(Ctx ctx, PbCtx pb) {
 // Passes 1 and 2 share the staging scheme: every record of a tile gets its
 // rank inside its bin from an LDS atomic, the bins' run offsets come from a
 // block scan and one cursor reservation per bin and tile, the records are
-// staged in bin order in LDS and written out four consecutive slots per
-// thread (staged slot s of bin b goes to dd[b] + s).
+// staged in bin order in LDS and written out one slot per lane, consecutive
+// over the lanes (staged slot s of bin b goes to dd[b] + s), so a wave's
+// store covers whole runs.
 // ---------------------------------------------------------------------------
 
 constexpr long long kPbSkip = -(1ll << 62);  // dd of a run that is not written
@@ -194,32 +201,9 @@ template <typename BT>
 __device__ __forceinline__ void pb_write_out(const uint32_t* buf, const BT* sbin,
                                              const long long* dd, uint32_t cnt,
                                              uint32_t* out) {
-  for (uint32_t s = 4 * threadIdx.x; s < cnt; s += 4 * kPbThreads) {
-    const uint4 v = *(const uint4*)&buf[s];
-    const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
-    BT b[4];
-    if (sizeof(BT) == 1) {
-      const uint32_t w = *(const uint32_t*)&sbin[s];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) b[u] = (BT)((w >> (8 * u)) & 0xFF);
-    } else {
-      const uint2 w = *(const uint2*)&sbin[s];
-      b[0] = (BT)(w.x & 0xFFFF);
-      b[1] = (BT)(w.x >> 16);
-      b[2] = (BT)(w.y & 0xFFFF);
-      b[3] = (BT)(w.y >> 16);
-    }
-    BT last = b[0];
-    long long o = dd[last];
-#pragma unroll
-    for (uint32_t u = 0; u < 4; ++u)
-      if (s + u < cnt) {
-        if (b[u] != last) {
-          last = b[u];
-          o = dd[last];
-        }
-        if (o != kPbSkip) out[o + s + u] = vv[u];
-      }
+  for (uint32_t s = threadIdx.x; s < cnt; s += kPbThreads) {
+    const long long o = dd[sbin[s]];
+    if (o != kPbSkip) out[o + s] = buf[s];
   }
 }
 
@@ -414,75 +398,47 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
   __shared__ uint32_t sh[kPbThreads / kWave];
   const uint32_t nf = 1u << pb.fbits;
   const uint32_t cmask = (1u << pb.cbits) - 1;
-  const uint32_t ntiles = pb.cnt->ntiles2;
   constexpr uint32_t kPer = kPbTile2 / kPbThreads;
-  // tile t: coarse bin, first record, record count
-  auto tile_of = [&](uint32_t t, uint32_t* cbo, uint64_t* ao, uint32_t* cnto) {
-    uint32_t lo = 0, hi = pb.nb1 - 1;  // last b with tile2_off[b] <= t
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi + 1) >> 1;
-      if (pb.tile2_off[mid] <= t) lo = mid; else hi = mid - 1;
-    }
-    *cbo = lo;
-    *ao = pb.bstart1[lo] + (uint64_t)(t - pb.tile2_off[lo]) * kPbTile2;
-    *cnto = (uint32_t)(min(pb.bstart1[lo + 1], *ao + kPbTile2) - *ao);
-  };
-  // records of the next tile are loaded while the current one is processed
-  uint32_t nxt[kPer];
-  uint32_t ncb = 0, ncnt = 0;
-  uint64_t na = 0;
-  if (blockIdx.x < ntiles) {
-    tile_of(blockIdx.x, &ncb, &na, &ncnt);
+  // block v: tile v / nb1 of coarse bin v % nb1 (neighbouring blocks work on
+  // different coarse bins, so their cursor reservations do not collide)
+  const uint32_t cb = blockIdx.x % pb.nb1, r = blockIdx.x / pb.nb1;
+  if (pb.tile2_off[cb] + r >= pb.tile2_off[cb + 1]) return;
+  const uint64_t a0 = pb.bstart1[cb] + (uint64_t)r * kPbTile2;
+  const uint32_t cnt = (uint32_t)(min(pb.bstart1[cb + 1], a0 + kPbTile2) - a0);
+  uint32_t rec[kPer];
 #pragma unroll
-    for (uint32_t k = 0; k < kPer; ++k) {
-      const uint32_t q = k * kPbThreads + threadIdx.x;
-      nxt[k] = q < ncnt ? pb.rec1[na + q] : 0u;
+  for (uint32_t k = 0; k < kPer; ++k) {
+    const uint32_t q = k * kPbThreads + threadIdx.x;
+    rec[k] = q < cnt ? pb.rec1[a0 + q] : 0u;
+  }
+  const uint32_t nfb = min(nf, pb.nfine - (cb << pb.fbits));
+  for (uint32_t b = threadIdx.x; b < nf; b += kPbThreads) hist[b] = 0;
+  __syncthreads();
+  uint32_t pk[kPer];
+#pragma unroll
+  for (uint32_t k = 0; k < kPer; ++k) {
+    pk[k] = 0xFFFFFFFFu;
+    if (k * kPbThreads + threadIdx.x < cnt) {
+      const uint32_t local = rec[k] >> pb.cbits;
+      const uint32_t b = min(local >> kPbFineShift, nfb - 1);
+      pk[k] = (b << 16) | atomicAdd(&hist[b], 1u);
+      rec[k] = ((local & (kPbFineRows - 1)) << pb.cbits) | (rec[k] & cmask);
     }
   }
-  for (uint32_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
-    const uint32_t cb = ncb, cnt = ncnt;
-    uint32_t rec[kPer];
+  __syncthreads();
+  pb_reserve(ctx, hist, dd, sh, nfb, pb.cur2 + ((uint64_t)cb << pb.fbits),
+             pb.bstartf + ((uint64_t)cb << pb.fbits));
+  __syncthreads();
 #pragma unroll
-    for (uint32_t k = 0; k < kPer; ++k) rec[k] = nxt[k];
-    if (t + gridDim.x < ntiles) {
-      tile_of(t + gridDim.x, &ncb, &na, &ncnt);
-#pragma unroll
-      for (uint32_t k = 0; k < kPer; ++k) {
-        const uint32_t q = k * kPbThreads + threadIdx.x;
-        nxt[k] = q < ncnt ? pb.rec1[na + q] : 0u;
-      }
+  for (uint32_t k = 0; k < kPer; ++k)
+    if (pk[k] != 0xFFFFFFFFu) {
+      const uint32_t b = pk[k] >> 16;
+      const uint32_t slot = hist[b] + (pk[k] & 0xFFFF);
+      buf[slot] = rec[k];
+      sbin[slot] = (uint16_t)b;
     }
-    const uint32_t nfb = min(nf, pb.nfine - (cb << pb.fbits));  // fine bins of this coarse bin
-    for (uint32_t b = threadIdx.x; b < nf; b += kPbThreads) hist[b] = 0;
-    __syncthreads();
-    // fine bin = (local >> kPbFineShift) of the coarse record; packed rank
-    uint32_t pk[kPer];
-#pragma unroll
-    for (uint32_t k = 0; k < kPer; ++k) {
-      pk[k] = 0xFFFFFFFFu;
-      if (k * kPbThreads + threadIdx.x < cnt) {
-        const uint32_t local = rec[k] >> pb.cbits;
-        const uint32_t b = min(local >> kPbFineShift, nfb - 1);
-        pk[k] = (b << 16) | atomicAdd(&hist[b], 1u);
-        rec[k] = ((local & (kPbFineRows - 1)) << pb.cbits) | (rec[k] & cmask);
-      }
-    }
-    __syncthreads();
-    pb_reserve(ctx, hist, dd, sh, nfb, pb.cur2 + ((uint64_t)cb << pb.fbits),
-               pb.bstartf + ((uint64_t)cb << pb.fbits));
-    __syncthreads();
-#pragma unroll
-    for (uint32_t k = 0; k < kPer; ++k)
-      if (pk[k] != 0xFFFFFFFFu) {
-        const uint32_t b = pk[k] >> 16;
-        const uint32_t slot = hist[b] + (pk[k] & 0xFFFF);
-        buf[slot] = rec[k];
-        sbin[slot] = (uint16_t)b;
-      }
-    __syncthreads();
-    pb_write_out<uint16_t>(buf, sbin, dd, cnt, pb.rec2);
-    __syncthreads();
-  }
+  __syncthreads();
+  pb_write_out<uint16_t>(buf, sbin, dd, cnt, pb.rec2);
 }
 
 // ---------------------------------------------------------------------------

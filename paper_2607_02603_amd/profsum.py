@@ -3,6 +3,7 @@ profiles/.
 
     python -m paper_2607_02603_amd.profsum trace DB CALLS TITLE COMMAND > out.md
     python -m paper_2607_02603_amd.profsum traffic FETCH_DB WRITE_DB KERNELS... > out.json
+    python -m paper_2607_02603_amd.profsum counters KERNELS -- DB... > out.md
 
 'trace' tabulates the library's kernels of a --kernel-trace run (per-call
 figures are totals divided by CALLS, the number of library calls the traced
@@ -11,7 +12,11 @@ program made).  'traffic' sums, per launch of the propagation-blocking image
 counters of two --pmc runs and scales them by what the same counters read for
 the 1 GiB device-to-device copy that bench.py --copy-probe issues first
 (bytes moved / counter value); the result records the SHA-256 of the source
-file of those kernels so that a stale figure is not reported.
+file of those kernels so that a stale figure is not reported.  'counters'
+tabulates, per kernel of the last library call (names matched by prefix,
+comma-separated), every counter of one or more --pmc databases (one per
+counter pass), summed over the kernel's dispatches and hardware instances,
+with the ratios that name a kernel's bound.
 """
 import hashlib
 import json
@@ -122,9 +127,95 @@ def traffic(fetch_db, write_db, kernels):
                      "top_kernels_bytes": top}}
 
 
+
+def _last_call(ev):
+    lib = [(n, c) for n, c in ev if _is_lib(n)]
+    starts = [i for i, (n, _) in enumerate(lib) if "k_iota_zero" in n]
+    return lib[starts[-1]:] if starts else lib
+
+
+def counters(kernels, dbs):
+    """{kernel: {counter: value summed over its dispatches}} over the last
+    library call of each database (one database per counter pass)."""
+    out = {k: {"dispatches": 0} for k in kernels}
+    npass = {k: {} for k in kernels}  # passes that collected each counter
+    for db in dbs:
+        seen = {k: 0 for k in kernels}
+        got = {k: {} for k in kernels}
+        for n, c in _last_call(_pmc(db)):
+            s = _short(n)
+            for k in kernels:
+                if s.startswith(k):
+                    seen[k] += 1
+                    for cn, v in c.items():
+                        got[k][cn] = got[k].get(cn, 0.0) + v
+        for k in kernels:
+            out[k]["dispatches"] = max(out[k]["dispatches"], seen[k])
+            for cn, v in got[k].items():
+                out[k][cn] = out[k].get(cn, 0.0) + v
+                npass[k][cn] = npass[k].get(cn, 0) + 1
+    # a counter collected in several passes (GRBM_GUI_ACTIVE): their mean
+    for k in kernels:
+        for cn, m in npass[k].items():
+            out[k][cn] /= m
+    return out
+
+
+def counters_markdown(kernels, dbs, cu_num=256):
+    res = counters(kernels, dbs)
+    names = sorted({cn for k in kernels for cn in res[k] if cn != "dispatches"})
+    out = ["| counter | " + " | ".join(kernels) + " |",
+           "|---|" + "---|" * len(kernels)]
+    for cn in ["dispatches"] + names:
+        out.append(f"| {cn} | " + " | ".join(f"{res[k].get(cn, float('nan')):.4g}"
+                                            for k in kernels) + " |")
+    # ratios used to name each kernel's bound
+    def row(label, f):
+        vals = []
+        for k in kernels:
+            try:
+                vals.append(f"{f(res[k]):.3g}")
+            except (KeyError, ZeroDivisionError):
+                vals.append("n/a")
+        out.append(f"| {label} | " + " | ".join(vals) + " |")
+    out += ["", "| derived | " + " | ".join(kernels) + " |", "|---|" + "---|" * len(kernels)]
+    # GRBM_GUI_ACTIVE is summed over the 8 XCDs: per XCD it is the
+    # dispatch's busy cycles
+    gui = lambda r: r["GRBM_GUI_ACTIVE"] / 8  # noqa: E731
+    row("busy cycles per dispatch (GRBM_GUI_ACTIVE / 8 / dispatches)",
+        lambda r: gui(r) / r["dispatches"])
+    row("mean waves per CU (4 x SQ_WAVE_CYCLES / busy cycles / CUs; 32 max)",
+        lambda r: 4 * r["SQ_WAVE_CYCLES"] / gui(r) / cu_num)
+    row("VALU busy, % (SQ_ACTIVE_INST_VALU / CUs / busy cycles)",
+        lambda r: 100 * r["SQ_ACTIVE_INST_VALU"] / cu_num / gui(r))
+    row("LDS busy, % (SQ_LDS_IDX_ACTIVE / CUs / busy cycles)",
+        lambda r: 100 * r["SQ_LDS_IDX_ACTIVE"] / cu_num / gui(r))
+    row("LDS bank-conflict stalls, % (SQ_LDS_BANK_CONFLICT / CUs / busy cycles)",
+        lambda r: 100 * r["SQ_LDS_BANK_CONFLICT"] / cu_num / gui(r))
+    row("LDS bank conflicts per LDS busy cycle",
+        lambda r: r["SQ_LDS_BANK_CONFLICT"] / r["SQ_LDS_IDX_ACTIVE"])
+    row("wave-cycles waiting on LDS / wave-cycles (SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES)",
+        lambda r: r["SQ_WAIT_INST_LDS"] / r["SQ_WAVE_CYCLES"])
+    row("wave-cycles waiting on anything / wave-cycles (SQ_WAIT_ANY / SQ_WAVE_CYCLES)",
+        lambda r: r["SQ_WAIT_ANY"] / r["SQ_WAVE_CYCLES"])
+    row("LDS instructions per wave", lambda r: r["SQ_INSTS_LDS"] / r["SQ_WAVES"])
+    row("LDS atomic instructions per wave", lambda r: r["SQ_INSTS_LDS_ATOMIC"] / r["SQ_WAVES"])
+    row("VALU instructions per wave", lambda r: r["SQ_INSTS_VALU"] / r["SQ_WAVES"])
+    row("vector memory reads per wave",
+        lambda r: r["SQ_INSTS_VMEM_RD"] / r["SQ_WAVES"])
+    row("vector memory writes per wave", lambda r: r["SQ_INSTS_VMEM_WR"] / r["SQ_WAVES"])
+    row("memory writes of 64 B, % of write requests (TCC_EA0_WRREQ_64B / TCC_EA0_WRREQ)",
+        lambda r: 100 * r["TCC_EA0_WRREQ_64B"] / r["TCC_EA0_WRREQ"])
+    row("memory reads of 32 B, % of read requests (TCC_EA0_RDREQ_32B / TCC_EA0_RDREQ)",
+        lambda r: 100 * r["TCC_EA0_RDREQ_32B"] / r["TCC_EA0_RDREQ"])
+    return "\n".join(out)
+
 def main(argv):
     if len(argv) >= 5 and argv[0] == "trace":
         print(trace_markdown(argv[1], int(argv[2]), argv[3], argv[4]))
+    elif len(argv) >= 4 and argv[0] == "counters" and "--" in argv:
+        cut = argv.index("--")
+        print(counters_markdown(argv[1].split(","), argv[cut + 1:]))
     elif len(argv) >= 4 and argv[0] == "traffic":
         print(json.dumps(traffic(argv[1], argv[2], argv[3:]), indent=1))
     else:
