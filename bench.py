@@ -12,6 +12,12 @@ dominant image launch (the step "z = A w" of a round; on R-MAT scale 27 the
 propagation-blocking image of the full round) and the CPU oracle timed on a
 bounded sample.  The roofline's HBM traffic comes from the rocprofv3 counter
 summary under profiles/ when it was taken on the current kernel source.
+config also carries the rate of the CSR entries the image launches actually
+read (active_edge_gteps: rows of classes that cannot split are skipped), the
+measured HBM traffic of the whole call over its kernel time (call_traffic,
+from the counter summary of all library kernels, when it matches the current
+sources), and, in the untimed run, whether the colour array equals the
+oracle's stored result for the workload (check).
 """
 import argparse
 import json
@@ -293,6 +299,8 @@ KIND_KERNELS = {
     "uniform": "k_deg_hist (one-colour round)",
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pb_image_rmat27_traffic.json")
+CALL_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "call_rmat27_traffic.json")
+GOLDEN_DIR = os.path.join(ROOT, "tests", "golden")
 
 
 def image_roofline(work, kind_ms, rp_bytes, workload, arith="fp"):
@@ -320,10 +328,50 @@ def image_roofline(work, kind_ms, rp_bytes, workload, arith="fp"):
             "bytes_per_launch": bytes_per_launch}
 
 
+def call_traffic(workload, arith, call_ms):
+    """Measured HBM traffic of the whole call: the counter bytes of every
+    library kernel of one call (profiles/call_rmat27_traffic.json, taken by
+    rocprofv3 on the same workload) over that call's summed kernel time, and
+    over this run's device time of the call.  None when the profile was taken
+    on other kernel sources."""
+    if workload != "rmat27" or arith != "fp" or not os.path.exists(CALL_TRAFFIC_FILE):
+        return None
+    from paper_2607_02603_amd import profsum
+    with open(CALL_TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t.get("sources_sha256") != profsum.sources_hash():
+        return None
+    return {"bytes": t["bytes"], "profiled_kernel_ms": t["kernel_ms"],
+            "frac_of_kernel_time": t["frac_of_8tbs"],
+            "frac_of_call_time": t["bytes"] / (call_ms / 1e3) / (HBM_PEAK_GBS * 1e9),
+            "source": os.path.relpath(CALL_TRAFFIC_FILE, ROOT)}
+
+
+def golden_check(workload, arith, colors, k, rounds):
+    """SHA-256 of the colour array against the oracle's stored result for
+    this workload (tests/golden, written from oracle/ only), or None."""
+    import hashlib
+    import numpy as np
+    name = {("rmat27", "fp"): "rmat27", ("rmat27", "ring64"): "rmat27_ring64",
+            ("chunglu", "fp"): "chunglu"}.get((workload, arith))
+    path = os.path.join(GOLDEN_DIR, f"full_{name}.json") if name else None
+    if not path or not os.path.exists(path):
+        return None
+    with open(path) as f:
+        gold = json.load(f)
+    host = colors.cpu().numpy().view(np.uint32)
+    sha = hashlib.sha256(host.astype("<u4").tobytes()).hexdigest()
+    return {"golden": os.path.relpath(path, ROOT),
+            "equal_to_oracle": sha == gold["sha256"] and (k, rounds) == (gold["colours"],
+                                                                         gold["rounds"])}
+
+
 def cpu_baseline(dg, seconds_target=15.0, q=0):
     """The CPU oracle (one randomized round: image + relabel) on a bounded
     sample of the same graph: the first rows of the CSR, with a pseudo-random
-    colouring of 2^20 colours.  Returns GTEPS of the sample."""
+    colouring of 2^20 colours.  Returns the sample's per-round rate in GTEPS
+    (entries of the sample over the time of that one round): a rate per
+    round, not a time to the stable colouring."""
     import numpy as np
     import oracle
     rp = dg.row_ptr.cpu().numpy().astype(np.uint64)
@@ -349,9 +397,10 @@ def cpu_baseline(dg, seconds_target=15.0, q=0):
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": m_s / dt / 1e9, "unit": "GTEPS", "cores": threads,
             "kind": "oracle",
-            "sample": f"one oracle round (image + relabel) over the first {rows} rows "
-                      f"({m_s} entries) of the same graph, 2^20 pseudo-random colours, "
-                      f"{dt:.2f} s"}
+            "sample": f"one oracle round over the first {rows} rows ({m_s} entries) of the "
+                      f"same graph with 2^20 pseudo-random colours, {dt:.2f} s: the image on "
+                      f"{threads} threads (OpenMP), the relabel (qsort) on 1 thread; a per-round "
+                      f"rate (entries / round time), not a time-to-stable"}
 
 
 def main():
@@ -411,12 +460,14 @@ def main():
         log(f"warmup {i}: colours={k} rounds={rounds}")
     # untimed run: work of every image launch (rows, entries read)
     wl.wl_stats_enable(wl.WL_STATS_TIME | wl.WL_STATS_WORK)
-    wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
+    _, k0, r0 = wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
     work = wl.wl_stats_get()
+    check = golden_check(args.workload, args.arith, colors, k0, r0)
+    log(f"result against the oracle's stored colouring: {check}")
     # timed runs: HIP events around every image launch on the library's stream
     wl.wl_stats_enable(wl.WL_STATS_TIME)
     torch.cuda.synchronize()
-    times, kind_ms = [], []
+    times, kind_ms, call_ms = [], [], []
     for i in range(args.steps):
         torch.cuda.synchronize()
         t1 = time.perf_counter()
@@ -425,6 +476,7 @@ def main():
         times.append(time.perf_counter() - t1)
         st = wl.wl_stats_get()
         kind_ms.append({kd: st[kd]["ms"] for kd in KINDS})
+        call_ms.append(st["call_ms"])
         log(f"step {i}: {times[-1] * 1e3:.2f} ms colours={k} rounds={rounds} image ms: "
             + ", ".join(f"{kd} {st[kd]['ms']:.2f} ({st[kd]['launches']})" for kd in KINDS))
     wl.wl_stats_enable(0)
@@ -432,7 +484,9 @@ def main():
     gteps = dg.nnz * rounds / step_s / 1e9
     rp_bytes = 8 if dg.row_ptr.dtype == torch.int64 else 4
     roofline = image_roofline(work, kind_ms, rp_bytes, args.workload, args.arith)
-    model_bytes = (12 * dg.nnz + (36 + rp_bytes) * dg.n) * rounds
+    # CSR entries the image launches actually read (rows of classes that
+    # cannot split are skipped)
+    active = sum(work[kd]["entries"] for kd in KINDS)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(dg, q=ARITH[args.arith][0])
@@ -457,7 +511,11 @@ def main():
                    "time_to_stable_ms": step_s * 1e3,
                    "image_ms_per_step": {kd: sum(m[kd] for m in kind_ms) / len(kind_ms)
                                          for kd in KINDS},
-                   "model_round_bytes_frac": model_bytes / step_s / 1e9 / HBM_PEAK_GBS},
+                   "active_entries_per_step": active,
+                   "active_edge_gteps": active / step_s / 1e9,
+                   "call_traffic": call_traffic(args.workload, args.arith,
+                                                sum(call_ms) / len(call_ms)),
+                   "check": check},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -870,7 +870,7 @@ struct Session {
     hipLaunchKernelGGL(k_pb_cursors, dim3(grid_for(P.nfine)), dim3(kBlock), 0, s, ctx, pb);
     timed_spmv(host.round, true, kImgPb, [&] {
       hipLaunchKernelGGL(k_pb_scatter1<RP>, dim3((uint32_t)std::min<uint64_t>(P.ntiles1, 2048)),
-                         dim3(kPbThreads), 0, s, ctx, pb);
+                         dim3(kPb1Threads), 0, s, ctx, pb);
       if (P.levels == 2) {
         hipLaunchKernelGGL(k_pb_scatter2, dim3(std::max<uint32_t>(1, pbc.maxtiles2 * P.nb1)),
                            dim3(kPbThreads), 0, s, ctx, pb);

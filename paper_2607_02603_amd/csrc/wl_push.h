@@ -38,9 +38,9 @@ constexpr uint32_t kPbMaxFine = 512;                  // fine bins per coarse bi
 constexpr uint32_t kPbTile = 8192;                    // entries per pass-1 tile
 constexpr uint32_t kPbTile2 = 4096;                   // records per pass-2 tile
 constexpr uint32_t kPbSlice = 1u << 20;               // records per pass-3 item
-constexpr int kPbThreads = 256;                       // pass 1 and 2
+constexpr int kPbThreads = 256;                       // pass 2 and the plan
+constexpr int kPb1Threads = 512;                      // pass 1
 constexpr int kPbAccThreads = 1024;                   // pass 3
-constexpr uint32_t kPbPerThread = kPbTile / kPbThreads;
 constexpr uint32_t kErrNotSymmetric = 16u;  // DevState::err bit
 constexpr uint64_t kPbMinEntries = 1ull << 22;  // smaller graphs stay in cache
 
@@ -197,11 +197,11 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_lists(Ctx ctx, PbCtx pb) {
 
 constexpr long long kPbSkip = -(1ll << 62);  // dd of a run that is not written
 
-template <typename BT>
+template <int T, typename BT>
 __device__ __forceinline__ void pb_write_out(const uint32_t* buf, const BT* sbin,
                                              const long long* dd, uint32_t cnt,
                                              uint32_t* out) {
-  for (uint32_t s = threadIdx.x; s < cnt; s += kPbThreads) {
+  for (uint32_t s = threadIdx.x; s < cnt; s += T) {
     const long long o = dd[sbin[s]];
     if (o != kPbSkip) out[o + s] = buf[s];
   }
@@ -239,16 +239,29 @@ __device__ __forceinline__ void pb_reserve(const Ctx& ctx, uint32_t* hist, long 
 // Pass 1: CSR entries -> records in pass-1 bins
 // ---------------------------------------------------------------------------
 
-// Each tile of kPbTile entries: the colour of every entry's row (row starts
-// marked in LDS; a block-wide "last mark at or before" scan in entry order,
-// one ballot and one lane permute per 4 x 64 entries), then the records are
-// staged by bin and written out (pb_reserve, pb_write_out).
+// Each tile of kPbTile entries, in the order that lets the latencies overlap:
+//   1. the column indices (registers) and the first row-start data are
+//      loaded together;
+//   2. row starts are marked in LDS (colour + 1 at the row's first entry in
+//      the tile) while every entry's bin is counted (non-returning LDS adds);
+//   3. a block scan gives each bin's run offset in the tile and one cursor
+//      reservation per bin is issued; while it is in flight, the colour of
+//      every entry's row is found from the marks (block-wide "last mark at
+//      or before" scan in entry order: one ballot and one lane permute per
+//      4 x 64 entries, the marks read twice from LDS instead of being held in
+//      registers) and the record is formed;
+//   4. the reservations give each run's output offset (dd), the records are
+//      staged by bin (one returning LDS add per record picks its slot) and
+//      written out (pb_write_out).
+// The packed bins of a thread's entries take 4 registers; no rank is kept.
+// 512 threads, 4 waves per SIMD: two workgroups per CU (at most 128 VGPRs).
 template <typename RP>
-__global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
+__global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx pb) {
+  static_assert(kPbMaxBins <= kPb1Threads, "one thread per pass-1 bin in the reservation");
   if (ctx.st->done) return;
-  constexpr uint32_t kRun = kPbTile / kPbThreads;  // entries per thread
+  constexpr uint32_t kRun = kPbTile / kPb1Threads;  // entries per thread
   constexpr uint32_t kGroups = kRun / 4;           // loads of 4 entries per thread
-  constexpr int kWaves = kPbThreads / kWave;
+  constexpr int kWaves = kPb1Threads / kWave;
   __shared__ __align__(16) uint32_t buf[kPbTile];  // row marks, then staged records
   __shared__ __align__(16) uint8_t sbin[kPbTile];  // bin of each staged record
   __shared__ uint32_t hist[kPbMaxBins];
@@ -268,12 +281,12 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
     const uint32_t cnt = (uint32_t)(e1 - e0);
     const uint32_t j0 = pb.tile_row[t];
     const uint32_t jend = t + 1 < pb.ntiles1 ? pb.tile_row[t + 1] : ctx.n - 1;
-    // column indices: slot (k, u) holds entry 4 * (k * kPbThreads + threadIdx.x) + u
+    // 1. column indices: slot (k, u) holds entry 4 * (k * kPb1Threads + threadIdx.x) + u
     uint32_t cix[kRun];
     if (cnt == kPbTile) {
 #pragma unroll
       for (uint32_t k = 0; k < kGroups; ++k) {
-        const uint4 v = col4[(e0 >> 2) + k * kPbThreads + threadIdx.x];
+        const uint4 v = col4[(e0 >> 2) + k * kPb1Threads + threadIdx.x];
         cix[4 * k] = v.x;
         cix[4 * k + 1] = v.y;
         cix[4 * k + 2] = v.z;
@@ -284,41 +297,78 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
       for (uint32_t k = 0; k < kGroups; ++k)
 #pragma unroll
         for (uint32_t u = 0; u < 4; ++u) {
-          const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
+          const uint32_t q = 4 * (k * kPb1Threads + threadIdx.x) + u;
           cix[4 * k + u] = q < cnt ? ctx.col[e0 + q] : 0u;
         }
+    }
+    // the first row starting in the tile for this thread
+    uint32_t r = j0 + 1 + threadIdx.x;
+    uint64_t rb = 0, re = 0;
+    uint32_t rc = 0;
+    if (r <= jend) {
+      rb = rp_at<RP>(ctx, r);
+      re = rp_at<RP>(ctx, r + 1);
+      rc = ctx.c[r];
     }
     const uint32_t c_first = ctx.c[j0];
     const uint4 z4 = make_uint4(0, 0, 0, 0);
 #pragma unroll
-    for (uint32_t k = 0; k < kGroups; ++k) ((uint4*)buf)[k * kPbThreads + threadIdx.x] = z4;
-    for (uint32_t b = threadIdx.x; b < kPbMaxBins; b += kPbThreads) hist[b] = 0;
+    for (uint32_t k = 0; k < kGroups; ++k) ((uint4*)buf)[k * kPb1Threads + threadIdx.x] = z4;
+    if (threadIdx.x < kPbMaxBins) hist[threadIdx.x] = 0;
     __syncthreads();
-    // colour + 1 at the first entry of every non-empty row starting in the tile
-    for (uint32_t r = j0 + 1 + threadIdx.x; r <= jend; r += kPbThreads) {
-      const uint64_t b = rp_at<RP>(ctx, r);
-      if (b < e1 && rp_at<RP>(ctx, r + 1) > b) buf[b - e0] = ctx.c[r] + 1;
+    // 2. row-start marks; bins counted
+    for (; r <= jend; r += kPb1Threads) {
+      if (rb < e1 && re > rb) buf[rb - e0] = rc + 1;
+      const uint32_t rn = r + kPb1Threads;
+      if (rn <= jend) {
+        rb = rp_at<RP>(ctx, rn);
+        re = rp_at<RP>(ctx, rn + 1);
+        rc = ctx.c[rn];
+      }
     }
-    __syncthreads();
-    // entry order is (k, thread, u): per k, the last mark of every group of
-    // 4, the last mark of the lower lanes (ballot + permute), the waves'
-    // totals through LDS
-    uint4 mk[kGroups];
-    uint32_t ex[kGroups];
+    // the 4 bins of group k, one byte each (every byte value is a bin), and
+    // bit 4k + u set when entry (k, u) has a record
+    static_assert(kRun <= 32 && kPbMaxBins <= 256, "bins packed in bytes, validity in 32 bits");
+    uint32_t bins[kGroups];
+    uint32_t valid = 0;
 #pragma unroll
     for (uint32_t k = 0; k < kGroups; ++k) {
-      mk[k] = ((const uint4*)buf)[k * kPbThreads + threadIdx.x];
-      const uint32_t g = mk[k].w ? mk[k].w : (mk[k].z ? mk[k].z : (mk[k].y ? mk[k].y : mk[k].x));
+      uint32_t w = 0;
+#pragma unroll
+      for (uint32_t u = 0; u < 4; ++u) {
+        const uint32_t q = 4 * (k * kPb1Threads + threadIdx.x) + u;
+        const uint32_t bn = cix[4 * k + u] >> pb.shift1;
+        if (q < cnt) {
+          if (bn < pb.nb1) {
+            atomicAdd(&hist[bn], 1u);
+            w |= bn << (8 * u);
+            valid |= 1u << (4 * k + u);
+          } else {  // a column >= n
+            atomicOr(&ctx.st->err, kErrNotSymmetric);
+          }
+        }
+      }
+      bins[k] = w;
+    }
+    __syncthreads();
+    // 3. run offsets and one cursor reservation per bin (thread = bin)
+    const uint32_t h = threadIdx.x < kPbMaxBins ? hist[threadIdx.x] : 0u;
+    uint32_t nrec;
+    const uint32_t ex = pb_block_scan<kPb1Threads>(h, sh, &nrec);
+    unsigned long long d = 0;
+    if (h) d = atomicAdd(&cur[threadIdx.x], (unsigned long long)h);
+    //    while it is in flight: the colour of every entry's row
+    uint32_t exk[kGroups];
+#pragma unroll
+    for (uint32_t k = 0; k < kGroups; ++k) {
+      const uint4 mk = ((const uint4*)buf)[k * kPb1Threads + threadIdx.x];
+      const uint32_t g = mk.w ? mk.w : (mk.z ? mk.z : (mk.y ? mk.y : mk.x));
       const unsigned long long m = __ballot(g != 0);
       const unsigned long long below = m & lt_mask;
       const uint32_t v = __shfl(g, below ? 63 - __builtin_clzll(below) : lane, kWave);
-      ex[k] = below ? v : 0u;
-      if (m) {
-        const uint32_t tot = __shfl(g, 63 - __builtin_clzll(m), kWave);
-        if (lane == 0) wtot[k][wid] = tot;
-      } else if (lane == 0) {
-        wtot[k][wid] = 0;
-      }
+      exk[k] = below ? v : 0u;
+      const uint32_t tot = __shfl(g, m ? 63 - __builtin_clzll(m) : 0, kWave);
+      if (lane == 0) wtot[k][wid] = m ? tot : 0u;
     }
     __syncthreads();
     uint32_t running = c_first + 1;  // last mark of every group before (k, wave)
@@ -332,47 +382,44 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter1(Ctx ctx, PbCtx pb) {
           running = x;
         }
       }
-      uint32_t c = ex[k] ? ex[k] : before;
-      uint32_t mv[4] = {mk[k].x, mk[k].y, mk[k].z, mk[k].w};
+      const uint4 mk = ((const uint4*)buf)[k * kPb1Threads + threadIdx.x];
+      const uint32_t mv[4] = {mk.x, mk.y, mk.z, mk.w};
+      uint32_t c = exk[k] ? exk[k] : before;
 #pragma unroll
       for (uint32_t u = 0; u < 4; ++u) {
         if (mv[u]) c = mv[u];
         const uint32_t i = cix[4 * k + u];
         cix[4 * k + u] = ((i & mask1) << pb.cbits) | (c - 1);  // the record
-        mv[u] = i >> pb.shift1;                                  // its bin
       }
-      mk[k] = make_uint4(mv[0], mv[1], mv[2], mv[3]);
     }
-    // ranks inside the bins: packed (bin << 16 | rank), or ~0 for no record
-    uint32_t pk[kRun];
+    // 4. output offsets of the runs (a bin without records in this tile
+    //    gets kPbSkip, so no slot can reach a stale offset), then staging
+    if (threadIdx.x < kPbMaxBins) {
+      if (!h) {
+        dd[threadIdx.x] = kPbSkip;
+      } else if (d + h > bstart[threadIdx.x + 1]) {
+        atomicOr(&ctx.st->err, kErrNotSymmetric);
+        dd[threadIdx.x] = kPbSkip;
+      } else {
+        dd[threadIdx.x] = (long long)d - (long long)ex;
+      }
+    }
+    __syncthreads();  // the marks in buf are consumed; dd is complete
+    if (threadIdx.x < kPbMaxBins) hist[threadIdx.x] = ex;
+    __syncthreads();
 #pragma unroll
-    for (uint32_t k = 0; k < kGroups; ++k) {
-      const uint32_t bv[4] = {mk[k].x, mk[k].y, mk[k].z, mk[k].w};
+    for (uint32_t k = 0; k < kGroups; ++k)
 #pragma unroll
-      for (uint32_t u = 0; u < 4; ++u) {
-        const uint32_t q = 4 * (k * kPbThreads + threadIdx.x) + u;
-        pk[4 * k + u] = 0xFFFFFFFFu;
-        if (q < cnt) {
-          if (bv[u] < pb.nb1)
-            pk[4 * k + u] = (bv[u] << 16) | atomicAdd(&hist[bv[u]], 1u);
-          else  // a column >= n
-            atomicOr(&ctx.st->err, kErrNotSymmetric);
+      for (uint32_t u = 0; u < 4; ++u)
+        if (valid & (1u << (4 * k + u))) {
+          const uint32_t bn = (bins[k] >> (8 * u)) & 0xFFu;
+          const uint32_t slot = atomicAdd(&hist[bn], 1u);
+          buf[slot] = cix[4 * k + u];
+          sbin[slot] = (uint8_t)bn;
         }
-      }
-    }
     __syncthreads();
-    pb_reserve(ctx, hist, dd, sh, pb.nb1, cur, bstart);
-    __syncthreads();
-#pragma unroll
-    for (uint32_t x = 0; x < kRun; ++x)
-      if (pk[x] != 0xFFFFFFFFu) {
-        const uint32_t b = pk[x] >> 16;
-        const uint32_t slot = hist[b] + (pk[x] & 0xFFFF);
-        buf[slot] = cix[x];
-        sbin[slot] = (uint8_t)b;
-      }
-    __syncthreads();
-    pb_write_out<uint8_t>(buf, sbin, dd, cnt, out);
+    // only the staged records (a column >= n has none)
+    pb_write_out<kPb1Threads, uint8_t>(buf, sbin, dd, nrec, out);
     __syncthreads();
   }
 }
@@ -438,7 +485,7 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
       sbin[slot] = (uint16_t)b;
     }
   __syncthreads();
-  pb_write_out<uint16_t>(buf, sbin, dd, cnt, pb.rec2);
+  pb_write_out<kPbThreads, uint16_t>(buf, sbin, dd, cnt, pb.rec2);
 }
 
 // ---------------------------------------------------------------------------

@@ -4,6 +4,7 @@ profiles/.
     python -m paper_2607_02603_amd.profsum trace DB CALLS TITLE COMMAND > out.md
     python -m paper_2607_02603_amd.profsum traffic FETCH_DB WRITE_DB KERNELS... > out.json
     python -m paper_2607_02603_amd.profsum counters KERNELS -- DB... > out.md
+    python -m paper_2607_02603_amd.profsum calltraffic FETCH_DB WRITE_DB TRACE_DB CALLS > out.json
 
 'trace' tabulates the library's kernels of a --kernel-trace run (per-call
 figures are totals divided by CALLS, the number of library calls the traced
@@ -16,7 +17,11 @@ file of those kernels so that a stale figure is not reported.  'counters'
 tabulates, per kernel of the last library call (names matched by prefix,
 comma-separated), every counter of one or more --pmc databases (one per
 counter pass), summed over the kernel's dispatches and hardware instances,
-with the ratios that name a kernel's bound.
+with the ratios that name a kernel's bound.  'calltraffic' gives the HBM
+bytes of every library kernel of one call (the last call of the two --pmc
+runs, calibrated like 'traffic') and the call's summed kernel time (from a
+--kernel-trace run making CALLS library calls), with the SHA-256 of all the
+library's kernel sources.
 """
 import hashlib
 import json
@@ -32,6 +37,18 @@ PB_SOURCE = os.path.join(_HERE, "csrc", "wl_push.h")
 def source_hash(path=PB_SOURCE):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()
+
+
+def sources_hash():
+    """SHA-256 over the library's sources (csrc/, sorted by name)."""
+    h = hashlib.sha256()
+    d = os.path.join(_HERE, "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".h", ".hip")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
 
 
 def _short(name):
@@ -210,12 +227,28 @@ def counters_markdown(kernels, dbs, cu_num=256):
         lambda r: 100 * r["TCC_EA0_RDREQ_32B"] / r["TCC_EA0_RDREQ"])
     return "\n".join(out)
 
+
+def call_traffic(fetch_db, write_db, trace_db, calls):
+    t = traffic(fetch_db, write_db, [])
+    _, kernel_ms = trace_table(trace_db, calls)
+    b = t["call"]["bytes"]
+    return {"what": "HBM bytes (FETCH_SIZE + WRITE_SIZE, calibrated on a 1 GiB copy) of every "
+                    "library kernel of one stable colouring, and the summed duration of those "
+                    "kernels",
+            "sources_sha256": sources_hash(), "bytes": b, "kernel_ms": kernel_ms,
+            "tb_per_s": b / (kernel_ms / 1e3) / 1e12,
+            "frac_of_8tbs": b / (kernel_ms / 1e3) / 8e12,
+            "fetch_scale": t["fetch"]["scale"], "write_scale": t["write"]["scale"],
+            "top_kernels_bytes": t["call"]["top_kernels_bytes"]}
+
 def main(argv):
     if len(argv) >= 5 and argv[0] == "trace":
         print(trace_markdown(argv[1], int(argv[2]), argv[3], argv[4]))
     elif len(argv) >= 4 and argv[0] == "counters" and "--" in argv:
         cut = argv.index("--")
         print(counters_markdown(argv[1].split(","), argv[cut + 1:]))
+    elif len(argv) == 5 and argv[0] == "calltraffic":
+        print(json.dumps(call_traffic(argv[1], argv[2], argv[3], int(argv[4])), indent=1))
     elif len(argv) >= 4 and argv[0] == "traffic":
         print(json.dumps(traffic(argv[1], argv[2], argv[3:]), indent=1))
     else:

@@ -3,6 +3,7 @@
     python tests/golden/make_full_size.py chunglu rmat27
     python tests/golden/make_full_size.py --ring64 rmat27
     python tests/golden/make_full_size.py --exact chunglu rmat27
+    python tests/golden/make_full_size.py rmat28
 
 For each workload: the seeded graph from the shared input generators (built on
 the GPU, which produces byte-identical CSRs to the CPU build of the same
@@ -17,6 +18,11 @@ With --exact the coarsest stable colouring is computed instead by oracle (b'),
 the splitter-based refinement (no rounds, no random weights), and
 full_<name>_exact.json stores its colour count and the SHA-256 of its
 first-occurrence ids (node 0 has colour 0, each new colour the next id).
+The R-MAT scale 28 graph (edge factor 32, 1.68e10 entries) is built into
+page-locked host memory by the shared generators, and each oracle round runs
+as its two steps (image, then relabel) with a progress line after each; its
+file stores no CSR checksum (a pass over 67 GB of column indices in numpy
+would take minutes), only n, nnz and the oracle's results.
 Nothing here calls the HIP library.
 """
 import hashlib
@@ -37,6 +43,7 @@ from paper_2607_02603_amd import inputs  # noqa: E402
 WORKLOADS = {
     "chunglu": "Chung-Lu n=4e6, 64e6 sampled pairs, exponent 2.1, seed 0",
     "rmat27": "R-MAT scale 27, edge factor 16, (0.57,0.19,0.19,0.05), symmetrised+dedup, seed 0",
+    "rmat28": "R-MAT scale 28, edge factor 32, (0.57,0.19,0.19,0.05), symmetrised+dedup, seed 0",
 }
 
 
@@ -47,6 +54,12 @@ def say(msg):
 def build(name):
     import torch
     dev = torch.device("cuda:0")
+    if name == "rmat28":
+        # page-locked host arrays, viewed without a copy
+        g = inputs.rmat(28, 32, device=dev, host_out=True)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        return g.row_ptr.numpy().view(np.uint64), g.col.numpy().view(np.uint32)
     g = inputs.chung_lu(device=dev) if name == "chunglu" else inputs.rmat(27, 16, device=dev)
     torch.cuda.synchronize()
     rp = g.row_ptr.cpu().numpy().view(np.uint64)
@@ -79,7 +92,14 @@ def run(name, q=0):
     r = 0
     while True:
         t0 = time.time()
-        c2, k2, _ = oracle.refine_round(rp, col, None, c, k, 0, r, q)
+        if name == "rmat28":
+            # the round's two steps, each followed by a progress line
+            z = oracle.image(rp, col, None, c, k, 0, r, q)
+            say(f"{name}: round {r}: image done ({time.time() - t0:.1f} s)")
+            c2, k2 = oracle.relabel(c, z)
+            del z
+        else:
+            c2, k2, _ = oracle.refine_round(rp, col, None, c, k, 0, r, q)
         r += 1
         hist.append(k2)
         say(f"{name}: round {r - 1}: {k} -> {k2} colours ({time.time() - t0:.1f} s)")
@@ -91,7 +111,8 @@ def run(name, q=0):
     sample = np.sort(rng.choice(n, size=min(n, 4096), replace=False)).astype(np.int64)
     out = {
         "workload": WORKLOADS[name], "seed": 0, "n": int(n), "nnz": int(col.size),
-        "csr_checksum": csr_checksum(rp, col), "k_per_round": hist, "rounds": r,
+        "csr_checksum": None if name == "rmat28" else csr_checksum(rp, col),
+        "k_per_round": hist, "rounds": r,
         "colours": int(k), "sha256": hashlib.sha256(c.astype("<u4").tobytes()).hexdigest(),
         "sample_nodes": sample.tolist(), "sample_colours": c[sample].astype(int).tolist(),
         "written_by": "tests/golden/make_full_size.py (oracle/ only)",

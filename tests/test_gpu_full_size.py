@@ -88,3 +88,49 @@ def test_full_size_ring64_bit_exact():
     assert np.array_equal(host[idx], np.asarray(gold["sample_colours"], np.uint32))
     assert hashlib.sha256(host.astype("<u4").tobytes()).hexdigest() == gold["sha256"]
     assert wl.wl_verify_stable(g, colors, k, ws=ws)
+
+
+def _rmat28_host():
+    # R-MAT scale 28, edge factor 32 (1.68e10 entries): generated on the
+    # device in bucket groups, held in page-locked host memory
+    dev = torch.device("cuda:0")
+    g = inputs.rmat(28, 32, device=dev, host_out=True)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return g, wl.Graph(g.n, g.row_ptr, g.col)
+
+
+def test_rmat28_out_of_core_bit_exact():
+    """The out-of-core configuration (R-MAT scale 28, edge factor 32, CSR in
+    host memory, a 32 GiB device workspace): Algorithm 1 with the image
+    streamed from host memory equals the oracle's Algorithm 1 on the same
+    graph (tests/golden/full_rmat28.json) in raw colour ids, colour count
+    and rounds.  Then Algorithm 2 under the same budget (five batches; the
+    contraction reaches its fixed point with several batches, termination
+    case (ii)) gives a stable colouring that refines the oracle's."""
+    gold = _golden("rmat28")
+    print("rmat28: generating", flush=True)
+    g, hg = _rmat28_host()
+    assert (g.n, g.nnz) == (gold["n"], gold["nnz"])
+    ws = wl.workspace(32 << 30)
+    colors, k, rounds = wl.wl_stable_coloring_streamed(hg, None, 0, ws=ws)
+    print(f"rmat28 streamed: colours={k} rounds={rounds}", flush=True)
+    assert (k, rounds) == (gold["colours"], gold["rounds"])
+    host = colors.numpy().view(np.uint32)
+    idx = np.asarray(gold["sample_nodes"], np.int64)
+    assert np.array_equal(host[idx], np.asarray(gold["sample_colours"], np.uint32))
+    assert hashlib.sha256(host.astype("<u4").tobytes()).hexdigest() == gold["sha256"]
+    # Algorithm 2 under the 32 GiB budget, to its fixed point
+    bc, kb, rb, outer, coarsest = wl.wl_stable_coloring_batched(hg, None, 0, 0, ws=ws)
+    print(f"rmat28 batched: colours={kb} rounds={rb} outer={outer} coarsest={coarsest}",
+          flush=True)
+    assert kb >= k and outer >= 2 and not coarsest
+    # every batched class lies inside one class of the oracle's colouring
+    dev = torch.device("cuda:0")
+    b = bc.to(dev).long()
+    o = colors.to(dev).long()
+    lo = torch.full((kb,), k, dtype=torch.int64, device=dev)
+    hi = torch.full((kb,), -1, dtype=torch.int64, device=dev)
+    lo.scatter_reduce_(0, b, o, reduce="amin")
+    hi.scatter_reduce_(0, b, o, reduce="amax")
+    assert bool(torch.equal(lo, hi))
