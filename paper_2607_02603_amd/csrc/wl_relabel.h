@@ -156,6 +156,15 @@ __device__ __forceinline__ TileRange tile_range(const Ctx& ctx, int cur,
   return r;
 }
 
+// Order in which the workgroups of a radix pass take the tiles: the i-th
+// tile taken is (i * (2^31 - 1)) mod nt, a bijection of [0, nt) (2^31 - 1 is
+// prime and nt < 2^31).  Workgroups running at one time then hold tiles of
+// many segments instead of consecutive tiles of one, so fewer of them
+// reserve slots on the same bucket cursors at once.
+__device__ __forceinline__ uint32_t tile_order(uint32_t i, uint32_t nt) {
+  return (uint32_t)(((uint64_t)i * 2147483647ull) % nt);
+}
+
 // First pass only: keys of the big segments in position order.
 __global__ void __launch_bounds__(kBlock) k_big_gather(Ctx ctx) {
   DevState* st = ctx.st;
@@ -193,8 +202,8 @@ __global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
   if (nb == 0) return;
   __shared__ uint32_t cnt[kRadix];
   __shared__ unsigned long long mn[kRadix], mx[kRadix];
-  for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
-    TileRange r = tile_range(ctx, cur, nb, t);
+  for (uint32_t i = blockIdx.x; i < nt; i += gridDim.x) {
+    TileRange r = tile_range(ctx, cur, nb, tile_order(i, nt));
     cnt[threadIdx.x] = 0;
     mn[threadIdx.x] = ~0ull;
     mx[threadIdx.x] = 0;
@@ -291,7 +300,10 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
 }
 
 // Scatter every element of the big segments into its bucket (keys_tmp,
-// perm_tmp).  Slots inside a bucket are taken with atomics.
+// perm_tmp).  A tile's elements are ranked inside their buckets with LDS
+// atomics, each bucket's run is reserved with one atomic on its cursor, and
+// the elements are staged in LDS in bucket order and written out one per
+// lane, consecutive over the lanes, so a wave's stores cover whole runs.
 __global__ void __launch_bounds__(kBlock) k_big_scatter(Ctx ctx, int pass) {
   DevState* st = ctx.st;
   if (st->done) return;
@@ -299,34 +311,55 @@ __global__ void __launch_bounds__(kBlock) k_big_scatter(Ctx ctx, int pass) {
   const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
   if (nb == 0) return;
   __shared__ uint32_t lcnt[kRadix];
-  __shared__ uint32_t lbase[kRadix];
-  for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
-    TileRange r = tile_range(ctx, cur, nb, t);
+  __shared__ uint32_t dbase[kRadix];  // output position of staged slot 0 of the bucket
+  __shared__ unsigned long long skey[kTile];
+  __shared__ uint32_t sval[kTile];
+  __shared__ uint8_t sdig[kTile];
+  __shared__ uint32_t sh[kBlock / kWave];
+  static_assert(kRadix == kBlock, "one thread per bucket");
+  for (uint32_t i = blockIdx.x; i < nt; i += gridDim.x) {
+    TileRange r = tile_range(ctx, cur, nb, tile_order(i, nt));
     if (ctx.bsame[r.seg]) continue;  // uniform across the block
     lcnt[threadIdx.x] = 0;
     __syncthreads();
     uint32_t slot[kTilePerThread];
     uint32_t dg[kTilePerThread];
+    unsigned long long kv[kTilePerThread];
 #pragma unroll
     for (uint32_t q = 0; q < kTilePerThread; ++q) {
       const uint32_t p = r.beg + q * kBlock + threadIdx.x;
       if (p < r.end) {
-        dg[q] = digit_of(ctx.keys[p], pass, ctx.ring);
+        kv[q] = ctx.keys[p];
+        dg[q] = digit_of(kv[q], pass, ctx.ring);
         slot[q] = atomicAdd(&lcnt[dg[q]], 1u);
       }
     }
     __syncthreads();
     const uint32_t b = threadIdx.x;
-    if (lcnt[b]) lbase[b] = atomicAdd(&ctx.bcur[r.seg * kRadix + b], lcnt[b]);
+    const uint32_t h = lcnt[b];
+    uint32_t tot;
+    const uint32_t lofs = block_excl_scan(h, sh, &tot);
+    const uint32_t gb = h ? atomicAdd(&ctx.bcur[r.seg * kRadix + b], h) : 0u;
+    // u32 arithmetic: the difference may wrap, the sum with a slot does not
+    dbase[b] = r.seg_start + gb - lofs;
+    lcnt[b] = lofs;
     __syncthreads();
 #pragma unroll
     for (uint32_t q = 0; q < kTilePerThread; ++q) {
       const uint32_t p = r.beg + q * kBlock + threadIdx.x;
       if (p < r.end) {
-        const uint32_t dst = r.seg_start + lbase[dg[q]] + slot[q];
-        ctx.keys_tmp[dst] = ctx.keys[p];
-        ctx.perm_tmp[dst] = ctx.perm[p];
+        const uint32_t at = lcnt[dg[q]] + slot[q];
+        skey[at] = kv[q];
+        sval[at] = ctx.perm[p];
+        sdig[at] = (uint8_t)dg[q];
       }
+    }
+    __syncthreads();
+    const uint32_t cnt = r.end - r.beg;
+    for (uint32_t t = threadIdx.x; t < cnt; t += kBlock) {
+      const uint32_t dst = dbase[sdig[t]] + t;
+      ctx.keys_tmp[dst] = skey[t];
+      ctx.perm_tmp[dst] = sval[t];
     }
     __syncthreads();
   }

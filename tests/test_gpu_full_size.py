@@ -92,9 +92,14 @@ def test_full_size_ring64_bit_exact():
 
 def _rmat28_host():
     # R-MAT scale 28, edge factor 32 (1.68e10 entries): generated on the
-    # device in bucket groups, held in page-locked host memory
+    # device in bucket groups, held in pageable host memory (after the other
+    # full-size tests, 67 GB of page-locked memory are not always granted;
+    # the library copies pageable memory through its staging buffers)
+    import gc
+    gc.collect()
+    torch.cuda.empty_cache()
     dev = torch.device("cuda:0")
-    g = inputs.rmat(28, 32, device=dev, host_out=True)
+    g = inputs.rmat(28, 32, device=dev, host_out=True, pinned=False)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return g, wl.Graph(g.n, g.row_ptr, g.col)
