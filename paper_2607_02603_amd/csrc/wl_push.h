@@ -242,14 +242,15 @@ __device__ __forceinline__ void pb_reserve(const Ctx& ctx, uint32_t* hist, long 
 // Each tile of kPbTile entries, in the order that lets the latencies overlap:
 //   1. the column indices (registers) and the first row-start data are
 //      loaded together;
-//   2. row starts are marked in LDS (colour + 1 at the row's first entry in
-//      the tile) while every entry's bin is counted (non-returning LDS adds);
+//   2. the first entry of every non-empty row starting in the tile is set
+//      in a bit mask (one bit per entry, 1 KB) while every entry's bin is
+//      counted (non-returning LDS adds);
 //   3. a block scan gives each bin's run offset in the tile and one cursor
-//      reservation per bin is issued; while it is in flight, the colour of
-//      every entry's row is found from the marks (block-wide "last mark at
-//      or before" scan in entry order: one ballot and one lane permute per
-//      4 x 64 entries, the marks read twice from LDS instead of being held in
-//      registers) and the record is formed;
+//      reservation per bin is issued; while it is in flight, one wave turns
+//      the mask into per-word prefix counts, every row start stores its
+//      colour at its rank among the tile's row starts, and every entry finds
+//      its row's colour from the number of row starts at or before it (the
+//      row holding the tile's first entry has rank 0);
 //   4. the reservations give each run's output offset (dd), the records are
 //      staged by bin (one returning LDS add per record picks its slot) and
 //      written out (pb_write_out).
@@ -261,15 +262,16 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
   if (ctx.st->done) return;
   constexpr uint32_t kRun = kPbTile / kPb1Threads;  // entries per thread
   constexpr uint32_t kGroups = kRun / 4;           // loads of 4 entries per thread
-  constexpr int kWaves = kPb1Threads / kWave;
-  __shared__ __align__(16) uint32_t buf[kPbTile];  // row marks, then staged records
+  constexpr uint32_t kWords = kPbTile / 32;         // words of the row-start mask
+  static_assert(kWords <= kPb1Threads && kWords % kWave == 0, "mask words per thread");
+  __shared__ __align__(16) uint32_t buf[kPbTile];  // row colours by rank, then staged records
   __shared__ __align__(16) uint8_t sbin[kPbTile];  // bin of each staged record
+  __shared__ uint32_t bits[kWords];                // row starts of the tile
+  __shared__ uint32_t wpre[kWords];                // row starts before each word
   __shared__ uint32_t hist[kPbMaxBins];
   __shared__ long long dd[kPbMaxBins];
-  __shared__ uint32_t wtot[kGroups][kWaves];
-  __shared__ uint32_t sh[kWaves];
-  const int lane = lane_id(), wid = threadIdx.x / kWave;
-  const unsigned long long lt_mask = (1ull << lane) - 1;
+  __shared__ uint32_t sh[kPb1Threads / kWave];
+  const int lane = lane_id();
   const uint32_t mask1 = (1u << pb.shift1) - 1;
   const bool two = pb.levels == 2;
   uint32_t* out = two ? pb.rec1 : pb.rec2;
@@ -301,30 +303,27 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
           cix[4 * k + u] = q < cnt ? ctx.col[e0 + q] : 0u;
         }
     }
-    // the first row starting in the tile for this thread
-    uint32_t r = j0 + 1 + threadIdx.x;
+    // the first row starting in the tile for this thread (rows j0 + 1 ..
+    // jend start after e0; the row holding e0 is j0)
+    const uint32_t r0 = j0 + 1 + threadIdx.x;
     uint64_t rb = 0, re = 0;
     uint32_t rc = 0;
-    if (r <= jend) {
-      rb = rp_at<RP>(ctx, r);
-      re = rp_at<RP>(ctx, r + 1);
-      rc = ctx.c[r];
+    if (r0 <= jend) {
+      rb = rp_at<RP>(ctx, r0);
+      re = rp_at<RP>(ctx, r0 + 1);
+      rc = ctx.c[r0];
     }
     const uint32_t c_first = ctx.c[j0];
-    const uint4 z4 = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (uint32_t k = 0; k < kGroups; ++k) ((uint4*)buf)[k * kPb1Threads + threadIdx.x] = z4;
+    if (threadIdx.x < kWords) bits[threadIdx.x] = 0;
     if (threadIdx.x < kPbMaxBins) hist[threadIdx.x] = 0;
     __syncthreads();
-    // 2. row-start marks; bins counted
-    for (; r <= jend; r += kPb1Threads) {
-      if (rb < e1 && re > rb) buf[rb - e0] = rc + 1;
-      const uint32_t rn = r + kPb1Threads;
-      if (rn <= jend) {
-        rb = rp_at<RP>(ctx, rn);
-        re = rp_at<RP>(ctx, rn + 1);
-        rc = ctx.c[rn];
-      }
+    // 2. row starts into the mask; bins counted
+    const bool first_starts = r0 <= jend && rb < e1 && re > rb;
+    if (first_starts) atomicOr(&bits[(rb - e0) >> 5], 1u << ((rb - e0) & 31));
+    for (uint32_t r = r0 + kPb1Threads; r <= jend; r += kPb1Threads) {
+      const uint64_t b = rp_at<RP>(ctx, r);
+      if (b < e1 && rp_at<RP>(ctx, r + 1) > b)
+        atomicOr(&bits[(b - e0) >> 5], 1u << ((b - e0) & 31));
     }
     // the 4 bins of group k, one byte each (every byte value is a bin), and
     // bit 4k + u set when entry (k, u) has a record
@@ -357,39 +356,47 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
     const uint32_t ex = pb_block_scan<kPb1Threads>(h, sh, &nrec);
     unsigned long long d = 0;
     if (h) d = atomicAdd(&cur[threadIdx.x], (unsigned long long)h);
-    //    while it is in flight: the colour of every entry's row
-    uint32_t exk[kGroups];
+    //    while it is in flight: row starts before each mask word (wave 0)
+    if (threadIdx.x < kWave) {
+      constexpr uint32_t kPer = kWords / kWave;
+      uint32_t pc[kPer];
+      uint32_t s = 0;
 #pragma unroll
-    for (uint32_t k = 0; k < kGroups; ++k) {
-      const uint4 mk = ((const uint4*)buf)[k * kPb1Threads + threadIdx.x];
-      const uint32_t g = mk.w ? mk.w : (mk.z ? mk.z : (mk.y ? mk.y : mk.x));
-      const unsigned long long m = __ballot(g != 0);
-      const unsigned long long below = m & lt_mask;
-      const uint32_t v = __shfl(g, below ? 63 - __builtin_clzll(below) : lane, kWave);
-      exk[k] = below ? v : 0u;
-      const uint32_t tot = __shfl(g, m ? 63 - __builtin_clzll(m) : 0, kWave);
-      if (lane == 0) wtot[k][wid] = m ? tot : 0u;
+      for (uint32_t u = 0; u < kPer; ++u) {
+        pc[u] = __popc(bits[lane * kPer + u]);
+        s += pc[u];
+      }
+      uint32_t run = wave_incl_scan(s) - s;
+#pragma unroll
+      for (uint32_t u = 0; u < kPer; ++u) {
+        wpre[lane * kPer + u] = run;
+        run += pc[u];
+      }
     }
     __syncthreads();
-    uint32_t running = c_first + 1;  // last mark of every group before (k, wave)
+    //    the colour of every row start at its rank
+    auto rank_below = [&](uint32_t pos) {  // row starts at positions < pos
+      return wpre[pos >> 5] + __popc(bits[pos >> 5] & ((1u << (pos & 31)) - 1u));
+    };
+    if (first_starts) buf[rank_below((uint32_t)(rb - e0))] = rc;
+    for (uint32_t r = r0 + kPb1Threads; r <= jend; r += kPb1Threads) {
+      const uint64_t b = rp_at<RP>(ctx, r);
+      if (b < e1 && rp_at<RP>(ctx, r + 1) > b) buf[rank_below((uint32_t)(b - e0))] = ctx.c[r];
+    }
+    __syncthreads();
+    //    every entry's row colour, and the record
 #pragma unroll
     for (uint32_t k = 0; k < kGroups; ++k) {
-      uint32_t before = running;
-      for (int w = 0; w < kWaves; ++w) {
-        const uint32_t x = wtot[k][w];
-        if (x) {
-          if (w < wid) before = x;
-          running = x;
-        }
-      }
-      const uint4 mk = ((const uint4*)buf)[k * kPb1Threads + threadIdx.x];
-      const uint32_t mv[4] = {mk.x, mk.y, mk.z, mk.w};
-      uint32_t c = exk[k] ? exk[k] : before;
+      const uint32_t q0 = 4 * (k * kPb1Threads + threadIdx.x);  // a multiple of 4
+      const uint32_t wbits = bits[q0 >> 5], wbase = wpre[q0 >> 5];
 #pragma unroll
       for (uint32_t u = 0; u < 4; ++u) {
-        if (mv[u]) c = mv[u];
+        const uint32_t q = q0 + u;
+        // row starts at positions <= q
+        const uint32_t rk = wbase + __popc(wbits & ((2u << (q & 31)) - 1u));
+        const uint32_t c = rk ? buf[rk - 1] : c_first;
         const uint32_t i = cix[4 * k + u];
-        cix[4 * k + u] = ((i & mask1) << pb.cbits) | (c - 1);  // the record
+        cix[4 * k + u] = ((i & mask1) << pb.cbits) | c;  // the record
       }
     }
     // 4. output offsets of the runs (a bin without records in this tile
@@ -404,7 +411,7 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
         dd[threadIdx.x] = (long long)d - (long long)ex;
       }
     }
-    __syncthreads();  // the marks in buf are consumed; dd is complete
+    __syncthreads();  // the row colours in buf are consumed; dd is complete
     if (threadIdx.x < kPbMaxBins) hist[threadIdx.x] = ex;
     __syncthreads();
 #pragma unroll
