@@ -751,24 +751,16 @@ struct Session {
     return WL_OK;
   }
 
-  // The sorting networks, with the tie-aware key order in Z/2^64.
-  void tiny_sort(uint32_t grid, int check_passes) {
+  // The sorting networks (one launch: gt workgroups for the tiny segments,
+  // gp for the pico ones, gs for the small ones), with the tie-aware key
+  // order in Z/2^64.
+  void sorts(uint32_t gt, uint32_t gp, uint32_t gs, int check_passes) {
+    const uint32_t g = gt + gp + gs;
+    if (g == 0) return;
     if (ctx.ring)
-      hipLaunchKernelGGL(k_tiny_sort<true>, dim3(grid), dim3(kBlock), 0, s, ctx, check_passes);
+      hipLaunchKernelGGL(k_sorts<true>, dim3(g), dim3(kBlock), 0, s, ctx, check_passes, gt, gp);
     else
-      hipLaunchKernelGGL(k_tiny_sort<false>, dim3(grid), dim3(kBlock), 0, s, ctx, check_passes);
-  }
-  void pico_sort(uint32_t grid) {
-    if (ctx.ring)
-      hipLaunchKernelGGL(k_pico_sort<true>, dim3(grid), dim3(kBlock), 0, s, ctx);
-    else
-      hipLaunchKernelGGL(k_pico_sort<false>, dim3(grid), dim3(kBlock), 0, s, ctx);
-  }
-  void small_sort(uint32_t grid) {
-    if (ctx.ring)
-      hipLaunchKernelGGL(k_small_sort<true>, dim3(grid), dim3(kBlock), 0, s, ctx);
-    else
-      hipLaunchKernelGGL(k_small_sort<false>, dim3(grid), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_sorts<false>, dim3(g), dim3(kBlock), 0, s, ctx, check_passes, gt, gp);
   }
 
   // SpMV schedule (row bins and heavy chunks); once per call.
@@ -985,8 +977,10 @@ struct Session {
         hipLaunchKernelGGL(k_heavy_clear, dim3(gh), dim3(kBlock), 0, s, ctx);
         hipLaunchKernelGGL(k_heavy_set, dim3(gh), dim3(kBlock), 0, s, ctx);
       }
-      hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
-                         live_heavy);
+      // rows of at most kShortRow entries are done by k_spmv_q alone
+      if (live_heavy || host.max_deg > kShortRow)
+        hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
+                           live_heavy);
     });
     if (live_heavy)
       hipLaunchKernelGGL(k_live_heavy_fix, dim3(grid_for(host.bin_cnt[3], kBlock, 1024)),
@@ -1041,9 +1035,9 @@ struct Session {
       if (int r = pull()) return r;
     }
     passes_seen = std::max(passes_seen, pass);
-    if (host.n_tiny) tiny_sort(grid_for(host.n_tiny, kBlock / kWave, 8192), -1);
-    if (host.n_pico) pico_sort(grid_for(host.n_pico, kBlock / 8, 8192));
-    if (host.n_small) small_sort(std::min<uint32_t>(host.n_small, 4096));
+    sorts(host.n_tiny ? grid_for(host.n_tiny, kBlock / kWave, 8192) : 0,
+          host.n_pico ? grid_for(host.n_pico, kBlock / 8, 8192) : 0,
+          host.n_small ? std::min<uint32_t>(host.n_small, 4096) : 0, -1);
     if (full) rank_scan();
     HIP_LAUNCH_CHECK();
     return WL_OK;
@@ -1285,9 +1279,8 @@ struct Session {
     for (int pass = 0; pass < ap; ++pass) radix_pass(pass, 1024);
     // the small sorts' grids: enough blocks to fill the device, the segments
     // taken in grid-stride loops
-    tiny_sort(grid_for(L.n / 2, kBlock / kWave, 1024), ap);
-    pico_sort(grid_for(L.n / 2, kBlock / 8, 1024));
-    small_sort(grid_for(L.n / (kTinyMax + 1), 1, 1024));
+    sorts(grid_for(L.n / 2, kBlock / kWave, 1024), grid_for(L.n / 2, kBlock / 8, 1024),
+          grid_for(L.n / (kTinyMax + 1), 1, 1024), ap);
     live_tail(true);
   }
 

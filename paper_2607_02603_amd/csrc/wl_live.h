@@ -429,15 +429,22 @@ __global__ void __launch_bounds__(kBlock) k_shift_scatter(Ctx ctx) {
 // New colour of every node: b + shift(b).  Members of the classes that
 // split are rewritten by k_live_emit afterwards.  Four nodes per thread and
 // step (16-byte accesses when the colour array allows).
+// With the split list in LDS, shift(b) = cumulative extras of the last split
+// colour below b.  With more than kShiftDirect splits the colours [0, k) are
+// cut into kShiftBuckets ranges of 2^bsh colours, and bidx[t] = first split
+// whose colour is in range t or above, so the search for b only visits the
+// splits of b's own range; with fewer, the search spans all of them.
+constexpr uint32_t kShiftBuckets = 1024;
+constexpr uint32_t kShiftDirect = 256;
+
+// The last split colour < b is at an index in [l, h], and scol[l] < b.
 __device__ __forceinline__ uint32_t shift_lds(const uint32_t* scol, const uint32_t* scum,
-                                              uint32_t S, uint32_t b) {
-  // b > scol[0]: last split colour < b
-  uint32_t lo = 0, hi = S - 1;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi + 1) >> 1;
-    if (scol[mid] < b) lo = mid; else hi = mid - 1;
+                                              uint32_t l, uint32_t h, uint32_t b) {
+  while (l < h) {
+    const uint32_t mid = (l + h + 1) >> 1;
+    if (scol[mid] < b) l = mid; else h = mid - 1;
   }
-  return scum[lo];
+  return scum[l];
 }
 
 __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
@@ -448,6 +455,11 @@ __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
   const bool big = st->shift_big != 0;
   __shared__ uint32_t scol[kShiftLds];
   __shared__ uint32_t scum[kShiftLds];
+  __shared__ uint32_t bidx[kShiftBuckets + 1];
+  // every colour is below k: (k - 1) >> bsh < kShiftBuckets
+  uint32_t bsh = 0;
+  while (((st->k - 1) >> bsh) >= kShiftBuckets) ++bsh;
+  const bool direct = S <= kShiftDirect;
   if (!big) {
     for (uint32_t t = threadIdx.x; t < S; t += kBlock) {
       const uint2 e = ctx.split[t];
@@ -455,11 +467,30 @@ __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
       scum[t] = e.y;
     }
     __syncthreads();
+    for (uint32_t t = threadIdx.x; !direct && t <= kShiftBuckets; t += kBlock) {
+      const uint64_t v = (uint64_t)t << bsh;
+      uint32_t lo = 0, hi = S;
+      while (lo < hi) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (scol[mid] < v) lo = mid + 1; else hi = mid;
+      }
+      bidx[t] = lo;
+    }
+    __syncthreads();
   }
   const uint32_t first = big ? 0u : scol[0];
   auto moved = [&](uint32_t b) -> uint32_t {
     if (big) return b + ctx.shift[b];
-    return b <= first ? b : b + shift_lds(scol, scum, S, b);
+    if (b <= first) return b;
+    // b > scol[0]: the last split colour below b
+    uint32_t l = 0, h = S - 1;
+    if (!direct) {
+      const uint32_t t = min(b >> bsh, kShiftBuckets - 1);
+      const uint32_t lo = bidx[t], hi = bidx[t + 1];
+      l = lo > 0 ? lo - 1 : 0;  // scol[lo - 1] < t << bsh <= b
+      h = max(hi, l + 1) - 1;   // scol[hi] >= (t + 1) << bsh > b
+    }
+    return b + shift_lds(scol, scum, l, h, b);
   };
   const uint32_t tid = blockIdx.x * kBlock + threadIdx.x, stride = gridDim.x * kBlock;
   uint32_t done4 = 0;

@@ -395,14 +395,13 @@ __device__ __forceinline__ bool key_less(unsigned long long a, uint32_t va,
 // One workgroup per small segment: bitonic sort of (z, node) in LDS, then
 // flags where z changes.
 template <bool TIE>
-__global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
+__device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, uint32_t nblk) {
   DevState* st = ctx.st;
-  if (st->done) return;
   const uint32_t ns = st->n_small;
   __shared__ unsigned long long skey[kSmallMax];
   __shared__ uint32_t sval[kSmallMax];
   __shared__ int differ, unsorted;
-  for (uint32_t si = blockIdx.x; si < ns; si += gridDim.x) {
+  for (uint32_t si = bid; si < ns; si += nblk) {
     const uint2 sg = ctx.small_list[si];
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
     const bool mat = (sg.y & kMatBit) != 0;
@@ -470,20 +469,20 @@ __global__ void __launch_bounds__(kBlock) k_small_sort(Ctx ctx) {
 // the lanes with shuffles, flags where z changes.  Skipped when all images of
 // the segment are equal.
 // check_passes >= 0: first halt the device (done = kHalted) if big segments
-// are left after that many radix passes; the blocks that still run sort
-// their segments, which the host-driven completion sorts again (a sort of
-// sorted keys changes nothing).
+// are left after that many radix passes; the workgroups of the launch that
+// still run (of all three sorts) sort their segments, which the host-driven
+// completion sorts again (the keys stay in order; only members with equal
+// keys may change places, and their order is irrelevant).
 template <bool TIE>
-__global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes) {
+__device__ __forceinline__ void tiny_sort_body(const Ctx& ctx, int check_passes, uint32_t bid,
+                                               uint32_t nblk) {
   DevState* st = ctx.st;
-  if (st->done) return;
-  if (check_passes >= 0 && blockIdx.x == 0 && threadIdx.x == 0 &&
-      st->n_big[check_passes & 1] > 0)
+  if (check_passes >= 0 && bid == 0 && threadIdx.x == 0 && st->n_big[check_passes & 1] > 0)
     st->done = kHalted;
   const uint32_t nt = st->n_tiny;
   const uint32_t lane = lane_id();
-  const uint32_t nwaves = gridDim.x * (kBlock / kWave);
-  for (uint32_t si = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave; si < nt;
+  const uint32_t nwaves = nblk * (kBlock / kWave);
+  for (uint32_t si = bid * (kBlock / kWave) + threadIdx.x / kWave; si < nt;
        si += nwaves) {
     const uint2 sg = ctx.tiny_list[si];
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
@@ -525,14 +524,13 @@ __global__ void __launch_bounds__(kBlock) k_tiny_sort(Ctx ctx, int check_passes)
 // list: eight per wave, eight lanes each, with the tiny sort's bitonic
 // network cut to eight elements.  Skipped when all keys of a segment agree.
 template <bool TIE>
-__global__ void __launch_bounds__(kBlock) k_pico_sort(Ctx ctx) {
+__device__ __forceinline__ void pico_sort_body(const Ctx& ctx, uint32_t bid, uint32_t nblk) {
   DevState* st = ctx.st;
-  if (st->done) return;
   const uint32_t np = st->n_pico;
   const uint32_t lane = lane_id(), sub = lane & 7u, g0 = lane & ~7u;
-  const uint32_t nwaves = gridDim.x * (kBlock / kWave);
+  const uint32_t nwaves = nblk * (kBlock / kWave);
   // loop bounds are the same for the whole wave (the shuffles need every lane)
-  for (uint32_t base = (blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave) * 8; base < np;
+  for (uint32_t base = (bid * (kBlock / kWave) + threadIdx.x / kWave) * 8; base < np;
        base += nwaves * 8) {
     const uint32_t si = base + (lane >> 3);
     uint32_t s = 0, len = 0;
@@ -575,6 +573,22 @@ __global__ void __launch_bounds__(kBlock) k_pico_sort(Ctx ctx) {
       if (sub > 0 && key != prev) ctx.flags[s + sub] = 1;
     }
   }
+}
+
+// The three sorts in one launch: workgroups [0, gt) take the tiny segments,
+// [gt, gt + gp) the pico ones and the rest the small ones (each kind in a
+// grid-stride loop over its own workgroups).
+template <bool TIE>
+__global__ void __launch_bounds__(kBlock) k_sorts(Ctx ctx, int check_passes, uint32_t gt,
+                                                  uint32_t gp) {
+  if (ctx.st->done) return;
+  const uint32_t b = blockIdx.x;
+  if (b < gt)
+    tiny_sort_body<TIE>(ctx, check_passes, b, gt);
+  else if (b < gt + gp)
+    pico_sort_body<TIE>(ctx, b - gt, gp);
+  else
+    small_sort_body<TIE>(ctx, b - gt - gp, gridDim.x - gt - gp);
 }
 
 // ---------------------------------------------------------------------------
