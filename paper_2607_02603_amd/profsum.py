@@ -5,6 +5,7 @@ profiles/.
     python -m paper_2607_02603_amd.profsum traffic FETCH_DB WRITE_DB KERNELS... > out.json
     python -m paper_2607_02603_amd.profsum counters KERNELS -- DB... > out.md
     python -m paper_2607_02603_amd.profsum calltraffic FETCH_DB WRITE_DB TRACE_DB CALLS > out.json
+    python -m paper_2607_02603_amd.profsum dispatches DB TITLE COMMAND > out.md
 
 'trace' tabulates the library's kernels of a --kernel-trace run (per-call
 figures are totals divided by CALLS, the number of library calls the traced
@@ -21,7 +22,9 @@ with the ratios that name a kernel's bound.  'calltraffic' gives the HBM
 bytes of every library kernel of one call (the last call of the two --pmc
 runs, calibrated like 'traffic') and the call's summed kernel time (from a
 --kernel-trace run making CALLS library calls), with the SHA-256 of all the
-library's kernel sources.
+library's kernel sources.  'dispatches' lists, for the last library call
+of a --kernel-trace run, every dispatch's duration per kernel in launch
+order.
 """
 import hashlib
 import json
@@ -241,6 +244,32 @@ def call_traffic(fetch_db, write_db, trace_db, calls):
             "fetch_scale": t["fetch"]["scale"], "write_scale": t["write"]["scale"],
             "top_kernels_bytes": t["call"]["top_kernels_bytes"]}
 
+def dispatches_markdown(db, title, command, top=20):
+    cur = sqlite3.connect(db).cursor()
+    cols = [r[1] for r in cur.execute("pragma table_info(kernels)")]
+    ki = cols.index("kernel_name") if "kernel_name" in cols else cols.index("name")
+    st, en = cols.index("start"), cols.index("end")
+    rows = [r for r in cur.execute("select * from kernels order by start").fetchall()
+            if _is_lib(r[ki])]
+    starts = [i for i, r in enumerate(rows) if "k_iota_zero" in r[ki]]
+    rows = rows[starts[-1]:] if starts else rows
+    per = {}
+    for r in rows:
+        per.setdefault(_short(r[ki]), []).append((r[en] - r[st]) / 1e6)
+    total = sum(sum(v) for v in per.values())
+    span = (rows[-1][en] - rows[0][st]) / 1e6 if rows else 0.0
+    out = [f"# {title}", "", "Command (repository root, on the MI355X machine):", "",
+           f"    {command}", "",
+           "The last library call of the trace; library kernels, ms per dispatch in launch "
+           f"order ({top} kernels of largest total).  Kernel time of the call: {total:.2f} ms; "
+           f"first start to last end: {span:.2f} ms.", "",
+           "| kernel | dispatches | ms per dispatch, in order | total ms |", "|---|---|---|---|"]
+    for name, v in sorted(per.items(), key=lambda kv: -sum(kv[1]))[:top]:
+        out.append(f"| {name} | {len(v)} | " + ", ".join(f"{x:.3f}" for x in v) +
+                   f" | {sum(v):.3f} |")
+    return "\n".join(out)
+
+
 def main(argv):
     if len(argv) >= 5 and argv[0] == "trace":
         print(trace_markdown(argv[1], int(argv[2]), argv[3], argv[4]))
@@ -249,6 +278,8 @@ def main(argv):
         print(counters_markdown(argv[1].split(","), argv[cut + 1:]))
     elif len(argv) == 5 and argv[0] == "calltraffic":
         print(json.dumps(call_traffic(argv[1], argv[2], argv[3], int(argv[4])), indent=1))
+    elif len(argv) == 4 and argv[0] == "dispatches":
+        print(dispatches_markdown(argv[1], argv[2], argv[3]))
     elif len(argv) >= 4 and argv[0] == "traffic":
         print(json.dumps(traffic(argv[1], argv[2], argv[3:]), indent=1))
     else:
