@@ -244,7 +244,8 @@ __device__ __forceinline__ void pb_reserve(const Ctx& ctx, uint32_t* hist, long 
 //      loaded together;
 //   2. the first entry of every non-empty row starting in the tile is set
 //      in a bit mask (one bit per entry, 1 KB) while every entry's bin is
-//      counted (non-returning LDS adds);
+//      counted (LDS adds whose returned old value is the entry's rank among
+//      the tile's entries of that bin);
 //   3. a block scan gives each bin's run offset in the tile and one cursor
 //      reservation per bin is issued; while it is in flight, one wave turns
 //      the mask into per-word prefix counts, every row start stores its
@@ -252,9 +253,9 @@ __device__ __forceinline__ void pb_reserve(const Ctx& ctx, uint32_t* hist, long 
 //      its row's colour from the number of row starts at or before it (the
 //      row holding the tile's first entry has rank 0);
 //   4. the reservations give each run's output offset (dd), the records are
-//      staged by bin (one returning LDS add per record picks its slot) and
+//      staged by bin at their run's offset in the tile plus their rank, and
 //      written out (pb_write_out).
-// The packed bins of a thread's entries take 4 registers; no rank is kept.
+// The packed bins of a thread's entries take 4 registers, their ranks 8.
 // 512 threads, 4 waves per SIMD: two workgroups per CU (at most 128 VGPRs).
 template <typename RP>
 __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx pb) {
@@ -329,6 +330,7 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
     // bit 4k + u set when entry (k, u) has a record
     static_assert(kRun <= 32 && kPbMaxBins <= 256, "bins packed in bytes, validity in 32 bits");
     uint32_t bins[kGroups];
+    uint32_t rk2[kRun / 2] = {};  // rank of each entry inside its bin in this tile, 16 bits
     uint32_t valid = 0;
 #pragma unroll
     for (uint32_t k = 0; k < kGroups; ++k) {
@@ -339,7 +341,7 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
         const uint32_t bn = cix[4 * k + u] >> pb.shift1;
         if (q < cnt) {
           if (bn < pb.nb1) {
-            atomicAdd(&hist[bn], 1u);
+            rk2[(4 * k + u) >> 1] |= atomicAdd(&hist[bn], 1u) << (16 * (u & 1));
             w |= bn << (8 * u);
             valid |= 1u << (4 * k + u);
           } else {  // a column >= n
@@ -420,7 +422,7 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
       for (uint32_t u = 0; u < 4; ++u)
         if (valid & (1u << (4 * k + u))) {
           const uint32_t bn = (bins[k] >> (8 * u)) & 0xFFu;
-          const uint32_t slot = atomicAdd(&hist[bn], 1u);
+          const uint32_t slot = hist[bn] + ((rk2[(4 * k + u) >> 1] >> (16 * (u & 1))) & 0xFFFFu);
           buf[slot] = cix[4 * k + u];
           sbin[slot] = (uint8_t)bn;
         }
