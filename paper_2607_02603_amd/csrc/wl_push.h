@@ -391,12 +391,13 @@ __global__ void __launch_bounds__(kPb1Threads, 4) k_pb_scatter1(Ctx ctx, PbCtx p
     for (uint32_t k = 0; k < kGroups; ++k) {
       const uint32_t q0 = 4 * (k * kPb1Threads + threadIdx.x);  // a multiple of 4
       const uint32_t wbits = bits[q0 >> 5], wbase = wpre[q0 >> 5];
+      // row starts at positions <= q0; the next three positions lie in the
+      // same mask word, and a set bit there starts the next row
+      uint32_t rk = wbase + __popc(wbits & ((2u << (q0 & 31)) - 1u));
+      uint32_t c = rk ? buf[rk - 1] : c_first;
 #pragma unroll
       for (uint32_t u = 0; u < 4; ++u) {
-        const uint32_t q = q0 + u;
-        // row starts at positions <= q
-        const uint32_t rk = wbase + __popc(wbits & ((2u << (q & 31)) - 1u));
-        const uint32_t c = rk ? buf[rk - 1] : c_first;
+        if (u > 0 && ((wbits >> ((q0 + u) & 31)) & 1u)) c = buf[rk++];
         const uint32_t i = cix[4 * k + u];
         cix[4 * k + u] = ((i & mask1) << pb.cbits) | c;  // the record
       }
