@@ -581,7 +581,8 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
         const uint64_t w =
             ok ? (TBL ? wtab[rv[u] & cmask] : color_weight(key, rv[u] & cmask, ctx.ring))
                : 0ull;
-        const uint32_t l0 = __shfl(local, 0, kWave);
+        // every lane is active here: lane 0's row, without an LDS permute
+        const uint32_t l0 = __builtin_amdgcn_readfirstlane(local);
         if (__all(!ok || local == l0)) {
           // the whole wave feeds one row (rows of high degree): add the 64
           // values exactly (low and high 32-bit halves) in registers first
