@@ -51,6 +51,13 @@ __device__ __forceinline__ uint32_t block_append(bool want, uint32_t* counter,
   return at;
 }
 
+// Lane l's value of v, for a lane index l that is the same in the whole
+// wave (a register read, not an LDS permute as a shuffle is).
+__device__ __forceinline__ uint64_t read_lane64(uint64_t v, int l) {
+  return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), l) << 32) |
+         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+}
+
 // Lanes of the wave that are active and hold the same key as this lane
 // (0 for an inactive lane); one pass per distinct key among the active
 // lanes.  Every lane of the calling control flow must call it.
@@ -59,7 +66,7 @@ __device__ __forceinline__ unsigned long long wave_peers(uint32_t key, bool acti
   unsigned long long mine = 0;
   while (todo) {
     const int leader = __ffsll((long long)todo) - 1;
-    const uint32_t lk = __shfl(key, leader, kWave);
+    const uint32_t lk = (uint32_t)__builtin_amdgcn_readlane((int)key, leader);
     const bool same = active && key == lk;
     const unsigned long long m = __ballot(same);
     if (same) mine = m;

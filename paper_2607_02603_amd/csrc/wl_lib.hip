@@ -433,7 +433,7 @@ __global__ void __launch_bounds__(kBlock) k_ring_rows(Ctx ctx) {
     }
     for (uint64_t m = __ballot(wide); m; m &= m - 1) {
       const int l = __builtin_ctzll(m);
-      const uint64_t b = __shfl(beg, l, kWave), e = __shfl(end, l, kWave);
+      const uint64_t b = read_lane64(beg, l), e = read_lane64(end, l);
       uint64_t sum = 0;
       for (uint64_t x = b + lane; x < e; x += kWave) sum += ctx.wgt[x];
       for (int off = kWave / 2; off > 0; off >>= 1) sum += __shfl_xor(sum, off, kWave);

@@ -54,7 +54,8 @@ __global__ void __launch_bounds__(kBlock) k_q_keys(Ctx ctx, const uint64_t* rp,
   for (uint64_t base = blockIdx.x * (uint64_t)kBlock + threadIdx.x - lane; base < ent;
        base += (uint64_t)gridDim.x * kBlock) {
     const uint64_t e = base + lane;
-    const uint32_t r0 = __shfl(lane == 0 ? q_row_of(rp, nrows, base) : 0u, 0, kWave);
+    const uint32_t r0 =
+        (uint32_t)__builtin_amdgcn_readlane((int)(lane == 0 ? q_row_of(rp, nrows, base) : 0u), 0);
     // window: row starts rp[r0 + 1 .. r0 + 64]; lane j holds rp[r0 + 1 + j]
     const uint32_t rj = r0 + 1 + lane;
     const uint64_t sj = rj <= nrows ? rp[rj] : ~0ull;
@@ -62,7 +63,7 @@ __global__ void __launch_bounds__(kBlock) k_q_keys(Ctx ctx, const uint64_t* rp,
     // of the wave; an entry past the window searches on its own
     uint32_t cnt = 0;
 #pragma unroll 8
-    for (int j = 0; j < kWave; ++j) cnt += __shfl(sj, j, kWave) <= e ? 1u : 0u;
+    for (int j = 0; j < kWave; ++j) cnt += read_lane64(sj, j) <= e ? 1u : 0u;
     if (e >= ent) continue;
     const uint32_t r = cnt == (uint32_t)kWave ? q_row_of(rp, nrows, e) : r0 + cnt;
     if (!isrep[row0 + r]) continue;
