@@ -7,7 +7,8 @@
 // and the relabel is a segmented sort of z inside every class of two or more
 // nodes:
 //   - classes (and later buckets) of at most kSmallMax nodes are sorted in
-//     LDS by one workgroup (bitonic network);
+//     LDS by one workgroup (a counting sort, or a bitonic network; 8 and 64
+//     nodes or fewer: bitonic networks across lanes);
 //   - larger ones go through most-significant-digit radix passes over 8-bit
 //     digits of z; a bucket whose smallest and largest key agree is finished
 //     at once (equal keys need no order), which is the common case in early
@@ -392,8 +393,14 @@ __device__ __forceinline__ bool key_less(unsigned long long a, uint32_t va,
   return a < b || (TIE && a == b && va < vb);
 }
 
-// One workgroup per small segment: bitonic sort of (z, node) in LDS, then
-// flags where z changes.
+constexpr uint32_t kCsBits = 10, kCsBuckets = 1u << kCsBits, kCsFix = 32;
+static_assert(kSmallMax <= 65536 && kCsBuckets % kBlock == 0, "counting sort of small segments");
+
+// One workgroup per small segment, keys in LDS: a counting sort by the ten
+// bits at and below the highest bit in which the keys differ, whose mixed
+// buckets of at most kCsFix keys are sorted by insertion; a larger mixed
+// bucket (rare for hashed images) falls back to a bitonic sort of (z, node).
+// Then flags where z changes.
 template <bool TIE>
 __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, uint32_t nblk) {
   DevState* st = ctx.st;
@@ -401,6 +408,12 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
   __shared__ unsigned long long skey[kSmallMax];
   __shared__ uint32_t sval[kSmallMax];
   __shared__ int differ, unsorted;
+  __shared__ uint32_t cnt[kCsBuckets + 1];
+  __shared__ uint16_t inv[kSmallMax];
+  __shared__ uint8_t mixed[kCsBuckets];
+  __shared__ unsigned long long xo;
+  __shared__ uint32_t csh[kBlock / kWave];
+  __shared__ int fallback;
   for (uint32_t si = bid; si < ns; si += nblk) {
     const uint2 sg = ctx.small_list[si];
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
@@ -434,6 +447,95 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
     if (!unsorted) {
       for (uint32_t t = threadIdx.x + 1; t < len; t += kBlock)
         if (skey[t] != skey[t - 1]) ctx.flags[s + t] = 1;
+      __syncthreads();
+      continue;
+    }
+    // Counting sort by the kCsBits bits at and below the highest bit in which
+    // the keys differ (above it they all agree), into inv (position ->
+    // element); then a bucket whose keys are not all equal is sorted by
+    // insertion when it holds at most kCsFix keys, and a larger one sends the
+    // segment to the sorting network below.
+    if (threadIdx.x == 0) {
+      xo = 0;
+      fallback = 0;
+    }
+    for (uint32_t b = threadIdx.x; b < kCsBuckets; b += kBlock) {
+      cnt[b] = 0;
+      mixed[b] = 0;
+    }
+    __syncthreads();
+    {
+      unsigned long long x = 0;
+      for (uint32_t t = threadIdx.x; t < len; t += kBlock) x |= skey[t] ^ skey[0];
+      if (x) atomicOr(&xo, x);
+    }
+    __syncthreads();
+    const int top = 63 - __clzll((long long)xo);  // xo != 0: the keys differ
+    const int sh = top >= (int)kCsBits - 1 ? top - ((int)kCsBits - 1) : 0;
+    uint32_t rk[kSmallMax / kBlock];
+#pragma unroll
+    for (uint32_t j = 0; j < kSmallMax / kBlock; ++j) {
+      const uint32_t t = threadIdx.x + j * kBlock;
+      if (t < len) rk[j] = atomicAdd(&cnt[(skey[t] >> sh) & (kCsBuckets - 1)], 1u);
+    }
+    __syncthreads();
+    {
+      // exclusive scan of the counts, kCsBuckets / kBlock per thread; cnt[kCsBuckets] = len
+      constexpr uint32_t kPer = kCsBuckets / kBlock;
+      uint32_t c[kPer], sum = 0;
+#pragma unroll
+      for (uint32_t u = 0; u < kPer; ++u) {
+        c[u] = cnt[threadIdx.x * kPer + u];
+        sum += c[u];
+      }
+      uint32_t tot;
+      uint32_t run = block_excl_scan(sum, csh, &tot);
+#pragma unroll
+      for (uint32_t u = 0; u < kPer; ++u) {
+        cnt[threadIdx.x * kPer + u] = run;
+        run += c[u];
+      }
+      if (threadIdx.x == 0) cnt[kCsBuckets] = len;
+    }
+    __syncthreads();
+#pragma unroll
+    for (uint32_t j = 0; j < kSmallMax / kBlock; ++j) {
+      const uint32_t t = threadIdx.x + j * kBlock;
+      if (t < len) inv[cnt[(skey[t] >> sh) & (kCsBuckets - 1)] + rk[j]] = (uint16_t)t;
+    }
+    __syncthreads();
+    for (uint32_t p = threadIdx.x + 1; p < len; p += kBlock) {
+      const unsigned long long k = skey[inv[p]];
+      const uint32_t d = (uint32_t)(k >> sh) & (kCsBuckets - 1);
+      if (p > cnt[d] && k != skey[inv[p - 1]]) mixed[d] = 1;
+    }
+    __syncthreads();
+    for (uint32_t b = threadIdx.x; b < kCsBuckets; b += kBlock) {
+      if (!mixed[b]) continue;
+      const uint32_t o = cnt[b], c = cnt[b + 1] - o;
+      if (c > kCsFix) {
+        fallback = 1;
+        continue;
+      }
+      for (uint32_t i = o + 1; i < o + c; ++i) {
+        const uint16_t e = inv[i];
+        const unsigned long long k = skey[e];
+        uint32_t j = i;
+        while (j > o && skey[inv[j - 1]] > k) {
+          inv[j] = inv[j - 1];
+          --j;
+        }
+        inv[j] = e;
+      }
+    }
+    __syncthreads();
+    if (!fallback) {
+      for (uint32_t p = threadIdx.x; p < len; p += kBlock) {
+        const uint32_t t = inv[p];
+        ctx.perm[s + p] = sval[t];
+        if (mat) ctx.keys[s + p] = skey[t];
+        if (p > 0 && skey[t] != skey[inv[p - 1]]) ctx.flags[s + p] = 1;
+      }
       __syncthreads();
       continue;
     }
