@@ -128,6 +128,7 @@ struct Ctx {
   int weighted;
   uint32_t ring;       // 0: image in F_p (p = 2^61 - 1); 1: in Z/2^64 (wl_device.h)
   int nt_stream;       // stream col_idx with non-temporal loads
+  uint32_t cs_fix;     // largest mixed bucket the small-segment sort fixes by insertion
   // Batch mode (Algorithm 2): the rows are nodes [ext_lo, ext_lo + n) of a
   // larger graph; a column outside that range is a node frozen as its own
   // singleton class, whose value is W(seed, r, 2^32 + column).

@@ -314,6 +314,13 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
     const char* nt = getenv("WL_NT_STREAM");
     c.nt_stream = nt && nt[0] == '1';
   }
+  {
+    // WL_SORT_FIX=0 sends every small segment with a mixed bucket to the
+    // sorting network (the tests use it to run that path)
+    const char* f = getenv("WL_SORT_FIX");
+    const long v = f ? strtol(f, nullptr, 10) : (long)kCsFix;
+    c.cs_fix = (uint32_t)std::min<long>(std::max<long>(v, 0), (long)kSmallMax);
+  }
   c.max_small = L.max_small;
   c.max_big = L.max_big;
   c.max_chunks = L.max_chunks;

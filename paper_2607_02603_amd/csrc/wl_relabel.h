@@ -398,8 +398,9 @@ static_assert(kSmallMax <= 65536 && kCsBuckets % kBlock == 0, "counting sort of 
 
 // One workgroup per small segment, keys in LDS: a counting sort by the ten
 // bits at and below the highest bit in which the keys differ, whose mixed
-// buckets of at most kCsFix keys are sorted by insertion; a larger mixed
-// bucket (rare for hashed images) falls back to a bitonic sort of (z, node).
+// buckets of at most ctx.cs_fix (default kCsFix) keys are sorted by insertion;
+// a larger mixed bucket (rare for hashed images) falls back to a bitonic sort
+// of (z, node).
 // Then flags where z changes.
 template <bool TIE>
 __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, uint32_t nblk) {
@@ -453,7 +454,7 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
     // Counting sort by the kCsBits bits at and below the highest bit in which
     // the keys differ (above it they all agree), into inv (position ->
     // element); then a bucket whose keys are not all equal is sorted by
-    // insertion when it holds at most kCsFix keys, and a larger one sends the
+    // insertion when it holds at most ctx.cs_fix keys, and a larger one sends the
     // segment to the sorting network below.
     if (threadIdx.x == 0) {
       xo = 0;
@@ -513,7 +514,7 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
     for (uint32_t b = threadIdx.x; b < kCsBuckets; b += kBlock) {
       if (!mixed[b]) continue;
       const uint32_t o = cnt[b], c = cnt[b + 1] - o;
-      if (c > kCsFix) {
+      if (c > ctx.cs_fix) {
         fallback = 1;
         continue;
       }
