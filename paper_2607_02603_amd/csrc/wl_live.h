@@ -201,8 +201,6 @@ __global__ void __launch_bounds__(kBlock) k_live_load(Ctx ctx) {
 __global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
-  __shared__ uint32_t sh[kBlock / kWave];
-  __shared__ uint32_t base_sh;
   const uint32_t nlive = st->n_live;
   const uint32_t stride = gridDim.x * kBlock;
   for (uint32_t j0 = blockIdx.x * kBlock; j0 < nlive; j0 += stride) {
@@ -212,18 +210,17 @@ __global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
       s = ctx.loff[j];
       len = ctx.llen[j];
     }
-    const bool pico = len >= 2 && len <= kPicoMax;
-    const bool tiny = len > kPicoMax && len <= kTinyMax;
-    const bool small = len > kTinyMax && len <= kSmallMax;
-    const bool big = len > kSmallMax;
-    const uint32_t pp = block_append(pico, &st->n_pico, sh, &base_sh);
-    if (pico) ctx.tiny_list[ctx.max_small - 1 - pp] = make_uint2(s, len | kMatBit);
-    const uint32_t t = block_append(tiny, &st->n_tiny, sh, &base_sh);
-    if (tiny) ctx.tiny_list[t] = make_uint2(s, len | kMatBit);
-    const uint32_t a = block_append(small, &st->n_small, sh, &base_sh);
-    if (small) ctx.small_list[a] = make_uint2(s, len | kMatBit);
-    const uint32_t b = block_append(big, &st->n_big[0], sh, &base_sh);
-    if (big) ctx.big_list0[b] = make_uint2(s, len);
+    // 0 pico, 1 tiny, 2 small, 3 big, 4 none
+    const uint32_t kind = len < 2 ? 4u
+                          : len <= kPicoMax ? 0u
+                          : len <= kTinyMax ? 1u
+                          : len <= kSmallMax ? 2u : 3u;
+    const uint32_t at =
+        block_append4(kind, &st->n_pico, &st->n_tiny, &st->n_small, &st->n_big[0]);
+    if (kind == 0) ctx.tiny_list[ctx.max_small - 1 - at] = make_uint2(s, len | kMatBit);
+    else if (kind == 1) ctx.tiny_list[at] = make_uint2(s, len | kMatBit);
+    else if (kind == 2) ctx.small_list[at] = make_uint2(s, len | kMatBit);
+    else if (kind == 3) ctx.big_list0[at] = make_uint2(s, len);
   }
 }
 
