@@ -10,7 +10,7 @@ constexpr int kBlock = 256;          // threads per workgroup (4 waves)
 constexpr uint32_t kSmallMax = 2048; // class/bucket size sorted in LDS
 constexpr uint32_t kTinyMax = 64;    // class/bucket size sorted in one wave
 constexpr uint32_t kPicoMax = 8;     // ... sorted by 8 lanes (kept at the back of the tiny list)
-constexpr uint32_t kTile = 4096;     // elements per tile in the MSD passes
+constexpr uint32_t kTile = 2048;     // elements per tile in the MSD passes
 constexpr uint32_t kTilePerThread = kTile / kBlock;
 constexpr int kRadixBits = 8;
 constexpr int kRadix = 1 << kRadixBits;
