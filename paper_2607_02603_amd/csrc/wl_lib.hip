@@ -659,7 +659,8 @@ struct Session {
 
   // after a synchronising pull
   int stats_collect() {
-    const uint32_t ran = host.round + (host.done == kHalted ? 1u : 0u);
+    const uint32_t ran =
+        host.round + (host.done == kHalted || host.done == kHaltedShift ? 1u : 0u);
     for (const TimedSpmv& t : timed) {
       if (!t.always && t.round >= ran) continue;
       float ms = 0;
@@ -1131,9 +1132,10 @@ struct Session {
   // After the sort: sub-classes, new colours of every node, next live
   // classes, end of the round.
   // prep: the round end also prepares the next round's gather tables (the
-  // next round is device-driven).
-  void live_tail(bool prep) {
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+  // next round is device-driven).  async: a device-driven round, which
+  // launches no kernels for the per-colour shift table; a round that needs
+  // the table halts the device in k_shift_sort (finish_halted builds it).
+  void live_tail(bool prep, bool async = false) {
     const uint32_t gl = live_grid(), ns = live_scan_blocks();
     const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
     DevState* st = ctx.st;
@@ -1145,10 +1147,23 @@ struct Session {
       hipLaunchKernelGGL(k_live_scan_final<uint32_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_subs_splits, dim3(std::max(gl, gc)), dim3(kBlock), 0, s, ctx);
     xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
-    hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx);
-    hipLaunchKernelGGL(k_shift_clear, dim3(gn), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_shift_scatter, dim3(gc), dim3(kBlock), 0, s, ctx);
-    xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr, nscan);
+    hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx, async ? 1 : 0);
+    live_shift_end(prep, !async);
+  }
+
+  // The per-colour shift table (when with_table; it is built only if the
+  // round's splits need it), the new colour of every node, the next live
+  // classes and the end of the round.
+  void live_shift_end(bool prep, bool with_table) {
+    const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    const uint32_t gl = live_grid();
+    const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
+    DevState* st = ctx.st;
+    if (with_table) {
+      hipLaunchKernelGGL(k_shift_clear, dim3(gn), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_shift_scatter, dim3(gc), dim3(kBlock), 0, s, ctx);
+      xscan(&st->shift_big, &st->k, ctx.shift, nullptr, nullptr, nullptr, nscan);
+    }
     // each block loads the split list into LDS: a capped grid loads it fewer times
     hipLaunchKernelGGL(k_shift_apply, dim3(std::min<uint32_t>(gn, 1024)), dim3(kBlock), 0, s,
                        ctx);
@@ -1288,7 +1303,7 @@ struct Session {
     // taken in grid-stride loops
     sorts(grid_for(L.n / 2, kBlock / kWave, 1024), grid_for(L.n / 2, kBlock / 8, 1024),
           grid_for(L.n / (kTinyMax + 1), 1, 1024), ap);
-    live_tail(true);
+    live_tail(true, true);
   }
 
   // The graph of rounds r, r + 1 for a first round of parity p = (r -
@@ -1344,15 +1359,21 @@ struct Session {
     return WL_OK;
   }
 
-  // The device halted in a round after async_passes radix passes: clear the
-  // halt and finish that round with host-driven passes.
+  // The device halted in a round, after async_passes radix passes
+  // (kHalted) or before the shift table (kHaltedShift): clear the halt and
+  // finish that round from there, host-driven.
   int finish_halted() {
+    const uint32_t why = host.done;
     use_round_ctx(host.round);
     hipLaunchKernelGGL(k_resume, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
-    if (int r = finish_sort(async_pass_count(), false)) return r;
-    live_tail(true);
+    if (why == kHaltedShift) {
+      live_shift_end(true, true);
+    } else {
+      if (int r = finish_sort(async_pass_count(), false)) return r;
+      live_tail(true);
+    }
     HIP_LAUNCH_CHECK();
     return pull();
   }
@@ -1393,7 +1414,7 @@ struct Session {
         if (int r = build_live_now()) return r;
       if (int r = launch_async_rounds(host.round, ahead)) return r;
       if (int r = pull()) return r;
-      if (host.done == kHalted)
+      if (host.done == kHalted || host.done == kHaltedShift)
         if (int r = finish_halted()) return r;
       if (host.err & kErrNotSymmetric)
         return fail(WL_EINVAL, "the graph is flagged symmetric but is not");

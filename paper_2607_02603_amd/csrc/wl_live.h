@@ -337,14 +337,19 @@ __global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx) {
 }
 
 // One block of 1024 threads: with at most kShiftLds splits, sort them by old
-// colour and replace the extras by their inclusive prefix sums.
+// colour and replace the extras by their inclusive prefix sums.  With more,
+// the shift table is needed: halt != 0 (a device-driven round, which does
+// not launch the table's kernels) halts the device for the host to build it.
 constexpr int kShiftThreads = 1024;
-__global__ void __launch_bounds__(kShiftThreads) k_shift_sort(Ctx ctx) {
+__global__ void __launch_bounds__(kShiftThreads) k_shift_sort(Ctx ctx, int halt) {
   DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
   const uint32_t S = st->n_split;
   if (S > kShiftLds) {
-    if (threadIdx.x == 0) ctx.st->shift_big = 1;
+    if (threadIdx.x == 0) {
+      ctx.st->shift_big = 1;
+      if (halt) ctx.st->done = kHaltedShift;
+    }
     return;
   }
   if (S == 0) return;

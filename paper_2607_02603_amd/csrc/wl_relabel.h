@@ -23,8 +23,10 @@
 namespace wl {
 
 // DevState::done of a device-driven round that stopped for the host to finish
-// its radix passes (k_resume clears it).
+// its radix passes, or (kHaltedShift) to build the per-colour shift table of
+// a round with more splits than the LDS search takes (k_resume clears both).
 constexpr uint32_t kHalted = 3;
+constexpr uint32_t kHaltedShift = 4;
 
 // Digit of a radix pass: 8-bit digits from the top of the key (61-bit
 // residues of F_p, or 64-bit values of Z/2^64), the last one shorter for F_p.
@@ -771,7 +773,7 @@ __global__ void __launch_bounds__(kBlock) k_scatter_colors(Ctx ctx) {
 
 // Clears the halt of a device-driven round before the host finishes it.
 __global__ void k_resume(Ctx ctx) {
-  if (ctx.st->done == kHalted) ctx.st->done = 0;
+  if (ctx.st->done == kHalted || ctx.st->done == kHaltedShift) ctx.st->done = 0;
 }
 
 __global__ void k_round_end(Ctx ctx, int count_round) {

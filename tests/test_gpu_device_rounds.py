@@ -4,7 +4,8 @@ give exactly the oracle's colours, colour count and round count.
 WL_HOST_ROUNDS sets how many rounds are host-driven before the groups start
 (0: every round is device-driven) and WL_ASYNC_PASSES how many radix passes a
 device-driven round runs before it halts for the host to finish it (0: every
-round with a class of more than 2048 nodes halts).  WL_GRAPH=1 replays the
+round with a class of more than 2048 nodes halts).  A device-driven round whose
+splits need the per-colour shift table (more than 4096 of them) halts too.  WL_GRAPH=1 replays the
 device-driven rounds from a captured HIP graph.  All are read at every call,
 so the cases below switch them per call.
 """
@@ -115,6 +116,19 @@ def test_graph_replay(knobs, host_rounds, passes):
     for cap in (7, 20):
         k, r, st = _same_as_oracle(g.row_ptr, g.col, seed=2, max_rounds=cap)
         assert r == cap and st == 1
+
+
+@pytest.mark.parametrize("host_rounds,passes,graph", [(0, 2, 0), (0, 0, 0), (1, 2, 0), (0, 2, 1)])
+def test_many_splits_halt_for_the_shift_table(knobs, host_rounds, passes, graph):
+    # 60,000 random labels on an R-MAT graph of 2^17 nodes: the first rounds
+    # split far more than 4096 classes at once, so a device-driven round
+    # halts before the per-colour shift table and the host finishes it
+    knobs(host_rounds, passes, graph)
+    g = inputs.rmat(17, 8, seed=9)
+    init = np.random.default_rng(4).integers(0, 60000, g.n).astype(np.uint32)
+    print(f"shift halt host_rounds={host_rounds} passes={passes} graph={graph}", flush=True)
+    k, r, st = _same_as_oracle(g.row_ptr, g.col, init=init, seed=5)
+    assert st == 0 and r >= 2
 
 
 @pytest.mark.parametrize("trial", range(8))
