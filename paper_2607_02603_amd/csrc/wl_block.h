@@ -37,6 +37,28 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* sh,
   return base + inc - v;
 }
 
+// Exclusive scan in place of p[0, n), n <= 4 * kBlock, by one block: each
+// thread takes four consecutive items, so one block scan does it.  Returns
+// the total.  Contains __syncthreads().
+__device__ __forceinline__ uint32_t block_scan_small(uint32_t* p, uint32_t n, uint32_t* sh) {
+  const uint32_t i0 = 4 * threadIdx.x;
+  uint32_t v[4], s = 0;
+#pragma unroll
+  for (uint32_t u = 0; u < 4; ++u) {
+    v[u] = i0 + u < n ? p[i0 + u] : 0u;
+    s += v[u];
+  }
+  uint32_t tot;
+  uint32_t run = block_excl_scan(s, sh, &tot);
+#pragma unroll
+  for (uint32_t u = 0; u < 4; ++u)
+    if (i0 + u < n) {
+      p[i0 + u] = run;
+      run += v[u];
+    }
+  return tot;
+}
+
 // Appends 'want' items to a device list: one atomic per block, slots
 // handed out by a block scan (order inside the list is irrelevant).
 // Contains __syncthreads(); every thread of the block must call it.

@@ -85,17 +85,9 @@ __global__ void __launch_bounds__(kBlock) k_xscan_top(const DevState* st, const 
                                                       uint32_t* tot_a, uint32_t* tot_b) {
   if (st->done || (run_if && !*run_if)) return;
   __shared__ uint32_t sh[kBlock / kWave];
+  static_assert(kScanBlocks <= 4 * kBlock, "block sums scanned by one block");
   for (int which = 0; which < 2; ++which) {
-    uint32_t* p = part + which * nblk;
-    uint32_t carry = 0;
-    for (uint32_t base = 0; base < nblk; base += kBlock) {
-      const uint32_t i = base + threadIdx.x;
-      const uint32_t v = i < nblk ? p[i] : 0;
-      uint32_t tot;
-      const uint32_t ex = block_excl_scan(v, sh, &tot);
-      if (i < nblk) p[i] = carry + ex;
-      carry += tot;
-    }
+    const uint32_t carry = block_scan_small(part + which * nblk, nblk, sh);
     uint32_t* dst = which ? tot_b : tot_a;
     if (threadIdx.x == 0 && dst) *dst = carry;
   }
@@ -250,15 +242,7 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_top(Ctx ctx, uint32_t nblk
   DevState* st = ctx.st;
   if (st->done) return;
   __shared__ uint32_t sh[kBlock / kWave];
-  uint32_t carry = 0;
-  for (uint32_t base = 0; base < nblk; base += kBlock) {
-    const uint32_t i = base + threadIdx.x;
-    const uint32_t v = i < nblk ? ctx.scan_part[i] : 0;
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan(v, sh, &tot);
-    if (i < nblk) ctx.scan_part[i] = carry + ex;
-    carry += tot;
-  }
+  const uint32_t carry = block_scan_small(ctx.scan_part, nblk, sh);
   if (threadIdx.x == 0) {
     st->nsub = carry;
     st->k_new = st->k + carry - st->n_live;

@@ -719,15 +719,7 @@ __global__ void __launch_bounds__(kBlock) k_scan_part(Ctx ctx) {
 __global__ void __launch_bounds__(kBlock) k_scan_top(Ctx ctx, uint32_t nblk) {
   if (ctx.st->done) return;
   __shared__ uint32_t sh[kBlock / kWave];
-  uint32_t carry = 0;
-  for (uint32_t base = 0; base < nblk; base += kBlock) {
-    const uint32_t i = base + threadIdx.x;
-    const uint32_t v = i < nblk ? ctx.scan_part[i] : 0;
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan(v, sh, &tot);
-    if (i < nblk) ctx.scan_part[i] = carry + ex;
-    carry += tot;
-  }
+  const uint32_t carry = block_scan_small(ctx.scan_part, nblk, sh);
   if (threadIdx.x == 0) ctx.st->k_new = carry;
 }
 
