@@ -356,6 +356,9 @@ int wl_stats_get(wl_stats *out);
  *   WL_ASYNC_PASSES=n    radix passes a device-driven round launches (0-8).
  *   WL_GRAPH=1           replay the device-driven rounds from a HIP graph.
  *   WL_NT_STREAM=1       non-temporal loads of the column indices.
+ *   WL_SORT_FIX=n        largest mixed bucket the counting sort of a small
+ *                        segment fixes by insertion (default 32; 0 sends
+ *                        every segment with one to the sorting network).
  *   WL_HOST_STAGING=0    copy pageable host memory without page-locked
  *                        staging buffers (as when they are refused).
  *   WL_TRACE_STREAMED=1, WL_TRACE_BATCHED=1
