@@ -42,8 +42,6 @@ struct DevState {
   uint32_t done;        // 0 running, 1 stable, 2 round cap reached
   uint32_t max_rounds;  // stop after this many rounds in total
   uint32_t n_small;     // entries in the small-segment list
-  uint32_t n_big[2];    // entries in the two big-segment lists
-  uint32_t n_tiles;     // tiles of the current big list
   uint32_t err;         // input errors seen on the device (bit mask)
   uint32_t n_chunks;    // heavy-row chunks of the SpMV schedule
   uint32_t bin_cnt[kNumBins];
@@ -66,6 +64,10 @@ struct DevState {
   uint32_t prep_round;  // the round whose gather tables the round end prepares
   uint32_t n_pico;      // segments of <= kPicoMax nodes (this round)
   uint64_t seed;
+  // The two big-segment lists: (entries << 32) | tiles.  One 64-bit atomic
+  // appends a segment and reserves its tiles, so the tile offsets come out
+  // in list order without a scan.
+  unsigned long long big[2];
   unsigned long long work[3][2];    // diagnostics: rows, entries per image kind
   unsigned long long act_entries;   // entries of the rows whose image is needed
   unsigned long long sym_hash[2];   // validation: hashes of (i, j) and (j, i)
@@ -113,7 +115,8 @@ struct Ctx {
   uint2* tiny_list;    // (start, len | kMatBit), 2 <= len <= 64
   uint2* big_list0;
   uint2* big_list1;
-  uint32_t* tile_off;  // tiles of the current big list (exclusive scan)
+  uint32_t* tile_off0; // first tile of every segment of big_list0 (list order)
+  uint32_t* tile_off1; // the same for big_list1
   uint32_t* bhist;     // per (big segment, bucket)
   unsigned long long* bmin;
   unsigned long long* bmax;

@@ -123,7 +123,7 @@ Layout make_layout(uint64_t n, uint64_t nnz, bool in_core = true) {
   L.off_tiny = take(8ull * L.max_small);
   L.off_big0 = take(8ull * L.max_big);
   L.off_big1 = take(8ull * L.max_big);
-  L.off_tile = take(4ull * (L.max_big + 1));
+  L.off_tile = take(8ull * (L.max_big + 1));
   L.off_bhist = take(4ull * L.max_big * kRadix);
   L.off_bmin = take(8ull * L.max_big * kRadix);
   L.off_bmax = take(8ull * L.max_big * kRadix);
@@ -257,7 +257,8 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.tiny_list = (uint2*)(ws + L.off_tiny);
   c.big_list0 = (uint2*)(ws + L.off_big0);
   c.big_list1 = (uint2*)(ws + L.off_big1);
-  c.tile_off = (uint32_t*)(ws + L.off_tile);
+  c.tile_off0 = (uint32_t*)(ws + L.off_tile);
+  c.tile_off1 = c.tile_off0 + L.max_big + 1;
   c.bhist = (uint32_t*)(ws + L.off_bhist);
   c.bmin = (unsigned long long*)(ws + L.off_bmin);
   c.bmax = (unsigned long long*)(ws + L.off_bmax);
@@ -1032,13 +1033,16 @@ struct Session {
     return finish_sort(0, true);
   }
 
+  // Entries of big-segment list 'which' at the last read-back.
+  uint32_t big_entries(int which) const { return (uint32_t)(host.big[which] >> 32); }
+
   // Radix passes from 'pass0' on while big segments are left (read back after
   // every pass), then the small sorts and, for the full relabel, the rank
   // scan.
   int finish_sort(int pass0, bool full) {
     int pass = pass0;
-    for (; pass < kPasses && host.n_big[pass & 1] > 0; ++pass) {
-      radix_pass(pass, std::min<uint32_t>(host.n_big[pass & 1], 4096));
+    for (; pass < kPasses && big_entries(pass & 1) > 0; ++pass) {
+      radix_pass(pass, std::min<uint32_t>(big_entries(pass & 1), 4096));
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
     }
@@ -1052,7 +1056,6 @@ struct Session {
   }
 
   void radix_pass(int pass, uint32_t scan_grid) {
-    hipLaunchKernelGGL(k_big_tiles, dim3(1), dim3(kBlock), 0, s, ctx, pass);
     if (pass == 0 && !ctx.keys_mat)
       hipLaunchKernelGGL(k_big_gather, dim3(2048), dim3(kBlock), 0, s, ctx);
     // the first pass of the call clears the histograms over their whole
@@ -1087,10 +1090,8 @@ struct Session {
              uint32_t* tot_a, uint32_t* tot_b, uint32_t nblk) {
     hipLaunchKernelGGL(k_xscan_part, dim3(nblk), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
                        b, ctx.scan_part);
-    hipLaunchKernelGGL(k_xscan_top, dim3(1), dim3(kBlock), 0, s, ctx.st, run_if, ctx.scan_part,
-                       nblk, tot_a, tot_b);
     hipLaunchKernelGGL(k_xscan_final, dim3(nblk), dim3(kBlock), 0, s, ctx.st, run_if, lenp, a,
-                       b, ctx.scan_part);
+                       b, ctx.scan_part, tot_a, tot_b);
   }
 
   // Live classes from the grouping of the canonical start (perm, cstart, ids
@@ -1140,7 +1141,6 @@ struct Session {
     const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
     DevState* st = ctx.st;
     hipLaunchKernelGGL(k_live_scan_part, dim3(ns), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_scan_top, dim3(1), dim3(kBlock), 0, s, ctx, ns);
     if (rp64)
       hipLaunchKernelGGL(k_live_scan_final<uint64_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
     else

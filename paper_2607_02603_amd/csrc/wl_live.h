@@ -46,8 +46,9 @@ constexpr uint32_t kShiftLds = 4096;  // splits searched in LDS; more use a tabl
 
 // ---------------------------------------------------------------------------
 // Generic exclusive scan of one or two u32 arrays in place, length read from
-// device memory, totals written to device memory.  Three launches:
-// part (kScanBlocks blocks), top (one block), final (kScanBlocks blocks).
+// device memory, totals written to device memory.  Two launches of the same
+// grid (at most kScanBlocks blocks): part (block sums), final (each block
+// sums the block sums below its own, then scans its range).
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ void xscan_range(uint32_t len, uint32_t b, uint32_t nblk,
@@ -79,28 +80,23 @@ __global__ void __launch_bounds__(kBlock) k_xscan_part(const DevState* st, const
   }
 }
 
-// One block: exclusive scan of the block sums; totals to *tot_a / *tot_b.
-__global__ void __launch_bounds__(kBlock) k_xscan_top(const DevState* st, const uint32_t* run_if,
-                                                      uint32_t* part, uint32_t nblk,
-                                                      uint32_t* tot_a, uint32_t* tot_b) {
-  if (st->done || (run_if && !*run_if)) return;
-  __shared__ uint32_t sh[kBlock / kWave];
-  static_assert(kScanBlocks <= 4 * kBlock, "block sums scanned by one block");
-  for (int which = 0; which < 2; ++which) {
-    const uint32_t carry = block_scan_small(part + which * nblk, nblk, sh);
-    uint32_t* dst = which ? tot_b : tot_a;
-    if (threadIdx.x == 0 && dst) *dst = carry;
-  }
-}
-
+// Totals to *tot_a / *tot_b (either may be NULL) by block 0.
 __global__ void __launch_bounds__(kBlock) k_xscan_final(const DevState* st, const uint32_t* run_if,
                                                         const uint32_t* lenp, uint32_t* a,
-                                                        uint32_t* b, const uint32_t* part) {
+                                                        uint32_t* b, const uint32_t* part,
+                                                        uint32_t* tot_a, uint32_t* tot_b) {
+  static_assert(kScanBlocks <= 4 * kBlock, "block sums summed by one block");
   if (st->done || (run_if && !*run_if)) return;
   uint32_t lo, hi;
   xscan_range(*lenp, blockIdx.x, gridDim.x, &lo, &hi);
-  uint32_t ra = part[blockIdx.x], rb = part[gridDim.x + blockIdx.x];
   __shared__ uint32_t sh[kBlock / kWave];
+  uint32_t sa, sb = 0;
+  uint32_t ra = block_part_prefix(part, gridDim.x, blockIdx.x, sh, &sa);
+  uint32_t rb = b ? block_part_prefix(part + gridDim.x, gridDim.x, blockIdx.x, sh, &sb) : 0u;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (tot_a) *tot_a = sa;
+    if (tot_b) *tot_b = sb;
+  }
   for (uint32_t base = lo; base < hi; base += kBlock) {
     const uint32_t i = base + threadIdx.x;
     const uint32_t va = i < hi ? a[i] : 0;
@@ -207,12 +203,11 @@ __global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
                           : len <= kPicoMax ? 0u
                           : len <= kTinyMax ? 1u
                           : len <= kSmallMax ? 2u : 3u;
-    const uint32_t at =
-        block_append4(kind, &st->n_pico, &st->n_tiny, &st->n_small, &st->n_big[0]);
+    const uint32_t at = block_append3(kind, &st->n_pico, &st->n_tiny, &st->n_small);
     if (kind == 0) ctx.tiny_list[ctx.max_small - 1 - at] = make_uint2(s, len | kMatBit);
     else if (kind == 1) ctx.tiny_list[at] = make_uint2(s, len | kMatBit);
     else if (kind == 2) ctx.small_list[at] = make_uint2(s, len | kMatBit);
-    else if (kind == 3) ctx.big_list0[at] = make_uint2(s, len);
+    else if (kind == 3) big_append(ctx, 0, s, len);
   }
 }
 
@@ -235,36 +230,34 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_part(Ctx ctx) {
   if (threadIdx.x == 0) ctx.scan_part[blockIdx.x] = tot;
 }
 
-// One block: block offsets; nsub = sub-classes of the live classes,
-// k_new = k + nsub - n_live; nosplit when no class split; the round whose
-// gather tables the round end prepares.
-__global__ void __launch_bounds__(kBlock) k_live_scan_top(Ctx ctx, uint32_t nblk) {
+// Every block: its offset among the block sums and their total, the number
+// of sub-classes of the live classes, nsub (block 0 records it with k_new =
+// k + nsub - n_live, nosplit when no class split, and the round whose
+// gather tables the round end prepares).  Then ids[q] = sub-class of q; per
+// sub-class g: first position, end, and whether it holds a non-empty row:
+// its key is non-zero (gnz), or a member with key 0 has one (its image
+// happens to be 0; nz0f).
+template <typename RP>
+__global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
+  static_assert(kScanBlocks <= 4 * kBlock, "block sums summed by one block");
   __shared__ uint32_t sh[kBlock / kWave];
-  const uint32_t carry = block_scan_small(ctx.scan_part, nblk, sh);
-  if (threadIdx.x == 0) {
-    st->nsub = carry;
-    st->k_new = st->k + carry - st->n_live;
-    st->nosplit = carry == st->n_live ? 1u : 0u;
-    st->split_any = 1u - st->nosplit;
+  uint32_t nsub;
+  uint32_t run = block_part_prefix(ctx.scan_part, gridDim.x, blockIdx.x, sh, &nsub);
+  const uint32_t nlive = st->n_live;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    st->nsub = nsub;
+    st->k_new = st->k + nsub - nlive;
+    st->nosplit = nsub == nlive ? 1u : 0u;
+    st->split_any = nsub == nlive ? 0u : 1u;
     st->shift_big = 0;
     st->prep_round = st->round + 1;
   }
-}
-
-// ids[q] = sub-class of q; per sub-class g: first position, end, and whether
-// it holds a non-empty row: its key is non-zero (gnz), or a member with key
-// 0 has one (its image happens to be 0; nz0f).
-template <typename RP>
-__global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
-  const DevState* st = ctx.st;
-  if (st->done || st->nosplit) return;
+  if (nsub == nlive) return;
   const uint32_t nl = st->nl;
   uint32_t lo, hi;
   xscan_range(nl, blockIdx.x, gridDim.x, &lo, &hi);
-  uint32_t run = ctx.scan_part[blockIdx.x];
-  __shared__ uint32_t sh[kBlock / kWave];
   for (uint32_t base = lo; base < hi; base += kBlock) {
     const uint32_t q = base + threadIdx.x;
     const uint32_t f = q < hi ? live_flag(ctx, q) : 0u;
@@ -596,9 +589,8 @@ __global__ void __launch_bounds__(kBlock) k_live_round_end(Ctx ctx, int prep) {
   st->n_small = 0;
   st->n_tiny = 0;
   st->n_pico = 0;
-  st->n_big[0] = 0;
-  st->n_big[1] = 0;
-  st->n_tiles = 0;
+  st->big[0] = 0;
+  st->big[1] = 0;
   st->act_entries = 0;
   st->n_split = 0;
   st->n_mid = 0;

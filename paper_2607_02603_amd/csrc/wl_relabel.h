@@ -42,9 +42,8 @@ __global__ void k_round_begin(Ctx ctx) {
   st->n_small = 0;
   st->n_tiny = 0;
   st->n_pico = 0;
-  st->n_big[0] = 0;
-  st->n_big[1] = 0;
-  st->n_tiles = 0;
+  st->big[0] = 0;
+  st->big[1] = 0;
   st->act_entries = 0;
   st->n_split = 0;
   st->n_mid = 0;
@@ -57,6 +56,37 @@ __global__ void __launch_bounds__(kBlock) k_fill_u8(Ctx ctx, uint8_t* p,
   for (uint64_t i = blockIdx.x * (uint64_t)kBlock + threadIdx.x; i < cnt;
        i += (uint64_t)gridDim.x * kBlock)
     p[i] = v;
+}
+
+__device__ __forceinline__ const uint2* big_list(const Ctx& c, int which) {
+  return which ? c.big_list1 : c.big_list0;
+}
+__device__ __forceinline__ uint2* big_list_w(const Ctx& c, int which) {
+  return which ? c.big_list1 : c.big_list0;
+}
+__device__ __forceinline__ uint32_t* tile_offsets(const Ctx& c, int which) {
+  return which ? c.tile_off1 : c.tile_off0;
+}
+__device__ __forceinline__ uint32_t big_count(const DevState* st, int which) {
+  return (uint32_t)(st->big[which] >> 32);
+}
+__device__ __forceinline__ uint32_t big_tiles(const DevState* st, int which) {
+  return (uint32_t)st->big[which];
+}
+
+// Appends segment (s, len) to big list 'which' with its first tile: the
+// 64-bit add bumps the entry count (high word) by one and the tile count
+// (low word) by the segment's tiles, so the returned pair is the segment's
+// slot and its first tile, and tile offsets grow with the slot.  The tile
+// count stays below 2^32 (at most one tile per kTile nodes plus one per
+// segment), so the low word never carries into the high one.
+__device__ __forceinline__ void big_append(const Ctx& ctx, int which, uint32_t s,
+                                           uint32_t len) {
+  const unsigned long long o =
+      atomicAdd(&ctx.st->big[which], (1ull << 32) | ((len + kTile - 1) / kTile));
+  const uint32_t at = (uint32_t)(o >> 32);
+  big_list_w(ctx, which)[at] = make_uint2(s, len);
+  tile_offsets(ctx, which)[at] = (uint32_t)o;
 }
 
 // One entry per class: flag its first position, queue it if it has >= 2
@@ -81,52 +111,15 @@ __global__ void __launch_bounds__(kBlock) k_segments(Ctx ctx) {
                           : len <= kPicoMax ? 0u
                           : len <= kTinyMax ? 1u
                           : len <= kSmallMax ? 2u : 3u;
-    const uint32_t at =
-        block_append4(kind, &st->n_pico, &st->n_tiny, &st->n_small, &st->n_big[0]);
+    const uint32_t at = block_append3(kind, &st->n_pico, &st->n_tiny, &st->n_small);
     if (kind == 0) ctx.tiny_list[ctx.max_small - 1 - at] = make_uint2(s, len | mat);
     else if (kind == 1) ctx.tiny_list[at] = make_uint2(s, len | mat);
     else if (kind == 2) ctx.small_list[at] = make_uint2(s, len | mat);
-    else if (kind == 3) ctx.big_list0[at] = make_uint2(s, len);
+    else if (kind == 3) big_append(ctx, 0, s, len);
   }
 }
 
-__device__ __forceinline__ const uint2* big_list(const Ctx& c, int which) {
-  return which ? c.big_list1 : c.big_list0;
-}
-__device__ __forceinline__ uint2* big_list_w(const Ctx& c, int which) {
-  return which ? c.big_list1 : c.big_list0;
-}
-
-// One block: tile offsets of the big list used by 'pass'.
-__global__ void __launch_bounds__(kBlock) k_big_tiles(Ctx ctx, int pass) {
-  DevState* st = ctx.st;
-  if (st->done) return;
-  const int cur = pass & 1;
-  const uint32_t nb = st->n_big[cur];
-  if (nb == 0) {
-    // nothing left: the other list must not be taken for a later pass
-    if (threadIdx.x == 0) st->n_big[cur ^ 1] = 0;
-    return;
-  }
-  const uint2* L = big_list(ctx, cur);
-  __shared__ uint32_t sh[kBlock / kWave];
-  uint32_t carry = 0;
-  for (uint32_t base = 0; base < nb; base += kBlock) {
-    uint32_t i = base + threadIdx.x;
-    uint32_t t = i < nb ? (L[i].y + kTile - 1) / kTile : 0;
-    uint32_t tot;
-    uint32_t ex = block_excl_scan(t, sh, &tot);
-    if (i < nb) ctx.tile_off[i] = carry + ex;
-    carry += tot;
-  }
-  if (threadIdx.x == 0) {
-    ctx.tile_off[nb] = carry;
-    st->n_tiles = carry;
-    st->n_big[cur ^ 1] = 0;
-  }
-}
-
-// Segment index of tile t: last i with tile_off[i] <= t.
+// Segment index of tile t: last i with off[i] <= t.
 __device__ __forceinline__ uint32_t tile_segment(const uint32_t* off,
                                                  uint32_t nb, uint32_t t) {
   uint32_t lo = 0, hi = nb - 1;
@@ -148,10 +141,11 @@ __device__ __forceinline__ TileRange tile_range(const Ctx& ctx, int cur,
                                                 uint32_t nb, uint32_t t) {
   const uint2* L = big_list(ctx, cur);
   TileRange r;
-  r.seg = tile_segment(ctx.tile_off, nb, t);
+  const uint32_t* off = tile_offsets(ctx, cur);
+  r.seg = tile_segment(off, nb, t);
   const uint2 s = L[r.seg];
   r.seg_start = s.x;
-  r.beg = s.x + (t - ctx.tile_off[r.seg]) * kTile;
+  r.beg = s.x + (t - off[r.seg]) * kTile;
   r.end = min(s.x + s.y, r.beg + kTile);
   return r;
 }
@@ -169,7 +163,7 @@ __device__ __forceinline__ uint32_t tile_order(uint32_t i, uint32_t nt) {
 __global__ void __launch_bounds__(kBlock) k_big_gather(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
-  const uint32_t nb = st->n_big[0], nt = st->n_tiles;
+  const uint32_t nb = big_count(st, 0), nt = big_tiles(st, 0);
   if (nb == 0) return;
   for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
     TileRange r = tile_range(ctx, 0, nb, t);
@@ -198,7 +192,10 @@ __global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
   DevState* st = ctx.st;
   if (st->done) return;
   const int cur = pass & 1;
-  const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
+  // the list this pass's k_big_scan fills starts empty (the previous pass
+  // consumed it; with nothing left it must not be taken for a later pass)
+  if (blockIdx.x == 0 && threadIdx.x == 0) st->big[cur ^ 1] = 0;
+  const uint32_t nb = big_count(st, cur), nt = big_tiles(st, cur);
   if (nb == 0) return;
   __shared__ uint32_t cnt[kRadix];
   __shared__ unsigned long long mn[kRadix], mx[kRadix];
@@ -254,9 +251,8 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
   DevState* st = ctx.st;
   if (st->done) return;
   const int cur = pass & 1;
-  const uint32_t nb = st->n_big[cur];
+  const uint32_t nb = big_count(st, cur);
   const uint2* L = big_list(ctx, cur);
-  uint2* N = big_list_w(ctx, cur ^ 1);
   __shared__ uint32_t sh[kBlock / kWave];
   for (uint32_t sgi = blockIdx.x; sgi < nb; sgi += gridDim.x) {
     const uint2 s = L[sgi];
@@ -291,8 +287,7 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
           uint32_t idx = atomicAdd(&st->n_small, 1u);
           ctx.small_list[idx] = make_uint2(pos, h | kMatBit);
         } else {
-          uint32_t idx = atomicAdd(&st->n_big[cur ^ 1], 1u);
-          N[idx] = make_uint2(pos, h);
+          big_append(ctx, cur ^ 1, pos, h);
         }
       }
     }
@@ -308,7 +303,7 @@ __global__ void __launch_bounds__(kBlock) k_big_scatter(Ctx ctx, int pass) {
   DevState* st = ctx.st;
   if (st->done) return;
   const int cur = pass & 1;
-  const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
+  const uint32_t nb = big_count(st, cur), nt = big_tiles(st, cur);
   if (nb == 0) return;
   __shared__ uint32_t lcnt[kRadix];
   __shared__ uint32_t dbase[kRadix];  // output position of staged slot 0 of the bucket
@@ -369,7 +364,7 @@ __global__ void __launch_bounds__(kBlock) k_big_copyback(Ctx ctx, int pass) {
   DevState* st = ctx.st;
   if (st->done) return;
   const int cur = pass & 1;
-  const uint32_t nb = st->n_big[cur], nt = st->n_tiles;
+  const uint32_t nb = big_count(st, cur), nt = big_tiles(st, cur);
   if (nb == 0) return;
   for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
     TileRange r = tile_range(ctx, cur, nb, t);
@@ -579,7 +574,7 @@ template <bool TIE>
 __device__ __forceinline__ void tiny_sort_body(const Ctx& ctx, int check_passes, uint32_t bid,
                                                uint32_t nblk) {
   DevState* st = ctx.st;
-  if (check_passes >= 0 && bid == 0 && threadIdx.x == 0 && st->n_big[check_passes & 1] > 0)
+  if (check_passes >= 0 && bid == 0 && threadIdx.x == 0 && big_count(st, check_passes & 1) > 0)
     st->done = kHalted;
   const uint32_t nt = st->n_tiny;
   const uint32_t lane = lane_id();
