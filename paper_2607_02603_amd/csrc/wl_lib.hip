@@ -979,15 +979,17 @@ struct Session {
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_live_count, dim3(gl), dim3(kBlock), 0, s, ctx, 1);
     const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
+    const int long_rows = live_heavy || host.max_deg > kShortRow;
     timed_spmv(round, always, kImgGather, [&] {
-      hipLaunchKernelGGL(k_spmv_q<W>, dim3(gl), dim3(kBlock), 0, s, ctx);
+      hipLaunchKernelGGL(k_spmv_q<W>, dim3(long_rows ? gl : grid_for(host.nl, 2 * kBlock, 4096)),
+                         dim3(kBlock), 0, s, ctx, long_rows);
       if (live_heavy) {
         const uint32_t gh = grid_for(host.bin_cnt[3], kBlock, 1024);
         hipLaunchKernelGGL(k_heavy_clear, dim3(gh), dim3(kBlock), 0, s, ctx);
         hipLaunchKernelGGL(k_heavy_set, dim3(gh), dim3(kBlock), 0, s, ctx);
       }
       // rows of at most kShortRow entries are done by k_spmv_q alone
-      if (live_heavy || host.max_deg > kShortRow)
+      if (long_rows)
         hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
                            live_heavy);
     });
@@ -1065,10 +1067,10 @@ struct Session {
                          dim3(kBlock), 0, s, ctx);
       hist_clean = true;
     }
-    hipLaunchKernelGGL(k_big_hist, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_hist, dim3(1024), dim3(kBlock), 0, s, ctx, pass);
     hipLaunchKernelGGL(k_big_scan, dim3(scan_grid), dim3(kBlock), 0, s, ctx, pass);
-    hipLaunchKernelGGL(k_big_scatter, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
-    hipLaunchKernelGGL(k_big_copyback, dim3(2048), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_scatter, dim3(1024), dim3(kBlock), 0, s, ctx, pass);
+    hipLaunchKernelGGL(k_big_copyback, dim3(1024), dim3(kBlock), 0, s, ctx, pass);
   }
 
   void rank_scan() {

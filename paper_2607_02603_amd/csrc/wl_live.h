@@ -51,11 +51,45 @@ constexpr uint32_t kShiftLds = 4096;  // splits searched in LDS; more use a tabl
 // sums the block sums below its own, then scans its range).
 // ---------------------------------------------------------------------------
 
+// Block b's range [lo, hi) of a scan over len items: a multiple of
+// kScanStep items (but the last), so every step of kScanStep items starts
+// at a multiple of kScanItems.
+constexpr uint32_t kScanItems = 4;                  // consecutive items per thread and step
+constexpr uint32_t kScanStep = kScanItems * kBlock;
 __device__ __forceinline__ void xscan_range(uint32_t len, uint32_t b, uint32_t nblk,
                                             uint32_t* lo, uint32_t* hi) {
-  const uint32_t per = ((len + nblk - 1) / nblk + kBlock - 1) / kBlock * kBlock;
-  *lo = min(len, b * per);
-  *hi = min(len, *lo + per);
+  const uint32_t per = ((len + nblk - 1) / nblk + kScanStep - 1) / kScanStep * kScanStep;
+  *lo = (uint32_t)min((uint64_t)len, (uint64_t)b * per);
+  *hi = (uint32_t)min((uint64_t)len, (uint64_t)*lo + per);
+}
+
+// v[u] = p[i + u] for the u with i + u < n (0 beyond); a whole group is one
+// 16-byte load when p + i is 16-byte aligned (i is a multiple of 4 here, so
+// that is a property of p alone).
+__device__ __forceinline__ void load4(const uint32_t* p, uint32_t i, uint32_t n, uint32_t v[4]) {
+  if (i + 3 < n && ((uintptr_t)(p + i) & 15) == 0) {
+    const uint4 w = *(const uint4*)(p + i);
+    v[0] = w.x;
+    v[1] = w.y;
+    v[2] = w.z;
+    v[3] = w.w;
+  } else {
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) v[u] = i + u < n ? p[i + u] : 0u;
+  }
+}
+__device__ __forceinline__ void load4(const uint64_t* p, uint32_t i, uint32_t n, uint64_t v[4]) {
+  if (i + 3 < n && ((uintptr_t)(p + i) & 15) == 0) {
+    const ulonglong2 w0 = *(const ulonglong2*)(p + i);
+    const ulonglong2 w1 = *(const ulonglong2*)(p + i + 2);
+    v[0] = w0.x;
+    v[1] = w0.y;
+    v[2] = w1.x;
+    v[3] = w1.y;
+  } else {
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) v[u] = i + u < n ? p[i + u] : 0ull;
+  }
 }
 
 // 'run_if' (device, may be NULL): the scan runs only when *run_if != 0.
@@ -66,9 +100,14 @@ __global__ void __launch_bounds__(kBlock) k_xscan_part(const DevState* st, const
   uint32_t lo, hi;
   xscan_range(*lenp, blockIdx.x, gridDim.x, &lo, &hi);
   uint32_t sa = 0, sb = 0;
-  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
-    sa += a[i];
-    if (b) sb += b[i];
+  for (uint32_t i = lo + kScanItems * threadIdx.x; i < hi; i += kScanStep) {
+    uint32_t v[4];
+    load4(a, i, hi, v);
+    sa += v[0] + v[1] + v[2] + v[3];
+    if (b) {
+      load4(b, i, hi, v);
+      sb += v[0] + v[1] + v[2] + v[3];
+    }
   }
   __shared__ uint32_t sh[kBlock / kWave];
   uint32_t ta, tb = 0;
@@ -97,20 +136,26 @@ __global__ void __launch_bounds__(kBlock) k_xscan_final(const DevState* st, cons
     if (tot_a) *tot_a = sa;
     if (tot_b) *tot_b = sb;
   }
-  for (uint32_t base = lo; base < hi; base += kBlock) {
-    const uint32_t i = base + threadIdx.x;
-    const uint32_t va = i < hi ? a[i] : 0;
-    uint32_t ta;
-    const uint32_t ea = block_excl_scan(va, sh, &ta);
-    if (i < hi) a[i] = ra + ea;
+  for (uint32_t base = lo; base < hi; base += kScanStep) {
+    const uint32_t i = base + kScanItems * threadIdx.x;
+    uint32_t va[4], vb[4] = {0, 0, 0, 0};
+    load4(a, i, hi, va);
+    if (b) load4(b, i, hi, vb);
+    uint32_t ta, tb = 0;
+    uint32_t xa = ra + block_excl_scan(va[0] + va[1] + va[2] + va[3], sh, &ta);
+    uint32_t xb = b ? rb + block_excl_scan(vb[0] + vb[1] + vb[2] + vb[3], sh, &tb) : 0u;
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u)
+      if (i + u < hi) {
+        a[i + u] = xa;
+        xa += va[u];
+        if (b) {
+          b[i + u] = xb;
+          xb += vb[u];
+        }
+      }
     ra += ta;
-    if (b) {
-      const uint32_t vb = i < hi ? b[i] : 0;
-      uint32_t tb;
-      const uint32_t eb = block_excl_scan(vb, sh, &tb);
-      if (i < hi) b[i] = rb + eb;
-      rb += tb;
-    }
+    rb += tb;
   }
 }
 
@@ -211,11 +256,26 @@ __global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
   }
 }
 
-// A sub-class starts at q: first position of a class, or a key change.
-__device__ __forceinline__ uint32_t live_flag(const Ctx& ctx, uint32_t q) {
-  return (q == 0 || ctx.qcls[q] != ctx.qcls[q - 1] || ctx.keys[q] != ctx.keys[q - 1]) ? 1u
-                                                                                      : 0u;
-}
+// Classes and keys of positions q0 - 1 .. q0 + 4 (q0 a multiple of 4, q0 <
+// nl; entries at or beyond nl, and before 0, are placeholders), from which
+// the sub-class flags of q0 .. q0 + 4 follow: a sub-class starts at q when q
+// is a class's first position or the key changes.
+struct FlagWindow {
+  uint32_t c[6];
+  uint64_t k[6];
+  __device__ __forceinline__ void load(const Ctx& ctx, uint32_t q0, uint32_t nl) {
+    load4(ctx.qcls, q0, nl, c + 1);
+    load4(ctx.keys, q0, nl, k + 1);
+    c[0] = q0 ? ctx.qcls[q0 - 1] : 0xFFFFFFFFu;
+    k[0] = q0 ? ctx.keys[q0 - 1] : 0ull;
+    c[5] = q0 + 4 < nl ? ctx.qcls[q0 + 4] : 0xFFFFFFFFu;
+    k[5] = q0 + 4 < nl ? ctx.keys[q0 + 4] : 0ull;
+  }
+  // flag of q0 + u, u <= 4 (q0 + u < nl)
+  __device__ __forceinline__ uint32_t flag(uint32_t q0, int u) const {
+    return (q0 + u == 0 || c[u + 1] != c[u] || k[u + 1] != k[u]) ? 1u : 0u;
+  }
+};
 
 __global__ void __launch_bounds__(kBlock) k_live_scan_part(Ctx ctx) {
   const DevState* st = ctx.st;
@@ -223,7 +283,13 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_part(Ctx ctx) {
   uint32_t lo, hi;
   xscan_range(st->nl, blockIdx.x, gridDim.x, &lo, &hi);
   uint32_t s = 0;
-  for (uint32_t q = lo + threadIdx.x; q < hi; q += kBlock) s += live_flag(ctx, q);
+  for (uint32_t q0 = lo + kScanItems * threadIdx.x; q0 < hi; q0 += kScanStep) {
+    FlagWindow w;
+    w.load(ctx, q0, st->nl);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (q0 + u < hi) s += w.flag(q0, u);
+  }
   __shared__ uint32_t sh[kBlock / kWave];
   uint32_t tot;
   block_excl_scan(s, sh, &tot);
@@ -258,20 +324,33 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
   const uint32_t nl = st->nl;
   uint32_t lo, hi;
   xscan_range(nl, blockIdx.x, gridDim.x, &lo, &hi);
-  for (uint32_t base = lo; base < hi; base += kBlock) {
-    const uint32_t q = base + threadIdx.x;
-    const uint32_t f = q < hi ? live_flag(ctx, q) : 0u;
+  for (uint32_t base = lo; base < hi; base += kScanStep) {
+    const uint32_t q0 = base + kScanItems * threadIdx.x;
+    FlagWindow w;
+    uint32_t f[5] = {0, 0, 0, 0, 0}, local = 0;
+    if (q0 < hi) {
+      w.load(ctx, q0, nl);
+#pragma unroll
+      for (int u = 0; u < 5; ++u) f[u] = q0 + u < nl ? w.flag(q0, u) : 0u;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) local += q0 + u < hi ? f[u] : 0u;
+    }
     uint32_t tot;
-    const uint32_t ex = block_excl_scan(f, sh, &tot);
-    if (q < hi) {
-      const uint32_t g = run + ex + f - 1;
+    // sub-class of q0 - 1: the ones of q0 .. q0 + u are added on the way
+    uint32_t g = run + block_excl_scan(local, sh, &tot) - 1;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t q = q0 + u;
+      if (q >= hi) break;
+      g += f[u];
       ctx.ids[q] = g;
-      if (f) {
+      const uint64_t key = w.k[u + 1];
+      if (f[u]) {
         ctx.gstart[g] = q;
-        ctx.gnz[g] = ctx.keys[q] != 0 ? 1 : 0;
+        ctx.gnz[g] = key != 0 ? 1 : 0;
       }
-      if (ctx.keys[q] == 0 && row_nonempty<RP>(ctx, ctx.lperm[q])) ctx.nz0f[g] = 1;
-      if (q + 1 == nl || live_flag(ctx, q + 1)) ctx.gend[g] = q + 1;
+      if (key == 0 && row_nonempty<RP>(ctx, ctx.lperm[q])) ctx.nz0f[g] = 1;
+      if (q + 1 == nl || f[u + 1]) ctx.gend[g] = q + 1;
     }
     run += tot;
   }

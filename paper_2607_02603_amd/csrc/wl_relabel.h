@@ -207,11 +207,20 @@ __global__ void __launch_bounds__(kBlock) k_big_hist(Ctx ctx, int pass) {
     __syncthreads();
     // runs of one digit among a thread's keys are counted in registers and
     // added with one set of atomics (classes with few distinct keys give
-    // long runs; the LDS atomics of a wave would all hit one bucket)
+    // long runs; the LDS atomics of a wave would all hit one bucket).  The
+    // thread's keys of the tile are loaded together first.
+    uint64_t kv[kTilePerThread];
+#pragma unroll
+    for (uint32_t q = 0; q < kTilePerThread; ++q) {
+      const uint32_t p = r.beg + q * kBlock + threadIdx.x;
+      kv[q] = p < r.end ? ctx.keys[p] : 0ull;
+    }
     uint32_t rd = 0xFFFFFFFFu, rc = 0;
     unsigned long long rmn = ~0ull, rmx = 0;
-    for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
-      const uint64_t key = ctx.keys[p];
+#pragma unroll
+    for (uint32_t q = 0; q < kTilePerThread; ++q) {
+      if (r.beg + q * kBlock + threadIdx.x >= r.end) break;
+      const uint64_t key = kv[q];
       const uint32_t d = digit_of(key, pass, ctx.ring);
       if (d != rd) {
         if (rc) {
@@ -369,9 +378,24 @@ __global__ void __launch_bounds__(kBlock) k_big_copyback(Ctx ctx, int pass) {
   for (uint32_t t = blockIdx.x; t < nt; t += gridDim.x) {
     TileRange r = tile_range(ctx, cur, nb, t);
     if (ctx.bsame[r.seg]) continue;
-    for (uint32_t p = r.beg + threadIdx.x; p < r.end; p += kBlock) {
-      ctx.keys[p] = ctx.keys_tmp[p];
-      ctx.perm[p] = ctx.perm_tmp[p];
+    // all loads of the thread's share of the tile before its stores
+    uint64_t kv[kTilePerThread];
+    uint32_t pv[kTilePerThread];
+#pragma unroll
+    for (uint32_t q = 0; q < kTilePerThread; ++q) {
+      const uint32_t p = r.beg + q * kBlock + threadIdx.x;
+      if (p < r.end) {
+        kv[q] = ctx.keys_tmp[p];
+        pv[q] = ctx.perm_tmp[p];
+      }
+    }
+#pragma unroll
+    for (uint32_t q = 0; q < kTilePerThread; ++q) {
+      const uint32_t p = r.beg + q * kBlock + threadIdx.x;
+      if (p < r.end) {
+        ctx.keys[p] = kv[q];
+        ctx.perm[p] = pv[q];
+      }
     }
   }
 }

@@ -376,10 +376,75 @@ __device__ __forceinline__ void spmv_q_body(const Ctx& ctx) {
   }
 }
 
+// The same when no row has more than kShortRow entries (nothing to queue):
+// two rows per thread, rows q and q + kBlock of a 2 * kBlock stretch, their
+// loads issued together so that each wave keeps twice the independent
+// memory chains (row span, columns, colours) in flight.
+template <bool W, int M>
+__device__ __forceinline__ void spmv_q_short_body(const Ctx& ctx) {
+  const DevState* st = ctx.st;
+  const uint64_t rkey = round_key(st->seed, st->round);
+  const uint32_t nl = st->nl;
+  constexpr int R = 2;
+  for (uint32_t q0 = blockIdx.x * (R * kBlock) + threadIdx.x; q0 < nl;
+       q0 += gridDim.x * (R * kBlock)) {
+    uint32_t q[R], len[R];
+    uint64_t beg[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      q[r] = q0 + r * kBlock;
+      const bool in = q[r] < nl;
+      len[r] = in ? ctx.rl[q[r]] : 0u;
+      beg[r] = in ? ctx.rs[q[r]] : 0ull;
+    }
+    Acc96 a[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) a[r] = Acc96{0, 0};
+    const uint32_t most = max(len[0], len[1]);
+    for (uint32_t t0 = 0; t0 < most; t0 += 4) {
+      uint32_t j[R][4];
+      bool ok[R][4];
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          ok[r][u] = t0 + u < len[r];
+          j[r][u] = ok[r][u] ? ctx.col[beg[r] + t0 + u] : 0u;
+        }
+      uint64_t v[R][4];
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          v[r][u] = ok[r][u] ? gather_value<M>(ctx, j[r][u], rkey) : 0ull;
+          if (W && ok[r][u]) v[r][u] = mul_small_q(ctx.wgt[beg[r] + t0 + u], v[r][u], ctx.ring);
+        }
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc_add(a[r], v[r][u]);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (q[r] < nl) ctx.keys[q[r]] = acc_value(a[r], ctx.ring);
+  }
+}
+
+// long_rows = 0: no live row has more than kShortRow entries (the graph's
+// longest row has at most that many).
 template <bool W>
-__global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx) {
+__global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx, int long_rows) {
   if (ctx.st->done) return;
   const int mode = gather_mode(ctx.st->k);
+  if (!long_rows) {
+    if (mode == kGather8)
+      spmv_q_short_body<W, kGather8>(ctx);
+    else if (mode == kGather16)
+      spmv_q_short_body<W, kGather16>(ctx);
+    else
+      spmv_q_short_body<W, kGatherC>(ctx);
+    return;
+  }
   if (mode == kGather8)
     spmv_q_body<W, kGather8>(ctx);
   else if (mode == kGather16)
