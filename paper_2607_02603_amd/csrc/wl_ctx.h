@@ -61,7 +61,6 @@ struct DevState {
   uint32_t deg_nd;      // distinct row lengths (one-colour round)
   uint32_t n_mid;       // live rows queued for one wave each (this round)
   uint32_t n_hlive;     // live heavy rows (this round)
-  uint32_t prep_round;  // the round whose gather tables the round end prepares
   uint32_t n_pico;      // segments of <= kPicoMax nodes (this round)
   uint64_t seed;
   // The two big-segment lists: (entries << 32) | tiles.  One 64-bit atomic
@@ -142,6 +141,8 @@ struct Ctx {
   // share memory with buffers of the full relabel that those rounds do not
   // use (see make_ctx).
   uint32_t* lperm;     // members of the live classes, class after class
+  uint32_t* pos;       // position of every node in lperm, ~0 outside the live
+                       // classes (NULL outside in-core sessions)
   uint32_t* lperm2;
   uint32_t* qcls;      // live class of every position of lperm
   uint32_t* qcls2;

@@ -212,7 +212,6 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
       st->k_new = k_new;
       st->nosplit = k_new == st->k ? 1u : 0u;
       st->split_any = 1u - st->nosplit;
-      st->prep_round = st->round + 1;
     }
   }
   __syncthreads();
@@ -302,8 +301,10 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d, con
     uint32_t b = 0;
     if (live && (int)lane == ldr) b = atomicAdd(&lc[r], (uint32_t)__popcll(peers));
     b = __shfl(b, ldr, kWave);
+    if (!live && ctx.pos) ctx.pos[i] = 0xFFFFFFFFu;
     if (live) {
       const uint32_t q = b + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
+      if (ctx.pos) ctx.pos[i] = q;
       ctx.lperm[q] = i;
       ctx.qcls[q] = d.rj[r];
       ctx.rs[q] = r0;

@@ -88,7 +88,7 @@ struct Layout {
       off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
       off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2],
-      off_rs[2], off_rl[2], off_hq, off_bsame, off_nz0f;
+      off_rs[2], off_rl[2], off_hq, off_bsame, off_nz0f, off_pos;
   uint64_t total;
 };
 
@@ -147,6 +147,7 @@ Layout make_layout(uint64_t n, uint64_t nnz, bool in_core = true) {
   L.off_hq = take(in_core ? 4ull * L.max_heavy : 0);
   L.off_bsame = take(L.max_big + 1);
   L.off_nz0f = take(in_core ? n + 1 : 0);
+  L.off_pos = take(in_core ? 4ull * n : 0);
   L.total = o;
   return L;
 }
@@ -309,7 +310,8 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.hq = (uint32_t*)(ws + L.off_hq);
   c.bsame = ws + L.off_bsame;
   c.nz0f = L.in_core ? ws + L.off_nz0f : nullptr;
-  c.lsplit = c.c8;    // written after the SpMV has read the compact colours
+  c.pos = L.in_core ? (uint32_t*)(ws + L.off_pos) : nullptr;
+  c.lsplit = c.c8;    // the live rounds do not use the compact colours
   c.weighted = g->weight != nullptr;
   {
     const char* nt = getenv("WL_NT_STREAM");
@@ -560,7 +562,6 @@ struct Session {
   // (r - live_r0) & 1 and writes the other; ctx0 has set 0 current.
   Ctx ctx0{};
   uint32_t live_r0 = 0;
-  bool next_async = false;  // the round after this host-driven one is device-driven
   bool hist_clean = false;  // radix histograms cleared (first pass of the call)
   hipStream_t s;
   bool rp64;
@@ -630,10 +631,13 @@ struct Session {
     return WL_OK;
   }
 
+  // Timing-only events: read after a synchronising read-back, so they take
+  // no system-scope fence (whose cache write-back and invalidation would
+  // slow the launches that follow each record).
   hipEvent_t next_event() {
     if (ev_used == ev_pool.size()) {
       hipEvent_t e = nullptr;
-      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
       ev_pool.push_back(e);
     }
     return ev_pool[ev_used++];
@@ -969,20 +973,25 @@ struct Session {
   }
 
   // Gathering image of the live rows; every count comes from the device.
+  // always: a host-driven round (timed on its own).
   template <bool W>
-  // always: a host-driven round, which prepares its gather tables itself; a
-  // device-driven round finds them prepared by the previous round's end.
   void live_gather(uint32_t round, bool always) {
-    const uint32_t gn = grid_for(L.n, kBlock, 4096);
     const uint32_t gl = live_grid();
-    if (always) hipLaunchKernelGGL(k_gather_prep, dim3(gn), dim3(kBlock), 0, s, ctx, -1);
     if (sflags & WL_STATS_WORK)
       hipLaunchKernelGGL(k_live_count, dim3(gl), dim3(kBlock), 0, s, ctx, 1);
     const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
     const int long_rows = live_heavy || host.max_deg > kShortRow;
     timed_spmv(round, always, kImgGather, [&] {
-      hipLaunchKernelGGL(k_spmv_q<W>, dim3(long_rows ? gl : grid_for(host.nl, 2 * kBlock, 4096)),
-                         dim3(kBlock), 0, s, ctx, long_rows);
+      // node order (coalesced rows and colours) where the position map is kept
+      if (ctx.pos && rp64)
+        hipLaunchKernelGGL((k_spmv_node<uint64_t, W>), dim3(grid_for(L.n, kBlock, 4096)),
+                           dim3(kBlock), 0, s, ctx, long_rows);
+      else if (ctx.pos)
+        hipLaunchKernelGGL((k_spmv_node<uint32_t, W>), dim3(grid_for(L.n, kBlock, 4096)),
+                           dim3(kBlock), 0, s, ctx, long_rows);
+      else
+        hipLaunchKernelGGL(k_spmv_q<W>, dim3(long_rows ? gl : grid_for(host.nl, 2 * kBlock, 4096)),
+                           dim3(kBlock), 0, s, ctx, long_rows);
       if (live_heavy) {
         const uint32_t gh = grid_for(host.bin_cnt[3], kBlock, 1024);
         hipLaunchKernelGGL(k_heavy_clear, dim3(gh), dim3(kBlock), 0, s, ctx);
@@ -1134,11 +1143,10 @@ struct Session {
 
   // After the sort: sub-classes, new colours of every node, next live
   // classes, end of the round.
-  // prep: the round end also prepares the next round's gather tables (the
-  // next round is device-driven).  async: a device-driven round, which
-  // launches no kernels for the per-colour shift table; a round that needs
-  // the table halts the device in k_shift_sort (finish_halted builds it).
-  void live_tail(bool prep, bool async = false) {
+  // async: a device-driven round, which launches no kernels for the
+  // per-colour shift table; a round that needs the table halts the device in
+  // k_shift_sort (finish_halted builds it).
+  void live_tail(bool async = false) {
     const uint32_t gl = live_grid(), ns = live_scan_blocks();
     const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
     DevState* st = ctx.st;
@@ -1150,13 +1158,13 @@ struct Session {
     hipLaunchKernelGGL(k_live_subs_splits, dim3(std::max(gl, gc)), dim3(kBlock), 0, s, ctx);
     xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
     hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx, async ? 1 : 0);
-    live_shift_end(prep, !async);
+    live_shift_end(!async);
   }
 
   // The per-colour shift table (when with_table; it is built only if the
   // round's splits need it), the new colour of every node, the next live
   // classes and the end of the round.
-  void live_shift_end(bool prep, bool with_table) {
+  void live_shift_end(bool with_table) {
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
     const uint32_t gl = live_grid();
     const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
@@ -1173,8 +1181,7 @@ struct Session {
       hipLaunchKernelGGL(k_live_emit<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
     else
       hipLaunchKernelGGL(k_live_emit<uint32_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_round_end, dim3(prep ? gn : 1), dim3(kBlock), 0, s, ctx,
-                       prep ? 1 : 0);
+    hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
   }
 
   // The one-colour round of an unweighted graph without a sort
@@ -1216,8 +1223,7 @@ struct Session {
     hipLaunchKernelGGL(k_deg_rowscan, dim3((uint32_t)std::min<uint64_t>(K, 4096)), dim3(kBlock), 0,
                        s, ctx, d, m, nblk);
     hipLaunchKernelGGL(k_deg_place<RP64>, dim3(nblk), dim3(kBlock), 0, s, ctx, d, m);
-    hipLaunchKernelGGL(k_live_round_end, dim3(next_async ? grid_for(L.n, kBlock, 4096) : 1),
-                       dim3(kBlock), 0, s, ctx, next_async ? 1 : 0);
+    hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     *handled = true;
@@ -1242,15 +1248,13 @@ struct Session {
   }
 
   // Builds the live classes into buffer set 0 for the coming round, whose
-  // counters and gather tables it also sets.
+  // counters it also sets.
   int build_live_now() {
     ctx = ctx0;
     if (int r = build_live()) return r;
     live_built = true;
     live_r0 = host.round;
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
-    hipLaunchKernelGGL(k_gather_prep, dim3(grid_for(L.n, kBlock, 4096)), dim3(kBlock), 0, s,
-                       ctx, -1);
     HIP_LAUNCH_CHECK();
     return WL_OK;
   }
@@ -1276,7 +1280,7 @@ struct Session {
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (int r = finish_sort(0, false)) return r;
-    live_tail(next_async);
+    live_tail();
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (host.err & kErrNotSymmetric)
@@ -1291,8 +1295,8 @@ struct Session {
   }
 
   // The same launched without reading anything back: grids are fixed for the
-  // call and counts come from the device state; the per-round counters and
-  // gather tables were set by the previous round's end.  A round that needs
+  // call and counts come from the device state; the per-round counters were
+  // set by the previous round's end.  A round that needs
   // more radix passes than it launches halts the device before its small
   // sorts (finish_halted completes it).
   void round_live_async(uint32_t round) {
@@ -1305,7 +1309,7 @@ struct Session {
     // taken in grid-stride loops
     sorts(grid_for(L.n / 2, kBlock / kWave, 1024), grid_for(L.n / 2, kBlock / 8, 1024),
           grid_for(L.n / (kTinyMax + 1), 1, 1024), ap);
-    live_tail(true, true);
+    live_tail(true);
   }
 
   // The graph of rounds r, r + 1 for a first round of parity p = (r -
@@ -1371,10 +1375,10 @@ struct Session {
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     if (why == kHaltedShift) {
-      live_shift_end(true, true);
+      live_shift_end(true);
     } else {
       if (int r = finish_sort(async_pass_count(), false)) return r;
-      live_tail(true);
+      live_tail();
     }
     HIP_LAUNCH_CHECK();
     return pull();
@@ -1393,6 +1397,10 @@ struct Session {
     }
     if (int r = build_schedule(true)) return r;
     ctx.keys_mat = 1;
+    // The live rows are gathered in node order only when every row is short:
+    // with long rows, node order puts rows of very different lengths in one
+    // wave, while the class order groups rows of equal length.
+    if (host.max_deg > kShortRow) ctx.pos = nullptr;
     ctx0 = ctx;
     // The live classes come from the grouping above, unless the first round
     // is the one-colour degree round, which builds them itself.
@@ -1407,7 +1415,6 @@ struct Session {
     uint32_t host_rounds = 0, ahead = 8;
     while (!host.done) {
       if (host_rounds < host_rounds_first) {
-        next_async = host_rounds + 1 >= host_rounds_first;
         if (int r = round_live()) return r;
         ++host_rounds;
         continue;

@@ -200,10 +200,14 @@ __global__ void __launch_bounds__(kBlock) k_live_build(Ctx ctx) {
   for (uint32_t p = blockIdx.x * kBlock + threadIdx.x; p < ctx.n; p += gridDim.x * kBlock) {
     const uint32_t b = ctx.ids[p], v = ctx.perm[p];
     const bool live = class_live(ctx, b);
-    if (!live) continue;
+    if (!live) {
+      if (ctx.pos) ctx.pos[v] = 0xFFFFFFFFu;
+      continue;
+    }
     const uint64_t r0 = rp[v], r1 = rp[v + 1];
     const uint32_t s = ctx.cstart[b];
     const uint32_t j = ctx.gl[b], q = ctx.go[b] + (p - s);
+    if (ctx.pos) ctx.pos[v] = q;
     ctx.lperm2[q] = v;
     ctx.qcls2[q] = j;
     ctx.rs2[q] = r0;
@@ -298,8 +302,8 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_part(Ctx ctx) {
 
 // Every block: its offset among the block sums and their total, the number
 // of sub-classes of the live classes, nsub (block 0 records it with k_new =
-// k + nsub - n_live, nosplit when no class split, and the round whose
-// gather tables the round end prepares).  Then ids[q] = sub-class of q; per
+// k + nsub - n_live and nosplit when no class split).  Then ids[q] =
+// sub-class of q; per
 // sub-class g: first position, end, and whether it holds a non-empty row:
 // its key is non-zero (gnz), or a member with key 0 has one (its image
 // happens to be 0; nz0f).
@@ -318,7 +322,6 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
     st->nosplit = nsub == nlive ? 1u : 0u;
     st->split_any = nsub == nlive ? 0u : 1u;
     st->shift_big = 0;
-    st->prep_round = st->round + 1;
   }
   if (nsub == nlive) return;
   const uint32_t nl = st->nl;
@@ -592,7 +595,10 @@ __global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
     uint32_t rlen;
     if (ctx.lsplit[j]) {
       ctx.c[v] = id;
-      if (!(len >= 2 && ctx.gnz[g])) continue;
+      if (!(len >= 2 && ctx.gnz[g])) {
+        if (ctx.pos) ctx.pos[v] = 0xFFFFFFFFu;  // its class leaves the live set
+        continue;
+      }
       r0 = rp[v];
       rlen = (uint32_t)(rp[v + 1] - r0);
     } else {
@@ -603,6 +609,7 @@ __global__ void __launch_bounds__(kBlock) k_live_emit(Ctx ctx) {
     }
     const uint32_t jn = ctx.gl[g], off = ctx.go[g];
     const uint32_t q2 = off + (q - gs);
+    if (ctx.pos) ctx.pos[v] = q2;
     ctx.lperm2[q2] = v;
     ctx.qcls2[q2] = jn;
     ctx.rs2[q2] = r0;
@@ -642,20 +649,13 @@ __global__ void k_live_adopt(Ctx ctx) {
   st->nl = st->nl2;
 }
 
-// End of a live round.  Every block prepares the next round's gather tables
-// (prep = 0 when the next round prepares its own; the colours are final
-// here, the next colour count is k_new and the round is prep_round, fields
-// this kernel does not change); block 0 sets the colour count, round
-// counter, termination and new live counts and clears the per-round
-// counters.  No argument depends on the round, so the launch can be
-// replayed.
-__global__ void __launch_bounds__(kBlock) k_live_round_end(Ctx ctx, int prep) {
+// End of a live round (one thread): the colour count, round counter,
+// termination and new live counts; the per-round counters are cleared.  No
+// argument depends on the round, so the launch can be replayed.
+__global__ void k_live_round_end(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done) return;
   const uint32_t kn = st->k_new;
-  if (prep && !st->nosplit)
-    gather_prep_body(ctx, gather_mode(kn), kn, round_key(st->seed, st->prep_round));
-  if (blockIdx.x != 0 || threadIdx.x != 0) return;
   st->round += 1;
   if (st->nosplit) {
     st->done = 1;

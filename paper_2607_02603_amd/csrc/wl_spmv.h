@@ -430,25 +430,77 @@ __device__ __forceinline__ void spmv_q_short_body(const Ctx& ctx) {
   }
 }
 
+// The gathering image of the live rows taken in node order: pos[v] is v's
+// position among the live rows (~0 if none), so consecutive lanes read
+// consecutive rows and, on graphs with locality, nearby colours.  Rows of
+// more than kShortRow entries are queued as in k_spmv_q (long_rows != 0).
+template <typename RP, bool W, int M>
+__device__ __forceinline__ void spmv_node_body(const Ctx& ctx, int long_rows) {
+  DevState* st = ctx.st;
+  const uint64_t rkey = round_key(st->seed, st->round);
+  const RP* rp = rowptr<RP>(ctx);
+  const uint32_t n = ctx.n;
+  __shared__ uint32_t sh[kBlock / kWave];
+  __shared__ uint32_t base_sh;
+  for (uint32_t v0 = blockIdx.x * kBlock; v0 < n; v0 += gridDim.x * kBlock) {
+    const uint32_t v = v0 + threadIdx.x;
+    uint32_t q = 0xFFFFFFFFu, len = 0;
+    uint64_t beg = 0;
+    if (v < n) {
+      q = ctx.pos[v];
+      if (q != 0xFFFFFFFFu) {
+        beg = rp[v];
+        len = (uint32_t)(rp[v + 1] - beg);
+      }
+    }
+    bool mid = false, heavy = false;
+    if (long_rows) {  // uniform
+      heavy = len > kHeavyChunk;
+      mid = len > kShortRow && !heavy;
+      const uint32_t am = block_append(mid, &st->n_mid, sh, &base_sh);
+      if (mid) ctx.midq[am] = q;
+      const uint32_t ah = block_append(heavy, &st->n_hlive, sh, &base_sh);
+      if (heavy) ctx.hq[ah] = q;
+    }
+    if (q == 0xFFFFFFFFu || mid || heavy) continue;
+    Acc96 a{0, 0};
+    for (uint32_t t0 = 0; t0 < len; t0 += 4) {
+      uint32_t j[4];
+      bool ok[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        ok[u] = t0 + u < len;
+        j[u] = ok[u] ? ctx.col[beg + t0 + u] : 0u;
+      }
+      uint64_t val[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        val[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
+        if (W && ok[u]) val[u] = mul_small_q(ctx.wgt[beg + t0 + u], val[u], ctx.ring);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc_add(a, val[u]);
+    }
+    ctx.keys[q] = acc_value(a, ctx.ring);
+  }
+}
+
+template <typename RP, bool W>
+__global__ void __launch_bounds__(kBlock) k_spmv_node(Ctx ctx, int long_rows) {
+  if (ctx.st->done) return;
+  spmv_node_body<RP, W, kGatherC>(ctx, long_rows);
+}
+
 // long_rows = 0: no live row has more than kShortRow entries (the graph's
 // longest row has at most that many).
+// The live rounds compute every neighbour's value from its colour
+// (kGatherC): the compact colour tables would cost a pass over all n
+// colours per round, and their lookups are random reads.
 template <bool W>
 __global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx, int long_rows) {
   if (ctx.st->done) return;
-  const int mode = gather_mode(ctx.st->k);
-  if (!long_rows) {
-    if (mode == kGather8)
-      spmv_q_short_body<W, kGather8>(ctx);
-    else if (mode == kGather16)
-      spmv_q_short_body<W, kGather16>(ctx);
-    else
-      spmv_q_short_body<W, kGatherC>(ctx);
-    return;
-  }
-  if (mode == kGather8)
-    spmv_q_body<W, kGather8>(ctx);
-  else if (mode == kGather16)
-    spmv_q_body<W, kGather16>(ctx);
+  if (!long_rows)
+    spmv_q_short_body<W, kGatherC>(ctx);
   else
     spmv_q_body<W, kGatherC>(ctx);
 }
@@ -480,13 +532,7 @@ __device__ __forceinline__ void spmv_mid_body(const Ctx& ctx, uint32_t heavy) {
 template <bool W>
 __global__ void __launch_bounds__(kBlock) k_spmv_mid(Ctx ctx, uint32_t heavy) {
   if (ctx.st->done) return;
-  const int mode = gather_mode(ctx.st->k);
-  if (mode == kGather8)
-    spmv_mid_body<W, kGather8>(ctx, heavy);
-  else if (mode == kGather16)
-    spmv_mid_body<W, kGather16>(ctx, heavy);
-  else
-    spmv_mid_body<W, kGatherC>(ctx, heavy);
+  spmv_mid_body<W, kGatherC>(ctx, heavy);
 }
 
 // act of the heavy rows for the static chunks: 0 for every heavy row, then 1
