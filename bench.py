@@ -480,6 +480,17 @@ def main():
         log(f"step {i}: {times[-1] * 1e3:.2f} ms colours={k} rounds={rounds} image ms: "
             + ", ".join(f"{kd} {st[kd]['ms']:.2f} ({st[kd]['launches']})" for kd in KINDS))
     wl.wl_stats_enable(0)
+    # the same calls without the per-launch events: each event record is one
+    # more queue packet (a few microseconds), which shows on workloads with
+    # hundreds of rounds
+    plain = []
+    for i in range(args.steps):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        wl.wl_stable_coloring(dg, None, 0, 0, colors, ws)
+        torch.cuda.synchronize()
+        plain.append(time.perf_counter() - t1)
+    log(f"without image timing events: {sum(plain) / len(plain) * 1e3:.2f} ms per call")
     step_s = sum(times) / len(times)
     gteps = dg.nnz * rounds / step_s / 1e9
     rp_bytes = 8 if dg.row_ptr.dtype == torch.int64 else 4
@@ -509,6 +520,7 @@ def main():
                    "arithmetic": ARITH[args.arith][1],
                    "nnz": dg.nnz, "colours": k, "rounds": rounds,
                    "time_to_stable_ms": step_s * 1e3,
+                   "time_to_stable_ms_without_image_events": sum(plain) / len(plain) * 1e3,
                    "image_ms_per_step": {kd: sum(m[kd] for m in kind_ms) / len(kind_ms)
                                          for kd in KINDS},
                    "active_entries_per_step": active,

@@ -79,6 +79,95 @@ __device__ __forceinline__ uint32_t block_part_prefix(const uint32_t* p, uint32_
   return tb;
 }
 
+// Chained scan (decoupled look-back) over chunks handed out in ticket order:
+// chunk c publishes its total, then its inclusive prefix, in desc[c]; chunk
+// c + 1 adds totals walking back until it finds an inclusive prefix.  A
+// descriptor packs an epoch (bits 63..34: the round and the scan site, so
+// words left by an earlier scan read as not ready), a state (bits 33..32:
+// 1 total, 2 inclusive prefix) and the 32-bit value, so relaxed agent-scope
+// atomics carry everything a reader needs and no fence is issued.  Chunks
+// are taken by ticket (an atomic counter), so every chunk a block waits for
+// belongs to a block that is already running: the walk ends.  A wait longer
+// than kChainSpins polls (far beyond any real one) sets kErrChain and gives
+// up, so a kernel never hangs.
+constexpr uint32_t kErrChain = 64u;  // DevState::err bit
+constexpr uint32_t kChainSpins = 1u << 22;
+constexpr int kChainSplits = 0, kChainFlags = 1, kChainA = 2, kChainB = 3;  // sites
+
+__device__ __forceinline__ uint32_t chain_epoch(uint32_t round, int site) {
+  return (round * 4u + (uint32_t)site) & 0x3FFFFFFFu;
+}
+
+// Every thread of the block calls it with the same c and total; returns the
+// exclusive prefix of chunk c.  The first wave walks back kWave descriptors
+// per poll (lane l reads chunk p - l).  Contains __syncthreads().
+__device__ __forceinline__ uint32_t chain_prefix(unsigned long long* desc, uint32_t c,
+                                                 uint32_t total, uint32_t epoch,
+                                                 uint32_t* err, uint32_t* sh1) {
+  if (threadIdx.x < kWave) {
+    const int lane = (int)threadIdx.x;
+    const unsigned long long tag = (unsigned long long)epoch << 34;
+    uint32_t excl = 0;
+    if (c > 0) {
+      if (lane == 0)
+        __hip_atomic_store(&desc[c], tag | (1ull << 32) | total, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      int64_t p = (int64_t)c - 1;
+      uint32_t spins = 0;
+      while (true) {
+        const int64_t idx = p - lane;
+        // before chunk 0: an inclusive prefix of 0 (chunk 0 itself only ever
+        // publishes its inclusive prefix, so the walk stops there first)
+        uint32_t state = 2, val = 0;
+        if (idx >= 0) {
+          const unsigned long long d =
+              __hip_atomic_load(&desc[idx], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          state = (uint32_t)(d >> 34) == epoch ? (uint32_t)(d >> 32) & 3u : 0u;
+          val = (uint32_t)d;
+        }
+        const unsigned long long inc = __ballot(state == 2);
+        const unsigned long long wait = __ballot(state == 0);
+        // lanes up to the nearest inclusive prefix (all lanes if none) must be ready
+        const int first = inc ? __ffsll((long long)inc) - 1 : kWave;
+        const unsigned long long need = first >= kWave - 1 ? ~0ull : (2ull << first) - 1;
+        if (wait & need) {
+          if (++spins > kChainSpins) {
+            if (lane == 0) atomicOr(err, kErrChain);
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+          continue;
+        }
+        uint32_t v = lane <= first ? val : 0u;
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
+        excl += v;
+        if (first < kWave) break;
+        p -= kWave;
+      }
+    }
+    if (lane == 0) {
+      __hip_atomic_store(&desc[c], tag | (2ull << 32) | (excl + total), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      *sh1 = excl;
+    }
+  }
+  __syncthreads();
+  const uint32_t r = *sh1;
+  __syncthreads();
+  return r;
+}
+
+// Next chunk ticket of a chained scan for the whole block.  Contains
+// __syncthreads().
+__device__ __forceinline__ uint32_t chain_ticket(uint32_t* counter, uint32_t* sh1) {
+  if (threadIdx.x == 0) *sh1 = atomicAdd(counter, 1u);
+  __syncthreads();
+  const uint32_t t = *sh1;
+  __syncthreads();
+  return t;
+}
+
 // Appends 'want' items to a device list: one atomic per block, slots
 // handed out by a block scan (order inside the list is irrelevant).
 // Contains __syncthreads(); every thread of the block must call it.

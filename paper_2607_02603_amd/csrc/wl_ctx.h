@@ -62,6 +62,7 @@ struct DevState {
   uint32_t n_mid;       // live rows queued for one wave each (this round)
   uint32_t n_hlive;     // live heavy rows (this round)
   uint32_t n_pico;      // segments of <= kPicoMax nodes (this round)
+  uint32_t tickets[4];  // chunk tickets of this round's chained scans (per site)
   uint64_t seed;
   // The two big-segment lists: (entries << 32) | tiles.  One 64-bit atomic
   // appends a segment and reserves its tiles, so the tile offsets come out
@@ -167,6 +168,9 @@ struct Ctx {
   uint32_t* hq;        // positions with heavy rows (this round)
   uint8_t* lsplit;     // per live class: 1 if it split in this round
   uint8_t* bsame;      // per big segment of a radix pass: 1 if all its keys are equal
+  unsigned long long* desc;  // chained-scan descriptors, 2 * desc_cap (NULL outside
+                             // in-core sessions); cleared at the start of a call
+  uint32_t desc_cap;
   uint8_t* nz0f;       // per sub-class: a member with key 0 has a non-empty row
                        // (set by k_live_scan_final, consumed and cleared by
                        // k_live_subs_splits; NULL outside in-core sessions)

@@ -88,7 +88,8 @@ struct Layout {
       off_ids, off_cstart, off_flags, off_act, off_small, off_tiny, off_big0, off_big1,
       off_tile, off_bhist, off_bmin, off_bmax, off_bcur, off_scan, off_rows,
       off_binpart, off_chunks, off_hacc, off_hcnt, off_wtab, off_c16, off_qcls2, off_lcls[2],
-      off_rs[2], off_rl[2], off_hq, off_bsame, off_nz0f, off_pos;
+      off_rs[2], off_rl[2], off_hq, off_bsame, off_nz0f, off_pos, off_desc;
+  uint32_t desc_cap;  // chunks of a chained scan (kBlock live classes, or more items)
   uint64_t total;
 };
 
@@ -148,6 +149,8 @@ Layout make_layout(uint64_t n, uint64_t nnz, bool in_core = true) {
   L.off_bsame = take(L.max_big + 1);
   L.off_nz0f = take(in_core ? n + 1 : 0);
   L.off_pos = take(in_core ? 4ull * n : 0);
+  L.desc_cap = (uint32_t)(n / kBlock + 2);
+  L.off_desc = take(in_core ? 16ull * L.desc_cap : 0);
   L.total = o;
   return L;
 }
@@ -311,6 +314,8 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.bsame = ws + L.off_bsame;
   c.nz0f = L.in_core ? ws + L.off_nz0f : nullptr;
   c.pos = L.in_core ? (uint32_t*)(ws + L.off_pos) : nullptr;
+  c.desc = L.in_core ? (unsigned long long*)(ws + L.off_desc) : nullptr;
+  c.desc_cap = L.desc_cap;
   c.lsplit = c.c8;    // the live rounds do not use the compact colours
   c.weighted = g->weight != nullptr;
   {
@@ -470,6 +475,12 @@ __global__ void __launch_bounds__(kBlock) k_iota_zero(Ctx ctx) {
     ctx.act[i] = ctx.n >= 2 ? 1 : 0;
     if (ctx.nz0f) ctx.nz0f[i] = 0;
   }
+  // chained-scan descriptors: nothing left from an earlier call may read as
+  // ready (their epochs restart with the rounds)
+  if (ctx.desc)
+    for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < 2 * ctx.desc_cap;
+         i += gridDim.x * kBlock)
+      ctx.desc[i] = 0;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctx.cstart[0] = 0;
     ctx.cstart[1] = ctx.n;
@@ -1145,7 +1156,7 @@ struct Session {
   // classes, end of the round.
   // async: a device-driven round, which launches no kernels for the
   // per-colour shift table; a round that needs the table halts the device in
-  // k_shift_sort (finish_halted builds it).
+  // k_shift_apply (finish_halted builds it).
   void live_tail(bool async = false) {
     const uint32_t gl = live_grid(), ns = live_scan_blocks();
     const uint32_t gc = grid_for(host.n_live, kBlock, 4096);
@@ -1157,7 +1168,6 @@ struct Session {
       hipLaunchKernelGGL(k_live_scan_final<uint32_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
     hipLaunchKernelGGL(k_live_subs_splits, dim3(std::max(gl, gc)), dim3(kBlock), 0, s, ctx);
     xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
-    hipLaunchKernelGGL(k_shift_sort, dim3(1), dim3(kShiftThreads), 0, s, ctx, async ? 1 : 0);
     live_shift_end(!async);
   }
 
@@ -1176,7 +1186,7 @@ struct Session {
     }
     // each block loads the split list into LDS: a capped grid loads it fewer times
     hipLaunchKernelGGL(k_shift_apply, dim3(std::min<uint32_t>(gn, 1024)), dim3(kBlock), 0, s,
-                       ctx);
+                       ctx, with_table ? 0 : 1);
     if (rp64)
       hipLaunchKernelGGL(k_live_emit<uint64_t>, dim3(gl), dim3(kBlock), 0, s, ctx);
     else
@@ -1285,6 +1295,7 @@ struct Session {
     if (int r = pull()) return r;
     if (host.err & kErrNotSymmetric)
       return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
+    if (host.err & kErrChain) return fail(WL_EHIP, "a chained scan did not complete");
     return WL_OK;
   }
 
@@ -1427,6 +1438,7 @@ struct Session {
         if (int r = finish_halted()) return r;
       if (host.err & kErrNotSymmetric)
         return fail(WL_EINVAL, "the graph is flagged symmetric but is not");
+      if (host.err & kErrChain) return fail(WL_EHIP, "a chained scan did not complete");
       ahead = std::min<uint32_t>(ahead * 2, 64);
     }
     return WL_OK;

@@ -361,7 +361,10 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
 
 // The live sub-classes (gl[g] = 1, go[g] = size; scanned next), with the
 // key-0 flags folded into gnz; and the classes that split: (old colour,
-// extra sub-classes), in any order.
+// extra sub-classes) in colour order (the live classes are in colour order,
+// and each chunk of kBlock of them finds its place in the list by a chained
+// scan of the chunks' split counts).  The block of the last chunk records
+// the number of splits and whether they need the per-colour shift table.
 __global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx) {
   DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
@@ -380,90 +383,34 @@ __global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx) {
     ctx.go[g] = live ? len : 0u;
   }
   __shared__ uint32_t sh[kBlock / kWave];
-  __shared__ uint32_t base_sh;
+  __shared__ uint32_t sh1;
   const uint32_t nlive = st->n_live;
-  for (uint32_t j0 = blockIdx.x * kBlock; j0 < nlive; j0 += stride) {
-    const uint32_t j = j0 + threadIdx.x;
+  const uint32_t nchunks = (nlive + kBlock - 1) / kBlock;
+  const uint32_t epoch = chain_epoch(st->round, kChainSplits);
+  // the first min(grid, nchunks) blocks take the chunks by ticket: one
+  // ticket each when the grid covers them, so that no more atomics than
+  // chunks hit the counter
+  if (blockIdx.x >= nchunks) return;
+  const bool one = gridDim.x >= nchunks;
+  for (bool first = true; first || !one; first = false) {
+    const uint32_t c = chain_ticket(&st->tickets[kChainSplits], &sh1);
+    if (c >= nchunks) break;
+    const uint32_t j = c * kBlock + threadIdx.x;
     uint32_t extra = 0;
     if (j < nlive) {
       const uint32_t s = ctx.loff[j];
       extra = ctx.ids[s + ctx.llen[j] - 1] - ctx.ids[s];
     }
-    const uint32_t at = block_append(extra > 0, &st->n_split, sh, &base_sh);
-    if (extra > 0) ctx.split[at] = make_uint2(ctx.lcold[j], extra);
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan(extra > 0 ? 1u : 0u, sh, &tot);
+    const uint32_t base = chain_prefix(ctx.desc, c, tot, epoch, &st->err, &sh1);
+    if (extra > 0) ctx.split[base + ex] = make_uint2(ctx.lcold[j], extra);
     if (j < nlive) ctx.lsplit[j] = extra > 0 ? 1 : 0;
-  }
-}
-
-// One block of 1024 threads: with at most kShiftLds splits, sort them by old
-// colour and replace the extras by their inclusive prefix sums.  With more,
-// the shift table is needed: halt != 0 (a device-driven round, which does
-// not launch the table's kernels) halts the device for the host to build it.
-constexpr int kShiftThreads = 1024;
-__global__ void __launch_bounds__(kShiftThreads) k_shift_sort(Ctx ctx, int halt) {
-  DevState* st = ctx.st;
-  if (st->done || st->nosplit) return;
-  const uint32_t S = st->n_split;
-  if (S > kShiftLds) {
-    if (threadIdx.x == 0) {
-      ctx.st->shift_big = 1;
-      if (halt) ctx.st->done = kHaltedShift;
-    }
-    return;
-  }
-  if (S == 0) return;
-  __shared__ uint32_t key[kShiftLds];
-  __shared__ uint32_t val[kShiftLds];
-  __shared__ uint32_t wsum[kShiftThreads / kWave];
-  uint32_t P = 1;
-  while (P < S) P <<= 1;
-  for (uint32_t t = threadIdx.x; t < P; t += kShiftThreads) {
-    if (t < S) {
-      const uint2 e = ctx.split[t];
-      key[t] = e.x;
-      val[t] = e.y;
-    } else {
-      key[t] = 0xFFFFFFFFu;
-      val[t] = 0;
+    if (c == nchunks - 1 && threadIdx.x == 0) {
+      st->n_split = base + tot;
+      st->shift_big = base + tot > kShiftLds ? 1u : 0u;
     }
   }
-  __syncthreads();
-  for (uint32_t kk = 2; kk <= P; kk <<= 1)
-    for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
-      for (uint32_t i = threadIdx.x; i < P; i += kShiftThreads) {
-        const uint32_t l = i ^ j;
-        if (l > i) {
-          const bool asc = (i & kk) == 0;
-          const uint32_t a = key[i], b = key[l];
-          if ((a > b) == asc) {
-            key[i] = b;
-            key[l] = a;
-            const uint32_t tv = val[i];
-            val[i] = val[l];
-            val[l] = tv;
-          }
-        }
-      }
-      __syncthreads();
-    }
-  // inclusive scan of val[0..S): each thread owns a run of consecutive items
-  constexpr uint32_t kPer = kShiftLds / kShiftThreads;
-  const uint32_t t0 = threadIdx.x * kPer;
-  uint32_t loc = 0;
-#pragma unroll
-  for (uint32_t u = 0; u < kPer; ++u) loc += (t0 + u < S) ? val[t0 + u] : 0u;
-  const int lane = lane_id(), wid = threadIdx.x / kWave;
-  const uint32_t inc = wave_incl_scan(loc);
-  if (lane == kWave - 1) wsum[wid] = inc;
-  __syncthreads();
-  uint32_t run = inc - loc;
-  for (int w = 0; w < wid; ++w) run += wsum[w];
-#pragma unroll
-  for (uint32_t u = 0; u < kPer; ++u)
-    if (t0 + u < S) {
-      run += val[t0 + u];
-      ctx.split[t0 + u] = make_uint2(key[t0 + u], run);
-    }
 }
 
 // More than kShiftLds splits: shift table over all colours, shift[b] =
@@ -508,25 +455,52 @@ __device__ __forceinline__ uint32_t shift_lds(const uint32_t* scol, const uint32
   return scum[l];
 }
 
-__global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx) {
-  const DevState* st = ctx.st;
+// halt != 0 (a device-driven round, which launched no kernels for the
+// shift table): splits that need the table halt the device instead, for the
+// host to build it and finish the round.
+__global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx, int halt) {
+  DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
   const uint32_t S = st->n_split;
   const uint32_t n = ctx.n;
   const bool big = st->shift_big != 0;
+  if (big && halt) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->done = kHaltedShift;
+    return;
+  }
   __shared__ uint32_t scol[kShiftLds];
   __shared__ uint32_t scum[kShiftLds];
   __shared__ uint32_t bidx[kShiftBuckets + 1];
+  __shared__ uint32_t sh[kBlock / kWave];
   // every colour is below k: (k - 1) >> bsh < kShiftBuckets
   uint32_t bsh = 0;
   while (((st->k - 1) >> bsh) >= kShiftBuckets) ++bsh;
   const bool direct = S <= kShiftDirect;
   if (!big) {
-    for (uint32_t t = threadIdx.x; t < S; t += kBlock) {
-      const uint2 e = ctx.split[t];
-      scol[t] = e.x;
-      scum[t] = e.y;
+    // the split list (S >= 1 when a class split), in colour order, with the
+    // extras replaced by their inclusive prefix sums: each thread takes
+    // kPer consecutive entries
+    constexpr uint32_t kPer = kShiftLds / kBlock;
+    const uint32_t t0 = threadIdx.x * kPer;
+    uint32_t v[kPer], loc = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u) {
+      v[u] = 0;
+      if (t0 + u < S) {
+        const uint2 e = ctx.split[t0 + u];
+        scol[t0 + u] = e.x;
+        v[u] = e.y;
+      }
+      loc += v[u];
     }
+    uint32_t tot;
+    uint32_t run = block_excl_scan(loc, sh, &tot);
+#pragma unroll
+    for (uint32_t u = 0; u < kPer; ++u)
+      if (t0 + u < S) {
+        run += v[u];
+        scum[t0 + u] = run;
+      }
     __syncthreads();
     for (uint32_t t = threadIdx.x; !direct && t <= kShiftBuckets; t += kBlock) {
       const uint64_t v = (uint64_t)t << bsh;
@@ -670,6 +644,7 @@ __global__ void k_live_round_end(Ctx ctx) {
   st->n_pico = 0;
   st->big[0] = 0;
   st->big[1] = 0;
+  for (int i = 0; i < 4; ++i) st->tickets[i] = 0;
   st->act_entries = 0;
   st->n_split = 0;
   st->n_mid = 0;

@@ -44,6 +44,7 @@ __global__ void k_round_begin(Ctx ctx) {
   st->n_pico = 0;
   st->big[0] = 0;
   st->big[1] = 0;
+  for (int i = 0; i < 4; ++i) st->tickets[i] = 0;
   st->act_entries = 0;
   st->n_split = 0;
   st->n_mid = 0;
