@@ -993,22 +993,22 @@ struct Session {
     const uint32_t mid = std::min(live_mid, grid_for(host.nl, kBlock / kWave, 2048));
     const int long_rows = live_heavy || host.max_deg > kShortRow;
     timed_spmv(round, always, kImgGather, [&] {
-      // node order (coalesced rows and colours) where the position map is kept
+      // node order (coalesced rows and colours) where the position map is kept:
+      // only graphs without long rows keep it
       if (ctx.pos && rp64)
         hipLaunchKernelGGL((k_spmv_node<uint64_t, W>), dim3(grid_for(L.n, kBlock, 4096)),
-                           dim3(kBlock), 0, s, ctx, long_rows);
+                           dim3(kBlock), 0, s, ctx);
       else if (ctx.pos)
         hipLaunchKernelGGL((k_spmv_node<uint32_t, W>), dim3(grid_for(L.n, kBlock, 4096)),
-                           dim3(kBlock), 0, s, ctx, long_rows);
+                           dim3(kBlock), 0, s, ctx);
       else
-        hipLaunchKernelGGL(k_spmv_q<W>, dim3(long_rows ? gl : grid_for(host.nl, 2 * kBlock, 4096)),
-                           dim3(kBlock), 0, s, ctx, long_rows);
+        hipLaunchKernelGGL(k_spmv_q<W>, dim3(gl), dim3(kBlock), 0, s, ctx);
       if (live_heavy) {
         const uint32_t gh = grid_for(host.bin_cnt[3], kBlock, 1024);
         hipLaunchKernelGGL(k_heavy_clear, dim3(gh), dim3(kBlock), 0, s, ctx);
         hipLaunchKernelGGL(k_heavy_set, dim3(gh), dim3(kBlock), 0, s, ctx);
       }
-      // rows of at most kShortRow entries are done by k_spmv_q alone
+      // rows of at most kShortRow entries are done by the first launch alone
       if (long_rows)
         hipLaunchKernelGGL(k_spmv_mid<W>, dim3(live_heavy + mid), dim3(kBlock), 0, s, ctx,
                            live_heavy);

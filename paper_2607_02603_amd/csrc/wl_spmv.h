@@ -376,93 +376,23 @@ __device__ __forceinline__ void spmv_q_body(const Ctx& ctx) {
   }
 }
 
-// The same when no row has more than kShortRow entries (nothing to queue):
-// two rows per thread, rows q and q + kBlock of a 2 * kBlock stretch, their
-// loads issued together so that each wave keeps twice the independent
-// memory chains (row span, columns, colours) in flight.
-template <bool W, int M>
-__device__ __forceinline__ void spmv_q_short_body(const Ctx& ctx) {
+// The gathering image of the live rows taken in node order, for graphs
+// whose rows have at most kShortRow entries (one lane per row, nothing to
+// queue): pos[v] is v's position among the live rows (~0 if none), so
+// consecutive lanes read consecutive rows and, on graphs with locality,
+// nearby colours.
+template <typename RP, bool W>
+__global__ void __launch_bounds__(kBlock) k_spmv_node(Ctx ctx) {
   const DevState* st = ctx.st;
-  const uint64_t rkey = round_key(st->seed, st->round);
-  const uint32_t nl = st->nl;
-  constexpr int R = 2;
-  for (uint32_t q0 = blockIdx.x * (R * kBlock) + threadIdx.x; q0 < nl;
-       q0 += gridDim.x * (R * kBlock)) {
-    uint32_t q[R], len[R];
-    uint64_t beg[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      q[r] = q0 + r * kBlock;
-      const bool in = q[r] < nl;
-      len[r] = in ? ctx.rl[q[r]] : 0u;
-      beg[r] = in ? ctx.rs[q[r]] : 0ull;
-    }
-    Acc96 a[R];
-#pragma unroll
-    for (int r = 0; r < R; ++r) a[r] = Acc96{0, 0};
-    const uint32_t most = max(len[0], len[1]);
-    for (uint32_t t0 = 0; t0 < most; t0 += 4) {
-      uint32_t j[R][4];
-      bool ok[R][4];
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          ok[r][u] = t0 + u < len[r];
-          j[r][u] = ok[r][u] ? ctx.col[beg[r] + t0 + u] : 0u;
-        }
-      uint64_t v[R][4];
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          v[r][u] = ok[r][u] ? gather_value<M>(ctx, j[r][u], rkey) : 0ull;
-          if (W && ok[r][u]) v[r][u] = mul_small_q(ctx.wgt[beg[r] + t0 + u], v[r][u], ctx.ring);
-        }
-#pragma unroll
-      for (int r = 0; r < R; ++r)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) acc_add(a[r], v[r][u]);
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-      if (q[r] < nl) ctx.keys[q[r]] = acc_value(a[r], ctx.ring);
-  }
-}
-
-// The gathering image of the live rows taken in node order: pos[v] is v's
-// position among the live rows (~0 if none), so consecutive lanes read
-// consecutive rows and, on graphs with locality, nearby colours.  Rows of
-// more than kShortRow entries are queued as in k_spmv_q (long_rows != 0).
-template <typename RP, bool W, int M>
-__device__ __forceinline__ void spmv_node_body(const Ctx& ctx, int long_rows) {
-  DevState* st = ctx.st;
+  if (st->done) return;
   const uint64_t rkey = round_key(st->seed, st->round);
   const RP* rp = rowptr<RP>(ctx);
   const uint32_t n = ctx.n;
-  __shared__ uint32_t sh[kBlock / kWave];
-  __shared__ uint32_t base_sh;
-  for (uint32_t v0 = blockIdx.x * kBlock; v0 < n; v0 += gridDim.x * kBlock) {
-    const uint32_t v = v0 + threadIdx.x;
-    uint32_t q = 0xFFFFFFFFu, len = 0;
-    uint64_t beg = 0;
-    if (v < n) {
-      q = ctx.pos[v];
-      if (q != 0xFFFFFFFFu) {
-        beg = rp[v];
-        len = (uint32_t)(rp[v + 1] - beg);
-      }
-    }
-    bool mid = false, heavy = false;
-    if (long_rows) {  // uniform
-      heavy = len > kHeavyChunk;
-      mid = len > kShortRow && !heavy;
-      const uint32_t am = block_append(mid, &st->n_mid, sh, &base_sh);
-      if (mid) ctx.midq[am] = q;
-      const uint32_t ah = block_append(heavy, &st->n_hlive, sh, &base_sh);
-      if (heavy) ctx.hq[ah] = q;
-    }
-    if (q == 0xFFFFFFFFu || mid || heavy) continue;
+  for (uint32_t v = blockIdx.x * kBlock + threadIdx.x; v < n; v += gridDim.x * kBlock) {
+    const uint32_t q = ctx.pos[v];
+    if (q == 0xFFFFFFFFu) continue;
+    const uint64_t beg = rp[v];
+    const uint32_t len = (uint32_t)(rp[v + 1] - beg);
     Acc96 a{0, 0};
     for (uint32_t t0 = 0; t0 < len; t0 += 4) {
       uint32_t j[4];
@@ -475,7 +405,7 @@ __device__ __forceinline__ void spmv_node_body(const Ctx& ctx, int long_rows) {
       uint64_t val[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        val[u] = ok[u] ? gather_value<M>(ctx, j[u], rkey) : 0ull;
+        val[u] = ok[u] ? gather_value<kGatherC>(ctx, j[u], rkey) : 0ull;
         if (W && ok[u]) val[u] = mul_small_q(ctx.wgt[beg + t0 + u], val[u], ctx.ring);
       }
 #pragma unroll
@@ -485,24 +415,13 @@ __device__ __forceinline__ void spmv_node_body(const Ctx& ctx, int long_rows) {
   }
 }
 
-template <typename RP, bool W>
-__global__ void __launch_bounds__(kBlock) k_spmv_node(Ctx ctx, int long_rows) {
-  if (ctx.st->done) return;
-  spmv_node_body<RP, W, kGatherC>(ctx, long_rows);
-}
-
-// long_rows = 0: no live row has more than kShortRow entries (the graph's
-// longest row has at most that many).
 // The live rounds compute every neighbour's value from its colour
 // (kGatherC): the compact colour tables would cost a pass over all n
 // colours per round, and their lookups are random reads.
 template <bool W>
-__global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx, int long_rows) {
+__global__ void __launch_bounds__(kBlock) k_spmv_q(Ctx ctx) {
   if (ctx.st->done) return;
-  if (!long_rows)
-    spmv_q_short_body<W, kGatherC>(ctx);
-  else
-    spmv_q_body<W, kGatherC>(ctx);
+  spmv_q_body<W, kGatherC>(ctx);
 }
 
 // Blocks [0, heavy): the static heavy chunks (rows whose act flag is set by
