@@ -440,6 +440,19 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
     const bool mat = (sg.y & kMatBit) != 0;
     uint32_t P = 2;
     while (P < len) P <<= 1;
+    // the segment into LDS; the flags and the bucket counts of the counting
+    // sort below are cleared on the way (nothing reads them before the
+    // barrier)
+    if (threadIdx.x == 0) {
+      differ = 0;
+      unsorted = 0;
+      xo = 0;
+      fallback = 0;
+    }
+    for (uint32_t b = threadIdx.x; b < kCsBuckets; b += kBlock) {
+      cnt[b] = 0;
+      mixed[b] = 0;
+    }
     for (uint32_t t = threadIdx.x; t < P; t += kBlock) {
       if (t < len) {
         const uint32_t v = ctx.perm[s + t];
@@ -452,18 +465,27 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
     }
     __syncthreads();
     // all images equal: nothing splits, nothing to reorder; already in
-    // order (the rows of a quotient): only the flags
-    if (threadIdx.x == 0) {
-      differ = 0;
-      unsorted = 0;
+    // order (the rows of a quotient): only the flags.  The same pass ORs the
+    // differences to the first key (the highest differing bit, below).
+    {
+      unsigned long long x = 0;
+      bool uns = false;
+      for (uint32_t t = threadIdx.x; t < len; t += kBlock) {
+        x |= skey[t] ^ skey[0];
+        uns = uns || (t + 1 < len && key_less<TIE>(skey[t + 1], sval[t + 1], skey[t], sval[t]));
+      }
+      if (x) {
+        differ = 1;
+        atomicOr(&xo, x);
+      }
+      if (uns) unsorted = 1;
     }
     __syncthreads();
-    for (uint32_t t = threadIdx.x; t < len; t += kBlock) {
-      if (skey[t] != skey[0]) differ = 1;
-      if (t + 1 < len && key_less<TIE>(skey[t + 1], sval[t + 1], skey[t], sval[t])) unsorted = 1;
+    if (!differ) {
+      // every thread has read the flag before the next segment clears it
+      __syncthreads();
+      continue;
     }
-    __syncthreads();
-    if (!differ) continue;
     if (!unsorted) {
       for (uint32_t t = threadIdx.x + 1; t < len; t += kBlock)
         if (skey[t] != skey[t - 1]) ctx.flags[s + t] = 1;
@@ -475,21 +497,6 @@ __device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, ui
     // element); then a bucket whose keys are not all equal is sorted by
     // insertion when it holds at most ctx.cs_fix keys, and a larger one sends the
     // segment to the sorting network below.
-    if (threadIdx.x == 0) {
-      xo = 0;
-      fallback = 0;
-    }
-    for (uint32_t b = threadIdx.x; b < kCsBuckets; b += kBlock) {
-      cnt[b] = 0;
-      mixed[b] = 0;
-    }
-    __syncthreads();
-    {
-      unsigned long long x = 0;
-      for (uint32_t t = threadIdx.x; t < len; t += kBlock) x |= skey[t] ^ skey[0];
-      if (x) atomicOr(&xo, x);
-    }
-    __syncthreads();
     const int top = 63 - __clzll((long long)xo);  // xo != 0: the keys differ
     const int sh = top >= (int)kCsBits - 1 ? top - ((int)kCsBits - 1) : 0;
     uint32_t rk[kSmallMax / kBlock];
