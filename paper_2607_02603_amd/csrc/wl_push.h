@@ -529,7 +529,7 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
   __shared__ unsigned long long acc[kPbFineRows];
   __shared__ uint32_t wraps[kPbFineRows];
   __shared__ uint64_t wtab[TBL ? kPbTableMax : 1];
-  constexpr uint32_t kU = 16;  // records per thread per step, loaded together
+  constexpr uint32_t kU = 4;  // records per thread per step, loaded together
   const uint64_t key = round_key(ctx.st->seed, ctx.st->round);
   const uint32_t cmask = (1u << pb.cbits) - 1;
   const uint32_t nitems = pb.cnt->nslices;
