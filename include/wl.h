@@ -359,6 +359,13 @@ int wl_stats_get(wl_stats *out);
  *   WL_SORT_FIX=n        largest mixed bucket the counting sort of a small
  *                        segment fixes by insertion (default 32; 0 sends
  *                        every segment with one to the sorting network).
+ *   WL_CHAIN_SPINS=n     polls a chained scan of the incremental rounds
+ *                        waits for an earlier chunk before it gives up
+ *                        (default and maximum 2^22, far beyond any real
+ *                        wait).  A test hook: with a tiny bound a call
+ *                        either completes with the same result or fails
+ *                        with WL_EHIP ("a chained scan did not complete"),
+ *                        never returns a different result.
  *   WL_HOST_STAGING=0    copy pageable host memory without page-locked
  *                        staging buffers (as when they are refused).
  *   WL_TRACE_STREAMED=1, WL_TRACE_BATCHED=1

@@ -88,9 +88,11 @@ __device__ __forceinline__ uint32_t block_part_prefix(const uint32_t* p, uint32_
 // atomics carry everything a reader needs and no fence is issued.  Chunks
 // are taken by ticket (an atomic counter), so every chunk a block waits for
 // belongs to a block that is already running: the walk ends.  A wait longer
-// than kChainSpins polls (far beyond any real one) sets kErrChain and gives
-// up, so a kernel never hangs.
-constexpr uint32_t kErrChain = 64u;  // DevState::err bit
+// than max_spins polls (by default kChainSpins, far beyond any real wait)
+// gives up, so a kernel never hangs: it sets kErrChain and stops the device
+// (kStoppedOnError), so that no later kernel uses the unfinished result.
+constexpr uint32_t kErrChain = 64u;       // DevState::err bit
+constexpr uint32_t kStoppedOnError = 5;   // DevState::done: stopped, err says why
 constexpr uint32_t kChainSpins = 1u << 22;
 constexpr int kChainSplits = 0, kChainFlags = 1, kChainA = 2, kChainB = 3;  // sites
 
@@ -103,7 +105,8 @@ __device__ __forceinline__ uint32_t chain_epoch(uint32_t round, int site) {
 // per poll (lane l reads chunk p - l).  Contains __syncthreads().
 __device__ __forceinline__ uint32_t chain_prefix(unsigned long long* desc, uint32_t c,
                                                  uint32_t total, uint32_t epoch,
-                                                 uint32_t* err, uint32_t* sh1) {
+                                                 uint32_t max_spins, DevState* st,
+                                                 uint32_t* sh1) {
   if (threadIdx.x < kWave) {
     const int lane = (int)threadIdx.x;
     const unsigned long long tag = (unsigned long long)epoch << 34;
@@ -131,8 +134,11 @@ __device__ __forceinline__ uint32_t chain_prefix(unsigned long long* desc, uint3
         const int first = inc ? __ffsll((long long)inc) - 1 : kWave;
         const unsigned long long need = first >= kWave - 1 ? ~0ull : (2ull << first) - 1;
         if (wait & need) {
-          if (++spins > kChainSpins) {
-            if (lane == 0) atomicOr(err, kErrChain);
+          if (++spins > max_spins) {
+            if (lane == 0) {
+              atomicOr(&st->err, kErrChain);
+              st->done = kStoppedOnError;
+            }
             break;
           }
           __builtin_amdgcn_s_sleep(1);

@@ -39,7 +39,8 @@ struct DevState {
   uint32_t k;           // colour count before the current round
   uint32_t k_new;       // colour count after it
   uint32_t round;       // index of the round to run next
-  uint32_t done;        // 0 running, 1 stable, 2 round cap reached
+  uint32_t done;        // 0 running, 1 stable, 2 round cap reached, 3 and 4 halted for
+                        // the host (wl_relabel.h), 5 stopped on an error (err)
   uint32_t max_rounds;  // stop after this many rounds in total
   uint32_t n_small;     // entries in the small-segment list
   uint32_t err;         // input errors seen on the device (bit mask)
@@ -132,6 +133,7 @@ struct Ctx {
   uint32_t ring;       // 0: image in F_p (p = 2^61 - 1); 1: in Z/2^64 (wl_device.h)
   int nt_stream;       // stream col_idx with non-temporal loads
   uint32_t cs_fix;     // largest mixed bucket the small-segment sort fixes by insertion
+  uint32_t chain_spins;  // polls a chained scan waits for an earlier chunk before it gives up
   // Batch mode (Algorithm 2): the rows are nodes [ext_lo, ext_lo + n) of a
   // larger graph; a column outside that range is a node frozen as its own
   // singleton class, whose value is W(seed, r, 2^32 + column).

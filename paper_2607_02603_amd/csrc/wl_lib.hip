@@ -329,6 +329,14 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
     const long v = f ? strtol(f, nullptr, 10) : (long)kCsFix;
     c.cs_fix = (uint32_t)std::min<long>(std::max<long>(v, 0), (long)kSmallMax);
   }
+  {
+    // WL_CHAIN_SPINS=n bounds the wait of a chained scan for an earlier chunk
+    // (the tests make it tiny to run the give-up path: the call then fails
+    // with WL_EHIP, or completes when no wait was needed)
+    const char* f = getenv("WL_CHAIN_SPINS");
+    const long v = f ? strtol(f, nullptr, 10) : (long)kChainSpins;
+    c.chain_spins = (uint32_t)std::min<long>(std::max<long>(v, 0), (long)kChainSpins);
+  }
   c.max_small = L.max_small;
   c.max_big = L.max_big;
   c.max_chunks = L.max_chunks;

@@ -403,7 +403,7 @@ __global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx) {
     }
     uint32_t tot;
     const uint32_t ex = block_excl_scan(extra > 0 ? 1u : 0u, sh, &tot);
-    const uint32_t base = chain_prefix(ctx.desc, c, tot, epoch, &st->err, &sh1);
+    const uint32_t base = chain_prefix(ctx.desc, c, tot, epoch, ctx.chain_spins, st, &sh1);
     if (extra > 0) ctx.split[base + ex] = make_uint2(ctx.lcold[j], extra);
     if (j < nlive) ctx.lsplit[j] = extra > 0 ? 1 : 0;
     if (c == nchunks - 1 && threadIdx.x == 0) {
