@@ -356,9 +356,10 @@ int wl_stats_get(wl_stats *out);
  *   WL_ASYNC_PASSES=n    radix passes a device-driven round launches (0-8).
  *   WL_GRAPH=1           replay the device-driven rounds from a HIP graph.
  *   WL_NT_STREAM=1       non-temporal loads of the column indices.
- *   WL_SORT_FIX=n        largest mixed bucket the counting sort of a small
- *                        segment fixes by insertion (default 32; 0 sends
- *                        every segment with one to the sorting network).
+ *   WL_SORT_FIX=n        largest mixed bucket the counting sorts of the
+ *                        segments of 65 to 2048 nodes fix by insertion
+ *                        (default 32; 0 sends every segment with one to the
+ *                        sorting networks).
  *   WL_CHAIN_SPINS=n     polls a chained scan of the incremental rounds
  *                        waits for an earlier chunk before it gives up
  *                        (default and maximum 2^22, far beyond any real

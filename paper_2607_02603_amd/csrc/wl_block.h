@@ -188,25 +188,25 @@ __device__ __forceinline__ uint32_t block_append(bool want, uint32_t* counter,
   return at;
 }
 
-// Appends items of three kinds to three device lists at once: 'kind' in
-// [0, 3), or 3 and above for no item; returns the item's slot in its kind's
+// Appends items of four kinds to four device lists at once: 'kind' in
+// [0, 4), or 4 and above for no item; returns the item's slot in its kind's
 // list (order inside a list is irrelevant).  Ranks inside a wave come from
-// ballots, one atomic per kind and block, the three issued together.
+// ballots, one atomic per kind and block, the four issued together.
 // Contains __syncthreads(); every thread of the block must call it.
-__device__ __forceinline__ uint32_t block_append3(uint32_t kind, uint32_t* c0, uint32_t* c1,
-                                                  uint32_t* c2) {
-  __shared__ uint32_t wc[kBlock / kWave][3];
-  __shared__ uint32_t base3[3];
+__device__ __forceinline__ uint32_t block_append4(uint32_t kind, uint32_t* c0, uint32_t* c1,
+                                                  uint32_t* c2, uint32_t* c3) {
+  __shared__ uint32_t wc[kBlock / kWave][4];
+  __shared__ uint32_t base4[4];
   const int lane = lane_id(), wid = threadIdx.x / kWave;
   uint32_t rank = 0;
 #pragma unroll
-  for (uint32_t k = 0; k < 3; ++k) {
+  for (uint32_t k = 0; k < 4; ++k) {
     const unsigned long long m = __ballot(kind == k);
     if (kind == k) rank = (uint32_t)__popcll(m & ((1ull << lane) - 1));
     if (lane == 0) wc[wid][k] = (uint32_t)__popcll(m);
   }
   __syncthreads();
-  if (threadIdx.x < 3) {
+  if (threadIdx.x < 4) {
     const uint32_t k = threadIdx.x;
     uint32_t tot = 0;
     for (int w = 0; w < kBlock / kWave; ++w) {
@@ -214,11 +214,11 @@ __device__ __forceinline__ uint32_t block_append3(uint32_t kind, uint32_t* c0, u
       wc[w][k] = tot;
       tot += c;
     }
-    uint32_t* const ctr = k == 0 ? c0 : (k == 1 ? c1 : c2);
-    base3[k] = tot ? atomicAdd(ctr, tot) : 0u;
+    uint32_t* const ctr = k == 0 ? c0 : (k == 1 ? c1 : (k == 2 ? c2 : c3));
+    base4[k] = tot ? atomicAdd(ctr, tot) : 0u;
   }
   __syncthreads();
-  const uint32_t at = kind < 3 ? base3[kind] + wc[wid][kind] + rank : 0u;
+  const uint32_t at = kind < 4 ? base4[kind] + wc[wid][kind] + rank : 0u;
   __syncthreads();
   return at;
 }

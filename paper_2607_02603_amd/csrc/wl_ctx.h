@@ -9,6 +9,7 @@ namespace wl {
 constexpr int kBlock = 256;          // threads per workgroup (4 waves)
 constexpr uint32_t kSmallMax = 2048; // class/bucket size sorted in LDS
 constexpr uint32_t kTinyMax = 64;    // class/bucket size sorted in one wave
+constexpr uint32_t kMidMax = 512;    // ... sorted by one wave in LDS (counting sort)
 constexpr uint32_t kPicoMax = 8;     // ... sorted by 8 lanes (kept at the back of the tiny list)
 constexpr uint32_t kTile = 2048;     // elements per tile in the MSD passes
 constexpr uint32_t kTilePerThread = kTile / kBlock;
@@ -63,6 +64,7 @@ struct DevState {
   uint32_t n_mid;       // live rows queued for one wave each (this round)
   uint32_t n_hlive;     // live heavy rows (this round)
   uint32_t n_pico;      // segments of <= kPicoMax nodes (this round)
+  uint32_t n_msort;     // segments of kTinyMax + 1 .. kMidMax nodes (this round)
   uint32_t tickets[4];  // chunk tickets of this round's chained scans (per site)
   uint64_t seed;
   // The two big-segment lists: (entries << 32) | tiles.  One 64-bit atomic
@@ -112,7 +114,8 @@ struct Ctx {
                        // incremental rounds: 1 for heavy rows of live classes
   uint32_t* ids;       // inclusive scan of flags minus one
   uint32_t* cstart;    // class c occupies perm[cstart[c] .. cstart[c+1])
-  uint2* small_list;   // (start, len | kMatBit), 64 < len <= kSmallMax
+  uint2* small_list;   // (start, len | kMatBit), kMidMax < len <= kSmallMax from the
+                       // front, kTinyMax < len <= kMidMax from the back
   uint2* tiny_list;    // (start, len | kMatBit), 2 <= len <= 64
   uint2* big_list0;
   uint2* big_list1;
@@ -129,6 +132,7 @@ struct Ctx {
   unsigned long long* hacc;  // two accumulators per heavy row
   uint32_t* hcnt;            // finished chunks per heavy row
   uint32_t max_small, max_big, max_chunks, max_heavy;
+  uint32_t max_sm;     // capacity of small_list (the mid segments fill it from the back)
   int weighted;
   uint32_t ring;       // 0: image in F_p (p = 2^61 - 1); 1: in Z/2^64 (wl_device.h)
   int nt_stream;       // stream col_idx with non-temporal loads

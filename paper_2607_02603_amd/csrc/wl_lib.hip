@@ -338,6 +338,7 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
     c.chain_spins = (uint32_t)std::min<long>(std::max<long>(v, 0), (long)kChainSpins);
   }
   c.max_small = L.max_small;
+  c.max_sm = (uint32_t)(L.n / (kTinyMax + 1) + 1);
   c.max_big = L.max_big;
   c.max_chunks = L.max_chunks;
   c.max_heavy = L.max_heavy;
@@ -786,6 +787,7 @@ struct Session {
   // The sorting networks (one launch: gt workgroups for the tiny segments,
   // gp for the pico ones, gs for the small ones), with the tie-aware key
   // order in Z/2^64.
+  // gs: workgroups of the mid and small sorts (mid segments one per wave)
   void sorts(uint32_t gt, uint32_t gp, uint32_t gs, int check_passes) {
     const uint32_t g = gt + gp + gs;
     if (g == 0) return;
@@ -1079,7 +1081,9 @@ struct Session {
     passes_seen = std::max(passes_seen, pass);
     sorts(host.n_tiny ? grid_for(host.n_tiny, kBlock / kWave, 8192) : 0,
           host.n_pico ? grid_for(host.n_pico, kBlock / 8, 8192) : 0,
-          host.n_small ? std::min<uint32_t>(host.n_small, 4096) : 0, -1);
+          std::max<uint32_t>(host.n_msort ? grid_for(host.n_msort, kBlock / kWave, 8192) : 0,
+                             std::min<uint32_t>(host.n_small + host.n_msort, 4096)),
+          -1);
     if (full) rank_scan();
     HIP_LAUNCH_CHECK();
     return WL_OK;

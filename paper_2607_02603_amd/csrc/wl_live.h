@@ -247,16 +247,19 @@ __global__ void __launch_bounds__(kBlock) k_live_segments(Ctx ctx) {
       s = ctx.loff[j];
       len = ctx.llen[j];
     }
-    // 0 pico, 1 tiny, 2 small, 3 big, 4 none
-    const uint32_t kind = len < 2 ? 4u
+    // 0 pico, 1 tiny, 2 mid, 3 small, 4 big, 5 none
+    const uint32_t kind = len < 2 ? 5u
                           : len <= kPicoMax ? 0u
                           : len <= kTinyMax ? 1u
-                          : len <= kSmallMax ? 2u : 3u;
-    const uint32_t at = block_append3(kind, &st->n_pico, &st->n_tiny, &st->n_small);
+                          : len <= kMidMax ? 2u
+                          : len <= kSmallMax ? 3u : 4u;
+    const uint32_t at =
+        block_append4(kind, &st->n_pico, &st->n_tiny, &st->n_msort, &st->n_small);
     if (kind == 0) ctx.tiny_list[ctx.max_small - 1 - at] = make_uint2(s, len | kMatBit);
     else if (kind == 1) ctx.tiny_list[at] = make_uint2(s, len | kMatBit);
-    else if (kind == 2) ctx.small_list[at] = make_uint2(s, len | kMatBit);
-    else if (kind == 3) big_append(ctx, 0, s, len);
+    else if (kind == 2) ctx.small_list[ctx.max_sm - 1 - at] = make_uint2(s, len | kMatBit);
+    else if (kind == 3) ctx.small_list[at] = make_uint2(s, len | kMatBit);
+    else if (kind == 4) big_append(ctx, 0, s, len);
   }
 }
 
@@ -642,6 +645,7 @@ __global__ void k_live_round_end(Ctx ctx) {
   st->n_small = 0;
   st->n_tiny = 0;
   st->n_pico = 0;
+  st->n_msort = 0;
   st->big[0] = 0;
   st->big[1] = 0;
   for (int i = 0; i < 4; ++i) st->tickets[i] = 0;

@@ -42,6 +42,7 @@ __global__ void k_round_begin(Ctx ctx) {
   st->n_small = 0;
   st->n_tiny = 0;
   st->n_pico = 0;
+  st->n_msort = 0;
   st->big[0] = 0;
   st->big[1] = 0;
   for (int i = 0; i < 4; ++i) st->tickets[i] = 0;
@@ -107,16 +108,19 @@ __global__ void __launch_bounds__(kBlock) k_segments(Ctx ctx) {
       if (len) ctx.flags[s] = 1;
     }
     const uint32_t mat = ctx.keys_mat ? kMatBit : 0u;
-    // 0 pico, 1 tiny, 2 small, 3 big, 4 none
-    const uint32_t kind = len < 2 ? 4u
+    // 0 pico, 1 tiny, 2 mid, 3 small, 4 big, 5 none
+    const uint32_t kind = len < 2 ? 5u
                           : len <= kPicoMax ? 0u
                           : len <= kTinyMax ? 1u
-                          : len <= kSmallMax ? 2u : 3u;
-    const uint32_t at = block_append3(kind, &st->n_pico, &st->n_tiny, &st->n_small);
+                          : len <= kMidMax ? 2u
+                          : len <= kSmallMax ? 3u : 4u;
+    const uint32_t at =
+        block_append4(kind, &st->n_pico, &st->n_tiny, &st->n_msort, &st->n_small);
     if (kind == 0) ctx.tiny_list[ctx.max_small - 1 - at] = make_uint2(s, len | mat);
     else if (kind == 1) ctx.tiny_list[at] = make_uint2(s, len | mat);
-    else if (kind == 2) ctx.small_list[at] = make_uint2(s, len | mat);
-    else if (kind == 3) big_append(ctx, 0, s, len);
+    else if (kind == 2) ctx.small_list[ctx.max_sm - 1 - at] = make_uint2(s, len | mat);
+    else if (kind == 3) ctx.small_list[at] = make_uint2(s, len | mat);
+    else if (kind == 4) big_append(ctx, 0, s, len);
   }
 }
 
@@ -293,6 +297,9 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
         } else if (h <= kTinyMax) {
           uint32_t idx = atomicAdd(&st->n_tiny, 1u);
           ctx.tiny_list[idx] = make_uint2(pos, h | kMatBit);
+        } else if (h <= kMidMax) {
+          uint32_t idx = atomicAdd(&st->n_msort, 1u);
+          ctx.small_list[ctx.max_sm - 1 - idx] = make_uint2(pos, h | kMatBit);
         } else if (h <= kSmallMax) {
           uint32_t idx = atomicAdd(&st->n_small, 1u);
           ctx.small_list[idx] = make_uint2(pos, h | kMatBit);
@@ -415,27 +422,42 @@ __device__ __forceinline__ bool key_less(unsigned long long a, uint32_t va,
 constexpr uint32_t kCsBits = 10, kCsBuckets = 1u << kCsBits, kCsFix = 32;
 static_assert(kSmallMax <= 65536 && kCsBuckets % kBlock == 0, "counting sort of small segments");
 
+// LDS of one small-segment sort (one workgroup).
+struct SmallLds {
+  unsigned long long skey[kSmallMax];
+  uint32_t sval[kSmallMax];
+  uint32_t cnt[kCsBuckets + 1];
+  uint16_t inv[kSmallMax];
+  uint8_t mixed[kCsBuckets];
+  unsigned long long xo;
+  uint32_t csh[kBlock / kWave];
+  int differ, unsorted, fallback;
+};
+
 // One workgroup per small segment, keys in LDS: a counting sort by the ten
 // bits at and below the highest bit in which the keys differ, whose mixed
 // buckets of at most ctx.cs_fix (default kCsFix) keys are sorted by insertion;
 // a larger mixed bucket (rare for hashed images) falls back to a bitonic sort
 // of (z, node).
 // Then flags where z changes.
+// 'extra' mid segments (from the back of the list) are sorted here too.
 template <bool TIE>
-__device__ __forceinline__ void small_sort_body(const Ctx& ctx, uint32_t bid, uint32_t nblk) {
+__device__ __forceinline__ void small_sort_body(const Ctx& ctx, SmallLds& L, uint32_t bid,
+                                                uint32_t nblk, uint32_t extra) {
   DevState* st = ctx.st;
   const uint32_t ns = st->n_small;
-  __shared__ unsigned long long skey[kSmallMax];
-  __shared__ uint32_t sval[kSmallMax];
-  __shared__ int differ, unsorted;
-  __shared__ uint32_t cnt[kCsBuckets + 1];
-  __shared__ uint16_t inv[kSmallMax];
-  __shared__ uint8_t mixed[kCsBuckets];
-  __shared__ unsigned long long xo;
-  __shared__ uint32_t csh[kBlock / kWave];
-  __shared__ int fallback;
-  for (uint32_t si = bid; si < ns; si += nblk) {
-    const uint2 sg = ctx.small_list[si];
+  unsigned long long* const skey = L.skey;
+  uint32_t* const sval = L.sval;
+  uint32_t* const cnt = L.cnt;
+  uint16_t* const inv = L.inv;
+  uint8_t* const mixed = L.mixed;
+  uint32_t* const csh = L.csh;
+  unsigned long long& xo = L.xo;
+  int& differ = L.differ;
+  int& unsorted = L.unsorted;
+  int& fallback = L.fallback;
+  for (uint32_t si = bid; si < ns + extra; si += nblk) {
+    const uint2 sg = si < ns ? ctx.small_list[si] : ctx.small_list[ctx.max_sm - 1 - (si - ns)];
     const uint32_t s = sg.x, len = sg.y & ~kMatBit;
     const bool mat = (sg.y & kMatBit) != 0;
     uint32_t P = 2;
@@ -704,20 +726,213 @@ __device__ __forceinline__ void pico_sort_body(const Ctx& ctx, uint32_t bid, uin
   }
 }
 
-// The three sorts in one launch: workgroups [0, gt) take the tiny segments,
-// [gt, gt + gp) the pico ones and the rest the small ones (each kind in a
-// grid-stride loop over its own workgroups).
+// Segments of kTinyMax + 1 .. kMidMax keys, one wave each (four per
+// workgroup, no workgroup barrier): a counting sort in LDS on the kMidBits
+// bits at and below the highest bit in which the keys differ, lane l owning
+// buckets kMidPer * l ..; a bucket whose keys differ is sorted by its lane by
+// insertion when it holds at most ctx.cs_fix keys (as in the small sort), and
+// a larger one sends the segment to a bitonic network in LDS.  A wave's LDS accesses are ordered by
+// the wave itself (the LDS executes a wave's instructions in order); the
+// fences only keep the compiler from moving them across a step.
+constexpr uint32_t kMidBits = 9, kMidBuckets = 1u << kMidBits;
+constexpr uint32_t kMidWaves = 1024;  // fewer mid segments go to the workgroup sort
+constexpr uint32_t kMidPer = kMidMax / kWave;  // keys, and buckets, per lane
+static_assert(kMidBuckets == kMidMax, "one bucket per key slot: lane l owns the same range of both");
+
+struct MidLds {  // one wave
+  unsigned long long skey[kMidMax];
+  uint32_t sval[kMidMax];
+  uint32_t cnt[kMidBuckets + 1];
+  uint16_t inv[kMidMax];
+};
+
+__device__ __forceinline__ void wave_lds_step() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <bool TIE>
+__device__ __forceinline__ void mid_sort_body(const Ctx& ctx, MidLds* lds, uint32_t bid,
+                                              uint32_t nblk) {
+  const DevState* st = ctx.st;
+  const uint32_t nm = st->n_msort;
+  const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
+  MidLds& L = lds[w];
+  const uint32_t nwaves = nblk * (kBlock / kWave);
+  for (uint32_t si = bid * (kBlock / kWave) + w; si < nm; si += nwaves) {
+    const uint2 sg = ctx.small_list[ctx.max_sm - 1 - si];
+    const uint32_t s = sg.x, len = sg.y & ~kMatBit;
+    const bool mat = (sg.y & kMatBit) != 0;
+    // entry t = lane + kWave * u of the segment in registers
+    unsigned long long kr[kMidPer];
+    uint32_t vr[kMidPer];
+#pragma unroll
+    for (uint32_t u = 0; u < kMidPer; ++u) {
+      const uint32_t t = lane + kWave * u;
+      kr[u] = ~0ull;
+      vr[u] = 0xFFFFFFFFu;
+      if (t < len) {
+        vr[u] = ctx.perm[s + t];
+        kr[u] = mat ? ctx.keys[s + t] : ctx.z[vr[u]];
+      }
+    }
+    // the bits in which the keys differ from the first (len > kTinyMax: lane 0 holds it)
+    const unsigned long long first = read_lane64(kr[0], 0);
+    unsigned long long x = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kMidPer; ++u)
+      if (lane + kWave * u < len) x |= kr[u] ^ first;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) x |= __shfl_xor(x, off, kWave);
+    if (x == 0) continue;  // all equal: nothing to reorder, no flag inside
+    const int top = 63 - __clzll((long long)x);
+    const int sh = top >= (int)kMidBits - 1 ? top - ((int)kMidBits - 1) : 0;
+    // (every lane is past the previous segment's last LDS access: the loop
+    // bounds are the same for the whole wave)
+#pragma unroll
+    for (uint32_t u = 0; u < kMidPer; ++u) {
+      const uint32_t t = lane + kWave * u;
+      L.cnt[lane * kMidPer + u] = 0;
+      if (t < len) {
+        L.skey[t] = kr[u];
+        L.sval[t] = vr[u];
+      }
+    }
+    wave_lds_step();
+    uint32_t rk[kMidPer];
+#pragma unroll
+    for (uint32_t u = 0; u < kMidPer; ++u)
+      if (lane + kWave * u < len)
+        rk[u] = atomicAdd(&L.cnt[(kr[u] >> sh) & (kMidBuckets - 1)], 1u);
+    wave_lds_step();
+    {
+      // exclusive scan of the counts; cnt[kMidBuckets] = len
+      uint32_t c[kMidPer], sum = 0;
+#pragma unroll
+      for (uint32_t u = 0; u < kMidPer; ++u) {
+        c[u] = L.cnt[lane * kMidPer + u];
+        sum += c[u];
+      }
+      uint32_t run = wave_incl_scan(sum) - sum;
+#pragma unroll
+      for (uint32_t u = 0; u < kMidPer; ++u) {
+        L.cnt[lane * kMidPer + u] = run;
+        run += c[u];
+      }
+      if (lane == 0) L.cnt[kMidBuckets] = len;
+    }
+    wave_lds_step();
+#pragma unroll
+    for (uint32_t u = 0; u < kMidPer; ++u) {
+      const uint32_t t = lane + kWave * u;
+      if (t < len) L.inv[L.cnt[(kr[u] >> sh) & (kMidBuckets - 1)] + rk[u]] = (uint16_t)t;
+    }
+    wave_lds_step();
+    // each lane fixes its own buckets
+    bool too_big = false;
+#pragma unroll
+    for (uint32_t u = 0; u < kMidPer; ++u) {
+      const uint32_t b = lane * kMidPer + u;
+      const uint32_t o = L.cnt[b], c = L.cnt[b + 1] - o;
+      if (c < 2) continue;
+      if (c > ctx.cs_fix) {
+        for (uint32_t i = o + 1; i < o + c; ++i)
+          if (L.skey[L.inv[i]] != L.skey[L.inv[o]]) too_big = true;
+        continue;
+      }
+      for (uint32_t i = o + 1; i < o + c; ++i) {
+        const uint16_t e = L.inv[i];
+        const unsigned long long k = L.skey[e];
+        uint32_t j = i;
+        while (j > o && L.skey[L.inv[j - 1]] > k) {
+          L.inv[j] = L.inv[j - 1];
+          --j;
+        }
+        L.inv[j] = e;
+      }
+    }
+    wave_lds_step();
+    if (__ballot(too_big) == 0) {
+#pragma unroll
+      for (uint32_t u = 0; u < kMidPer; ++u) {
+        const uint32_t p = lane + kWave * u;
+        if (p < len) {
+          const uint32_t e = L.inv[p];
+          ctx.perm[s + p] = L.sval[e];
+          if (mat) ctx.keys[s + p] = L.skey[e];
+          if (p > 0 && L.skey[e] != L.skey[L.inv[p - 1]]) ctx.flags[s + p] = 1;
+        }
+      }
+      wave_lds_step();
+      continue;
+    }
+    // a bucket of more than cs_fix keys that differ: bitonic network over
+    // the segment in LDS, padded with the largest key (node 0xFFFFFFFF)
+    uint32_t P = 2;
+    while (P < len) P <<= 1;
+    for (uint32_t t = len + lane; t < P; t += kWave) {
+      L.skey[t] = ~0ull;
+      L.sval[t] = 0xFFFFFFFFu;
+    }
+    wave_lds_step();
+    for (uint32_t kk = 2; kk <= P; kk <<= 1)
+      for (uint32_t j = kk >> 1; j > 0; j >>= 1) {
+        for (uint32_t i = lane; i < P; i += kWave) {
+          const uint32_t l = i ^ j;
+          if (l > i) {
+            const bool asc = (i & kk) == 0;
+            const unsigned long long a = L.skey[i], b = L.skey[l];
+            const uint32_t va = L.sval[i], vb = L.sval[l];
+            if (key_less<TIE>(b, vb, a, va) == asc) {
+              L.skey[i] = b;
+              L.skey[l] = a;
+              L.sval[i] = vb;
+              L.sval[l] = va;
+            }
+          }
+        }
+        wave_lds_step();
+      }
+    for (uint32_t t = lane; t < len; t += kWave) {
+      ctx.perm[s + t] = L.sval[t];
+      if (mat) ctx.keys[s + t] = L.skey[t];
+      if (t > 0 && L.skey[t] != L.skey[t - 1]) ctx.flags[s + t] = 1;
+    }
+    wave_lds_step();
+  }
+}
+
+// The sorts in one launch: workgroups [0, gt) take the tiny segments,
+// [gt, gt + gp) the pico ones and the rest the mid ones and then the small
+// ones (each kind in a grid-stride loop over its workgroups).  The mid
+// segments take one wave each when there are at least kMidWaves of them
+// (throughput); fewer are sorted like the small ones, by whole workgroups,
+// which finish one segment sooner.  The mid and small sorts share the
+// workgroup's LDS.
 template <bool TIE>
 __global__ void __launch_bounds__(kBlock) k_sorts(Ctx ctx, int check_passes, uint32_t gt,
                                                   uint32_t gp) {
   if (ctx.st->done) return;
+  __shared__ union {
+    SmallLds small;
+    MidLds mid[kBlock / kWave];
+  } lds;
   const uint32_t b = blockIdx.x;
-  if (b < gt)
+  if (b < gt) {
     tiny_sort_body<TIE>(ctx, check_passes, b, gt);
-  else if (b < gt + gp)
+  } else if (b < gt + gp) {
     pico_sort_body<TIE>(ctx, b - gt, gp);
-  else
-    small_sort_body<TIE>(ctx, b - gt - gp, gridDim.x - gt - gp);
+  } else {
+    const uint32_t bid = b - gt - gp, nblk = gridDim.x - gt - gp;
+    const uint32_t nm = ctx.st->n_msort;
+    const bool by_wave = nm >= kMidWaves;
+    if (by_wave) {
+      mid_sort_body<TIE>(ctx, lds.mid, bid, nblk);
+      __syncthreads();  // every wave is done with the mid LDS
+    }
+    small_sort_body<TIE>(ctx, lds.small, bid, nblk, by_wave ? 0u : nm);
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -2,11 +2,13 @@
 H on which z is symmetric": the ranks of (c, z) by lexicographic sorting).
 
 A class of 65 to 2048 members is sorted in LDS by a counting sort on ten bits
-of z; a bucket whose keys differ is fixed by an insertion sort when it holds
-at most WL_SORT_FIX keys (default 32), and the whole segment otherwise goes
-to the bitonic network.  WL_SORT_FIX=0 sends every segment with a mixed
-bucket to the network, so both paths give the oracle's colours, colour count
-and round count bit for bit, in F_p and in Z/2^64.
+of z (a workgroup per segment; segments of at most 512 take one wave each
+with nine bits when a round has at least 1024 of them); a bucket whose keys
+differ is fixed by an insertion sort when it holds at most WL_SORT_FIX keys
+(default 32), and the whole segment otherwise goes to a bitonic network.
+WL_SORT_FIX=0 sends every segment with a mixed bucket to the network, so
+all paths give the oracle's colours, colour count and round count bit for
+bit, in F_p and in Z/2^64.
 """
 import os
 
@@ -71,3 +73,18 @@ def test_grid_with_labels_both_sort_paths(sort_fix, fix):
     g = inputs.grid_graph(150)
     init = (np.arange(g.n) * 2654435761 % 3).astype(np.uint32)
     _check(g.row_ptr, g.col, 61, init=init)
+
+
+@pytest.mark.parametrize("fix", [0, 32])
+@pytest.mark.parametrize("q", [61, 64])
+def test_many_mid_segments_by_wave(sort_fix, fix, q):
+    # 2000 labelled classes of 200 nodes over a random graph: every class
+    # splits in the first rounds, so a round has well over 1024 segments of
+    # 65 to 512 nodes, which one wave each sorts (the canonical start with
+    # the images gathered, the later rounds with them materialised); with
+    # WL_SORT_FIX=0 a mixed bucket sends its segment to the wave's network
+    sort_fix(fix)
+    g = inputs.er_graph(400000, 1000000, seed=7)
+    init = (np.arange(g.n) // 200).astype(np.uint32)
+    print(f"er400k labels q={q} fix={fix}", flush=True)
+    _check(g.row_ptr, g.col, q, init=init)
