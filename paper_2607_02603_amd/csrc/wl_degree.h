@@ -42,18 +42,32 @@ __global__ void __launch_bounds__(kBlock) k_deg_clear(Ctx ctx, DegScratch d, uin
   if (blockIdx.x == 0 && threadIdx.x == 0) *d.nd = 0;
 }
 
+// The loops over the nodes below take kDegStep nodes per thread and step
+// (i, i + kBlock, ...), their loads issued together.
+constexpr uint32_t kDegStep = 4;
+
 // Nodes per degree.
 template <bool RP64>
 __global__ void __launch_bounds__(kBlock) k_deg_hist(Ctx ctx, DegScratch d) {
   __shared__ uint32_t h[kDegLds];
   for (uint32_t x = threadIdx.x; x < kDegLds; x += kBlock) h[x] = 0;
   __syncthreads();
-  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < ctx.n; i += gridDim.x * kBlock) {
-    const uint32_t g = degree_of(ctx, i, RP64);
-    if (g < kDegLds)
-      atomicAdd(&h[g], 1u);
-    else
-      atomicAdd(&d.dcount[g], 1u);
+  const uint32_t stride = gridDim.x * kBlock * kDegStep;
+  for (uint32_t i0 = blockIdx.x * kBlock * kDegStep + threadIdx.x; i0 < ctx.n; i0 += stride) {
+    uint32_t g[kDegStep];
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) {
+      const uint32_t i = i0 + u * kBlock;
+      g[u] = i < ctx.n ? degree_of(ctx, i, RP64) : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) {
+      if (g[u] == 0xFFFFFFFFu) continue;
+      if (g[u] < kDegLds)
+        atomicAdd(&h[g[u]], 1u);
+      else
+        atomicAdd(&d.dcount[g[u]], 1u);
+    }
   }
   __syncthreads();
   for (uint32_t x = threadIdx.x; x < kDegLds; x += kBlock)
@@ -243,9 +257,18 @@ __global__ void __launch_bounds__(kBlock) k_deg_count(Ctx ctx, DegScratch d, uin
   deg_block_range(ctx.n, &lo, &hi);
   for (uint32_t r = threadIdx.x; r < K; r += kBlock) lc[r] = 0;
   __syncthreads();
-  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
-    const uint32_t e = d.dcount[degree_of(ctx, i, RP64)];
-    if (e & kDegLive) atomicAdd(&lc[e & ~kDegLive], 1u);
+  for (uint32_t i0 = lo + threadIdx.x; i0 < hi; i0 += kBlock * kDegStep) {
+    uint32_t g[kDegStep], e[kDegStep];
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) {
+      const uint32_t i = i0 + u * kBlock;
+      g[u] = i < hi ? degree_of(ctx, i, RP64) : 0u;
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) e[u] = i0 + u * kBlock < hi ? d.dcount[g[u]] : 0u;
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u)
+      if (e[u] & kDegLive) atomicAdd(&lc[e[u] & ~kDegLive], 1u);
   }
   __syncthreads();
   for (uint32_t r = threadIdx.x; r < K; r += kBlock) m[(uint64_t)r * nblk + blockIdx.x] = lc[r];
@@ -287,28 +310,46 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d, con
   for (uint32_t r = threadIdx.x; r < K; r += kBlock) lc[r] = m[(uint64_t)r * nblk + blockIdx.x];
   __syncthreads();
   const uint32_t lane = lane_id();
-  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
-    const uint64_t r0 = RP64 ? ctx.rp64[i] : ctx.rp32[i];
-    const uint32_t g = degree_of(ctx, i, RP64);
-    const uint32_t e = d.dcount[g];
-    const uint32_t r = e & ~kDegLive;
-    ctx.c[i] = r;
-    const bool live = (e & kDegLive) != 0;
-    // slots: one LDS atomic per rank present in the wave, ranks of the lanes
-    // inside it by their position
-    const unsigned long long peers = wave_peers(r, live);
-    const int ldr = live ? __ffsll((long long)peers) - 1 : (int)lane;
-    uint32_t b = 0;
-    if (live && (int)lane == ldr) b = atomicAdd(&lc[r], (uint32_t)__popcll(peers));
-    b = __shfl(b, ldr, kWave);
-    if (!live && ctx.pos) ctx.pos[i] = 0xFFFFFFFFu;
-    if (live) {
-      const uint32_t q = b + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
-      if (ctx.pos) ctx.pos[i] = q;
-      ctx.lperm[q] = i;
-      ctx.qcls[q] = d.rj[r];
-      ctx.rs[q] = r0;
-      ctx.rl[q] = g;
+  // the loop bounds are the same for the whole wave (hi - lo is a multiple of
+  // kBlock or the block's last range; lanes past hi take part inactive)
+  for (uint32_t i0 = lo + threadIdx.x - lane; i0 < hi; i0 += kBlock * kDegStep) {
+    uint64_t r0[kDegStep];
+    uint32_t g[kDegStep], e[kDegStep];
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) {
+      const uint32_t i = i0 + lane + u * kBlock;
+      r0[u] = 0;
+      g[u] = 0;
+      if (i < hi) {
+        r0[u] = RP64 ? ctx.rp64[i] : ctx.rp32[i];
+        g[u] = (uint32_t)((RP64 ? ctx.rp64[i + 1] : (uint64_t)ctx.rp32[i + 1]) - r0[u]);
+      }
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) e[u] = i0 + lane + u * kBlock < hi ? d.dcount[g[u]] : 0u;
+#pragma unroll
+    for (uint32_t u = 0; u < kDegStep; ++u) {
+      const uint32_t i = i0 + lane + u * kBlock;
+      const bool in = i < hi;
+      const uint32_t r = e[u] & ~kDegLive;
+      if (in) ctx.c[i] = r;
+      const bool live = in && (e[u] & kDegLive) != 0;
+      // slots: one LDS atomic per rank present in the wave, ranks of the
+      // lanes inside it by their position
+      const unsigned long long peers = wave_peers(r, live);
+      const int ldr = live ? __ffsll((long long)peers) - 1 : (int)lane;
+      uint32_t b = 0;
+      if (live && (int)lane == ldr) b = atomicAdd(&lc[r], (uint32_t)__popcll(peers));
+      b = __shfl(b, ldr, kWave);
+      if (in && !live && ctx.pos) ctx.pos[i] = 0xFFFFFFFFu;
+      if (live) {
+        const uint32_t q = b + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
+        if (ctx.pos) ctx.pos[i] = q;
+        ctx.lperm[q] = i;
+        ctx.qcls[q] = d.rj[r];
+        ctx.rs[q] = r0[u];
+        ctx.rl[q] = g[u];
+      }
     }
   }
 }
