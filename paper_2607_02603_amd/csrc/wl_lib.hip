@@ -1178,8 +1178,11 @@ struct Session {
       hipLaunchKernelGGL(k_live_scan_final<uint64_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
     else
       hipLaunchKernelGGL(k_live_scan_final<uint32_t>, dim3(ns), dim3(kBlock), 0, s, ctx);
-    hipLaunchKernelGGL(k_live_subs_splits, dim3(std::max(gl, gc)), dim3(kBlock), 0, s, ctx);
-    xscan(&st->split_any, &st->nsub, ctx.gl, ctx.go, &st->n_live2, &st->nl2, ns);
+    // its first ns blocks leave the block sums of the scan of gl and go
+    hipLaunchKernelGGL(k_live_subs_splits, dim3(std::max(std::max(gl, gc), ns)), dim3(kBlock), 0,
+                       s, ctx, ns);
+    hipLaunchKernelGGL(k_xscan_final, dim3(ns), dim3(kBlock), 0, s, ctx.st, &st->split_any,
+                       &st->nsub, ctx.gl, ctx.go, ctx.scan_part, &st->n_live2, &st->nl2);
     live_shift_end(!async);
   }
 

@@ -368,24 +368,46 @@ __global__ void __launch_bounds__(kBlock) k_live_scan_final(Ctx ctx) {
 // and each chunk of kBlock of them finds its place in the list by a chained
 // scan of the chunks' split counts).  The block of the last chunk records
 // the number of splits and whether they need the per-colour shift table.
-__global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx) {
+// The first nscan blocks take the sub-classes in the ranges of the scan of
+// gl and go that follows (k_xscan_final over nscan blocks), four consecutive
+// ones per thread and step, and leave that scan its block sums in scan_part,
+// in place of a launch of k_xscan_part.
+__global__ void __launch_bounds__(kBlock) k_live_subs_splits(Ctx ctx, uint32_t nscan) {
   DevState* st = ctx.st;
   if (st->done || st->nosplit) return;
-  const uint32_t stride = gridDim.x * kBlock;
   const uint32_t ns = st->nsub;
-  for (uint32_t g = blockIdx.x * kBlock + threadIdx.x; g < ns; g += stride) {
-    bool nz = ctx.gnz[g] != 0;
-    if (ctx.nz0f[g]) {
-      ctx.nz0f[g] = 0;
-      ctx.gnz[g] = 1;
-      nz = true;
-    }
-    const uint32_t len = ctx.gend[g] - ctx.gstart[g];
-    const bool live = len >= 2 && nz;
-    ctx.gl[g] = live ? 1u : 0u;
-    ctx.go[g] = live ? len : 0u;
-  }
   __shared__ uint32_t sh[kBlock / kWave];
+  if (blockIdx.x < nscan) {
+    uint32_t lo, hi;
+    xscan_range(ns, blockIdx.x, nscan, &lo, &hi);
+    uint32_t sa = 0, sb = 0;
+    for (uint32_t g0 = lo + kScanItems * threadIdx.x; g0 < hi; g0 += kScanStep) {
+#pragma unroll
+      for (uint32_t u = 0; u < kScanItems; ++u) {
+        const uint32_t g = g0 + u;
+        if (g >= hi) break;
+        bool nz = ctx.gnz[g] != 0;
+        if (ctx.nz0f[g]) {
+          ctx.nz0f[g] = 0;
+          ctx.gnz[g] = 1;
+          nz = true;
+        }
+        const uint32_t len = ctx.gend[g] - ctx.gstart[g];
+        const bool live = len >= 2 && nz;
+        ctx.gl[g] = live ? 1u : 0u;
+        ctx.go[g] = live ? len : 0u;
+        sa += live ? 1u : 0u;
+        sb += live ? len : 0u;
+      }
+    }
+    uint32_t ta, tb;
+    block_excl_scan(sa, sh, &ta);
+    block_excl_scan(sb, sh, &tb);
+    if (threadIdx.x == 0) {
+      ctx.scan_part[blockIdx.x] = ta;
+      ctx.scan_part[nscan + blockIdx.x] = tb;
+    }
+  }
   __shared__ uint32_t sh1;
   const uint32_t nlive = st->n_live;
   const uint32_t nchunks = (nlive + kBlock - 1) / kBlock;
