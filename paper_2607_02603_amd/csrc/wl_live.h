@@ -555,16 +555,30 @@ __global__ void __launch_bounds__(kBlock) k_shift_apply(Ctx ctx, int halt) {
   const uint32_t tid = blockIdx.x * kBlock + threadIdx.x, stride = gridDim.x * kBlock;
   uint32_t done4 = 0;
   if (((uintptr_t)ctx.c & 15) == 0) {
+    // with at least four groups of four colours per thread: four per step
+    // (i, i + stride, ...), loaded together
+    constexpr uint32_t kStep = 4;
     uint4* c4 = (uint4*)ctx.c;
     const uint32_t n4 = n / 4;
-    for (uint32_t i = tid; i < n4; i += stride) {
-      const uint4 a = c4[i];
-      uint4 r;
-      r.x = moved(a.x);
-      r.y = moved(a.y);
-      r.z = moved(a.z);
-      r.w = moved(a.w);
-      if (r.x != a.x || r.y != a.y || r.z != a.z || r.w != a.w) c4[i] = r;
+    const uint32_t step = (uint64_t)n4 >= (uint64_t)kStep * stride ? kStep : 1u;
+    for (uint32_t i0 = tid; i0 < n4; i0 += step * stride) {
+      uint4 a[kStep];
+#pragma unroll
+      for (uint32_t u = 0; u < kStep; ++u) {
+        const uint32_t i = i0 + u * stride;
+        if (u < step && i < n4) a[u] = c4[i];
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kStep; ++u) {
+        const uint32_t i = i0 + u * stride;
+        if (u >= step || i >= n4) break;
+        uint4 r;
+        r.x = moved(a[u].x);
+        r.y = moved(a[u].y);
+        r.z = moved(a[u].z);
+        r.w = moved(a[u].w);
+        if (r.x != a[u].x || r.y != a[u].y || r.z != a[u].z || r.w != a[u].w) c4[i] = r;
+      }
     }
     done4 = n4 * 4;
   }
