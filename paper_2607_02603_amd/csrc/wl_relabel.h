@@ -287,27 +287,23 @@ __global__ void __launch_bounds__(kBlock) k_big_scan(Ctx ctx, int pass) {
     const bool none_full = __syncthreads_or(all_here) == 0;
     if (all_here) ctx.bsame[sgi] = bmn == bmx ? 1 : 0;
     else if (none_full && threadIdx.x == 0) ctx.bsame[sgi] = 0;
-    if (h) {
-      const uint32_t pos = s.x + off;
-      ctx.flags[pos] = 1;
-      if (h >= 2 && bmn != bmx) {
-        if (h <= kPicoMax) {
-          uint32_t idx = atomicAdd(&st->n_pico, 1u);
-          ctx.tiny_list[ctx.max_small - 1 - idx] = make_uint2(pos, h | kMatBit);
-        } else if (h <= kTinyMax) {
-          uint32_t idx = atomicAdd(&st->n_tiny, 1u);
-          ctx.tiny_list[idx] = make_uint2(pos, h | kMatBit);
-        } else if (h <= kMidMax) {
-          uint32_t idx = atomicAdd(&st->n_msort, 1u);
-          ctx.small_list[ctx.max_sm - 1 - idx] = make_uint2(pos, h | kMatBit);
-        } else if (h <= kSmallMax) {
-          uint32_t idx = atomicAdd(&st->n_small, 1u);
-          ctx.small_list[idx] = make_uint2(pos, h | kMatBit);
-        } else {
-          big_append(ctx, cur ^ 1, pos, h);
-        }
-      }
-    }
+    const uint32_t pos = s.x + off;
+    if (h) ctx.flags[pos] = 1;
+    // buckets of two or more distinct keys are sorted further; the list
+    // slots of the workgroup's buckets are taken with one atomic per list
+    // 0 pico, 1 tiny, 2 mid, 3 small, 4 big, 5 none
+    const uint32_t kind = !(h >= 2 && bmn != bmx) ? 5u
+                          : h <= kPicoMax ? 0u
+                          : h <= kTinyMax ? 1u
+                          : h <= kMidMax ? 2u
+                          : h <= kSmallMax ? 3u : 4u;
+    const uint32_t at =
+        block_append4(kind, &st->n_pico, &st->n_tiny, &st->n_msort, &st->n_small);
+    if (kind == 0) ctx.tiny_list[ctx.max_small - 1 - at] = make_uint2(pos, h | kMatBit);
+    else if (kind == 1) ctx.tiny_list[at] = make_uint2(pos, h | kMatBit);
+    else if (kind == 2) ctx.small_list[ctx.max_sm - 1 - at] = make_uint2(pos, h | kMatBit);
+    else if (kind == 3) ctx.small_list[at] = make_uint2(pos, h | kMatBit);
+    else if (kind == 4) big_append(ctx, cur ^ 1, pos, h);
   }
 }
 
