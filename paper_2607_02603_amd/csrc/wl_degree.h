@@ -27,10 +27,15 @@ struct DegScratch {
   uint32_t* dlist;   // kDegRanks: present degrees (unordered)
   uint32_t* roff;    // kDegRanks: first member-list position of each rank
   uint32_t* rj;      // kDegRanks: live class index of each rank
+  uint32_t* rdeg;    // kDegRanks: degree of each rank's nodes (kDegMixed: several)
   uint32_t* nd;      // number of present degrees (DevState::deg_nd)
 };
 
-constexpr uint32_t kDegLive = 0x80000000u;
+// degree table entries after the ranking: rank | flags
+constexpr uint32_t kDegLive = 0x80000000u;   // the rank is a live class
+constexpr uint32_t kDegShared = 0x40000000u; // several degrees share the rank
+constexpr uint32_t kDegRankMask = 0x3FFFFFFFu;
+constexpr uint32_t kDegMixed = 0xFFFFFFFFu;
 
 __device__ __forceinline__ uint32_t degree_of(const Ctx& ctx, uint32_t i, bool rp64) {
   return rp64 ? (uint32_t)(ctx.rp64[i + 1] - ctx.rp64[i]) : ctx.rp32[i + 1] - ctx.rp32[i];
@@ -172,10 +177,12 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
       if (t < D && (t == 0 || rk[t] != rk[t - 1])) {
         uint32_t size = 0;
         bool nonnull = false;
-        for (uint32_t s = t; s < D && rk[s] == rk[t]; ++s) {
+        uint32_t s = t;
+        for (; s < D && rk[s] == rk[t]; ++s) {
           size += d.dcount[deg[s]];
           nonnull = nonnull || deg[s] > 0;
         }
+        d.rdeg[rk[t]] = s == t + 1 ? deg[t] : kDegMixed;
         const bool live = size >= 2 && nonnull;
         // stash size and liveness in the rank table entry of the first slot
         d.roff[rk[t]] = live ? size : 0u;
@@ -229,10 +236,56 @@ __global__ void __launch_bounds__(kDegThreads) k_deg_ranks(Ctx ctx, DegScratch d
     }
   }
   __syncthreads();
-  // degree table -> rank | live bit
+  // degree table -> rank | flags
   for (uint32_t t = threadIdx.x; t < D; t += kDegThreads) {
     const uint32_t r = rk[t];
-    d.dcount[deg[t]] = r | (d.rj[r] != 0xFFFFFFFFu ? kDegLive : 0u);
+    d.dcount[deg[t]] = r | (d.rj[r] != 0xFFFFFFFFu ? kDegLive : 0u) |
+                       (d.rdeg[r] == kDegMixed ? kDegShared : 0u);
+  }
+}
+
+// Class index and row length of every member-list position.  Both are the
+// same over a live class's range (the class of its rank, the rank's degree),
+// so they are written here in position order, four positions per thread;
+// k_deg_place writes the member's own row length only in a rank that several
+// degrees share.  Runs before k_deg_place.
+__global__ void __launch_bounds__(kBlock) k_deg_fill(Ctx ctx, DegScratch d) {
+  const DevState* st = ctx.st;
+  if (*d.nd > kDegRanks || st->nosplit) return;
+  const uint32_t nl = st->nl2, J = st->n_live2;  // J <= kDegRanks
+  __shared__ uint32_t off[kDegRanks];
+  __shared__ uint32_t dg[kDegRanks];
+  for (uint32_t j = threadIdx.x; j < J; j += kBlock) {
+    off[j] = ctx.loff[j];
+    dg[j] = d.rdeg[ctx.lcold[j]];
+  }
+  __syncthreads();
+  const bool vec = (((uintptr_t)ctx.qcls | (uintptr_t)ctx.rl) & 15) == 0;
+  const uint32_t stride = gridDim.x * kBlock * 4;
+  for (uint32_t q0 = (blockIdx.x * kBlock + threadIdx.x) * 4; q0 < nl; q0 += stride) {
+    // the class holding q0: last j with off[j] <= q0 (off[0] = 0, J >= 1)
+    uint32_t lo = 0, hi = J - 1;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= q0) lo = mid; else hi = mid - 1;
+    }
+    uint32_t qc[4], rl[4];
+    uint32_t j = lo;
+#pragma unroll
+    for (uint32_t u = 0; u < 4; ++u) {
+      while (j + 1 < J && off[j + 1] <= q0 + u) ++j;
+      qc[u] = j;
+      rl[u] = dg[j];
+    }
+    if (vec && q0 + 4 <= nl) {
+      *(uint4*)(ctx.qcls + q0) = make_uint4(qc[0], qc[1], qc[2], qc[3]);
+      *(uint4*)(ctx.rl + q0) = make_uint4(rl[0], rl[1], rl[2], rl[3]);
+    } else {
+      for (uint32_t u = 0; u < 4 && q0 + u < nl; ++u) {
+        ctx.qcls[q0 + u] = qc[u];
+        ctx.rl[q0 + u] = rl[u];
+      }
+    }
   }
 }
 
@@ -268,7 +321,7 @@ __global__ void __launch_bounds__(kBlock) k_deg_count(Ctx ctx, DegScratch d, uin
     for (uint32_t u = 0; u < kDegStep; ++u) e[u] = i0 + u * kBlock < hi ? d.dcount[g[u]] : 0u;
 #pragma unroll
     for (uint32_t u = 0; u < kDegStep; ++u)
-      if (e[u] & kDegLive) atomicAdd(&lc[e[u] & ~kDegLive], 1u);
+      if (e[u] & kDegLive) atomicAdd(&lc[e[u] & kDegRankMask], 1u);
   }
   __syncthreads();
   for (uint32_t r = threadIdx.x; r < K; r += kBlock) m[(uint64_t)r * nblk + blockIdx.x] = lc[r];
@@ -331,7 +384,7 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d, con
     for (uint32_t u = 0; u < kDegStep; ++u) {
       const uint32_t i = i0 + lane + u * kBlock;
       const bool in = i < hi;
-      const uint32_t r = e[u] & ~kDegLive;
+      const uint32_t r = e[u] & kDegRankMask;
       if (in) ctx.c[i] = r;
       const bool live = in && (e[u] & kDegLive) != 0;
       // slots: one LDS atomic per rank present in the wave, ranks of the
@@ -346,9 +399,8 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d, con
         const uint32_t q = b + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
         if (ctx.pos) ctx.pos[i] = q;
         ctx.lperm[q] = i;
-        ctx.qcls[q] = d.rj[r];
         ctx.rs[q] = r0[u];
-        ctx.rl[q] = g[u];
+        if (e[u] & kDegShared) ctx.rl[q] = g[u];  // k_deg_fill wrote the rest
       }
     }
   }

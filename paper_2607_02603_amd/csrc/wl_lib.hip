@@ -1222,6 +1222,7 @@ struct Session {
     d.dlist = base + (uint64_t)maxd + 1;
     d.roff = d.dlist + kDegRanks;
     d.rj = d.roff + kDegRanks;
+    d.rdeg = d.rj + kDegRanks;
     d.nd = &ctx.st->deg_nd;
     const uint32_t gd = grid_for((uint64_t)maxd + 1, kBlock, 4096);
     using RPT = typename std::conditional<RP64, uint64_t, uint32_t>::type;
@@ -1247,6 +1248,8 @@ struct Session {
     hipLaunchKernelGGL(k_deg_count<RP64>, dim3(nblk), dim3(kBlock), 0, s, ctx, d, m);
     hipLaunchKernelGGL(k_deg_rowscan, dim3((uint32_t)std::min<uint64_t>(K, 4096)), dim3(kBlock), 0,
                        s, ctx, d, m, nblk);
+    hipLaunchKernelGGL(k_deg_fill, dim3(grid_for((uint64_t)L.n / 4 + 1, kBlock, 1024)),
+                       dim3(kBlock), 0, s, ctx, d);
     hipLaunchKernelGGL(k_deg_place<RP64>, dim3(nblk), dim3(kBlock), 0, s, ctx, d, m);
     hipLaunchKernelGGL(k_live_round_end, dim3(1), dim3(1), 0, s, ctx);
     HIP_LAUNCH_CHECK();
@@ -1258,7 +1261,7 @@ struct Session {
   // Whether the degree round's table and lists fit the scratch it uses (the
   // keys_tmp region, two words per node).
   bool degree_round_fits() const {
-    const uint64_t words = (uint64_t)host.max_deg + 1 + 3ull * kDegRanks;
+    const uint64_t words = (uint64_t)host.max_deg + 1 + 4ull * kDegRanks;
     return host.max_deg < 0x7FFFFFFFu && words <= 2 * L.n;
   }
 
