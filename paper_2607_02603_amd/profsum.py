@@ -6,6 +6,7 @@ profiles/.
     python -m paper_2607_02603_amd.profsum counters KERNELS -- DB... > out.md
     python -m paper_2607_02603_amd.profsum calltraffic FETCH_DB WRITE_DB TRACE_DB CALLS > out.json
     python -m paper_2607_02603_amd.profsum dispatches DB TITLE COMMAND > out.md
+    python -m paper_2607_02603_amd.profsum reqsizes REQ_DB FETCH_DB TITLE COMMAND > out.md
 
 'trace' tabulates the library's kernels of a --kernel-trace run (per-call
 figures are totals divided by CALLS, the number of library calls the traced
@@ -24,7 +25,14 @@ runs, calibrated like 'traffic') and the call's summed kernel time (from a
 --kernel-trace run making CALLS library calls), with the SHA-256 of all the
 library's kernel sources.  'dispatches' lists, for the last library call
 of a --kernel-trace run, every dispatch's duration per kernel in launch
-order.
+order.  'reqsizes' checks the copy calibration of FETCH_SIZE per kernel: from
+a --pmc run of TCC_EA0_RDREQ and its 32-, 64- and 128-byte parts, the read
+bytes 32 R32 + 64 R64 + 128 R128 of every library kernel of the last call
+(and of the copy, which must come out at 1 GiB), beside FETCH_SIZE scaled by
+the copy factor.  FETCH_SIZE's formula takes 128-byte requests from
+TCC_BUBBLE; where that does not count them, a 128-byte read counts as 64
+bytes, so the copy factor is right for kernels that read whole 128-byte lines
+and too large for kernels whose reads are 32 or 64 bytes.
 """
 import hashlib
 import json
@@ -270,6 +278,73 @@ def dispatches_markdown(db, title, command, top=20):
     return "\n".join(out)
 
 
+_REQ = ("TCC_EA0_RDREQ", "TCC_EA0_RDREQ_32B", "TCC_EA0_RDREQ_64B", "TCC_EA0_RDREQ_128B")
+
+
+def _req_bytes(c):
+    return 32.0 * c["TCC_EA0_RDREQ_32B"] + 64.0 * c["TCC_EA0_RDREQ_64B"] + \
+        128.0 * c["TCC_EA0_RDREQ_128B"]
+
+
+def reqsizes(req_db, fetch_db):
+    """Per kernel of the last library call: read requests by size, the read
+    bytes they give, and FETCH_SIZE scaled by the copy factor."""
+    ev_r, ev_f = _pmc(req_db), _pmc(fetch_db)
+    copy_r = [c for n, c in ev_r if "copyBuffer" in n and all(k in c for k in _REQ)]
+    copy_f = [c["FETCH_SIZE"] for n, c in ev_f if "copyBuffer" in n and "FETCH_SIZE" in c]
+    if not copy_r or not copy_f:
+        raise SystemExit("no copy-kernel dispatch in the request or FETCH_SIZE run")
+    scale = (1 << 30) / (copy_f[0] * 1024.0)
+    per = {}
+    for n, c in _last_call(ev_r):
+        e = per.setdefault(_short(n), {k: 0.0 for k in _REQ})
+        for k in _REQ:
+            e[k] += c.get(k, 0.0)
+    fetch = {}
+    for n, c in _last_call(ev_f):
+        fetch[_short(n)] = fetch.get(_short(n), 0.0) + c.get("FETCH_SIZE", 0.0) * 1024.0 * scale
+    rows = []
+    for name, e in per.items():
+        rows.append({"kernel": name, **{k: e[k] for k in _REQ}, "bytes": _req_bytes(e),
+                     "fetch_scaled": fetch.get(name, 0.0),
+                     "unsized": e["TCC_EA0_RDREQ"] - e["TCC_EA0_RDREQ_32B"] -
+                     e["TCC_EA0_RDREQ_64B"] - e["TCC_EA0_RDREQ_128B"]})
+    rows.sort(key=lambda r: -r["fetch_scaled"])
+    c0 = copy_r[0]
+    return {"copy": {"bytes": _req_bytes(c0), "expected": float(1 << 30),
+                     **{k: c0[k] for k in _REQ}, "fetch_kib": copy_f[0], "fetch_scale": scale},
+            "kernels": rows,
+            "total_bytes": sum(r["bytes"] for r in rows),
+            "total_fetch_scaled": sum(r["fetch_scaled"] for r in rows)}
+
+
+def reqsizes_markdown(req_db, fetch_db, title, command, top=20):
+    r = reqsizes(req_db, fetch_db)
+    c = r["copy"]
+    out = [f"# {title}", "", "Commands (repository root, on the MI355X machine):", ""]
+    out += [f"    {x}" for x in command.split(" ;; ")]
+    out += ["",
+            f"The 1 GiB copy that `--copy-probe` issues first: {c['TCC_EA0_RDREQ_128B']:,.0f} "
+            f"128-byte, {c['TCC_EA0_RDREQ_64B']:,.0f} 64-byte and {c['TCC_EA0_RDREQ_32B']:,.0f} "
+            f"32-byte read requests, {c['bytes'] / (1 << 30):.4f} GiB by request size; "
+            f"FETCH_SIZE reads {c['fetch_kib']:,.0f} KiB, a factor of {c['fetch_scale']:.3f}.",
+            "",
+            "Library kernels of the last call, by scaled FETCH_SIZE (GB = 1e9 bytes; "
+            "`by size` = 32 R32 + 64 R64 + 128 R128):", "",
+            "| kernel | R32 | R64 | R128 | read GB by size | FETCH_SIZE x factor, GB | ratio |",
+            "|---|---|---|---|---|---|---|"]
+    for k in r["kernels"][:top]:
+        ratio = k["fetch_scaled"] / k["bytes"] if k["bytes"] else float("nan")
+        out.append(f"| {k['kernel']} | {k['TCC_EA0_RDREQ_32B']:,.0f} | "
+                   f"{k['TCC_EA0_RDREQ_64B']:,.0f} | {k['TCC_EA0_RDREQ_128B']:,.0f} | "
+                   f"{k['bytes'] / 1e9:.3f} | {k['fetch_scaled'] / 1e9:.3f} | {ratio:.2f} |")
+    unsized = sum(k["unsized"] for k in r["kernels"])
+    out += ["", f"All library kernels of the call: {r['total_bytes'] / 1e9:.2f} GB read by "
+            f"request size against {r['total_fetch_scaled'] / 1e9:.2f} GB of scaled FETCH_SIZE; "
+            f"read requests outside the three sizes: {unsized:,.0f}."]
+    return "\n".join(out)
+
+
 def main(argv):
     if len(argv) >= 5 and argv[0] == "trace":
         print(trace_markdown(argv[1], int(argv[2]), argv[3], argv[4]))
@@ -280,6 +355,8 @@ def main(argv):
         print(json.dumps(call_traffic(argv[1], argv[2], argv[3], int(argv[4])), indent=1))
     elif len(argv) == 4 and argv[0] == "dispatches":
         print(dispatches_markdown(argv[1], argv[2], argv[3]))
+    elif len(argv) == 5 and argv[0] == "reqsizes":
+        print(reqsizes_markdown(argv[1], argv[2], argv[3], argv[4]))
     elif len(argv) >= 4 and argv[0] == "traffic":
         print(json.dumps(traffic(argv[1], argv[2], argv[3:]), indent=1))
     else:
