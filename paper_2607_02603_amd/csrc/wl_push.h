@@ -449,7 +449,6 @@ __global__ void __launch_bounds__(kBlock) k_pb_cursors(Ctx ctx, PbCtx pb) {
 __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
   if (ctx.st->done || (ctx.st->err & kErrNotSymmetric)) return;
   __shared__ __align__(16) uint32_t buf[kPbTile2];
-  __shared__ __align__(16) uint16_t sbin[kPbTile2];
   __shared__ uint32_t hist[kPbMaxFine];
   __shared__ long long dd[kPbMaxFine];
   __shared__ uint32_t sh[kPbThreads / kWave];
@@ -479,7 +478,6 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
       const uint32_t local = rec[k] >> pb.cbits;
       const uint32_t b = min(local >> kPbFineShift, nfb - 1);
       pk[k] = (b << 16) | atomicAdd(&hist[b], 1u);
-      rec[k] = ((local & (kPbFineRows - 1)) << pb.cbits) | (rec[k] & cmask);
     }
   }
   __syncthreads();
@@ -490,12 +488,18 @@ __global__ void __launch_bounds__(kPbThreads) k_pb_scatter2(Ctx ctx, PbCtx pb) {
   for (uint32_t k = 0; k < kPer; ++k)
     if (pk[k] != 0xFFFFFFFFu) {
       const uint32_t b = pk[k] >> 16;
-      const uint32_t slot = hist[b] + (pk[k] & 0xFFFF);
-      buf[slot] = rec[k];
-      sbin[slot] = (uint16_t)b;
+      buf[hist[b] + (pk[k] & 0xFFFF)] = rec[k];
     }
   __syncthreads();
-  pb_write_out<kPbThreads, uint16_t>(buf, sbin, dd, cnt, pb.rec2);
+  // the staged pass-1 records name their fine bin (the high bits of their
+  // row), and are rewritten to the row inside it on the way out
+  for (uint32_t s = threadIdx.x; s < cnt; s += kPbThreads) {
+    const uint32_t r1 = buf[s];
+    const uint32_t local = r1 >> pb.cbits;
+    const long long o = dd[min(local >> kPbFineShift, nfb - 1)];
+    if (o != kPbSkip)
+      pb.rec2[o + s] = ((local & (kPbFineRows - 1)) << pb.cbits) | (r1 & cmask);
+  }
 }
 
 // ---------------------------------------------------------------------------
