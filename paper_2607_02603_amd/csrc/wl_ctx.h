@@ -148,6 +148,8 @@ struct Ctx {
   // share memory with buffers of the full relabel that those rounds do not
   // use (see make_ctx).
   uint32_t* lperm;     // members of the live classes, class after class
+  uint32_t* pos_deg;   // the same map as written by the one-colour round (the
+                       // same buffer; kept for graphs whose rounds do not keep it)
   uint32_t* pos;       // position of every node in lperm, ~0 outside the live
                        // classes (NULL outside in-core sessions)
   uint32_t* lperm2;

@@ -394,10 +394,10 @@ __global__ void __launch_bounds__(kBlock) k_deg_place(Ctx ctx, DegScratch d, con
       uint32_t b = 0;
       if (live && (int)lane == ldr) b = atomicAdd(&lc[r], (uint32_t)__popcll(peers));
       b = __shfl(b, ldr, kWave);
-      if (in && !live && ctx.pos) ctx.pos[i] = 0xFFFFFFFFu;
+      if (in && !live && ctx.pos_deg) ctx.pos_deg[i] = 0xFFFFFFFFu;
       if (live) {
         const uint32_t q = b + (uint32_t)__popcll(peers & ((1ull << lane) - 1));
-        if (ctx.pos) ctx.pos[i] = q;
+        if (ctx.pos_deg) ctx.pos_deg[i] = q;
         ctx.lperm[q] = i;
         ctx.rs[q] = r0[u];
         if (e[u] & kDegShared) ctx.rl[q] = g[u];  // k_deg_fill wrote the rest

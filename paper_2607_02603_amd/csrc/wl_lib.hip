@@ -314,6 +314,7 @@ Ctx make_ctx(const Layout& L, const wl_csr* g, uint8_t* ws, uint32_t* colors) {
   c.bsame = ws + L.off_bsame;
   c.nz0f = L.in_core ? ws + L.off_nz0f : nullptr;
   c.pos = L.in_core ? (uint32_t*)(ws + L.off_pos) : nullptr;
+  c.pos_deg = c.pos;
   c.desc = L.in_core ? (unsigned long long*)(ws + L.off_desc) : nullptr;
   c.desc_cap = L.desc_cap;
   c.lsplit = c.c8;    // the live rounds do not use the compact colours
@@ -601,6 +602,9 @@ struct Session {
   bool deg_mode = true;
   PbCounts pbc{};
   bool pb_avail = false, pb_planned = false, pb_stop = false;
+  // pos_deg holds the member-list positions of the coming round's live
+  // classes (set by the one-colour round, cleared by the next image)
+  bool deg_pos_fresh = false;
   bool sym_flag = false;
   int pb_mode = 1;
   DevState host;      // last copy of the device state
@@ -965,12 +969,20 @@ struct Session {
     const DevState& h = host;
     const bool uniform = !W && h.k == 1 && !ctx.batch;
     const uint32_t gn = grid_for(L.n, kBlock, 4096);
+    // right after the one-colour round the member list is the one whose
+    // positions that round recorded
+    const bool fresh = deg_pos_fresh;
+    deg_pos_fresh = false;
     if (!W && !uniform && !ctx.batch) {
       bool use = false;
       if (int r = pb_wanted<RP>(&use)) return r;
       if (use) {
-        if (int r = pb_round<RP>()) return r;
-        hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
+        // then the image goes to the sort keys directly
+        pb.kpos = fresh ? ctx.pos_deg : nullptr;
+        const int r = pb_round<RP>();
+        pb.kpos = nullptr;
+        if (r) return r;
+        if (!fresh) hipLaunchKernelGGL(k_live_load, dim3(gn), dim3(kBlock), 0, s, ctx);
         return WL_OK;
       }
     }
@@ -1255,6 +1267,7 @@ struct Session {
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
     *handled = true;
+    deg_pos_fresh = ctx.pos_deg != nullptr && !host.done;
     return WL_OK;
   }
 

@@ -74,6 +74,11 @@ struct PbCtx {
   uint32_t* mlist;           // fine bins with several slices
   uint64_t* part;            // partial images, kPbFineRows per slot
   PbCounts* cnt;
+  // Non-null in the incremental round that follows the one-colour round:
+  // the member-list position of every node (~0 outside the live classes).
+  // Each live row's image then goes straight to its sort key (ctx.keys)
+  // instead of to z in node order.
+  const uint32_t* kpos;
 };
 
 template <typename RP>
@@ -610,7 +615,12 @@ __global__ void __launch_bounds__(kPbAccThreads) k_pb_accum(Ctx ctx, PbCtx pb) {
     __syncthreads();
     const uint64_t row0 = (uint64_t)f << kPbFineShift;
     const uint32_t nrows = (uint32_t)min((uint64_t)kPbFineRows, (uint64_t)ctx.n - row0);
-    if (ns == 1) {
+    if (ns == 1 && pb.kpos) {
+      for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads) {
+        const uint32_t q = pb.kpos[row0 + r];
+        if (q != 0xFFFFFFFFu) ctx.keys[q] = pb_reduce(acc[r], wraps[r], ctx.ring);
+      }
+    } else if (ns == 1) {
       for (uint32_t r = threadIdx.x; r < nrows; r += kPbAccThreads)
         ctx.z[row0 + r] = pb_reduce(acc[r], wraps[r], ctx.ring);
     } else {
@@ -637,7 +647,12 @@ __global__ void __launch_bounds__(kBlock) k_pb_combine(Ctx ctx, PbCtx pb) {
     uint64_t z = 0;
     for (uint32_t s = s0; s < s1; ++s)
       z = add_q(z, pb.part[(uint64_t)s * kPbFineRows + r], ctx.ring);
-    ctx.z[row] = z;
+    if (!pb.kpos) {
+      ctx.z[row] = z;
+    } else {
+      const uint32_t q = pb.kpos[row];
+      if (q != 0xFFFFFFFFu) ctx.keys[q] = z;
+    }
   }
 }
 
