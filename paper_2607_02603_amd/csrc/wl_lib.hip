@@ -1090,7 +1090,7 @@ struct Session {
       HIP_LAUNCH_CHECK();
       if (int r = pull()) return r;
     }
-    passes_seen = std::max(passes_seen, pass);
+    if (pass > pass0) passes_seen = std::max(passes_seen, pass);
     sorts(host.n_tiny ? grid_for(host.n_tiny, kBlock / kWave, 8192) : 0,
           host.n_pico ? grid_for(host.n_pico, kBlock / 8, 8192) : 0,
           std::max<uint32_t>(host.n_msort ? grid_for(host.n_msort, kBlock / kWave, 8192) : 0,
@@ -1300,6 +1300,10 @@ struct Session {
     return WL_OK;
   }
 
+  // Live positions from which a host-driven round launches its first two
+  // radix passes before reading anything back.
+  static constexpr uint32_t kBlindPassesMin = 1u << 20;
+
   int round_live() {
     if (degree_round_applies()) {
       ctx = ctx0;
@@ -1318,9 +1322,22 @@ struct Session {
     hipLaunchKernelGGL(k_round_begin, dim3(1), dim3(1), 0, s, ctx);
     if (int r = spmv_live()) return r;
     live_segments();
-    HIP_LAUNCH_CHECK();
-    if (int r = pull()) return r;
-    if (int r = finish_sort(0, false)) return r;
+    if (host.nl >= kBlindPassesMin) {
+      // a large live set: the first two radix passes go out without a
+      // read-back (a pass whose list is empty returns at once); the
+      // read-back after them sizes the small sorts and shows whether more
+      // passes are needed.  Pass 1 had work when pass 0 left big buckets.
+      radix_pass(0, 1024);
+      radix_pass(1, 1024);
+      HIP_LAUNCH_CHECK();
+      if (int r = pull()) return r;
+      passes_seen = std::max(passes_seen, big_entries(1) > 0 ? 2 : 1);
+      if (int r = finish_sort(2, false)) return r;
+    } else {
+      HIP_LAUNCH_CHECK();
+      if (int r = pull()) return r;
+      if (int r = finish_sort(0, false)) return r;
+    }
     live_tail();
     HIP_LAUNCH_CHECK();
     if (int r = pull()) return r;
