@@ -7,6 +7,7 @@ profiles/.
     python -m paper_2607_02603_amd.profsum calltraffic FETCH_DB WRITE_DB TRACE_DB CALLS > out.json
     python -m paper_2607_02603_amd.profsum dispatches DB TITLE COMMAND > out.md
     python -m paper_2607_02603_amd.profsum reqsizes REQ_DB FETCH_DB TITLE COMMAND > out.md
+    python -m paper_2607_02603_amd.profsum bandwidth REQ_DB WRITE_DB TRACE_DB TITLE COMMAND > out.md
 
 'trace' tabulates the library's kernels of a --kernel-trace run (per-call
 figures are totals divided by CALLS, the number of library calls the traced
@@ -32,7 +33,10 @@ bytes 32 R32 + 64 R64 + 128 R128 of every library kernel of the last call
 the copy factor.  FETCH_SIZE's formula takes 128-byte requests from
 TCC_BUBBLE; where that does not count them, a 128-byte read counts as 64
 bytes, so the copy factor is right for kernels that read whole 128-byte lines
-and too large for kernels whose reads are 32 or 64 bytes.
+and too large for kernels whose reads are 32 or 64 bytes.  'bandwidth' lists
+every library kernel of the last call with its summed duration (from a
+--kernel-trace run), its read bytes by request size and its WRITE_SIZE bytes
+(scaled by the copy's factor), and the rate they give.
 """
 import hashlib
 import json
@@ -345,6 +349,60 @@ def reqsizes_markdown(req_db, fetch_db, title, command, top=20):
     return "\n".join(out)
 
 
+def _trace_last_call(db):
+    """{kernel: (dispatches, ms)} over the last library call of a trace."""
+    cur = sqlite3.connect(db).cursor()
+    cols = [r[1] for r in cur.execute("pragma table_info(kernels)")]
+    ki = cols.index("kernel_name") if "kernel_name" in cols else cols.index("name")
+    st, en = cols.index("start"), cols.index("end")
+    rows = [r for r in cur.execute("select * from kernels order by start").fetchall()
+            if _is_lib(r[ki])]
+    starts = [i for i, r in enumerate(rows) if "k_iota_zero" in r[ki]]
+    rows = rows[starts[-1]:] if starts else rows
+    out = {}
+    for r in rows:
+        d, ms = out.get(_short(r[ki]), (0, 0.0))
+        out[_short(r[ki])] = (d + 1, ms + (r[en] - r[st]) / 1e6)
+    return out
+
+
+def bandwidth(req_db, write_db, trace_db):
+    ev_r, ev_w = _pmc(req_db), _pmc(write_db)
+    copy_w = [c["WRITE_SIZE"] for n, c in ev_w if "copyBuffer" in n and "WRITE_SIZE" in c]
+    if not copy_w:
+        raise SystemExit(f"{write_db}: no copy-kernel dispatch to calibrate WRITE_SIZE")
+    wscale = (1 << 30) / (copy_w[0] * 1024.0)
+    rd, wr = {}, {}
+    for n, c in _last_call(ev_r):
+        rd[_short(n)] = rd.get(_short(n), 0.0) + _req_bytes({k: c.get(k, 0.0) for k in _REQ})
+    for n, c in _last_call(ev_w):
+        wr[_short(n)] = wr.get(_short(n), 0.0) + c.get("WRITE_SIZE", 0.0) * 1024.0 * wscale
+    tr = _trace_last_call(trace_db)
+    rows = []
+    for name, (d, ms) in tr.items():
+        r, w = rd.get(name, 0.0), wr.get(name, 0.0)
+        rows.append({"kernel": name, "dispatches": d, "ms": ms, "read": r, "write": w,
+                     "tb_per_s": (r + w) / (ms / 1e3) / 1e12 if ms > 0 else 0.0})
+    rows.sort(key=lambda x: -x["ms"])
+    return {"write_scale": wscale, "kernels": rows}
+
+
+def bandwidth_markdown(req_db, write_db, trace_db, title, command, top=25):
+    b = bandwidth(req_db, write_db, trace_db)
+    out = [f"# {title}", "", "Commands (repository root, on the MI355X machine):", ""]
+    out += [f"    {x}" for x in command.split(" ;; ")]
+    out += ["", "Library kernels of the last call by duration: read bytes by request size "
+            "(32 R32 + 64 R64 + 128 R128), WRITE_SIZE scaled by the 1 GiB copy "
+            f"(x {b['write_scale']:.3f}); GB = 1e9 bytes; the rate is (read + write) / duration "
+            "against 8 TB/s.", "",
+            "| kernel | dispatches | ms | read GB | write GB | TB/s | % of 8 TB/s |",
+            "|---|---|---|---|---|---|---|"]
+    for k in b["kernels"][:top]:
+        out.append(f"| {k['kernel']} | {k['dispatches']} | {k['ms']:.3f} | {k['read'] / 1e9:.3f} | "
+                   f"{k['write'] / 1e9:.3f} | {k['tb_per_s']:.2f} | {k['tb_per_s'] / 8 * 100:.1f} |")
+    return "\n".join(out)
+
+
 def main(argv):
     if len(argv) >= 5 and argv[0] == "trace":
         print(trace_markdown(argv[1], int(argv[2]), argv[3], argv[4]))
@@ -355,6 +413,8 @@ def main(argv):
         print(json.dumps(call_traffic(argv[1], argv[2], argv[3], int(argv[4])), indent=1))
     elif len(argv) == 4 and argv[0] == "dispatches":
         print(dispatches_markdown(argv[1], argv[2], argv[3]))
+    elif len(argv) == 6 and argv[0] == "bandwidth":
+        print(bandwidth_markdown(argv[1], argv[2], argv[3], argv[4], argv[5]))
     elif len(argv) == 5 and argv[0] == "reqsizes":
         print(reqsizes_markdown(argv[1], argv[2], argv[3], argv[4]))
     elif len(argv) >= 4 and argv[0] == "traffic":

@@ -10,6 +10,9 @@ value), so the profile summaries' figures can be checked without a GPU.
   when FETCH_SIZE counts those 64-byte reads as 64 bytes.
 * traffic: FETCH_SIZE and WRITE_SIZE scaled by the copy's factors, per
   named kernel.
+* bandwidth: per kernel of the last call of a hand-made kernel trace, its
+  summed duration, read bytes by request size and scaled WRITE_SIZE, and
+  the rate they give.
 """
 import sqlite3
 
@@ -98,3 +101,46 @@ def test_traffic(tmp_path):
     assert t["write"]["bytes"] == pytest.approx(50 * 1024)
     assert t["traffic_bytes_per_launch"] == pytest.approx(100 * 2048 + 50 * 1024)
     assert t["call"]["bytes"] == pytest.approx((1 + 100) * 2048 + (2 + 50) * 1024)
+
+
+def _trace(path, kernels):
+    con = sqlite3.connect(path)
+    con.execute("create table kernels (kernel_name text, start integer, end integer)")
+    for name, start, end in kernels:
+        con.execute("insert into kernels values (?, ?, ?)", (name, start, end))
+    con.commit()
+    con.close()
+    return str(path)
+
+
+def test_bandwidth(tmp_path):
+    req = _db(tmp_path / "req.db", [
+        (COPY, _req(0, 0, (1 << 30) // 128)),
+        (IOTA, _req(0, 0, 1)),
+        (EMIT, _req(0, 0, 1000)),
+        (EMIT, _req(0, 10, 0)),
+    ])
+    write = _db(tmp_path / "w.db", [
+        (COPY, {"WRITE_SIZE": (1 << 30) / 1024}),
+        (IOTA, {"WRITE_SIZE": 1.0}),
+        (EMIT, {"WRITE_SIZE": 4.0}),
+        (EMIT, {"WRITE_SIZE": 6.0}),
+    ])
+    # times in ns; an earlier call (before the last k_iota_zero) is ignored
+    tr = _trace(tmp_path / "t.db", [
+        (EMIT, 0, 5_000_000),
+        (IOTA, 10_000_000, 10_001_000),
+        (EMIT, 10_002_000, 10_004_000),
+        (EMIT, 10_005_000, 10_006_000),
+    ])
+    b = profsum.bandwidth(req, write, tr)
+    k = {x["kernel"]: x for x in b["kernels"]}
+    e = k["k_live_emit<unsigned long>"]
+    assert e["dispatches"] == 2
+    assert e["ms"] == pytest.approx(0.003)
+    assert e["read"] == 1000 * 128 + 10 * 64
+    assert e["write"] == pytest.approx(10 * 1024)
+    assert e["tb_per_s"] == pytest.approx((1000 * 128 + 640 + 10240) / 3e-6 / 1e12)
+    assert b["kernels"][0]["kernel"] == "k_live_emit<unsigned long>"
+    md = profsum.bandwidth_markdown(req, write, tr, "T", "a ;; b")
+    assert "| k_live_emit<unsigned long> | 2 | 0.003 |" in md
