@@ -37,10 +37,21 @@ __global__ void __launch_bounds__(kBlock) k_bins_count(Ctx ctx) {
   const uint32_t lo = min(n, blockIdx.x * per), hi = min(n, lo + per);
   uint32_t cnt[kNumBins] = {0, 0, 0, 0};
   uint64_t mx = 0;
-  for (uint32_t i = lo + threadIdx.x; i < hi; i += kBlock) {
-    const uint64_t len = (uint64_t)(rp[i + 1] - rp[i]);
-    cnt[row_bin(len)]++;
-    mx = len > mx ? len : mx;
+  // four rows per thread and step (i, i + kBlock, ...), loaded together
+  constexpr uint32_t kStep = 4;
+  for (uint32_t i0 = lo + threadIdx.x; i0 < hi; i0 += kStep * kBlock) {
+    uint64_t len[kStep];
+#pragma unroll
+    for (uint32_t u = 0; u < kStep; ++u) {
+      const uint32_t i = i0 + u * kBlock;
+      len[u] = i < hi ? (uint64_t)(rp[i + 1] - rp[i]) : ~0ull;
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kStep; ++u)
+      if (len[u] != ~0ull) {
+        cnt[row_bin(len[u])]++;
+        mx = len[u] > mx ? len[u] : mx;
+      }
   }
   __shared__ uint32_t sh[kNumBins];
   __shared__ uint32_t smx;
@@ -91,15 +102,29 @@ __global__ void __launch_bounds__(kBlock) k_bins_fill(Ctx ctx) {
   uint32_t run[kNumBins];
   for (int b = 0; b < kNumBins; ++b)
     run[b] = ctx.st->bin_start[b] + ctx.bin_part[b * gridDim.x + blockIdx.x];
-  for (uint32_t base = lo; base < hi; base += kBlock) {
-    uint32_t i = base + threadIdx.x;
-    int mybin = -1;
-    if (i < hi) mybin = row_bin((uint64_t)(rp[i + 1] - rp[i]));
-    for (int b = HEAVY ? 3 : 0; b < kNumBins; ++b) {
-      uint32_t tot;
-      uint32_t ex = block_excl_scan(mybin == b ? 1u : 0u, sh, &tot);
-      if (mybin == b) ctx.rows[run[b] + ex] = i;
-      run[b] += tot;
+  // four groups of kBlock rows per step, their row lengths loaded together;
+  // the groups are listed in order, so every list stays in node order
+  constexpr uint32_t kStep = 4;
+  for (uint32_t base = lo; base < hi; base += kStep * kBlock) {
+    int mb[kStep];
+    bool heavy = false;
+#pragma unroll
+    for (uint32_t u = 0; u < kStep; ++u) {
+      const uint32_t i = base + u * kBlock + threadIdx.x;
+      mb[u] = i < hi ? row_bin((uint64_t)(rp[i + 1] - rp[i])) : -1;
+      heavy = heavy || mb[u] == 3;
+    }
+    // heavy rows are rare: a step without one needs no scan
+    if (HEAVY && !__syncthreads_or(heavy)) continue;
+#pragma unroll
+    for (uint32_t u = 0; u < kStep; ++u) {
+      const uint32_t i = base + u * kBlock + threadIdx.x;
+      for (int b = HEAVY ? 3 : 0; b < kNumBins; ++b) {
+        uint32_t tot;
+        uint32_t ex = block_excl_scan(mb[u] == b ? 1u : 0u, sh, &tot);
+        if (mb[u] == b) ctx.rows[run[b] + ex] = i;
+        run[b] += tot;
+      }
     }
   }
 }
